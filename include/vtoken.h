@@ -1,0 +1,188 @@
+/*
+ * vtoken.h - C ABI of the vToken KV repack for AMD Instinct MI355X (gfx950).
+ *
+ * The repack turns token-level liveness into reusable KV blocks, as described in
+ * "vToken: Token-Level Virtualization for Reclaimable KV Caches" (arXiv 2608.13263):
+ * the token table of Sec. 3.2, the reclamation backend of Sec. 3.3 (headroom-aware
+ * admission Sec. 3.3.2, relocation planning Sec. 3.3.3, copy Sec. 3.3.4) and the slot
+ * formula of Sec. 3.4 (slot = block_id * block_size + offset).
+ *
+ * One repack pass is three calls, enqueued in this order on one HIP stream:
+ *
+ *   vtoken_build_token_table   per-request exclusive scan of the live mask, admission of
+ *                              requests against the free list, token table, new block
+ *                              tables and the per-destination-block source plan
+ *   vtoken_repack              gathers every live K/V row of every admitted request into
+ *                              densely packed destination blocks, all layers, K and V, and
+ *                              all KV heads in one launch (the only call touching KV bytes)
+ *   vtoken_free_blocks         emits the list of freed source blocks
+ *
+ * General conventions (all calls):
+ *   - Pointers inside the structs are DEVICE pointers unless a field says [host].
+ *   - The caller owns every buffer; the library keeps no pointer after a call returns,
+ *     allocates no memory and never synchronises: every call only enqueues kernels on
+ *     `stream` and returns. The calls therefore may be captured into a HIP graph.
+ *   - Host-side argument errors return a negative status synchronously and enqueue
+ *     nothing. Errors that only the device can see (a bad block id, inconsistent CSR
+ *     lengths, a capacity exceeded) are written to plan->counters[3] by the first
+ *     kernel of vtoken_build_token_table; every later kernel reads that word and does
+ *     nothing when it is not VTOKEN_OK. The caller inspects it after its own sync.
+ *     Every kernel bounds-checks what it dereferences, so no status path writes
+ *     outside the buffers the caller described.
+ *   - The library is re-entrant: calls on different streams with disjoint buffers may
+ *     run concurrently. Calls that share a plan or a KV cache must be stream-ordered.
+ *
+ * Conventions the paper leaves open (frozen here; the CPU oracle follows the same ones):
+ *   - Out-of-place relocation (Sec. 3.3.2): destinations are taken from the caller's
+ *     free list front to back, requests in ascending index order; sources are never
+ *     written; source blocks are released only by vtoken_free_blocks, after the copy
+ *     (Sec. 3.3.4, invariant I3 of Sec. 3.5).
+ *   - Every block of a request is a relocation source (the source batch of Sec. 3.3.3
+ *     is the whole request); a request needs ceil(live / block_size) destinations.
+ *   - A request is profitable iff it needs strictly fewer blocks than it holds (Sec.
+ *     3.3.3, invariant I4). Profitable requests are admitted in ascending order while
+ *     the free list can supply their destinations; once one is deferred every later
+ *     profitable request is deferred too (prefix admission, Sec. 3.3.2). Unprofitable
+ *     and deferred requests keep their block table and slots.
+ *   - Live tokens keep their logical order and fill each destination block completely
+ *     before the next (Sec. 3.3.3): the token of rank k goes to destination block
+ *     k / block_size, offset k % block_size.
+ *   - Dead tokens get token_slot -1 (Sec. 3.2, evict_token). The tail slots of the last
+ *     destination block and all non-destination bytes keep their previous contents.
+ *   - freed = concatenation over admitted requests (ascending) of all their old blocks
+ *     in block-table order.
+ *
+ * KV layout: one contiguous buffer of 2*num_layers planes, plane index 2*layer + (0 for K,
+ * 1 for V); each plane is [num_blocks][block_size][num_kv_heads][head_dim] elements of
+ * elem_bytes bytes. The row of one token in one plane is num_kv_heads*head_dim*elem_bytes
+ * contiguous bytes (head_dim fastest). The payload is copied as opaque bytes, so any
+ * 1- or 2-byte element type (fp8, fp16, bf16) is supported and NaN payloads survive.
+ * One token table and one block table drive all planes: the table is per sequence, not
+ * per layer or head (Sec. 3.2).
+ */
+#ifndef VTOKEN_H
+#define VTOKEN_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum vtoken_status {
+  VTOKEN_OK = 0,
+  VTOKEN_ERR_NULL = -1,       /* a required pointer is NULL                                */
+  VTOKEN_ERR_SHAPE = -2,      /* a dimension <= 0, elem_bytes not 1 or 2, a row not a      */
+                              /* multiple of 16 bytes, num_blocks*block_size >= 2^31,      */
+                              /* num_tokens >= 2^31 or negative lengths                    */
+  VTOKEN_ERR_CAPACITY = -3,   /* an output capacity below the documented minimum           */
+  VTOKEN_ERR_HIP = -4,        /* the HIP runtime reported an error at launch               */
+  VTOKEN_ERR_ARGUMENT = -5,   /* an invalid tuning option (vtoken_repack_ex)               */
+  /* device-detected, written to plan->counters[3]: */
+  VTOKEN_ERR_BLOCK_RANGE = -10, /* a block id in block_ids or in the consumed part of    */
+                                /* free_list lies outside [0, num_blocks)                */
+  VTOKEN_ERR_BT_LEN = -11,      /* bt_indptr[r+1]-bt_indptr[r] != ceil(seq_lens[r]/S),   */
+                                /* or bt_indptr outside [0, num_bt_entries]              */
+  VTOKEN_ERR_TOK_LEN = -12      /* tok_indptr[r+1]-tok_indptr[r] != seq_lens[r] or       */
+                                /* tok_indptr outside [0, num_tokens]                    */
+} vtoken_status;
+
+/* The paged KV cache (Sec. 2.1). */
+typedef struct vtoken_cache {
+  void*   kv;            /* device, [2*num_layers][num_blocks][block_size][H][D], see above */
+  int32_t num_layers;    /* L                                                               */
+  int32_t num_kv_heads;  /* H (KV heads; GQA/MQA only change H, Sec. 6)                     */
+  int32_t head_dim;      /* D                                                               */
+  int32_t block_size;    /* S, tokens per block                                             */
+  int32_t num_blocks;    /* blocks per plane; block ids are shared by all planes            */
+  int32_t elem_bytes;    /* 1 (fp8) or 2 (fp16, bf16)                                       */
+} vtoken_cache;
+
+/* The requests of one repack pass, in CSR form. Request r has seq_lens[r] tokens; its
+ * tokens' live bits are live[tok_indptr[r] .. tok_indptr[r+1]) (1 live, 0 evicted: the
+ * evict_token call of Sec. 3.2 is a write of 0 there), and its block table (Sec. 2.1) is
+ * block_ids[bt_indptr[r] .. bt_indptr[r+1]) with exactly ceil(seq_lens[r]/S) entries.
+ * Token position p of request r lives at slot block_ids[bt_indptr[r] + p/S]*S + p%S. */
+typedef struct vtoken_batch {
+  int32_t        num_reqs;       /* R                                     [host]            */
+  int64_t        num_tokens;     /* T = tok_indptr[R]                     [host]            */
+  int64_t        num_bt_entries; /* M = bt_indptr[R]                      [host]            */
+  const int32_t* seq_lens;       /* [R]                                                     */
+  const int32_t* tok_indptr;     /* [R+1]                                                   */
+  const int32_t* bt_indptr;      /* [R+1]                                                   */
+  const int32_t* block_ids;      /* [M]                                                     */
+  const uint8_t* live;           /* [T]                                                     */
+  const int32_t* free_list;      /* [free_len] destination supply, consumed front to back   */
+  int32_t        free_len;       /* f                                     [host]            */
+} vtoken_batch;
+
+/* Caller-allocated outputs of vtoken_build_token_table; read by the two later calls.
+ * They form the bulk apply_moves of Sec. 3.2: token_slot and the new block tables are
+ * valid for attention once vtoken_repack has executed on the stream. */
+typedef struct vtoken_plan {
+  int32_t* token_slot;      /* [T]   slot of every token after the pass; -1 if dead         */
+  int32_t* live_count;      /* [R]   live tokens per request                                */
+  int32_t* admitted;        /* [R]   1 repacked in this pass, 0 unchanged                   */
+  int32_t* dst_indptr;      /* [R+1] exclusive scan of admitted*need: request r's          */
+                            /*       destinations are free_list[dst_indptr[r] ..)           */
+  int32_t* new_bt_indptr;   /* [R+1] exclusive scan of the new block-table lengths          */
+  int32_t* new_block_ids;   /* [new_bt_capacity] new block tables, CSR by new_bt_indptr     */
+  int32_t* src_plan;        /* [src_plan_capacity] for destination block g (the g-th       */
+                            /*       consumed free-list entry) and offset j, entry g*S+j is */
+                            /*       the source slot of the token placed there, -1 if none */
+  int32_t* freed_indptr;    /* [R+1] exclusive scan of admitted*old_blocks                  */
+  int32_t* counters;        /* [4]   used free-list entries, admitted requests, freed       */
+                            /*       blocks, status (VTOKEN_OK or a device error code)      */
+  int64_t  new_bt_capacity;   /* entries in new_block_ids, >= M            [host]           */
+  int64_t  src_plan_capacity; /* entries in src_plan, >= min(free_len, M)*S [host]         */
+} vtoken_plan;
+
+/* Step 1 (Sec. 3.2, 3.3.2, 3.3.3): scan, admission, token table, block tables, plan.
+ * Writes every field of *plan (device memory) except new_bt/src_plan capacity beyond
+ * what is used. Returns VTOKEN_OK once the kernels are enqueued. */
+vtoken_status vtoken_build_token_table(const vtoken_cache* cache, const vtoken_batch* batch,
+                                       const vtoken_plan* plan, hipStream_t stream);
+
+/* Step 2 (Sec. 3.3, lazy compaction; Sec. 3.3.4 copy): for every admitted request r, every
+ * live token and every plane, copies the token's row from its old slot to its new slot.
+ * Reads plan->src_plan, plan->counters and batch->free_list; writes KV bytes of the
+ * destination rows only. Idempotent on unchanged inputs (sources are never written).
+ * Must follow vtoken_build_token_table on the same stream. */
+vtoken_status vtoken_repack(const vtoken_cache* cache, const vtoken_batch* batch,
+                            const vtoken_plan* plan, hipStream_t stream);
+
+/* Step 3 (Sec. 3.3.4: sources are returned only after the packed layout is committed):
+ * writes freed[0 .. counters[2]) = old blocks of the admitted requests. Stream order
+ * after vtoken_repack is what makes reuse of these blocks safe. freed_capacity >= M. */
+vtoken_status vtoken_free_blocks(const vtoken_batch* batch, const vtoken_plan* plan,
+                                 int32_t* freed, int64_t freed_capacity, hipStream_t stream);
+
+/* Tuning entry for the copy of step 2; vtoken_repack uses the defaults (all fields 0).
+ *   variant: 0 default, 1 direct (registers, plain loads/stores), 2 direct with
+ *            non-temporal loads and stores, 3 staged through LDS
+ *   grid:    workgroups of the persistent launch, 0 = from occupancy
+ *   order:   0 plane-major work order, 1 block-major                                      */
+typedef struct vtoken_repack_options {
+  int32_t variant;
+  int32_t grid;
+  int32_t order;
+  int32_t reserved;
+} vtoken_repack_options;
+
+vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* batch,
+                               const vtoken_plan* plan, const vtoken_repack_options* options,
+                               hipStream_t stream);
+
+/* Static string naming a status code; never NULL. */
+const char* vtoken_status_string(int32_t status);
+
+/* Library ABI version: major*10000 + minor*100 + patch. */
+int32_t vtoken_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VTOKEN_H */

@@ -1,0 +1,442 @@
+"""Seeded synthetic inputs for the KV repack: paged caches, block tables and liveness.
+
+This module only builds inputs. It holds none of the repack's arithmetic (no scan, no
+admission, no packing); both the HIP path and the CPU oracle take its arrays as given.
+
+The paper evaluates on ShareGPT / LongBench prompts with Llama-3.1-8B and Mistral-7B
+(Sec. 5.1). Those datasets and models are not used here: the generators below reproduce
+the shapes that matter to the repack - the KV geometry, request-length mix, physical
+scatter of blocks in the pool, and the liveness pattern an eviction policy leaves
+behind (Random, H2O, Scissorhands; Sec. 2.2 and the policy-adapter figure of Sec. 4).
+
+Physical scatter: the block pool is a seeded permutation of [0, num_blocks); requests
+take consecutive chunks of it as block tables and the rest, in permuted order, is the
+free list. Lengths are integer-uniform and inclusive. Seeds go into numpy's PCG64.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Callable, Dict, List, Optional, Sequence
+
+import numpy as np
+
+__all__ = [
+    "KVShape",
+    "RepackInputs",
+    "CONFIGS",
+    "make",
+    "from_masks",
+    "tiny_cache",
+    "llama3_8b_random",
+    "llama3_8b_h2o",
+    "llama3_70b_h2o",
+    "ScissorhandsStream",
+    "kv_host",
+    "kv_device",
+    "bernoulli_live",
+    "random_live",
+    "h2o_live",
+]
+
+
+@dataclasses.dataclass(frozen=True)
+class KVShape:
+    """Geometry of a paged KV cache (Sec. 2.1: per-token bytes 2*L*H*D*dtype)."""
+
+    num_layers: int
+    num_kv_heads: int
+    head_dim: int
+    block_size: int
+    dtype: str  # "fp16", "bf16" or "fp8_e4m3"
+
+    @property
+    def elem_bytes(self) -> int:
+        return {"fp16": 2, "bf16": 2, "fp8_e4m3": 1}[self.dtype]
+
+    @property
+    def row_bytes(self) -> int:
+        """Bytes of one token's row in one plane: H * D * elem_bytes."""
+        return self.num_kv_heads * self.head_dim * self.elem_bytes
+
+    @property
+    def num_planes(self) -> int:
+        """Planes of the cache: one K and one V plane per layer."""
+        return 2 * self.num_layers
+
+    @property
+    def token_bytes(self) -> int:
+        """KV bytes of one token over all layers, K and V (Sec. 2.1)."""
+        return self.num_planes * self.row_bytes
+
+    @property
+    def block_bytes(self) -> int:
+        """Bytes one block id stands for over all planes."""
+        return self.token_bytes * self.block_size
+
+
+@dataclasses.dataclass
+class RepackInputs:
+    """One batch of requests over one paged pool (host arrays, CSR layout)."""
+
+    name: str
+    shape: KVShape
+    num_blocks: int
+    seq_lens: np.ndarray   # int32 [R]
+    tok_indptr: np.ndarray  # int32 [R+1]
+    bt_indptr: np.ndarray   # int32 [R+1]
+    block_ids: np.ndarray   # int32 [M]
+    live: np.ndarray        # uint8 [T]
+    free_list: np.ndarray   # int32 [f]
+    seed: int = 0
+    note: str = ""
+
+    @property
+    def num_reqs(self) -> int:
+        return int(self.seq_lens.shape[0])
+
+    @property
+    def num_tokens(self) -> int:
+        return int(self.live.shape[0])
+
+    @property
+    def num_bt_entries(self) -> int:
+        return int(self.block_ids.shape[0])
+
+    def request_live(self, r: int) -> np.ndarray:
+        return self.live[self.tok_indptr[r]:self.tok_indptr[r + 1]]
+
+    def request_blocks(self, r: int) -> np.ndarray:
+        return self.block_ids[self.bt_indptr[r]:self.bt_indptr[r + 1]]
+
+    def pool_bytes(self) -> int:
+        return self.num_blocks * self.shape.block_bytes
+
+
+def _blocks_for(n: int, block_size: int) -> int:
+    # a request of n tokens occupies ceil(n / S) blocks of a paged layout (Sec. 2.1)
+    return (int(n) + block_size - 1) // block_size
+
+
+def _assemble(name: str, shape: KVShape, rng: np.random.Generator, seq_lens: Sequence[int],
+              masks: Sequence[np.ndarray], free_blocks: int, seed: int,
+              note: str = "") -> RepackInputs:
+    """Lay requests out in a shuffled pool of len(tables) + free_blocks blocks."""
+    S = shape.block_size
+    seq_lens = np.asarray(seq_lens, dtype=np.int64)
+    blocks_per_req = np.array([_blocks_for(n, S) for n in seq_lens], dtype=np.int64)
+    M = int(blocks_per_req.sum())
+    num_blocks = M + int(free_blocks)
+    perm = rng.permutation(num_blocks).astype(np.int32)
+    tok_indptr = np.zeros(len(seq_lens) + 1, dtype=np.int64)
+    tok_indptr[1:] = np.cumsum(seq_lens)
+    bt_indptr = np.zeros(len(seq_lens) + 1, dtype=np.int64)
+    bt_indptr[1:] = np.cumsum(blocks_per_req)
+    live = np.concatenate([np.asarray(m, dtype=np.uint8) for m in masks]) if len(masks) else \
+        np.zeros(0, dtype=np.uint8)
+    assert live.shape[0] == tok_indptr[-1]
+    return RepackInputs(
+        name=name, shape=shape, num_blocks=num_blocks,
+        seq_lens=seq_lens.astype(np.int32), tok_indptr=tok_indptr.astype(np.int32),
+        bt_indptr=bt_indptr.astype(np.int32), block_ids=perm[:M].copy(),
+        live=live, free_list=perm[M:].copy(), seed=seed, note=note)
+
+
+# ----------------------------------------------------------------------------------------
+# Liveness stand-ins for the eviction policies the paper evaluates (Sec. 2.2, Sec. 4).
+# ----------------------------------------------------------------------------------------
+
+def bernoulli_live(rng: np.random.Generator, n: int, keep: float, sink: int = 0) -> np.ndarray:
+    """Each token live with probability `keep`; the first `sink` tokens always live."""
+    live = (rng.random(n) < keep).astype(np.uint8)
+    live[:min(sink, n)] = 1
+    return live
+
+
+def random_live(rng: np.random.Generator, n: int, keep: float, recent: int) -> np.ndarray:
+    """Random policy: floor(keep*n) victims-survivors sampled uniformly without replacement
+    from the evictable range [0, n - recent), plus the last `recent` tokens live."""
+    live = np.zeros(n, dtype=np.uint8)
+    evictable = max(n - recent, 0)
+    k = min(int(math.floor(keep * n)), evictable)
+    if k > 0:
+        live[rng.choice(evictable, size=k, replace=False)] = 1
+    live[evictable:] = 1
+    return live
+
+
+def h2o_live(rng: np.random.Generator, n: int, keep: float, recent: int,
+             zipf_s: float = 1.1) -> np.ndarray:
+    """H2O-style: cumulative attention hits drawn as n samples of a Zipf(s) law over
+    positions (P(p) proportional to (p+1)^-s); keep the top floor(keep*n) positions of
+    [0, n - recent) by (hits desc, position asc), plus the last `recent` tokens."""
+    live = np.zeros(n, dtype=np.uint8)
+    evictable = max(n - recent, 0)
+    if n > 0:
+        w = np.arange(1, n + 1, dtype=np.float64) ** (-zipf_s)
+        hits = np.bincount(rng.choice(n, size=n, p=w / w.sum()), minlength=n)
+        k = min(int(math.floor(keep * n)), evictable)
+        if k > 0:
+            pos = np.arange(evictable)
+            order = np.lexsort((pos, -hits[:evictable]))
+            live[order[:k]] = 1
+    live[evictable:] = 1
+    return live
+
+
+# ----------------------------------------------------------------------------------------
+# The workloads.
+# ----------------------------------------------------------------------------------------
+
+def tiny_cache(seed: int = 101) -> RepackInputs:
+    """1 layer, 2 KV heads, head_dim 64, fp16, block 16; 8 requests of U[100,500] tokens in a
+    shuffled 512-block pool; Bernoulli(0.5) liveness with the first 4 tokens live."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    shape = KVShape(1, 2, 64, 16, "fp16")
+    lens = rng.integers(100, 500, size=8, endpoint=True)
+    masks = [bernoulli_live(rng, int(n), 0.5, sink=4) for n in lens]
+    M = sum(_blocks_for(n, 16) for n in lens)
+    return _assemble("tiny", shape, rng, lens, masks, 512 - M, seed,
+                     "fp16 1x2x64, S=16, 8 req U[100,500], Bernoulli 0.5 + 4 sink, 512-block pool")
+
+
+def llama3_8b_random(seed: int = 201, num_reqs: int = 64, num_layers: int = 32,
+                     len_range=(2048, 8192), keep: float = 0.3, recent: int = 64,
+                     slack_blocks: int = 1024) -> RepackInputs:
+    """Llama-3-8B KV geometry (32 layers, 8 KV heads, head_dim 128, bf16, block 16); 64 requests
+    of U[2048,8192] tokens; Random policy keeping 30% of the evictable tokens plus the last 64.
+    The free pool holds keep*M + R*(recent/S + 1) + slack blocks."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    shape = KVShape(num_layers, 8, 128, 16, "bf16")
+    lens = rng.integers(len_range[0], len_range[1], size=num_reqs, endpoint=True)
+    masks = [random_live(rng, int(n), keep, recent) for n in lens]
+    M = sum(_blocks_for(n, 16) for n in lens)
+    free = int(math.ceil(keep * M)) + num_reqs * (recent // 16 + 1) + slack_blocks
+    return _assemble("llama3_8b_random", shape, rng, lens, masks, free, seed,
+                     f"bf16 {num_layers}x8x128, S=16, {num_reqs} req U{list(len_range)}, "
+                     f"Random keep {keep} + last {recent}")
+
+
+def llama3_8b_h2o(seed: int = 301, num_reqs: int = 128, num_layers: int = 32,
+                  len_range=(4096, 16384), keep: float = 0.2, recent: int = 128,
+                  slack_blocks: int = 1024) -> RepackInputs:
+    """Llama-3-8B geometry; 128 requests of U[4096,16384] tokens; H2O-style liveness: Zipf(1.1)
+    attention hits, top 20% by score plus a 128-token recent window."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    shape = KVShape(num_layers, 8, 128, 16, "bf16")
+    lens = rng.integers(len_range[0], len_range[1], size=num_reqs, endpoint=True)
+    masks = [h2o_live(rng, int(n), keep, recent) for n in lens]
+    M = sum(_blocks_for(n, 16) for n in lens)
+    free = int(math.ceil(keep * M)) + num_reqs * (recent // 16 + 1) + slack_blocks
+    return _assemble("llama3_8b_h2o", shape, rng, lens, masks, free, seed,
+                     f"bf16 {num_layers}x8x128, S=16, {num_reqs} req U{list(len_range)}, "
+                     f"H2O Zipf(1.1) keep {keep} + last {recent}")
+
+
+def llama3_70b_h2o(seed: int = 501, keep: float = 0.3, dtype: str = "fp8_e4m3",
+                   num_reqs: int = 32, num_layers: int = 80, num_kv_heads: int = 8,
+                   len_range=(16384, 65536), recent: int = 128,
+                   pool_bytes: Optional[int] = None, resident_frac: float = 0.8) -> RepackInputs:
+    """Llama-3-70B KV geometry (80 layers, 8 KV heads, head_dim 128, block 32) in fp8 (OCP
+    e4m3) or bf16; up to 32 requests of U[16384,65536] tokens; H2O-style Zipf liveness at
+    keep ratio k plus the last 128 tokens.
+
+    The literal batch does not fit one GPU (bf16 averages ~400 GiB resident). Fit rule: with
+    a device budget `pool_bytes`, keep the longest request prefix whose blocks take at most
+    `resident_frac` of the pool; every remaining block is free."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    shape = KVShape(num_layers, num_kv_heads, 128, 32, dtype)
+    lens = rng.integers(len_range[0], len_range[1], size=num_reqs, endpoint=True)
+    if pool_bytes is None:
+        pool_blocks = sum(_blocks_for(n, 32) for n in lens) * 2
+    else:
+        pool_blocks = int(pool_bytes // shape.block_bytes)
+    keep_n, used = 0, 0
+    for n in lens:
+        b = _blocks_for(n, 32)
+        if used + b > resident_frac * pool_blocks:
+            break
+        keep_n += 1
+        used += b
+    lens = lens[:keep_n]
+    masks = [h2o_live(rng, int(n), keep, recent) for n in lens]
+    return _assemble(f"llama3_70b_h2o_{dtype}_k{keep}", shape, rng, lens, masks,
+                     pool_blocks - used, seed,
+                     f"{dtype} {num_layers}x{num_kv_heads}x128, S=32, {keep_n} of {num_reqs} "
+                     f"req U{list(len_range)}, H2O keep {keep} + last {recent}")
+
+
+def from_masks(masks: Sequence[Sequence[int]], shape: KVShape, free_blocks: int,
+               seed: int = 0, name: str = "custom") -> RepackInputs:
+    """Inputs from explicit per-request live masks (edge cases: empty, all-dead, ragged)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    masks = [np.asarray(m, dtype=np.uint8) for m in masks]
+    return _assemble(name, shape, rng, [len(m) for m in masks], masks, free_blocks, seed)
+
+
+class ScissorhandsStream:
+    """Scissorhands-style repeated repack over a long decode (Sec. 2.2; policy figure, Sec. 4).
+
+    Request r has a logical length that grows by `decode_steps` tokens per round. Its
+    resident layout at each round is: the tokens kept after the previous round, packed, then
+    the tokens decoded since. Each token carries a persistence score: every round it is
+    attended with probability min(1, 1/sqrt(1+age)) at each of the round's decode steps, so
+    the score grows by Binomial(decode_steps, p). Liveness keeps the top floor(budget*len)
+    non-window resident tokens by (score desc, logical position asc) plus the last `window`.
+
+    The stream yields RepackInputs; after the caller has run the repack on round i, it calls
+    `advance(new_block_tables, freed, free_list_rest)` with the pass's outputs, and the next
+    round appends `decode_steps` tokens per request (new blocks from the front of the free
+    list) before drawing liveness again. Only inputs are produced here: the packed layout
+    of each round is what the repack under test returned.
+    """
+
+    def __init__(self, seed: int = 401, num_reqs: int = 256, num_layers: int = 32,
+                 len_range=(2048, 32768), budget: float = 0.25, window: int = 256,
+                 decode_steps: int = 512, pool_blocks: Optional[int] = None):
+        self.rng = np.random.Generator(np.random.PCG64(seed))
+        self.seed = seed
+        self.shape = KVShape(num_layers, 8, 128, 16, "bf16")
+        self.budget, self.window, self.decode_steps = budget, window, decode_steps
+        S = self.shape.block_size
+        self.logical_len = self.rng.integers(len_range[0], len_range[1], size=num_reqs,
+                                             endpoint=True).astype(np.int64)
+        # steady state before round 1: kept older tokens (sorted random subset), the prior
+        # window, then `decode_steps` fresh tokens
+        self.pos: List[np.ndarray] = []
+        for L in self.logical_len:
+            older = int(L) - decode_steps - window
+            kept = int(math.floor(budget * (int(L) - decode_steps)))
+            kept = max(min(kept, older), 0)
+            sel = np.sort(self.rng.choice(older, size=kept, replace=False)) if kept else \
+                np.zeros(0, dtype=np.int64)
+            self.pos.append(np.concatenate([sel, np.arange(older, int(L))]).astype(np.int64))
+        self.score = [self.rng.binomial(decode_steps, 0.5, size=len(p)).astype(np.int64)
+                      for p in self.pos]
+        seq_lens = np.array([len(p) for p in self.pos], dtype=np.int64)
+        M = int(sum(_blocks_for(n, S) for n in seq_lens))
+        if pool_blocks is None:
+            pool_blocks = 2 * M
+        self.num_blocks = int(pool_blocks)
+        perm = self.rng.permutation(self.num_blocks).astype(np.int32)
+        self.tables: List[np.ndarray] = []
+        o = 0
+        for n in seq_lens:
+            b = _blocks_for(int(n), S)
+            self.tables.append(perm[o:o + b].copy())
+            o += b
+        self.free = perm[o:].copy()
+        self.round = 0
+
+    def inputs(self) -> RepackInputs:
+        """Liveness for the current resident layout (the policy's SelectVictims step)."""
+        S = self.shape.block_size
+        masks = []
+        for r, pos in enumerate(self.pos):
+            L = int(self.logical_len[r])
+            age = (L - pos).astype(np.float64)
+            p = np.minimum(1.0, 1.0 / np.sqrt(1.0 + age))
+            self.score[r] = self.score[r] + self.rng.binomial(self.decode_steps, p)
+            n = len(pos)
+            live = np.zeros(n, dtype=np.uint8)
+            win = pos >= L - self.window
+            live[win] = 1
+            cand = np.nonzero(~win)[0]
+            k = min(int(math.floor(self.budget * L)) - int(win.sum()), len(cand))
+            if k > 0:
+                order = np.lexsort((pos[cand], -self.score[r][cand]))
+                live[cand[order[:k]]] = 1
+            masks.append(live)
+        seq_lens = np.array([len(p) for p in self.pos], dtype=np.int64)
+        tok_indptr = np.zeros(len(seq_lens) + 1, dtype=np.int64)
+        tok_indptr[1:] = np.cumsum(seq_lens)
+        lens_b = np.array([len(t) for t in self.tables], dtype=np.int64)
+        bt_indptr = np.zeros(len(seq_lens) + 1, dtype=np.int64)
+        bt_indptr[1:] = np.cumsum(lens_b)
+        return RepackInputs(
+            name=f"llama3_8b_scissorhands_round{self.round}", shape=self.shape,
+            num_blocks=self.num_blocks, seq_lens=seq_lens.astype(np.int32),
+            tok_indptr=tok_indptr.astype(np.int32), bt_indptr=bt_indptr.astype(np.int32),
+            block_ids=np.concatenate(self.tables).astype(np.int32) if self.tables else
+            np.zeros(0, np.int32),
+            live=np.concatenate(masks) if masks else np.zeros(0, np.uint8),
+            free_list=self.free.copy(), seed=self.seed,
+            note=f"Scissorhands budget {self.budget} window {self.window}, round {self.round}")
+
+    def advance(self, live: np.ndarray, token_slot_order: Sequence[np.ndarray],
+                new_tables: Sequence[np.ndarray], free_list: np.ndarray) -> None:
+        """Carry the state to the next round.
+
+        live: the mask returned by inputs() for this round. token_slot_order[r]: indices (into
+        request r's resident tokens) of its tokens in their new slot order, i.e. the tokens
+        that are still resident after the pass, in the order they now occupy their block
+        table. new_tables[r]: the request's block table after the pass. free_list: the free
+        list after the pass. Then `decode_steps` tokens are appended to every request."""
+        S = self.shape.block_size
+        free = list(free_list)
+        for r in range(len(self.pos)):
+            keep = np.asarray(token_slot_order[r], dtype=np.int64)
+            self.pos[r] = self.pos[r][keep]
+            self.score[r] = self.score[r][keep]
+            table = list(np.asarray(new_tables[r], dtype=np.int32))
+            L = int(self.logical_len[r])
+            fresh = np.arange(L, L + self.decode_steps, dtype=np.int64)
+            self.pos[r] = np.concatenate([self.pos[r], fresh])
+            self.score[r] = np.concatenate([self.score[r], np.zeros(len(fresh), np.int64)])
+            need = _blocks_for(len(self.pos[r]), S) - len(table)
+            if need > len(free):
+                raise RuntimeError("pool exhausted while appending decoded tokens")
+            table.extend(free[:need])
+            free = free[need:]
+            self.tables[r] = np.asarray(table, dtype=np.int32)
+            self.logical_len[r] = L + self.decode_steps
+        self.free = np.asarray(free, dtype=np.int32)
+        self.round += 1
+
+
+CONFIGS: Dict[str, Callable[..., RepackInputs]] = {
+    "tiny": tiny_cache,
+    "llama3_8b_random": llama3_8b_random,
+    "llama3_8b_h2o": llama3_8b_h2o,
+    "llama3_70b_h2o": llama3_70b_h2o,
+}
+
+
+def make(name: str, **kw) -> RepackInputs:
+    return CONFIGS[name](**kw)
+
+
+# ----------------------------------------------------------------------------------------
+# KV payloads. The repack copies opaque bytes; values only matter to the attention check.
+# ----------------------------------------------------------------------------------------
+
+def kv_host(shape: KVShape, num_blocks: int, seed: int) -> np.ndarray:
+    """Random KV bytes on the host, uint8 [2L][num_blocks*S][row_bytes]."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    n = shape.num_planes * num_blocks * shape.block_size * shape.row_bytes
+    return rng.integers(0, 256, size=n, dtype=np.uint8).reshape(
+        shape.num_planes, num_blocks * shape.block_size, shape.row_bytes)
+
+
+def torch_dtype(shape: KVShape):
+    import torch
+    return {"fp16": torch.float16, "bf16": torch.bfloat16,
+            "fp8_e4m3": torch.float8_e4m3fn}[shape.dtype]
+
+
+def kv_device(shape: KVShape, num_blocks: int, seed: int, device="cuda"):
+    """KV values ~N(0,1) in the cache dtype on `device`, [2L][num_blocks][S][H][D]
+    (fp8 values are N(0,1) draws rounded to OCP e4m3)."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    dims = (shape.num_planes, num_blocks, shape.block_size, shape.num_kv_heads, shape.head_dim)
+    out = torch.empty(dims, dtype=torch_dtype(shape), device=device)
+    # fill plane by plane to bound the temporary
+    for p in range(shape.num_planes):
+        if shape.dtype == "fp8_e4m3":
+            out[p].copy_(torch.randn(dims[1:], generator=g, device=device,
+                                     dtype=torch.float16).to(torch.float8_e4m3fn))
+        else:
+            out[p].normal_(generator=g)
+    return out
