@@ -1,0 +1,258 @@
+#!/usr/bin/env python3
+"""Throughput of the vToken KV repack hot path on one MI355X.
+
+One step is one whole repack pass over one batch: vtoken_build_token_table (live-mask scan,
+admission, token table, plan), vtoken_repack (gather of every live K/V row of every layer
+into packed blocks) and vtoken_free_blocks, all enqueued on one stream. Inputs are resident
+in HBM before the timed region. The pass is idempotent on unchanged inputs (out-of-place:
+sources are never written), so every timed step does the full work again.
+
+The default workload is the Llama-3-8B-shaped cache: 32 layers, 8 KV heads, head_dim 128,
+bf16, block 16, 64 requests of U[2048, 8192] tokens in a shuffled ~56 GiB pool, Random
+eviction keeping 30% of each request plus its last 64 tokens.
+
+Prints one JSON line. `value` is repacked KV GB/s over the whole step (read+write bytes of
+the live rows: 2 * live tokens * 2*L*H*D*elem_bytes); `roofline` prices the repack kernel
+alone against the 8 TB/s HBM peak, timed with HIP events on its launch stream.
+
+    python bench.py [--steps K] [--warmup W] [--config NAME] [--variant V] [--grid G]
+    python bench.py --mode copy      # plain device-to-device copy of known size
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+HBM_PEAK_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_13263_amd", "csrc", "vtoken_kernels.hip")
+
+
+def parse_args(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="llama3_8b_random",
+                    choices=["llama3_8b_random", "llama3_8b_h2o", "llama3_70b_h2o", "tiny"])
+    ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--keep", type=float, default=0.3, help="keep ratio (70B config)")
+    ap.add_argument("--kv-dtype", default="fp8_e4m3", help="70B config: fp8_e4m3 or bf16")
+    ap.add_argument("--variant", type=int, default=0)
+    ap.add_argument("--grid", type=int, default=0)
+    ap.add_argument("--order", type=int, default=0)
+    ap.add_argument("--mode", default="repack", choices=["repack", "copy"])
+    ap.add_argument("--copy-gib", type=float, default=8.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-planes", type=int, default=4,
+                    help="planes of the workload the CPU oracle is timed on")
+    return ap.parse_args(argv)
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def make_workload(args):
+    from paper_2608_13263_amd import workloads as W
+    if args.config == "llama3_8b_random":
+        return W.llama3_8b_random(args.seed if args.seed is not None else 201)
+    if args.config == "llama3_8b_h2o":
+        return W.llama3_8b_h2o(args.seed if args.seed is not None else 301)
+    if args.config == "tiny":
+        return W.tiny_cache(args.seed if args.seed is not None else 101)
+    import torch
+    free, _ = torch.cuda.mem_get_info()
+    budget = min(240 * 2 ** 30, int(0.85 * free))
+    return W.llama3_70b_h2o(args.seed if args.seed is not None else 501, keep=args.keep,
+                            dtype=args.kv_dtype, pool_bytes=budget)
+
+
+def recorded_traffic(config: str):
+    """HBM bytes per repack launch from the committed rocprofv3 --pmc summary, if it was
+    taken on the current kernel source; None otherwise."""
+    path = os.path.join(PROFILES, f"repack_{config}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
+    m_bytes = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_sha or not m_bytes:
+        return None
+    sha = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    return float(m_bytes.group(1)) if sha == m_sha.group(1) else None
+
+
+def cpu_baseline(inp, planes: int):
+    """The CPU oracle as it stands, on the full metadata and `planes` planes of host KV."""
+    import numpy as np
+    from oracle.repack import oracle_repack_inputs
+    from paper_2608_13263_amd import workloads as W
+    sh = inp.shape
+    planes = max(2, min(planes, sh.num_planes)) // 2 * 2
+    sample_shape = W.KVShape(planes // 2, sh.num_kv_heads, sh.head_dim, sh.block_size, sh.dtype)
+    n = planes * inp.num_blocks * sh.block_size * sh.row_bytes
+    rng = np.random.Generator(np.random.PCG64(17))
+    kv = np.frombuffer(rng.bytes(n), dtype=np.uint8).reshape(
+        planes, inp.num_blocks * sh.block_size, sh.row_bytes)
+    t0 = time.perf_counter()
+    res = oracle_repack_inputs(inp, kv)
+    dt = time.perf_counter() - t0
+    live = int(np.asarray(res.live_count, dtype=np.int64)[np.asarray(res.admitted) == 1].sum())
+    bytes_alg = 2 * live * sample_shape.token_bytes
+    ncpu = len(os.sched_getaffinity(0))
+    return {"value": round(bytes_alg / dt / 1e9, 3), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{inp.name}: full metadata, {planes} of {sh.num_planes} KV planes "
+                      f"({n / 2**30:.1f} GiB host), {live} live tokens, {dt:.2f} s; numpy "
+                      f"single-threaded, 1 core used of {ncpu} available",
+            "seconds": round(dt, 3),
+            "live_tokens_per_ms": round(live * planes / sh.num_planes / (dt * 1e3), 3)}
+
+
+def run_copy(args):
+    """A plain device-to-device copy of known size: the practical HBM ceiling, and the
+    calibration kernel for the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    n = int(args.copy_gib * 2 ** 30)
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    src.fill_(3)
+    dst = torch.empty_like(src)
+    for _ in range(args.warmup):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for a, b in evs:
+        a.record()
+        dst.copy_(src)
+        b.record()
+    torch.cuda.synchronize()
+    ms = sum(a.elapsed_time(b) for a, b in evs) / len(evs)
+    gbs = 2 * n / (ms / 1e3) / 1e9
+    print(json.dumps({"mode": "copy", "bytes_each_way": n, "ms": round(ms, 4),
+                      "GBps_read_plus_write": round(gbs, 1),
+                      "frac_of_8TBps": round(gbs / HBM_PEAK_GBS, 4)}), flush=True)
+
+
+def main(argv=None):
+    args = parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the repack shards by request (each GPU owns "
+              f"its requests and its block pool) with no cross-GPU traffic, so there is no "
+              f"multi-GPU path to time; got --gpus {args.gpus}", file=sys.stderr)
+        return 2
+    import torch
+    from paper_2608_13263_amd import binding as B
+    B.load_library()
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU (MI355X, gfx950)")
+    if args.mode == "copy":
+        return run_copy(args)
+
+    t_setup = time.perf_counter()
+    inp = make_workload(args)
+    from paper_2608_13263_amd import workloads as W
+    sh = inp.shape
+    log(f"{inp.name}: {inp.num_reqs} requests, {inp.num_tokens} tokens, pool "
+        f"{inp.num_blocks} blocks = {inp.pool_bytes() / 2**30:.1f} GiB")
+    kv = W.kv_device(sh, inp.num_blocks, 1)
+    cache = B.KVCache(kv, sh.num_layers, sh.num_kv_heads, sh.head_dim, sh.block_size)
+    batch = B.Batch.from_inputs(inp)
+    plan = B.Plan.allocate(batch, sh.block_size)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+    log(f"setup {time.perf_counter() - t_setup:.1f} s; warmup {args.warmup} steps")
+
+    def step(ev=None):
+        B.build_token_table(cache, batch, plan, stream)
+        if ev is not None:
+            ev[0].record(stream)
+        B.repack_ex(cache, batch, plan, args.variant, args.grid, args.order, stream)
+        if ev is not None:
+            ev[1].record(stream)
+        B.free_blocks(batch, plan, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    log(f"timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    repack_ms = [a.elapsed_time(b) for a, b in evs]
+    repack_avg = sum(repack_ms) / len(repack_ms)
+
+    counters = plan.counters.cpu().tolist()
+    if counters[3] != 0:
+        raise SystemExit(f"device status {B.STATUS.get(counters[3], counters[3])}")
+    R = inp.num_reqs
+    live = plan.live_count[:R].to(torch.int64)
+    adm = plan.admitted[:R].to(torch.int64)
+    moved_tokens = int((live * adm).sum().item())
+    bytes_alg = 2 * moved_tokens * sh.token_bytes
+    value = bytes_alg / (ms_per_step / 1e3) / 1e9
+    achieved = bytes_alg / (repack_avg / 1e3) / 1e9
+    traffic = recorded_traffic(args.config)
+    log(f"step {ms_per_step:.3f} ms, repack {repack_avg:.3f} ms "
+        f"(min {min(repack_ms):.3f}), {achieved:.0f} GB/s repack")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"CPU oracle on {args.cpu_planes} planes")
+        cpu = cpu_baseline(inp, args.cpu_planes)
+
+    out = {
+        "metric": "repacked KV GB/s (read+write) as % of HBM peak; live tokens repacked/ms",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8",
+        "data": "synthetic",
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "live_tokens_per_ms": round(moved_tokens / ms_per_step, 1),
+        "repack_ms": round(repack_avg, 4),
+        "repack_ms_min": round(min(repack_ms), 4),
+        "config": {
+            "workload": inp.name,
+            "recipe": inp.note,
+            "layers": sh.num_layers, "kv_heads": sh.num_kv_heads, "head_dim": sh.head_dim,
+            "block_size": sh.block_size, "kv_dtype": sh.dtype, "requests": inp.num_reqs,
+            "tokens": inp.num_tokens, "live_tokens_repacked": moved_tokens,
+            "pool_blocks": inp.num_blocks, "pool_gib": round(inp.pool_bytes() / 2 ** 30, 2),
+            "used_blocks": counters[0], "admitted": counters[1], "freed_blocks": counters[2],
+            "bytes_alg_per_step": bytes_alg, "variant": args.variant, "grid": args.grid,
+            "order": args.order,
+        },
+        "roofline": {
+            "bound": "hbm", "kernel": "repack_direct_kernel",
+            "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

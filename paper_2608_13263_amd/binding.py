@@ -1,0 +1,243 @@
+"""ctypes binding of libvtoken.so (include/vtoken.h): argument marshalling only.
+
+Every step of the repack runs in the library's HIP kernels; this module turns torch device
+tensors into the C structs, passes the current HIP stream and raises on a negative status.
+It never falls back to another implementation: without the built library, or without a
+GPU, the calls raise.
+
+    cache = KVCache(kv_tensor, num_layers, num_kv_heads, head_dim, block_size)
+    batch = Batch.from_host(seq_lens, tok_indptr, bt_indptr, block_ids, live, free_list)
+    plan  = Plan.allocate(batch, block_size)
+    build_token_table(cache, batch, plan)
+    repack(cache, batch, plan)
+    free_blocks(batch, plan)             # plan.freed[:plan.counters[2]]
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libvtoken.so")
+
+VTOKEN_OK = 0
+STATUS = {
+    0: "VTOKEN_OK", -1: "VTOKEN_ERR_NULL", -2: "VTOKEN_ERR_SHAPE", -3: "VTOKEN_ERR_CAPACITY",
+    -4: "VTOKEN_ERR_HIP", -5: "VTOKEN_ERR_ARGUMENT", -10: "VTOKEN_ERR_BLOCK_RANGE",
+    -11: "VTOKEN_ERR_BT_LEN", -12: "VTOKEN_ERR_TOK_LEN",
+}
+STATUS_CODE = {v: k for k, v in STATUS.items()}
+
+
+class VTokenError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {STATUS.get(status, status)}")
+        self.status = status
+
+
+class CCache(ctypes.Structure):
+    _fields_ = [("kv", ctypes.c_void_p), ("num_layers", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("block_size", ctypes.c_int32), ("num_blocks", ctypes.c_int32),
+                ("elem_bytes", ctypes.c_int32)]
+
+
+class CBatch(ctypes.Structure):
+    _fields_ = [("num_reqs", ctypes.c_int32), ("num_tokens", ctypes.c_int64),
+                ("num_bt_entries", ctypes.c_int64), ("seq_lens", ctypes.c_void_p),
+                ("tok_indptr", ctypes.c_void_p), ("bt_indptr", ctypes.c_void_p),
+                ("block_ids", ctypes.c_void_p), ("live", ctypes.c_void_p),
+                ("free_list", ctypes.c_void_p), ("free_len", ctypes.c_int32)]
+
+
+class CPlan(ctypes.Structure):
+    _fields_ = [("token_slot", ctypes.c_void_p), ("live_count", ctypes.c_void_p),
+                ("admitted", ctypes.c_void_p), ("dst_indptr", ctypes.c_void_p),
+                ("new_bt_indptr", ctypes.c_void_p), ("new_block_ids", ctypes.c_void_p),
+                ("src_plan", ctypes.c_void_p), ("freed_indptr", ctypes.c_void_p),
+                ("counters", ctypes.c_void_p), ("new_bt_capacity", ctypes.c_int64),
+                ("src_plan_capacity", ctypes.c_int64)]
+
+
+class CRepackOptions(ctypes.Structure):
+    _fields_ = [("variant", ctypes.c_int32), ("grid", ctypes.c_int32),
+                ("order", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+# Every extern "C" symbol of include/vtoken.h with its ctypes signature.
+_SIGNATURES = {
+    "vtoken_build_token_table": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
+                                                  ctypes.POINTER(CPlan), ctypes.c_void_p]),
+    "vtoken_repack": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
+                                       ctypes.POINTER(CPlan), ctypes.c_void_p]),
+    "vtoken_repack_ex": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
+                                          ctypes.POINTER(CPlan), ctypes.POINTER(CRepackOptions),
+                                          ctypes.c_void_p]),
+    "vtoken_free_blocks": (ctypes.c_int32, [ctypes.POINTER(CBatch), ctypes.POINTER(CPlan),
+                                            ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]),
+    "vtoken_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
+    "vtoken_version": (ctypes.c_int32, []),
+}
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libvtoken.so (built by paper_2608_13263_amd.build) and set the signatures."""
+    global _lib
+    if _lib is not None and path == LIB_PATH:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with "
+                           "`python -m paper_2608_13263_amd.build` (hipcc, gfx950)")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    if path == LIB_PATH:
+        _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().vtoken_status_string(int(status)).decode()
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _check(status: int, where: str):
+    if status != VTOKEN_OK:
+        raise VTokenError(status, where)
+
+
+def _stream(stream) -> int:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+
+
+class KVCache:
+    """A paged KV cache tensor [2L][num_blocks][S][H][D] (any 1- or 2-byte dtype)."""
+
+    def __init__(self, kv, num_layers: int, num_kv_heads: int, head_dim: int, block_size: int):
+        if not kv.is_cuda or not kv.is_contiguous():
+            raise ValueError("kv must be a contiguous device tensor")
+        self.kv = kv
+        self.num_layers, self.num_kv_heads = int(num_layers), int(num_kv_heads)
+        self.head_dim, self.block_size = int(head_dim), int(block_size)
+        self.elem_bytes = kv.element_size()
+        per_block = 2 * self.num_layers * block_size * num_kv_heads * head_dim
+        if kv.numel() % per_block:
+            raise ValueError("kv size is not a whole number of blocks")
+        self.num_blocks = kv.numel() // per_block
+
+    def c(self) -> CCache:
+        return CCache(_ptr(self.kv), self.num_layers, self.num_kv_heads, self.head_dim,
+                      self.block_size, self.num_blocks, self.elem_bytes)
+
+
+class Batch:
+    """Device-resident request batch (CSR), matching vtoken_batch."""
+
+    def __init__(self, seq_lens, tok_indptr, bt_indptr, block_ids, live, free_list):
+        self.seq_lens, self.tok_indptr, self.bt_indptr = seq_lens, tok_indptr, bt_indptr
+        self.block_ids, self.live, self.free_list = block_ids, live, free_list
+        self.num_reqs = int(seq_lens.numel())
+        self.num_tokens = int(live.numel())
+        self.num_bt_entries = int(block_ids.numel())
+        self.free_len = int(free_list.numel())
+
+    @classmethod
+    def from_host(cls, seq_lens, tok_indptr, bt_indptr, block_ids, live, free_list,
+                  device="cuda"):
+        import numpy as np
+        import torch
+
+        def i32(x):
+            return torch.from_numpy(np.ascontiguousarray(x, dtype=np.int32)).to(device)
+        return cls(i32(seq_lens), i32(tok_indptr), i32(bt_indptr), i32(block_ids),
+                   torch.from_numpy(np.ascontiguousarray(live, dtype=np.uint8)).to(device),
+                   i32(free_list))
+
+    @classmethod
+    def from_inputs(cls, inp, device="cuda"):
+        return cls.from_host(inp.seq_lens, inp.tok_indptr, inp.bt_indptr, inp.block_ids,
+                             inp.live, inp.free_list, device)
+
+    def c(self) -> CBatch:
+        return CBatch(self.num_reqs, self.num_tokens, self.num_bt_entries, _ptr(self.seq_lens),
+                      _ptr(self.tok_indptr), _ptr(self.bt_indptr), _ptr(self.block_ids),
+                      _ptr(self.live), _ptr(self.free_list), self.free_len)
+
+
+class Plan:
+    """Caller-allocated outputs (vtoken_plan) plus the freed-list buffer."""
+
+    FIELDS = ("token_slot", "live_count", "admitted", "dst_indptr", "new_bt_indptr",
+              "new_block_ids", "src_plan", "freed_indptr", "counters")
+
+    def __init__(self, **tensors):
+        for k in self.FIELDS + ("freed",):
+            setattr(self, k, tensors[k])
+
+    @classmethod
+    def allocate(cls, batch: Batch, block_size: int, device="cuda"):
+        import torch
+        R, T, M, f = batch.num_reqs, batch.num_tokens, batch.num_bt_entries, batch.free_len
+
+        def e(n):
+            return torch.empty(max(int(n), 1), dtype=torch.int32, device=device)
+        return cls(token_slot=e(T), live_count=e(R), admitted=e(R), dst_indptr=e(R + 1),
+                   new_bt_indptr=e(R + 1), new_block_ids=e(M),
+                   src_plan=e(min(f, M) * block_size), freed_indptr=e(R + 1), counters=e(4),
+                   freed=e(M))
+
+    def c(self) -> CPlan:
+        return CPlan(*(_ptr(getattr(self, k)) for k in self.FIELDS),
+                     int(self.new_block_ids.numel()), int(self.src_plan.numel()))
+
+
+def build_token_table(cache: KVCache, batch: Batch, plan: Plan, stream=None) -> None:
+    lib = load_library()
+    c, b, p = cache.c(), batch.c(), plan.c()
+    _check(lib.vtoken_build_token_table(ctypes.byref(c), ctypes.byref(b), ctypes.byref(p),
+                                        _stream(stream)), "vtoken_build_token_table")
+
+
+def repack(cache: KVCache, batch: Batch, plan: Plan, stream=None) -> None:
+    lib = load_library()
+    c, b, p = cache.c(), batch.c(), plan.c()
+    _check(lib.vtoken_repack(ctypes.byref(c), ctypes.byref(b), ctypes.byref(p),
+                             _stream(stream)), "vtoken_repack")
+
+
+def repack_ex(cache: KVCache, batch: Batch, plan: Plan, variant: int = 0, grid: int = 0,
+              order: int = 0, stream=None) -> None:
+    lib = load_library()
+    c, b, p = cache.c(), batch.c(), plan.c()
+    o = CRepackOptions(variant, grid, order, 0)
+    _check(lib.vtoken_repack_ex(ctypes.byref(c), ctypes.byref(b), ctypes.byref(p),
+                                ctypes.byref(o), _stream(stream)), "vtoken_repack_ex")
+
+
+def free_blocks(batch: Batch, plan: Plan, freed=None, stream=None) -> None:
+    lib = load_library()
+    b, p = batch.c(), plan.c()
+    out = plan.freed if freed is None else freed
+    _check(lib.vtoken_free_blocks(ctypes.byref(b), ctypes.byref(p), _ptr(out),
+                                  int(out.numel()), _stream(stream)), "vtoken_free_blocks")
+
+
+def run_pass(cache: KVCache, batch: Batch, plan: Optional[Plan] = None, stream=None) -> Plan:
+    """The three calls of one repack pass, enqueued in order on one stream."""
+    if plan is None:
+        plan = Plan.allocate(batch, cache.block_size, device=cache.kv.device)
+    build_token_table(cache, batch, plan, stream)
+    repack(cache, batch, plan, stream)
+    free_blocks(batch, plan, stream=stream)
+    return plan

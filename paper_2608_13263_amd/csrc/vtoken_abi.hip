@@ -1,0 +1,193 @@
+// C ABI of the vToken repack (include/vtoken.h): host-side argument validation and launch.
+// Nothing here allocates, synchronises or keeps pointers; each call enqueues kernels on the
+// caller's stream and returns.
+#include <stdint.h>
+
+#include "vtoken_internal.h"
+
+namespace {
+
+constexpr int64_t kInt32Limit = 2147483647LL;
+
+vtoken_status check_cache(const vtoken_cache* c) {
+  if (c == nullptr || c->kv == nullptr) return VTOKEN_ERR_NULL;
+  if (c->num_layers <= 0 || c->num_kv_heads <= 0 || c->head_dim <= 0 || c->block_size <= 0 ||
+      c->num_blocks <= 0) {
+    return VTOKEN_ERR_SHAPE;
+  }
+  if (c->elem_bytes != 1 && c->elem_bytes != 2) return VTOKEN_ERR_SHAPE;
+  const int64_t row = (int64_t)c->num_kv_heads * c->head_dim * c->elem_bytes;
+  if (row % 16 != 0 || row > kInt32Limit) return VTOKEN_ERR_SHAPE;
+  if ((int64_t)c->num_blocks * c->block_size > kInt32Limit) return VTOKEN_ERR_SHAPE;
+  if ((int64_t)c->block_size * (row / 16) > kInt32Limit) return VTOKEN_ERR_SHAPE;
+  return VTOKEN_OK;
+}
+
+vtoken_status check_batch(const vtoken_batch* b) {
+  if (b == nullptr) return VTOKEN_ERR_NULL;
+  if (b->num_reqs < 0 || b->num_tokens < 0 || b->num_bt_entries < 0 || b->free_len < 0) {
+    return VTOKEN_ERR_SHAPE;
+  }
+  if (b->num_tokens > kInt32Limit || b->num_bt_entries > kInt32Limit ||
+      (int64_t)b->num_reqs + 1 > kInt32Limit) {
+    return VTOKEN_ERR_SHAPE;
+  }
+  if (b->tok_indptr == nullptr || b->bt_indptr == nullptr) return VTOKEN_ERR_NULL;
+  if (b->num_reqs > 0 && b->seq_lens == nullptr) return VTOKEN_ERR_NULL;
+  if (b->num_tokens > 0 && b->live == nullptr) return VTOKEN_ERR_NULL;
+  if (b->num_bt_entries > 0 && b->block_ids == nullptr) return VTOKEN_ERR_NULL;
+  if (b->free_len > 0 && b->free_list == nullptr) return VTOKEN_ERR_NULL;
+  return VTOKEN_OK;
+}
+
+int64_t min_src_plan_capacity(const vtoken_batch* b, int32_t block_size) {
+  const int64_t f = b->free_len < b->num_bt_entries ? b->free_len : b->num_bt_entries;
+  return f * block_size;
+}
+
+vtoken_status check_plan(const vtoken_plan* p, const vtoken_batch* b, int32_t block_size) {
+  if (p == nullptr) return VTOKEN_ERR_NULL;
+  if (p->dst_indptr == nullptr || p->new_bt_indptr == nullptr || p->freed_indptr == nullptr ||
+      p->counters == nullptr) {
+    return VTOKEN_ERR_NULL;
+  }
+  if (b->num_tokens > 0 && p->token_slot == nullptr) return VTOKEN_ERR_NULL;
+  if (b->num_reqs > 0 && (p->live_count == nullptr || p->admitted == nullptr)) {
+    return VTOKEN_ERR_NULL;
+  }
+  if (b->num_bt_entries > 0 && p->new_block_ids == nullptr) return VTOKEN_ERR_NULL;
+  const int64_t plan_min = min_src_plan_capacity(b, block_size);
+  if (plan_min > 0 && p->src_plan == nullptr) return VTOKEN_ERR_NULL;
+  if (p->new_bt_capacity < b->num_bt_entries) return VTOKEN_ERR_CAPACITY;
+  if (p->src_plan_capacity < plan_min) return VTOKEN_ERR_CAPACITY;
+  return VTOKEN_OK;
+}
+
+vtoken::MetaArgs meta_args(const vtoken_cache* c, const vtoken_batch* b, const vtoken_plan* p) {
+  vtoken::MetaArgs a;
+  a.seq_lens = b->seq_lens;
+  a.tok_indptr = b->tok_indptr;
+  a.bt_indptr = b->bt_indptr;
+  a.block_ids = b->block_ids;
+  a.live = b->live;
+  a.free_list = b->free_list;
+  a.num_reqs = b->num_reqs;
+  a.num_tokens = static_cast<int32_t>(b->num_tokens);
+  a.num_bt_entries = static_cast<int32_t>(b->num_bt_entries);
+  a.free_len = b->free_len;
+  a.block_size = c->block_size;
+  a.num_blocks = c->num_blocks;
+  a.token_slot = p->token_slot;
+  a.live_count = p->live_count;
+  a.admitted = p->admitted;
+  a.dst_indptr = p->dst_indptr;
+  a.new_bt_indptr = p->new_bt_indptr;
+  a.new_block_ids = p->new_block_ids;
+  a.src_plan = p->src_plan;
+  a.freed_indptr = p->freed_indptr;
+  a.counters = p->counters;
+  a.new_bt_capacity = p->new_bt_capacity;
+  a.src_plan_capacity = p->src_plan_capacity;
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+vtoken_status vtoken_build_token_table(const vtoken_cache* cache, const vtoken_batch* batch,
+                                       const vtoken_plan* plan, hipStream_t stream) {
+  vtoken_status s = check_cache(cache);
+  if (s != VTOKEN_OK) return s;
+  if ((s = check_batch(batch)) != VTOKEN_OK) return s;
+  if ((s = check_plan(plan, batch, cache->block_size)) != VTOKEN_OK) return s;
+  const vtoken::MetaArgs a = meta_args(cache, batch, plan);
+  return vtoken::launch_build(a, stream) == hipSuccess ? VTOKEN_OK : VTOKEN_ERR_HIP;
+}
+
+vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* batch,
+                               const vtoken_plan* plan, const vtoken_repack_options* options,
+                               hipStream_t stream) {
+  vtoken_status s = check_cache(cache);
+  if (s != VTOKEN_OK) return s;
+  if ((s = check_batch(batch)) != VTOKEN_OK) return s;
+  if (plan == nullptr || plan->counters == nullptr) return VTOKEN_ERR_NULL;
+  const int64_t plan_min = min_src_plan_capacity(batch, cache->block_size);
+  if (plan_min > 0 && plan->src_plan == nullptr) return VTOKEN_ERR_NULL;
+  if (plan->src_plan_capacity < plan_min) return VTOKEN_ERR_CAPACITY;
+  int variant = 0, grid = 0, order = 0;
+  if (options != nullptr) {
+    variant = options->variant;
+    grid = options->grid;
+    order = options->order;
+  }
+  if (variant < 0 || variant > 2 || grid < 0 || (order != 0 && order != 1)) {
+    return VTOKEN_ERR_ARGUMENT;
+  }
+  // the copy never needs more destination blocks than the free list or the plan holds
+  const int64_t by_plan = plan->src_plan_capacity / cache->block_size;
+  int64_t max_used = batch->free_len < by_plan ? batch->free_len : by_plan;
+  if (max_used == 0) return VTOKEN_OK;  // nothing can have been admitted
+  vtoken::CopyArgs a;
+  a.kv = static_cast<uint8_t*>(cache->kv);
+  a.row_bytes = (int64_t)cache->num_kv_heads * cache->head_dim * cache->elem_bytes;
+  a.plane_bytes = (int64_t)cache->num_blocks * cache->block_size * a.row_bytes;
+  a.num_planes = 2 * cache->num_layers;
+  a.block_size = cache->block_size;
+  a.num_blocks = cache->num_blocks;
+  a.num_slots = cache->num_blocks * cache->block_size;
+  a.row_units = static_cast<int32_t>(a.row_bytes / 16);
+  a.chunk_units = cache->block_size * a.row_units;
+  a.max_used = static_cast<int32_t>(max_used);
+  a.src_plan = plan->src_plan;
+  a.free_list = batch->free_list;
+  a.counters = plan->counters;
+  return vtoken::launch_repack(a, variant, grid, order, stream) == hipSuccess ? VTOKEN_OK
+                                                                              : VTOKEN_ERR_HIP;
+}
+
+vtoken_status vtoken_repack(const vtoken_cache* cache, const vtoken_batch* batch,
+                            const vtoken_plan* plan, hipStream_t stream) {
+  return vtoken_repack_ex(cache, batch, plan, nullptr, stream);
+}
+
+vtoken_status vtoken_free_blocks(const vtoken_batch* batch, const vtoken_plan* plan,
+                                 int32_t* freed, int64_t freed_capacity, hipStream_t stream) {
+  vtoken_status s = check_batch(batch);
+  if (s != VTOKEN_OK) return s;
+  if (plan == nullptr || plan->counters == nullptr || plan->freed_indptr == nullptr) {
+    return VTOKEN_ERR_NULL;
+  }
+  if (batch->num_reqs > 0 && plan->admitted == nullptr) return VTOKEN_ERR_NULL;
+  if (freed_capacity < batch->num_bt_entries) return VTOKEN_ERR_CAPACITY;
+  if (batch->num_bt_entries > 0 && freed == nullptr) return VTOKEN_ERR_NULL;
+  vtoken::MetaArgs a = {};
+  a.bt_indptr = batch->bt_indptr;
+  a.block_ids = batch->block_ids;
+  a.num_reqs = batch->num_reqs;
+  a.num_bt_entries = static_cast<int32_t>(batch->num_bt_entries);
+  a.admitted = plan->admitted;
+  a.freed_indptr = plan->freed_indptr;
+  a.counters = plan->counters;
+  return vtoken::launch_free(a, freed, freed_capacity, stream) == hipSuccess ? VTOKEN_OK
+                                                                            : VTOKEN_ERR_HIP;
+}
+
+const char* vtoken_status_string(int32_t status) {
+  switch (status) {
+    case VTOKEN_OK: return "VTOKEN_OK";
+    case VTOKEN_ERR_NULL: return "VTOKEN_ERR_NULL: a required pointer is NULL";
+    case VTOKEN_ERR_SHAPE: return "VTOKEN_ERR_SHAPE: invalid cache geometry or batch sizes";
+    case VTOKEN_ERR_CAPACITY: return "VTOKEN_ERR_CAPACITY: an output buffer is too small";
+    case VTOKEN_ERR_HIP: return "VTOKEN_ERR_HIP: the HIP runtime reported an error";
+    case VTOKEN_ERR_ARGUMENT: return "VTOKEN_ERR_ARGUMENT: invalid repack option";
+    case VTOKEN_ERR_BLOCK_RANGE: return "VTOKEN_ERR_BLOCK_RANGE: block id outside the pool";
+    case VTOKEN_ERR_BT_LEN: return "VTOKEN_ERR_BT_LEN: block table length != ceil(len/S)";
+    case VTOKEN_ERR_TOK_LEN: return "VTOKEN_ERR_TOK_LEN: token range != sequence length";
+    default: return "unknown vtoken status";
+  }
+}
+
+int32_t vtoken_version(void) { return 100; }
+
+}  // extern "C"

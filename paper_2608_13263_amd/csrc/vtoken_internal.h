@@ -1,0 +1,76 @@
+// Internal declarations shared by the kernels (vtoken_kernels.hip) and the C ABI front end
+// (vtoken_abi.hip). Not installed; the public interface is include/vtoken.h.
+#pragma once
+
+#include <stdint.h>
+#include <hip/hip_runtime.h>
+
+#include "vtoken.h"
+
+namespace vtoken {
+
+// Launch geometry of the metadata kernels.
+constexpr int kScanThreads = 1024;              // one workgroup per request
+constexpr int kScanWaves = kScanThreads / 64;   // wave64 on CDNA4
+constexpr int kScanBallots = 8;                 // ballots per wave per tile
+constexpr int kScanTile = kScanThreads * kScanBallots;  // tokens per tile (8192)
+constexpr int kAdmitThreads = 1024;             // single workgroup over requests
+constexpr int kFreeThreads = 256;
+
+// Copy kernel geometry: 256 threads, each moving 16-byte units.
+constexpr int kCopyThreads = 256;
+
+struct MetaArgs {
+  // batch
+  const int32_t* seq_lens;
+  const int32_t* tok_indptr;
+  const int32_t* bt_indptr;
+  const int32_t* block_ids;
+  const uint8_t* live;
+  const int32_t* free_list;
+  int32_t num_reqs;
+  int32_t num_tokens;
+  int32_t num_bt_entries;
+  int32_t free_len;
+  // cache geometry
+  int32_t block_size;
+  int32_t num_blocks;
+  // plan
+  int32_t* token_slot;
+  int32_t* live_count;
+  int32_t* admitted;
+  int32_t* dst_indptr;
+  int32_t* new_bt_indptr;
+  int32_t* new_block_ids;
+  int32_t* src_plan;
+  int32_t* freed_indptr;
+  int32_t* counters;
+  int64_t new_bt_capacity;
+  int64_t src_plan_capacity;
+};
+
+struct CopyArgs {
+  uint8_t* kv;
+  int64_t plane_bytes;      // num_blocks * S * row_bytes
+  int64_t row_bytes;        // H * D * elem_bytes, a multiple of 16
+  int32_t num_planes;       // 2 * L
+  int32_t block_size;       // S
+  int32_t num_blocks;
+  int32_t num_slots;        // num_blocks * S
+  int32_t row_units;        // row_bytes / 16
+  int32_t chunk_units;      // S * row_units
+  int32_t max_used;         // upper bound on counters[0] the buffers can hold
+  const int32_t* src_plan;
+  const int32_t* free_list;
+  const int32_t* counters;
+};
+
+hipError_t launch_build(const MetaArgs& a, hipStream_t stream);
+hipError_t launch_free(const MetaArgs& a, int32_t* freed, int64_t freed_capacity,
+                       hipStream_t stream);
+// variant/grid/order as in vtoken_repack_options; returns hipErrorInvalidValue for an
+// unknown variant or order.
+hipError_t launch_repack(const CopyArgs& a, int variant, int grid, int order,
+                         hipStream_t stream);
+
+}  // namespace vtoken

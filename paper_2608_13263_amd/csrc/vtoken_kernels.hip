@@ -1,0 +1,517 @@
+// HIP kernels of the vToken repack for CDNA4 (gfx950, wave64).
+//
+//   scan_kernel    one workgroup per request: exclusive scan of the live mask with wave
+//                  ballots (token table of Sec. 3.2, order-preserving fill of Sec. 3.3.3);
+//                  also validates the request's CSR ranges and block ids.
+//   admit_kernel   one workgroup over all requests: destination need ceil(live/S),
+//                  strict-gain test (Sec. 3.3.3, I4 of Sec. 3.5), prefix admission against
+//                  the free list (Sec. 3.3.2), and the CSR offsets of every output.
+//   table_kernel   one workgroup per request: new block table, token slots
+//                  (slot = block * S + offset, Sec. 3.4) and the per-destination source plan.
+//   repack kernel  the gather copy (Sec. 3.3, 3.3.4): persistent grid over
+//                  (destination block, plane) work items; 16-byte vector loads of the
+//                  scattered source rows, one contiguous destination chunk per item.
+//   free_kernel    the freed list: old blocks of admitted requests (Sec. 3.3.4).
+//
+// All kernels read the status word plan->counters[3] written by admit_kernel and do
+// nothing when it is set; every dereference of caller data is bounds-checked.
+#include <limits.h>
+
+#include "vtoken_internal.h"
+
+namespace vtoken {
+namespace {
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+// Number of set bits of a wave-wide ballot in the lanes below this one.
+__device__ __forceinline__ int lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
+}
+
+__device__ __forceinline__ int wave_inclusive_scan(int v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int t = __shfl_up(v, d, 64);
+    if (lane >= d) v += t;
+  }
+  return v;
+}
+
+// Exclusive scan of NV values per thread across the workgroup; total[k] is the sum.
+template <int NV>
+__device__ __forceinline__ void block_exclusive_scan(int (&v)[NV], int (&total)[NV],
+                                                     int (*lds)[NV]) {
+  const int lane = lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  int incl[NV];
+#pragma unroll
+  for (int k = 0; k < NV; ++k) incl[k] = wave_inclusive_scan(v[k]);
+  if (lane == 63) {
+#pragma unroll
+    for (int k = 0; k < NV; ++k) lds[wave][k] = incl[k];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    int off = 0, tot = 0;
+    for (int w = 0; w < nwaves; ++w) {
+      const int x = lds[w][k];
+      off += (w < wave) ? x : 0;
+      tot += x;
+    }
+    v[k] = off + incl[k] - v[k];
+    total[k] = tot;
+  }
+  __syncthreads();
+}
+
+// ------------------------------------------------------------------------------------------
+// Step 1a: per-request live-mask scan. Writes the rank of every live token (or -1) into
+// token_slot, which table_kernel later turns into the final slot.
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kScanThreads) void scan_kernel(MetaArgs a) {
+  const int r = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int S = a.block_size;
+  const int n = a.seq_lens[r];
+  const int t0 = a.tok_indptr[r], t1 = a.tok_indptr[r + 1];
+  const int b0 = a.bt_indptr[r], b1 = a.bt_indptr[r + 1];
+
+  int code = 0;
+  if (n < 0 || t0 < 0 || t1 > a.num_tokens || (int64_t)t1 - t0 != n) {
+    code = VTOKEN_ERR_TOK_LEN;
+  } else if (b0 < 0 || b1 > a.num_bt_entries ||
+             (int64_t)b1 - b0 != ((int64_t)n + S - 1) / S) {
+    code = VTOKEN_ERR_BT_LEN;
+  }
+  if (code == 0) {
+    int bad = 0;
+    for (int j = b0 + tid; j < b1; j += kScanThreads) {
+      const int blk = a.block_ids[j];
+      bad |= (blk < 0) | (blk >= a.num_blocks);
+    }
+    if (__syncthreads_or(bad)) code = VTOKEN_ERR_BLOCK_RANGE;
+  }
+  if (code != 0) {
+    if (tid == 0) a.live_count[r] = code;  // negative: picked up by admit_kernel
+    return;
+  }
+
+  __shared__ int wave_total[kScanWaves];
+  const uint8_t* lv = a.live + t0;
+  int32_t* out = a.token_slot + t0;
+  int carry = 0;
+  for (int base = 0; base < n; base += kScanTile) {
+    const int wbase = base + wave * (64 * kScanBallots);
+    int rank[kScanBallots];
+    int local = 0;
+#pragma unroll
+    for (int i = 0; i < kScanBallots; ++i) {
+      const int p = wbase + i * 64 + lane;
+      const bool l = (p < n) && (lv[p] != 0);
+      const uint64_t m = __ballot(l);
+      rank[i] = l ? local + lanes_below(m) : -1;
+      local += __popcll(m);
+    }
+    if (lane == 0) wave_total[wave] = local;
+    __syncthreads();
+    int off = carry, tile = 0;
+#pragma unroll
+    for (int w = 0; w < kScanWaves; ++w) {
+      const int x = wave_total[w];
+      off += (w < wave) ? x : 0;
+      tile += x;
+    }
+#pragma unroll
+    for (int i = 0; i < kScanBallots; ++i) {
+      const int p = wbase + i * 64 + lane;
+      if (p < n) out[p] = rank[i] < 0 ? -1 : off + rank[i];
+    }
+    carry += tile;
+    __syncthreads();
+  }
+  if (tid == 0) a.live_count[r] = carry;
+}
+
+// ------------------------------------------------------------------------------------------
+// Step 1b: admission over requests (one workgroup).
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kAdmitThreads) void admit_kernel(MetaArgs a) {
+  __shared__ int lds[kAdmitThreads / 64][4];
+  __shared__ int first_error_req;
+  const int tid = threadIdx.x;
+  const int R = a.num_reqs;
+  const int S = a.block_size;
+  if (tid == 0) first_error_req = INT_MAX;
+  __syncthreads();
+
+  int carry_e = 0, carry_dst = 0, carry_new = 0, carry_freed = 0, n_admitted = 0;
+  for (int base = 0; base < R; base += kAdmitThreads) {
+    const int r = base + tid;
+    const bool valid = r < R;
+    const int c = valid ? a.live_count[r] : 0;
+    if (valid && c < 0) atomicMin(&first_error_req, r);
+    const int m = valid ? a.bt_indptr[r + 1] - a.bt_indptr[r] : 0;
+    const int need = c > 0 ? (c + S - 1) / S : 0;
+    const bool profitable = valid && c >= 0 && need < m;
+    // position of this request's destinations in the free list: needs of every earlier
+    // profitable request (admitted or not - once one is deferred all later ones are)
+    int s1[4] = {profitable ? need : 0, 0, 0, 0};
+    int t1[4];
+    block_exclusive_scan<4>(s1, t1, lds);
+    const bool adm = profitable && (carry_e + s1[0] + need <= a.free_len);
+    int s2[4] = {adm ? need : 0, adm ? need : m, adm ? m : 0, adm ? 1 : 0};
+    int t2[4];
+    block_exclusive_scan<4>(s2, t2, lds);
+    if (valid) {
+      a.admitted[r] = adm ? 1 : 0;
+      a.dst_indptr[r] = carry_dst + s2[0];
+      a.new_bt_indptr[r] = carry_new + s2[1];
+      a.freed_indptr[r] = carry_freed + s2[2];
+    }
+    carry_e += t1[0];
+    carry_dst += t2[0];
+    carry_new += t2[1];
+    carry_freed += t2[2];
+    n_admitted += t2[3];
+  }
+  if (tid == 0) {
+    a.dst_indptr[R] = carry_dst;
+    a.new_bt_indptr[R] = carry_new;
+    a.freed_indptr[R] = carry_freed;
+  }
+  __syncthreads();
+  int status = 0;
+  if (first_error_req != INT_MAX) status = a.live_count[first_error_req];
+  const int used = carry_dst;
+  if (status == 0 && ((int64_t)carry_new > a.new_bt_capacity ||
+                      (int64_t)used * S > a.src_plan_capacity || used > a.free_len)) {
+    status = VTOKEN_ERR_CAPACITY;
+  }
+  if (status == 0) {
+    int bad = 0;
+    for (int j = tid; j < used; j += kAdmitThreads) {
+      const int blk = a.free_list[j];
+      bad |= (blk < 0) | (blk >= a.num_blocks);
+    }
+    if (__syncthreads_or(bad)) status = VTOKEN_ERR_BLOCK_RANGE;
+  }
+  if (tid == 0) {
+    a.counters[0] = status == 0 ? used : 0;
+    a.counters[1] = status == 0 ? n_admitted : 0;
+    a.counters[2] = status == 0 ? carry_freed : 0;
+    a.counters[3] = status;
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Step 1c: token slots, new block tables and the source plan (bulk apply_moves).
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kScanThreads) void table_kernel(MetaArgs a) {
+  if (a.counters[3] != 0) return;
+  const int r = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int S = a.block_size;
+  const int n = a.seq_lens[r];
+  const int32_t* bt = a.block_ids + a.bt_indptr[r];
+  int32_t* ts = a.token_slot + a.tok_indptr[r];
+  int32_t* nbt = a.new_block_ids + a.new_bt_indptr[r];
+  if (a.admitted[r]) {
+    const int o = a.dst_indptr[r];
+    const int need = a.dst_indptr[r + 1] - o;
+    const int32_t* dest = a.free_list + o;
+    int32_t* plan = a.src_plan + (int64_t)o * S;
+    for (int j = tid; j < need; j += kScanThreads) nbt[j] = dest[j];
+    for (int p = tid; p < n; p += kScanThreads) {
+      const int k = ts[p];
+      if (k >= 0) {
+        const int q = p / S;
+        plan[k] = bt[q] * S + (p - q * S);
+        const int qk = k / S;
+        ts[p] = dest[qk] * S + (k - qk * S);
+      }
+    }
+    // destination slots past the last live token: nothing to copy
+    for (int k = a.live_count[r] + tid; k < need * S; k += kScanThreads) plan[k] = -1;
+  } else {
+    const int m = a.bt_indptr[r + 1] - a.bt_indptr[r];
+    for (int j = tid; j < m; j += kScanThreads) nbt[j] = bt[j];
+    for (int p = tid; p < n; p += kScanThreads) {
+      const int k = ts[p];
+      if (k >= 0) {
+        const int q = p / S;
+        ts[p] = bt[q] * S + (p - q * S);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Step 3: freed list.
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kFreeThreads) void free_kernel(MetaArgs a, int32_t* freed,
+                                                            int64_t capacity) {
+  if (a.counters[3] != 0) return;
+  const int r = blockIdx.x;
+  if (!a.admitted[r]) return;
+  const int b0 = a.bt_indptr[r];
+  const int m = a.bt_indptr[r + 1] - b0;
+  const int64_t o = a.freed_indptr[r];
+  if (b0 < 0 || m < 0 || (int64_t)b0 + m > a.num_bt_entries || o < 0) return;
+  for (int j = threadIdx.x; j < m; j += kFreeThreads) {
+    if (o + j < capacity) freed[o + j] = a.block_ids[b0 + j];
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Step 2: the gather-repack. A work item is (destination block g, plane): it gathers up to
+// S rows, each from the source slot src_plan[g*S + j], and writes them as one contiguous
+// chunk of S*row_bytes bytes at block free_list[g] of the same plane. A thread moves
+// 16-byte units; kV units per thread are loaded before any is stored, so every wave keeps
+// kV*1 KiB of reads in flight. Rows are head_dim-contiguous, so a wave's 64 lanes read and
+// write 1 KiB of consecutive bytes per instruction (a whole 2 KiB row takes two).
+// ------------------------------------------------------------------------------------------
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <bool kNT>
+__device__ __forceinline__ u32x4 load16(const u32x4* p) {
+  if constexpr (kNT) {
+    return __builtin_nontemporal_load(p);
+  } else {
+    return *p;
+  }
+}
+
+
+// Source slots of one destination block: with S <= 64, lane j of every wave holds
+// src_plan[g*S + j] and rows are picked with a cross-lane shuffle; otherwise each unit reads
+// its entry from memory. The copy is branch-free so the compiler can keep every load of a
+// round in flight (a conditional load or store would force a full wait on the vector
+// memory counter): lanes of padding rows (src_plan -1, the tail of a request's last block)
+// load row 0 of the same destination block, which is always live and already being read,
+// and their stores go through a buffer resource spanning only the destination chunk with
+// an out-of-range offset, which the hardware drops.
+constexpr uint32_t kBufferDword3 = 0x00020000u;  // raw buffer, 32-bit data format (gfx9)
+constexpr uint32_t kDropOffset = 0x80000000u;    // beyond every chunk: store discarded
+
+// The destination pointer is the same for the whole workgroup; say so, so that the
+// buffer resource lives in scalar registers.
+__device__ __forceinline__ uint8_t* uniform_ptr(uint8_t* p) {
+  const uint64_t x = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(x));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(x >> 32));
+  return reinterpret_cast<uint8_t*>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+template <bool kNT>
+__device__ __forceinline__ void store16_buffer(u32x4 v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, kNT ? 2 : 0);  // aux bit 1: nt
+}
+
+template <int kV, bool kPow2, bool kNT, int kOrder, bool kSmallS, bool kOneRound>
+__global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a) {
+  if (a.counters[3] != 0) return;
+  int used = a.counters[0];
+  used = used < 0 ? 0 : (used > a.max_used ? a.max_used : used);
+  if (used == 0) return;
+  const int P = a.num_planes;
+  const int64_t items = (int64_t)used * P;
+  const int S = a.block_size;
+  const int chunk = a.chunk_units;
+  const uint32_t chunk_bytes = static_cast<uint32_t>(chunk) * 16u;
+  const int U = a.row_units;
+  const int log2u = kPow2 ? __builtin_ctz(static_cast<unsigned>(U)) : 0;
+  const int lane = threadIdx.x & 63;
+  const int tid = static_cast<int>(threadIdx.x);
+  // (hi, lo) = (plane, g) for the plane-major order, (g, plane) for the block-major order
+  const int inner = kOrder == 0 ? used : P;
+  int64_t w = blockIdx.x;
+  if (w >= items) return;
+  int hi = static_cast<int>(w / inner);
+  int lo = static_cast<int>(w - (int64_t)hi * inner);
+  const int step_hi = static_cast<int>(gridDim.x / inner);
+  const int step_lo = static_cast<int>(gridDim.x - (int64_t)step_hi * inner);
+
+  // prefetch of the next item's destination block and plan entry (lanes >= S read entry
+  // S-1 and never use it; the loads are unconditional so no branch splits the copy loop)
+  const int plane_lane = lane < S ? lane : S - 1;
+  int next_g = kOrder == 0 ? lo : hi;
+  int next_dblk = a.free_list[next_g];
+  int next_pv = kSmallS ? a.src_plan[(int64_t)next_g * S + plane_lane] : -1;
+
+  for (; w < items; w += gridDim.x) {
+    const int plane = kOrder == 0 ? hi : lo;
+    const int g = next_g;
+    const int dblk = __builtin_amdgcn_readfirstlane(next_dblk);
+    const int pv = next_pv;
+    lo += step_lo;
+    hi += step_hi;
+    if (lo >= inner) {
+      lo -= inner;
+      ++hi;
+    }
+    // past the last item the prefetch re-reads item 0's entries (in bounds, unused)
+    next_g = (w + gridDim.x < items) ? (kOrder == 0 ? lo : hi) : 0;
+    next_dblk = a.free_list[next_g];
+    if (kSmallS) next_pv = a.src_plan[(int64_t)next_g * S + plane_lane];
+    const bool dst_ok = static_cast<unsigned>(dblk) < static_cast<unsigned>(a.num_blocks);
+    const uint8_t* pbase = a.kv + (int64_t)plane * a.plane_bytes;
+    uint8_t* dptr = uniform_ptr(a.kv + (int64_t)plane * a.plane_bytes +
+                                (dst_ok ? (int64_t)dblk * S * a.row_bytes : 0));
+    const __amdgpu_buffer_rsrc_t drsrc =
+        __builtin_amdgcn_make_buffer_rsrc(dptr, 0, dst_ok ? chunk_bytes : 0u, kBufferDword3);
+    const int32_t* plan = a.src_plan + (int64_t)g * S;
+    int s0 = kSmallS ? __builtin_amdgcn_readlane(pv, 0) : __builtin_amdgcn_readfirstlane(plan[0]);
+    s0 = static_cast<unsigned>(s0) < static_cast<unsigned>(a.num_slots) ? s0 : 0;
+    // kOneRound: the chunk is exactly kCopyThreads*kV units, a compile-time trip count
+    const int rounds_end = kOneRound ? kCopyThreads * kV : chunk;
+    for (int u0 = 0; u0 < rounds_end; u0 += kCopyThreads * kV) {
+      int src[kV];
+      int col[kV];
+      uint32_t off[kV];
+#pragma unroll
+      for (int v = 0; v < kV; ++v) {
+        const int u = u0 + v * kCopyThreads + tid;
+        int j;
+        if (kPow2) {
+          j = u >> log2u;
+          col[v] = u & (U - 1);
+        } else {
+          j = u / U;
+          col[v] = u - j * U;
+        }
+        int s;
+        if (kSmallS) {
+          s = __shfl(pv, j & 63, 64);
+        } else {
+          s = u < chunk ? plan[j] : -1;
+        }
+        const bool ok = (u < chunk) && static_cast<unsigned>(s) < static_cast<unsigned>(a.num_slots);
+        src[v] = ok ? s : s0;
+        off[v] = ok ? static_cast<uint32_t>(u) * 16u : kDropOffset;
+      }
+      u32x4 buf[kV];
+#pragma unroll
+      for (int v = 0; v < kV; ++v) {
+        buf[v] = load16<kNT>(reinterpret_cast<const u32x4*>(pbase + (int64_t)src[v] * a.row_bytes) +
+                             col[v]);
+      }
+#pragma unroll
+      for (int v = 0; v < kV; ++v) store16_buffer<kNT>(buf[v], drsrc, off[v]);
+    }
+  }
+}
+
+int device_cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0) {
+      cus = 256;
+    }
+    cached[dev] = cus;
+  }
+  return cached[dev];
+}
+
+// Persistent launch: by default as many workgroups as fit on the device at once (the
+// occupancy of this kernel, cached per instantiation, times the CU count).
+template <void (*kKernel)(CopyArgs)>
+hipError_t launch_kernel(const CopyArgs& a, int grid, hipStream_t stream) {
+  if (grid <= 0) {
+    static int per_cu = 0;
+    if (per_cu == 0) {
+      int nb = 0;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kKernel, kCopyThreads, 0) !=
+              hipSuccess || nb <= 0) {
+        nb = 4;
+      }
+      per_cu = nb;
+    }
+    grid = per_cu * device_cu_count();
+  }
+  hipLaunchKernelGGL(kKernel, dim3(grid), dim3(kCopyThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+template <int kV, bool kPow2, bool kNT, int kOrder>
+hipError_t launch_direct(const CopyArgs& a, int grid, hipStream_t stream) {
+  if (a.block_size <= 64) {
+    if (a.chunk_units == kCopyThreads * kV) {
+      return launch_kernel<repack_direct_kernel<kV, kPow2, kNT, kOrder, true, true>>(a, grid,
+                                                                                     stream);
+    }
+    return launch_kernel<repack_direct_kernel<kV, kPow2, kNT, kOrder, true, false>>(a, grid,
+                                                                                    stream);
+  }
+  return launch_kernel<repack_direct_kernel<kV, kPow2, kNT, kOrder, false, false>>(a, grid,
+                                                                                   stream);
+}
+
+template <bool kPow2, bool kNT, int kOrder>
+hipError_t launch_direct_v(const CopyArgs& a, int grid, hipStream_t stream) {
+  // enough 16-byte units per thread to cover one chunk, at most 8
+  const int per_thread = a.chunk_units / kCopyThreads;
+  if (per_thread >= 8) return launch_direct<8, kPow2, kNT, kOrder>(a, grid, stream);
+  if (per_thread >= 4) return launch_direct<4, kPow2, kNT, kOrder>(a, grid, stream);
+  if (per_thread >= 2) return launch_direct<2, kPow2, kNT, kOrder>(a, grid, stream);
+  return launch_direct<1, kPow2, kNT, kOrder>(a, grid, stream);
+}
+
+template <bool kNT>
+hipError_t launch_direct_nt(const CopyArgs& a, int grid, int order, hipStream_t stream) {
+  const bool pow2 = (a.row_units & (a.row_units - 1)) == 0;
+  if (order == 0) {
+    return pow2 ? launch_direct_v<true, kNT, 0>(a, grid, stream)
+                : launch_direct_v<false, kNT, 0>(a, grid, stream);
+  }
+  return pow2 ? launch_direct_v<true, kNT, 1>(a, grid, stream)
+              : launch_direct_v<false, kNT, 1>(a, grid, stream);
+}
+
+}  // namespace
+
+hipError_t launch_build(const MetaArgs& a, hipStream_t stream) {
+  if (a.num_reqs > 0) {
+    hipLaunchKernelGGL(scan_kernel, dim3(a.num_reqs), dim3(kScanThreads), 0, stream, a);
+  }
+  hipLaunchKernelGGL(admit_kernel, dim3(1), dim3(kAdmitThreads), 0, stream, a);
+  if (a.num_reqs > 0) {
+    hipLaunchKernelGGL(table_kernel, dim3(a.num_reqs), dim3(kScanThreads), 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_free(const MetaArgs& a, int32_t* freed, int64_t freed_capacity,
+                       hipStream_t stream) {
+  if (a.num_reqs > 0) {
+    hipLaunchKernelGGL(free_kernel, dim3(a.num_reqs), dim3(kFreeThreads), 0, stream, a, freed,
+                       freed_capacity);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_repack(const CopyArgs& a, int variant, int grid, int order,
+                         hipStream_t stream) {
+  if (order != 0 && order != 1) return hipErrorInvalidValue;
+  switch (variant) {
+    case 0:
+    case 2:
+      return launch_direct_nt<true>(a, grid, order, stream);
+    case 1:
+      return launch_direct_nt<false>(a, grid, order, stream);
+    default:
+      return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace vtoken

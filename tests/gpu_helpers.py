@@ -1,0 +1,97 @@
+"""Shared helpers of the GPU tests: run one repack pass through the C ABI and compare every
+output with the CPU oracle."""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle.repack import oracle_repack_inputs
+from paper_2608_13263_amd import workloads as W
+
+
+def torch():
+    import torch as t
+    return t
+
+
+def kv_bytes(kv, shape: W.KVShape):
+    """uint8 host view [2L][num_blocks*S][row_bytes] of a device KV tensor."""
+    t = torch()
+    n = kv.shape[1] * shape.block_size
+    return kv.view(t.uint8).reshape(shape.num_planes, n, shape.row_bytes).cpu().numpy()
+
+
+def gpu_pass(inp: W.RepackInputs, kv, variant=0, grid=0, order=0, label=""):
+    """build_token_table -> repack_ex -> free_blocks on the current stream; returns host
+    copies of every plan output, trimmed to the sizes the counters report."""
+    t = torch()
+    from paper_2608_13263_amd import binding as B
+    print(f"[gpu] {label or inp.name}: R={inp.num_reqs} T={inp.num_tokens} "
+          f"M={inp.num_bt_entries} f={len(inp.free_list)} S={inp.shape.block_size} "
+          f"row={inp.shape.row_bytes}B planes={inp.shape.num_planes} "
+          f"variant={variant} grid={grid} order={order}", flush=True)
+    cache = B.KVCache(kv, inp.shape.num_layers, inp.shape.num_kv_heads, inp.shape.head_dim,
+                      inp.shape.block_size)
+    batch = B.Batch.from_inputs(inp)
+    plan = B.Plan.allocate(batch, inp.shape.block_size)
+    B.build_token_table(cache, batch, plan)
+    B.repack_ex(cache, batch, plan, variant=variant, grid=grid, order=order)
+    B.free_blocks(batch, plan)
+    t.cuda.synchronize()
+    return plan_to_host(plan, inp)
+
+
+def plan_to_host(plan, inp):
+    h = {k: getattr(plan, k).cpu().numpy() for k in plan.FIELDS + ("freed",)}
+    used, n_adm, n_freed, status = (int(x) for x in h["counters"][:4])
+    R, T = inp.num_reqs, inp.num_tokens
+    S = inp.shape.block_size
+    out = dict(status=status, used=used, n_admitted=n_adm, n_freed=n_freed)
+    if status != 0:
+        return out
+    out.update(token_slot=h["token_slot"][:T], live_count=h["live_count"][:R],
+               admitted=h["admitted"][:R], dst_indptr=h["dst_indptr"][:R + 1],
+               new_bt_indptr=h["new_bt_indptr"][:R + 1],
+               freed_indptr=h["freed_indptr"][:R + 1], src_plan=h["src_plan"][:used * S],
+               freed=h["freed"][:n_freed])
+    out["new_block_ids"] = h["new_block_ids"][:int(out["new_bt_indptr"][-1])] if R else \
+        h["new_block_ids"][:0]
+    return out
+
+
+def assert_plan_equal(gpu: dict, orc) -> None:
+    assert gpu["status"] == 0, f"device status {gpu['status']}"
+    assert gpu["used"] == orc.used
+    assert gpu["n_admitted"] == orc.n_admitted
+    assert gpu["n_freed"] == orc.n_freed
+    for key in ("token_slot", "live_count", "admitted", "dst_indptr", "new_bt_indptr",
+                "new_block_ids", "src_plan", "freed_indptr", "freed"):
+        g = np.asarray(gpu[key], dtype=np.int64)
+        o = np.asarray(getattr(orc, key), dtype=np.int64)
+        assert g.shape == o.shape, f"{key}: shape {g.shape} vs oracle {o.shape}"
+        if not np.array_equal(g, o):
+            bad = np.nonzero(g != o)[0]
+            raise AssertionError(f"{key}: {len(bad)} mismatches, first at {bad[:5]}: "
+                                 f"gpu {g[bad[:5]]} oracle {o[bad[:5]]}")
+
+
+def assert_kv_equal(got: np.ndarray, expect: np.ndarray) -> None:
+    if not np.array_equal(got, expect):
+        diff = np.nonzero((got != expect).any(axis=2))
+        raise AssertionError(f"KV bytes differ in {len(diff[0])} rows; first (plane, slot): "
+                             f"{list(zip(diff[0][:5], diff[1][:5]))}")
+
+
+def full_parity(inp: W.RepackInputs, seed: int = 0, variant=0, grid=0, order=0,
+                kv_dtype_shape=None):
+    """Seeded KV on the device, one pass through the C ABI, every output and every KV byte
+    against the oracle run on the pre-call bytes."""
+    t = torch()
+    kv = W.kv_device(inp.shape, inp.num_blocks, seed)
+    before = kv_bytes(kv, inp.shape)
+    orc = oracle_repack_inputs(inp, before)
+    gpu = gpu_pass(inp, kv, variant=variant, grid=grid, order=order)
+    assert_plan_equal(gpu, orc)
+    assert_kv_equal(kv_bytes(kv, inp.shape), orc.kv)
+    del kv
+    t.cuda.empty_cache()
+    return gpu, orc

@@ -1,0 +1,142 @@
+"""The C-ABI library on a host without a GPU: it loads, exports every function that
+include/vtoken.h declares, and its host-side argument checks return the documented status
+codes before any device work (no compute call is made here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_13263_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "vtoken.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(B.LIB_PATH),
+                                reason="libvtoken.so not built (run __graft_entry__.build())")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(vtoken_[a-z_]+)\s*\(", text)))
+
+
+def header_status_codes():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    return {m.group(1): int(m.group(2)) for m in re.finditer(r"(VTOKEN_[A-Z_]+)\s*=\s*(-?\d+)", text)}
+
+
+def test_exports_every_declared_function():
+    lib = B.load_library()
+    names = header_functions()
+    assert {"vtoken_build_token_table", "vtoken_repack", "vtoken_free_blocks"} <= set(names)
+    for name in names:
+        assert hasattr(lib, name), f"{name} declared in vtoken.h but not exported"
+    assert set(names) == set(B._SIGNATURES), "binding signatures out of sync with the header"
+
+
+def test_status_codes_match_binding():
+    codes = header_status_codes()
+    assert codes == B.STATUS_CODE
+    for name, code in codes.items():
+        assert B.status_string(code).startswith(name)
+    assert B.status_string(12345) == "unknown vtoken status"
+    assert B.load_library().vtoken_version() == 100
+
+
+def test_struct_layouts_match_header(tmp_path):
+    """Field offsets and sizes of the ctypes structs equal what the C compiler lays out
+    for include/vtoken.h."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    structs = {"vtoken_cache": B.CCache, "vtoken_batch": B.CBatch, "vtoken_plan": B.CPlan,
+               "vtoken_repack_options": B.CRepackOptions}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "vtoken.h"', "int main(void){"]
+    for cname, cls in structs.items():
+        lines.append(f'printf("{cname} sizeof %zu\\n", sizeof({cname}));')
+        for fname, _ in cls._fields_:
+            lines.append(f'printf("{cname} {fname} %zu\\n", offsetof({cname}, {fname}));')
+    lines.append("return 0;}")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"),
+                    "-I", "/opt/rocm/include", str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout
+    got = {}
+    for line in out.splitlines():
+        cname, field, val = line.split()
+        got[(cname, field)] = int(val)
+    for cname, cls in structs.items():
+        assert got[(cname, "sizeof")] == ctypes.sizeof(cls), cname
+        for fname, _ in cls._fields_:
+            assert got[(cname, fname)] == getattr(cls, fname).offset, (cname, fname)
+
+
+def _fake_ptr():
+    # a non-NULL host address that host validation only compares against NULL
+    return ctypes.cast(ctypes.create_string_buffer(64), ctypes.c_void_p).value
+
+
+def _good():
+    p = _fake_ptr()
+    cache = B.CCache(p, 2, 8, 128, 16, 100, 2)
+    batch = B.CBatch(2, 40, 4, p, p, p, p, p, p, 10)
+    plan = B.CPlan(p, p, p, p, p, p, p, p, p, 4, 4 * 16)
+    return cache, batch, plan
+
+
+@pytest.mark.parametrize("mutate,code", [
+    (lambda c, b, p: setattr(c, "kv", None), "VTOKEN_ERR_NULL"),
+    (lambda c, b, p: setattr(c, "elem_bytes", 4), "VTOKEN_ERR_SHAPE"),
+    (lambda c, b, p: setattr(c, "num_kv_heads", 1) or setattr(c, "head_dim", 4),
+     "VTOKEN_ERR_SHAPE"),                                                 # 8-byte rows
+    (lambda c, b, p: setattr(c, "num_kv_heads", 1) or setattr(c, "head_dim", 3),
+     "VTOKEN_ERR_SHAPE"),                                                 # 6-byte rows
+    (lambda c, b, p: setattr(c, "num_blocks", 2 ** 28), "VTOKEN_ERR_SHAPE"),  # slots >= 2^31
+    (lambda c, b, p: setattr(c, "block_size", 0), "VTOKEN_ERR_SHAPE"),
+    (lambda c, b, p: setattr(b, "num_reqs", -1), "VTOKEN_ERR_SHAPE"),
+    (lambda c, b, p: setattr(b, "num_tokens", 2 ** 31), "VTOKEN_ERR_SHAPE"),
+    (lambda c, b, p: setattr(b, "tok_indptr", None), "VTOKEN_ERR_NULL"),
+    (lambda c, b, p: setattr(b, "live", None), "VTOKEN_ERR_NULL"),
+    (lambda c, b, p: setattr(p, "counters", None), "VTOKEN_ERR_NULL"),
+    (lambda c, b, p: setattr(p, "src_plan", None), "VTOKEN_ERR_NULL"),
+    (lambda c, b, p: setattr(p, "new_bt_capacity", 3), "VTOKEN_ERR_CAPACITY"),
+    (lambda c, b, p: setattr(p, "src_plan_capacity", 4 * 16 - 1), "VTOKEN_ERR_CAPACITY"),
+])
+def test_build_rejects_bad_arguments(mutate, code):
+    lib = B.load_library()
+    cache, batch, plan = _good()
+    mutate(cache, batch, plan)
+    st = lib.vtoken_build_token_table(ctypes.byref(cache), ctypes.byref(batch),
+                                      ctypes.byref(plan), None)
+    assert st == B.STATUS_CODE[code], (st, code)
+
+
+def test_repack_and_free_reject_bad_arguments():
+    lib = B.load_library()
+    cache, batch, plan = _good()
+    opts = B.CRepackOptions(7, 0, 0, 0)
+    assert lib.vtoken_repack_ex(ctypes.byref(cache), ctypes.byref(batch), ctypes.byref(plan),
+                                ctypes.byref(opts), None) == B.STATUS_CODE["VTOKEN_ERR_ARGUMENT"]
+    opts = B.CRepackOptions(0, 0, 2, 0)
+    assert lib.vtoken_repack_ex(ctypes.byref(cache), ctypes.byref(batch), ctypes.byref(plan),
+                                ctypes.byref(opts), None) == B.STATUS_CODE["VTOKEN_ERR_ARGUMENT"]
+    assert lib.vtoken_repack(None, ctypes.byref(batch), ctypes.byref(plan), None) == \
+        B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    assert lib.vtoken_free_blocks(ctypes.byref(batch), ctypes.byref(plan), _fake_ptr(), 3,
+                                  None) == B.STATUS_CODE["VTOKEN_ERR_CAPACITY"]
+    assert lib.vtoken_free_blocks(ctypes.byref(batch), ctypes.byref(plan), None, 4, None) == \
+        B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    # a batch that cannot have admitted anything returns before any launch
+    batch.free_len = 0
+    assert lib.vtoken_repack(ctypes.byref(cache), ctypes.byref(batch), ctypes.byref(plan),
+                             None) == 0
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    with pytest.raises(RuntimeError, match="missing"):
+        B.load_library(str(tmp_path / "libvtoken.so"))

@@ -1,0 +1,205 @@
+"""HIP path vs CPU oracle through the C ABI: bit-exact on every output and every KV byte.
+
+Sizes here finish in seconds on the oracle yet span many 32 KiB copy items, several scan
+tiles and ragged tails; the full Llama-3-8B-shaped cache is covered in
+test_parity_full_gpu.py."""
+import numpy as np
+import pytest
+
+from gpu_helpers import (assert_kv_equal, assert_plan_equal, full_parity, gpu_pass, kv_bytes,
+                         torch)
+from oracle.repack import oracle_repack_inputs
+from paper_2608_13263_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def test_tiny_cache():
+    full_parity(W.tiny_cache(101), seed=1)
+
+
+def test_tiny_cache_other_seed():
+    full_parity(W.tiny_cache(7), seed=2)
+
+
+def test_llama3_8b_random_two_layers():
+    full_parity(W.llama3_8b_random(201, num_layers=2, num_reqs=8), seed=3)
+
+
+def test_llama3_8b_h2o_one_layer():
+    full_parity(W.llama3_8b_h2o(301, num_layers=1, num_reqs=6), seed=4)
+
+
+@pytest.mark.parametrize("dtype", ["fp8_e4m3", "bf16"])
+def test_llama3_70b_shape_block32(dtype):
+    # S = 32; bf16 rows make 64 KiB chunks (two copy rounds per item), fp8 rows 32 KiB
+    inp = W.llama3_70b_h2o(501, keep=0.3, dtype=dtype, num_layers=2, num_reqs=3,
+                           len_range=(3000, 7000))
+    full_parity(inp, seed=5)
+
+
+@pytest.mark.parametrize("keep", [0.1, 0.6])
+def test_llama3_70b_keep_ratios(keep):
+    inp = W.llama3_70b_h2o(502, keep=keep, dtype="fp8_e4m3", num_layers=1, num_reqs=3,
+                           len_range=(2000, 5000))
+    full_parity(inp, seed=6)
+
+
+def _edge_masks(S, rng):
+    return [
+        [],                                       # empty request: nothing to do
+        [0] * 37,                                 # all dead: every block released
+        [1] * 40,                                 # all live: unprofitable, unchanged
+        [1],                                      # single token
+        list((rng.random(2 * S) < 0.5).astype(int)),  # exact multiple of S
+        list((rng.random(3 * S + 5) < 0.3).astype(int)),  # ragged tail
+        [1] + [0] * (4 * S) + [1],                # two live tokens far apart
+        list((rng.random(7 * S + 3) < 0.9).astype(int)),  # mostly live
+    ]
+
+
+@pytest.mark.parametrize("S", [1, 2, 16, 32, 48, 128])
+def test_edge_masks_block_sizes(S):
+    # S = 48 (not a power of two, several copy rounds) and S = 128 (plan read from memory)
+    rng = np.random.default_rng(S)
+    shape = W.KVShape(1, 2, 64, S, "fp16")
+    inp = W.from_masks(_edge_masks(S, rng), shape, free_blocks=64, seed=S)
+    full_parity(inp, seed=S)
+
+
+@pytest.mark.parametrize("heads,dim,dtype", [(3, 8, "fp16"), (1, 8, "fp16"), (1, 16, "fp8_e4m3"),
+                                             (5, 48, "bf16"), (1, 128, "fp8_e4m3")])
+def test_row_geometries(heads, dim, dtype):
+    # rows of 48 B (3 units, not a power of two), 16 B (one unit), 16 B fp8, 480 B, 128 B
+    rng = np.random.default_rng(heads * 1000 + dim)
+    shape = W.KVShape(2, heads, dim, 16, dtype)
+    masks = [list((rng.random(int(n)) < 0.4).astype(int)) for n in rng.integers(1, 300, 12)]
+    full_parity(W.from_masks(masks, shape, free_blocks=80, seed=3), seed=9)
+
+
+@pytest.mark.parametrize("free_blocks", [0, 1, 3, 6])
+def test_headroom_deferral(free_blocks):
+    # a short free list: the admitted requests are a prefix of the profitable ones
+    rng = np.random.default_rng(11)
+    shape = W.KVShape(1, 2, 64, 16, "fp16")
+    masks = [list((rng.random(int(n)) < 0.3).astype(int)) for n in rng.integers(40, 120, 8)]
+    inp = W.from_masks(masks, shape, free_blocks=free_blocks, seed=5)
+    gpu, orc = full_parity(inp, seed=12)
+    assert orc.used <= free_blocks
+
+
+def test_no_requests():
+    shape = W.KVShape(1, 2, 64, 16, "fp16")
+    full_parity(W.from_masks([], shape, free_blocks=8, seed=1), seed=1)
+
+
+def test_nan_payloads_are_copied_bit_exactly():
+    t = torch()
+    inp = W.llama3_8b_random(203, num_layers=1, num_reqs=4, len_range=(300, 900))
+    kv = W.kv_device(inp.shape, inp.num_blocks, 0)
+    g = t.Generator(device="cuda")
+    g.manual_seed(5)
+    raw = kv.view(t.uint8)
+    raw.copy_(t.randint(0, 256, raw.shape, generator=g, device="cuda", dtype=t.uint8))
+    assert t.isnan(kv.float()).any()
+    before = kv_bytes(kv, inp.shape)
+    orc = oracle_repack_inputs(inp, before)
+    gpu = gpu_pass(inp, kv)
+    assert_plan_equal(gpu, orc)
+    assert_kv_equal(kv_bytes(kv, inp.shape), orc.kv)
+
+
+@pytest.mark.parametrize("variant,order,grid", [(1, 0, 0), (2, 0, 0), (2, 1, 0), (1, 1, 7),
+                                                (2, 0, 1), (2, 0, 3), (0, 1, 1)])
+def test_copy_variants_agree(variant, order, grid):
+    inp = W.llama3_8b_random(204, num_layers=2, num_reqs=6, len_range=(500, 2500))
+    full_parity(inp, seed=13, variant=variant, order=order, grid=grid)
+
+
+def test_repack_is_idempotent():
+    t = torch()
+    from paper_2608_13263_amd import binding as B
+    inp = W.llama3_8b_random(205, num_layers=2, num_reqs=6, len_range=(500, 2500))
+    kv = W.kv_device(inp.shape, inp.num_blocks, 3)
+    before = kv_bytes(kv, inp.shape)
+    orc = oracle_repack_inputs(inp, before)
+    cache = B.KVCache(kv, 2, 8, 128, 16)
+    batch = B.Batch.from_inputs(inp)
+    plan = B.Plan.allocate(batch, 16)
+    print("[gpu] idempotence: two passes on unchanged inputs", flush=True)
+    for _ in range(2):
+        B.run_pass(cache, batch, plan)
+        t.cuda.synchronize()
+        assert_kv_equal(kv_bytes(kv, inp.shape), orc.kv)
+
+
+def test_side_stream_and_stream_order():
+    """All three calls on a non-default stream; a consumer on the default stream that waits
+    on an event recorded after free_blocks sees the packed cache (invariant I3)."""
+    t = torch()
+    from paper_2608_13263_amd import binding as B
+    inp = W.llama3_8b_random(206, num_layers=2, num_reqs=6, len_range=(500, 2500))
+    kv = W.kv_device(inp.shape, inp.num_blocks, 4)
+    before = kv_bytes(kv, inp.shape)
+    orc = oracle_repack_inputs(inp, before)
+    cache = B.KVCache(kv, 2, 8, 128, 16)
+    batch = B.Batch.from_inputs(inp)
+    plan = B.Plan.allocate(batch, 16)
+    side = t.cuda.Stream()
+    side.wait_stream(t.cuda.current_stream())
+    print("[gpu] side stream pass", flush=True)
+    with t.cuda.stream(side):
+        B.run_pass(cache, batch, plan, stream=side)
+        done = t.cuda.Event()
+        done.record(side)
+    t.cuda.current_stream().wait_event(done)
+    snap = kv.clone()          # runs on the default stream, after the event
+    t.cuda.synchronize()
+    assert_kv_equal(kv_bytes(snap, inp.shape), orc.kv)
+
+
+# ------------------------------------------------------------------------------------------
+# device-detected errors: status word set, no KV byte written
+# ------------------------------------------------------------------------------------------
+
+def _error_case(mutate, expect):
+    t = torch()
+    from paper_2608_13263_amd import binding as B
+    inp = W.llama3_8b_random(207, num_layers=1, num_reqs=5, len_range=(300, 900))
+    mutate(inp)
+    kv = W.kv_device(inp.shape, inp.num_blocks, 5)
+    before = kv_bytes(kv, inp.shape)
+    gpu = gpu_pass(inp, kv, label=f"error case {expect}")
+    assert gpu["status"] == B.STATUS_CODE[expect]
+    assert gpu["used"] == 0 and gpu["n_admitted"] == 0 and gpu["n_freed"] == 0
+    assert_kv_equal(kv_bytes(kv, inp.shape), before)
+
+
+def test_error_block_id_out_of_range():
+    def m(inp):
+        inp.block_ids[3] = inp.num_blocks
+    _error_case(m, "VTOKEN_ERR_BLOCK_RANGE")
+
+
+def test_error_negative_block_id():
+    def m(inp):
+        inp.block_ids[-1] = -2
+    _error_case(m, "VTOKEN_ERR_BLOCK_RANGE")
+
+
+def test_error_free_list_entry_out_of_range():
+    def m(inp):
+        inp.free_list[0] = inp.num_blocks + 5
+    _error_case(m, "VTOKEN_ERR_BLOCK_RANGE")
+
+
+def test_error_block_table_length():
+    def m(inp):
+        inp.bt_indptr[2] += 1
+    _error_case(m, "VTOKEN_ERR_BT_LEN")
+
+
+def test_error_token_range():
+    def m(inp):
+        inp.seq_lens[1] += 1
+    _error_case(m, "VTOKEN_ERR_TOK_LEN")
