@@ -160,10 +160,17 @@ vtoken_status vtoken_free_blocks(const vtoken_batch* batch, const vtoken_plan* p
                                  int32_t* freed, int64_t freed_capacity, hipStream_t stream);
 
 /* Tuning entry for the copy of step 2; vtoken_repack uses the defaults (all fields 0).
- *   variant: 0 default, 1 direct (registers, plain loads/stores), 2 direct with
- *            non-temporal loads and stores, 3 staged through LDS
- *   grid:    workgroups of the persistent launch, 0 = from occupancy
- *   order:   0 plane-major work order, 1 block-major                                      */
+ *   variant: cache policy of the copy's 16-byte loads and stores (CDNA4 cache-policy bits)
+ *            0 default (= 4), 1 plain loads and stores, 2 non-temporal loads and stores,
+ *            3 non-temporal loads and plain stores, 4 non-temporal loads and sc1 stores,
+ *            5 non-temporal loads and sc0 sc1 stores, 6 non-temporal loads, sc1 nt stores
+ *   grid:    workgroups of the copy launch; 0 = one per (destination block, plane) work
+ *            item that the free list and plan can hold, capped at 2^19 (a grid-stride loop
+ *            covers any remainder)
+ *   order:   work order over (destination block, plane) items: 0 default (= 2),
+ *            1 plane-major, 2 block-major (all planes of one destination block together)
+ * All settings produce identical bytes; they differ only in speed. Invalid values return
+ * VTOKEN_ERR_ARGUMENT. */
 typedef struct vtoken_repack_options {
   int32_t variant;
   int32_t grid;

@@ -19,7 +19,8 @@ vtoken_status check_cache(const vtoken_cache* c) {
   const int64_t row = (int64_t)c->num_kv_heads * c->head_dim * c->elem_bytes;
   if (row % 16 != 0 || row > kInt32Limit) return VTOKEN_ERR_SHAPE;
   if ((int64_t)c->num_blocks * c->block_size > kInt32Limit) return VTOKEN_ERR_SHAPE;
-  if ((int64_t)c->block_size * (row / 16) > kInt32Limit) return VTOKEN_ERR_SHAPE;
+  if (row / 16 > vtoken::kMaxRowUnits) return VTOKEN_ERR_SHAPE;
+  if ((int64_t)c->block_size * (row / 16) > vtoken::kMaxChunkUnits) return VTOKEN_ERR_SHAPE;
   return VTOKEN_OK;
 }
 
@@ -121,7 +122,8 @@ vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* ba
     grid = options->grid;
     order = options->order;
   }
-  if (variant < 0 || variant > 2 || grid < 0 || (order != 0 && order != 1)) {
+  if (variant < 0 || variant >= vtoken::num_repack_variants() || grid < 0 || order < 0 ||
+      order > 2) {
     return VTOKEN_ERR_ARGUMENT;
   }
   // the copy never needs more destination blocks than the free list or the plan holds
@@ -139,6 +141,8 @@ vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* ba
   a.row_units = static_cast<int32_t>(a.row_bytes / 16);
   a.chunk_units = cache->block_size * a.row_units;
   a.max_used = static_cast<int32_t>(max_used);
+  a.row_magic = a.row_units > 1 ? static_cast<uint32_t>((1ULL << 32) / a.row_units + 1) : 0u;
+  a.order = order;
   a.src_plan = plan->src_plan;
   a.free_list = batch->free_list;
   a.counters = plan->counters;

@@ -60,6 +60,8 @@ struct CopyArgs {
   int32_t row_units;        // row_bytes / 16
   int32_t chunk_units;      // S * row_units
   int32_t max_used;         // upper bound on counters[0] the buffers can hold
+  uint32_t row_magic;       // floor(2^32 / row_units) + 1 (0 if row_units == 1)
+  int32_t order;            // 1 plane-major, otherwise block-major work order
   const int32_t* src_plan;
   const int32_t* free_list;
   const int32_t* counters;
@@ -72,5 +74,11 @@ hipError_t launch_free(const MetaArgs& a, int32_t* freed, int64_t freed_capacity
 // unknown variant or order.
 hipError_t launch_repack(const CopyArgs& a, int variant, int grid, int order,
                          hipStream_t stream);
+int num_repack_variants();
+
+// Largest chunk (S * row_bytes / 16 units) and row (row_bytes / 16 units) the copy kernel's
+// multiply-high division is exact for.
+constexpr int64_t kMaxChunkUnits = (1 << 20) - 1;
+constexpr int64_t kMaxRowUnits = 1 << 12;
 
 }  // namespace vtoken

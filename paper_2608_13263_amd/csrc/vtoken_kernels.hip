@@ -276,8 +276,36 @@ __global__ __launch_bounds__(kFreeThreads) void free_kernel(MetaArgs a, int32_t*
 // 16-byte units; kV units per thread are loaded before any is stored, so every wave keeps
 // kV*1 KiB of reads in flight. Rows are head_dim-contiguous, so a wave's 64 lanes read and
 // write 1 KiB of consecutive bytes per instruction (a whole 2 KiB row takes two).
+//
+// Source slots of one destination block: with S <= 64, lane j of every wave holds
+// src_plan[g*S + j] and rows are picked with a cross-lane shuffle; otherwise each unit reads
+// its entry from memory. The copy is branch-free so the compiler can keep every load of a
+// round in flight (a conditional load or store would force a full wait on the vector
+// memory counter): lanes of padding rows (src_plan -1, the tail of a request's last block)
+// load row 0 of the same destination block, which is always live and already being read,
+// and their stores go through a buffer resource spanning only the destination chunk with
+// an out-of-range offset, which the hardware drops.
 // ------------------------------------------------------------------------------------------
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr uint32_t kBufferDword3 = 0x00020000u;  // raw buffer, 32-bit data format (gfx9)
+constexpr uint32_t kDropOffset = 0x80000000u;    // beyond every chunk: store discarded
+
+// Cache policies of the copy (CDNA4 cache-policy bits: sc0 = 1, nt = 2, sc1 = 16).
+struct Policy {
+  bool load_nt;
+  int store_aux;
+};
+constexpr Policy kPolicies[] = {
+    {true, 16},   // 0: default - non-temporal loads, sc1 stores (as 4)
+    {false, 0},   // 1: plain loads, plain stores
+    {true, 2},    // 2: non-temporal loads and stores
+    {true, 0},    // 3: non-temporal loads, plain stores
+    {true, 16},   // 4: non-temporal loads, sc1 stores
+    {true, 17},   // 5: non-temporal loads, sc0 sc1 stores
+    {true, 18},   // 6: non-temporal loads, sc1 nt stores
+};
+constexpr int kNumPolicies = sizeof(kPolicies) / sizeof(kPolicies[0]);
 
 template <bool kNT>
 __device__ __forceinline__ u32x4 load16(const u32x4* p) {
@@ -288,18 +316,6 @@ __device__ __forceinline__ u32x4 load16(const u32x4* p) {
   }
 }
 
-
-// Source slots of one destination block: with S <= 64, lane j of every wave holds
-// src_plan[g*S + j] and rows are picked with a cross-lane shuffle; otherwise each unit reads
-// its entry from memory. The copy is branch-free so the compiler can keep every load of a
-// round in flight (a conditional load or store would force a full wait on the vector
-// memory counter): lanes of padding rows (src_plan -1, the tail of a request's last block)
-// load row 0 of the same destination block, which is always live and already being read,
-// and their stores go through a buffer resource spanning only the destination chunk with
-// an out-of-range offset, which the hardware drops.
-constexpr uint32_t kBufferDword3 = 0x00020000u;  // raw buffer, 32-bit data format (gfx9)
-constexpr uint32_t kDropOffset = 0x80000000u;    // beyond every chunk: store discarded
-
 // The destination pointer is the same for the whole workgroup; say so, so that the
 // buffer resource lives in scalar registers.
 __device__ __forceinline__ uint8_t* uniform_ptr(uint8_t* p) {
@@ -309,13 +325,9 @@ __device__ __forceinline__ uint8_t* uniform_ptr(uint8_t* p) {
   return reinterpret_cast<uint8_t*>((static_cast<uint64_t>(hi) << 32) | lo);
 }
 
-template <bool kNT>
-__device__ __forceinline__ void store16_buffer(u32x4 v, __amdgpu_buffer_rsrc_t r, uint32_t off) {
-  __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, kNT ? 2 : 0);  // aux bit 1: nt
-}
-
-template <int kV, bool kPow2, bool kNT, int kOrder, bool kSmallS, bool kOneRound>
+template <int kPolicy, bool kSmallS, bool kOneRound, int kV>
 __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a) {
+  constexpr Policy pol = kPolicies[kPolicy];
   if (a.counters[3] != 0) return;
   int used = a.counters[0];
   used = used < 0 ? 0 : (used > a.max_used ? a.max_used : used);
@@ -326,11 +338,15 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
   const int chunk = a.chunk_units;
   const uint32_t chunk_bytes = static_cast<uint32_t>(chunk) * 16u;
   const int U = a.row_units;
-  const int log2u = kPow2 ? __builtin_ctz(static_cast<unsigned>(U)) : 0;
+  // j = u / U as a multiply-high with floor(2^32/U)+1: exact for u < 2^20 and
+  // 2 <= U <= 2^12 (checked on the host)
+  const uint32_t magic = a.row_magic;
+  const bool unit_rows = U == 1;  // 16-byte rows: j = u (the constant would not fit)
   const int lane = threadIdx.x & 63;
   const int tid = static_cast<int>(threadIdx.x);
   // (hi, lo) = (plane, g) for the plane-major order, (g, plane) for the block-major order
-  const int inner = kOrder == 0 ? used : P;
+  const bool plane_major = a.order == 1;
+  const int inner = plane_major ? used : P;
   int64_t w = blockIdx.x;
   if (w >= items) return;
   int hi = static_cast<int>(w / inner);
@@ -340,13 +356,13 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
 
   // prefetch of the next item's destination block and plan entry (lanes >= S read entry
   // S-1 and never use it; the loads are unconditional so no branch splits the copy loop)
-  const int plane_lane = lane < S ? lane : S - 1;
-  int next_g = kOrder == 0 ? lo : hi;
+  const int plan_lane = lane < S ? lane : S - 1;
+  int next_g = plane_major ? lo : hi;
   int next_dblk = a.free_list[next_g];
-  int next_pv = kSmallS ? a.src_plan[(int64_t)next_g * S + plane_lane] : -1;
+  int next_pv = kSmallS ? a.src_plan[(int64_t)next_g * S + plan_lane] : -1;
 
   for (; w < items; w += gridDim.x) {
-    const int plane = kOrder == 0 ? hi : lo;
+    const int plane = plane_major ? hi : lo;
     const int g = next_g;
     const int dblk = __builtin_amdgcn_readfirstlane(next_dblk);
     const int pv = next_pv;
@@ -357,9 +373,10 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
       ++hi;
     }
     // past the last item the prefetch re-reads item 0's entries (in bounds, unused)
-    next_g = (w + gridDim.x < items) ? (kOrder == 0 ? lo : hi) : 0;
+    next_g = (w + gridDim.x < items) ? (plane_major ? lo : hi) : 0;
     next_dblk = a.free_list[next_g];
-    if (kSmallS) next_pv = a.src_plan[(int64_t)next_g * S + plane_lane];
+    if (kSmallS) next_pv = a.src_plan[(int64_t)next_g * S + plan_lane];
+
     const bool dst_ok = static_cast<unsigned>(dblk) < static_cast<unsigned>(a.num_blocks);
     const uint8_t* pbase = a.kv + (int64_t)plane * a.plane_bytes;
     uint8_t* dptr = uniform_ptr(a.kv + (int64_t)plane * a.plane_bytes +
@@ -378,104 +395,70 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
 #pragma unroll
       for (int v = 0; v < kV; ++v) {
         const int u = u0 + v * kCopyThreads + tid;
-        int j;
-        if (kPow2) {
-          j = u >> log2u;
-          col[v] = u & (U - 1);
-        } else {
-          j = u / U;
-          col[v] = u - j * U;
-        }
+        const int j = unit_rows ? u : static_cast<int>(__umulhi(static_cast<uint32_t>(u), magic));
+        col[v] = u - j * U;
         int s;
         if (kSmallS) {
           s = __shfl(pv, j & 63, 64);
         } else {
           s = u < chunk ? plan[j] : -1;
         }
-        const bool ok = (u < chunk) && static_cast<unsigned>(s) < static_cast<unsigned>(a.num_slots);
+        const bool ok =
+            (u < chunk) && static_cast<unsigned>(s) < static_cast<unsigned>(a.num_slots);
         src[v] = ok ? s : s0;
         off[v] = ok ? static_cast<uint32_t>(u) * 16u : kDropOffset;
       }
       u32x4 buf[kV];
 #pragma unroll
       for (int v = 0; v < kV; ++v) {
-        buf[v] = load16<kNT>(reinterpret_cast<const u32x4*>(pbase + (int64_t)src[v] * a.row_bytes) +
-                             col[v]);
+        buf[v] = load16<pol.load_nt>(
+            reinterpret_cast<const u32x4*>(pbase + (int64_t)src[v] * a.row_bytes) + col[v]);
       }
 #pragma unroll
-      for (int v = 0; v < kV; ++v) store16_buffer<kNT>(buf[v], drsrc, off[v]);
+      for (int v = 0; v < kV; ++v) {
+        __builtin_amdgcn_raw_buffer_store_b128(buf[v], drsrc, off[v], 0, pol.store_aux);
+      }
     }
   }
 }
 
-int device_cu_count() {
-  static int cached[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] == 0) {
-    int cus = 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        cus <= 0) {
-      cus = 256;
-    }
-    cached[dev] = cus;
-  }
-  return cached[dev];
-}
+// Default launch: one workgroup per work item, for as many items as the buffers can hold
+// (the device-side count is not known on the host), capped at kMaxCopyGrid workgroups; the
+// kernel's grid-stride loop covers the rest and surplus workgroups exit at once. Measured on
+// MI355X, one item per workgroup beats a persistent grid sized from occupancy: the hardware
+// dispatcher refills CUs as workgroups retire, while a persistent wave has to drain its
+// stores before its next item's loads.
+constexpr int64_t kMaxCopyGrid = 1 << 19;
 
-// Persistent launch: by default as many workgroups as fit on the device at once (the
-// occupancy of this kernel, cached per instantiation, times the CU count).
 template <void (*kKernel)(CopyArgs)>
 hipError_t launch_kernel(const CopyArgs& a, int grid, hipStream_t stream) {
   if (grid <= 0) {
-    static int per_cu = 0;
-    if (per_cu == 0) {
-      int nb = 0;
-      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kKernel, kCopyThreads, 0) !=
-              hipSuccess || nb <= 0) {
-        nb = 4;
-      }
-      per_cu = nb;
-    }
-    grid = per_cu * device_cu_count();
+    const int64_t items = (int64_t)a.max_used * a.num_planes;
+    grid = static_cast<int>(items < kMaxCopyGrid ? items : kMaxCopyGrid);
   }
   hipLaunchKernelGGL(kKernel, dim3(grid), dim3(kCopyThreads), 0, stream, a);
   return hipGetLastError();
 }
 
-template <int kV, bool kPow2, bool kNT, int kOrder>
+template <int kPolicy, int kV>
 hipError_t launch_direct(const CopyArgs& a, int grid, hipStream_t stream) {
   if (a.block_size <= 64) {
     if (a.chunk_units == kCopyThreads * kV) {
-      return launch_kernel<repack_direct_kernel<kV, kPow2, kNT, kOrder, true, true>>(a, grid,
-                                                                                     stream);
+      return launch_kernel<repack_direct_kernel<kPolicy, true, true, kV>>(a, grid, stream);
     }
-    return launch_kernel<repack_direct_kernel<kV, kPow2, kNT, kOrder, true, false>>(a, grid,
-                                                                                    stream);
+    return launch_kernel<repack_direct_kernel<kPolicy, true, false, kV>>(a, grid, stream);
   }
-  return launch_kernel<repack_direct_kernel<kV, kPow2, kNT, kOrder, false, false>>(a, grid,
-                                                                                   stream);
+  return launch_kernel<repack_direct_kernel<kPolicy, false, false, kV>>(a, grid, stream);
 }
 
-template <bool kPow2, bool kNT, int kOrder>
-hipError_t launch_direct_v(const CopyArgs& a, int grid, hipStream_t stream) {
+template <int kPolicy>
+hipError_t launch_policy(const CopyArgs& a, int grid, hipStream_t stream) {
   // enough 16-byte units per thread to cover one chunk, at most 8
   const int per_thread = a.chunk_units / kCopyThreads;
-  if (per_thread >= 8) return launch_direct<8, kPow2, kNT, kOrder>(a, grid, stream);
-  if (per_thread >= 4) return launch_direct<4, kPow2, kNT, kOrder>(a, grid, stream);
-  if (per_thread >= 2) return launch_direct<2, kPow2, kNT, kOrder>(a, grid, stream);
-  return launch_direct<1, kPow2, kNT, kOrder>(a, grid, stream);
-}
-
-template <bool kNT>
-hipError_t launch_direct_nt(const CopyArgs& a, int grid, int order, hipStream_t stream) {
-  const bool pow2 = (a.row_units & (a.row_units - 1)) == 0;
-  if (order == 0) {
-    return pow2 ? launch_direct_v<true, kNT, 0>(a, grid, stream)
-                : launch_direct_v<false, kNT, 0>(a, grid, stream);
-  }
-  return pow2 ? launch_direct_v<true, kNT, 1>(a, grid, stream)
-              : launch_direct_v<false, kNT, 1>(a, grid, stream);
+  if (per_thread >= 8) return launch_direct<kPolicy, 8>(a, grid, stream);
+  if (per_thread >= 4) return launch_direct<kPolicy, 4>(a, grid, stream);
+  if (per_thread >= 2) return launch_direct<kPolicy, 2>(a, grid, stream);
+  return launch_direct<kPolicy, 1>(a, grid, stream);
 }
 
 }  // namespace
@@ -500,18 +483,23 @@ hipError_t launch_free(const MetaArgs& a, int32_t* freed, int64_t freed_capacity
   return hipGetLastError();
 }
 
-hipError_t launch_repack(const CopyArgs& a, int variant, int grid, int order,
+hipError_t launch_repack(const CopyArgs& a_in, int variant, int grid, int order,
                          hipStream_t stream) {
-  if (order != 0 && order != 1) return hipErrorInvalidValue;
+  if (order < 0 || order > 2) return hipErrorInvalidValue;
+  CopyArgs a = a_in;
+  a.order = order;
   switch (variant) {
-    case 0:
-    case 2:
-      return launch_direct_nt<true>(a, grid, order, stream);
-    case 1:
-      return launch_direct_nt<false>(a, grid, order, stream);
-    default:
-      return hipErrorInvalidValue;
+    case 0: return launch_policy<0>(a, grid, stream);
+    case 1: return launch_policy<1>(a, grid, stream);
+    case 2: return launch_policy<2>(a, grid, stream);
+    case 3: return launch_policy<3>(a, grid, stream);
+    case 4: return launch_policy<4>(a, grid, stream);
+    case 5: return launch_policy<5>(a, grid, stream);
+    case 6: return launch_policy<6>(a, grid, stream);
+    default: return hipErrorInvalidValue;
   }
 }
+
+int num_repack_variants() { return kNumPolicies; }
 
 }  // namespace vtoken

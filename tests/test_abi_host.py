@@ -122,7 +122,7 @@ def test_repack_and_free_reject_bad_arguments():
     opts = B.CRepackOptions(7, 0, 0, 0)
     assert lib.vtoken_repack_ex(ctypes.byref(cache), ctypes.byref(batch), ctypes.byref(plan),
                                 ctypes.byref(opts), None) == B.STATUS_CODE["VTOKEN_ERR_ARGUMENT"]
-    opts = B.CRepackOptions(0, 0, 2, 0)
+    opts = B.CRepackOptions(0, 0, 3, 0)
     assert lib.vtoken_repack_ex(ctypes.byref(cache), ctypes.byref(batch), ctypes.byref(plan),
                                 ctypes.byref(opts), None) == B.STATUS_CODE["VTOKEN_ERR_ARGUMENT"]
     assert lib.vtoken_repack(None, ctypes.byref(batch), ctypes.byref(plan), None) == \

@@ -109,9 +109,10 @@ def test_nan_payloads_are_copied_bit_exactly():
     assert_kv_equal(kv_bytes(kv, inp.shape), orc.kv)
 
 
-@pytest.mark.parametrize("variant,order,grid", [(1, 0, 0), (2, 0, 0), (2, 1, 0), (1, 1, 7),
-                                                (2, 0, 1), (2, 0, 3), (0, 1, 1)])
+@pytest.mark.parametrize("variant,order,grid", [(v, 0, 0) for v in range(7)] + [
+    (0, 1, 0), (0, 2, 0), (4, 1, 1), (1, 2, 7), (2, 1, 3), (5, 2, 1), (6, 1, 2048)])
 def test_copy_variants_agree(variant, order, grid):
+    # every cache policy, both work orders, persistent grids down to one workgroup
     inp = W.llama3_8b_random(204, num_layers=2, num_reqs=6, len_range=(500, 2500))
     full_parity(inp, seed=13, variant=variant, order=order, grid=grid)
 
