@@ -1,12 +1,15 @@
 """Parity at full size, in the launch configuration the benchmark times.
 
-The whole Llama-3-8B-shaped cache (32 layers, 8 KV heads, head_dim 128, bf16, block 16, 64
-requests of 2K-8K tokens, ~56 GiB) is repacked once through the C ABI. Then:
+Each full-size cache is repacked once through the C ABI. Then:
   - every metadata output equals the oracle's, element by element;
-  - three sampled planes (first, middle, last) equal the oracle run on their pre-call bytes;
-  - every plane: each row the oracle moves equals the pre-call source row, and every other
-    byte equals its pre-call value (a device-side comparison against a pre-call clone, using
-    the oracle's move list)."""
+  - three sampled planes (first, middle, last) equal, byte for byte, the oracle run on their
+    pre-call bytes;
+  - every plane: each row the oracle moves equals its pre-call source row and every other row
+    equals its pre-call value. For the 56 GiB Llama-3-8B cache this compares bytes against a
+    pre-call clone on the device; pools too large to clone compare 64-bit weighted row
+    checksums taken before and after the pass."""
+import gc
+
 import numpy as np
 import pytest
 
@@ -31,7 +34,15 @@ def _plane_bytes(kv, p, shape):
     return kv[p].view(t.uint8).reshape(-1, shape.row_bytes)
 
 
-def run_full(inp, seed, sample_planes):
+def _row_sums(kv, p, shape):
+    """Weighted 64-bit checksum of every row of plane p (wrapping integer arithmetic)."""
+    t = torch()
+    x = _plane_bytes(kv, p, shape).view(t.int64)
+    w = t.arange(1, x.shape[1] + 1, dtype=t.int64, device=x.device) * 2654435761 + 1
+    return (x * w).sum(dim=1)
+
+
+def run_full(inp, seed, sample_planes, clone=True):
     t = torch()
     shape = inp.shape
     print(f"[gpu] full-size {inp.name}: pool {inp.pool_bytes() / 2**30:.1f} GiB, "
@@ -39,7 +50,10 @@ def run_full(inp, seed, sample_planes):
     orc_meta = oracle_repack_inputs(inp)
     kv = W.kv_device(shape, inp.num_blocks, seed)
     pre = np.stack([_plane_bytes(kv, p, shape).cpu().numpy() for p in sample_planes])
-    clone = kv.clone()
+    if clone:
+        before = kv.clone()
+    else:
+        before = t.stack([_row_sums(kv, p, shape) for p in range(shape.num_planes)])
     gpu = gpu_pass(inp, kv, label=f"full-size {inp.name}")
     assert_plan_equal(gpu, orc_meta)
 
@@ -47,20 +61,54 @@ def run_full(inp, seed, sample_planes):
     post = np.stack([_plane_bytes(kv, p, shape).cpu().numpy() for p in sample_planes])
     assert_kv_equal(post, orc.kv)
 
+    _check_all_planes(kv, before, clone, orc_meta, inp)
+    live = int(np.asarray(orc_meta.live_count)[np.asarray(orc_meta.admitted) == 1].sum())
+    print(f"[gpu] full-size {inp.name}: {live} live tokens repacked, used {orc_meta.used} "
+          f"blocks, freed {orc_meta.n_freed}", flush=True)
+    del kv, before
+    gc.collect()
+    t.cuda.empty_cache()
+
+
+def _check_all_planes(kv, before, clone, orc_meta, inp):
+    t = torch()
+    shape = inp.shape
     src, dst = _moves(orc_meta, inp)
     src_t = t.from_numpy(src).cuda()
     dst_t = t.from_numpy(dst).cuda()
     for p in range(shape.num_planes):
-        cb = _plane_bytes(clone, p, shape)
-        cb[dst_t] = cb[src_t]
-        assert t.equal(_plane_bytes(kv, p, shape), cb), f"plane {p} differs"
-    live = int(np.asarray(orc_meta.live_count)[np.asarray(orc_meta.admitted) == 1].sum())
-    print(f"[gpu] full-size {inp.name}: {live} live tokens repacked, used {orc_meta.used} "
-          f"blocks, freed {orc_meta.n_freed}", flush=True)
-    del kv, clone
-    t.cuda.empty_cache()
+        if clone:
+            cb = _plane_bytes(before, p, shape)
+            cb[dst_t] = cb[src_t]
+            assert t.equal(_plane_bytes(kv, p, shape), cb), f"plane {p} differs"
+        else:
+            expect = before[p].clone()
+            expect[dst_t] = before[p][src_t]
+            assert t.equal(_row_sums(kv, p, shape), expect), f"plane {p} row checksums differ"
 
 
 def test_llama3_8b_random_full_size():
     inp = W.llama3_8b_random(201)
     run_full(inp, seed=1, sample_planes=[0, 31, 63])
+
+
+def _budget():
+    t = torch()
+    free, _ = t.cuda.mem_get_info()
+    return free
+
+
+def test_llama3_8b_h2o_full_size():
+    # 128 requests of 4K-16K tokens, ~198 GiB pool
+    inp = W.llama3_8b_h2o(301)
+    assert inp.pool_bytes() < 0.8 * _budget()
+    run_full(inp, seed=2, sample_planes=[0, 33, 63], clone=False)
+
+
+@pytest.mark.parametrize("dtype,keep", [("fp8_e4m3", 0.3), ("bf16", 0.3), ("fp8_e4m3", 0.1),
+                                        ("fp8_e4m3", 0.6)])
+def test_llama3_70b_h2o_full_size(dtype, keep):
+    # fit rule: requests whose blocks take <= 80% of a min(240 GiB, 0.85 x free) pool
+    budget = min(240 * 2 ** 30, int(0.85 * _budget()))
+    inp = W.llama3_70b_h2o(501, keep=keep, dtype=dtype, pool_bytes=budget)
+    run_full(inp, seed=3, sample_planes=[0, 81, 159], clone=False)
