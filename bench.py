@@ -8,8 +8,10 @@ in HBM before the timed region. The pass is idempotent on unchanged inputs (out-
 sources are never written), so every timed step does the full work again.
 
 The default workload is the Llama-3-8B-shaped cache: 32 layers, 8 KV heads, head_dim 128,
-bf16, block 16, 64 requests of U[2048, 8192] tokens in a shuffled ~56 GiB pool, Random
-eviction keeping 30% of each request plus its last 64 tokens.
+bf16, block 16, 64 requests of U[2048, 8192] tokens, Random eviction keeping 30% of each
+request plus its last 64 tokens, their blocks shuffled through a KV pool of 90% of free HBM
+(a serving engine's whole KV cache; --pool-frac 0 packs the pool to the requests' blocks,
+their destinations and 1024 spare blocks, 56 GiB).
 
 Prints one JSON line. `value` is repacked KV GB/s over the whole step (read+write bytes of
 the live rows: 2 * live tokens * 2*L*H*D*elem_bytes); `roofline` prices the repack kernel
@@ -47,10 +49,15 @@ def parse_args(argv=None):
     ap.add_argument("--variant", type=int, default=0)
     ap.add_argument("--grid", type=int, default=0)
     ap.add_argument("--order", type=int, default=0)
+    ap.add_argument("--pool-frac", type=float, default=0.9,
+                    help="llama3_8b_random: size the block pool to this fraction of free HBM, "
+                         "as a serving engine sizes its KV cache (the paper runs with "
+                         "gpu_mem_util 0.90); 0 = the requests' blocks plus their "
+                         "destinations plus 1024 spare blocks (56 GiB)")
     ap.add_argument("--mode", default="repack", choices=["repack", "copy"])
     ap.add_argument("--copy-gib", type=float, default=8.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-planes", type=int, default=16,
+    ap.add_argument("--cpu-planes", type=int, default=4,
                     help="planes of the workload the CPU oracle is timed on")
     return ap.parse_args(argv)
 
@@ -62,7 +69,12 @@ def log(msg):
 def make_workload(args):
     from paper_2608_13263_amd import workloads as W
     if args.config == "llama3_8b_random":
-        return W.llama3_8b_random(args.seed if args.seed is not None else 201)
+        pool = None
+        if args.pool_frac > 0:
+            import torch
+            free, _ = torch.cuda.mem_get_info()
+            pool = int(args.pool_frac * free)
+        return W.llama3_8b_random(args.seed if args.seed is not None else 201, pool_bytes=pool)
     if args.config == "llama3_8b_h2o":
         return W.llama3_8b_h2o(args.seed if args.seed is not None else 301)
     if args.config == "tiny":
@@ -91,7 +103,7 @@ def recorded_traffic(config: str):
 
 def cpu_baseline(inp, planes: int, min_seconds: float = 10.0, max_repeats: int = 8):
     """The CPU oracle as it stands, on the full metadata and `planes` planes of host KV
-    (one random plane replicated; the oracle's cost does not depend on the values), timed
+    (64 MiB of random bytes tiled; the oracle's cost does not depend on the values), timed
     over repeated passes until at least `min_seconds` of CPU work."""
     import numpy as np
     from oracle.repack import oracle_repack_inputs
@@ -101,10 +113,12 @@ def cpu_baseline(inp, planes: int, min_seconds: float = 10.0, max_repeats: int =
     sample_shape = W.KVShape(planes // 2, sh.num_kv_heads, sh.head_dim, sh.block_size, sh.dtype)
     slots = inp.num_blocks * sh.block_size
     rng = np.random.Generator(np.random.PCG64(17))
-    one = np.frombuffer(rng.bytes(slots * sh.row_bytes), dtype=np.uint8).reshape(
-        slots, sh.row_bytes)
+    tile = np.frombuffer(rng.bytes(1 << 26), dtype=np.uint8)
     kv = np.empty((planes, slots, sh.row_bytes), dtype=np.uint8)
-    kv[:] = one
+    flat = kv.reshape(-1)
+    for o in range(0, flat.size, tile.size):
+        n = min(tile.size, flat.size - o)
+        flat[o:o + n] = tile[:n]
     times = []
     while len(times) < max_repeats and sum(times) < min_seconds:
         t0 = time.perf_counter()

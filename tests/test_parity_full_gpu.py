@@ -92,6 +92,12 @@ def test_llama3_8b_random_full_size():
     run_full(inp, seed=1, sample_planes=[0, 31, 63])
 
 
+def test_llama3_8b_random_full_size_serving_pool():
+    # the benchmark's default: the same requests in a pool of 90% of free HBM (~258 GiB)
+    inp = W.llama3_8b_random(201, pool_bytes=int(0.9 * _budget()))
+    run_full(inp, seed=1, sample_planes=[0, 31, 63], clone=False)
+
+
 def _budget():
     t = torch()
     free, _ = t.cuda.mem_get_info()
