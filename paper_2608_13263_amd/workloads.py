@@ -283,121 +283,137 @@ def from_masks(masks: Sequence[Sequence[int]], shape: KVShape, free_blocks: int,
 class ScissorhandsStream:
     """Scissorhands-style repeated repack over a long decode (Sec. 2.2; policy figure, Sec. 4).
 
-    Request r has a logical length that grows by `decode_steps` tokens per round. Its
-    resident layout at each round is: the tokens kept after the previous round, packed, then
-    the tokens decoded since. Each token carries a persistence score: every round it is
-    attended with probability min(1, 1/sqrt(1+age)) at each of the round's decode steps, so
-    the score grows by Binomial(decode_steps, p). Liveness keeps the top floor(budget*len)
-    non-window resident tokens by (score desc, logical position asc) plus the last `window`.
+    The caller's side of a serving loop, as inputs for the repack:
+      decode()   every request appends `decode_steps` tokens (blocks from the front of the
+                 free list once its last block is full), each resident live token's
+                 persistence score grows by Binomial(decode_steps, min(1, 1/sqrt(1+age))),
+                 and liveness keeps the top floor(budget * L) - |window| live non-window
+                 tokens by (score desc, logical position asc) plus the live tokens of the last
+                 `window` positions; everything else is evicted. An evicted token stays dead.
+      inputs()   the current layout as RepackInputs (a request's tokens in slot order).
+      commit()   apply one pass's outputs: repacked requests keep only their live tokens, in
+                 order, in their new block table; the free list becomes the unconsumed
+                 entries followed by the freed blocks.
+    A round is decode() followed by passes ("waves") until a pass repacks nothing: a pool
+    too small for every destination at once defers the later requests to the next wave.
 
-    The stream yields RepackInputs; after the caller has run the repack on round i, it calls
-    `advance(new_block_tables, freed, free_list_rest)` with the pass's outputs, and the next
-    round appends `decode_steps` tokens per request (new blocks from the front of the free
-    list) before drawing liveness again. Only inputs are produced here: the packed layout
-    of each round is what the repack under test returned.
+    Initial state (before round 1): logical length L0 ~ U[len_range] - decode_steps; the
+    request was packed by the previous round, holding a sorted random subset of
+    [0, L0 - window) of size floor(budget * L0) - window plus the window [L0 - window, L0),
+    with persistence scores Binomial(2 * decode_steps, min(1, 1/sqrt(1+age))).
+    The pool has `pool_blocks` blocks (default: twice the resident blocks), shuffled.
     """
 
     def __init__(self, seed: int = 401, num_reqs: int = 256, num_layers: int = 32,
                  len_range=(2048, 32768), budget: float = 0.25, window: int = 256,
-                 decode_steps: int = 512, pool_blocks: Optional[int] = None):
+                 decode_steps: int = 512, pool_blocks: Optional[int] = None,
+                 num_kv_heads: int = 8, head_dim: int = 128, block_size: int = 16):
         self.rng = np.random.Generator(np.random.PCG64(seed))
         self.seed = seed
-        self.shape = KVShape(num_layers, 8, 128, 16, "bf16")
+        self.shape = KVShape(num_layers, num_kv_heads, head_dim, block_size, "bf16")
         self.budget, self.window, self.decode_steps = budget, window, decode_steps
-        S = self.shape.block_size
-        self.logical_len = self.rng.integers(len_range[0], len_range[1], size=num_reqs,
-                                             endpoint=True).astype(np.int64)
-        # steady state before round 1: kept older tokens (sorted random subset), the prior
-        # window, then `decode_steps` fresh tokens
+        S = block_size
+        L_end = self.rng.integers(len_range[0], len_range[1], size=num_reqs, endpoint=True)
+        self.L = (L_end - decode_steps).astype(np.int64)
         self.pos: List[np.ndarray] = []
-        for L in self.logical_len:
-            older = int(L) - decode_steps - window
-            kept = int(math.floor(budget * (int(L) - decode_steps)))
-            kept = max(min(kept, older), 0)
+        self.score: List[np.ndarray] = []
+        self.alive: List[np.ndarray] = []
+        for L0 in self.L:
+            L0 = int(L0)
+            older = max(L0 - window, 0)
+            kept = min(max(int(math.floor(budget * L0)) - window, 0), older)
             sel = np.sort(self.rng.choice(older, size=kept, replace=False)) if kept else \
                 np.zeros(0, dtype=np.int64)
-            self.pos.append(np.concatenate([sel, np.arange(older, int(L))]).astype(np.int64))
-        self.score = [self.rng.binomial(decode_steps, 0.5, size=len(p)).astype(np.int64)
-                      for p in self.pos]
-        seq_lens = np.array([len(p) for p in self.pos], dtype=np.int64)
-        M = int(sum(_blocks_for(n, S) for n in seq_lens))
-        if pool_blocks is None:
-            pool_blocks = 2 * M
-        self.num_blocks = int(pool_blocks)
+            pos = np.concatenate([sel.astype(np.int64), np.arange(older, L0, dtype=np.int64)])
+            p = np.minimum(1.0, 1.0 / np.sqrt(1.0 + (L0 - pos)))
+            self.pos.append(pos)
+            self.score.append(self.rng.binomial(2 * decode_steps, p).astype(np.int64))
+            self.alive.append(np.ones(len(pos), dtype=bool))
+        resident = sum(_blocks_for(len(p), S) for p in self.pos)
+        self.num_blocks = int(pool_blocks) if pool_blocks is not None else 2 * resident
+        if self.num_blocks < resident:
+            raise ValueError("pool smaller than the resident blocks")
         perm = self.rng.permutation(self.num_blocks).astype(np.int32)
         self.tables: List[np.ndarray] = []
         o = 0
-        for n in seq_lens:
-            b = _blocks_for(int(n), S)
+        for pos in self.pos:
+            b = _blocks_for(len(pos), S)
             self.tables.append(perm[o:o + b].copy())
             o += b
         self.free = perm[o:].copy()
         self.round = 0
+        self.wave = 0
 
-    def inputs(self) -> RepackInputs:
-        """Liveness for the current resident layout (the policy's SelectVictims step)."""
+    def decode(self) -> None:
         S = self.shape.block_size
-        masks = []
-        for r, pos in enumerate(self.pos):
-            L = int(self.logical_len[r])
-            age = (L - pos).astype(np.float64)
-            p = np.minimum(1.0, 1.0 / np.sqrt(1.0 + age))
-            self.score[r] = self.score[r] + self.rng.binomial(self.decode_steps, p)
-            n = len(pos)
-            live = np.zeros(n, dtype=np.uint8)
-            win = pos >= L - self.window
-            live[win] = 1
-            cand = np.nonzero(~win)[0]
-            k = min(int(math.floor(self.budget * L)) - int(win.sum()), len(cand))
-            if k > 0:
-                order = np.lexsort((pos[cand], -self.score[r][cand]))
-                live[cand[order[:k]]] = 1
-            masks.append(live)
-        seq_lens = np.array([len(p) for p in self.pos], dtype=np.int64)
-        tok_indptr = np.zeros(len(seq_lens) + 1, dtype=np.int64)
-        tok_indptr[1:] = np.cumsum(seq_lens)
-        lens_b = np.array([len(t) for t in self.tables], dtype=np.int64)
-        bt_indptr = np.zeros(len(seq_lens) + 1, dtype=np.int64)
-        bt_indptr[1:] = np.cumsum(lens_b)
-        return RepackInputs(
-            name=f"llama3_8b_scissorhands_round{self.round}", shape=self.shape,
-            num_blocks=self.num_blocks, seq_lens=seq_lens.astype(np.int32),
-            tok_indptr=tok_indptr.astype(np.int32), bt_indptr=bt_indptr.astype(np.int32),
-            block_ids=np.concatenate(self.tables).astype(np.int32) if self.tables else
-            np.zeros(0, np.int32),
-            live=np.concatenate(masks) if masks else np.zeros(0, np.uint8),
-            free_list=self.free.copy(), seed=self.seed,
-            note=f"Scissorhands budget {self.budget} window {self.window}, round {self.round}")
-
-    def advance(self, live: np.ndarray, token_slot_order: Sequence[np.ndarray],
-                new_tables: Sequence[np.ndarray], free_list: np.ndarray) -> None:
-        """Carry the state to the next round.
-
-        live: the mask returned by inputs() for this round. token_slot_order[r]: indices (into
-        request r's resident tokens) of its tokens in their new slot order, i.e. the tokens
-        that are still resident after the pass, in the order they now occupy their block
-        table. new_tables[r]: the request's block table after the pass. free_list: the free
-        list after the pass. Then `decode_steps` tokens are appended to every request."""
-        S = self.shape.block_size
-        free = list(free_list)
+        free = list(self.free)
         for r in range(len(self.pos)):
-            keep = np.asarray(token_slot_order[r], dtype=np.int64)
-            self.pos[r] = self.pos[r][keep]
-            self.score[r] = self.score[r][keep]
-            table = list(np.asarray(new_tables[r], dtype=np.int32))
-            L = int(self.logical_len[r])
+            L = int(self.L[r])
             fresh = np.arange(L, L + self.decode_steps, dtype=np.int64)
             self.pos[r] = np.concatenate([self.pos[r], fresh])
             self.score[r] = np.concatenate([self.score[r], np.zeros(len(fresh), np.int64)])
-            need = _blocks_for(len(self.pos[r]), S) - len(table)
-            if need > len(free):
+            self.alive[r] = np.concatenate([self.alive[r], np.ones(len(fresh), dtype=bool)])
+            grow = _blocks_for(len(self.pos[r]), S) - len(self.tables[r])
+            if grow > len(free):
                 raise RuntimeError("pool exhausted while appending decoded tokens")
-            table.extend(free[:need])
-            free = free[need:]
-            self.tables[r] = np.asarray(table, dtype=np.int32)
-            self.logical_len[r] = L + self.decode_steps
+            if grow > 0:
+                self.tables[r] = np.concatenate([self.tables[r],
+                                                 np.asarray(free[:grow], dtype=np.int32)])
+                free = free[grow:]
+            L += self.decode_steps
+            self.L[r] = L
+            pos, alive = self.pos[r], self.alive[r]
+            p = np.minimum(1.0, 1.0 / np.sqrt(1.0 + (L - pos)))
+            self.score[r] = self.score[r] + np.where(alive, self.rng.binomial(
+                self.decode_steps, p), 0)
+            win = alive & (pos >= L - self.window)
+            cand = np.nonzero(alive & ~win)[0]
+            k = max(int(math.floor(self.budget * L)) - int(win.sum()), 0)
+            new_alive = win.copy()
+            if k > 0 and len(cand):
+                order = np.lexsort((pos[cand], -self.score[r][cand]))
+                new_alive[cand[order[:k]]] = True
+            self.alive[r] = new_alive
         self.free = np.asarray(free, dtype=np.int32)
         self.round += 1
+        self.wave = 0
+
+    def inputs(self) -> RepackInputs:
+        seq_lens = np.array([len(p) for p in self.pos], dtype=np.int64)
+        tok_indptr = np.zeros(len(seq_lens) + 1, dtype=np.int64)
+        tok_indptr[1:] = np.cumsum(seq_lens)
+        bt_indptr = np.zeros(len(seq_lens) + 1, dtype=np.int64)
+        bt_indptr[1:] = np.cumsum([len(t) for t in self.tables])
+        return RepackInputs(
+            name="llama3_8b_scissorhands", shape=self.shape, num_blocks=self.num_blocks,
+            seq_lens=seq_lens.astype(np.int32), tok_indptr=tok_indptr.astype(np.int32),
+            bt_indptr=bt_indptr.astype(np.int32),
+            block_ids=np.concatenate(self.tables).astype(np.int32) if self.tables else
+            np.zeros(0, np.int32),
+            live=np.concatenate(self.alive).astype(np.uint8) if self.alive else
+            np.zeros(0, np.uint8),
+            free_list=self.free.copy(), seed=self.seed,
+            note=f"Scissorhands budget {self.budget} window {self.window}, "
+                 f"{len(self.pos)} req, round {self.round} wave {self.wave}")
+
+    def commit(self, admitted, new_bt_indptr, new_block_ids, used: int, freed) -> None:
+        """Apply one pass's outputs (admitted [R], new tables in CSR, consumed free-list
+        entries, freed blocks)."""
+        for r in range(len(self.pos)):
+            if not admitted[r]:
+                continue
+            keep = np.nonzero(self.alive[r])[0]
+            self.pos[r] = self.pos[r][keep]
+            self.score[r] = self.score[r][keep]
+            self.alive[r] = np.ones(len(keep), dtype=bool)
+            self.tables[r] = np.asarray(new_block_ids[new_bt_indptr[r]:new_bt_indptr[r + 1]],
+                                        dtype=np.int32)
+        self.free = np.concatenate([self.free[int(used):],
+                                    np.asarray(freed, dtype=np.int32)]).astype(np.int32)
+        self.wave += 1
+
+    def resident_blocks(self) -> int:
+        return sum(len(t) for t in self.tables)
 
 
 CONFIGS: Dict[str, Callable[..., RepackInputs]] = {

@@ -118,3 +118,47 @@ def test_llama3_70b_h2o_full_size(dtype, keep):
     budget = min(240 * 2 ** 30, int(0.85 * _budget()))
     inp = W.llama3_70b_h2o(501, keep=keep, dtype=dtype, pool_bytes=budget)
     run_full(inp, seed=3, sample_planes=[0, 81, 159], clone=False)
+
+
+def test_llama3_8b_scissorhands_rounds_with_waves():
+    """256 requests, a repack every 512 decode steps in a pool too small for one pass: each
+    round runs passes until one repacks nothing. The stream is driven by the oracle's outputs;
+    every pass's GPU outputs must equal the oracle's, the sampled planes must equal the
+    oracle's bytes (tracked on the host from the initial snapshot), and every plane must
+    satisfy the row-checksum check of that pass."""
+    t = torch()
+    budget = min(240 * 2 ** 30, int(0.85 * _budget()))
+    shape = W.KVShape(32, 8, 128, 16, "bf16")
+    stream = W.ScissorhandsStream(seed=401, pool_blocks=int(budget // shape.block_bytes))
+    sample = [0, 27, 63]
+    kv = W.kv_device(shape, stream.num_blocks, 4)
+    host = np.stack([_plane_bytes(kv, p, shape).cpu().numpy() for p in sample])
+    total_moved = 0
+    for rnd in range(2):
+        stream.decode()
+        for wave in range(8):
+            inp = stream.inputs()
+            orc_meta = oracle_repack_inputs(inp)
+            before = t.stack([_row_sums(kv, p, shape) for p in range(shape.num_planes)])
+            gpu = gpu_pass(inp, kv, label=f"scissorhands round {rnd} wave {wave}")
+            assert_plan_equal(gpu, orc_meta)
+            orc = oracle_repack_inputs(inp, host)
+            host = orc.kv
+            post = np.stack([_plane_bytes(kv, p, shape).cpu().numpy() for p in sample])
+            assert_kv_equal(post, host)
+            _check_all_planes(kv, before, False, orc_meta, inp)
+            del before
+            moved = int(np.asarray(orc_meta.live_count)[np.asarray(orc_meta.admitted) == 1].sum())
+            total_moved += moved
+            print(f"[gpu] round {rnd} wave {wave}: {orc_meta.n_admitted} admitted, {moved} live "
+                  f"tokens moved, {orc_meta.used} destinations, {orc_meta.n_freed} freed",
+                  flush=True)
+            stream.commit(orc_meta.admitted, orc_meta.new_bt_indptr, orc_meta.new_block_ids,
+                          orc_meta.used, orc_meta.freed)
+            if orc_meta.n_admitted == 0:
+                break
+        assert wave >= 1, "the pool should force at least two passes per round"
+    assert total_moved > 0
+    del kv
+    gc.collect()
+    t.cuda.empty_cache()
