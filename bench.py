@@ -42,7 +42,8 @@ def parse_args(argv=None):
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="llama3_8b_random",
-                    choices=["llama3_8b_random", "llama3_8b_h2o", "llama3_70b_h2o", "tiny"])
+                    choices=["llama3_8b_random", "llama3_8b_h2o", "llama3_70b_h2o", "tiny",
+                             "llama3_8b_scissorhands"])
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--keep", type=float, default=0.3, help="keep ratio (70B config)")
     ap.add_argument("--kv-dtype", default="fp8_e4m3", help="70B config: fp8_e4m3 or bf16")
@@ -165,6 +166,90 @@ def run_copy(args):
                       "frac_of_8TBps": round(gbs / HBM_PEAK_GBS, 4)}), flush=True)
 
 
+def run_scissorhands(args):
+    """Scissorhands-style repeated repack: 256 requests, a repack every 512 decode steps in a
+    pool of min(240 GiB, 85% of free HBM). A round is the host-side decode bookkeeping
+    followed by passes until one repacks nothing; every pass (build + repack + free) is timed
+    with HIP events. One warm-up round, then `--steps` timed rounds (default 4)."""
+    import numpy as np
+    import torch
+    from paper_2608_13263_amd import binding as B
+    from paper_2608_13263_amd import workloads as W
+    free, _ = torch.cuda.mem_get_info()
+    shape = W.KVShape(32, 8, 128, 16, "bf16")
+    budget = min(240 * 2 ** 30, int(0.85 * free))
+    stream = W.ScissorhandsStream(seed=args.seed if args.seed is not None else 401,
+                                  pool_blocks=budget // shape.block_bytes)
+    kv = W.kv_device(shape, stream.num_blocks, 1)
+    cache = B.KVCache(kv, shape.num_layers, shape.num_kv_heads, shape.head_dim,
+                      shape.block_size)
+    S = shape.block_size
+
+    def one_round():
+        stream.decode()
+        passes = []
+        while True:
+            inp = stream.inputs()
+            batch = B.Batch.from_inputs(inp)
+            plan = B.Plan.allocate(batch, S)
+            ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+                  torch.cuda.Event(enable_timing=True))
+            torch.cuda.synchronize()
+            ev[0].record()
+            B.build_token_table(cache, batch, plan)
+            ev[1].record()
+            B.repack(cache, batch, plan)
+            B.free_blocks(batch, plan)
+            ev[2].record()
+            torch.cuda.synchronize()
+            cnt = plan.counters.cpu().tolist()
+            if cnt[3] != 0:
+                raise SystemExit(f"device status {B.STATUS.get(cnt[3], cnt[3])}")
+            R = inp.num_reqs
+            adm = plan.admitted[:R].cpu().numpy()
+            live = plan.live_count[:R].cpu().numpy().astype(np.int64)
+            nbi = plan.new_bt_indptr[:R + 1].cpu().numpy()
+            nbids = plan.new_block_ids[:int(nbi[-1])].cpu().numpy()
+            freed = plan.freed[:cnt[2]].cpu().numpy()
+            passes.append(dict(ms=ev[0].elapsed_time(ev[2]), moved=int((live * adm).sum()),
+                               admitted=cnt[1], used=cnt[0]))
+            stream.commit(adm, nbi, nbids, cnt[0], freed)
+            if cnt[1] == 0:
+                return passes
+
+    log(f"scissorhands: {len(stream.pos)} requests, pool {stream.num_blocks} blocks = "
+        f"{stream.num_blocks * shape.block_bytes / 2**30:.1f} GiB; warm-up round")
+    one_round()
+    rounds = []
+    for i in range(args.steps if args.steps != 20 else 4):
+        rounds.append(one_round())
+        log(f"round {i}: " + ", ".join(f"{p['admitted']} req / {p['moved']} tok / "
+                                      f"{p['ms']:.2f} ms" for p in rounds[-1]))
+    moved = sum(p["moved"] for r in rounds for p in r)
+    ms = sum(p["ms"] for r in rounds for p in r)
+    bytes_alg = 2 * moved * shape.token_bytes
+    value = bytes_alg / (ms / 1e3) / 1e9
+    out = {
+        "metric": "repacked KV GB/s (read+write) as % of HBM peak; live tokens repacked/ms",
+        "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": len(rounds),
+        "warmup": 1, "ms_per_step": round(ms / len(rounds), 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u8", "data": "synthetic",
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "live_tokens_per_ms": round(moved / ms, 1),
+        "config": {"workload": "llama3_8b_scissorhands",
+                   "recipe": "bf16 32x8x128, S=16, 256 req, logical length U[2048,32768], "
+                             "Scissorhands budget 0.25 + window 256, repack every 512 decode "
+                             "steps, passes until one repacks nothing",
+                   "pool_gib": round(stream.num_blocks * shape.block_bytes / 2 ** 30, 2),
+                   "rounds": [[{k: (round(v, 3) if isinstance(v, float) else v)
+                                for k, v in p.items()} for p in r] for r in rounds],
+                   "live_tokens_repacked": moved, "bytes_alg_total": bytes_alg},
+        "roofline": None, "cpu_baseline": None,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main(argv=None):
     args = parse_args(argv)
     if args.gpus != 1:
@@ -179,6 +264,8 @@ def main(argv=None):
         raise SystemExit("bench.py needs a GPU (MI355X, gfx950)")
     if args.mode == "copy":
         return run_copy(args)
+    if args.config == "llama3_8b_scissorhands":
+        return run_scissorhands(args)
 
     t_setup = time.perf_counter()
     inp = make_workload(args)
