@@ -55,6 +55,9 @@ def parse_args(argv=None):
                          "as a serving engine sizes its KV cache (the paper runs with "
                          "gpu_mem_util 0.90); 0 = the requests' blocks plus their "
                          "destinations plus 1024 spare blocks (56 GiB)")
+    ap.add_argument("--inplace", action="store_true",
+                    help="in-place mode: destinations are each request's own leading blocks; "
+                         "bytes count only the rows that move")
     ap.add_argument("--mode", default="repack", choices=["repack", "copy"])
     ap.add_argument("--copy-gib", type=float, default=8.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -250,6 +253,71 @@ def run_scissorhands(args):
     return 0
 
 
+def run_inplace(args, inp, kv, cache, batch, plan, stream):
+    """In-place mode. The pass is re-run on the same inputs: every step computes the same
+    plan and moves the same rows between the same addresses (after the first step the bytes
+    it moves are ones it already moved, which does not change the traffic)."""
+    import numpy as np
+    import torch
+    from paper_2608_13263_amd import binding as B
+    sh = inp.shape
+    S = sh.block_size
+
+    def step(ev=None):
+        B.build_token_table_inplace(cache, batch, plan, stream)
+        if ev is not None:
+            ev[0].record(stream)
+        B.repack_inplace(cache, batch, plan, stream)
+        if ev is not None:
+            ev[1].record(stream)
+        B.free_blocks(batch, plan, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    step_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    kern = sum(a.elapsed_time(b) for a, b in evs) / args.steps
+    cnt = plan.counters.cpu().tolist()
+    if cnt[3] != 0:
+        raise SystemExit(f"device status {B.STATUS.get(cnt[3], cnt[3])}")
+    # rows that move: live tokens of repacked requests whose slot changes
+    old_slot = np.empty(inp.num_tokens, dtype=np.int64)
+    for r in range(inp.num_reqs):
+        a, n = int(inp.tok_indptr[r]), int(inp.seq_lens[r])
+        bt = inp.block_ids[inp.bt_indptr[r]:inp.bt_indptr[r + 1]].astype(np.int64)
+        pos = np.arange(n)
+        old_slot[a:a + n] = bt[pos // S] * S + pos % S
+    ts = plan.token_slot[:inp.num_tokens].cpu().numpy().astype(np.int64)
+    moved = int(((ts != old_slot) & (inp.live != 0)).sum())
+    R = inp.num_reqs
+    repacked = int((plan.live_count[:R].long() * plan.admitted[:R].long()).sum())
+    bytes_alg = 2 * moved * sh.token_bytes
+    out = {
+        "metric": "repacked KV GB/s (read+write) as % of HBM peak; live tokens repacked/ms",
+        "mode": "inplace", "value": round(bytes_alg / (step_ms / 1e3) / 1e9, 2), "unit": "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
+        "pct_of_hbm_peak": round(100 * bytes_alg / (step_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 2),
+        "live_tokens_per_ms": round(repacked / step_ms, 1), "repack_ms": round(kern, 4),
+        "config": {"workload": inp.name, "recipe": inp.note, "live_tokens_repacked": repacked,
+                   "rows_moved": moved, "rows_in_place": repacked - moved,
+                   "pool_gib": round(inp.pool_bytes() / 2 ** 30, 2),
+                   "bytes_alg_per_step": bytes_alg, "admitted": cnt[1], "freed_blocks": cnt[2]},
+        "roofline": {"bound": "hbm", "kernel": "repack_inplace_kernel",
+                     "achieved": round(bytes_alg / (kern / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s",
+                     "frac": round(bytes_alg / (kern / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "traffic": None},
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main(argv=None):
     args = parse_args(argv)
     if args.gpus != 1:
@@ -276,8 +344,10 @@ def main(argv=None):
     kv = W.kv_device(sh, inp.num_blocks, 1)
     cache = B.KVCache(kv, sh.num_layers, sh.num_kv_heads, sh.head_dim, sh.block_size)
     batch = B.Batch.from_inputs(inp)
-    plan = B.Plan.allocate(batch, sh.block_size)
+    plan = B.Plan.allocate(batch, sh.block_size, inplace=args.inplace)
     stream = torch.cuda.current_stream()
+    if args.inplace:
+        return run_inplace(args, inp, kv, cache, batch, plan, stream)
     torch.cuda.synchronize()
     log(f"setup {time.perf_counter() - t_setup:.1f} s; warmup {args.warmup} steps")
 

@@ -154,10 +154,29 @@ vtoken_status vtoken_repack(const vtoken_cache* cache, const vtoken_batch* batch
                             const vtoken_plan* plan, hipStream_t stream);
 
 /* Step 3 (Sec. 3.3.4: sources are returned only after the packed layout is committed):
- * writes freed[0 .. counters[2]) = old blocks of the admitted requests. Stream order
+ * writes freed[0 .. counters[2]) = old blocks of the admitted requests (in-place mode: the
+ * blocks past each admitted request's new table). Stream order
  * after vtoken_repack is what makes reuse of these blocks safe. freed_capacity >= M. */
 vtoken_status vtoken_free_blocks(const vtoken_batch* batch, const vtoken_plan* plan,
                                  int32_t* freed, int64_t freed_capacity, hipStream_t stream);
+
+/* In-place mode (an extension beyond the paper's out-of-place relocation, Sec. 3.3.2):
+ * the destinations of a repacked request are its own first ceil(live/S) blocks, so no free
+ * list is needed and every profitable request is repacked; the freed blocks are the rest of
+ * its old table, and rows already in place are not copied. batch->free_list is ignored.
+ * plan outputs have the same meaning as out of place, except that counters[0] counts the
+ * destination blocks (rows of src_plan) and dst_indptr indexes src_plan only; the plan must
+ * hold src_plan_capacity >= M*S. Call order: vtoken_build_token_table_inplace, then
+ * vtoken_repack_inplace, then vtoken_free_blocks (the freed list is the released tails).
+ * vtoken_repack_inplace requires block_size*row_bytes <= 64 KiB (VTOKEN_ERR_SHAPE otherwise):
+ * it stages one destination block at a time through LDS, walking each (request, plane) in
+ * block order so that a block is written only after every read of its own and earlier
+ * destination blocks. */
+vtoken_status vtoken_build_token_table_inplace(const vtoken_cache* cache,
+                                               const vtoken_batch* batch,
+                                               const vtoken_plan* plan, hipStream_t stream);
+vtoken_status vtoken_repack_inplace(const vtoken_cache* cache, const vtoken_batch* batch,
+                                    const vtoken_plan* plan, hipStream_t stream);
 
 /* Tuning entry for the copy of step 2; vtoken_repack uses the defaults (all fields 0).
  *   variant: cache policy of the copy's 16-byte loads and stores (CDNA4 cache-policy bits)

@@ -20,10 +20,13 @@ from typing import Dict, List, Optional, Sequence
 
 def brute_repack(seq_lens: Sequence[int], block_tables: Sequence[Sequence[int]],
                  live_masks: Sequence[Sequence[int]], free_list: Sequence[int], S: int,
-                 planes: Optional[List[Dict[int, bytes]]] = None):
+                 planes: Optional[List[Dict[int, bytes]]] = None, inplace: bool = False):
     """Returns a dict with token_slot (list per request), admitted, new_tables, freed, used,
     src_plan (flat list) and, if `planes` (slot -> row bytes per plane) is given, the new
-    planes."""
+    planes. With inplace=True a request that gains blocks reuses its own leading blocks as
+    destinations (no free list, nothing deferred) and releases the blocks it no longer
+    fills. Moves are applied one token at a time, in logical order: a token only moves to
+    an earlier or equal slot position, and every slot it overwrites has already been read."""
     free = list(free_list)
     handed_out = 0
     refused = False
@@ -48,7 +51,7 @@ def brute_repack(seq_lens: Sequence[int], block_tables: Sequence[Sequence[int]],
             blocks += 1
 
         plan_ok = blocks < len(table)
-        if plan_ok and (refused or handed_out + blocks > len(free)):
+        if plan_ok and not inplace and (refused or handed_out + blocks > len(free)):
             refused = True
             plan_ok = False
         if not plan_ok:
@@ -57,7 +60,10 @@ def brute_repack(seq_lens: Sequence[int], block_tables: Sequence[Sequence[int]],
             token_slot.append([old_slot[p] if live[p] else -1 for p in range(n)])
             continue
 
-        dest = free[handed_out:handed_out + blocks]
+        if inplace:
+            dest = table[:blocks]
+        else:
+            dest = free[handed_out:handed_out + blocks]
         handed_out += blocks
         dest_slots = []
         for blk in dest:
@@ -72,7 +78,7 @@ def brute_repack(seq_lens: Sequence[int], block_tables: Sequence[Sequence[int]],
         admitted.append(1)
         new_tables.append(dest)
         token_slot.append(slots)
-        freed.extend(table)
+        freed.extend(table[blocks:] if inplace else table)
 
     out = dict(token_slot=token_slot, admitted=admitted, new_tables=new_tables, freed=freed,
                used=handed_out, src_plan=src_plan,
@@ -82,7 +88,9 @@ def brute_repack(seq_lens: Sequence[int], block_tables: Sequence[Sequence[int]],
         for plane in planes:
             q = dict(plane)
             for old, new in moves:
-                q[new] = plane[old]
+                # out of place the source is untouched; in place it is read from the plane
+                # being built, which the logical order keeps valid (see the docstring)
+                q[new] = q[old] if inplace else plane[old]
             new_planes.append(q)
         out["planes"] = new_planes
     return out

@@ -43,8 +43,10 @@ def _waste(tables, live_slot_lists, S):
 def check_invariants(seq_lens, tok_indptr, bt_indptr, block_ids, live, free_list, S: int,
                      num_blocks: int, token_slot, new_bt_indptr, new_block_ids, freed,
                      used: int, kv_before: Optional[np.ndarray] = None,
-                     kv_after: Optional[np.ndarray] = None) -> None:
-    """Raise AssertionError naming the first violated invariant."""
+                     kv_after: Optional[np.ndarray] = None, inplace: bool = False) -> None:
+    """Raise AssertionError naming the first violated invariant. With inplace=True the
+    destinations of a repacked request must be the leading blocks of its own table, its other
+    blocks must be released, and the free list must stay untouched."""
     R = len(seq_lens)
     live = np.asarray(live, dtype=np.uint8)
     token_slot = np.asarray(token_slot, dtype=np.int64)
@@ -94,18 +96,29 @@ def check_invariants(seq_lens, tok_indptr, bt_indptr, block_ids, live, free_list
     if len(set(all_live_slots)) != len(all_live_slots):
         _fail("I2: a slot is referenced by two live tokens")
 
-    # destinations come from the free pool, freed = old blocks of repacked requests
-    if used < 0 or used > len(free_list):
-        _fail("3.3.2: more destinations than the free list holds")
-    dest_blocks = Counter(b for r in range(R) if repacked[r] for b in new_tables[r])
-    if dest_blocks != Counter(int(x) for x in free_list[:used]):
-        _fail("3.3.3: destination blocks are not the consumed free-list entries")
-    if Counter(int(x) for x in freed) != Counter(b for r in range(R) if repacked[r]
-                                                 for b in old_tables[r]):
-        _fail("3.3.4: freed blocks are not exactly the old blocks of repacked requests")
+    if inplace:
+        # destinations are the request's own leading blocks; the rest is released
+        for r in range(R):
+            if repacked[r] and new_tables[r] != old_tables[r][:len(new_tables[r])]:
+                _fail(f"in place: request {r} destinations are not its leading blocks")
+        if Counter(int(x) for x in freed) != Counter(
+                b for r in range(R) if repacked[r] for b in old_tables[r][len(new_tables[r]):]):
+            _fail("in place: freed blocks are not the released tails of repacked requests")
+        consumed = 0
+    else:
+        # destinations come from the free pool, freed = old blocks of repacked requests
+        if used < 0 or used > len(free_list):
+            _fail("3.3.2: more destinations than the free list holds")
+        dest_blocks = Counter(b for r in range(R) if repacked[r] for b in new_tables[r])
+        if dest_blocks != Counter(int(x) for x in free_list[:used]):
+            _fail("3.3.3: destination blocks are not the consumed free-list entries")
+        if Counter(int(x) for x in freed) != Counter(b for r in range(R) if repacked[r]
+                                                     for b in old_tables[r]):
+            _fail("3.3.4: freed blocks are not exactly the old blocks of repacked requests")
+        consumed = used
     before = Counter(b for t in old_tables for b in t) + Counter(int(x) for x in free_list)
     after = Counter(b for t in new_tables for b in t) + Counter(int(x) for x in freed) + \
-        Counter(int(x) for x in free_list[used:])
+        Counter(int(x) for x in free_list[consumed:])
     if before != after:
         _fail("block conservation: tables + pool differ before and after")
     if _waste(new_tables, new_live_slots, S) > _waste(old_tables, old_live_slots, S) + 1e-12:

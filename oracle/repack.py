@@ -20,6 +20,12 @@ layout; once one profitable request is deferred, later ones are deferred too; de
 map to -1; tail slots of the last destination block and all other bytes keep their prior
 contents; freed = all old blocks of admitted requests, requests ascending, table order.
 
+In-place mode (an extension, not in the paper): the destinations of a repacked request are
+its own first ceil(T_live / S) blocks instead of free blocks, every profitable request is
+repacked (no headroom is needed), and the freed blocks are the tail of its old table. The
+token table, fill order and copy are the same (O1, O2, O4, O5); the copy reads every source
+before it writes (the definition of a move), whatever order an implementation uses.
+
 KV is handled as opaque bytes: kv[plane, slot, :] is the row of one token in one plane
 (plane = 2*layer + {0: K, 1: V}), so the oracle is independent of the element type.
 """
@@ -107,11 +113,14 @@ def _validate(seq_lens, tok_indptr, bt_indptr, block_ids, live, S, num_blocks):
 
 
 def oracle_repack(seq_lens, tok_indptr, bt_indptr, block_ids, live, free_list, block_size: int,
-                  num_blocks: int, kv: Optional[np.ndarray] = None) -> OracleResult:
+                  num_blocks: int, kv: Optional[np.ndarray] = None,
+                  inplace: bool = False) -> OracleResult:
     """One repack pass over host arrays; returns every output of the pass.
 
     kv, if given, is uint8 [P][num_blocks*S][row_bytes] and is not modified; the result
-    holds a modified copy."""
+    holds a modified copy. With inplace=True the free list is ignored and each repacked
+    request's destinations are its own first blocks (see the module docstring); `used` then
+    counts destination blocks."""
     S = int(block_size)
     seq_lens = np.asarray(seq_lens, dtype=np.int64)
     tok_indptr = np.asarray(tok_indptr, dtype=np.int64)
@@ -135,10 +144,13 @@ def oracle_repack(seq_lens, tok_indptr, bt_indptr, block_ids, live, free_list, b
     # O2 + O3: need, profitability, headroom admission
     old_blocks = bt_indptr[1:] - bt_indptr[:-1]
     need, profitable, admitted, o = plan_requests(live_count, old_blocks, f, S)
+    if inplace:
+        admitted = profitable  # destinations are the request's own blocks: nothing to defer
     used = int((need * admitted).sum())
-    consumed = free_list[:used]
-    if used and (consumed.min() < 0 or consumed.max() >= num_blocks):
-        raise OracleInputError("block_range", "free list")
+    if not inplace:
+        consumed = free_list[:used]
+        if used and (consumed.min() < 0 or consumed.max() >= num_blocks):
+            raise OracleInputError("block_range", "free list")
 
     # O4: destination tables, token table and source plan
     dst_indptr = np.zeros(R + 1, dtype=np.int64)
@@ -157,7 +169,7 @@ def oracle_repack(seq_lens, tok_indptr, bt_indptr, block_ids, live, free_list, b
         live_pos = np.nonzero(rk >= 0)[0]
         old_slots = slot_of_position(bt, live_pos, S)
         if admitted[r]:
-            dest = free_list[dst_indptr[r]:dst_indptr[r + 1]]
+            dest = bt[:need[r]] if inplace else free_list[dst_indptr[r]:dst_indptr[r + 1]]
             new_block_ids[new_bt_indptr[r]:new_bt_indptr[r + 1]] = dest
             new_slots = slot_of_position(dest, rk[live_pos], S)
             token_slot[a + live_pos] = new_slots
@@ -168,10 +180,11 @@ def oracle_repack(seq_lens, tok_indptr, bt_indptr, block_ids, live, free_list, b
             new_block_ids[new_bt_indptr[r]:new_bt_indptr[r + 1]] = bt
             token_slot[a + live_pos] = old_slots
 
-    # O6: freed = old blocks of every admitted request
+    # O6: freed = old blocks of every admitted request (in-place: the ones past its need)
+    first_freed = need if inplace else np.zeros(R, dtype=np.int64)
     freed_indptr = np.zeros(R + 1, dtype=np.int64)
-    freed_indptr[1:] = np.cumsum(old_blocks * admitted)
-    freed = np.concatenate([block_ids[bt_indptr[r]:bt_indptr[r + 1]]
+    freed_indptr[1:] = np.cumsum((old_blocks - first_freed) * admitted)
+    freed = np.concatenate([block_ids[bt_indptr[r] + first_freed[r]:bt_indptr[r + 1]]
                             for r in range(R) if admitted[r]] or [np.zeros(0, np.int64)])
 
     # O5: out-of-place copy of every live row in every plane
@@ -192,10 +205,11 @@ def oracle_repack(seq_lens, tok_indptr, bt_indptr, block_ids, live, free_list, b
         n_admitted=int(admitted.sum()), n_freed=int(freed_indptr[-1]), kv=kv_out)
 
 
-def oracle_repack_inputs(inp, kv: Optional[np.ndarray] = None) -> OracleResult:
+def oracle_repack_inputs(inp, kv: Optional[np.ndarray] = None,
+                         inplace: bool = False) -> OracleResult:
     """oracle_repack over a RepackInputs-like object (attribute access only)."""
     return oracle_repack(inp.seq_lens, inp.tok_indptr, inp.bt_indptr, inp.block_ids, inp.live,
-                         inp.free_list, inp.shape.block_size, inp.num_blocks, kv)
+                         inp.free_list, inp.shape.block_size, inp.num_blocks, kv, inplace)
 
 
 def block_live_counts(block_table: np.ndarray, slots_of_live: np.ndarray, S: int) -> np.ndarray:

@@ -8,11 +8,13 @@ library (`paper_2608_13263_amd.binding`) and the seeded workload generators
 can be used on hosts without a GPU.
 """
 
-__all__ = ["build_token_table", "repack", "repack_ex", "free_blocks", "binding", "workloads"]
+__all__ = ["build_token_table", "repack", "repack_ex", "free_blocks",
+           "build_token_table_inplace", "repack_inplace", "binding", "workloads"]
 
 
 def __getattr__(name):
-    if name in ("build_token_table", "repack", "repack_ex", "free_blocks"):
+    if name in ("build_token_table", "repack", "repack_ex", "free_blocks",
+                "build_token_table_inplace", "repack_inplace"):
         from . import binding
         return getattr(binding, name)
     if name in ("binding", "workloads"):

@@ -71,6 +71,12 @@ _SIGNATURES = {
                                                   ctypes.POINTER(CPlan), ctypes.c_void_p]),
     "vtoken_repack": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
                                        ctypes.POINTER(CPlan), ctypes.c_void_p]),
+    "vtoken_build_token_table_inplace": (ctypes.c_int32, [ctypes.POINTER(CCache),
+                                                          ctypes.POINTER(CBatch),
+                                                          ctypes.POINTER(CPlan),
+                                                          ctypes.c_void_p]),
+    "vtoken_repack_inplace": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
+                                               ctypes.POINTER(CPlan), ctypes.c_void_p]),
     "vtoken_repack_ex": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
                                           ctypes.POINTER(CPlan), ctypes.POINTER(CRepackOptions),
                                           ctypes.c_void_p]),
@@ -186,15 +192,18 @@ class Plan:
             setattr(self, k, tensors[k])
 
     @classmethod
-    def allocate(cls, batch: Batch, block_size: int, device="cuda"):
+    def allocate(cls, batch: Batch, block_size: int, device="cuda", inplace: bool = False):
+        """Outputs sized for out-of-place mode, or for in-place mode (src_plan holds up to
+        M destination blocks)."""
         import torch
         R, T, M, f = batch.num_reqs, batch.num_tokens, batch.num_bt_entries, batch.free_len
 
         def e(n):
             return torch.empty(max(int(n), 1), dtype=torch.int32, device=device)
+        rows = M if inplace else min(f, M)
         return cls(token_slot=e(T), live_count=e(R), admitted=e(R), dst_indptr=e(R + 1),
                    new_bt_indptr=e(R + 1), new_block_ids=e(M),
-                   src_plan=e(min(f, M) * block_size), freed_indptr=e(R + 1), counters=e(4),
+                   src_plan=e(rows * block_size), freed_indptr=e(R + 1), counters=e(4),
                    freed=e(M))
 
     def c(self) -> CPlan:
@@ -207,6 +216,21 @@ def build_token_table(cache: KVCache, batch: Batch, plan: Plan, stream=None) -> 
     c, b, p = cache.c(), batch.c(), plan.c()
     _check(lib.vtoken_build_token_table(ctypes.byref(c), ctypes.byref(b), ctypes.byref(p),
                                         _stream(stream)), "vtoken_build_token_table")
+
+
+def build_token_table_inplace(cache: KVCache, batch: Batch, plan: Plan, stream=None) -> None:
+    lib = load_library()
+    c, b, p = cache.c(), batch.c(), plan.c()
+    _check(lib.vtoken_build_token_table_inplace(ctypes.byref(c), ctypes.byref(b),
+                                                ctypes.byref(p), _stream(stream)),
+           "vtoken_build_token_table_inplace")
+
+
+def repack_inplace(cache: KVCache, batch: Batch, plan: Plan, stream=None) -> None:
+    lib = load_library()
+    c, b, p = cache.c(), batch.c(), plan.c()
+    _check(lib.vtoken_repack_inplace(ctypes.byref(c), ctypes.byref(b), ctypes.byref(p),
+                                     _stream(stream)), "vtoken_repack_inplace")
 
 
 def repack(cache: KVCache, batch: Batch, plan: Plan, stream=None) -> None:
@@ -233,11 +257,16 @@ def free_blocks(batch: Batch, plan: Plan, freed=None, stream=None) -> None:
                                   int(out.numel()), _stream(stream)), "vtoken_free_blocks")
 
 
-def run_pass(cache: KVCache, batch: Batch, plan: Optional[Plan] = None, stream=None) -> Plan:
+def run_pass(cache: KVCache, batch: Batch, plan: Optional[Plan] = None, stream=None,
+             inplace: bool = False) -> Plan:
     """The three calls of one repack pass, enqueued in order on one stream."""
     if plan is None:
-        plan = Plan.allocate(batch, cache.block_size, device=cache.kv.device)
-    build_token_table(cache, batch, plan, stream)
-    repack(cache, batch, plan, stream)
+        plan = Plan.allocate(batch, cache.block_size, device=cache.kv.device, inplace=inplace)
+    if inplace:
+        build_token_table_inplace(cache, batch, plan, stream)
+        repack_inplace(cache, batch, plan, stream)
+    else:
+        build_token_table(cache, batch, plan, stream)
+        repack(cache, batch, plan, stream)
     free_blocks(batch, plan, stream=stream)
     return plan

@@ -41,12 +41,14 @@ vtoken_status check_batch(const vtoken_batch* b) {
   return VTOKEN_OK;
 }
 
-int64_t min_src_plan_capacity(const vtoken_batch* b, int32_t block_size) {
-  const int64_t f = b->free_len < b->num_bt_entries ? b->free_len : b->num_bt_entries;
+int64_t min_src_plan_capacity(const vtoken_batch* b, int32_t block_size, bool inplace) {
+  // at most min(free_len, M) destinations out of place; at most M in place
+  const int64_t f = inplace || b->num_bt_entries < b->free_len ? b->num_bt_entries : b->free_len;
   return f * block_size;
 }
 
-vtoken_status check_plan(const vtoken_plan* p, const vtoken_batch* b, int32_t block_size) {
+vtoken_status check_plan(const vtoken_plan* p, const vtoken_batch* b, int32_t block_size,
+                         bool inplace) {
   if (p == nullptr) return VTOKEN_ERR_NULL;
   if (p->dst_indptr == nullptr || p->new_bt_indptr == nullptr || p->freed_indptr == nullptr ||
       p->counters == nullptr) {
@@ -57,7 +59,7 @@ vtoken_status check_plan(const vtoken_plan* p, const vtoken_batch* b, int32_t bl
     return VTOKEN_ERR_NULL;
   }
   if (b->num_bt_entries > 0 && p->new_block_ids == nullptr) return VTOKEN_ERR_NULL;
-  const int64_t plan_min = min_src_plan_capacity(b, block_size);
+  const int64_t plan_min = min_src_plan_capacity(b, block_size, inplace);
   if (plan_min > 0 && p->src_plan == nullptr) return VTOKEN_ERR_NULL;
   if (p->new_bt_capacity < b->num_bt_entries) return VTOKEN_ERR_CAPACITY;
   if (p->src_plan_capacity < plan_min) return VTOKEN_ERR_CAPACITY;
@@ -89,6 +91,7 @@ vtoken::MetaArgs meta_args(const vtoken_cache* c, const vtoken_batch* b, const v
   a.counters = p->counters;
   a.new_bt_capacity = p->new_bt_capacity;
   a.src_plan_capacity = p->src_plan_capacity;
+  a.inplace = 0;
   return a;
 }
 
@@ -101,9 +104,56 @@ vtoken_status vtoken_build_token_table(const vtoken_cache* cache, const vtoken_b
   vtoken_status s = check_cache(cache);
   if (s != VTOKEN_OK) return s;
   if ((s = check_batch(batch)) != VTOKEN_OK) return s;
-  if ((s = check_plan(plan, batch, cache->block_size)) != VTOKEN_OK) return s;
-  const vtoken::MetaArgs a = meta_args(cache, batch, plan);
+  if ((s = check_plan(plan, batch, cache->block_size, false)) != VTOKEN_OK) return s;
+  vtoken::MetaArgs a = meta_args(cache, batch, plan);
+  a.inplace = 0;
   return vtoken::launch_build(a, stream) == hipSuccess ? VTOKEN_OK : VTOKEN_ERR_HIP;
+}
+
+vtoken_status vtoken_build_token_table_inplace(const vtoken_cache* cache,
+                                               const vtoken_batch* batch,
+                                               const vtoken_plan* plan, hipStream_t stream) {
+  vtoken_status s = check_cache(cache);
+  if (s != VTOKEN_OK) return s;
+  if ((s = check_batch(batch)) != VTOKEN_OK) return s;
+  if ((s = check_plan(plan, batch, cache->block_size, true)) != VTOKEN_OK) return s;
+  vtoken::MetaArgs a = meta_args(cache, batch, plan);
+  a.inplace = 1;
+  a.free_list = nullptr;
+  a.free_len = 0;
+  return vtoken::launch_build(a, stream) == hipSuccess ? VTOKEN_OK : VTOKEN_ERR_HIP;
+}
+
+vtoken_status vtoken_repack_inplace(const vtoken_cache* cache, const vtoken_batch* batch,
+                                    const vtoken_plan* plan, hipStream_t stream) {
+  vtoken_status s = check_cache(cache);
+  if (s != VTOKEN_OK) return s;
+  if ((s = check_batch(batch)) != VTOKEN_OK) return s;
+  if ((s = check_plan(plan, batch, cache->block_size, true)) != VTOKEN_OK) return s;
+  const int64_t row = (int64_t)cache->num_kv_heads * cache->head_dim * cache->elem_bytes;
+  if ((int64_t)cache->block_size * row > vtoken::kMaxInplaceChunkBytes) return VTOKEN_ERR_SHAPE;
+  if ((int64_t)batch->num_reqs * 2 * cache->num_layers > kInt32Limit) return VTOKEN_ERR_SHAPE;
+  vtoken::InplaceArgs a;
+  a.kv = static_cast<uint8_t*>(cache->kv);
+  a.row_bytes = row;
+  a.plane_bytes = (int64_t)cache->num_blocks * cache->block_size * row;
+  a.num_planes = 2 * cache->num_layers;
+  a.block_size = cache->block_size;
+  a.num_blocks = cache->num_blocks;
+  a.num_slots = cache->num_blocks * cache->block_size;
+  a.row_units = static_cast<int32_t>(row / 16);
+  a.chunk_units = cache->block_size * a.row_units;
+  a.row_magic = a.row_units > 1 ? static_cast<uint32_t>((1ULL << 32) / a.row_units + 1) : 0u;
+  a.num_reqs = batch->num_reqs;
+  a.src_plan_capacity = plan->src_plan_capacity;
+  a.new_bt_capacity = plan->new_bt_capacity;
+  a.src_plan = plan->src_plan;
+  a.new_block_ids = plan->new_block_ids;
+  a.dst_indptr = plan->dst_indptr;
+  a.new_bt_indptr = plan->new_bt_indptr;
+  a.admitted = plan->admitted;
+  a.counters = plan->counters;
+  return vtoken::launch_repack_inplace(a, stream) == hipSuccess ? VTOKEN_OK : VTOKEN_ERR_HIP;
 }
 
 vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* batch,
@@ -113,7 +163,7 @@ vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* ba
   if (s != VTOKEN_OK) return s;
   if ((s = check_batch(batch)) != VTOKEN_OK) return s;
   if (plan == nullptr || plan->counters == nullptr) return VTOKEN_ERR_NULL;
-  const int64_t plan_min = min_src_plan_capacity(batch, cache->block_size);
+  const int64_t plan_min = min_src_plan_capacity(batch, cache->block_size, false);
   if (plan_min > 0 && plan->src_plan == nullptr) return VTOKEN_ERR_NULL;
   if (plan->src_plan_capacity < plan_min) return VTOKEN_ERR_CAPACITY;
   int variant = 0, grid = 0, order = 0;

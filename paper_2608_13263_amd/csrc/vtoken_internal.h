@@ -47,6 +47,7 @@ struct MetaArgs {
   int32_t* counters;
   int64_t new_bt_capacity;
   int64_t src_plan_capacity;
+  int32_t inplace;          // 1: destinations are each request's own leading blocks
 };
 
 struct CopyArgs {
@@ -67,7 +68,34 @@ struct CopyArgs {
   const int32_t* counters;
 };
 
+// Arguments of the in-place copy: one workgroup per (request, plane) chain.
+struct InplaceArgs {
+  uint8_t* kv;
+  int64_t plane_bytes;
+  int64_t row_bytes;
+  int32_t num_planes;
+  int32_t block_size;
+  int32_t num_blocks;
+  int32_t num_slots;
+  int32_t row_units;
+  int32_t chunk_units;
+  uint32_t row_magic;
+  int32_t num_reqs;
+  int64_t src_plan_capacity;
+  int64_t new_bt_capacity;
+  const int32_t* src_plan;
+  const int32_t* new_block_ids;
+  const int32_t* dst_indptr;
+  const int32_t* new_bt_indptr;
+  const int32_t* admitted;
+  const int32_t* counters;
+};
+
+// Largest chunk (S * row_bytes) the in-place copy stages through LDS.
+constexpr int64_t kMaxInplaceChunkBytes = 64 * 1024;
+
 hipError_t launch_build(const MetaArgs& a, hipStream_t stream);
+hipError_t launch_repack_inplace(const InplaceArgs& a, hipStream_t stream);
 hipError_t launch_free(const MetaArgs& a, int32_t* freed, int64_t freed_capacity,
                        hipStream_t stream);
 // variant/grid/order as in vtoken_repack_options; returns hipErrorInvalidValue for an

@@ -165,8 +165,11 @@ __global__ __launch_bounds__(kAdmitThreads) void admit_kernel(MetaArgs a) {
     int s1[4] = {profitable ? need : 0, 0, 0, 0};
     int t1[4];
     block_exclusive_scan<4>(s1, t1, lds);
-    const bool adm = profitable && (carry_e + s1[0] + need <= a.free_len);
-    int s2[4] = {adm ? need : 0, adm ? need : m, adm ? m : 0, adm ? 1 : 0};
+    // in place the destinations are the request's own blocks: nothing to wait for
+    const bool adm = profitable && (a.inplace || carry_e + s1[0] + need <= a.free_len);
+    // freed: all old blocks out of place, the blocks past the need in place
+    const int n_free = adm ? (a.inplace ? m - need : m) : 0;
+    int s2[4] = {adm ? need : 0, adm ? need : m, n_free, adm ? 1 : 0};
     int t2[4];
     block_exclusive_scan<4>(s2, t2, lds);
     if (valid) {
@@ -191,10 +194,11 @@ __global__ __launch_bounds__(kAdmitThreads) void admit_kernel(MetaArgs a) {
   if (first_error_req != INT_MAX) status = a.live_count[first_error_req];
   const int used = carry_dst;
   if (status == 0 && ((int64_t)carry_new > a.new_bt_capacity ||
-                      (int64_t)used * S > a.src_plan_capacity || used > a.free_len)) {
+                      (int64_t)used * S > a.src_plan_capacity ||
+                      (!a.inplace && used > a.free_len))) {
     status = VTOKEN_ERR_CAPACITY;
   }
-  if (status == 0) {
+  if (status == 0 && !a.inplace) {
     int bad = 0;
     for (int j = tid; j < used; j += kAdmitThreads) {
       const int blk = a.free_list[j];
@@ -225,7 +229,7 @@ __global__ __launch_bounds__(kScanThreads) void table_kernel(MetaArgs a) {
   if (a.admitted[r]) {
     const int o = a.dst_indptr[r];
     const int need = a.dst_indptr[r + 1] - o;
-    const int32_t* dest = a.free_list + o;
+    const int32_t* dest = a.inplace ? bt : a.free_list + o;
     int32_t* plan = a.src_plan + (int64_t)o * S;
     for (int j = tid; j < need; j += kScanThreads) nbt[j] = dest[j];
     for (int p = tid; p < n; p += kScanThreads) {
@@ -260,12 +264,16 @@ __global__ __launch_bounds__(kFreeThreads) void free_kernel(MetaArgs a, int32_t*
   if (a.counters[3] != 0) return;
   const int r = blockIdx.x;
   if (!a.admitted[r]) return;
+  // the freed blocks are the last n entries of the old table (all of it out of place, the
+  // part past the new table in place)
   const int b0 = a.bt_indptr[r];
   const int m = a.bt_indptr[r + 1] - b0;
   const int64_t o = a.freed_indptr[r];
-  if (b0 < 0 || m < 0 || (int64_t)b0 + m > a.num_bt_entries || o < 0) return;
-  for (int j = threadIdx.x; j < m; j += kFreeThreads) {
-    if (o + j < capacity) freed[o + j] = a.block_ids[b0 + j];
+  const int n = a.freed_indptr[r + 1] - a.freed_indptr[r];
+  if (b0 < 0 || m < 0 || (int64_t)b0 + m > a.num_bt_entries || o < 0 || n < 0 || n > m) return;
+  const int first = b0 + m - n;
+  for (int j = threadIdx.x; j < n; j += kFreeThreads) {
+    if (o + j < capacity) freed[o + j] = a.block_ids[first + j];
   }
 }
 
@@ -461,7 +469,141 @@ hipError_t launch_policy(const CopyArgs& a, int grid, hipStream_t stream) {
   return launch_direct<kPolicy, 1>(a, grid, stream);
 }
 
+// ------------------------------------------------------------------------------------------
+// In-place copy. Destination block b of request r is r's own b-th block, and the token of
+// rank k sits at position p >= k, so the sources of destination block b lie in blocks >= b
+// of the same request: block b may be written only after every read for blocks <= b.
+// One workgroup walks one (request, plane) chain in block order: it stages the rows of
+// block b that move (rows already in place are skipped) into LDS with direct 16-byte
+// global->LDS loads, waits for them, synchronises, and writes them back from LDS. Reads for
+// block b+1 touch blocks >= b+1 only, so they may start while block b is being written.
+// With two LDS buffers one barrier per block suffices: a thread stages block b+1 into buffer
+// (b+1)%2 only after passing barrier b, and every thread reaches barrier b only after its
+// writes of block b-1, the last use of that buffer. With one buffer a second barrier after
+// the writes protects it.
+// ------------------------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+template <int kV, bool kSmallS, bool kDouble>
+__global__ __launch_bounds__(kCopyThreads) void repack_inplace_kernel(InplaceArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t stage[];
+  if (a.counters[3] != 0) return;
+  const int P = a.num_planes;
+  const int r = static_cast<int>(blockIdx.x / P);
+  const int plane = static_cast<int>(blockIdx.x - (int64_t)r * P);
+  if (r >= a.num_reqs || !a.admitted[r]) return;
+  const int g0 = a.dst_indptr[r];
+  const int need = a.dst_indptr[r + 1] - g0;
+  const int nb0 = a.new_bt_indptr[r];
+  const int S = a.block_size;
+  if (g0 < 0 || need <= 0 || nb0 < 0 || (int64_t)(g0 + need) * S > a.src_plan_capacity ||
+      (int64_t)nb0 + need > a.new_bt_capacity) {
+    return;
+  }
+  const int U = a.row_units;
+  const int chunk = a.chunk_units;
+  const uint32_t magic = a.row_magic;
+  const bool unit_rows = U == 1;
+  const int tid = static_cast<int>(threadIdx.x);
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  uint8_t* pbase = a.kv + (int64_t)plane * a.plane_bytes;
+  const int chunk_bytes = chunk * 16;
+  const int plan_lane = lane < S ? lane : S - 1;
+  // the next block's table entry and plan entry are fetched one block ahead; the barrier
+  // that ends each block has retired them by the time they are used
+  int next_pv = kSmallS ? a.src_plan[(int64_t)g0 * S + plan_lane] : -1;
+  int next_dblk = a.new_block_ids[nb0];
+
+  for (int b = 0; b < need; ++b) {
+    const int dblk = __builtin_amdgcn_readfirstlane(next_dblk);
+    const int pv = next_pv;
+    const int bn = b + 1 < need ? b + 1 : b;
+    next_dblk = a.new_block_ids[nb0 + bn];
+    if (kSmallS) next_pv = a.src_plan[(int64_t)(g0 + bn) * S + plan_lane];
+    if (static_cast<unsigned>(dblk) >= static_cast<unsigned>(a.num_blocks)) continue;
+    const int32_t* plan = a.src_plan + (int64_t)(g0 + b) * S;
+    const int dslot0 = dblk * S;
+    // LDS buffer of this block (offsets into `stage`: the direct-load builtin needs an
+    // address derived from the shared array itself)
+    const int buf = kDouble ? (b & 1) * chunk_bytes : 0;
+    int src[kV];
+    int col[kV];
+    bool mv[kV];
+#pragma unroll
+    for (int v = 0; v < kV; ++v) {
+      const int u = v * kCopyThreads + tid;
+      const int j = unit_rows ? u : static_cast<int>(__umulhi(static_cast<uint32_t>(u), magic));
+      col[v] = u - j * U;
+      if (kSmallS) {
+        src[v] = __shfl(pv, j & 63, 64);
+      } else {
+        src[v] = u < chunk ? plan[j] : -1;
+      }
+      // rows already in place (source slot == destination slot) are not copied
+      mv[v] = (u < chunk) && static_cast<unsigned>(src[v]) < static_cast<unsigned>(a.num_slots) &&
+              src[v] != dslot0 + j;
+    }
+    // stage the moving rows of block b: lane i of a wave lands at wave base + 16 i
+#pragma unroll
+    for (int v = 0; v < kV; ++v) {
+      if (mv[v]) {
+        // addresses in locals of non-dependent type: a template-dependent argument makes
+        // the host pass drop the kernel without a diagnostic
+        const uint8_t* gsrc = pbase + (int64_t)src[v] * a.row_bytes + col[v] * 16;
+        const int loff = buf + (v * kCopyThreads + wave * 64) * 16;
+        __builtin_amdgcn_global_load_lds(gsrc, (lds_ptr_t)(stage + loff), 16, 0, 0);
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < kV; ++v) {
+      if (mv[v]) {
+        const int u = v * kCopyThreads + tid;
+        const u32x4 val = *reinterpret_cast<const u32x4*>(stage + buf + u * 16);
+        *reinterpret_cast<u32x4*>(pbase + (int64_t)dslot0 * a.row_bytes + (int64_t)u * 16) = val;
+      }
+    }
+    if (!kDouble) __syncthreads();
+  }
+}
+
+template <int kV, bool kSmallS>
+hipError_t launch_inplace_v(const InplaceArgs& a, hipStream_t stream) {
+  const int64_t grid = (int64_t)a.num_reqs * a.num_planes;
+  const int64_t chunk_bytes = (int64_t)a.chunk_units * 16;
+  if (chunk_bytes * 2 <= kMaxInplaceChunkBytes) {
+    auto kernel = repack_inplace_kernel<kV, kSmallS, true>;
+    hipLaunchKernelGGL(kernel, dim3(static_cast<unsigned>(grid)), dim3(kCopyThreads),
+                       static_cast<size_t>(2 * chunk_bytes), stream, a);
+  } else {
+    auto kernel = repack_inplace_kernel<kV, kSmallS, false>;
+    hipLaunchKernelGGL(kernel, dim3(static_cast<unsigned>(grid)), dim3(kCopyThreads),
+                       static_cast<size_t>(chunk_bytes), stream, a);
+  }
+  return hipGetLastError();
+}
+
+template <bool kSmallS>
+hipError_t launch_inplace_s(const InplaceArgs& a, hipStream_t stream) {
+  // units per thread that cover one chunk (at most 16: chunks are at most 64 KiB)
+  const int per_thread = (a.chunk_units + kCopyThreads - 1) / kCopyThreads;
+  if (per_thread <= 1) return launch_inplace_v<1, kSmallS>(a, stream);
+  if (per_thread <= 2) return launch_inplace_v<2, kSmallS>(a, stream);
+  if (per_thread <= 4) return launch_inplace_v<4, kSmallS>(a, stream);
+  if (per_thread <= 8) return launch_inplace_v<8, kSmallS>(a, stream);
+  return launch_inplace_v<16, kSmallS>(a, stream);
+}
+
 }  // namespace
+
+hipError_t launch_repack_inplace(const InplaceArgs& a, hipStream_t stream) {
+  if ((int64_t)a.num_reqs * a.num_planes <= 0) return hipSuccess;
+  if ((int64_t)a.chunk_units * 16 > kMaxInplaceChunkBytes) return hipErrorInvalidValue;
+  return a.block_size <= 64 ? launch_inplace_s<true>(a, stream)
+                            : launch_inplace_s<false>(a, stream);
+}
 
 hipError_t launch_build(const MetaArgs& a, hipStream_t stream) {
   if (a.num_reqs > 0) {

@@ -20,7 +20,7 @@ def kv_bytes(kv, shape: W.KVShape):
     return kv.view(t.uint8).reshape(shape.num_planes, n, shape.row_bytes).cpu().numpy()
 
 
-def gpu_pass(inp: W.RepackInputs, kv, variant=0, grid=0, order=0, label=""):
+def gpu_pass(inp: W.RepackInputs, kv, variant=0, grid=0, order=0, label="", inplace=False):
     """build_token_table -> repack_ex -> free_blocks on the current stream; returns host
     copies of every plan output, trimmed to the sizes the counters report."""
     t = torch()
@@ -28,13 +28,17 @@ def gpu_pass(inp: W.RepackInputs, kv, variant=0, grid=0, order=0, label=""):
     print(f"[gpu] {label or inp.name}: R={inp.num_reqs} T={inp.num_tokens} "
           f"M={inp.num_bt_entries} f={len(inp.free_list)} S={inp.shape.block_size} "
           f"row={inp.shape.row_bytes}B planes={inp.shape.num_planes} "
-          f"variant={variant} grid={grid} order={order}", flush=True)
+          f"variant={variant} grid={grid} order={order} inplace={inplace}", flush=True)
     cache = B.KVCache(kv, inp.shape.num_layers, inp.shape.num_kv_heads, inp.shape.head_dim,
                       inp.shape.block_size)
     batch = B.Batch.from_inputs(inp)
-    plan = B.Plan.allocate(batch, inp.shape.block_size)
-    B.build_token_table(cache, batch, plan)
-    B.repack_ex(cache, batch, plan, variant=variant, grid=grid, order=order)
+    plan = B.Plan.allocate(batch, inp.shape.block_size, inplace=inplace)
+    if inplace:
+        B.build_token_table_inplace(cache, batch, plan)
+        B.repack_inplace(cache, batch, plan)
+    else:
+        B.build_token_table(cache, batch, plan)
+        B.repack_ex(cache, batch, plan, variant=variant, grid=grid, order=order)
     B.free_blocks(batch, plan)
     t.cuda.synchronize()
     return plan_to_host(plan, inp)
@@ -82,14 +86,14 @@ def assert_kv_equal(got: np.ndarray, expect: np.ndarray) -> None:
 
 
 def full_parity(inp: W.RepackInputs, seed: int = 0, variant=0, grid=0, order=0,
-                kv_dtype_shape=None):
+                inplace=False):
     """Seeded KV on the device, one pass through the C ABI, every output and every KV byte
     against the oracle run on the pre-call bytes."""
     t = torch()
     kv = W.kv_device(inp.shape, inp.num_blocks, seed)
     before = kv_bytes(kv, inp.shape)
-    orc = oracle_repack_inputs(inp, before)
-    gpu = gpu_pass(inp, kv, variant=variant, grid=grid, order=order)
+    orc = oracle_repack_inputs(inp, before, inplace=inplace)
+    gpu = gpu_pass(inp, kv, variant=variant, grid=grid, order=order, inplace=inplace)
     assert_plan_equal(gpu, orc)
     assert_kv_equal(kv_bytes(kv, inp.shape), orc.kv)
     del kv

@@ -140,3 +140,16 @@ def test_repack_and_free_reject_bad_arguments():
 def test_binding_fails_loudly_without_library(tmp_path):
     with pytest.raises(RuntimeError, match="missing"):
         B.load_library(str(tmp_path / "libvtoken.so"))
+
+
+def test_no_undefined_library_symbols():
+    """Every kernel the library launches is defined in it (a template kernel the host pass
+    silently drops would leave an undefined handle that only fails at load time)."""
+    import shutil
+    import subprocess
+    if shutil.which("nm") is None:
+        pytest.skip("nm not available")
+    out = subprocess.run(["nm", "-D", "--undefined-only", B.LIB_PATH], check=True,
+                         capture_output=True, text=True).stdout
+    bad = [ln for ln in out.splitlines() if "vtoken" in ln]
+    assert not bad, bad

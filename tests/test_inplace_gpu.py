@@ -1,0 +1,100 @@
+"""In-place mode through the C ABI vs the oracle's in-place mode: bit-exact on every output
+and every KV byte. Overlap-heavy masks check the block-order hazard rule: a destination
+block is written only after every read of its own and earlier destination blocks."""
+import numpy as np
+import pytest
+
+from gpu_helpers import assert_kv_equal, assert_plan_equal, full_parity, gpu_pass, kv_bytes, torch
+from oracle.repack import oracle_repack_inputs
+from paper_2608_13263_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def test_inplace_tiny():
+    full_parity(W.tiny_cache(101), seed=1, inplace=True)
+
+
+def test_inplace_llama3_8b_random_two_layers():
+    full_parity(W.llama3_8b_random(201, num_layers=2, num_reqs=8), seed=3, inplace=True)
+
+
+def test_inplace_llama3_8b_h2o_one_layer():
+    full_parity(W.llama3_8b_h2o(301, num_layers=1, num_reqs=6), seed=4, inplace=True)
+
+
+@pytest.mark.parametrize("dtype", ["fp8_e4m3", "bf16"])
+def test_inplace_llama3_70b_shape(dtype):
+    # bf16 at S = 32 stages 64 KiB blocks (single LDS buffer), fp8 32 KiB (double buffer)
+    inp = W.llama3_70b_h2o(501, keep=0.3, dtype=dtype, num_layers=2, num_reqs=3,
+                           len_range=(3000, 7000))
+    full_parity(inp, seed=5, inplace=True)
+
+
+def _overlap_masks(S, rng):
+    n = 9 * S + 3
+    return [
+        [0] + [1] * (n - 1),                      # every row shifts by one slot
+        [1] * S + [0] + [1] * (n - S - 1),        # identity first block, then a one-slot shift
+        [0] * S + [1] * (n - S),                  # every row moves back by a whole block
+        list((rng.random(n) < 0.97).astype(int)),  # few holes: long overlapping chains
+        list((rng.random(n) < 0.5).astype(int)),
+        [1] * (n - 1) + [0],                      # only the tail is dead: pure identity
+        [],
+        [0] * 40,
+        [1] * 33,
+    ]
+
+
+@pytest.mark.parametrize("S", [1, 2, 16, 32, 48, 128])
+def test_inplace_overlap_masks(S):
+    rng = np.random.default_rng(100 + S)
+    shape = W.KVShape(1, 2, 64, S, "fp16")
+    inp = W.from_masks(_overlap_masks(S, rng), shape, free_blocks=4, seed=S)
+    full_parity(inp, seed=S, inplace=True)
+
+
+@pytest.mark.parametrize("heads,dim,dtype", [(3, 8, "fp16"), (1, 8, "fp16"), (5, 48, "bf16"),
+                                             (8, 128, "bf16"), (1, 128, "fp8_e4m3")])
+def test_inplace_row_geometries(heads, dim, dtype):
+    rng = np.random.default_rng(heads * 100 + dim)
+    shape = W.KVShape(2, heads, dim, 16, dtype)
+    masks = [list((rng.random(int(n)) < 0.6).astype(int)) for n in rng.integers(1, 400, 10)]
+    full_parity(W.from_masks(masks, shape, free_blocks=0, seed=4), seed=8, inplace=True)
+
+
+def test_inplace_second_pass_moves_nothing():
+    """After a pass, the packed layout (live tokens only) needs no further repack."""
+    t = torch()
+    from paper_2608_13263_amd import binding as B
+    inp = W.llama3_8b_random(212, num_layers=2, num_reqs=6, len_range=(500, 2500))
+    kv = W.kv_device(inp.shape, inp.num_blocks, 6)
+    before = kv_bytes(kv, inp.shape)
+    orc = oracle_repack_inputs(inp, before, inplace=True)
+    gpu = gpu_pass(inp, kv, inplace=True)
+    assert_plan_equal(gpu, orc)
+    assert_kv_equal(kv_bytes(kv, inp.shape), orc.kv)
+    # second pass over the committed layout
+    R = inp.num_reqs
+    masks, tables = [], []
+    for r in range(R):
+        a = int(inp.tok_indptr[r])
+        lv = inp.live[a:a + int(inp.seq_lens[r])]
+        nbt = orc.new_block_ids[orc.new_bt_indptr[r]:orc.new_bt_indptr[r + 1]]
+        masks.append(np.ones(int(lv.sum()), np.uint8) if orc.admitted[r] else lv)
+        tables.append(nbt)
+    nxt = W.RepackInputs(
+        name="second pass", shape=inp.shape, num_blocks=inp.num_blocks,
+        seq_lens=np.array([len(m) for m in masks], np.int32),
+        tok_indptr=np.concatenate([[0], np.cumsum([len(m) for m in masks])]).astype(np.int32),
+        bt_indptr=np.concatenate([[0], np.cumsum([len(x) for x in tables])]).astype(np.int32),
+        block_ids=np.concatenate(tables).astype(np.int32),
+        live=np.concatenate(masks).astype(np.uint8),
+        free_list=np.concatenate([inp.free_list, orc.freed]).astype(np.int32))
+    snap = kv_bytes(kv, inp.shape)
+    gpu2 = gpu_pass(nxt, kv, inplace=True, label="in-place second pass")
+    orc2 = oracle_repack_inputs(nxt, snap, inplace=True)
+    assert_plan_equal(gpu2, orc2)
+    assert_kv_equal(kv_bytes(kv, inp.shape), snap)
+    del kv
+    t.cuda.empty_cache()
