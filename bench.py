@@ -267,7 +267,7 @@ def run_inplace(args, inp, kv, cache, batch, plan, stream):
         B.build_token_table_inplace(cache, batch, plan, stream)
         if ev is not None:
             ev[0].record(stream)
-        B.repack_inplace(cache, batch, plan, stream)
+        B.repack_inplace_ex(cache, batch, plan, args.variant, stream)
         if ev is not None:
             ev[1].record(stream)
         B.free_blocks(batch, plan, stream=stream)

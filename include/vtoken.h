@@ -201,6 +201,17 @@ vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* ba
                                const vtoken_plan* plan, const vtoken_repack_options* options,
                                hipStream_t stream);
 
+/* Tuning entry for the in-place copy; vtoken_repack_inplace uses the default (variant 0).
+ *   variant: how a destination block is staged between its reads and its writes:
+ *            0 default (= 3), 1 LDS double buffer (direct global->LDS loads; falls back to
+ *            2 when two blocks exceed 64 KiB), 2 LDS single buffer, 3 registers
+ *   grid, order: must be 0 (one workgroup per (request, plane) chain)
+ * All variants produce identical bytes. */
+vtoken_status vtoken_repack_inplace_ex(const vtoken_cache* cache, const vtoken_batch* batch,
+                                       const vtoken_plan* plan,
+                                       const vtoken_repack_options* options,
+                                       hipStream_t stream);
+
 /* Static string naming a status code; never NULL. */
 const char* vtoken_status_string(int32_t status);
 

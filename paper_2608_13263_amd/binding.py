@@ -77,6 +77,10 @@ _SIGNATURES = {
                                                           ctypes.c_void_p]),
     "vtoken_repack_inplace": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
                                                ctypes.POINTER(CPlan), ctypes.c_void_p]),
+    "vtoken_repack_inplace_ex": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
+                                                  ctypes.POINTER(CPlan),
+                                                  ctypes.POINTER(CRepackOptions),
+                                                  ctypes.c_void_p]),
     "vtoken_repack_ex": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
                                           ctypes.POINTER(CPlan), ctypes.POINTER(CRepackOptions),
                                           ctypes.c_void_p]),
@@ -231,6 +235,16 @@ def repack_inplace(cache: KVCache, batch: Batch, plan: Plan, stream=None) -> Non
     c, b, p = cache.c(), batch.c(), plan.c()
     _check(lib.vtoken_repack_inplace(ctypes.byref(c), ctypes.byref(b), ctypes.byref(p),
                                      _stream(stream)), "vtoken_repack_inplace")
+
+
+def repack_inplace_ex(cache: KVCache, batch: Batch, plan: Plan, variant: int = 0,
+                      stream=None) -> None:
+    lib = load_library()
+    c, b, p = cache.c(), batch.c(), plan.c()
+    o = CRepackOptions(variant, 0, 0, 0)
+    _check(lib.vtoken_repack_inplace_ex(ctypes.byref(c), ctypes.byref(b), ctypes.byref(p),
+                                        ctypes.byref(o), _stream(stream)),
+           "vtoken_repack_inplace_ex")
 
 
 def repack(cache: KVCache, batch: Batch, plan: Plan, stream=None) -> None:

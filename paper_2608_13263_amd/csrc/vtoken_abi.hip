@@ -126,6 +126,18 @@ vtoken_status vtoken_build_token_table_inplace(const vtoken_cache* cache,
 
 vtoken_status vtoken_repack_inplace(const vtoken_cache* cache, const vtoken_batch* batch,
                                     const vtoken_plan* plan, hipStream_t stream) {
+  return vtoken_repack_inplace_ex(cache, batch, plan, nullptr, stream);
+}
+
+vtoken_status vtoken_repack_inplace_ex(const vtoken_cache* cache, const vtoken_batch* batch,
+                                       const vtoken_plan* plan,
+                                       const vtoken_repack_options* options,
+                                       hipStream_t stream) {
+  const int variant = options != nullptr ? options->variant : 0;
+  if (variant < 0 || variant > 3 || (options != nullptr && (options->grid != 0 ||
+                                                            options->order != 0))) {
+    return VTOKEN_ERR_ARGUMENT;
+  }
   vtoken_status s = check_cache(cache);
   if (s != VTOKEN_OK) return s;
   if ((s = check_batch(batch)) != VTOKEN_OK) return s;
@@ -153,7 +165,8 @@ vtoken_status vtoken_repack_inplace(const vtoken_cache* cache, const vtoken_batc
   a.new_bt_indptr = plan->new_bt_indptr;
   a.admitted = plan->admitted;
   a.counters = plan->counters;
-  return vtoken::launch_repack_inplace(a, stream) == hipSuccess ? VTOKEN_OK : VTOKEN_ERR_HIP;
+  return vtoken::launch_repack_inplace(a, variant, stream) == hipSuccess ? VTOKEN_OK
+                                                                          : VTOKEN_ERR_HIP;
 }
 
 vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* batch,

@@ -95,7 +95,8 @@ struct InplaceArgs {
 constexpr int64_t kMaxInplaceChunkBytes = 64 * 1024;
 
 hipError_t launch_build(const MetaArgs& a, hipStream_t stream);
-hipError_t launch_repack_inplace(const InplaceArgs& a, hipStream_t stream);
+// variant: 0 default, 1 LDS double buffer, 2 LDS single buffer, 3 registers
+hipError_t launch_repack_inplace(const InplaceArgs& a, int variant, hipStream_t stream);
 hipError_t launch_free(const MetaArgs& a, int32_t* freed, int64_t freed_capacity,
                        hipStream_t stream);
 // variant/grid/order as in vtoken_repack_options; returns hipErrorInvalidValue for an

@@ -484,7 +484,11 @@ hipError_t launch_policy(const CopyArgs& a, int grid, hipStream_t stream) {
 // ------------------------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
-template <int kV, bool kSmallS, bool kDouble>
+// kStage: 0 LDS double buffer, 1 LDS single buffer, 2 registers (no LDS; the barrier alone
+// orders a block's reads before its writes, since every thread holds its own rows).
+enum InplaceStage { kLdsDouble = 0, kLdsSingle = 1, kRegisters = 2 };
+
+template <int kV, bool kSmallS, int kStage>
 __global__ __launch_bounds__(kCopyThreads) void repack_inplace_kernel(InplaceArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t stage[];
   if (a.counters[3] != 0) return;
@@ -514,6 +518,7 @@ __global__ __launch_bounds__(kCopyThreads) void repack_inplace_kernel(InplaceArg
   // that ends each block has retired them by the time they are used
   int next_pv = kSmallS ? a.src_plan[(int64_t)g0 * S + plan_lane] : -1;
   int next_dblk = a.new_block_ids[nb0];
+  int phase = 0;
 
   for (int b = 0; b < need; ++b) {
     const int dblk = __builtin_amdgcn_readfirstlane(next_dblk);
@@ -522,11 +527,19 @@ __global__ __launch_bounds__(kCopyThreads) void repack_inplace_kernel(InplaceArg
     next_dblk = a.new_block_ids[nb0 + bn];
     if (kSmallS) next_pv = a.src_plan[(int64_t)(g0 + bn) * S + plan_lane];
     if (static_cast<unsigned>(dblk) >= static_cast<unsigned>(a.num_blocks)) continue;
-    const int32_t* plan = a.src_plan + (int64_t)(g0 + b) * S;
     const int dslot0 = dblk * S;
+    if (kSmallS) {
+      // every wave holds the same plan row, so this ballot is uniform over the workgroup:
+      // a block whose rows are all in place needs no copy and no barrier
+      const bool row_moves = lane < S && static_cast<unsigned>(pv) <
+                             static_cast<unsigned>(a.num_slots) && pv != dslot0 + lane;
+      if (__ballot(row_moves) == 0) continue;
+    }
+    const int32_t* plan = a.src_plan + (int64_t)(g0 + b) * S;
     // LDS buffer of this block (offsets into `stage`: the direct-load builtin needs an
     // address derived from the shared array itself)
-    const int buf = kDouble ? (b & 1) * chunk_bytes : 0;
+    const int buf = kStage == kLdsDouble ? phase * chunk_bytes : 0;
+    phase ^= 1;
     int src[kV];
     int col[kV];
     bool mv[kV];
@@ -544,15 +557,20 @@ __global__ __launch_bounds__(kCopyThreads) void repack_inplace_kernel(InplaceArg
       mv[v] = (u < chunk) && static_cast<unsigned>(src[v]) < static_cast<unsigned>(a.num_slots) &&
               src[v] != dslot0 + j;
     }
-    // stage the moving rows of block b: lane i of a wave lands at wave base + 16 i
+    u32x4 regs[kStage == kRegisters ? kV : 1];
 #pragma unroll
     for (int v = 0; v < kV; ++v) {
       if (mv[v]) {
         // addresses in locals of non-dependent type: a template-dependent argument makes
         // the host pass drop the kernel without a diagnostic
         const uint8_t* gsrc = pbase + (int64_t)src[v] * a.row_bytes + col[v] * 16;
-        const int loff = buf + (v * kCopyThreads + wave * 64) * 16;
-        __builtin_amdgcn_global_load_lds(gsrc, (lds_ptr_t)(stage + loff), 16, 0, 0);
+        if (kStage == kRegisters) {
+          regs[kStage == kRegisters ? v : 0] = load16<true>(reinterpret_cast<const u32x4*>(gsrc));
+        } else {
+          // lane i of a wave lands at the wave's base + 16 i
+          const int loff = buf + (v * kCopyThreads + wave * 64) * 16;
+          __builtin_amdgcn_global_load_lds(gsrc, (lds_ptr_t)(stage + loff), 16, 0, 0);
+        }
       }
     }
     __builtin_amdgcn_s_waitcnt(0);
@@ -561,48 +579,57 @@ __global__ __launch_bounds__(kCopyThreads) void repack_inplace_kernel(InplaceArg
     for (int v = 0; v < kV; ++v) {
       if (mv[v]) {
         const int u = v * kCopyThreads + tid;
-        const u32x4 val = *reinterpret_cast<const u32x4*>(stage + buf + u * 16);
+        const u32x4 val = kStage == kRegisters
+                              ? regs[kStage == kRegisters ? v : 0]
+                              : *reinterpret_cast<const u32x4*>(stage + buf + u * 16);
         *reinterpret_cast<u32x4*>(pbase + (int64_t)dslot0 * a.row_bytes + (int64_t)u * 16) = val;
       }
     }
-    if (!kDouble) __syncthreads();
+    if (kStage == kLdsSingle) __syncthreads();
   }
 }
 
 template <int kV, bool kSmallS>
-hipError_t launch_inplace_v(const InplaceArgs& a, hipStream_t stream) {
+hipError_t launch_inplace_v(const InplaceArgs& a, int variant, hipStream_t stream) {
   const int64_t grid = (int64_t)a.num_reqs * a.num_planes;
   const int64_t chunk_bytes = (int64_t)a.chunk_units * 16;
-  if (chunk_bytes * 2 <= kMaxInplaceChunkBytes) {
-    auto kernel = repack_inplace_kernel<kV, kSmallS, true>;
-    hipLaunchKernelGGL(kernel, dim3(static_cast<unsigned>(grid)), dim3(kCopyThreads),
-                       static_cast<size_t>(2 * chunk_bytes), stream, a);
+  // default: registers (measured fastest); LDS double buffer when asked and two fit
+  int stage = variant == 1 ? kLdsDouble : variant == 2 ? kLdsSingle : kRegisters;
+  if (stage == kLdsDouble && chunk_bytes * 2 > kMaxInplaceChunkBytes) stage = kLdsSingle;
+  const dim3 g(static_cast<unsigned>(grid));
+  const dim3 t(kCopyThreads);
+  if (stage == kLdsDouble) {
+    auto kernel = repack_inplace_kernel<kV, kSmallS, kLdsDouble>;
+    hipLaunchKernelGGL(kernel, g, t, static_cast<size_t>(2 * chunk_bytes), stream, a);
+  } else if (stage == kLdsSingle) {
+    auto kernel = repack_inplace_kernel<kV, kSmallS, kLdsSingle>;
+    hipLaunchKernelGGL(kernel, g, t, static_cast<size_t>(chunk_bytes), stream, a);
   } else {
-    auto kernel = repack_inplace_kernel<kV, kSmallS, false>;
-    hipLaunchKernelGGL(kernel, dim3(static_cast<unsigned>(grid)), dim3(kCopyThreads),
-                       static_cast<size_t>(chunk_bytes), stream, a);
+    auto kernel = repack_inplace_kernel<kV, kSmallS, kRegisters>;
+    hipLaunchKernelGGL(kernel, g, t, 0, stream, a);
   }
   return hipGetLastError();
 }
 
 template <bool kSmallS>
-hipError_t launch_inplace_s(const InplaceArgs& a, hipStream_t stream) {
+hipError_t launch_inplace_s(const InplaceArgs& a, int variant, hipStream_t stream) {
   // units per thread that cover one chunk (at most 16: chunks are at most 64 KiB)
   const int per_thread = (a.chunk_units + kCopyThreads - 1) / kCopyThreads;
-  if (per_thread <= 1) return launch_inplace_v<1, kSmallS>(a, stream);
-  if (per_thread <= 2) return launch_inplace_v<2, kSmallS>(a, stream);
-  if (per_thread <= 4) return launch_inplace_v<4, kSmallS>(a, stream);
-  if (per_thread <= 8) return launch_inplace_v<8, kSmallS>(a, stream);
-  return launch_inplace_v<16, kSmallS>(a, stream);
+  if (per_thread <= 1) return launch_inplace_v<1, kSmallS>(a, variant, stream);
+  if (per_thread <= 2) return launch_inplace_v<2, kSmallS>(a, variant, stream);
+  if (per_thread <= 4) return launch_inplace_v<4, kSmallS>(a, variant, stream);
+  if (per_thread <= 8) return launch_inplace_v<8, kSmallS>(a, variant, stream);
+  return launch_inplace_v<16, kSmallS>(a, variant, stream);
 }
 
 }  // namespace
 
-hipError_t launch_repack_inplace(const InplaceArgs& a, hipStream_t stream) {
+hipError_t launch_repack_inplace(const InplaceArgs& a, int variant, hipStream_t stream) {
+  if (variant < 0 || variant > 3) return hipErrorInvalidValue;
   if ((int64_t)a.num_reqs * a.num_planes <= 0) return hipSuccess;
   if ((int64_t)a.chunk_units * 16 > kMaxInplaceChunkBytes) return hipErrorInvalidValue;
-  return a.block_size <= 64 ? launch_inplace_s<true>(a, stream)
-                            : launch_inplace_s<false>(a, stream);
+  return a.block_size <= 64 ? launch_inplace_s<true>(a, variant, stream)
+                            : launch_inplace_s<false>(a, variant, stream);
 }
 
 hipError_t launch_build(const MetaArgs& a, hipStream_t stream) {

@@ -35,7 +35,7 @@ def gpu_pass(inp: W.RepackInputs, kv, variant=0, grid=0, order=0, label="", inpl
     plan = B.Plan.allocate(batch, inp.shape.block_size, inplace=inplace)
     if inplace:
         B.build_token_table_inplace(cache, batch, plan)
-        B.repack_inplace(cache, batch, plan)
+        B.repack_inplace_ex(cache, batch, plan, variant=variant)
     else:
         B.build_token_table(cache, batch, plan)
         B.repack_ex(cache, batch, plan, variant=variant, grid=grid, order=order)

@@ -98,3 +98,15 @@ def test_inplace_second_pass_moves_nothing():
     assert_kv_equal(kv_bytes(kv, inp.shape), snap)
     del kv
     t.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("variant", [1, 2, 3])
+@pytest.mark.parametrize("S", [16, 32])
+def test_inplace_staging_variants(variant, S):
+    # LDS double buffer, LDS single buffer, registers: identical bytes
+    rng = np.random.default_rng(300 + S)
+    shape = W.KVShape(2, 8, 128, S, "bf16")
+    masks = _overlap_masks(S, rng) + [list((rng.random(int(n)) < 0.7).astype(int))
+                                      for n in rng.integers(50, 900, 6)]
+    full_parity(W.from_masks(masks, shape, free_blocks=0, seed=7), seed=11, inplace=True,
+                variant=variant)
