@@ -212,6 +212,46 @@ vtoken_status vtoken_repack_inplace_ex(const vtoken_cache* cache, const vtoken_b
                                        const vtoken_repack_options* options,
                                        hipStream_t stream);
 
+/* ---- Consumer side (Sec. 3.4: slot mapping; Sec. 3.3.4 and I3 of Sec. 3.5: ordering) ----
+ *
+ * The attention slot mapping: for every request, the slots of its live tokens in logical
+ * order, looked up once per token through the token table (Sec. 3.4). Reads plan->token_slot,
+ * plan->live_count and plan->counters of a preceding vtoken_build_token_table[_inplace] on the
+ * same stream (no-op when counters[3] is set); the slots are valid for attention once the
+ * matching repack has executed on the stream. slot_indptr [R+1] is the exclusive scan of the
+ * live counts; slots [slots_capacity >= num_tokens] receives the slots in CSR order. */
+vtoken_status vtoken_build_slot_mapping(const vtoken_batch* batch, const vtoken_plan* plan,
+                                        int32_t* slot_indptr, int32_t* slots,
+                                        int64_t slots_capacity, hipStream_t stream);
+
+/* Decode attention of one layer over the paged cache through a slot mapping: for request r
+ * and query head qh (GQA: KV head qh / (num_q_heads / num_kv_heads)),
+ *   out[r][qh] = softmax(scale * q[r][qh] . K[slot]^T) @ V[slot] over the slots of r,
+ * K and V being the layer's K and V planes (float32 math; zeros for a request with no slots).
+ * Flash-decoding: 256-token splits, then a merge; the workspace holds the split partials and
+ * is overwritten by every call (calls sharing it must be stream-ordered). */
+enum { VTOKEN_KV_FP16 = 0, VTOKEN_KV_BF16 = 1, VTOKEN_KV_FP8_E4M3 = 2 };
+
+typedef struct vtoken_decode {
+  const float* q;          /* device [R][num_q_heads][head_dim] float32                    */
+  float*       out;        /* device [R][num_q_heads][head_dim] float32                    */
+  int32_t      num_q_heads; /* num_kv_heads times 1, 2, 4 or 8                              */
+  int32_t      layer;      /* 0 <= layer < num_layers                                       */
+  int32_t      kv_dtype;   /* VTOKEN_KV_*; fp8 (OCP e4m3) iff elem_bytes == 1               */
+  float        scale;      /* softmax scale, usually 1/sqrt(head_dim)                       */
+  int32_t      max_tokens; /* [host] >= the slot count of every request                     */
+  float*       workspace;  /* device, >= vtoken_decode_workspace_bytes() bytes              */
+  int64_t      workspace_bytes;
+} vtoken_decode;
+
+/* head_dim*elem_bytes must be 64, 128 or 256 bytes (VTOKEN_ERR_SHAPE otherwise). Returns -1
+ * for invalid sizes. */
+int64_t vtoken_decode_workspace_bytes(int32_t num_reqs, int32_t num_q_heads, int32_t head_dim,
+                                      int32_t max_tokens);
+vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode* decode,
+                                  int32_t num_reqs, const int32_t* slot_indptr,
+                                  const int32_t* slots, hipStream_t stream);
+
 /* Static string naming a status code; never NULL. */
 const char* vtoken_status_string(int32_t status);
 

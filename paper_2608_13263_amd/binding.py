@@ -65,6 +65,17 @@ class CRepackOptions(ctypes.Structure):
                 ("order", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
+class CDecode(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("out", ctypes.c_void_p),
+                ("num_q_heads", ctypes.c_int32), ("layer", ctypes.c_int32),
+                ("kv_dtype", ctypes.c_int32), ("scale", ctypes.c_float),
+                ("max_tokens", ctypes.c_int32), ("workspace", ctypes.c_void_p),
+                ("workspace_bytes", ctypes.c_int64)]
+
+
+KV_FP16, KV_BF16, KV_FP8_E4M3 = 0, 1, 2
+
+
 # Every extern "C" symbol of include/vtoken.h with its ctypes signature.
 _SIGNATURES = {
     "vtoken_build_token_table": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
@@ -86,6 +97,15 @@ _SIGNATURES = {
                                           ctypes.c_void_p]),
     "vtoken_free_blocks": (ctypes.c_int32, [ctypes.POINTER(CBatch), ctypes.POINTER(CPlan),
                                             ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]),
+    "vtoken_build_slot_mapping": (ctypes.c_int32, [ctypes.POINTER(CBatch),
+                                                   ctypes.POINTER(CPlan), ctypes.c_void_p,
+                                                   ctypes.c_void_p, ctypes.c_int64,
+                                                   ctypes.c_void_p]),
+    "vtoken_decode_workspace_bytes": (ctypes.c_int64, [ctypes.c_int32, ctypes.c_int32,
+                                                       ctypes.c_int32, ctypes.c_int32]),
+    "vtoken_paged_decode": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CDecode),
+                                             ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                             ctypes.c_void_p]),
     "vtoken_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
     "vtoken_version": (ctypes.c_int32, []),
 }
@@ -284,3 +304,71 @@ def run_pass(cache: KVCache, batch: Batch, plan: Optional[Plan] = None, stream=N
         repack(cache, batch, plan, stream)
     free_blocks(batch, plan, stream=stream)
     return plan
+
+
+def build_slot_mapping(batch: Batch, plan: Plan, slot_indptr=None, slots=None,
+                       stream=None):
+    """Slots of every request's live tokens in logical order (CSR); returns
+    (slot_indptr [R+1], slots [T]) device tensors."""
+    import torch
+    lib = load_library()
+    dev = plan.counters.device
+    if slot_indptr is None:
+        slot_indptr = torch.empty(batch.num_reqs + 1, dtype=torch.int32, device=dev)
+    if slots is None:
+        slots = torch.empty(max(batch.num_tokens, 1), dtype=torch.int32, device=dev)
+    b, p = batch.c(), plan.c()
+    _check(lib.vtoken_build_slot_mapping(ctypes.byref(b), ctypes.byref(p), _ptr(slot_indptr),
+                                         _ptr(slots), int(slots.numel()), _stream(stream)),
+           "vtoken_build_slot_mapping")
+    return slot_indptr, slots
+
+
+def decode_workspace_bytes(num_reqs: int, num_q_heads: int, head_dim: int,
+                           max_tokens: int) -> int:
+    n = load_library().vtoken_decode_workspace_bytes(int(num_reqs), int(num_q_heads),
+                                                     int(head_dim), int(max_tokens))
+    if n < 0:
+        raise VTokenError(STATUS_CODE["VTOKEN_ERR_SHAPE"], "vtoken_decode_workspace_bytes")
+    return n
+
+
+def kv_dtype_code(dtype) -> int:
+    import torch
+    codes = {torch.float16: KV_FP16, torch.bfloat16: KV_BF16}
+    if hasattr(torch, "float8_e4m3fn"):
+        codes[torch.float8_e4m3fn] = KV_FP8_E4M3
+    if dtype not in codes:
+        raise ValueError(f"paged decode reads fp16, bf16 or fp8 e4m3 KV, not {dtype}")
+    return codes[dtype]
+
+
+def paged_decode(cache: KVCache, q, slot_indptr, slots, layer: int, max_tokens: int,
+                 scale: Optional[float] = None, out=None, workspace=None, kv_dtype=None,
+                 stream=None):
+    """Decode attention of one layer through a slot mapping; q and out are float32
+    [R][num_q_heads][head_dim] device tensors. kv_dtype defaults to the cache tensor's
+    dtype (a uint8 view of fp8 data needs KV_FP8_E4M3)."""
+    import torch
+    lib = load_library()
+    if q.dtype != torch.float32 or not q.is_contiguous() or q.dim() != 3:
+        raise ValueError("q must be a contiguous float32 [R][Hq][D] tensor")
+    R, Hq, D = (int(x) for x in q.shape)
+    if D != cache.head_dim:
+        raise ValueError("q head_dim differs from the cache's")
+    if out is None:
+        out = torch.empty_like(q)
+    if out.shape != q.shape or out.dtype != torch.float32 or not out.is_contiguous():
+        raise ValueError("out must match q")
+    need = decode_workspace_bytes(R, Hq, D, max_tokens)
+    if workspace is None:
+        workspace = torch.empty(max(need // 4, 1), dtype=torch.float32, device=q.device)
+    code = kv_dtype_code(cache.kv.dtype) if kv_dtype is None else int(kv_dtype)
+    if scale is None:
+        scale = D ** -0.5
+    d = CDecode(_ptr(q), _ptr(out), Hq, int(layer), code, float(scale), int(max_tokens),
+                _ptr(workspace), int(workspace.numel() * workspace.element_size()))
+    c = cache.c()
+    _check(lib.vtoken_paged_decode(ctypes.byref(c), ctypes.byref(d), R, _ptr(slot_indptr),
+                                   _ptr(slots), _stream(stream)), "vtoken_paged_decode")
+    return out

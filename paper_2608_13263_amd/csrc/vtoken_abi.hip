@@ -240,6 +240,93 @@ vtoken_status vtoken_free_blocks(const vtoken_batch* batch, const vtoken_plan* p
                                                                             : VTOKEN_ERR_HIP;
 }
 
+vtoken_status vtoken_build_slot_mapping(const vtoken_batch* batch, const vtoken_plan* plan,
+                                        int32_t* slot_indptr, int32_t* slots,
+                                        int64_t slots_capacity, hipStream_t stream) {
+  vtoken_status s = check_batch(batch);
+  if (s != VTOKEN_OK) return s;
+  if (plan == nullptr || plan->counters == nullptr || slot_indptr == nullptr) {
+    return VTOKEN_ERR_NULL;
+  }
+  if (batch->num_reqs > 0 && plan->live_count == nullptr) return VTOKEN_ERR_NULL;
+  if (batch->num_tokens > 0 && (plan->token_slot == nullptr || slots == nullptr)) {
+    return VTOKEN_ERR_NULL;
+  }
+  if (slots_capacity < batch->num_tokens) return VTOKEN_ERR_CAPACITY;
+  vtoken::SlotMapArgs a;
+  a.num_reqs = batch->num_reqs;
+  a.num_tokens = static_cast<int32_t>(batch->num_tokens);
+  a.tok_indptr = batch->tok_indptr;
+  a.token_slot = plan->token_slot;
+  a.live_count = plan->live_count;
+  a.counters = plan->counters;
+  a.slot_indptr = slot_indptr;
+  a.slots = slots;
+  a.slots_capacity = slots_capacity;
+  return vtoken::launch_slot_mapping(a, stream) == hipSuccess ? VTOKEN_OK : VTOKEN_ERR_HIP;
+}
+
+int64_t vtoken_decode_workspace_bytes(int32_t num_reqs, int32_t num_q_heads, int32_t head_dim,
+                                      int32_t max_tokens) {
+  if (num_reqs < 0 || num_q_heads <= 0 || head_dim <= 0 || max_tokens < 0) return -1;
+  const int64_t split = vtoken::attention_split_tokens();
+  const int64_t splits = max_tokens > 0 ? (max_tokens + split - 1) / split : 1;
+  return (int64_t)num_reqs * num_q_heads * splits * (head_dim + 2) * 4;
+}
+
+vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode* d,
+                                  int32_t num_reqs, const int32_t* slot_indptr,
+                                  const int32_t* slots, hipStream_t stream) {
+  vtoken_status s = check_cache(cache);
+  if (s != VTOKEN_OK) return s;
+  if (d == nullptr || slot_indptr == nullptr) return VTOKEN_ERR_NULL;
+  if (num_reqs < 0 || d->layer < 0 || d->layer >= cache->num_layers || d->max_tokens < 0) {
+    return VTOKEN_ERR_SHAPE;
+  }
+  if (num_reqs == 0) return VTOKEN_OK;
+  if (d->q == nullptr || d->out == nullptr || d->workspace == nullptr || slots == nullptr) {
+    return VTOKEN_ERR_NULL;
+  }
+  const int kind = d->kv_dtype;
+  if (kind < 0 || kind > 2 || (kind == 2) != (cache->elem_bytes == 1)) return VTOKEN_ERR_SHAPE;
+  const int g = cache->num_kv_heads > 0 ? d->num_q_heads / cache->num_kv_heads : 0;
+  if (d->num_q_heads <= 0 || d->num_q_heads % cache->num_kv_heads != 0 ||
+      (g != 1 && g != 2 && g != 4 && g != 8)) {
+    return VTOKEN_ERR_SHAPE;
+  }
+  const int lanes = cache->head_dim * cache->elem_bytes / 16;
+  if (cache->head_dim * cache->elem_bytes % 16 != 0 || (lanes != 4 && lanes != 8 && lanes != 16)) {
+    return VTOKEN_ERR_SHAPE;
+  }
+  const int64_t need = vtoken_decode_workspace_bytes(num_reqs, d->num_q_heads, cache->head_dim,
+                                                     d->max_tokens);
+  if (d->workspace_bytes < need) return VTOKEN_ERR_CAPACITY;
+  vtoken::AttnArgs a;
+  a.kv = static_cast<const uint8_t*>(cache->kv);
+  a.row_bytes = (int64_t)cache->num_kv_heads * cache->head_dim * cache->elem_bytes;
+  a.plane_bytes = (int64_t)cache->num_blocks * cache->block_size * a.row_bytes;
+  a.num_kv_heads = cache->num_kv_heads;
+  a.num_q_heads = d->num_q_heads;
+  a.head_dim = cache->head_dim;
+  a.layer = d->layer;
+  a.kv_kind = kind;
+  a.num_slots = cache->num_blocks * cache->block_size;
+  a.num_reqs = num_reqs;
+  const int split = vtoken::attention_split_tokens();
+  a.splits = d->max_tokens > 0 ? (d->max_tokens + split - 1) / split : 1;
+  if ((int64_t)num_reqs * cache->num_kv_heads * a.splits > INT32_MAX ||
+      (int64_t)num_reqs * d->num_q_heads > INT32_MAX) {
+    return VTOKEN_ERR_SHAPE;
+  }
+  a.scale = d->scale;
+  a.q = d->q;
+  a.out = d->out;
+  a.workspace = d->workspace;
+  a.slot_indptr = slot_indptr;
+  a.slots = slots;
+  return vtoken::launch_paged_decode(a, stream) == hipSuccess ? VTOKEN_OK : VTOKEN_ERR_HIP;
+}
+
 const char* vtoken_status_string(int32_t status) {
   switch (status) {
     case VTOKEN_OK: return "VTOKEN_OK";

@@ -94,6 +94,44 @@ struct InplaceArgs {
 // Largest chunk (S * row_bytes) the in-place copy stages through LDS.
 constexpr int64_t kMaxInplaceChunkBytes = 64 * 1024;
 
+// Slot mapping (live tokens' slots per request, logical order).
+struct SlotMapArgs {
+  int32_t num_reqs;
+  int32_t num_tokens;
+  const int32_t* tok_indptr;
+  const int32_t* token_slot;
+  const int32_t* live_count;
+  const int32_t* counters;
+  int32_t* slot_indptr;
+  int32_t* slots;
+  int64_t slots_capacity;
+};
+
+// Paged decode attention of one layer through a slot mapping.
+struct AttnArgs {
+  const uint8_t* kv;
+  int64_t plane_bytes;
+  int64_t row_bytes;
+  int32_t num_kv_heads;
+  int32_t num_q_heads;
+  int32_t head_dim;
+  int32_t layer;
+  int32_t kv_kind;   // 0 fp16, 1 bf16, 2 fp8 e4m3
+  int32_t num_slots;
+  int32_t num_reqs;
+  int32_t splits;    // split records per (request, query head) in the workspace
+  float scale;
+  const float* q;
+  float* out;
+  float* workspace;
+  const int32_t* slot_indptr;
+  const int32_t* slots;
+};
+
+hipError_t launch_slot_mapping(const SlotMapArgs& a, hipStream_t stream);
+hipError_t launch_paged_decode(const AttnArgs& a, hipStream_t stream);
+int attention_split_tokens();
+
 hipError_t launch_build(const MetaArgs& a, hipStream_t stream);
 // variant: 0 default, 1 LDS double buffer, 2 LDS single buffer, 3 registers
 hipError_t launch_repack_inplace(const InplaceArgs& a, int variant, hipStream_t stream);

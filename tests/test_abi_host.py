@@ -53,7 +53,7 @@ def test_struct_layouts_match_header(tmp_path):
     if shutil.which("gcc") is None:
         pytest.skip("gcc not available")
     structs = {"vtoken_cache": B.CCache, "vtoken_batch": B.CBatch, "vtoken_plan": B.CPlan,
-               "vtoken_repack_options": B.CRepackOptions}
+               "vtoken_repack_options": B.CRepackOptions, "vtoken_decode": B.CDecode}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "vtoken.h"', "int main(void){"]
     for cname, cls in structs.items():
         lines.append(f'printf("{cname} sizeof %zu\\n", sizeof({cname}));')
@@ -135,6 +135,78 @@ def test_repack_and_free_reject_bad_arguments():
     batch.free_len = 0
     assert lib.vtoken_repack(ctypes.byref(cache), ctypes.byref(batch), ctypes.byref(plan),
                              None) == 0
+
+
+def test_decode_workspace_bytes():
+    lib = B.load_library()
+    # R * Hq * ceil(max_tokens / 256) * (D + 2) float32 partial records; at least one split
+    assert lib.vtoken_decode_workspace_bytes(3, 32, 128, 1000) == 3 * 32 * 4 * 130 * 4
+    assert lib.vtoken_decode_workspace_bytes(3, 32, 128, 1024) == 3 * 32 * 4 * 130 * 4
+    assert lib.vtoken_decode_workspace_bytes(3, 32, 128, 1025) == 3 * 32 * 5 * 130 * 4
+    assert lib.vtoken_decode_workspace_bytes(2, 8, 64, 0) == 2 * 8 * 1 * 66 * 4
+    assert lib.vtoken_decode_workspace_bytes(2, 0, 64, 10) == -1
+    assert lib.vtoken_decode_workspace_bytes(-1, 8, 64, 10) == -1
+
+
+def _good_decode(cache, nreq=2, hq=32, max_tokens=700):
+    ws = lib_ws = B.load_library().vtoken_decode_workspace_bytes(nreq, hq, cache.head_dim,
+                                                                 max_tokens)
+    p = _fake_ptr()
+    return B.CDecode(p, p, hq, 1, B.KV_BF16, 0.088, max_tokens, p, ws), lib_ws
+
+
+@pytest.mark.parametrize("mutate,code", [
+    (lambda c, d: setattr(d, "num_q_heads", 24), "VTOKEN_ERR_SHAPE"),      # G = 3
+    (lambda c, d: setattr(d, "num_q_heads", 12), "VTOKEN_ERR_SHAPE"),      # not a multiple
+    (lambda c, d: setattr(d, "num_q_heads", 128), "VTOKEN_ERR_SHAPE"),     # G = 16
+    (lambda c, d: setattr(d, "layer", 2), "VTOKEN_ERR_SHAPE"),
+    (lambda c, d: setattr(d, "layer", -1), "VTOKEN_ERR_SHAPE"),
+    (lambda c, d: setattr(d, "kv_dtype", B.KV_FP8_E4M3), "VTOKEN_ERR_SHAPE"),  # 2-byte cache
+    (lambda c, d: setattr(d, "kv_dtype", 3), "VTOKEN_ERR_SHAPE"),
+    (lambda c, d: setattr(c, "head_dim", 256) or setattr(c, "num_kv_heads", 4),
+     "VTOKEN_ERR_SHAPE"),                                                  # 512-byte heads
+    (lambda c, d: setattr(c, "head_dim", 8) or setattr(c, "num_kv_heads", 64),
+     "VTOKEN_ERR_SHAPE"),                                                  # 16-byte heads
+    (lambda c, d: setattr(d, "workspace_bytes", d.workspace_bytes - 4), "VTOKEN_ERR_CAPACITY"),
+    (lambda c, d: setattr(d, "max_tokens", 5000), "VTOKEN_ERR_CAPACITY"),
+    (lambda c, d: setattr(d, "q", None), "VTOKEN_ERR_NULL"),
+    (lambda c, d: setattr(d, "workspace", None), "VTOKEN_ERR_NULL"),
+])
+def test_paged_decode_rejects_bad_arguments(mutate, code):
+    lib = B.load_library()
+    cache, _, _ = _good()
+    d, _ = _good_decode(cache)
+    mutate(cache, d)
+    p = _fake_ptr()
+    st = lib.vtoken_paged_decode(ctypes.byref(cache), ctypes.byref(d), 2, p, p, None)
+    assert st == B.STATUS_CODE[code], (st, code)
+
+
+def test_paged_decode_fp8_kind_requires_one_byte_cache():
+    lib = B.load_library()
+    cache, _, _ = _good()
+    cache.elem_bytes = 1
+    d, _ = _good_decode(cache)      # bf16 kind on a 1-byte cache
+    p = _fake_ptr()
+    assert lib.vtoken_paged_decode(ctypes.byref(cache), ctypes.byref(d), 2, p, p, None) == \
+        B.STATUS_CODE["VTOKEN_ERR_SHAPE"]
+    # no requests: nothing to do, no launch
+    assert lib.vtoken_paged_decode(ctypes.byref(cache), ctypes.byref(d), 0, p, None, None) == 0
+
+
+def test_slot_mapping_rejects_bad_arguments():
+    lib = B.load_library()
+    _, batch, plan = _good()
+    p = _fake_ptr()
+    assert lib.vtoken_build_slot_mapping(ctypes.byref(batch), ctypes.byref(plan), p, p, 39,
+                                         None) == B.STATUS_CODE["VTOKEN_ERR_CAPACITY"]
+    assert lib.vtoken_build_slot_mapping(ctypes.byref(batch), ctypes.byref(plan), None, p, 40,
+                                         None) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    assert lib.vtoken_build_slot_mapping(ctypes.byref(batch), ctypes.byref(plan), p, None, 40,
+                                         None) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    plan.token_slot = None
+    assert lib.vtoken_build_slot_mapping(ctypes.byref(batch), ctypes.byref(plan), p, p, 40,
+                                         None) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
 
 
 def test_binding_fails_loudly_without_library(tmp_path):

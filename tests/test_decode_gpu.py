@@ -1,0 +1,352 @@
+"""Consumer side of the repack through the C ABI: the attention slot mapping (Sec. 3.4), the
+HIP paged decode that reads the cache through it, the relocation-stream / event ordering of
+Sec. 3.3.4 and invariant I3 (Sec. 3.5), and graph replay with a mutable slot buffer (Sec. 3.4,
+CUDA Graph compatibility).
+
+Parity bars:
+  slot mapping   bit-exact against oracle.attention.slot_mapping of the oracle's token table
+  decode         against oracle.attention.decode_batch (float64) over the oracle's post-pass
+                 cache, |diff| <= 1e-4 + 1e-4 |ref|. The kernel computes in float32 from
+                 inputs that are exact in float32 (fp16 / bf16 / e4m3 values): dot products
+                 of at most 256 terms of magnitude < 40 err by < 1e-5 before the softmax
+                 scale, exp and the normalising sum add a few float32 ulps per weight, so
+                 outputs (values of magnitude < 5) err by well under 1e-4.
+  decode of one key returns that key's value row exactly, so every fp16, bf16 and e4m3 code
+                 is checked bit for bit against torch's CPU conversion
+  before/after   decode through the old slots over the old cache and through the new slots
+                 over the repacked cache are bit-identical (the same values in the same
+                 order), also after the released blocks are overwritten (I1, Sec. 3.5)
+"""
+import numpy as np
+import pytest
+
+from gpu_helpers import kv_bytes, torch
+from oracle.attention import decode_batch, slot_mapping
+from oracle.repack import oracle_repack_inputs
+from paper_2608_13263_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+ATOL, RTOL = 1e-4, 1e-4
+
+
+def _B():
+    from paper_2608_13263_amd import binding as B
+    return B
+
+
+def _values(kv_u8: np.ndarray, shape: W.KVShape) -> np.ndarray:
+    """uint8 [P][slots][row_bytes] -> float64 [P][slots][H][D] via torch's CPU conversion."""
+    t = torch()
+    x = t.from_numpy(np.ascontiguousarray(kv_u8)).view(W.torch_dtype(shape)).float()
+    return x.reshape(kv_u8.shape[0], kv_u8.shape[1], shape.num_kv_heads,
+                     shape.head_dim).double().numpy()
+
+
+def _old_slot_mapping(inp: W.RepackInputs):
+    """Slots of the live tokens in the layout before the pass: slot = block * S + offset of
+    the logical position in the request's table (Sec. 3.4), live tokens in order."""
+    S = inp.shape.block_size
+    indptr, slots = [0], []
+    for r in range(inp.num_reqs):
+        a = int(inp.tok_indptr[r])
+        bt = inp.block_ids[inp.bt_indptr[r]:inp.bt_indptr[r + 1]].astype(np.int64)
+        pos = np.nonzero(inp.live[a:a + int(inp.seq_lens[r])])[0]
+        slots.extend((bt[pos // S] * S + pos % S).tolist())
+        indptr.append(len(slots))
+    return np.asarray(indptr, np.int64), np.asarray(slots, np.int64)
+
+
+def _dev_i32(x):
+    t = torch()
+    return t.from_numpy(np.ascontiguousarray(x, dtype=np.int32)).cuda()
+
+
+def _device_pass(inp, kv, inplace=False, stream=None):
+    """One repack pass and the slot-mapping refresh, enqueued on `stream`."""
+    B = _B()
+    sh = inp.shape
+    cache = B.KVCache(kv, sh.num_layers, sh.num_kv_heads, sh.head_dim, sh.block_size)
+    batch = B.Batch.from_inputs(inp)
+    plan = B.Plan.allocate(batch, sh.block_size, inplace=inplace)
+    B.run_pass(cache, batch, plan, stream=stream, inplace=inplace)
+    indptr, slots = B.build_slot_mapping(batch, plan, stream=stream)
+    return cache, batch, plan, indptr, slots
+
+
+def _label(msg):
+    print(f"[gpu] {msg}", flush=True)
+
+
+# ------------------------------------------------------------------------------------------
+# slot mapping
+# ------------------------------------------------------------------------------------------
+def _edge_inputs():
+    sh = W.KVShape(1, 2, 64, 16, "fp16")
+    rng = np.random.default_rng(7)
+    masks = [[], [0] * 40, [1] * 17, [1, 0] * 600, [0] * 15 + [1],
+             (rng.random(3000) < 0.4).astype(int).tolist(), [1]]
+    return W.from_masks(masks, sh, free_blocks=400, seed=7, name="edge")
+
+
+def _many_requests():
+    sh = W.KVShape(1, 1, 64, 4, "fp16")
+    rng = np.random.default_rng(8)
+    masks = [(rng.random(int(n)) < 0.5).astype(int).tolist()
+             for n in rng.integers(0, 40, size=1300)]
+    return W.from_masks(masks, sh, free_blocks=4000, seed=8, name="many_requests")
+
+
+SLOT_CASES = {
+    "tiny": lambda: W.tiny_cache(101),
+    "edge": _edge_inputs,
+    "many_requests": _many_requests,
+    "llama3_8b_random": lambda: W.llama3_8b_random(221, num_layers=1, num_reqs=16),
+    "llama3_70b_fp8": lambda: W.llama3_70b_h2o(521, num_layers=1, num_reqs=4,
+                                               len_range=(2000, 9000)),
+}
+
+
+@pytest.mark.parametrize("inplace", [False, True], ids=["out_of_place", "in_place"])
+@pytest.mark.parametrize("case", sorted(SLOT_CASES))
+def test_slot_mapping_parity(case, inplace):
+    t = torch()
+    inp = SLOT_CASES[case]()
+    _label(f"slot mapping {case} inplace={inplace}: R={inp.num_reqs} T={inp.num_tokens}")
+    kv = W.kv_device(inp.shape, inp.num_blocks, 3)
+    orc = oracle_repack_inputs(inp, None, inplace=inplace)
+    _, _, plan, indptr, slots = _device_pass(inp, kv, inplace=inplace)
+    t.cuda.synchronize()
+    assert int(plan.counters[3]) == 0
+    ref_indptr, ref_slots = slot_mapping(orc.token_slot, inp.tok_indptr, inp.seq_lens)
+    got_indptr = indptr.cpu().numpy().astype(np.int64)
+    assert np.array_equal(got_indptr, ref_indptr)
+    got = slots.cpu().numpy()[:int(ref_indptr[-1])].astype(np.int64)
+    assert np.array_equal(got, ref_slots)
+
+
+# ------------------------------------------------------------------------------------------
+# paged decode parity
+# ------------------------------------------------------------------------------------------
+def _decode_inputs(dtype, H, D, S, seed):
+    """Two layers; live counts 0, 1, 255, 256, 257, 514 and Bernoulli(0.5) requests up to
+    3000 tokens (several 256-token splits with ragged tails)."""
+    sh = W.KVShape(2, H, D, S, dtype)
+    rng = np.random.default_rng(seed)
+    masks = [[0] * 50, [0] * 9 + [1], [1] * 255, [1] * 256 + [0] * 7, [1] * 257,
+             [1, 1, 0] * 257]
+    masks += [(rng.random(int(n)) < 0.5).astype(int).tolist()
+              for n in rng.integers(1, 3000, size=6)]
+    M = sum(-(-len(m) // S) for m in masks)
+    return W.from_masks(masks, sh, free_blocks=M + 64, seed=seed, name=f"decode_{dtype}")
+
+
+DECODE_CASES = [
+    # dtype, H, D, G, S        (lanes per head row = D * elem_bytes / 16)
+    ("bf16", 8, 128, 4, 16),   # Llama-3-8B KV geometry, 16 lanes
+    ("fp16", 2, 64, 1, 16),    # 8 lanes, no GQA
+    ("bf16", 4, 32, 2, 16),    # 4 lanes
+    ("fp16", 4, 128, 8, 16),   # 16 lanes, G = 8
+    ("fp8_e4m3", 8, 128, 8, 32),  # Llama-3-70B fp8 geometry, 8 lanes
+    ("fp8_e4m3", 2, 64, 2, 16),   # 4 lanes
+    ("fp8_e4m3", 2, 256, 4, 16),  # 16 lanes, two value passes
+]
+
+
+@pytest.mark.parametrize("dtype,H,D,G,S", DECODE_CASES,
+                         ids=[f"{c[0]}_H{c[1]}_D{c[2]}_G{c[3]}" for c in DECODE_CASES])
+def test_paged_decode_parity(dtype, H, D, G, S):
+    t = torch()
+    B = _B()
+    inp = _decode_inputs(dtype, H, D, S, seed=31 + D + G)
+    sh = inp.shape
+    _label(f"paged decode {dtype} H={H} D={D} G={G} S={S}: R={inp.num_reqs}")
+    kv = W.kv_device(sh, inp.num_blocks, 5)
+    orc = oracle_repack_inputs(inp, kv_bytes(kv, sh))
+    cache, _, _, indptr, slots = _device_pass(inp, kv)
+    ref_indptr, ref_slots = slot_mapping(orc.token_slot, inp.tok_indptr, inp.seq_lens)
+    vals = _values(orc.kv, sh)
+    rng = np.random.default_rng(D * G)
+    max_tokens = int(np.diff(ref_indptr).max())
+    worst = 0.0
+    for layer in (0, 1):
+        q = rng.standard_normal((inp.num_reqs, H * G, D)).astype(np.float32)
+        out = B.paged_decode(cache, t.from_numpy(q).cuda(), indptr, slots, layer, max_tokens)
+        got = out.cpu().numpy().astype(np.float64)
+        ref = decode_batch(q, vals[2 * layer], vals[2 * layer + 1], ref_indptr, ref_slots)
+        np.testing.assert_allclose(got, ref, atol=ATOL, rtol=RTOL)
+        assert np.array_equal(got[0], np.zeros_like(got[0])), "no live tokens -> zeros"
+        worst = max(worst, float(np.abs(got - ref).max()))
+    _label(f"paged decode {dtype} H={H} D={D} G={G}: max |diff| {worst:.2e}")
+
+
+@pytest.mark.parametrize("dtype", ["fp8_e4m3", "fp16", "bf16"])
+def test_decode_one_key_returns_value_codes_exactly(dtype):
+    """Requests of one live token with a zero key: softmax weight exactly 1, so the output is
+    the value row converted to float32; the value rows hold every code of the type."""
+    t = torch()
+    B = _B()
+    e = 1 if dtype == "fp8_e4m3" else 2
+    H, D = (1, 64) if e == 1 else (8, 128)
+    per_row = H * D
+    codes = np.arange(256 if e == 1 else 65536, dtype=np.uint8 if e == 1 else np.uint16)
+    R = len(codes) // per_row
+    sh = W.KVShape(1, H, D, 16, dtype)
+    num_blocks = R
+    raw = np.zeros((2, num_blocks * 16, per_row), dtype=codes.dtype)
+    for r in range(R):
+        raw[1, r * 16, :] = codes[r * per_row:(r + 1) * per_row]   # V row of slot r*16
+    kv = t.from_numpy(raw.view(np.uint8)).cuda().view(W.torch_dtype(sh)).reshape(
+        2, num_blocks, 16, H, D).contiguous()
+    cache = B.KVCache(kv, 1, H, D, 16)
+    indptr = _dev_i32(np.arange(R + 1))
+    slots = _dev_i32(np.arange(R) * 16)
+    q = t.randn(R, H, D, device="cuda")
+    _label(f"one-key decode {dtype}: {len(codes)} codes in {R} requests")
+    got = B.paged_decode(cache, q, indptr, slots, 0, 1).cpu().numpy().reshape(R, per_row)
+    expect = t.from_numpy(codes.view(np.uint8 if e == 1 else np.int16).copy()).view(
+        W.torch_dtype(sh)).float().numpy().reshape(R, per_row)
+    # -0.0 comes out as +0.0 (0 + -0 = +0 in the accumulation); == treats them as equal
+    same = (got == expect) | (np.isnan(got) & np.isnan(expect))
+    bad = np.nonzero(~same.reshape(-1))[0]
+    assert len(bad) == 0, (f"{len(bad)} codes differ, first {codes[bad[:5]]}: "
+                           f"got {got.reshape(-1)[bad[:5]]} expect {expect.reshape(-1)[bad[:5]]}")
+
+
+# ------------------------------------------------------------------------------------------
+# before / after the repack, stream-event ordering, graph replay
+# ------------------------------------------------------------------------------------------
+def _layout_inputs(seed=41):
+    return W.llama3_8b_random(seed, num_layers=4, num_reqs=12, len_range=(600, 3000))
+
+
+def _scribble_freed(kv, plan, sh):
+    """Overwrite every released block in every plane (what a reuse of the block does)."""
+    t = torch()
+    n = int(plan.counters[2])
+    freed = plan.freed[:n].long()
+    if n:
+        kv.view(sh.num_planes, -1, sh.block_size * sh.num_kv_heads * sh.head_dim)[:, freed] = \
+            float("nan")
+    return n
+
+
+@pytest.mark.parametrize("inplace", [False, True], ids=["out_of_place", "in_place"])
+def test_decode_bit_identical_across_repack_on_relocation_stream(inplace):
+    """The schedule of Sec. 3.3.4: decode on the main stream through the old slots; the
+    repack pass and the slot-mapping refresh on a relocation stream (waiting for the main
+    stream's decode first, which the in-place mode needs since it overwrites what that decode
+    reads); an event recorded on the relocation stream and waited for by the main stream
+    before the next decode (I3). Both decodes agree bit for bit, also after the released
+    blocks are overwritten."""
+    t = torch()
+    B = _B()
+    inp = _layout_inputs()
+    sh = inp.shape
+    _label(f"relocation stream inplace={inplace}: R={inp.num_reqs} T={inp.num_tokens}")
+    kv = W.kv_device(sh, inp.num_blocks, 9)
+    cache = B.KVCache(kv, sh.num_layers, sh.num_kv_heads, sh.head_dim, sh.block_size)
+    old_indptr, old_slots = _old_slot_mapping(inp)
+    max_tokens = int(np.diff(old_indptr).max())
+    q = t.randn(inp.num_reqs, 4 * sh.num_kv_heads, sh.head_dim, device="cuda")
+    main = t.cuda.current_stream()
+    before = [B.paged_decode(cache, q, _dev_i32(old_indptr), _dev_i32(old_slots), layer,
+                             max_tokens) for layer in range(sh.num_layers)]
+    reloc = t.cuda.Stream()
+    reloc.wait_stream(main)
+    with t.cuda.stream(reloc):
+        batch = B.Batch.from_inputs(inp)
+        plan = B.Plan.allocate(batch, sh.block_size, inplace=inplace)
+        B.run_pass(cache, batch, plan, inplace=inplace)
+        indptr, slots = B.build_slot_mapping(batch, plan)
+        done = t.cuda.Event()
+        done.record(reloc)
+    main.wait_event(done)
+    after = [B.paged_decode(cache, q, indptr, slots, layer, max_tokens)
+             for layer in range(sh.num_layers)]
+    for a, b in zip(before, after):
+        assert t.equal(a, b), "decode changed across the repack"
+    assert int(plan.counters[1]) > 0, "the pass repacked nothing"
+    n = _scribble_freed(kv, plan, sh)
+    again = [B.paged_decode(cache, q, indptr, slots, layer, max_tokens)
+             for layer in range(sh.num_layers)]
+    for a, b in zip(before, again):
+        assert t.equal(a, b), "decode read a released block"
+    t.cuda.synchronize()
+    _label(f"relocation stream inplace={inplace}: {int(plan.counters[1])} requests repacked, "
+           f"{n} blocks released and overwritten")
+
+
+def test_graph_replay_with_mutable_slot_buffer():
+    """Decode captured once in a HIP graph over fixed slot / query / output buffers. The
+    repack and the refresh of the slot buffer run outside the graph on a relocation stream;
+    the main stream waits for its event before the replay. Every replay equals the eager
+    decode of the same state, with unrelated eager work between replays."""
+    t = torch()
+    B = _B()
+    inp = _layout_inputs(43)
+    sh = inp.shape
+    layer = 2
+    _label(f"graph replay: R={inp.num_reqs} T={inp.num_tokens}")
+    kv = W.kv_device(sh, inp.num_blocks, 11)
+    cache = B.KVCache(kv, sh.num_layers, sh.num_kv_heads, sh.head_dim, sh.block_size)
+    old_indptr, old_slots = _old_slot_mapping(inp)
+    max_tokens = int(np.diff(old_indptr).max())
+    R, Hq, D = inp.num_reqs, 2 * sh.num_kv_heads, sh.head_dim
+    slot_indptr = _dev_i32(old_indptr)
+    slots = t.zeros(max(inp.num_tokens, 1), dtype=t.int32, device="cuda")
+    slots[:len(old_slots)] = _dev_i32(old_slots)
+    q = t.randn(R, Hq, D, device="cuda")
+    out = t.empty_like(q)
+    ws = t.empty(B.decode_workspace_bytes(R, Hq, D, max_tokens) // 4, dtype=t.float32,
+                 device="cuda")
+
+    def decode(o):
+        return B.paged_decode(cache, q, slot_indptr, slots, layer, max_tokens, out=o,
+                              workspace=ws)
+
+    side = t.cuda.Stream()
+    side.wait_stream(t.cuda.current_stream())
+    with t.cuda.stream(side):
+        decode(out)
+    t.cuda.current_stream().wait_stream(side)
+    graph = t.cuda.CUDAGraph()
+    with t.cuda.graph(graph):
+        decode(out)
+
+    def replay_and_check(tag):
+        eager = decode(t.empty_like(q))
+        t.cuda.synchronize()
+        noise = t.randn(512, 512, device="cuda")
+        noise = noise @ noise
+        graph.replay()
+        t.cuda.synchronize()
+        assert t.equal(out, eager), f"replay differs from eager decode ({tag})"
+        return out.clone()
+
+    first = replay_and_check("old layout")
+    first_again = replay_and_check("old layout, second replay")
+    assert t.equal(first, first_again)
+
+    main = t.cuda.current_stream()
+    reloc = t.cuda.Stream()
+    reloc.wait_stream(main)     # the slot buffer is read by the replay before
+    with t.cuda.stream(reloc):
+        batch = B.Batch.from_inputs(inp)
+        plan = B.Plan.allocate(batch, sh.block_size)
+        B.run_pass(cache, batch, plan)
+        B.build_slot_mapping(batch, plan, slot_indptr=slot_indptr, slots=slots)
+        done = t.cuda.Event()
+        done.record(reloc)
+    main.wait_event(done)
+    graph.replay()
+    t.cuda.synchronize()
+    assert t.equal(out, first), "replay after the repack differs"
+    assert int(plan.counters[1]) > 0
+    assert not np.array_equal(slots.cpu().numpy()[:len(old_slots)], old_slots)
+    _scribble_freed(kv, plan, sh)
+    replayed = replay_and_check("released blocks overwritten")
+    assert t.equal(replayed, first)
+    # a new query in the captured input buffer
+    q.copy_(t.randn(R, Hq, D, device="cuda"))
+    replay_and_check("new query")
