@@ -58,7 +58,10 @@ def parse_args(argv=None):
     ap.add_argument("--inplace", action="store_true",
                     help="in-place mode: destinations are each request's own leading blocks; "
                          "bytes count only the rows that move")
-    ap.add_argument("--mode", default="repack", choices=["repack", "copy"])
+    ap.add_argument("--mode", default="repack", choices=["repack", "copy", "decode"],
+                    help="decode: the consumer side, paged decode attention of every layer "
+                         "through the slot mapping, before and after the repack")
+    ap.add_argument("--q-heads", type=int, default=32, help="decode mode: query heads")
     ap.add_argument("--copy-gib", type=float, default=8.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-planes", type=int, default=4,
@@ -318,6 +321,84 @@ def run_inplace(args, inp, kv, cache, batch, plan, stream):
     return 0
 
 
+def run_decode(args, inp, kv, cache, batch, plan, stream):
+    """Consumer side: decode attention of every layer for every request, reading the live
+    K/V rows through the slot mapping. Timed on the layout before the repack (slots in the
+    requests' original blocks) and after it (the repacked blocks), same bytes either way:
+    each live token's head row of K and V, per layer."""
+    import numpy as np
+    import torch
+    from paper_2608_13263_amd import binding as B
+    sh = inp.shape
+    S = sh.block_size
+    R, Hq, D = inp.num_reqs, args.q_heads, sh.head_dim
+    old_indptr, old_slots = [0], []
+    for r in range(R):
+        a = int(inp.tok_indptr[r])
+        bt = inp.block_ids[inp.bt_indptr[r]:inp.bt_indptr[r + 1]].astype(np.int64)
+        pos = np.nonzero(inp.live[a:a + int(inp.seq_lens[r])])[0]
+        old_slots.extend((bt[pos // S] * S + pos % S).tolist())
+        old_indptr.append(len(old_slots))
+    dev = lambda x: torch.from_numpy(np.asarray(x, dtype=np.int32)).cuda()  # noqa: E731
+    layouts = {"before_repack": (dev(old_indptr), dev(old_slots))}
+    B.run_pass(cache, batch, plan, stream=stream)
+    layouts["after_repack"] = B.build_slot_mapping(batch, plan, stream=stream)
+    torch.cuda.synchronize()
+    live = np.diff(np.asarray(old_indptr))
+    max_tokens = int(live.max())
+    q = torch.randn(R, Hq, D, device="cuda")
+    out = torch.empty_like(q)
+    ws = torch.empty(B.decode_workspace_bytes(R, Hq, D, max_tokens) // 4, dtype=torch.float32,
+                     device="cuda")
+    bytes_layer = int(live.sum()) * 2 * sh.num_kv_heads * D * sh.elem_bytes
+    bytes_step = bytes_layer * sh.num_layers
+    res = {}
+    for name, (indptr, slots) in layouts.items():
+        def step(ev=None):
+            for layer in range(sh.num_layers):
+                if ev is not None:
+                    ev[layer][0].record(stream)
+                B.paged_decode(cache, q, indptr, slots, layer, max_tokens, out=out,
+                               workspace=ws, stream=stream)
+                if ev is not None:
+                    ev[layer][1].record(stream)
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                for _ in range(sh.num_layers)] for _ in range(args.steps)]
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            step(evs[i])
+        torch.cuda.synchronize()
+        step_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        call_ms = sum(a.elapsed_time(b) for e in evs for a, b in e) / (args.steps * sh.num_layers)
+        res[name] = dict(step_ms=step_ms, call_ms=call_ms,
+                         gbs=bytes_step / (step_ms / 1e3) / 1e9,
+                         call_gbs=bytes_layer / (call_ms / 1e3) / 1e9)
+        log(f"decode {name}: step {step_ms:.3f} ms ({res[name]['gbs']:.0f} GB/s), per layer "
+            f"{call_ms * 1e3:.1f} us ({res[name]['call_gbs']:.0f} GB/s)")
+    after = res["after_repack"]
+    out_json = {
+        "metric": "paged decode K/V GB/s through the slot mapping (all layers, all requests)",
+        "mode": "decode", "value": round(after["gbs"], 2), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(after["step_ms"], 4),
+        "higher_is_better": True, "dtype": "f32",
+        "config": {"workload": inp.name, "recipe": inp.note, "q_heads": Hq,
+                   "live_tokens": int(live.sum()), "max_live_tokens": max_tokens,
+                   "bytes_alg_per_layer": bytes_layer,
+                   "admitted": int(plan.counters[1])},
+        "before_repack": {k: round(v, 4) for k, v in res["before_repack"].items()},
+        "after_repack": {k: round(v, 4) for k, v in after.items()},
+        "roofline": {"bound": "hbm", "kernel": "vtoken_paged_decode (split + combine)",
+                     "achieved": round(after["call_gbs"], 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(after["call_gbs"] / HBM_PEAK_GBS, 4),
+                     "traffic": None},
+    }
+    print(json.dumps(out_json), flush=True)
+    return 0
+
+
 def main(argv=None):
     args = parse_args(argv)
     if args.gpus != 1:
@@ -348,6 +429,8 @@ def main(argv=None):
     stream = torch.cuda.current_stream()
     if args.inplace:
         return run_inplace(args, inp, kv, cache, batch, plan, stream)
+    if args.mode == "decode":
+        return run_decode(args, inp, kv, cache, batch, plan, stream)
     torch.cuda.synchronize()
     log(f"setup {time.perf_counter() - t_setup:.1f} s; warmup {args.warmup} steps")
 

@@ -228,8 +228,8 @@ vtoken_status vtoken_build_slot_mapping(const vtoken_batch* batch, const vtoken_
  * and query head qh (GQA: KV head qh / (num_q_heads / num_kv_heads)),
  *   out[r][qh] = softmax(scale * q[r][qh] . K[slot]^T) @ V[slot] over the slots of r,
  * K and V being the layer's K and V planes (float32 math; zeros for a request with no slots).
- * Flash-decoding: 256-token splits, then a merge; the workspace holds the split partials and
- * is overwritten by every call (calls sharing it must be stream-ordered). */
+ * Flash-decoding: splits of 16384/head_dim tokens, then a merge; the workspace holds the split
+ * partials and is overwritten by every call (calls sharing it must be stream-ordered). */
 enum { VTOKEN_KV_FP16 = 0, VTOKEN_KV_BF16 = 1, VTOKEN_KV_FP8_E4M3 = 2 };
 
 typedef struct vtoken_decode {
@@ -244,13 +244,17 @@ typedef struct vtoken_decode {
   int64_t      workspace_bytes;
 } vtoken_decode;
 
-/* head_dim*elem_bytes must be 64, 128 or 256 bytes (VTOKEN_ERR_SHAPE otherwise). Returns -1
- * for invalid sizes. */
+/* Bytes of workspace: num_reqs * num_q_heads * ceil(max_tokens / (16384 / head_dim)) (at
+ * least one split) * (head_dim + 2) * 4. head_dim must be 32, 64, 128 or 256 (also for
+ * vtoken_paged_decode: VTOKEN_ERR_SHAPE otherwise). Returns -1 for invalid sizes. */
 int64_t vtoken_decode_workspace_bytes(int32_t num_reqs, int32_t num_q_heads, int32_t head_dim,
                                       int32_t max_tokens);
 vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode* decode,
                                   int32_t num_reqs, const int32_t* slot_indptr,
                                   const int32_t* slots, hipStream_t stream);
+
+/* The hipError_t behind the calling thread's most recent VTOKEN_ERR_HIP (0 if none yet). */
+int32_t vtoken_last_hip_error(void);
 
 /* Static string naming a status code; never NULL. */
 const char* vtoken_status_string(int32_t status);

@@ -106,6 +106,7 @@ _SIGNATURES = {
     "vtoken_paged_decode": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CDecode),
                                              ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                              ctypes.c_void_p]),
+    "vtoken_last_hip_error": (ctypes.c_int32, []),
     "vtoken_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
     "vtoken_version": (ctypes.c_int32, []),
 }
@@ -121,6 +122,10 @@ def load_library(path: str = LIB_PATH):
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it with "
                            "`python -m paper_2608_13263_amd.build` (hipcc, gfx950)")
+    # torch first: the library must bind to the HIP runtime torch has loaded, since the
+    # streams and device pointers it is handed are torch's (loaded the other way round, the
+    # library's calls found no device)
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     for name, (res, args) in _SIGNATURES.items():
         fn = getattr(lib, name)
@@ -140,6 +145,8 @@ def _ptr(t) -> int:
 
 
 def _check(status: int, where: str):
+    if status == STATUS_CODE["VTOKEN_ERR_HIP"]:
+        raise VTokenError(status, f"{where} (hipError_t {load_library().vtoken_last_hip_error()})")
     if status != VTOKEN_OK:
         raise VTokenError(status, where)
 

@@ -9,6 +9,15 @@ namespace {
 
 constexpr int64_t kInt32Limit = 2147483647LL;
 
+// The HIP error behind the calling thread's most recent VTOKEN_ERR_HIP.
+thread_local int32_t g_last_hip_error = 0;
+
+vtoken_status hip_status(hipError_t e) {
+  if (e == hipSuccess) return VTOKEN_OK;
+  g_last_hip_error = static_cast<int32_t>(e);
+  return VTOKEN_ERR_HIP;
+}
+
 vtoken_status check_cache(const vtoken_cache* c) {
   if (c == nullptr || c->kv == nullptr) return VTOKEN_ERR_NULL;
   if (c->num_layers <= 0 || c->num_kv_heads <= 0 || c->head_dim <= 0 || c->block_size <= 0 ||
@@ -107,7 +116,7 @@ vtoken_status vtoken_build_token_table(const vtoken_cache* cache, const vtoken_b
   if ((s = check_plan(plan, batch, cache->block_size, false)) != VTOKEN_OK) return s;
   vtoken::MetaArgs a = meta_args(cache, batch, plan);
   a.inplace = 0;
-  return vtoken::launch_build(a, stream) == hipSuccess ? VTOKEN_OK : VTOKEN_ERR_HIP;
+  return hip_status(vtoken::launch_build(a, stream));
 }
 
 vtoken_status vtoken_build_token_table_inplace(const vtoken_cache* cache,
@@ -121,7 +130,7 @@ vtoken_status vtoken_build_token_table_inplace(const vtoken_cache* cache,
   a.inplace = 1;
   a.free_list = nullptr;
   a.free_len = 0;
-  return vtoken::launch_build(a, stream) == hipSuccess ? VTOKEN_OK : VTOKEN_ERR_HIP;
+  return hip_status(vtoken::launch_build(a, stream));
 }
 
 vtoken_status vtoken_repack_inplace(const vtoken_cache* cache, const vtoken_batch* batch,
@@ -165,8 +174,7 @@ vtoken_status vtoken_repack_inplace_ex(const vtoken_cache* cache, const vtoken_b
   a.new_bt_indptr = plan->new_bt_indptr;
   a.admitted = plan->admitted;
   a.counters = plan->counters;
-  return vtoken::launch_repack_inplace(a, variant, stream) == hipSuccess ? VTOKEN_OK
-                                                                          : VTOKEN_ERR_HIP;
+  return hip_status(vtoken::launch_repack_inplace(a, variant, stream));
 }
 
 vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* batch,
@@ -209,8 +217,7 @@ vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* ba
   a.src_plan = plan->src_plan;
   a.free_list = batch->free_list;
   a.counters = plan->counters;
-  return vtoken::launch_repack(a, variant, grid, order, stream) == hipSuccess ? VTOKEN_OK
-                                                                              : VTOKEN_ERR_HIP;
+  return hip_status(vtoken::launch_repack(a, variant, grid, order, stream));
 }
 
 vtoken_status vtoken_repack(const vtoken_cache* cache, const vtoken_batch* batch,
@@ -236,8 +243,7 @@ vtoken_status vtoken_free_blocks(const vtoken_batch* batch, const vtoken_plan* p
   a.admitted = plan->admitted;
   a.freed_indptr = plan->freed_indptr;
   a.counters = plan->counters;
-  return vtoken::launch_free(a, freed, freed_capacity, stream) == hipSuccess ? VTOKEN_OK
-                                                                            : VTOKEN_ERR_HIP;
+  return hip_status(vtoken::launch_free(a, freed, freed_capacity, stream));
 }
 
 vtoken_status vtoken_build_slot_mapping(const vtoken_batch* batch, const vtoken_plan* plan,
@@ -263,13 +269,14 @@ vtoken_status vtoken_build_slot_mapping(const vtoken_batch* batch, const vtoken_
   a.slot_indptr = slot_indptr;
   a.slots = slots;
   a.slots_capacity = slots_capacity;
-  return vtoken::launch_slot_mapping(a, stream) == hipSuccess ? VTOKEN_OK : VTOKEN_ERR_HIP;
+  return hip_status(vtoken::launch_slot_mapping(a, stream));
 }
 
 int64_t vtoken_decode_workspace_bytes(int32_t num_reqs, int32_t num_q_heads, int32_t head_dim,
                                       int32_t max_tokens) {
-  if (num_reqs < 0 || num_q_heads <= 0 || head_dim <= 0 || max_tokens < 0) return -1;
-  const int64_t split = vtoken::attention_split_tokens();
+  if (num_reqs < 0 || num_q_heads <= 0 || max_tokens < 0) return -1;
+  if (head_dim != 32 && head_dim != 64 && head_dim != 128 && head_dim != 256) return -1;
+  const int64_t split = vtoken::decode_split_tokens(head_dim);
   const int64_t splits = max_tokens > 0 ? (max_tokens + split - 1) / split : 1;
   return (int64_t)num_reqs * num_q_heads * splits * (head_dim + 2) * 4;
 }
@@ -294,10 +301,8 @@ vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode
       (g != 1 && g != 2 && g != 4 && g != 8)) {
     return VTOKEN_ERR_SHAPE;
   }
-  const int lanes = cache->head_dim * cache->elem_bytes / 16;
-  if (cache->head_dim * cache->elem_bytes % 16 != 0 || (lanes != 4 && lanes != 8 && lanes != 16)) {
-    return VTOKEN_ERR_SHAPE;
-  }
+  const int D = cache->head_dim;
+  if (D != 32 && D != 64 && D != 128 && D != 256) return VTOKEN_ERR_SHAPE;
   const int64_t need = vtoken_decode_workspace_bytes(num_reqs, d->num_q_heads, cache->head_dim,
                                                      d->max_tokens);
   if (d->workspace_bytes < need) return VTOKEN_ERR_CAPACITY;
@@ -312,7 +317,8 @@ vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode
   a.kv_kind = kind;
   a.num_slots = cache->num_blocks * cache->block_size;
   a.num_reqs = num_reqs;
-  const int split = vtoken::attention_split_tokens();
+  const int split = vtoken::decode_split_tokens(D);
+  a.split_tokens = split;
   a.splits = d->max_tokens > 0 ? (d->max_tokens + split - 1) / split : 1;
   if ((int64_t)num_reqs * cache->num_kv_heads * a.splits > INT32_MAX ||
       (int64_t)num_reqs * d->num_q_heads > INT32_MAX) {
@@ -324,8 +330,10 @@ vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode
   a.workspace = d->workspace;
   a.slot_indptr = slot_indptr;
   a.slots = slots;
-  return vtoken::launch_paged_decode(a, stream) == hipSuccess ? VTOKEN_OK : VTOKEN_ERR_HIP;
+  return hip_status(vtoken::launch_paged_decode(a, stream));
 }
+
+int32_t vtoken_last_hip_error(void) { return g_last_hip_error; }
 
 const char* vtoken_status_string(int32_t status) {
   switch (status) {

@@ -5,14 +5,14 @@
 //   slot_map_kernel      one workgroup per request: wave-ballot compaction of token_slot,
 //                        the live tokens' slots in logical order (Sec. 3.4: the slot mapping
 //                        is built through the token table, once per token)
-//   decode_split_kernel  one workgroup per (request, KV head, 256-token split): scores of the
-//                        G query heads that share the KV head, split-local softmax, partial
-//                        weighted sum of V (flash-decoding partials)
+//   decode_split_kernel  one workgroup per (request, KV head, split of 2048*8/D tokens):
+//                        scores of the G query heads that share the KV head, split-local
+//                        softmax, partial weighted sum of V (flash-decoding partials)
 //   decode_combine_kernel  one workgroup per (request, query head): merges the splits
 //
-// Decode attention is HBM-bound (about G flops per byte of K/V), so the dot products run on
-// the fp32 vector ALUs; K/V rows are read as 16-byte pieces, a head's D elements by a group
-// of D*e/16 consecutive lanes.
+// Decode attention is HBM-bound (about 2G flops per byte of K/V), so the dot products run on
+// the fp32 vector ALUs; a head's D elements are read by D/8 consecutive lanes, 8 elements
+// (16 bytes of fp16 / bf16, 8 of fp8) each.
 #include <math.h>
 
 #include "vtoken_internal.h"
@@ -21,7 +21,6 @@ namespace vtoken {
 namespace {
 
 constexpr int kAttnThreads = 256;
-constexpr int kAttnSplit = 256;   // tokens per split workgroup
 
 __device__ __forceinline__ int lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
@@ -97,19 +96,20 @@ __global__ __launch_bounds__(1024) void slot_map_kernel(SlotMapArgs a) {
 // Paged decode attention.
 // ------------------------------------------------------------------------------------------
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
-// OCP e4m3 (fp8, no infinities): sign, 4 exponent bits with bias 7, 3 mantissa bits.
-__device__ __forceinline__ float fp8e4m3_to_float(uint32_t b) {
-  const uint32_t sign = (b & 0x80u) << 24;
-  const uint32_t e = (b >> 3) & 0xFu;
-  const uint32_t m = b & 0x7u;
-  if (e == 0xFu && m == 0x7u) return __uint_as_float(0x7FC00000u | sign);
-  if (e == 0) {
-    const float v = static_cast<float>(m) * 0.001953125f;  // m * 2^-9
-    return sign ? -v : v;
-  }
-  return __uint_as_float(sign | ((e + 120u) << 23) | (m << 20));
-}
+constexpr int kPer = 8;  // elements of a head row per lane
+
+// Eight consecutive elements of a K or V head row: 16 bytes of fp16 / bf16, 8 bytes of fp8.
+template <int kKind>
+struct Piece {
+  typedef u32x4 type;
+};
+template <>
+struct Piece<2> {
+  typedef u32x2 type;
+};
 
 __device__ __forceinline__ float half_bits_to_float(uint32_t h) {
   _Float16 x;
@@ -118,37 +118,78 @@ __device__ __forceinline__ float half_bits_to_float(uint32_t h) {
   return static_cast<float>(x);
 }
 
-// A 16-byte piece of a K or V row as float: 8 values (2-byte types) or 16 (fp8); kind
-// 0 fp16, 1 bf16, 2 fp8 e4m3.
+// kind 0 fp16, 1 bf16 (widening by shifts), 2 fp8: the gfx950 conversion instruction, which
+// reads OCP e4m3 (no infinities, 0x7F / 0xFF are NaN).
 template <int kKind>
-__device__ __forceinline__ void piece_to_float(u32x4 w, float* out) {
-  const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+__device__ __forceinline__ void piece_to_float(typename Piece<kKind>::type w, float* out) {
+  if constexpr (kKind == 2) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    if (kKind == 1) {
-      out[2 * i] = __uint_as_float(ws[i] << 16);
-      out[2 * i + 1] = __uint_as_float(ws[i] & 0xFFFF0000u);
-    } else if (kKind == 0) {
-      out[2 * i] = half_bits_to_float(ws[i] & 0xFFFFu);
-      out[2 * i + 1] = half_bits_to_float(ws[i] >> 16);
-    } else {
+    for (int i = 0; i < 2; ++i) {
+      const f32x2 lo = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w[i]), false);
+      const f32x2 hi = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w[i]), true);
+      out[4 * i] = lo.x;
+      out[4 * i + 1] = lo.y;
+      out[4 * i + 2] = hi.x;
+      out[4 * i + 3] = hi.y;
+    }
+  } else {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) out[4 * i + k] = fp8e4m3_to_float((ws[i] >> (8 * k)) & 0xFFu);
+    for (int i = 0; i < 4; ++i) {
+      if constexpr (kKind == 1) {
+        out[2 * i] = __uint_as_float(w[i] << 16);
+        out[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+      } else {
+        out[2 * i] = half_bits_to_float(w[i] & 0xFFFFu);
+        out[2 * i + 1] = half_bits_to_float(w[i] >> 16);
+      }
     }
   }
 }
 
-// kKind: element type; kLanes: lanes per head row (D*e/16, a power of two <= 64);
-// kG: query heads per KV head (GQA group), at most 8.
+// Sum over each aligned group of kLanes (4, 8, 16 or 32) lanes, the result in every lane of
+// the group: DPP lane permutations inside a row of 16 (swap neighbours, swap pairs, mirrored
+// half-row, mirrored row), then one cross-row exchange for 32.
+template <int kLanes>
+__device__ __forceinline__ float group_sum(float x) {
+  auto dpp = [](float v, int ctrl) -> float {
+    const int i = __builtin_bit_cast(int, v);
+    int o;
+    switch (ctrl) {
+      case 0: o = __builtin_amdgcn_update_dpp(0, i, 0xB1, 0xF, 0xF, false); break;   // [1,0,3,2]
+      case 1: o = __builtin_amdgcn_update_dpp(0, i, 0x4E, 0xF, 0xF, false); break;   // [2,3,0,1]
+      case 2: o = __builtin_amdgcn_update_dpp(0, i, 0x141, 0xF, 0xF, false); break;  // half mirror
+      default: o = __builtin_amdgcn_update_dpp(0, i, 0x140, 0xF, 0xF, false); break; // mirror
+    }
+    return __builtin_bit_cast(float, o);
+  };
+  x += dpp(x, 0);
+  x += dpp(x, 1);
+  if constexpr (kLanes >= 8) x += dpp(x, 2);
+  if constexpr (kLanes >= 16) x += dpp(x, 3);
+  if constexpr (kLanes >= 32) x += __shfl_xor(x, 16, 64);
+  return x;
+}
+
+// kKind: element type; kLanes: lanes per head row (head_dim / 8); kG: query heads per KV
+// head (GQA group), at most 8.
+//
+// One workgroup covers kSplit = 8 * 256 / kLanes tokens of one (request, KV head). Every
+// thread first issues all of its loads: the slots of its 8 tokens, then the K piece and the V
+// piece of each (16 loads in flight per thread); then it computes the scores, the
+// split-local softmax and the weighted V sum from registers.
 template <int kKind, int kLanes, int kG>
 __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) {
-  constexpr int kPer = kKind == 2 ? 16 : 8;          // elements per 16-byte piece
+  using PieceT = typename Piece<kKind>::type;
+  constexpr int kElem = kKind == 2 ? 1 : 2;
   constexpr int kD = kLanes * kPer;                  // head_dim
-  constexpr int kTokPerPass = kAttnThreads / kLanes; // tokens processed per pass
-  __shared__ float q_s[kG][kD];
-  __shared__ float p_s[kG][kAttnSplit];
-  __shared__ float red_s[kAttnThreads / 64][kG];
-  __shared__ float acc_s[kAttnThreads / 64][kG][kD];
+  constexpr int kTokPerPass = kAttnThreads / kLanes; // tokens per pass of the workgroup
+  constexpr int kIters = kDecodeTokensPerThread;     // tokens per thread
+  constexpr int kSplit = kIters * kTokPerPass;
+  static_assert(kSplit == decode_split_tokens(kD), "split size");
+  constexpr int kWaves = kAttnThreads / 64;
+  __shared__ float p_s[kG][kSplit];
+  __shared__ float red_s[kWaves][kG];
+  __shared__ float acc_s[kWaves][kG][kD];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -159,40 +200,55 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
   if (r >= a.num_reqs) return;
   const int s0 = a.slot_indptr[r];
   const int c = a.slot_indptr[r + 1] - s0;
-  const int t0 = split * kAttnSplit;
+  const int t0 = split * kSplit;
   if (t0 >= c || s0 < 0) return;
-  const int nt = c - t0 < kAttnSplit ? c - t0 : kAttnSplit;
+  const int nt = c - t0 < kSplit ? c - t0 : kSplit;
   const int* slots = a.slots + s0 + t0;
 
-  // the G query rows of this KV head
-  for (int i = tid; i < kG * kD; i += kAttnThreads) {
-    const int g = i / kD, d = i - g * kD;
-    q_s[g][d] = a.q[((int64_t)r * a.num_q_heads + h * kG + g) * kD + d];
-  }
-  __syncthreads();
-
-  const int piece = tid % kLanes;       // which 16-byte piece of the head row
+  const int piece = tid % kLanes;       // which 8 elements of the head row
   const int tg = tid / kLanes;          // token group
   const uint8_t* kplane = a.kv + (int64_t)(2 * a.layer) * a.plane_bytes;
   const uint8_t* vplane = kplane + a.plane_bytes;
-  const int64_t head_off = (int64_t)h * kD * (kKind == 2 ? 1 : 2) + piece * 16;
+  const int64_t head_off = (int64_t)h * kD * kElem + piece * kPer * kElem;
+
+  // all loads of the split first; tokens past its end re-read its last token (dropped later)
+  int64_t off[kIters];
+  bool ok[kIters];
+#pragma unroll
+  for (int i = 0; i < kIters; ++i) {
+    const int t = tg + i * kTokPerPass;
+    const int s = slots[t < nt ? t : nt - 1];
+    ok[i] = static_cast<unsigned>(s) < static_cast<unsigned>(a.num_slots);
+    off[i] = (int64_t)(ok[i] ? s : 0) * a.row_bytes + head_off;
+  }
+  PieceT kw[kIters], vw[kIters];
+#pragma unroll
+  for (int i = 0; i < kIters; ++i) kw[i] = *reinterpret_cast<const PieceT*>(kplane + off[i]);
+#pragma unroll
+  for (int i = 0; i < kIters; ++i) vw[i] = *reinterpret_cast<const PieceT*>(vplane + off[i]);
+
+  const float* qrow = a.q + ((int64_t)r * a.num_q_heads + h * kG) * kD + piece * kPer;
+  float q_r[kG][kPer];
+#pragma unroll
+  for (int g = 0; g < kG; ++g)
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) q_r[g][e] = qrow[g * kD + e];
 
   // scores
-  for (int t = tg; t < nt; t += kTokPerPass) {
-    const int s = slots[t];
+#pragma unroll
+  for (int i = 0; i < kIters; ++i) {
+    const int t = tg + i * kTokPerPass;
     float kf[kPer];
-    const bool ok = static_cast<unsigned>(s) < static_cast<unsigned>(a.num_slots);
-    u32x4 w = {0u, 0u, 0u, 0u};
-    if (ok) w = *reinterpret_cast<const u32x4*>(kplane + (int64_t)s * a.row_bytes + head_off);
+    PieceT w = kw[i];
+    if (!ok[i]) w = PieceT{};
     piece_to_float<kKind>(w, kf);
 #pragma unroll
     for (int g = 0; g < kG; ++g) {
       float acc = 0.f;
 #pragma unroll
-      for (int i = 0; i < kPer; ++i) acc += q_s[g][piece * kPer + i] * kf[i];
-#pragma unroll
-      for (int d = 1; d < kLanes; d <<= 1) acc += __shfl_xor(acc, d, 64);
-      if (piece == 0) p_s[g][t] = acc * a.scale;
+      for (int e = 0; e < kPer; ++e) acc += q_r[g][e] * kf[e];
+      acc = group_sum<kLanes>(acc);
+      if (piece == 0 && t < nt) p_s[g][t] = acc * a.scale;
     }
   }
   __syncthreads();
@@ -211,7 +267,7 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
 #pragma unroll
   for (int g = 0; g < kG; ++g) {
     float m = red_s[0][g];
-    for (int w = 1; w < kAttnThreads / 64; ++w) m = fmaxf(m, red_s[w][g]);
+    for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red_s[w][g]);
     m_g[g] = m;
   }
   __syncthreads();
@@ -231,54 +287,52 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
 #pragma unroll
   for (int g = 0; g < kG; ++g) {
     float l = 0.f;
-    for (int w = 0; w < kAttnThreads / 64; ++w) l += red_s[w][g];
+    for (int w = 0; w < kWaves; ++w) l += red_s[w][g];
     l_g[g] = l;
   }
 
-  // weighted sum of V over this split, kGB query heads at a time (at most 64 accumulators
-  // per thread; a second pass re-reads the split's V rows from cache)
-  constexpr int kGB = kG * kPer <= 64 ? kG : (64 / kPer);
-  for (int g0 = 0; g0 < kG; g0 += kGB) {
-    float acc[kGB][kPer];
+  // weighted sum of V from the registers (kG * 8 <= 64 accumulators per thread)
+  float acc[kG][kPer];
 #pragma unroll
-    for (int g = 0; g < kGB; ++g)
+  for (int g = 0; g < kG; ++g)
 #pragma unroll
-      for (int i = 0; i < kPer; ++i) acc[g][i] = 0.f;
-    for (int t = tg; t < nt; t += kTokPerPass) {
-      const int s = slots[t];
+    for (int e = 0; e < kPer; ++e) acc[g][e] = 0.f;
+#pragma unroll
+  for (int i = 0; i < kIters; ++i) {
+    const int t = tg + i * kTokPerPass;
+    if (t < nt) {
       float vf[kPer];
-      const bool ok = static_cast<unsigned>(s) < static_cast<unsigned>(a.num_slots);
-      u32x4 w = {0u, 0u, 0u, 0u};
-      if (ok) w = *reinterpret_cast<const u32x4*>(vplane + (int64_t)s * a.row_bytes + head_off);
+      PieceT w = vw[i];
+      if (!ok[i]) w = PieceT{};
       piece_to_float<kKind>(w, vf);
 #pragma unroll
-      for (int g = 0; g < kGB; ++g) {
-        const float p = p_s[g0 + g][t];
+      for (int g = 0; g < kG; ++g) {
+        const float p = p_s[g][t];
 #pragma unroll
-        for (int i = 0; i < kPer; ++i) acc[g][i] += p * vf[i];
+        for (int e = 0; e < kPer; ++e) acc[g][e] += p * vf[e];
       }
     }
-    // reduce over the token groups: inside the wave (lanes with the same piece), then across
-    // waves through LDS
+  }
+  // reduce over the token groups: inside the wave (lanes with the same piece), then across
+  // waves through LDS
 #pragma unroll
-    for (int g = 0; g < kGB; ++g)
+  for (int g = 0; g < kG; ++g)
 #pragma unroll
-      for (int i = 0; i < kPer; ++i)
+    for (int e = 0; e < kPer; ++e)
 #pragma unroll
-        for (int d = kLanes; d < 64; d <<= 1) acc[g][i] += __shfl_xor(acc[g][i], d, 64);
-    if (lane < kLanes) {
+      for (int d = kLanes; d < 64; d <<= 1) acc[g][e] += __shfl_xor(acc[g][e], d, 64);
+  if (lane < kLanes) {
 #pragma unroll
-      for (int g = 0; g < kGB; ++g)
+    for (int g = 0; g < kG; ++g)
 #pragma unroll
-        for (int i = 0; i < kPer; ++i) acc_s[wave][g0 + g][piece * kPer + i] = acc[g][i];
-    }
+      for (int e = 0; e < kPer; ++e) acc_s[wave][g][piece * kPer + e] = acc[g][e];
   }
   __syncthreads();
   // partial record per (request, query head, split): [m, l, acc[D]]
   for (int i = tid; i < kG * kD; i += kAttnThreads) {
     const int g = i / kD, d = i - g * kD;
     float v = 0.f;
-    for (int w = 0; w < kAttnThreads / 64; ++w) v += acc_s[w][g][d];
+    for (int w = 0; w < kWaves; ++w) v += acc_s[w][g][d];
     float* rec = a.workspace +
                  (((int64_t)r * a.num_q_heads + h * kG + g) * a.splits + split) * (kD + 2);
     rec[2 + d] = v;
@@ -289,31 +343,79 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
   }
 }
 
-__global__ __launch_bounds__(64) void decode_combine_kernel(AttnArgs a) {
+// Merge of the split partials of one (request, query head): M = max of the split maxima,
+// weights w_s = exp(m_s - M), out = sum_s w_s acc_s / sum_s w_s l_s. The splits are spread
+// over the threads (maxima, weights) and the head elements over the threads (weighted sum,
+// 128 splits per chunk with their weights in LDS), so no thread walks the splits alone.
+constexpr int kCombineThreads = 128;
+
+__device__ __forceinline__ float block_reduce(float v, bool is_max, float* red) {
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const float o = __shfl_xor(v, d, 64);
+    v = is_max ? fmaxf(v, o) : v + o;
+  }
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  v = red[0];
+#pragma unroll
+  for (int w = 1; w < kCombineThreads / 64; ++w) v = is_max ? fmaxf(v, red[w]) : v + red[w];
+  __syncthreads();
+  return v;
+}
+
+__global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(AttnArgs a) {
+  __shared__ float red[kCombineThreads / 64];
+  __shared__ float w_s[kCombineThreads];
   const int qh = blockIdx.x % a.num_q_heads;
   const int r = blockIdx.x / a.num_q_heads;
   if (r >= a.num_reqs) return;
+  const int tid = threadIdx.x;
   const int c = a.slot_indptr[r + 1] - a.slot_indptr[r];
   const int D = a.head_dim;
+  const int64_t rs = D + 2;  // record stride
   float* out = a.out + ((int64_t)r * a.num_q_heads + qh) * D;
-  int ns = c <= 0 ? 0 : (c + kAttnSplit - 1) / kAttnSplit;
+  int ns = c <= 0 ? 0 : (c + a.split_tokens - 1) / a.split_tokens;
   ns = ns < a.splits ? ns : a.splits;  // the workspace holds a.splits records
-  const float* rec0 = a.workspace + ((int64_t)r * a.num_q_heads + qh) * a.splits * (D + 2);
-  float M = -INFINITY;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, rec0[(int64_t)s * (D + 2)]);
-  float L = 0.f;
-  for (int s = 0; s < ns; ++s) {
-    const float* rec = rec0 + (int64_t)s * (D + 2);
-    L += rec[1] * __expf(rec[0] - M);
+  if (ns == 0) {
+    for (int d = tid; d < D; d += kCombineThreads) out[d] = 0.f;
+    return;
   }
-  for (int d = threadIdx.x; d < D; d += 64) {
-    float v = 0.f;
-    for (int s = 0; s < ns; ++s) {
-      const float* rec = rec0 + (int64_t)s * (D + 2);
-      v += rec[2 + d] * __expf(rec[0] - M);
+  const float* rec0 = a.workspace + ((int64_t)r * a.num_q_heads + qh) * a.splits * rs;
+  float m = -INFINITY;
+  for (int s = tid; s < ns; s += kCombineThreads) m = fmaxf(m, rec0[s * rs]);
+  const float M = block_reduce(m, true, red);
+  float l = 0.f;
+  for (int s = tid; s < ns; s += kCombineThreads) l += rec0[s * rs + 1] * __expf(rec0[s * rs] - M);
+  const float L = block_reduce(l, false, red);
+  const float inv = 1.f / L;
+  // each thread owns head elements d = tid, tid + 128 (head_dim <= 256)
+  float v0 = 0.f, v1 = 0.f;
+  const int d0 = tid, d1 = tid + kCombineThreads;
+  for (int base = 0; base < ns; base += kCombineThreads) {
+    const int n = ns - base < kCombineThreads ? ns - base : kCombineThreads;
+    if (tid < n) w_s[tid] = __expf(rec0[(base + tid) * rs] - M);
+    __syncthreads();
+    const float* rb = rec0 + (int64_t)base * rs + 2;
+    int j = 0;
+    for (; j + 4 <= n; j += 4) {
+      if (d0 < D) {
+        v0 += rb[j * rs + d0] * w_s[j] + rb[(j + 1) * rs + d0] * w_s[j + 1] +
+              rb[(j + 2) * rs + d0] * w_s[j + 2] + rb[(j + 3) * rs + d0] * w_s[j + 3];
+      }
+      if (d1 < D) {
+        v1 += rb[j * rs + d1] * w_s[j] + rb[(j + 1) * rs + d1] * w_s[j + 1] +
+              rb[(j + 2) * rs + d1] * w_s[j + 2] + rb[(j + 3) * rs + d1] * w_s[j + 3];
+      }
     }
-    out[d] = ns ? v / L : 0.f;
+    for (; j < n; ++j) {
+      if (d0 < D) v0 += rb[j * rs + d0] * w_s[j];
+      if (d1 < D) v1 += rb[j * rs + d1] * w_s[j];
+    }
+    __syncthreads();
   }
+  if (d0 < D) out[d0] = v0 * inv;
+  if (d1 < D) out[d1] = v1 * inv;
 }
 
 template <int kKind, int kLanes, int kG>
@@ -337,11 +439,11 @@ hipError_t launch_decode_g(const AttnArgs& a, hipStream_t stream) {
 
 template <int kKind>
 hipError_t launch_decode_k(const AttnArgs& a, hipStream_t stream) {
-  const int lanes = a.head_dim * (kKind == 2 ? 1 : 2) / 16;
-  switch (lanes) {
-    case 4: return launch_decode_g<kKind, 4>(a, stream);
-    case 8: return launch_decode_g<kKind, 8>(a, stream);
-    case 16: return launch_decode_g<kKind, 16>(a, stream);
+  switch (a.head_dim) {
+    case 32: return launch_decode_g<kKind, 4>(a, stream);
+    case 64: return launch_decode_g<kKind, 8>(a, stream);
+    case 128: return launch_decode_g<kKind, 16>(a, stream);
+    case 256: return launch_decode_g<kKind, 32>(a, stream);
     default: return hipErrorInvalidValue;
   }
 }
@@ -356,10 +458,9 @@ hipError_t launch_slot_mapping(const SlotMapArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-int attention_split_tokens() { return kAttnSplit; }
-
 hipError_t launch_paged_decode(const AttnArgs& a, hipStream_t stream) {
   if (a.num_reqs <= 0) return hipSuccess;
+  if (a.split_tokens != decode_split_tokens(a.head_dim)) return hipErrorInvalidValue;
   hipError_t e;
   switch (a.kv_kind) {
     case 0: e = launch_decode_k<0>(a, stream); break;
@@ -369,7 +470,8 @@ hipError_t launch_paged_decode(const AttnArgs& a, hipStream_t stream) {
   }
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(decode_combine_kernel, dim3(static_cast<unsigned>(
-                         (int64_t)a.num_reqs * a.num_q_heads)), dim3(64), 0, stream, a);
+                         (int64_t)a.num_reqs * a.num_q_heads)), dim3(kCombineThreads), 0,
+                     stream, a);
   return hipGetLastError();
 }
 

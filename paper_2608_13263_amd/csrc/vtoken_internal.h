@@ -120,6 +120,7 @@ struct AttnArgs {
   int32_t num_slots;
   int32_t num_reqs;
   int32_t splits;    // split records per (request, query head) in the workspace
+  int32_t split_tokens;  // tokens per split: decode_split_tokens(head_dim)
   float scale;
   const float* q;
   float* out;
@@ -130,7 +131,12 @@ struct AttnArgs {
 
 hipError_t launch_slot_mapping(const SlotMapArgs& a, hipStream_t stream);
 hipError_t launch_paged_decode(const AttnArgs& a, hipStream_t stream);
-int attention_split_tokens();
+// Tokens one decode workgroup covers: 8 per thread, 256 threads, head_dim / 8 lanes per
+// token (32, 64, 128 or 256 head_dim -> 512, 256, 128, 64 tokens).
+constexpr int kDecodeTokensPerThread = 8;
+constexpr int decode_split_tokens(int head_dim) {
+  return kDecodeTokensPerThread * 256 * 8 / head_dim;
+}
 
 hipError_t launch_build(const MetaArgs& a, hipStream_t stream);
 // variant: 0 default, 1 LDS double buffer, 2 LDS single buffer, 3 registers

@@ -139,13 +139,16 @@ def test_repack_and_free_reject_bad_arguments():
 
 def test_decode_workspace_bytes():
     lib = B.load_library()
-    # R * Hq * ceil(max_tokens / 256) * (D + 2) float32 partial records; at least one split
-    assert lib.vtoken_decode_workspace_bytes(3, 32, 128, 1000) == 3 * 32 * 4 * 130 * 4
-    assert lib.vtoken_decode_workspace_bytes(3, 32, 128, 1024) == 3 * 32 * 4 * 130 * 4
-    assert lib.vtoken_decode_workspace_bytes(3, 32, 128, 1025) == 3 * 32 * 5 * 130 * 4
+    # R * Hq * ceil(max_tokens / (16384 / D)) * (D + 2) float32 partial records, at least one
+    assert lib.vtoken_decode_workspace_bytes(3, 32, 128, 1000) == 3 * 32 * 8 * 130 * 4
+    assert lib.vtoken_decode_workspace_bytes(3, 32, 128, 1024) == 3 * 32 * 8 * 130 * 4
+    assert lib.vtoken_decode_workspace_bytes(3, 32, 128, 1025) == 3 * 32 * 9 * 130 * 4
     assert lib.vtoken_decode_workspace_bytes(2, 8, 64, 0) == 2 * 8 * 1 * 66 * 4
+    assert lib.vtoken_decode_workspace_bytes(2, 8, 32, 513) == 2 * 8 * 2 * 34 * 4
+    assert lib.vtoken_decode_workspace_bytes(2, 8, 256, 65) == 2 * 8 * 2 * 258 * 4
     assert lib.vtoken_decode_workspace_bytes(2, 0, 64, 10) == -1
     assert lib.vtoken_decode_workspace_bytes(-1, 8, 64, 10) == -1
+    assert lib.vtoken_decode_workspace_bytes(2, 8, 96, 10) == -1
 
 
 def _good_decode(cache, nreq=2, hq=32, max_tokens=700):
@@ -163,12 +166,12 @@ def _good_decode(cache, nreq=2, hq=32, max_tokens=700):
     (lambda c, d: setattr(d, "layer", -1), "VTOKEN_ERR_SHAPE"),
     (lambda c, d: setattr(d, "kv_dtype", B.KV_FP8_E4M3), "VTOKEN_ERR_SHAPE"),  # 2-byte cache
     (lambda c, d: setattr(d, "kv_dtype", 3), "VTOKEN_ERR_SHAPE"),
-    (lambda c, d: setattr(c, "head_dim", 256) or setattr(c, "num_kv_heads", 4),
-     "VTOKEN_ERR_SHAPE"),                                                  # 512-byte heads
-    (lambda c, d: setattr(c, "head_dim", 8) or setattr(c, "num_kv_heads", 64),
-     "VTOKEN_ERR_SHAPE"),                                                  # 16-byte heads
+    (lambda c, d: setattr(c, "head_dim", 512) or setattr(c, "num_kv_heads", 2),
+     "VTOKEN_ERR_SHAPE"),                                                  # head_dim 512
+    (lambda c, d: setattr(c, "head_dim", 16) or setattr(c, "num_kv_heads", 64),
+     "VTOKEN_ERR_SHAPE"),                                                  # head_dim 16
     (lambda c, d: setattr(d, "workspace_bytes", d.workspace_bytes - 4), "VTOKEN_ERR_CAPACITY"),
-    (lambda c, d: setattr(d, "max_tokens", 5000), "VTOKEN_ERR_CAPACITY"),
+    (lambda c, d: setattr(d, "max_tokens", 1100), "VTOKEN_ERR_CAPACITY"),
     (lambda c, d: setattr(d, "q", None), "VTOKEN_ERR_NULL"),
     (lambda c, d: setattr(d, "workspace", None), "VTOKEN_ERR_NULL"),
 ])

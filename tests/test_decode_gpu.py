@@ -142,14 +142,16 @@ def _decode_inputs(dtype, H, D, S, seed):
 
 
 DECODE_CASES = [
-    # dtype, H, D, G, S        (lanes per head row = D * elem_bytes / 16)
-    ("bf16", 8, 128, 4, 16),   # Llama-3-8B KV geometry, 16 lanes
-    ("fp16", 2, 64, 1, 16),    # 8 lanes, no GQA
-    ("bf16", 4, 32, 2, 16),    # 4 lanes
-    ("fp16", 4, 128, 8, 16),   # 16 lanes, G = 8
-    ("fp8_e4m3", 8, 128, 8, 32),  # Llama-3-70B fp8 geometry, 8 lanes
-    ("fp8_e4m3", 2, 64, 2, 16),   # 4 lanes
-    ("fp8_e4m3", 2, 256, 4, 16),  # 16 lanes, two value passes
+    # dtype, H, D, G, S        (lanes per head row = D / 8; tokens per split = 16384 / D)
+    ("bf16", 8, 128, 4, 16),   # Llama-3-8B KV geometry
+    ("fp16", 2, 64, 1, 16),    # no GQA
+    ("bf16", 4, 32, 2, 16),    # 512-token splits
+    ("fp16", 4, 128, 8, 16),   # G = 8
+    ("bf16", 2, 256, 2, 16),   # 32 lanes per head row, 64-token splits
+    ("fp8_e4m3", 8, 128, 8, 32),  # Llama-3-70B fp8 geometry
+    ("fp8_e4m3", 2, 64, 2, 16),
+    ("fp8_e4m3", 2, 256, 4, 16),
+    ("fp8_e4m3", 4, 32, 1, 16),
 ]
 
 
