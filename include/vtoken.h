@@ -85,8 +85,12 @@ typedef enum vtoken_status {
                                 /* free_list lies outside [0, num_blocks)                */
   VTOKEN_ERR_BT_LEN = -11,      /* bt_indptr[r+1]-bt_indptr[r] != ceil(seq_lens[r]/S),   */
                                 /* or bt_indptr outside [0, num_bt_entries]              */
-  VTOKEN_ERR_TOK_LEN = -12      /* tok_indptr[r+1]-tok_indptr[r] != seq_lens[r] or       */
+  VTOKEN_ERR_TOK_LEN = -12,     /* tok_indptr[r+1]-tok_indptr[r] != seq_lens[r] or       */
                                 /* tok_indptr outside [0, num_tokens]                    */
+  VTOKEN_ERR_SLOT = -13         /* vtoken_plan_partial: a live token's slot lies outside */
+                                /* [0, num_blocks*S), or the live tokens of a request's  */
+                                /* sources do not match the live slots counted in them   */
+                                /* (two tokens on one slot, a slot outside its table)    */
 } vtoken_status;
 
 /* The paged KV cache (Sec. 2.1). */
@@ -211,6 +215,68 @@ vtoken_status vtoken_repack_inplace_ex(const vtoken_cache* cache, const vtoken_b
                                        const vtoken_plan* plan,
                                        const vtoken_repack_options* options,
                                        hipStream_t stream);
+
+/* ---- Partial reclamation pass (Sec. 3.3.1-3.3.3; I4 of Sec. 3.5; Sec. 5.7) ----
+ *
+ * The paper's planner: per-block live counts n_b and the waste ratio F (Sec. 2.3.1), the
+ * trigger F > theta_F with enough low-utilisation blocks and the free list near its low
+ * watermark (Sec. 3.3.2), and per request its low-utilisation source blocks only, at most B
+ * source blocks considered in the pass (Sec. 3.3.3). Shared-prefix blocks - blocks that appear
+ * in more than one request's table - and pinned blocks are never sources (I4, Sec. 5.7).
+ *
+ * Input is a token table: slot_in[t] (device, int32 [num_tokens]) is the current slot of
+ * logical token t, -1 if it holds none; a live token's slot must lie in a block of its own
+ * request's table (blocks of a table may be in any order and hold tokens in any order, so
+ * passes can follow each other). bt_indptr gives each request's table (any length); the
+ * token CSR is as for the full pass. block_size <= 64.
+ *
+ * Readings (also those of the CPU reference): a block is a candidate iff it is in exactly
+ * one table, not pinned, and n_b <= max_live_per_source; F > theta_num/theta_den is decided
+ * exactly in integers; the pass is attempted iff F > theta_F, at least min_eligible
+ * candidates exist and (free_watermark < 0 or free_len <= free_watermark); candidates are
+ * considered in request order, table order within a request, until max_sources (B) have
+ * been considered, admitted or not; T_live = live tokens of a request's considered sources,
+ * need = ceil(T_live/S), a plan exists iff 0 < sources and need < sources; admission is the
+ * prefix rule of the full pass over free_list; the move list takes the live tokens of the
+ * sources in logical order into the destinations (each filled before the next); the new table
+ * is the kept blocks in order followed by the destinations; dead tokens map to -1.
+ *
+ * Outputs go to the vtoken_plan (sizes as for vtoken_build_token_table: token_slot [T],
+ * live_count / admitted [R], CSR offsets [R+1], new_block_ids with new_bt_capacity >= M,
+ * src_plan with src_plan_capacity >= min(free_len, M)*S, counters [4] = {destination blocks
+ * used, requests admitted, sources released, status}) and to the state buffers below. The
+ * copy is vtoken_repack on the same plan, enqueued after this call. The released sources are
+ * state->sources[0 .. counters[2]) (CSR by freed_indptr): reuse them only after the copy has
+ * executed on the stream; vtoken_free_blocks does not apply to this pass. */
+typedef struct vtoken_planner_params {
+  int32_t theta_num;            /* theta_F = theta_num / theta_den (paper default 1/4)       */
+  int32_t theta_den;            /* > 0                                                        */
+  int32_t max_live_per_source;  /* < 0: the block's own waste exceeds theta_F, i.e.          */
+                                /* n_b * theta_den < (theta_den - theta_num) * S             */
+  int32_t min_eligible;         /* candidates needed for an attempt (>= 0)                   */
+  int32_t free_watermark;       /* attempt only if free_len <= this; < 0: no condition      */
+  int32_t reserved;             /* 0                                                          */
+  int64_t max_sources;          /* B, >= 0                                                    */
+} vtoken_planner_params;
+
+typedef struct vtoken_planner_state {   /* caller-allocated device buffers */
+  uint64_t* live_bits;   /* [num_blocks] scratch: live slots of each block                   */
+  int32_t*  refs;        /* [num_blocks] out: tables holding each block                      */
+  int32_t*  n_b;         /* [num_blocks] out: live tokens of each block (0 if unallocated)   */
+  int32_t*  selected;    /* [num_blocks] scratch                                             */
+  int32_t*  elig_cum;    /* [num_bt_entries] scratch                                         */
+  int32_t*  src_count;   /* [num_reqs] out: sources considered per request                   */
+  int32_t*  sources;     /* [num_bt_entries] out: released source blocks (CSR freed_indptr)  */
+  int64_t*  stats;       /* [8] out: sum n_b, allocated blocks N, candidates, attempted      */
+                         /* (0/1), sources considered, tokens moved, sources released,       */
+                         /* destination blocks used                                          */
+  const uint8_t* pinned; /* [num_blocks] or NULL: nonzero = never a source                   */
+} vtoken_planner_state;
+
+vtoken_status vtoken_plan_partial(const vtoken_cache* cache, const vtoken_batch* batch,
+                                  const int32_t* slot_in, const vtoken_planner_params* params,
+                                  const vtoken_planner_state* state, const vtoken_plan* plan,
+                                  hipStream_t stream);
 
 /* ---- Consumer side (Sec. 3.4: slot mapping; Sec. 3.3.4 and I3 of Sec. 3.5: ordering) ----
  *

@@ -94,3 +94,99 @@ def brute_repack(seq_lens: Sequence[int], block_tables: Sequence[Sequence[int]],
             new_planes.append(q)
         out["planes"] = new_planes
     return out
+
+
+def brute_plan_partial(seq_lens: Sequence[int], block_tables: Sequence[Sequence[int]],
+                       live_masks: Sequence[Sequence[int]], slots: Sequence[Sequence[int]],
+                       free_list: Sequence[int], S: int, theta=(1, 4), max_live=None,
+                       max_sources=1 << 30, min_eligible=1, free_watermark=-1,
+                       pinned: Sequence[int] = (), planes: Optional[List[Dict[int, bytes]]] = None):
+    """Literal walk of the partial pass (Sec. 3.3.1-3.3.4) on Python lists, sharing no code
+    with planner.py: live tokens per block are counted one slot at a time, the waste ratio is
+    compared as a fraction, candidates are collected block by block while a budget counter
+    runs down, destinations are handed out slot by slot. Returns a dict of lists."""
+    from fractions import Fraction
+    R = len(seq_lens)
+    holders: Dict[int, int] = {}
+    for t in block_tables:
+        for b in t:
+            holders[b] = holders.get(b, 0) + 1
+    live_at = set()
+    for r in range(R):
+        for p in range(seq_lens[r]):
+            if live_masks[r][p]:
+                live_at.add(slots[r][p])
+    count = {b: 0 for b in holders}
+    for b in holders:
+        for off in range(S):
+            if b * S + off in live_at:
+                count[b] += 1
+    total_live = sum(count.values())
+    n_alloc = len(holders)
+    waste = Fraction(0) if n_alloc == 0 else 1 - Fraction(total_live, n_alloc * S)
+    theta_f = Fraction(theta[0], theta[1])
+    if max_live is None:
+        # a block is low-utilisation when its own waste exceeds theta_F
+        ok = lambda b: 1 - Fraction(count[b], S) > theta_f  # noqa: E731
+    else:
+        ok = lambda b: count[b] <= max_live  # noqa: E731
+    pinned_set = set(pinned)
+    candidates = [[b for b in block_tables[r] if holders[b] == 1 and b not in pinned_set
+                   and ok(b)] for r in range(R)]
+    n_cand = sum(len(c) for c in candidates)
+    go = (n_alloc > 0 and waste > theta_f and n_cand >= min_eligible
+          and (free_watermark < 0 or len(free_list) <= free_watermark))
+
+    chosen = [[] for _ in range(R)]
+    if go:
+        left = max_sources
+        for r in range(R):
+            for b in candidates[r]:
+                if left > 0:
+                    chosen[r].append(b)
+                left -= 1
+    free = list(free_list)
+    handed = 0
+    refused = False
+    admitted, new_tables, freed, token_slot, src_plan = [], [], [], [], []
+    moves = []
+    for r in range(R):
+        moving = [p for p in range(seq_lens[r])
+                  if live_masks[r][p] and slots[r][p] // S in chosen[r]]
+        blocks = 0
+        while blocks * S < len(moving):
+            blocks += 1
+        good = len(chosen[r]) > 0 and blocks < len(chosen[r])
+        if good and (refused or handed + blocks > len(free)):
+            refused = True
+            good = False
+        out = [slots[r][p] if live_masks[r][p] else -1 for p in range(seq_lens[r])]
+        if not good:
+            admitted.append(0)
+            new_tables.append(list(block_tables[r]))
+            token_slot.append(out)
+            continue
+        dest = free[handed:handed + blocks]
+        handed += blocks
+        dest_slots = [blk * S + off for blk in dest for off in range(S)]
+        for i, p in enumerate(moving):
+            out[p] = dest_slots[i]
+            moves.append((slots[r][p], dest_slots[i]))
+        src_plan.extend(slots[r][moving[i]] if i < len(moving) else -1
+                        for i in range(len(dest_slots)))
+        admitted.append(1)
+        new_tables.append([b for b in block_tables[r] if b not in chosen[r]] + dest)
+        freed.extend(b for b in block_tables[r] if b in chosen[r])
+        token_slot.append(out)
+    out = dict(triggered=go, count=count, chosen=[len(c) for c in chosen], admitted=admitted,
+               new_tables=new_tables, freed=freed, token_slot=token_slot, used=handed,
+               src_plan=src_plan)
+    if planes is not None:
+        new_planes = []
+        for plane in planes:
+            q = dict(plane)
+            for old, new in moves:
+                q[new] = plane[old]
+            new_planes.append(q)
+        out["planes"] = new_planes
+    return out

@@ -25,7 +25,7 @@ VTOKEN_OK = 0
 STATUS = {
     0: "VTOKEN_OK", -1: "VTOKEN_ERR_NULL", -2: "VTOKEN_ERR_SHAPE", -3: "VTOKEN_ERR_CAPACITY",
     -4: "VTOKEN_ERR_HIP", -5: "VTOKEN_ERR_ARGUMENT", -10: "VTOKEN_ERR_BLOCK_RANGE",
-    -11: "VTOKEN_ERR_BT_LEN", -12: "VTOKEN_ERR_TOK_LEN",
+    -11: "VTOKEN_ERR_BT_LEN", -12: "VTOKEN_ERR_TOK_LEN", -13: "VTOKEN_ERR_SLOT",
 }
 STATUS_CODE = {v: k for k, v in STATUS.items()}
 
@@ -76,6 +76,21 @@ class CDecode(ctypes.Structure):
 KV_FP16, KV_BF16, KV_FP8_E4M3 = 0, 1, 2
 
 
+class CPlannerParams(ctypes.Structure):
+    _fields_ = [("theta_num", ctypes.c_int32), ("theta_den", ctypes.c_int32),
+                ("max_live_per_source", ctypes.c_int32), ("min_eligible", ctypes.c_int32),
+                ("free_watermark", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("max_sources", ctypes.c_int64)]
+
+
+class CPlannerState(ctypes.Structure):
+    _fields_ = [("live_bits", ctypes.c_void_p), ("refs", ctypes.c_void_p),
+                ("n_b", ctypes.c_void_p), ("selected", ctypes.c_void_p),
+                ("elig_cum", ctypes.c_void_p), ("src_count", ctypes.c_void_p),
+                ("sources", ctypes.c_void_p), ("stats", ctypes.c_void_p),
+                ("pinned", ctypes.c_void_p)]
+
+
 # Every extern "C" symbol of include/vtoken.h with its ctypes signature.
 _SIGNATURES = {
     "vtoken_build_token_table": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
@@ -106,6 +121,10 @@ _SIGNATURES = {
     "vtoken_paged_decode": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CDecode),
                                              ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                              ctypes.c_void_p]),
+    "vtoken_plan_partial": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
+                                             ctypes.c_void_p, ctypes.POINTER(CPlannerParams),
+                                             ctypes.POINTER(CPlannerState),
+                                             ctypes.POINTER(CPlan), ctypes.c_void_p]),
     "vtoken_last_hip_error": (ctypes.c_int32, []),
     "vtoken_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
     "vtoken_version": (ctypes.c_int32, []),
@@ -379,3 +398,77 @@ def paged_decode(cache: KVCache, q, slot_indptr, slots, layer: int, max_tokens: 
     _check(lib.vtoken_paged_decode(ctypes.byref(c), ctypes.byref(d), R, _ptr(slot_indptr),
                                    _ptr(slots), _stream(stream)), "vtoken_paged_decode")
     return out
+
+
+class PlannerParams:
+    """Parameters of the partial pass (vtoken_planner_params); theta_F = theta[0]/theta[1]
+    (the paper's default 0.25), max_live_per_source < 0 derives the utilisation bound from
+    theta_F, max_sources is B, free_watermark < 0 drops the watermark condition."""
+
+    def __init__(self, theta=(1, 4), max_live_per_source: int = -1, max_sources: int = 1 << 40,
+                 min_eligible: int = 1, free_watermark: int = -1):
+        self.theta = (int(theta[0]), int(theta[1]))
+        self.max_live_per_source = int(max_live_per_source)
+        self.max_sources = int(max_sources)
+        self.min_eligible = int(min_eligible)
+        self.free_watermark = int(free_watermark)
+
+    def c(self) -> CPlannerParams:
+        return CPlannerParams(self.theta[0], self.theta[1], self.max_live_per_source,
+                              self.min_eligible, self.free_watermark, 0, self.max_sources)
+
+
+class PlannerState:
+    """Caller-allocated buffers of the partial pass (vtoken_planner_state)."""
+
+    FIELDS = ("live_bits", "refs", "n_b", "selected", "elig_cum", "src_count", "sources",
+              "stats")
+
+    def __init__(self, pinned=None, **tensors):
+        for k in self.FIELDS:
+            setattr(self, k, tensors[k])
+        self.pinned = pinned
+
+    @classmethod
+    def allocate(cls, num_blocks: int, batch: Batch, device="cuda", pinned=None):
+        import torch
+
+        def e(n, dt=torch.int32):
+            return torch.empty(max(int(n), 1), dtype=dt, device=device)
+        M, R = batch.num_bt_entries, batch.num_reqs
+        if pinned is not None and not isinstance(pinned, torch.Tensor):
+            import numpy as np
+            pinned = torch.from_numpy(np.ascontiguousarray(pinned, dtype=np.uint8)).to(device)
+        return cls(live_bits=e(num_blocks, torch.int64), refs=e(num_blocks), n_b=e(num_blocks),
+                   selected=e(num_blocks), elig_cum=e(M), src_count=e(R), sources=e(M),
+                   stats=e(8, torch.int64), pinned=pinned)
+
+    def c(self) -> CPlannerState:
+        return CPlannerState(*(_ptr(getattr(self, k)) for k in self.FIELDS), _ptr(self.pinned))
+
+
+def plan_partial(cache: KVCache, batch: Batch, slot_in, plan: Plan, state: PlannerState,
+                 params: Optional[PlannerParams] = None, stream=None) -> None:
+    """The partial pass's planning kernels; follow with repack() on the same plan."""
+    lib = load_library()
+    c, b, p = cache.c(), batch.c(), plan.c()
+    prm = (params or PlannerParams()).c()
+    st = state.c()
+    _check(lib.vtoken_plan_partial(ctypes.byref(c), ctypes.byref(b), _ptr(slot_in),
+                                   ctypes.byref(prm), ctypes.byref(st), ctypes.byref(p),
+                                   _stream(stream)), "vtoken_plan_partial")
+
+
+def run_partial_pass(cache: KVCache, batch: Batch, slot_in, plan: Optional[Plan] = None,
+                     state: Optional[PlannerState] = None,
+                     params: Optional[PlannerParams] = None, pinned=None, stream=None):
+    """Plan and copy of one partial pass, enqueued in order on one stream; returns
+    (plan, state). The released sources are state.sources[:plan.counters[2]]."""
+    if plan is None:
+        plan = Plan.allocate(batch, cache.block_size, device=cache.kv.device)
+    if state is None:
+        state = PlannerState.allocate(cache.num_blocks, batch, device=cache.kv.device,
+                                      pinned=pinned)
+    plan_partial(cache, batch, slot_in, plan, state, params, stream)
+    repack(cache, batch, plan, stream)
+    return plan, state

@@ -16,7 +16,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB_PATH = os.path.join(HERE, "libvtoken.so")
 SOURCES = [os.path.join(HERE, "csrc", f)
-           for f in ("vtoken_abi.hip", "vtoken_kernels.hip", "vtoken_attention.hip")]
+           for f in ("vtoken_abi.hip", "vtoken_kernels.hip", "vtoken_attention.hip",
+                     "vtoken_planner.hip")]
 HEADERS = [os.path.join(ROOT, "include", "vtoken.h"),
            os.path.join(HERE, "csrc", "vtoken_internal.h")]
 ARCH = "gfx950"

@@ -333,6 +333,91 @@ vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode
   return hip_status(vtoken::launch_paged_decode(a, stream));
 }
 
+vtoken_status vtoken_plan_partial(const vtoken_cache* cache, const vtoken_batch* batch,
+                                  const int32_t* slot_in, const vtoken_planner_params* params,
+                                  const vtoken_planner_state* st, const vtoken_plan* plan,
+                                  hipStream_t stream) {
+  vtoken_status s = check_cache(cache);
+  if (s != VTOKEN_OK) return s;
+  if ((s = check_batch(batch)) != VTOKEN_OK) return s;
+  if (params == nullptr || st == nullptr || plan == nullptr) return VTOKEN_ERR_NULL;
+  const int S = cache->block_size;
+  if (S > 64) return VTOKEN_ERR_SHAPE;
+  if (params->theta_den <= 0 || params->max_sources < 0 || params->min_eligible < 0 ||
+      params->reserved != 0) {
+    return VTOKEN_ERR_ARGUMENT;
+  }
+  const int32_t R = batch->num_reqs;
+  const int64_t T = batch->num_tokens, M = batch->num_bt_entries;
+  if (st->live_bits == nullptr || st->refs == nullptr || st->n_b == nullptr ||
+      st->selected == nullptr || st->stats == nullptr || plan->counters == nullptr ||
+      plan->dst_indptr == nullptr || plan->new_bt_indptr == nullptr ||
+      plan->freed_indptr == nullptr) {
+    return VTOKEN_ERR_NULL;
+  }
+  if (R > 0 && (st->src_count == nullptr || plan->live_count == nullptr ||
+                plan->admitted == nullptr)) {
+    return VTOKEN_ERR_NULL;
+  }
+  if (T > 0 && (slot_in == nullptr || plan->token_slot == nullptr)) return VTOKEN_ERR_NULL;
+  if (M > 0 && (st->elig_cum == nullptr || st->sources == nullptr ||
+                plan->new_block_ids == nullptr)) {
+    return VTOKEN_ERR_NULL;
+  }
+  if (plan->new_bt_capacity < M) return VTOKEN_ERR_CAPACITY;
+  const int64_t plan_min = (batch->free_len < M ? batch->free_len : M) * (int64_t)S;
+  if (plan_min > 0 && plan->src_plan == nullptr) return VTOKEN_ERR_NULL;
+  if (plan->src_plan_capacity < plan_min) return VTOKEN_ERR_CAPACITY;
+  vtoken::PlannerArgs a = {};
+  a.num_reqs = R;
+  a.num_tokens = static_cast<int32_t>(T);
+  a.num_bt_entries = static_cast<int32_t>(M);
+  a.block_size = S;
+  a.num_blocks = cache->num_blocks;
+  a.num_slots = cache->num_blocks * S;
+  a.free_len = batch->free_len;
+  a.theta_num = params->theta_num;
+  a.theta_den = params->theta_den;
+  if (params->max_live_per_source >= 0) {
+    a.max_live = params->max_live_per_source;
+  } else {
+    // largest n with n * den < (den - num) * S: the block's own waste exceeds theta_F
+    const int64_t lim = ((int64_t)params->theta_den - params->theta_num) * S;
+    a.max_live = lim > 0 ? static_cast<int32_t>((lim - 1) / params->theta_den) : -1;
+  }
+  a.min_eligible = params->min_eligible;
+  a.free_watermark = params->free_watermark;
+  a.max_sources = params->max_sources;
+  a.seq_lens = batch->seq_lens;
+  a.tok_indptr = batch->tok_indptr;
+  a.bt_indptr = batch->bt_indptr;
+  a.block_ids = batch->block_ids;
+  a.live = batch->live;
+  a.slot_in = slot_in;
+  a.free_list = batch->free_list;
+  a.pinned = st->pinned;
+  a.live_bits = st->live_bits;
+  a.refs = st->refs;
+  a.n_b = st->n_b;
+  a.selected = st->selected;
+  a.elig_cum = st->elig_cum;
+  a.src_count = st->src_count;
+  a.sources = st->sources;
+  a.stats = st->stats;
+  a.token_slot = plan->token_slot;
+  a.live_count = plan->live_count;
+  a.admitted = plan->admitted;
+  a.dst_indptr = plan->dst_indptr;
+  a.new_bt_indptr = plan->new_bt_indptr;
+  a.new_block_ids = plan->new_block_ids;
+  a.src_plan = plan->src_plan;
+  a.freed_indptr = plan->freed_indptr;
+  a.counters = plan->counters;
+  a.new_bt_capacity = plan->new_bt_capacity;
+  a.src_plan_capacity = plan->src_plan_capacity;
+  return hip_status(vtoken::launch_planner(a, stream));
+}
+
 int32_t vtoken_last_hip_error(void) { return g_last_hip_error; }
 
 const char* vtoken_status_string(int32_t status) {
@@ -346,6 +431,7 @@ const char* vtoken_status_string(int32_t status) {
     case VTOKEN_ERR_BLOCK_RANGE: return "VTOKEN_ERR_BLOCK_RANGE: block id outside the pool";
     case VTOKEN_ERR_BT_LEN: return "VTOKEN_ERR_BT_LEN: block table length != ceil(len/S)";
     case VTOKEN_ERR_TOK_LEN: return "VTOKEN_ERR_TOK_LEN: token range != sequence length";
+    case VTOKEN_ERR_SLOT: return "VTOKEN_ERR_SLOT: a live token's slot is invalid for its table";
     default: return "unknown vtoken status";
   }
 }

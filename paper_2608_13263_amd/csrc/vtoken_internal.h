@@ -129,6 +129,51 @@ struct AttnArgs {
   const int32_t* slots;
 };
 
+// Arguments of the partial reclamation pass (vtoken_plan_partial).
+struct PlannerArgs {
+  int32_t num_reqs;
+  int32_t num_tokens;
+  int32_t num_bt_entries;
+  int32_t block_size;
+  int32_t num_blocks;
+  int32_t num_slots;
+  int32_t free_len;
+  int32_t theta_num, theta_den;
+  int32_t max_live;
+  int32_t min_eligible;
+  int32_t free_watermark;
+  int64_t max_sources;
+  const int32_t* seq_lens;
+  const int32_t* tok_indptr;
+  const int32_t* bt_indptr;
+  const int32_t* block_ids;
+  const uint8_t* live;
+  const int32_t* slot_in;
+  const int32_t* free_list;
+  const uint8_t* pinned;  // may be null
+  uint64_t* live_bits;
+  int32_t* refs;
+  int32_t* n_b;
+  int32_t* selected;
+  int32_t* elig_cum;
+  int32_t* src_count;
+  int32_t* sources;
+  int64_t* stats;
+  int32_t* token_slot;
+  int32_t* live_count;
+  int32_t* admitted;
+  int32_t* dst_indptr;
+  int32_t* new_bt_indptr;
+  int32_t* new_block_ids;
+  int32_t* src_plan;
+  int32_t* freed_indptr;
+  int32_t* counters;
+  int64_t new_bt_capacity;
+  int64_t src_plan_capacity;
+};
+
+hipError_t launch_planner(const PlannerArgs& a, hipStream_t stream);
+
 hipError_t launch_slot_mapping(const SlotMapArgs& a, hipStream_t stream);
 hipError_t launch_paged_decode(const AttnArgs& a, hipStream_t stream);
 // Tokens one decode workgroup covers: 8 per thread, 256 threads, head_dim / 8 lanes per

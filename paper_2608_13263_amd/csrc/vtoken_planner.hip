@@ -1,0 +1,397 @@
+// The paper's partial reclamation pass (Sec. 3.3) on CDNA4 (gfx950): per-block liveness,
+// the waste-ratio trigger, low-utilisation sources under a bound B, the move list and the
+// token-table update. The copy itself is the same gather kernel as the full pass (a source
+// plan per destination block), launched by vtoken_repack.
+//
+//   pl_clear_kernel    zero the per-block live bitmaps and reference counts, the statistics
+//                      and the counters
+//   pl_count_kernel    references of every block over all tables; one bit per live slot
+//                      (a slot held live by several requests of a shared prefix counts once)
+//   pl_blocks_kernel   n_b = live bits of each allocated block (Sec. 2.3.1, Sec. 3.3.1); the
+//                      totals behind the waste ratio F
+//   pl_request_kernel  one workgroup per request: live count, its candidate blocks (unshared,
+//                      unpinned, n_b <= max_live) in table order with their cumulative live
+//                      tokens
+//   pl_admit_kernel    one workgroup: the trigger (F > theta_F, enough candidates, free list at
+//                      or below the watermark, Sec. 3.3.2), the bound B over the candidates in
+//                      request order, T_live, ceil(T_live / S), strict gain, admission against
+//                      the free list, and every CSR offset (Sec. 3.3.3)
+//   pl_table_kernel    one workgroup per request: selected sources, new block table (kept
+//                      blocks then destinations), released sources, and the move list in
+//                      logical order written as token slots and the per-destination source
+//                      plan (Sec. 3.3.3, Sec. 3.2 apply_moves)
+//
+// Every kernel after pl_count_kernel does nothing once plan->counters[3] holds an error;
+// every dereference of caller data is bounds-checked.
+#include "vtoken_internal.h"
+
+namespace vtoken {
+namespace {
+
+constexpr int kPlThreads = 256;
+constexpr int kPlWaves = kPlThreads / 64;
+constexpr int kPlAdmitThreads = 1024;
+constexpr int kPlAdmitWaves = kPlAdmitThreads / 64;
+
+__device__ __forceinline__ int pl_lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
+}
+
+__device__ __forceinline__ void pl_error(int32_t* counters, int code) {
+  atomicCAS(&counters[3], 0, code);
+}
+
+// Exclusive scan over the workgroup of NV int64 values per thread; tot[k] is the sum.
+template <int NV, int kWaves>
+__device__ __forceinline__ void pl_scan(int64_t (&v)[NV], int64_t (&tot)[NV],
+                                        int64_t (*lds)[NV]) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  int64_t incl[NV];
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    int64_t x = v[k];
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int64_t t = __shfl_up(x, d, 64);
+      if (lane >= d) x += t;
+    }
+    incl[k] = x;
+  }
+  if (lane == 63) {
+#pragma unroll
+    for (int k = 0; k < NV; ++k) lds[wave][k] = incl[k];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    int64_t off = 0, t = 0;
+    for (int w = 0; w < kWaves; ++w) {
+      const int64_t x = lds[w][k];
+      off += w < wave ? x : 0;
+      t += x;
+    }
+    v[k] = off + incl[k] - v[k];
+    tot[k] = t;
+  }
+  __syncthreads();
+}
+
+// Rank of `flag` among the flagged threads of the workgroup (ballots), and their count.
+__device__ __forceinline__ int pl_rank(bool flag, int* total, int* lds) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const uint64_t m = __ballot(flag);
+  if (lane == 0) lds[wave] = __popcll(m);
+  __syncthreads();
+  int off = 0, t = 0;
+#pragma unroll
+  for (int w = 0; w < kPlWaves; ++w) {
+    const int x = lds[w];
+    off += w < wave ? x : 0;
+    t += x;
+  }
+  __syncthreads();
+  *total = t;
+  return off + pl_lanes_below(m);
+}
+
+__device__ __forceinline__ bool pl_candidate(const PlannerArgs& a, int b) {
+  if (b < 0 || b >= a.num_blocks) return false;
+  if (a.refs[b] != 1) return false;                      // shared-prefix blocks never move
+  if (a.pinned != nullptr && a.pinned[b] != 0) return false;
+  return a.n_b[b] <= a.max_live;
+}
+
+__global__ __launch_bounds__(256) void pl_clear_kernel(PlannerArgs a) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < a.num_blocks;
+       i += stride) {
+    a.live_bits[i] = 0ull;
+    a.refs[i] = 0;
+  }
+  if (blockIdx.x == 0 && threadIdx.x < 8) a.stats[threadIdx.x] = 0;
+  if (blockIdx.x == 0 && threadIdx.x < 4) a.counters[threadIdx.x] = 0;
+}
+
+__global__ __launch_bounds__(256) void pl_count_kernel(PlannerArgs a) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t n = (int64_t)a.num_bt_entries + a.num_tokens;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    if (i < a.num_bt_entries) {
+      const int b = a.block_ids[i];
+      if (b < 0 || b >= a.num_blocks) {
+        pl_error(a.counters, VTOKEN_ERR_BLOCK_RANGE);
+      } else {
+        atomicAdd(&a.refs[b], 1);
+      }
+    } else {
+      const int64_t t = i - a.num_bt_entries;
+      if (a.live[t] == 0) continue;
+      const int s = a.slot_in[t];
+      if (s < 0 || s >= a.num_slots) {
+        pl_error(a.counters, VTOKEN_ERR_SLOT);
+      } else {
+        atomicOr(&a.live_bits[s / a.block_size], 1ull << (s % a.block_size));
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void pl_blocks_kernel(PlannerArgs a) {
+  __shared__ int64_t red[2][4];
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  int64_t live = 0, alloc = 0;
+  for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < a.num_blocks;
+       b += stride) {
+    const bool held = a.refs[b] > 0;
+    const int n = held ? __popcll(a.live_bits[b]) : 0;
+    a.n_b[b] = n;
+    live += n;
+    alloc += held ? 1 : 0;
+  }
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    live += __shfl_xor(live, d, 64);
+    alloc += __shfl_xor(alloc, d, 64);
+  }
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    red[0][wave] = live;
+    red[1][wave] = alloc;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t l = 0, al = 0;
+    for (int w = 0; w < 4; ++w) {
+      l += red[0][w];
+      al += red[1][w];
+    }
+    if (l) atomicAdd(reinterpret_cast<unsigned long long*>(&a.stats[0]),
+                     static_cast<unsigned long long>(l));
+    if (al) atomicAdd(reinterpret_cast<unsigned long long*>(&a.stats[1]),
+                      static_cast<unsigned long long>(al));
+  }
+}
+
+__global__ __launch_bounds__(kPlThreads) void pl_request_kernel(PlannerArgs a) {
+  __shared__ int lds_rank[kPlWaves];
+  __shared__ int64_t lds_scan[kPlWaves][1];
+  const int r = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int n = a.seq_lens[r];
+  const int t0 = a.tok_indptr[r], t1 = a.tok_indptr[r + 1];
+  const int b0 = a.bt_indptr[r], b1 = a.bt_indptr[r + 1];
+  if (n < 0 || t0 < 0 || t1 > a.num_tokens || (int64_t)t1 - t0 != n) {
+    if (tid == 0) {
+      pl_error(a.counters, VTOKEN_ERR_TOK_LEN);
+      a.src_count[r] = 0;
+    }
+    return;
+  }
+  if (b0 < 0 || b1 > a.num_bt_entries || b1 < b0) {
+    if (tid == 0) {
+      pl_error(a.counters, VTOKEN_ERR_BT_LEN);
+      a.src_count[r] = 0;
+    }
+    return;
+  }
+  // live count of the request
+  int lc = 0;
+  for (int p = tid; p < n; p += kPlThreads) lc += a.live[t0 + p] != 0;
+  int64_t v[1] = {lc}, tot[1];
+  pl_scan<1, kPlWaves>(v, tot, lds_scan);
+  if (tid == 0) a.live_count[r] = static_cast<int32_t>(tot[0]);
+
+  // candidates in table order, with the cumulative live tokens of the candidates so far
+  int carry = 0;
+  int live_carry = 0;
+  for (int base = 0; base < b1 - b0; base += kPlThreads) {
+    const int j = base + tid;
+    const int b = j < b1 - b0 ? a.block_ids[b0 + j] : -1;
+    const bool cand = j < b1 - b0 && pl_candidate(a, b);
+    int cnt;
+    const int rank = pl_rank(cand, &cnt, lds_rank);
+    int64_t lv[1] = {cand ? a.n_b[b] : 0}, ltot[1];
+    pl_scan<1, kPlWaves>(lv, ltot, lds_scan);
+    if (cand) a.elig_cum[b0 + carry + rank] = live_carry + static_cast<int>(lv[0]) + a.n_b[b];
+    carry += cnt;
+    live_carry += static_cast<int>(ltot[0]);
+  }
+  if (tid == 0) {
+    a.src_count[r] = carry;
+    if (carry) atomicAdd(reinterpret_cast<unsigned long long*>(&a.stats[2]),
+                         static_cast<unsigned long long>(carry));
+  }
+}
+
+__global__ __launch_bounds__(kPlAdmitThreads) void pl_admit_kernel(PlannerArgs a) {
+  __shared__ int64_t lds1[kPlAdmitWaves][1];
+  __shared__ int64_t lds3[kPlAdmitWaves][3];
+  if (a.counters[3] != 0) return;
+  const int tid = threadIdx.x;
+  const int S = a.block_size;
+  const int64_t L = a.stats[0], A = a.stats[1], E = a.stats[2];
+  const int64_t cap = A * S;
+  const bool trig = cap > 0 && (cap - L) * a.theta_den > (int64_t)a.theta_num * cap &&
+                    E >= a.min_eligible &&
+                    (a.free_watermark < 0 || a.free_len <= a.free_watermark);
+  // carries over the chunks: candidates of earlier requests, needs of earlier profitable
+  // requests, destinations, new table entries, released sources; and the totals
+  int64_t c_e = 0, c_o = 0, c_dst = 0, c_len = 0, c_free = 0;
+  int64_t s_k = 0, s_moved = 0, n_adm = 0;
+  for (int base = 0; base < a.num_reqs; base += kPlAdmitThreads) {
+    const int r = base + tid;
+    const bool in = r < a.num_reqs;
+    const int m = in ? a.bt_indptr[r + 1] - a.bt_indptr[r] : 0;
+    const int64_t e = in && trig ? a.src_count[r] : 0;
+    int64_t v1[1] = {e}, t1[1];
+    pl_scan<1, kPlAdmitWaves>(v1, t1, lds1);
+    const int64_t room = a.max_sources - (c_e + v1[0]);    // bound B over the candidates
+    const int64_t k = room <= 0 ? 0 : (e < room ? e : room);
+    c_e += t1[0];
+    const int64_t T = k > 0 ? a.elig_cum[a.bt_indptr[r] + k - 1] : 0;
+    const int64_t need = (T + S - 1) / S;
+    const bool prof = k > 0 && need < k;                   // strict block reduction (I4)
+    v1[0] = prof ? need : 0;
+    pl_scan<1, kPlAdmitWaves>(v1, t1, lds1);
+    const bool adm = prof && c_o + v1[0] + need <= a.free_len;
+    c_o += t1[0];
+    int64_t y[3] = {adm ? need : 0, adm ? m - k + need : m, adm ? k : 0}, ty[3];
+    pl_scan<3, kPlAdmitWaves>(y, ty, lds3);
+    if (in) {
+      a.src_count[r] = static_cast<int32_t>(k);
+      a.admitted[r] = adm ? 1 : 0;
+      a.dst_indptr[r] = static_cast<int32_t>(c_dst + y[0]);
+      a.new_bt_indptr[r] = static_cast<int32_t>(c_len + y[1]);
+      a.freed_indptr[r] = static_cast<int32_t>(c_free + y[2]);
+    }
+    c_dst += ty[0];
+    c_len += ty[1];
+    c_free += ty[2];
+    int64_t z[3] = {k, adm ? T : 0, adm ? 1 : 0}, tz[3];
+    pl_scan<3, kPlAdmitWaves>(z, tz, lds3);
+    s_k += tz[0];
+    s_moved += tz[1];
+    n_adm += tz[2];
+  }
+  if (tid == 0) {
+    a.dst_indptr[a.num_reqs] = static_cast<int32_t>(c_dst);
+    a.new_bt_indptr[a.num_reqs] = static_cast<int32_t>(c_len);
+    a.freed_indptr[a.num_reqs] = static_cast<int32_t>(c_free);
+    a.stats[3] = trig ? 1 : 0;
+    if (c_dst * S > a.src_plan_capacity || c_len > a.new_bt_capacity) {
+      a.counters[3] = VTOKEN_ERR_CAPACITY;
+      return;
+    }
+    a.counters[0] = static_cast<int32_t>(c_dst);
+    a.counters[1] = static_cast<int32_t>(n_adm);
+    a.counters[2] = static_cast<int32_t>(c_free);
+    a.stats[4] = s_k;
+    a.stats[5] = s_moved;
+    a.stats[6] = c_free;
+    a.stats[7] = c_dst;
+  }
+}
+
+__global__ __launch_bounds__(kPlThreads) void pl_table_kernel(PlannerArgs a) {
+  __shared__ int lds_rank[kPlWaves];
+  if (a.counters[3] != 0) return;
+  const int r = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int S = a.block_size;
+  const int t0 = a.tok_indptr[r], n = a.tok_indptr[r + 1] - t0;
+  const int b0 = a.bt_indptr[r], m = a.bt_indptr[r + 1] - b0;
+  const bool adm = a.admitted[r] != 0;
+  const int k = adm ? a.src_count[r] : 0;
+  const int d0 = a.dst_indptr[r];
+  const int need = a.dst_indptr[r + 1] - d0;
+  const int nb0 = a.new_bt_indptr[r];
+  const int f0 = a.freed_indptr[r];
+
+  // sources: the first k candidates in table order; kept blocks and released sources
+  int cand_carry = 0, keep_carry = 0, sel_carry = 0;
+  for (int base = 0; base < m; base += kPlThreads) {
+    const int j = base + tid;
+    const bool in = j < m;
+    const int b = in ? a.block_ids[b0 + j] : -1;
+    const bool cand = in && adm && pl_candidate(a, b);
+    int cnt;
+    const int crank = cand_carry + pl_rank(cand, &cnt, lds_rank);
+    cand_carry += cnt;
+    const bool sel = cand && crank < k;
+    if (in && b >= 0 && b < a.num_blocks) a.selected[b] = sel ? 1 : 0;
+    int nkeep;
+    const int krank = keep_carry + pl_rank(in && !sel, &nkeep, lds_rank);
+    keep_carry += nkeep;
+    int nsel;
+    const int srank = sel_carry + pl_rank(sel, &nsel, lds_rank);
+    sel_carry += nsel;
+    if (in && !sel && nb0 + krank < a.new_bt_capacity) a.new_block_ids[nb0 + krank] = b;
+    if (sel) a.sources[f0 + srank] = b;
+  }
+  for (int i = tid; i < need; i += kPlThreads) {
+    a.new_block_ids[nb0 + keep_carry + i] = a.free_list[d0 + i];
+  }
+  __syncthreads();  // this workgroup's selected[] entries are visible to it from here on
+
+  // move list in logical order: live tokens whose slot lies in a selected source
+  const int64_t plan0 = (int64_t)d0 * S;
+  const int64_t plan_n = (int64_t)need * S;
+  int q_carry = 0;
+  bool overflow = false;
+  for (int base = 0; base < n; base += kPlThreads) {
+    const int p = base + tid;
+    const bool in = p < n;
+    const bool lv = in && a.live[t0 + p] != 0;
+    const int s = in ? a.slot_in[t0 + p] : -1;
+    const bool valid = s >= 0 && s < a.num_slots;
+    const bool mv = adm && lv && valid && a.selected[s / S] != 0;
+    int cnt;
+    const int q = q_carry + pl_rank(mv, &cnt, lds_rank);
+    q_carry += cnt;
+    if (in) {
+      int out = lv && valid ? s : -1;
+      if (mv) {
+        if (q < plan_n) {
+          out = a.free_list[d0 + q / S] * S + q % S;
+          a.src_plan[plan0 + q] = s;
+        } else {
+          overflow = true;
+        }
+      }
+      a.token_slot[t0 + p] = out;
+    }
+  }
+  if (adm) {
+    // the moved tokens must be exactly the live tokens counted in the sources
+    const int expect = k > 0 ? a.elig_cum[b0 + k - 1] : 0;
+    if (overflow || (tid == 0 && q_carry != expect)) pl_error(a.counters, VTOKEN_ERR_SLOT);
+    for (int64_t q = q_carry + tid; q < plan_n; q += kPlThreads) a.src_plan[plan0 + q] = -1;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_planner(const PlannerArgs& a, hipStream_t stream) {
+  auto grid_for = [](int64_t n) {
+    int64_t g = (n + 255) / 256;
+    g = g < 1 ? 1 : g;
+    return static_cast<unsigned>(g < 2048 ? g : 2048);
+  };
+  hipLaunchKernelGGL(pl_clear_kernel, dim3(grid_for(a.num_blocks)), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(pl_count_kernel, dim3(grid_for((int64_t)a.num_bt_entries + a.num_tokens)),
+                     dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(pl_blocks_kernel, dim3(grid_for(a.num_blocks)), dim3(256), 0, stream, a);
+  if (a.num_reqs > 0) {
+    hipLaunchKernelGGL(pl_request_kernel, dim3(a.num_reqs), dim3(kPlThreads), 0, stream, a);
+  }
+  hipLaunchKernelGGL(pl_admit_kernel, dim3(1), dim3(kPlAdmitThreads), 0, stream, a);
+  if (a.num_reqs > 0) {
+    hipLaunchKernelGGL(pl_table_kernel, dim3(a.num_reqs), dim3(kPlThreads), 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace vtoken

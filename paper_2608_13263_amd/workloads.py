@@ -16,6 +16,7 @@ free list. Lengths are integer-uniform and inclusive. Seeds go into numpy's PCG6
 from __future__ import annotations
 
 import dataclasses
+import collections
 import math
 from typing import Callable, Dict, List, Optional, Sequence
 
@@ -90,6 +91,23 @@ class RepackInputs:
     free_list: np.ndarray   # int32 [f]
     seed: int = 0
     note: str = ""
+    # token-table inputs of the partial pass: current slot of every token (-1: none) and
+    # blocks the caller protects; None for a positional layout
+    slot_in: Optional[np.ndarray] = None   # int32 [T]
+    pinned: Optional[np.ndarray] = None    # uint8 [num_blocks]
+
+    def slots(self) -> np.ndarray:
+        """slot_in, or the positional slots block_table[p // S] * S + p % S (Sec. 3.4)."""
+        if self.slot_in is not None:
+            return self.slot_in
+        S = self.shape.block_size
+        out = np.empty(self.num_tokens, dtype=np.int32)
+        for r in range(self.num_reqs):
+            a, n = int(self.tok_indptr[r]), int(self.seq_lens[r])
+            bt = self.request_blocks(r).astype(np.int64)
+            p = np.arange(n)
+            out[a:a + n] = bt[p // S] * S + p % S
+        return out
 
     @property
     def num_reqs(self) -> int:
@@ -410,6 +428,227 @@ class ScissorhandsStream:
                                         dtype=np.int32)
         self.free = np.concatenate([self.free[int(used):],
                                     np.asarray(freed, dtype=np.int32)]).astype(np.int32)
+        self.wave += 1
+
+    def resident_blocks(self) -> int:
+        return sum(len(t) for t in self.tables)
+
+
+def token_table_inputs(seed: int = 601, shape: Optional[KVShape] = None, num_reqs: int = 64,
+                       len_range=(2048, 8192), keep: float = 0.3, recent: int = 64,
+                       shared_groups: int = 0, group_size: int = 4, prefix_tokens: int = 0,
+                       shuffled_frac: float = 0.5, dropped_frac: float = 0.1,
+                       pin_tail: bool = True, free_blocks: Optional[int] = None,
+                       name: str = "token_table") -> RepackInputs:
+    """Requests as token tables, the input of the partial pass.
+
+    Request r has L_r ~ U[len_range] logical tokens in its own blocks of a shuffled pool,
+    positional (token p at block_table[p // S] * S + p % S) except that for a fraction
+    `shuffled_frac` of requests the tokens are permuted over the occupied slots (a layout left
+    by earlier passes: token order no longer follows table order). Liveness is the Random
+    policy (keep a fraction `keep` of the evictable tokens plus the last `recent`); a fraction
+    `dropped_frac` of the dead tokens hold no slot any more (-1, their slot left empty).
+    `shared_groups` groups of `group_size` requests share their first `prefix_tokens` tokens
+    (rounded down to whole blocks): one set of blocks at the front of every member's table,
+    every member's first tokens on the same slots, liveness drawn per member. With `pin_tail`
+    each request's last table block (where decoding appends) is pinned."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    shape = shape or KVShape(2, 8, 128, 16, "bf16")
+    S = shape.block_size
+    R = int(num_reqs)
+    lens = rng.integers(len_range[0], len_range[1], size=R, endpoint=True).astype(np.int64)
+    prefix = (int(prefix_tokens) // S) * S
+    groups = []
+    members = rng.permutation(R)
+    for g in range(int(shared_groups)):
+        grp = members[g * group_size:(g + 1) * group_size]
+        if len(grp) >= 2 and prefix > 0:
+            groups.append([int(x) for x in grp])
+            lens[grp] = np.maximum(lens[grp], prefix + 1)
+    group_of = {r: gi for gi, grp in enumerate(groups) for r in grp}
+    own_blocks = [_blocks_for(int(lens[r]) - (prefix if r in group_of else 0), S)
+                  for r in range(R)]
+    M_shared = len(groups) * (prefix // S)
+    M_own = int(sum(own_blocks))
+    if free_blocks is None:
+        free_blocks = int(math.ceil(keep * M_own)) + R * (recent // S + 1) + 256
+    num_blocks = M_shared + M_own + int(free_blocks)
+    perm = rng.permutation(num_blocks).astype(np.int64)
+    o = 0
+    shared_tables = []
+    for _ in groups:
+        shared_tables.append(perm[o:o + prefix // S])
+        o += prefix // S
+    tables, slots, lives = [], [], []
+    for r in range(R):
+        n = int(lens[r])
+        own = perm[o:o + own_blocks[r]]
+        o += own_blocks[r]
+        sh = shared_tables[group_of[r]] if r in group_of else perm[:0]
+        table = np.concatenate([sh, own])
+        p0 = prefix if r in group_of else 0
+        pos = np.arange(n - p0)
+        own_slots = own[pos // S] * S + pos % S
+        if rng.random() < shuffled_frac:
+            own_slots = own_slots[rng.permutation(len(own_slots))]
+        sl = np.concatenate([sh[np.arange(p0) // S] * S + np.arange(p0) % S, own_slots])
+        lv = random_live(rng, n, keep, recent)
+        dead = np.nonzero(lv == 0)[0]
+        drop = dead[rng.random(len(dead)) < dropped_frac]
+        sl = sl.copy()
+        sl[drop] = -1
+        tables.append(table)
+        slots.append(sl)
+        lives.append(lv)
+    seq_lens = lens.astype(np.int32)
+    tok_indptr = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    bt_indptr = np.concatenate([[0], np.cumsum([len(t) for t in tables])]).astype(np.int32)
+    pinned = np.zeros(num_blocks, dtype=np.uint8)
+    if pin_tail:
+        for t in tables:
+            if len(t):
+                pinned[int(t[-1])] = 1
+    return RepackInputs(
+        name=name, shape=shape, num_blocks=num_blocks, seq_lens=seq_lens,
+        tok_indptr=tok_indptr, bt_indptr=bt_indptr,
+        block_ids=np.concatenate(tables).astype(np.int32) if tables else np.zeros(0, np.int32),
+        live=np.concatenate(lives).astype(np.uint8) if lives else np.zeros(0, np.uint8),
+        free_list=perm[o:].astype(np.int32), seed=seed,
+        slot_in=np.concatenate(slots).astype(np.int32) if slots else np.zeros(0, np.int32),
+        pinned=pinned,
+        note=f"{shape.dtype} {shape.num_layers}x{shape.num_kv_heads}x{shape.head_dim}, S={S}, "
+             f"{R} req U{list(len_range)} as token tables ({shuffled_frac:.0%} permuted), "
+             f"Random keep {keep} + last {recent}, {len(groups)} shared prefixes of {prefix} "
+             f"tokens x {group_size}")
+
+
+class PartialStream:
+    """The Scissorhands-style serving loop of ScissorhandsStream, driven by the partial pass:
+    requests are token tables, so a pass can move a few low-utilisation blocks of a request
+    and leave the rest in place.
+
+      decode()   as in ScissorhandsStream: `decode_steps` tokens appended per request (into the
+                 free slots of its append block, then blocks from the front of the free list,
+                 each becoming the append block), persistence scores, eviction to
+                 floor(budget * L) plus the window.
+      inputs()   the token tables as RepackInputs (slot_in set); every request's append block
+                 is pinned.
+      commit()   apply one pass's outputs: token slots from the new token table, tokens that
+                 lost their slot dropped, the new tables, the free list = unconsumed entries
+                 followed by the released sources.
+    The initial state is ScissorhandsStream's (same seed, same draws)."""
+
+    def __init__(self, **kw):
+        base = ScissorhandsStream(**kw)
+        self.base_kw = kw
+        self.rng = base.rng
+        self.seed = base.seed
+        self.shape = base.shape
+        self.budget, self.window, self.decode_steps = base.budget, base.window, base.decode_steps
+        self.L = base.L
+        self.pos, self.score, self.alive = base.pos, base.score, base.alive
+        self.tables = [list(int(b) for b in t) for t in base.tables]
+        self.num_blocks = base.num_blocks
+        self.free = list(int(b) for b in base.free)
+        S = self.shape.block_size
+        self.slot = []
+        self.fill = {}
+        self.tail = []
+        for pos, t in zip(self.pos, self.tables):
+            i = np.arange(len(pos))
+            tb = np.asarray(t, dtype=np.int64)
+            self.slot.append(tb[i // S] * S + i % S)
+            for j, b in enumerate(t):
+                self.fill[b] = min(S, len(pos) - j * S)
+            self.tail.append(t[-1] if t else None)
+        self.round = 0
+        self.wave = 0
+
+    def decode(self) -> None:
+        S = self.shape.block_size
+        for r in range(len(self.pos)):
+            L = int(self.L[r])
+            new_slots = []
+            for _ in range(self.decode_steps):
+                last = self.tail[r]
+                if last is None or self.fill[last] >= S:
+                    if not self.free:
+                        raise RuntimeError("pool exhausted while appending decoded tokens")
+                    last = self.free.pop(0)
+                    self.tables[r].append(last)
+                    self.fill[last] = 0
+                    self.tail[r] = last
+                new_slots.append(last * S + self.fill[last])
+                self.fill[last] += 1
+            fresh = np.arange(L, L + self.decode_steps, dtype=np.int64)
+            self.pos[r] = np.concatenate([self.pos[r], fresh])
+            self.slot[r] = np.concatenate([self.slot[r], np.asarray(new_slots, np.int64)])
+            self.score[r] = np.concatenate([self.score[r], np.zeros(len(fresh), np.int64)])
+            self.alive[r] = np.concatenate([self.alive[r], np.ones(len(fresh), dtype=bool)])
+            L += self.decode_steps
+            self.L[r] = L
+            pos, alive = self.pos[r], self.alive[r]
+            p = np.minimum(1.0, 1.0 / np.sqrt(1.0 + (L - pos)))
+            self.score[r] = self.score[r] + np.where(alive, self.rng.binomial(
+                self.decode_steps, p), 0)
+            win = alive & (pos >= L - self.window)
+            cand = np.nonzero(alive & ~win)[0]
+            k = max(int(math.floor(self.budget * L)) - int(win.sum()), 0)
+            new_alive = win.copy()
+            if k > 0 and len(cand):
+                order = np.lexsort((pos[cand], -self.score[r][cand]))
+                new_alive[cand[order[:k]]] = True
+            self.alive[r] = new_alive
+        self.round += 1
+        self.wave = 0
+
+    def inputs(self) -> RepackInputs:
+        seq_lens = np.array([len(p) for p in self.pos], dtype=np.int64)
+        tok_indptr = np.concatenate([[0], np.cumsum(seq_lens)]).astype(np.int32)
+        bt_indptr = np.concatenate([[0], np.cumsum([len(t) for t in self.tables])]).astype(
+            np.int32)
+        pinned = np.zeros(self.num_blocks, dtype=np.uint8)
+        for b in self.tail:
+            if b is not None:
+                pinned[b] = 1
+        return RepackInputs(
+            name="llama3_8b_scissorhands_partial", shape=self.shape, num_blocks=self.num_blocks,
+            seq_lens=seq_lens.astype(np.int32), tok_indptr=tok_indptr, bt_indptr=bt_indptr,
+            block_ids=np.asarray([b for t in self.tables for b in t], dtype=np.int32),
+            live=np.concatenate(self.alive).astype(np.uint8) if self.alive else
+            np.zeros(0, np.uint8),
+            free_list=np.asarray(self.free, dtype=np.int32), seed=self.seed,
+            slot_in=np.concatenate(self.slot).astype(np.int32) if self.slot else
+            np.zeros(0, np.int32),
+            pinned=pinned,
+            note=f"Scissorhands budget {self.budget} window {self.window}, {len(self.pos)} req, "
+                 f"token tables, round {self.round} wave {self.wave}")
+
+    def commit(self, token_slot, new_bt_indptr, new_block_ids, used: int, sources) -> None:
+        """Apply one partial pass's outputs (token table [T], new tables in CSR, consumed
+        free-list entries, released sources)."""
+        S = self.shape.block_size
+        a = 0
+        for r in range(len(self.pos)):
+            n = len(self.pos[r])
+            ts = np.asarray(token_slot[a:a + n], dtype=np.int64)
+            a += n
+            keep = ts >= 0
+            self.pos[r] = self.pos[r][keep]
+            self.score[r] = self.score[r][keep]
+            self.alive[r] = self.alive[r][keep]
+            self.slot[r] = ts[keep]
+            old = self.tables[r]
+            new = [int(b) for b in new_block_ids[new_bt_indptr[r]:new_bt_indptr[r + 1]]]
+            fresh = [b for b in new if b not in set(old)]
+            if fresh:
+                counts = collections.Counter(int(s) // S for s in self.slot[r])
+                for b in fresh:
+                    self.fill[b] = counts.get(b, 0)
+            self.tables[r] = new
+        for b in sources:
+            self.fill.pop(int(b), None)
+        self.free = self.free[int(used):] + [int(b) for b in sources]
         self.wave += 1
 
     def resident_blocks(self) -> int:

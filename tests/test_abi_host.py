@@ -53,7 +53,9 @@ def test_struct_layouts_match_header(tmp_path):
     if shutil.which("gcc") is None:
         pytest.skip("gcc not available")
     structs = {"vtoken_cache": B.CCache, "vtoken_batch": B.CBatch, "vtoken_plan": B.CPlan,
-               "vtoken_repack_options": B.CRepackOptions, "vtoken_decode": B.CDecode}
+               "vtoken_repack_options": B.CRepackOptions, "vtoken_decode": B.CDecode,
+               "vtoken_planner_params": B.CPlannerParams,
+               "vtoken_planner_state": B.CPlannerState}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "vtoken.h"', "int main(void){"]
     for cname, cls in structs.items():
         lines.append(f'printf("{cname} sizeof %zu\\n", sizeof({cname}));')
@@ -210,6 +212,36 @@ def test_slot_mapping_rejects_bad_arguments():
     plan.token_slot = None
     assert lib.vtoken_build_slot_mapping(ctypes.byref(batch), ctypes.byref(plan), p, p, 40,
                                          None) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
+
+
+def test_plan_partial_rejects_bad_arguments():
+    lib = B.load_library()
+    cache, batch, plan = _good()
+    p = _fake_ptr()
+    st = B.CPlannerState(p, p, p, p, p, p, p, p, None)
+    good = B.PlannerParams().c()
+
+    def call(c=cache, prm=good, s=st, pl=plan, slot=p):
+        return lib.vtoken_plan_partial(ctypes.byref(c), ctypes.byref(batch), slot,
+                                       ctypes.byref(prm), ctypes.byref(s), ctypes.byref(pl),
+                                       None)
+    bad = B.PlannerParams(theta=(1, 0)).c()
+    assert call(prm=bad) == B.STATUS_CODE["VTOKEN_ERR_ARGUMENT"]
+    bad = B.PlannerParams(max_sources=-1).c()
+    assert call(prm=bad) == B.STATUS_CODE["VTOKEN_ERR_ARGUMENT"]
+    bad = B.PlannerParams(min_eligible=-2).c()
+    assert call(prm=bad) == B.STATUS_CODE["VTOKEN_ERR_ARGUMENT"]
+    big = B.CCache(p, 2, 8, 128, 128, 100, 2)          # block_size 128 > 64
+    assert call(c=big) == B.STATUS_CODE["VTOKEN_ERR_SHAPE"]
+    assert call(slot=None) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    s2 = B.CPlannerState(p, p, p, p, None, p, p, p, None)
+    assert call(s=s2) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    s3 = B.CPlannerState(p, p, p, p, p, p, p, None, None)
+    assert call(s=s3) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    small = B.CPlan(p, p, p, p, p, p, p, p, p, 3, 4 * 16)
+    assert call(pl=small) == B.STATUS_CODE["VTOKEN_ERR_CAPACITY"]
+    small = B.CPlan(p, p, p, p, p, p, p, p, p, 4, 4 * 16 - 1)
+    assert call(pl=small) == B.STATUS_CODE["VTOKEN_ERR_CAPACITY"]
 
 
 def test_binding_fails_loudly_without_library(tmp_path):

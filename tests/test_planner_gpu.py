@@ -1,0 +1,244 @@
+"""The partial reclamation pass (vtoken_plan_partial + vtoken_repack) through the C ABI
+against the CPU oracle of oracle/planner.py: every output bit-exact (per-block n_b and
+reference counts, the statistics, sources considered, admission, CSR offsets, token table,
+new tables, source plan, released sources) and every KV byte after the copy."""
+import numpy as np
+import pytest
+
+from gpu_helpers import kv_bytes, torch
+from oracle.planner import PlannerParams as OracleParams
+from oracle.planner import plan_partial
+from oracle.repack import oracle_repack_inputs
+from paper_2608_13263_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _B():
+    from paper_2608_13263_amd import binding as B
+    return B
+
+
+def gpu_partial(inp, kv, params=None, label=""):
+    t = torch()
+    B = _B()
+    sh = inp.shape
+    params = params or B.PlannerParams()
+    print(f"[gpu] partial {label or inp.name}: R={inp.num_reqs} T={inp.num_tokens} "
+          f"M={inp.num_bt_entries} f={len(inp.free_list)} S={sh.block_size} theta={params.theta} "
+          f"B={params.max_sources} wm={params.free_watermark}", flush=True)
+    cache = B.KVCache(kv, sh.num_layers, sh.num_kv_heads, sh.head_dim, sh.block_size)
+    batch = B.Batch.from_inputs(inp)
+    slot_in = t.from_numpy(np.ascontiguousarray(inp.slots(), dtype=np.int32)).cuda()
+    plan = B.Plan.allocate(batch, sh.block_size)
+    state = B.PlannerState.allocate(inp.num_blocks, batch, pinned=inp.pinned)
+    B.plan_partial(cache, batch, slot_in, plan, state, params)
+    B.repack(cache, batch, plan)
+    t.cuda.synchronize()
+    h = {k: getattr(plan, k).cpu().numpy() for k in plan.FIELDS}
+    for k in state.FIELDS:
+        h[k] = getattr(state, k).cpu().numpy()
+    R, T = inp.num_reqs, inp.num_tokens
+    used, n_adm, n_freed, status = (int(x) for x in h["counters"][:4])
+    out = dict(status=status, used=used, n_admitted=n_adm, n_freed=n_freed)
+    if status != 0:
+        return out
+    out.update(token_slot=h["token_slot"][:T], live_count=h["live_count"][:R],
+               admitted=h["admitted"][:R], src_count=h["src_count"][:R],
+               dst_indptr=h["dst_indptr"][:R + 1], new_bt_indptr=h["new_bt_indptr"][:R + 1],
+               freed_indptr=h["freed_indptr"][:R + 1], src_plan=h["src_plan"][:used * sh.block_size],
+               freed=h["sources"][:n_freed], stats=h["stats"][:8], n_b=h["n_b"],
+               refs=h["refs"])
+    out["new_block_ids"] = h["new_block_ids"][:int(out["new_bt_indptr"][-1])] if R else \
+        h["new_block_ids"][:0]
+    return out
+
+
+def oracle_params(p):
+    return OracleParams(theta_num=p.theta[0], theta_den=p.theta[1],
+                        max_live_per_source=None if p.max_live_per_source < 0
+                        else p.max_live_per_source,
+                        max_sources=p.max_sources, min_eligible=p.min_eligible,
+                        free_watermark=p.free_watermark)
+
+
+def run_oracle(inp, kv_host, params):
+    return plan_partial(inp.seq_lens, inp.tok_indptr, inp.bt_indptr, inp.block_ids, inp.live,
+                        inp.slots(), inp.free_list, inp.shape.block_size, inp.num_blocks,
+                        oracle_params(params), pinned=inp.pinned, kv=kv_host)
+
+
+def assert_partial_equal(g, o, inp):
+    assert g["status"] == 0, f"device status {g['status']}"
+    assert g["used"] == o.used and g["n_admitted"] == o.n_admitted and g["n_freed"] == o.n_freed
+    stats = [o.live_total, o.allocated, o.eligible, int(o.triggered),
+             int(o.src_count.sum()), o.tokens_moved, o.n_freed, o.used]
+    assert [int(x) for x in g["stats"]] == stats, (list(g["stats"]), stats)
+    for key in ("token_slot", "live_count", "admitted", "src_count", "dst_indptr",
+                "new_bt_indptr", "new_block_ids", "src_plan", "freed_indptr", "freed"):
+        a = np.asarray(g[key], dtype=np.int64)
+        b = np.asarray(getattr(o, key), dtype=np.int64)
+        assert a.shape == b.shape, f"{key}: shape {a.shape} vs oracle {b.shape}"
+        if not np.array_equal(a, b):
+            bad = np.nonzero(a != b)[0]
+            raise AssertionError(f"{key}: {len(bad)} mismatches, first at {bad[:5]}: "
+                                 f"gpu {a[bad[:5]]} oracle {b[bad[:5]]}")
+    for b, n in o.n_b.items():
+        assert int(g["n_b"][b]) == n, f"n_b[{b}]"
+        assert int(g["refs"][b]) == o.refs[b], f"refs[{b}]"
+
+
+def partial_parity(inp, params=None, seed=0, label=""):
+    t = torch()
+    B = _B()
+    params = params or B.PlannerParams()
+    kv = W.kv_device(inp.shape, inp.num_blocks, seed)
+    before = kv_bytes(kv, inp.shape)
+    o = run_oracle(inp, before, params)
+    g = gpu_partial(inp, kv, params, label)
+    assert_partial_equal(g, o, inp)
+    after = kv_bytes(kv, inp.shape)
+    if not np.array_equal(after, o.kv):
+        diff = np.nonzero((after != o.kv).any(axis=2))
+        raise AssertionError(f"KV bytes differ in {len(diff[0])} rows")
+    del kv
+    t.cuda.empty_cache()
+    return g, o
+
+
+CASES = {
+    "tiny_shared": lambda: W.token_table_inputs(
+        611, W.KVShape(1, 2, 64, 16, "fp16"), num_reqs=8, len_range=(100, 500),
+        shared_groups=1, group_size=3, prefix_tokens=64),
+    "llama3_8b_shared": lambda: W.token_table_inputs(
+        612, W.KVShape(2, 8, 128, 16, "bf16"), num_reqs=32, len_range=(600, 3000),
+        shared_groups=3, group_size=4, prefix_tokens=512),
+    "llama3_70b_fp8": lambda: W.token_table_inputs(
+        613, W.KVShape(2, 8, 128, 32, "fp8_e4m3"), num_reqs=6, len_range=(2000, 9000),
+        keep=0.3, recent=128),
+    "block_64": lambda: W.token_table_inputs(
+        614, W.KVShape(1, 4, 64, 64, "bf16"), num_reqs=10, len_range=(300, 2000),
+        shared_groups=1, group_size=2, prefix_tokens=128),
+    "block_1": lambda: W.token_table_inputs(
+        615, W.KVShape(1, 2, 32, 1, "fp16"), num_reqs=6, len_range=(20, 300)),
+    "positional": lambda: W.token_table_inputs(
+        616, W.KVShape(1, 2, 64, 16, "fp16"), num_reqs=12, len_range=(100, 900),
+        shuffled_frac=0.0, dropped_frac=0.0, pin_tail=False),
+    "many_requests": lambda: W.token_table_inputs(
+        617, W.KVShape(1, 1, 64, 4, "fp16"), num_reqs=1500, len_range=(1, 60), recent=4,
+        shared_groups=20, group_size=3, prefix_tokens=8),
+}
+
+
+@pytest.mark.parametrize("case", sorted(CASES))
+def test_partial_parity_default_params(case):
+    g, o = partial_parity(CASES[case](), label=case)
+    print(f"[gpu] {case}: triggered={o.triggered} admitted={o.n_admitted} moved={o.tokens_moved} "
+          f"released={o.n_freed}", flush=True)
+
+
+@pytest.mark.parametrize("params", [
+    dict(max_sources=5), dict(max_sources=0), dict(max_sources=37),
+    dict(theta=(99, 100)), dict(theta=(0, 1)), dict(free_watermark=0),
+    dict(free_watermark=100000), dict(min_eligible=100000), dict(max_live_per_source=2),
+    dict(max_live_per_source=0), dict(theta=(-1, 1), max_live_per_source=16, min_eligible=0),
+], ids=lambda d: ",".join(f"{k}={v}" for k, v in d.items()))
+def test_partial_parity_params(params):
+    B = _B()
+    inp = W.token_table_inputs(621, W.KVShape(1, 2, 64, 16, "bf16"), num_reqs=16,
+                               len_range=(200, 1500), shared_groups=2, group_size=3,
+                               prefix_tokens=96)
+    partial_parity(inp, B.PlannerParams(**params), label=str(params))
+
+
+def test_partial_pool_short_defers():
+    B = _B()
+    inp = W.token_table_inputs(622, W.KVShape(1, 2, 64, 16, "fp16"), num_reqs=12,
+                               len_range=(300, 1200), free_blocks=30)
+    g, o = partial_parity(inp, B.PlannerParams(), label="short pool")
+    assert 0 < o.n_admitted < int((o.src_count > 0).sum())
+
+
+def test_partial_forced_equals_full_pass():
+    """Every block a candidate, no bound, trigger forced, positional layout: the partial pass
+    must give the full pass's outputs on the GPU too."""
+    t = torch()
+    B = _B()
+    inp = W.token_table_inputs(623, W.KVShape(2, 4, 64, 16, "bf16"), num_reqs=10,
+                               len_range=(100, 900), shuffled_frac=0.0, dropped_frac=0.0,
+                               pin_tail=False)
+    prm = B.PlannerParams(theta=(-1, 1), max_live_per_source=16, min_eligible=0)
+    g, _ = partial_parity(inp, prm, seed=4, label="forced")
+    kv = W.kv_device(inp.shape, inp.num_blocks, 4)
+    before = kv_bytes(kv, inp.shape)
+    full = oracle_repack_inputs(inp, before)
+    for key in ("token_slot", "admitted", "new_bt_indptr", "new_block_ids", "src_plan",
+                "freed_indptr", "freed"):
+        assert np.array_equal(np.asarray(g[key], np.int64),
+                              np.asarray(getattr(full, key), np.int64)), key
+    del kv
+    t.cuda.empty_cache()
+
+
+def test_partial_chained_passes():
+    """Pass 2 runs on the token tables pass 1 left (non-positional), as a serving loop does."""
+    t = torch()
+    B = _B()
+    inp = W.token_table_inputs(624, W.KVShape(1, 2, 64, 16, "bf16"), num_reqs=20,
+                               len_range=(300, 2000), shared_groups=2, group_size=3,
+                               prefix_tokens=64)
+    kv = W.kv_device(inp.shape, inp.num_blocks, 6)
+    for step in range(3):
+        before = kv_bytes(kv, inp.shape)
+        prm = B.PlannerParams(max_sources=40)
+        o = run_oracle(inp, before, prm)
+        g = gpu_partial(inp, kv, prm, label=f"chained pass {step}")
+        assert_partial_equal(g, o, inp)
+        assert np.array_equal(kv_bytes(kv, inp.shape), o.kv)
+        # next state: the new token table and tables; evict a few more tokens
+        rng = np.random.default_rng(step)
+        live = inp.live.copy()
+        live[(rng.random(len(live)) < 0.1)] = 0
+        slot = np.asarray(g["token_slot"], np.int32)
+        slot[(live == 0) & (rng.random(len(live)) < 0.5)] = -1
+        used = g["used"]
+        inp = W.RepackInputs(
+            name=inp.name, shape=inp.shape, num_blocks=inp.num_blocks, seq_lens=inp.seq_lens,
+            tok_indptr=inp.tok_indptr, bt_indptr=np.asarray(g["new_bt_indptr"], np.int32),
+            block_ids=np.asarray(g["new_block_ids"], np.int32), live=live,
+            free_list=np.concatenate([inp.free_list[used:], g["freed"]]).astype(np.int32),
+            seed=inp.seed, slot_in=slot, pinned=inp.pinned)
+    del kv
+    t.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("fault", ["slot_range", "duplicate_slot", "block_range"])
+def test_partial_device_errors(fault):
+    """Inconsistent token tables set the status word; the copy then writes nothing."""
+    t = torch()
+    B = _B()
+    inp = W.token_table_inputs(625, W.KVShape(1, 2, 64, 16, "fp16"), num_reqs=6,
+                               len_range=(100, 400), pin_tail=False)
+    slot = inp.slots().copy()
+    live = inp.live
+    first_live = np.nonzero(live)[0]
+    code = "VTOKEN_ERR_SLOT"
+    if fault == "slot_range":
+        slot[first_live[3]] = inp.num_blocks * inp.shape.block_size + 5
+    elif fault == "duplicate_slot":
+        a, b = first_live[1], first_live[2]       # same request: its first live tokens
+        slot[b] = slot[a]
+    else:
+        inp.block_ids = inp.block_ids.copy()
+        inp.block_ids[2] = inp.num_blocks + 3
+        code = "VTOKEN_ERR_BLOCK_RANGE"
+    inp.slot_in = slot
+    kv = W.kv_device(inp.shape, inp.num_blocks, 8)
+    before = kv_bytes(kv, inp.shape)
+    # an attempt is forced so that the duplicate slot lands in a source
+    prm = B.PlannerParams(theta=(-1, 1), max_live_per_source=16, min_eligible=0)
+    g = gpu_partial(inp, kv, prm, label=f"fault {fault}")
+    assert g["status"] == B.STATUS_CODE[code], (g["status"], code)
+    assert np.array_equal(kv_bytes(kv, inp.shape), before), "KV written despite the error"
+    del kv
+    t.cuda.empty_cache()
