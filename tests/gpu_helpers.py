@@ -4,6 +4,8 @@ from __future__ import annotations
 
 import numpy as np
 
+from oracle.planner import PlannerParams as OracleParams
+from oracle.planner import plan_partial
 from oracle.repack import oracle_repack_inputs
 from paper_2608_13263_amd import workloads as W
 
@@ -99,3 +101,74 @@ def full_parity(inp: W.RepackInputs, seed: int = 0, variant=0, grid=0, order=0,
     del kv
     t.cuda.empty_cache()
     return gpu, orc
+
+
+def gpu_partial(inp, kv, params=None, label=""):
+    """plan_partial -> repack on the current stream; host copies of every output, trimmed
+    to the sizes the counters report."""
+    t = torch()
+    from paper_2608_13263_amd import binding as B
+    sh = inp.shape
+    params = params or B.PlannerParams()
+    print(f"[gpu] partial {label or inp.name}: R={inp.num_reqs} T={inp.num_tokens} "
+          f"M={inp.num_bt_entries} f={len(inp.free_list)} S={sh.block_size} theta={params.theta} "
+          f"B={params.max_sources} wm={params.free_watermark}", flush=True)
+    cache = B.KVCache(kv, sh.num_layers, sh.num_kv_heads, sh.head_dim, sh.block_size)
+    batch = B.Batch.from_inputs(inp)
+    slot_in = t.from_numpy(np.ascontiguousarray(inp.slots(), dtype=np.int32)).cuda()
+    plan = B.Plan.allocate(batch, sh.block_size)
+    state = B.PlannerState.allocate(inp.num_blocks, batch, pinned=inp.pinned)
+    B.plan_partial(cache, batch, slot_in, plan, state, params)
+    B.repack(cache, batch, plan)
+    t.cuda.synchronize()
+    h = {k: getattr(plan, k).cpu().numpy() for k in plan.FIELDS}
+    for k in state.FIELDS:
+        h[k] = getattr(state, k).cpu().numpy()
+    R, T = inp.num_reqs, inp.num_tokens
+    used, n_adm, n_freed, status = (int(x) for x in h["counters"][:4])
+    out = dict(status=status, used=used, n_admitted=n_adm, n_freed=n_freed)
+    if status != 0:
+        return out
+    out.update(token_slot=h["token_slot"][:T], live_count=h["live_count"][:R],
+               admitted=h["admitted"][:R], src_count=h["src_count"][:R],
+               dst_indptr=h["dst_indptr"][:R + 1], new_bt_indptr=h["new_bt_indptr"][:R + 1],
+               freed_indptr=h["freed_indptr"][:R + 1], src_plan=h["src_plan"][:used * sh.block_size],
+               freed=h["sources"][:n_freed], stats=h["stats"][:8], n_b=h["n_b"],
+               refs=h["refs"])
+    out["new_block_ids"] = h["new_block_ids"][:int(out["new_bt_indptr"][-1])] if R else \
+        h["new_block_ids"][:0]
+    return out
+
+
+def oracle_params(p):
+    return OracleParams(theta_num=p.theta[0], theta_den=p.theta[1],
+                        max_live_per_source=None if p.max_live_per_source < 0
+                        else p.max_live_per_source,
+                        max_sources=p.max_sources, min_eligible=p.min_eligible,
+                        free_watermark=p.free_watermark)
+
+
+def run_partial_oracle(inp, kv_host, params):
+    return plan_partial(inp.seq_lens, inp.tok_indptr, inp.bt_indptr, inp.block_ids, inp.live,
+                        inp.slots(), inp.free_list, inp.shape.block_size, inp.num_blocks,
+                        oracle_params(params), pinned=inp.pinned, kv=kv_host)
+
+
+def assert_partial_equal(g, o, inp):
+    assert g["status"] == 0, f"device status {g['status']}"
+    assert g["used"] == o.used and g["n_admitted"] == o.n_admitted and g["n_freed"] == o.n_freed
+    stats = [o.live_total, o.allocated, o.eligible, int(o.triggered),
+             int(o.src_count.sum()), o.tokens_moved, o.n_freed, o.used]
+    assert [int(x) for x in g["stats"]] == stats, (list(g["stats"]), stats)
+    for key in ("token_slot", "live_count", "admitted", "src_count", "dst_indptr",
+                "new_bt_indptr", "new_block_ids", "src_plan", "freed_indptr", "freed"):
+        a = np.asarray(g[key], dtype=np.int64)
+        b = np.asarray(getattr(o, key), dtype=np.int64)
+        assert a.shape == b.shape, f"{key}: shape {a.shape} vs oracle {b.shape}"
+        if not np.array_equal(a, b):
+            bad = np.nonzero(a != b)[0]
+            raise AssertionError(f"{key}: {len(bad)} mismatches, first at {bad[:5]}: "
+                                 f"gpu {a[bad[:5]]} oracle {b[bad[:5]]}")
+    for b, n in o.n_b.items():
+        assert int(g["n_b"][b]) == n, f"n_b[{b}]"
+        assert int(g["refs"][b]) == o.refs[b], f"refs[{b}]"

@@ -13,7 +13,8 @@ import gc
 import numpy as np
 import pytest
 
-from gpu_helpers import assert_kv_equal, assert_plan_equal, gpu_pass, torch
+from gpu_helpers import (assert_kv_equal, assert_partial_equal, assert_plan_equal, gpu_partial,
+                         gpu_pass, run_partial_oracle, torch)
 from oracle.repack import oracle_repack_inputs
 from paper_2608_13263_amd import workloads as W
 
@@ -159,6 +160,52 @@ def test_llama3_8b_scissorhands_rounds_with_waves():
                 break
         assert wave >= 1, "the pool should force at least two passes per round"
     assert total_moved > 0
+    del kv
+    gc.collect()
+    t.cuda.empty_cache()
+
+
+def test_llama3_8b_scissorhands_partial_rounds():
+    """The same loop driven by the partial pass at full size (token tables, append blocks
+    pinned, theta_F = 0.25): rounds until a pass is attempted and admits requests. Every
+    pass's GPU outputs equal the oracle's; the sampled planes equal the oracle's bytes
+    (tracked on the host); every plane passes the row-checksum check of the moves."""
+    t = torch()
+    from paper_2608_13263_amd import binding as B
+    budget = min(240 * 2 ** 30, int(0.85 * _budget()))
+    shape = W.KVShape(32, 8, 128, 16, "bf16")
+    stream = W.PartialStream(seed=401, pool_blocks=int(budget // shape.block_bytes))
+    sample = [0, 40, 63]
+    kv = W.kv_device(shape, stream.num_blocks, 5)
+    host = np.stack([_plane_bytes(kv, p, shape).cpu().numpy() for p in sample])
+    params = B.PlannerParams()
+    moved_total = 0
+    for rnd in range(6):
+        stream.decode()
+        for wave in range(8):
+            inp = stream.inputs()
+            orc_meta = run_partial_oracle(inp, None, params)
+            before = t.stack([_row_sums(kv, p, shape) for p in range(shape.num_planes)])
+            gpu = gpu_partial(inp, kv, params, label=f"round {rnd} wave {wave}")
+            assert_partial_equal(gpu, orc_meta, inp)
+            orc = run_partial_oracle(inp, host, params)
+            host = orc.kv
+            post = np.stack([_plane_bytes(kv, p, shape).cpu().numpy() for p in sample])
+            assert_kv_equal(post, host)
+            _check_all_planes(kv, before, False, orc_meta, inp)
+            del before
+            moved_total += orc_meta.tokens_moved
+            print(f"[gpu] partial round {rnd} wave {wave}: F {1 - orc_meta.live_total / (16 * max(orc_meta.allocated, 1)):.3f}, "
+                  f"attempted {orc_meta.triggered}, {orc_meta.n_admitted} admitted, "
+                  f"{orc_meta.tokens_moved} tokens moved, {orc_meta.n_freed} released",
+                  flush=True)
+            stream.commit(orc_meta.token_slot, orc_meta.new_bt_indptr, orc_meta.new_block_ids,
+                          orc_meta.used, orc_meta.freed)
+            if orc_meta.n_admitted == 0:
+                break
+        if moved_total > 0:
+            break
+    assert moved_total > 0, "no round triggered the partial pass"
     del kv
     gc.collect()
     t.cuda.empty_cache()

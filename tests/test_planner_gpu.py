@@ -5,9 +5,7 @@ new tables, source plan, released sources) and every KV byte after the copy."""
 import numpy as np
 import pytest
 
-from gpu_helpers import kv_bytes, torch
-from oracle.planner import PlannerParams as OracleParams
-from oracle.planner import plan_partial
+from gpu_helpers import assert_partial_equal, gpu_partial, kv_bytes, run_partial_oracle, torch
 from oracle.repack import oracle_repack_inputs
 from paper_2608_13263_amd import workloads as W
 
@@ -19,82 +17,13 @@ def _B():
     return B
 
 
-def gpu_partial(inp, kv, params=None, label=""):
-    t = torch()
-    B = _B()
-    sh = inp.shape
-    params = params or B.PlannerParams()
-    print(f"[gpu] partial {label or inp.name}: R={inp.num_reqs} T={inp.num_tokens} "
-          f"M={inp.num_bt_entries} f={len(inp.free_list)} S={sh.block_size} theta={params.theta} "
-          f"B={params.max_sources} wm={params.free_watermark}", flush=True)
-    cache = B.KVCache(kv, sh.num_layers, sh.num_kv_heads, sh.head_dim, sh.block_size)
-    batch = B.Batch.from_inputs(inp)
-    slot_in = t.from_numpy(np.ascontiguousarray(inp.slots(), dtype=np.int32)).cuda()
-    plan = B.Plan.allocate(batch, sh.block_size)
-    state = B.PlannerState.allocate(inp.num_blocks, batch, pinned=inp.pinned)
-    B.plan_partial(cache, batch, slot_in, plan, state, params)
-    B.repack(cache, batch, plan)
-    t.cuda.synchronize()
-    h = {k: getattr(plan, k).cpu().numpy() for k in plan.FIELDS}
-    for k in state.FIELDS:
-        h[k] = getattr(state, k).cpu().numpy()
-    R, T = inp.num_reqs, inp.num_tokens
-    used, n_adm, n_freed, status = (int(x) for x in h["counters"][:4])
-    out = dict(status=status, used=used, n_admitted=n_adm, n_freed=n_freed)
-    if status != 0:
-        return out
-    out.update(token_slot=h["token_slot"][:T], live_count=h["live_count"][:R],
-               admitted=h["admitted"][:R], src_count=h["src_count"][:R],
-               dst_indptr=h["dst_indptr"][:R + 1], new_bt_indptr=h["new_bt_indptr"][:R + 1],
-               freed_indptr=h["freed_indptr"][:R + 1], src_plan=h["src_plan"][:used * sh.block_size],
-               freed=h["sources"][:n_freed], stats=h["stats"][:8], n_b=h["n_b"],
-               refs=h["refs"])
-    out["new_block_ids"] = h["new_block_ids"][:int(out["new_bt_indptr"][-1])] if R else \
-        h["new_block_ids"][:0]
-    return out
-
-
-def oracle_params(p):
-    return OracleParams(theta_num=p.theta[0], theta_den=p.theta[1],
-                        max_live_per_source=None if p.max_live_per_source < 0
-                        else p.max_live_per_source,
-                        max_sources=p.max_sources, min_eligible=p.min_eligible,
-                        free_watermark=p.free_watermark)
-
-
-def run_oracle(inp, kv_host, params):
-    return plan_partial(inp.seq_lens, inp.tok_indptr, inp.bt_indptr, inp.block_ids, inp.live,
-                        inp.slots(), inp.free_list, inp.shape.block_size, inp.num_blocks,
-                        oracle_params(params), pinned=inp.pinned, kv=kv_host)
-
-
-def assert_partial_equal(g, o, inp):
-    assert g["status"] == 0, f"device status {g['status']}"
-    assert g["used"] == o.used and g["n_admitted"] == o.n_admitted and g["n_freed"] == o.n_freed
-    stats = [o.live_total, o.allocated, o.eligible, int(o.triggered),
-             int(o.src_count.sum()), o.tokens_moved, o.n_freed, o.used]
-    assert [int(x) for x in g["stats"]] == stats, (list(g["stats"]), stats)
-    for key in ("token_slot", "live_count", "admitted", "src_count", "dst_indptr",
-                "new_bt_indptr", "new_block_ids", "src_plan", "freed_indptr", "freed"):
-        a = np.asarray(g[key], dtype=np.int64)
-        b = np.asarray(getattr(o, key), dtype=np.int64)
-        assert a.shape == b.shape, f"{key}: shape {a.shape} vs oracle {b.shape}"
-        if not np.array_equal(a, b):
-            bad = np.nonzero(a != b)[0]
-            raise AssertionError(f"{key}: {len(bad)} mismatches, first at {bad[:5]}: "
-                                 f"gpu {a[bad[:5]]} oracle {b[bad[:5]]}")
-    for b, n in o.n_b.items():
-        assert int(g["n_b"][b]) == n, f"n_b[{b}]"
-        assert int(g["refs"][b]) == o.refs[b], f"refs[{b}]"
-
-
 def partial_parity(inp, params=None, seed=0, label=""):
     t = torch()
     B = _B()
     params = params or B.PlannerParams()
     kv = W.kv_device(inp.shape, inp.num_blocks, seed)
     before = kv_bytes(kv, inp.shape)
-    o = run_oracle(inp, before, params)
+    o = run_partial_oracle(inp, before, params)
     g = gpu_partial(inp, kv, params, label)
     assert_partial_equal(g, o, inp)
     after = kv_bytes(kv, inp.shape)
@@ -191,7 +120,7 @@ def test_partial_chained_passes():
     for step in range(3):
         before = kv_bytes(kv, inp.shape)
         prm = B.PlannerParams(max_sources=40)
-        o = run_oracle(inp, before, prm)
+        o = run_partial_oracle(inp, before, prm)
         g = gpu_partial(inp, kv, prm, label=f"chained pass {step}")
         assert_partial_equal(g, o, inp)
         assert np.array_equal(kv_bytes(kv, inp.shape), o.kv)
@@ -242,3 +171,41 @@ def test_partial_device_errors(fault):
     assert np.array_equal(kv_bytes(kv, inp.shape), before), "KV written despite the error"
     del kv
     t.cuda.empty_cache()
+
+
+def test_two_cache_groups_share_liveness():
+    """Multiple KV-cache groups (Sec. 6): one liveness state, group-specific placement. Two
+    pools with their own geometry, block tables and token tables are reclaimed with the same
+    live mask on the device; each group matches the oracle run on its own placement."""
+    t = torch()
+    B = _B()
+    a = W.token_table_inputs(631, W.KVShape(2, 8, 128, 16, "bf16"), num_reqs=12,
+                             len_range=(400, 2000), shared_groups=1, group_size=3,
+                             prefix_tokens=128)
+    # group b: same requests and liveness, another pool (4 KV heads of 64, block 32)
+    b = W.token_table_inputs(632, W.KVShape(1, 4, 64, 32, "fp16"), num_reqs=12,
+                             len_range=(400, 2000))
+    b.seq_lens, b.tok_indptr, b.live = a.seq_lens, a.tok_indptr, a.live
+    b_slots = []
+    S = b.shape.block_size
+    # lay group b out positionally over fresh tables sized for the shared lengths
+    rng = np.random.default_rng(5)
+    nb = sum(-(-int(n) // S) for n in a.seq_lens) + 256
+    perm = rng.permutation(nb).astype(np.int32)
+    o, tables = 0, []
+    for n in a.seq_lens:
+        m = -(-int(n) // S)
+        tables.append(perm[o:o + m])
+        p = np.arange(int(n))
+        b_slots.append(perm[o:o + m][p // S].astype(np.int64) * S + p % S)
+        o += m
+    b.num_blocks = nb
+    b.bt_indptr = np.concatenate([[0], np.cumsum([len(x) for x in tables])]).astype(np.int32)
+    b.block_ids = np.concatenate(tables).astype(np.int32)
+    b.free_list = perm[o:].copy()
+    b.slot_in = np.concatenate(b_slots).astype(np.int32)
+    b.pinned = None
+    b.slot_in[a.live == 0] = np.where(rng.random(int((a.live == 0).sum())) < 0.1, -1,
+                                      b.slot_in[a.live == 0])
+    for inp, seed in ((a, 1), (b, 2)):
+        partial_parity(inp, B.PlannerParams(), seed=seed, label=f"group {inp.shape.dtype}")
