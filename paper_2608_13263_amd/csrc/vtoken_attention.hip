@@ -5,14 +5,17 @@
 //   slot_map_kernel      one workgroup per request: wave-ballot compaction of token_slot,
 //                        the live tokens' slots in logical order (Sec. 3.4: the slot mapping
 //                        is built through the token table, once per token)
-//   decode_split_kernel  one workgroup per (request, KV head, split of 2048*8/D tokens):
-//                        scores of the G query heads that share the KV head, split-local
-//                        softmax, partial weighted sum of V (flash-decoding partials)
+//   decode_split_kernel  one workgroup per (request, KV head, split of 16384/D tokens):
+//                        scores of the G query heads that share the KV head on the matrix
+//                        cores, split-local softmax, partial weighted sum of V on the vector
+//                        ALUs (flash-decoding partials)
 //   decode_combine_kernel  one workgroup per (request, query head): merges the splits
 //
-// Decode attention is HBM-bound (about 2G flops per byte of K/V), so the dot products run on
-// the fp32 vector ALUs; a head's D elements are read by D/8 consecutive lanes, 8 elements
-// (16 bytes of fp16 / bf16, 8 of fp8) each.
+// Decode attention is HBM-bound up to GQA groups of about 4 (2G flops per byte of K/V);
+// the score product is a small dense contraction (16 tokens x D x the G heads of a KV head)
+// and runs on MFMA, which leaves the vector ALUs to the softmax and the weighted V sum, where
+// a head's D elements are read by D/8 consecutive lanes, 8 elements (16 bytes of fp16 / bf16,
+// 8 of fp8) each.
 #include <math.h>
 
 #include "vtoken_internal.h"
@@ -146,47 +149,84 @@ __device__ __forceinline__ void piece_to_float(typename Piece<kKind>::type w, fl
   }
 }
 
-// Sum over each aligned group of kLanes (4, 8, 16 or 32) lanes, the result in every lane of
-// the group: DPP lane permutations inside a row of 16 (swap neighbours, swap pairs, mirrored
-// half-row, mirrored row), then one cross-row exchange for 32.
-template <int kLanes>
-__device__ __forceinline__ float group_sum(float x) {
-  auto dpp = [](float v, int ctrl) -> float {
-    const int i = __builtin_bit_cast(int, v);
-    int o;
-    switch (ctrl) {
-      case 0: o = __builtin_amdgcn_update_dpp(0, i, 0xB1, 0xF, 0xF, false); break;   // [1,0,3,2]
-      case 1: o = __builtin_amdgcn_update_dpp(0, i, 0x4E, 0xF, 0xF, false); break;   // [2,3,0,1]
-      case 2: o = __builtin_amdgcn_update_dpp(0, i, 0x141, 0xF, 0xF, false); break;  // half mirror
-      default: o = __builtin_amdgcn_update_dpp(0, i, 0x140, 0xF, 0xF, false); break; // mirror
-    }
-    return __builtin_bit_cast(float, o);
-  };
-  x += dpp(x, 0);
-  x += dpp(x, 1);
-  if constexpr (kLanes >= 8) x += dpp(x, 2);
-  if constexpr (kLanes >= 16) x += dpp(x, 3);
-  if constexpr (kLanes >= 32) x += __shfl_xor(x, 16, 64);
-  return x;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// The matrix-core operand type of the scores: fp16 caches multiply in fp16, bf16 and fp8
+// caches in bf16 (every e4m3 value is exact in bf16).
+template <int kKind>
+struct ScoreOp {
+  typedef bf16x8 type;
+  typedef __bf16 elem;
+};
+template <>
+struct ScoreOp<0> {
+  typedef f16x8 type;
+  typedef _Float16 elem;
+};
+
+template <int kKind>
+__device__ __forceinline__ f32x4 score_mfma(typename ScoreOp<kKind>::type k,
+                                            typename ScoreOp<kKind>::type q, f32x4 acc) {
+  if constexpr (kKind == 0) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(k, q, acc, 0, 0, 0);
+  } else {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(k, q, acc, 0, 0, 0);
+  }
 }
 
-// kKind: element type; kLanes: lanes per head row (head_dim / 8); kG: query heads per KV
-// head (GQA group), at most 8.
+// Eight K elements as a matrix-core operand: the 16 loaded bytes as they are (fp16, bf16), or
+// 8 fp8 bytes widened to bf16 by the gfx950 conversion instruction (scale 1).
+template <int kKind>
+__device__ __forceinline__ typename ScoreOp<kKind>::type k_operand(
+    typename Piece<kKind>::type w) {
+  if constexpr (kKind == 2) {
+    bf16x8 o;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const bf16x2 a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(static_cast<int>(w[i]), 1.f,
+                                                                 false);
+      const bf16x2 b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(static_cast<int>(w[i]), 1.f,
+                                                                 true);
+      o[4 * i] = a.x;
+      o[4 * i + 1] = a.y;
+      o[4 * i + 2] = b.x;
+      o[4 * i + 3] = b.y;
+    }
+    return o;
+  } else {
+    return __builtin_bit_cast(typename ScoreOp<kKind>::type, w);
+  }
+}
+
+// kKind: element type; kD: head_dim (32, 64, 128, 256); kG: query heads per KV head (1-8).
 //
-// One workgroup covers kSplit = 8 * 256 / kLanes tokens of one (request, KV head). Every
-// thread first issues all of its loads: the slots of its 8 tokens, then the K piece and the V
-// piece of each (16 loads in flight per thread); then it computes the scores, the
-// split-local softmax and the weighted V sum from registers.
-template <int kKind, int kLanes, int kG>
+// One workgroup (4 waves) covers kSplit = 16384 / kD tokens of one (request, KV head).
+// Scores on the matrix cores: for a tile of 16 tokens, S[token][head] = K_tile (16 x kD) times
+// Q^T (kD x 16, the kG query heads of this KV head, zero-padded), as kD/32 MFMA 16x16x32 steps;
+// the float32 query is split into a high and a low 16-bit part (q = hi + lo to about 2^-17
+// relative) and both are multiplied, so the scores keep float32 accuracy. Lane l holds token
+// l%16 and elements 8*(l/16)..+7 of each 32-element chunk (the operand layout of the
+// instruction), and receives the scores of tokens 4*(l/16)..+3 for head l%16.
+// Weighted V sum on the vector ALUs: kD/8 lanes per token, 8 elements each.
+// Every thread issues all of its K and V loads (8 + 8 pieces) before any arithmetic.
+template <int kKind, int kD, int kG>
 __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) {
   using PieceT = typename Piece<kKind>::type;
+  using OpT = typename ScoreOp<kKind>::type;
+  using ElemT = typename ScoreOp<kKind>::elem;
   constexpr int kElem = kKind == 2 ? 1 : 2;
-  constexpr int kD = kLanes * kPer;                  // head_dim
-  constexpr int kTokPerPass = kAttnThreads / kLanes; // tokens per pass of the workgroup
-  constexpr int kIters = kDecodeTokensPerThread;     // tokens per thread
-  constexpr int kSplit = kIters * kTokPerPass;
-  static_assert(kSplit == decode_split_tokens(kD), "split size");
+  constexpr int kChunks = kD / 32;
+  constexpr int kSplit = decode_split_tokens(kD);
   constexpr int kWaves = kAttnThreads / 64;
+  constexpr int kTilesPerWave = kSplit / 16 / kWaves;
+  constexpr int kLanes = kD / kPer;                  // V: lanes per token row
+  constexpr int kTokPerPass = kAttnThreads / kLanes;
+  constexpr int kIters = kSplit / kTokPerPass;       // V: tokens per thread
+  static_assert(kTilesPerWave * 16 * kWaves == kSplit && kIters == kDecodeTokensPerThread,
+                "split geometry");
   __shared__ float p_s[kG][kSplit];
   __shared__ float red_s[kWaves][kG];
   __shared__ float acc_s[kWaves][kG][kD];
@@ -204,56 +244,84 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
   if (t0 >= c || s0 < 0) return;
   const int nt = c - t0 < kSplit ? c - t0 : kSplit;
   const int* slots = a.slots + s0 + t0;
-
-  const int piece = tid % kLanes;       // which 8 elements of the head row
-  const int tg = tid / kLanes;          // token group
   const uint8_t* kplane = a.kv + (int64_t)(2 * a.layer) * a.plane_bytes;
   const uint8_t* vplane = kplane + a.plane_bytes;
-  const int64_t head_off = (int64_t)h * kD * kElem + piece * kPer * kElem;
+  const int64_t head0 = (int64_t)h * kD * kElem;
 
-  // all loads of the split first; tokens past its end re-read its last token (dropped later)
-  int64_t off[kIters];
-  bool ok[kIters];
+  // ---- all loads first; tokens past the split's end re-read its last token (dropped later)
+  const int grp = lane >> 4;    // which 8 elements of each 32-element chunk (scores)
+  const int row = lane & 15;    // token of the tile (scores) / query head (operand, result)
+  // query operand first (needed first): head `row` (zero past kG), scaled, split into high
+  // and low parts
+  OpT qh[kChunks], ql[kChunks];
+  {
+    const bool real = row < kG;
+    const float* qrow = a.q + ((int64_t)r * a.num_q_heads + h * kG + (real ? row : 0)) * kD;
 #pragma unroll
-  for (int i = 0; i < kIters; ++i) {
-    const int t = tg + i * kTokPerPass;
-    const int s = slots[t < nt ? t : nt - 1];
-    ok[i] = static_cast<unsigned>(s) < static_cast<unsigned>(a.num_slots);
-    off[i] = (int64_t)(ok[i] ? s : 0) * a.row_bytes + head_off;
+    for (int ch = 0; ch < kChunks; ++ch) {
+#pragma unroll
+      for (int e = 0; e < kPer; ++e) {
+        // unconditional load (a padded head re-reads head 0), then a select: a conditional
+        // load would wait for every outstanding K/V load
+        const float qv = qrow[ch * 32 + grp * kPer + e] * a.scale;
+        const float q = real ? qv : 0.f;
+        const ElemT hi = static_cast<ElemT>(q);
+        qh[ch][e] = hi;
+        ql[ch][e] = static_cast<ElemT>(q - static_cast<float>(hi));
+      }
+    }
   }
-  PieceT kw[kIters], vw[kIters];
-#pragma unroll
-  for (int i = 0; i < kIters; ++i) kw[i] = *reinterpret_cast<const PieceT*>(kplane + off[i]);
-#pragma unroll
-  for (int i = 0; i < kIters; ++i) vw[i] = *reinterpret_cast<const PieceT*>(vplane + off[i]);
 
-  const float* qrow = a.q + ((int64_t)r * a.num_q_heads + h * kG) * kD + piece * kPer;
-  float q_r[kG][kPer];
+  PieceT kw[kTilesPerWave][kChunks];
+  bool kok[kTilesPerWave];
 #pragma unroll
-  for (int g = 0; g < kG; ++g)
+  for (int i = 0; i < kTilesPerWave; ++i) {
+    const int t = (wave * kTilesPerWave + i) * 16 + row;
+    const int sl = slots[t < nt ? t : nt - 1];
+    kok[i] = static_cast<unsigned>(sl) < static_cast<unsigned>(a.num_slots);
+    const uint8_t* base = kplane + (int64_t)(kok[i] ? sl : 0) * a.row_bytes + head0 +
+                          grp * kPer * kElem;
 #pragma unroll
-    for (int e = 0; e < kPer; ++e) q_r[g][e] = qrow[g * kD + e];
-
-  // scores
+    for (int ch = 0; ch < kChunks; ++ch) {
+      kw[i][ch] = *reinterpret_cast<const PieceT*>(base + ch * 32 * kElem);
+    }
+  }
+  const int piece = tid % kLanes;
+  const int tg = tid / kLanes;
+  PieceT vw[kIters];
+  bool vok[kIters];
 #pragma unroll
   for (int i = 0; i < kIters; ++i) {
     const int t = tg + i * kTokPerPass;
-    float kf[kPer];
-    PieceT w = kw[i];
-    if (!ok[i]) w = PieceT{};
-    piece_to_float<kKind>(w, kf);
+    const int sl = slots[t < nt ? t : nt - 1];
+    vok[i] = static_cast<unsigned>(sl) < static_cast<unsigned>(a.num_slots);
+    vw[i] = *reinterpret_cast<const PieceT*>(vplane + (int64_t)(vok[i] ? sl : 0) * a.row_bytes +
+                                             head0 + piece * kPer * kElem);
+  }
+
+  // ---- scores
 #pragma unroll
-    for (int g = 0; g < kG; ++g) {
-      float acc = 0.f;
+  for (int i = 0; i < kTilesPerWave; ++i) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int e = 0; e < kPer; ++e) acc += q_r[g][e] * kf[e];
-      acc = group_sum<kLanes>(acc);
-      if (piece == 0 && t < nt) p_s[g][t] = acc * a.scale;
+    for (int ch = 0; ch < kChunks; ++ch) {
+      PieceT w = kw[i][ch];
+      if (!kok[i]) w = PieceT{};
+      const OpT kop = k_operand<kKind>(w);
+      acc = score_mfma<kKind>(kop, qh[ch], acc);
+      acc = score_mfma<kKind>(kop, ql[ch], acc);
+    }
+    if (row < kG) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int t = (wave * kTilesPerWave + i) * 16 + grp * 4 + j;
+        if (t < nt) p_s[row][t] = acc[j];
+      }
     }
   }
   __syncthreads();
 
-  // split-local softmax: max and sum of exp per query head
+  // ---- split-local softmax: max and sum of exp per query head
   float m_g[kG], l_g[kG];
 #pragma unroll
   for (int g = 0; g < kG; ++g) {
@@ -291,7 +359,7 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
     l_g[g] = l;
   }
 
-  // weighted sum of V from the registers (kG * 8 <= 64 accumulators per thread)
+  // ---- weighted sum of V from the registers (kG * 8 <= 64 accumulators per thread)
   float acc[kG][kPer];
 #pragma unroll
   for (int g = 0; g < kG; ++g)
@@ -303,7 +371,7 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
     if (t < nt) {
       float vf[kPer];
       PieceT w = vw[i];
-      if (!ok[i]) w = PieceT{};
+      if (!vok[i]) w = PieceT{};
       piece_to_float<kKind>(w, vf);
 #pragma unroll
       for (int g = 0; g < kG; ++g) {
@@ -418,21 +486,21 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(AttnArg
   if (d1 < D) out[d1] = v1 * inv;
 }
 
-template <int kKind, int kLanes, int kG>
+template <int kKind, int kD, int kG>
 hipError_t launch_split(const AttnArgs& a, hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>((int64_t)a.num_reqs * a.num_kv_heads * a.splits));
-  auto kernel = decode_split_kernel<kKind, kLanes, kG>;
+  auto kernel = decode_split_kernel<kKind, kD, kG>;
   hipLaunchKernelGGL(kernel, grid, dim3(kAttnThreads), 0, stream, a);
   return hipGetLastError();
 }
 
-template <int kKind, int kLanes>
+template <int kKind, int kD>
 hipError_t launch_decode_g(const AttnArgs& a, hipStream_t stream) {
   switch (a.num_q_heads / a.num_kv_heads) {
-    case 1: return launch_split<kKind, kLanes, 1>(a, stream);
-    case 2: return launch_split<kKind, kLanes, 2>(a, stream);
-    case 4: return launch_split<kKind, kLanes, 4>(a, stream);
-    case 8: return launch_split<kKind, kLanes, 8>(a, stream);
+    case 1: return launch_split<kKind, kD, 1>(a, stream);
+    case 2: return launch_split<kKind, kD, 2>(a, stream);
+    case 4: return launch_split<kKind, kD, 4>(a, stream);
+    case 8: return launch_split<kKind, kD, 8>(a, stream);
     default: return hipErrorInvalidValue;
   }
 }
@@ -440,10 +508,10 @@ hipError_t launch_decode_g(const AttnArgs& a, hipStream_t stream) {
 template <int kKind>
 hipError_t launch_decode_k(const AttnArgs& a, hipStream_t stream) {
   switch (a.head_dim) {
-    case 32: return launch_decode_g<kKind, 4>(a, stream);
-    case 64: return launch_decode_g<kKind, 8>(a, stream);
-    case 128: return launch_decode_g<kKind, 16>(a, stream);
-    case 256: return launch_decode_g<kKind, 32>(a, stream);
+    case 32: return launch_decode_g<kKind, 32>(a, stream);
+    case 64: return launch_decode_g<kKind, 64>(a, stream);
+    case 128: return launch_decode_g<kKind, 128>(a, stream);
+    case 256: return launch_decode_g<kKind, 256>(a, stream);
     default: return hipErrorInvalidValue;
   }
 }

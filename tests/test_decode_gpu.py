@@ -215,6 +215,37 @@ def test_decode_one_key_returns_value_codes_exactly(dtype):
                            f"got {got.reshape(-1)[bad[:5]]} expect {expect.reshape(-1)[bad[:5]]}")
 
 
+def test_decode_fp8_key_codes():
+    """Every e4m3 key code reaches the score exactly: requests of two tokens, token 0 with key
+    x * e_0 (x = the code's value), token 1 with a zero key; value rows e_0 and 0; query e_0 at
+    scale 1/64. Then out[0] = sigmoid(x / 64), checked against torch's CPU conversion of the
+    code (NaN codes excluded)."""
+    t = torch()
+    B = _B()
+    H, D, S = 1, 64, 16
+    codes = np.arange(256, dtype=np.uint8)
+    codes = codes[(codes & 0x7F) != 0x7F]            # the two NaN codes
+    R = len(codes)
+    sh = W.KVShape(1, H, D, S, "fp8_e4m3")
+    raw = np.zeros((2, R * S, H * D), dtype=np.uint8)
+    one = np.frombuffer(t.tensor([1.0]).to(t.float8_e4m3fn).view(t.uint8).numpy().tobytes(),
+                        np.uint8)[0]
+    for r, code in enumerate(codes):
+        raw[0, r * S, 0] = code                        # K of token 0: x at dimension 0
+        raw[1, r * S, 0] = one                         # V of token 0: e_0
+    kv = t.from_numpy(raw).cuda().view(t.float8_e4m3fn).reshape(2, R, S, H, D).contiguous()
+    cache = B.KVCache(kv, 1, H, D, S)
+    indptr = _dev_i32(np.arange(R + 1) * 2)
+    slots = _dev_i32(np.stack([np.arange(R) * S, np.arange(R) * S + 1], 1).reshape(-1))
+    q = t.zeros(R, H, D, device="cuda")
+    q[:, :, 0] = 1.0
+    _label(f"fp8 key codes: {R} codes")
+    got = B.paged_decode(cache, q, indptr, slots, 0, 2, scale=1.0 / 64).cpu().numpy()[:, 0, 0]
+    x = t.from_numpy(codes.copy()).view(t.float8_e4m3fn).float().numpy().astype(np.float64)
+    expect = 1.0 / (1.0 + np.exp(-x / 64))
+    np.testing.assert_allclose(got, expect, rtol=2e-6, atol=1e-7)
+
+
 # ------------------------------------------------------------------------------------------
 # before / after the repack, stream-event ordering, graph replay
 # ------------------------------------------------------------------------------------------
