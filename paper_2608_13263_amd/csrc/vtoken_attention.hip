@@ -201,7 +201,31 @@ __device__ __forceinline__ typename ScoreOp<kKind>::type k_operand(
   }
 }
 
-// kKind: element type; kD: head_dim (32, 64, 128, 256); kG: query heads per KV head (1-8).
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+// Eight V elements as 16-bit values of the matrix-core type: fp16 / bf16 as loaded, fp8
+// widened to bf16 (exact).
+template <int kKind>
+__device__ __forceinline__ u32x4 v_row16(typename Piece<kKind>::type w) {
+  if constexpr (kKind == 2) {
+    return __builtin_bit_cast(u32x4, k_operand<2>(w));
+  } else {
+    return w;
+  }
+}
+
+// LDS transpose read of gfx950 (ds_read_b64_tr_b16): in each group of 16 lanes, lane
+// 4a + b receives element b of the four 16-bit values addressed by lanes a, a+4, a+8 and
+// a+12 of its group (in that order).
+__device__ __forceinline__ i16x4 lds_read_tr16(const uint8_t* lds_addr) {
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_i16x4*)(reinterpret_cast<uintptr_t>(lds_addr)));
+}
+
+// Variant for GQA groups up to 4: scores on the matrix cores, weighted V sum on the vector ALUs.
+//
+// kKind: element type; kD: head_dim (32, 64, 128, 256); kG: query heads per KV head.
 //
 // One workgroup (4 waves) covers kSplit = 16384 / kD tokens of one (request, KV head).
 // Scores on the matrix cores: for a tile of 16 tokens, S[token][head] = K_tile (16 x kD) times
@@ -411,6 +435,240 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
   }
 }
 
+// Variant for large GQA groups (kG = 8), where the weighted V sum (2 kG flops per V byte)
+// would bound the vector ALUs: both products on the matrix cores.
+//
+// kKind: element type; kD: head_dim (32, 64, 128, 256); kG: query heads per KV head.
+//
+// One workgroup (4 waves) covers kSplit = 16384 / kD tokens of one (request, KV head); wave w
+// owns tokens [w*kTW, (w+1)*kTW), kTW = kSplit / 4, and computes for them, on the matrix
+// cores (MFMA 16x16x32, fp16 for fp16 caches, bf16 otherwise; fp8 widened to bf16):
+//   scores  S[token][head] = K_tile (16 x kD) . Q^T (kD x 16: the kG query heads, zero-padded),
+//           the float32 query split into high and low 16-bit parts (q = hi + lo to ~2^-17),
+//           each multiplied, so the scores keep float32 accuracy;
+//   weights p = exp(S - m_w) with the wave's own maximum m_w per head, l_w = sum of p;
+//   values  O_w[head][d] = P (16 x 32 tokens) . V (32 tokens x 16 elements) per 16-element
+//           chunk, P again split into high and low parts. V goes through LDS (16-bit rows,
+//           padded by 32 bytes against bank conflicts) and comes back in operand layout by
+//           transpose reads. The operand layout fixes which tokens a lane holds: lane l has
+//           head l%16 and, of each 32-token chunk, tokens 4*(l/16)..+3 of its first
+//           16-token tile and the same of its second; the V rows are read in that order.
+// The four waves are merged with the usual max-rescaling into the split's record.
+// Every thread issues all of its K and V loads (8 + 8 pieces) before any arithmetic.
+// Non-finite K or V values are outside the contract (a zero weight times an infinite value
+// gives NaN).
+template <int kKind, int kD, int kG>
+__global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArgs a) {
+  using PieceT = typename Piece<kKind>::type;
+  using OpT = typename ScoreOp<kKind>::type;
+  using ElemT = typename ScoreOp<kKind>::elem;
+  constexpr int kElem = kKind == 2 ? 1 : 2;
+  constexpr int kChunks = kD / 32;                   // score k-steps
+  constexpr int kSplit = decode_split_tokens(kD);
+  constexpr int kWaves = kAttnThreads / 64;
+  constexpr int kTW = kSplit / kWaves;               // tokens per wave: 128, 64, 32, 16
+  constexpr int kTiles = kTW / 16;                   // 16-token score tiles per wave
+  constexpr int kKC = (kTiles + 1) / 2;              // 32-token value k-steps per wave
+  constexpr int kDC = kD / 16;                       // 16-element value chunks
+  constexpr int kLanesV = kD / kPer;                 // V load: lanes per token row
+  constexpr int kTokV = 64 / kLanesV;                // V load: tokens per wave pass
+  constexpr int kItV = kTW / kTokV;                  // V load: pieces per lane
+  constexpr int kRowB = kD * 2 + 32;                 // LDS bytes per V row
+  static_assert(kTiles * 16 == kTW && kItV == kDecodeTokensPerThread, "split geometry");
+  constexpr int kMergeB = kWaves * kG * (kD + 2) * 4;
+  constexpr int kLdsB = kSplit * kRowB > kMergeB ? kSplit * kRowB : kMergeB;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsB];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int split = blockIdx.x % a.splits;
+  const int h = (blockIdx.x / a.splits) % a.num_kv_heads;
+  const int r = blockIdx.x / (a.splits * a.num_kv_heads);
+  if (r >= a.num_reqs) return;
+  const int s0 = a.slot_indptr[r];
+  const int c = a.slot_indptr[r + 1] - s0;
+  const int t0 = split * kSplit;
+  if (t0 >= c || s0 < 0) return;
+  const int nt = c - t0 < kSplit ? c - t0 : kSplit;
+  const int* slots = a.slots + s0 + t0;
+  const uint8_t* kplane = a.kv + (int64_t)(2 * a.layer) * a.plane_bytes;
+  const uint8_t* vplane = kplane + a.plane_bytes;
+  const int64_t head0 = (int64_t)h * kD * kElem;
+  const int grp = lane >> 4;    // operand k-group / result row group
+  const int row = lane & 15;    // token of a tile (K operand) / head (Q, P operands)
+  const int wt0 = wave * kTW;   // first token of this wave
+
+  // ---- query operand first (needed first): head `row` (zero past kG), scaled, split into
+  // high and low parts; the load is unconditional (a padded head re-reads head 0), a
+  // conditional load would wait for every outstanding K/V load
+  OpT qh[kChunks], ql[kChunks];
+  {
+    const bool real = row < kG;
+    const float* qrow = a.q + ((int64_t)r * a.num_q_heads + h * kG + (real ? row : 0)) * kD;
+#pragma unroll
+    for (int ch = 0; ch < kChunks; ++ch) {
+#pragma unroll
+      for (int e = 0; e < kPer; ++e) {
+        const float qv = qrow[ch * 32 + grp * kPer + e] * a.scale;
+        const float q = real ? qv : 0.f;
+        const ElemT hi = static_cast<ElemT>(q);
+        qh[ch][e] = hi;
+        ql[ch][e] = static_cast<ElemT>(q - static_cast<float>(hi));
+      }
+    }
+  }
+
+  // ---- all K and V loads; tokens past the split's end re-read its last token
+  PieceT kw[kTiles][kChunks];
+  bool kok[kTiles];
+#pragma unroll
+  for (int i = 0; i < kTiles; ++i) {
+    const int t = wt0 + i * 16 + row;
+    const int sl = slots[t < nt ? t : nt - 1];
+    kok[i] = static_cast<unsigned>(sl) < static_cast<unsigned>(a.num_slots);
+    const uint8_t* base = kplane + (int64_t)(kok[i] ? sl : 0) * a.row_bytes + head0 +
+                          grp * kPer * kElem;
+#pragma unroll
+    for (int ch = 0; ch < kChunks; ++ch) {
+      kw[i][ch] = *reinterpret_cast<const PieceT*>(base + ch * 32 * kElem);
+    }
+  }
+  const int vpiece = lane % kLanesV;
+  PieceT vw[kItV];
+  bool vok[kItV];
+#pragma unroll
+  for (int i = 0; i < kItV; ++i) {
+    const int t = wt0 + lane / kLanesV + i * kTokV;
+    const int sl = slots[t < nt ? t : nt - 1];
+    vok[i] = t < nt && static_cast<unsigned>(sl) < static_cast<unsigned>(a.num_slots);
+    vw[i] = *reinterpret_cast<const PieceT*>(vplane + (int64_t)(vok[i] ? sl : 0) * a.row_bytes +
+                                             head0 + vpiece * kPer * kElem);
+  }
+
+  // ---- scores of this wave's tiles: lane holds tokens wt0 + 16i + 4*grp + j, head `row`
+  f32x4 sc[kTiles];
+#pragma unroll
+  for (int i = 0; i < kTiles; ++i) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ch = 0; ch < kChunks; ++ch) {
+      PieceT w = kw[i][ch];
+      if (!kok[i]) w = PieceT{};
+      const OpT kop = k_operand<kKind>(w);
+      acc = score_mfma<kKind>(kop, qh[ch], acc);
+      acc = score_mfma<kKind>(kop, ql[ch], acc);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (wt0 + 16 * i + 4 * grp + j >= nt) acc[j] = -INFINITY;
+    }
+    sc[i] = acc;
+  }
+
+  // ---- V rows into this wave's LDS rows (zero rows past the split's end)
+#pragma unroll
+  for (int i = 0; i < kItV; ++i) {
+    const int tl = wt0 + lane / kLanesV + i * kTokV;     // row within the split
+    PieceT w = vw[i];
+    if (!vok[i]) w = PieceT{};
+    *reinterpret_cast<u32x4*>(lds + tl * kRowB + vpiece * 16) = v_row16<kKind>(w);
+  }
+
+  // ---- wave-local softmax per head (the four lanes of a head share `row`)
+  float m = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < kTiles; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) m = fmaxf(m, sc[i][j]);
+  m = fmaxf(m, __shfl_xor(m, 16, 64));
+  m = fmaxf(m, __shfl_xor(m, 32, 64));
+  const float msafe = m == -INFINITY ? 0.f : m;   // a wave with no valid token
+  float l = 0.f;
+#pragma unroll
+  for (int i = 0; i < kTiles; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float e = __expf(sc[i][j] - msafe);
+      sc[i][j] = row < kG ? e : 0.f;
+      l += sc[i][j];
+    }
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  __syncthreads();  // V rows written (each wave reads only its own rows)
+
+  // ---- O_w = P . V on the matrix cores
+  f32x4 o[kDC];
+#pragma unroll
+  for (int dc = 0; dc < kDC; ++dc) o[dc] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kc = 0; kc < kKC; ++kc) {
+    // A operand: head `row`, tokens 4*grp..+3 of tile 2kc then of tile 2kc+1 (zero if absent)
+    OpT ph, pl;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int tile = 2 * kc + (j >> 2);
+      const float p = tile < kTiles ? sc[tile < kTiles ? tile : 0][j & 3] : 0.f;
+      const ElemT hi = static_cast<ElemT>(p);
+      ph[j] = hi;
+      pl[j] = static_cast<ElemT>(p - static_cast<float>(hi));
+    }
+    // B operand rows: lane 16*grp + rho supplies the row of token 4*grp + rho/4 of the first
+    // tile (then of the second), elements 4*(rho%4)..+3 of the 16-element chunk
+    const int t1 = 2 * kc * 16 + 4 * grp + row / 4;
+    const int t2 = (2 * kc + 1 < kTiles ? (2 * kc + 1) * 16 : 2 * kc * 16) + 4 * grp + row / 4;
+    const uint8_t* r1 = lds + (wt0 + t1) * kRowB + (row % 4) * 8;
+    const uint8_t* r2 = lds + (wt0 + t2) * kRowB + (row % 4) * 8;
+#pragma unroll
+    for (int dc = 0; dc < kDC; ++dc) {
+      const i16x4 x1 = lds_read_tr16(r1 + dc * 32);
+      const i16x4 x2 = lds_read_tr16(r2 + dc * 32);
+      typedef short i16x8 __attribute__((ext_vector_type(8)));
+      const i16x8 xv = {x1[0], x1[1], x1[2], x1[3], x2[0], x2[1], x2[2], x2[3]};
+      const OpT vop = __builtin_bit_cast(OpT, xv);
+      o[dc] = score_mfma<kKind>(ph, vop, o[dc]);
+      o[dc] = score_mfma<kKind>(pl, vop, o[dc]);
+    }
+  }
+  __syncthreads();  // the LDS rows are reused for the merge
+
+  // ---- merge the four waves: [m_w, l_w] and O_w[head][d] per wave into LDS
+  float* mrg = reinterpret_cast<float*>(lds);        // [wave][head][kD + 2]
+  if (grp == 0 && row < kG) {
+    mrg[(wave * kG + row) * (kD + 2)] = m;
+    mrg[(wave * kG + row) * (kD + 2) + 1] = l;
+  }
+#pragma unroll
+  for (int dc = 0; dc < kDC; ++dc)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int g = 4 * grp + j;                     // result row = head
+      if (g < kG) mrg[(wave * kG + g) * (kD + 2) + 2 + dc * 16 + row] = o[dc][j];
+    }
+  __syncthreads();
+  for (int i = tid; i < kG * kD; i += kAttnThreads) {
+    const int g = i / kD, d = i - g * kD;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, mrg[(w * kG + g) * (kD + 2)]);
+    float v = 0.f, L = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float* wr = mrg + (w * kG + g) * (kD + 2);
+      const float f = wr[0] == -INFINITY ? 0.f : __expf(wr[0] - M);
+      v += wr[2 + d] * f;
+      L += wr[1] * f;
+    }
+    float* rec = a.workspace +
+                 (((int64_t)r * a.num_q_heads + h * kG + g) * a.splits + split) * (kD + 2);
+    rec[2 + d] = v;
+    if (d == 0) {
+      rec[0] = M;
+      rec[1] = L;
+    }
+  }
+}
+
 // Merge of the split partials of one (request, query head): M = max of the split maxima,
 // weights w_s = exp(m_s - M), out = sum_s w_s acc_s / sum_s w_s l_s. The splits are spread
 // over the threads (maxima, weights) and the head elements over the threads (weighted sum,
@@ -489,8 +747,15 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(AttnArg
 template <int kKind, int kD, int kG>
 hipError_t launch_split(const AttnArgs& a, hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>((int64_t)a.num_reqs * a.num_kv_heads * a.splits));
-  auto kernel = decode_split_kernel<kKind, kD, kG>;
-  hipLaunchKernelGGL(kernel, grid, dim3(kAttnThreads), 0, stream, a);
+  // GQA groups of 8 have both products on the matrix cores; smaller groups keep the value sum
+  // on the vector ALUs (measured faster for them)
+  if constexpr (kG >= 8) {
+    auto kernel = decode_split_mfma_kernel<kKind, kD, kG>;
+    hipLaunchKernelGGL(kernel, grid, dim3(kAttnThreads), 0, stream, a);
+  } else {
+    auto kernel = decode_split_kernel<kKind, kD, kG>;
+    hipLaunchKernelGGL(kernel, grid, dim3(kAttnThreads), 0, stream, a);
+  }
   return hipGetLastError();
 }
 
