@@ -290,6 +290,25 @@ vtoken_status vtoken_build_slot_mapping(const vtoken_batch* batch, const vtoken_
                                         int32_t* slot_indptr, int32_t* slots,
                                         int64_t slots_capacity, hipStream_t stream);
 
+/* The slot mapping as a translation cache that grows append-only (Sec. 3.2: the cached
+ * translation array is extended by the new entries as a sequence grows, and rebuilt only after
+ * a structural change - eviction or relocation). vtoken_build_slot_table is the rebuild: like
+ * vtoken_build_slot_mapping, but request r's region is slot_start[r] .. slot_start[r+1] with
+ * room for `reserve` more slots after its live_count[r] ones; slot_count[r] = live_count[r].
+ * slots_capacity >= num_tokens + num_reqs * reserve. vtoken_append_slots appends
+ * append_slots[append_indptr[r] .. append_indptr[r+1]) (device, int32) to request r's region
+ * and adds their number to slot_count[r]; a request whose region would overflow is left
+ * unchanged and *status (device int32, written by the call) becomes VTOKEN_ERR_CAPACITY (a
+ * rebuild is due), else 0. Decode reads a slot table with vtoken_decode.slot_count set. */
+vtoken_status vtoken_build_slot_table(const vtoken_batch* batch, const vtoken_plan* plan,
+                                      int32_t reserve, int32_t* slot_start, int32_t* slot_count,
+                                      int32_t* slots, int64_t slots_capacity,
+                                      hipStream_t stream);
+vtoken_status vtoken_append_slots(int32_t num_reqs, const int32_t* append_indptr,
+                                  const int32_t* append_slots, const int32_t* slot_start,
+                                  int32_t* slot_count, int32_t* slots, int32_t* status,
+                                  hipStream_t stream);
+
 /* Decode attention of one layer over the paged cache through a slot mapping: for request r
  * and query head qh (GQA: KV head qh / (num_q_heads / num_kv_heads)),
  *   out[r][qh] = softmax(scale * q[r][qh] . K[slot]^T) @ V[slot] over the slots of r,
@@ -308,6 +327,9 @@ typedef struct vtoken_decode {
   int32_t      max_tokens; /* [host] >= the slot count of every request                     */
   float*       workspace;  /* device, >= vtoken_decode_workspace_bytes() bytes              */
   int64_t      workspace_bytes;
+  const int32_t* slot_count; /* device [R] or NULL: request r's slots are                   */
+                           /* slots[slot_indptr[r] .. + slot_count[r]) (a slot table, below);*/
+                           /* NULL: slots[slot_indptr[r] .. slot_indptr[r+1])               */
 } vtoken_decode;
 
 /* Bytes of workspace: num_reqs * num_q_heads * ceil(max_tokens / (16384 / head_dim)) (at

@@ -60,6 +60,37 @@ def slot_mapping(token_slot, tok_indptr, seq_lens):
     return np.asarray(indptr, dtype=np.int64), np.asarray(slots, dtype=np.int64)
 
 
+def slot_table(token_slot, tok_indptr, seq_lens, reserve: int):
+    """The slot mapping laid out with room for `reserve` more slots per request (the
+    append-only translation cache of Sec. 3.2): (slot_start [R+1], slot_count [R], slots),
+    request r's live slots at slots[slot_start[r] ..][:slot_count[r]], unused room -1."""
+    indptr, packed = slot_mapping(token_slot, tok_indptr, seq_lens)
+    counts = np.diff(indptr)
+    start = np.concatenate([[0], np.cumsum(counts + reserve)]).astype(np.int64)
+    slots = np.full(int(start[-1]), -1, dtype=np.int64)
+    for r in range(len(counts)):
+        slots[start[r]:start[r] + counts[r]] = packed[indptr[r]:indptr[r + 1]]
+    return start, counts.astype(np.int64), slots
+
+
+def append_to_table(start, count, slots, new_slots_per_request):
+    """Append each request's new slots after its current ones if its region has room;
+    returns (count, slots, overflowed) with overflowing requests left unchanged."""
+    count = np.array(count, dtype=np.int64)
+    slots = np.array(slots, dtype=np.int64)
+    overflow = False
+    for r, new in enumerate(new_slots_per_request):
+        n = len(new)
+        if n == 0:
+            continue
+        if count[r] + n > start[r + 1] - start[r]:
+            overflow = True
+            continue
+        slots[start[r] + count[r]:start[r] + count[r] + n] = new
+        count[r] += n
+    return count, slots, overflow
+
+
 def decode_batch(q: np.ndarray, k_plane: np.ndarray, v_plane: np.ndarray, slot_indptr,
                  slots, scale=None) -> np.ndarray:
     """Decode attention of every request through a slot mapping. q [R, Hq, D]; k_plane,

@@ -70,7 +70,7 @@ class CDecode(ctypes.Structure):
                 ("num_q_heads", ctypes.c_int32), ("layer", ctypes.c_int32),
                 ("kv_dtype", ctypes.c_int32), ("scale", ctypes.c_float),
                 ("max_tokens", ctypes.c_int32), ("workspace", ctypes.c_void_p),
-                ("workspace_bytes", ctypes.c_int64)]
+                ("workspace_bytes", ctypes.c_int64), ("slot_count", ctypes.c_void_p)]
 
 
 KV_FP16, KV_BF16, KV_FP8_E4M3 = 0, 1, 2
@@ -116,6 +116,13 @@ _SIGNATURES = {
                                                    ctypes.POINTER(CPlan), ctypes.c_void_p,
                                                    ctypes.c_void_p, ctypes.c_int64,
                                                    ctypes.c_void_p]),
+    "vtoken_build_slot_table": (ctypes.c_int32, [ctypes.POINTER(CBatch), ctypes.POINTER(CPlan),
+                                                 ctypes.c_int32, ctypes.c_void_p,
+                                                 ctypes.c_void_p, ctypes.c_void_p,
+                                                 ctypes.c_int64, ctypes.c_void_p]),
+    "vtoken_append_slots": (ctypes.c_int32, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                             ctypes.c_void_p, ctypes.c_void_p]),
     "vtoken_decode_workspace_bytes": (ctypes.c_int64, [ctypes.c_int32, ctypes.c_int32,
                                                        ctypes.c_int32, ctypes.c_int32]),
     "vtoken_paged_decode": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CDecode),
@@ -350,6 +357,40 @@ def build_slot_mapping(batch: Batch, plan: Plan, slot_indptr=None, slots=None,
     return slot_indptr, slots
 
 
+def build_slot_table(batch: Batch, plan: Plan, reserve: int, stream=None):
+    """The slot mapping as an append-only translation cache: returns (slot_start [R+1],
+    slot_count [R], slots) with room for `reserve` more slots per request."""
+    import torch
+    lib = load_library()
+    dev = plan.counters.device
+    R = batch.num_reqs
+    start = torch.empty(R + 1, dtype=torch.int32, device=dev)
+    count = torch.empty(max(R, 1), dtype=torch.int32, device=dev)
+    slots = torch.empty(max(batch.num_tokens + R * int(reserve), 1), dtype=torch.int32,
+                        device=dev)
+    b, p = batch.c(), plan.c()
+    _check(lib.vtoken_build_slot_table(ctypes.byref(b), ctypes.byref(p), int(reserve),
+                                       _ptr(start), _ptr(count), _ptr(slots),
+                                       int(slots.numel()), _stream(stream)),
+           "vtoken_build_slot_table")
+    return start, count, slots
+
+
+def append_slots(slot_start, slot_count, slots, append_indptr, append_slots, status=None,
+                 stream=None):
+    """Append each request's new slots to its region of a slot table; returns the device
+    status word (0, or VTOKEN_ERR_CAPACITY when a region is full and a rebuild is due)."""
+    import torch
+    lib = load_library()
+    if status is None:
+        status = torch.empty(1, dtype=torch.int32, device=slots.device)
+    R = int(append_indptr.numel()) - 1
+    _check(lib.vtoken_append_slots(R, _ptr(append_indptr), _ptr(append_slots),
+                                   _ptr(slot_start), _ptr(slot_count), _ptr(slots),
+                                   _ptr(status), _stream(stream)), "vtoken_append_slots")
+    return status
+
+
 def decode_workspace_bytes(num_reqs: int, num_q_heads: int, head_dim: int,
                            max_tokens: int) -> int:
     n = load_library().vtoken_decode_workspace_bytes(int(num_reqs), int(num_q_heads),
@@ -371,10 +412,11 @@ def kv_dtype_code(dtype) -> int:
 
 def paged_decode(cache: KVCache, q, slot_indptr, slots, layer: int, max_tokens: int,
                  scale: Optional[float] = None, out=None, workspace=None, kv_dtype=None,
-                 stream=None):
+                 stream=None, slot_count=None):
     """Decode attention of one layer through a slot mapping; q and out are float32
     [R][num_q_heads][head_dim] device tensors. kv_dtype defaults to the cache tensor's
-    dtype (a uint8 view of fp8 data needs KV_FP8_E4M3)."""
+    dtype (a uint8 view of fp8 data needs KV_FP8_E4M3). With slot_count, (slot_indptr,
+    slot_count, slots) is a slot table (build_slot_table / append_slots)."""
     import torch
     lib = load_library()
     if q.dtype != torch.float32 or not q.is_contiguous() or q.dim() != 3:
@@ -393,7 +435,8 @@ def paged_decode(cache: KVCache, q, slot_indptr, slots, layer: int, max_tokens: 
     if scale is None:
         scale = D ** -0.5
     d = CDecode(_ptr(q), _ptr(out), Hq, int(layer), code, float(scale), int(max_tokens),
-                _ptr(workspace), int(workspace.numel() * workspace.element_size()))
+                _ptr(workspace), int(workspace.numel() * workspace.element_size()),
+                _ptr(slot_count))
     c = cache.c()
     _check(lib.vtoken_paged_decode(ctypes.byref(c), ctypes.byref(d), R, _ptr(slot_indptr),
                                    _ptr(slots), _stream(stream)), "vtoken_paged_decode")

@@ -246,9 +246,11 @@ vtoken_status vtoken_free_blocks(const vtoken_batch* batch, const vtoken_plan* p
   return hip_status(vtoken::launch_free(a, freed, freed_capacity, stream));
 }
 
-vtoken_status vtoken_build_slot_mapping(const vtoken_batch* batch, const vtoken_plan* plan,
-                                        int32_t* slot_indptr, int32_t* slots,
-                                        int64_t slots_capacity, hipStream_t stream) {
+namespace {
+
+vtoken_status build_slots(const vtoken_batch* batch, const vtoken_plan* plan, int32_t reserve,
+                          int32_t* slot_indptr, int32_t* slot_count, int32_t* slots,
+                          int64_t slots_capacity, hipStream_t stream) {
   vtoken_status s = check_batch(batch);
   if (s != VTOKEN_OK) return s;
   if (plan == nullptr || plan->counters == nullptr || slot_indptr == nullptr) {
@@ -258,7 +260,11 @@ vtoken_status vtoken_build_slot_mapping(const vtoken_batch* batch, const vtoken_
   if (batch->num_tokens > 0 && (plan->token_slot == nullptr || slots == nullptr)) {
     return VTOKEN_ERR_NULL;
   }
-  if (slots_capacity < batch->num_tokens) return VTOKEN_ERR_CAPACITY;
+  if (reserve < 0) return VTOKEN_ERR_ARGUMENT;
+  const int64_t need = batch->num_tokens + (int64_t)batch->num_reqs * reserve;
+  if (need > kInt32Limit) return VTOKEN_ERR_SHAPE;
+  if (slots_capacity < need) return VTOKEN_ERR_CAPACITY;
+  if (need > 0 && slots == nullptr) return VTOKEN_ERR_NULL;
   vtoken::SlotMapArgs a;
   a.num_reqs = batch->num_reqs;
   a.num_tokens = static_cast<int32_t>(batch->num_tokens);
@@ -269,7 +275,47 @@ vtoken_status vtoken_build_slot_mapping(const vtoken_batch* batch, const vtoken_
   a.slot_indptr = slot_indptr;
   a.slots = slots;
   a.slots_capacity = slots_capacity;
+  a.reserve = reserve;
+  a.slot_count = slot_count;
   return hip_status(vtoken::launch_slot_mapping(a, stream));
+}
+
+}  // namespace
+
+vtoken_status vtoken_build_slot_mapping(const vtoken_batch* batch, const vtoken_plan* plan,
+                                        int32_t* slot_indptr, int32_t* slots,
+                                        int64_t slots_capacity, hipStream_t stream) {
+  return build_slots(batch, plan, 0, slot_indptr, nullptr, slots, slots_capacity, stream);
+}
+
+vtoken_status vtoken_build_slot_table(const vtoken_batch* batch, const vtoken_plan* plan,
+                                      int32_t reserve, int32_t* slot_start, int32_t* slot_count,
+                                      int32_t* slots, int64_t slots_capacity,
+                                      hipStream_t stream) {
+  if (batch != nullptr && batch->num_reqs > 0 && slot_count == nullptr) return VTOKEN_ERR_NULL;
+  return build_slots(batch, plan, reserve, slot_start, slot_count, slots, slots_capacity,
+                     stream);
+}
+
+vtoken_status vtoken_append_slots(int32_t num_reqs, const int32_t* append_indptr,
+                                  const int32_t* append_slots, const int32_t* slot_start,
+                                  int32_t* slot_count, int32_t* slots, int32_t* status,
+                                  hipStream_t stream) {
+  if (num_reqs < 0) return VTOKEN_ERR_SHAPE;
+  if (status == nullptr || append_indptr == nullptr) return VTOKEN_ERR_NULL;
+  if (num_reqs > 0 && (append_slots == nullptr || slot_start == nullptr ||
+                       slot_count == nullptr || slots == nullptr)) {
+    return VTOKEN_ERR_NULL;
+  }
+  vtoken::AppendArgs a;
+  a.num_reqs = num_reqs;
+  a.append_indptr = append_indptr;
+  a.append_slots = append_slots;
+  a.slot_start = slot_start;
+  a.slot_count = slot_count;
+  a.slots = slots;
+  a.status = status;
+  return hip_status(vtoken::launch_append_slots(a, stream));
 }
 
 int64_t vtoken_decode_workspace_bytes(int32_t num_reqs, int32_t num_q_heads, int32_t head_dim,
@@ -330,6 +376,7 @@ vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode
   a.workspace = d->workspace;
   a.slot_indptr = slot_indptr;
   a.slots = slots;
+  a.slot_count = d->slot_count;
   return hip_status(vtoken::launch_paged_decode(a, stream));
 }
 
@@ -436,6 +483,6 @@ const char* vtoken_status_string(int32_t status) {
   }
 }
 
-int32_t vtoken_version(void) { return 100; }
+int32_t vtoken_version(void) { return 110; }
 
 }  // extern "C"

@@ -42,8 +42,10 @@ __global__ __launch_bounds__(1024) void slot_indptr_kernel(SlotMapArgs a) {
   int carry = 0;
   for (int base = 0; base < a.num_reqs; base += 1024) {
     const int r = base + tid;
-    int v = r < a.num_reqs ? a.live_count[r] : 0;
-    v = v < 0 ? 0 : v;
+    int live = r < a.num_reqs ? a.live_count[r] : 0;
+    live = live < 0 ? 0 : live;
+    if (r < a.num_reqs && a.slot_count != nullptr) a.slot_count[r] = live;
+    int v = r < a.num_reqs ? live + a.reserve : 0;
     int incl = v;
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
@@ -93,6 +95,29 @@ __global__ __launch_bounds__(1024) void slot_map_kernel(SlotMapArgs a) {
     carry += tot;
     __syncthreads();
   }
+}
+
+// Append-only growth of a slot table: one workgroup per request copies its new slots after
+// its current ones if its region has room.
+__global__ __launch_bounds__(256) void append_status_kernel(AppendArgs a) {
+  if (threadIdx.x == 0) a.status[0] = 0;
+}
+
+__global__ __launch_bounds__(256) void append_slots_kernel(AppendArgs a) {
+  const int r = blockIdx.x;
+  const int a0 = a.append_indptr[r];
+  const int n = a.append_indptr[r + 1] - a0;
+  if (n <= 0) return;
+  const int start = a.slot_start[r];
+  const int cap = a.slot_start[r + 1] - start;
+  const int cnt = a.slot_count[r];
+  if (a0 < 0 || cnt < 0 || (int64_t)cnt + n > cap) {
+    if (threadIdx.x == 0) atomicCAS(a.status, 0, VTOKEN_ERR_CAPACITY);
+    return;
+  }
+  for (int i = threadIdx.x; i < n; i += 256) a.slots[start + cnt + i] = a.append_slots[a0 + i];
+  __syncthreads();
+  if (threadIdx.x == 0) a.slot_count[r] = cnt + n;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -263,7 +288,7 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
   const int r = blockIdx.x / (a.splits * a.num_kv_heads);
   if (r >= a.num_reqs) return;
   const int s0 = a.slot_indptr[r];
-  const int c = a.slot_indptr[r + 1] - s0;
+  const int c = a.slot_count != nullptr ? a.slot_count[r] : a.slot_indptr[r + 1] - s0;
   const int t0 = split * kSplit;
   if (t0 >= c || s0 < 0) return;
   const int nt = c - t0 < kSplit ? c - t0 : kSplit;
@@ -487,7 +512,7 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
   const int r = blockIdx.x / (a.splits * a.num_kv_heads);
   if (r >= a.num_reqs) return;
   const int s0 = a.slot_indptr[r];
-  const int c = a.slot_indptr[r + 1] - s0;
+  const int c = a.slot_count != nullptr ? a.slot_count[r] : a.slot_indptr[r + 1] - s0;
   const int t0 = split * kSplit;
   if (t0 >= c || s0 < 0) return;
   const int nt = c - t0 < kSplit ? c - t0 : kSplit;
@@ -697,7 +722,8 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(AttnArg
   const int r = blockIdx.x / a.num_q_heads;
   if (r >= a.num_reqs) return;
   const int tid = threadIdx.x;
-  const int c = a.slot_indptr[r + 1] - a.slot_indptr[r];
+  const int c = a.slot_count != nullptr ? a.slot_count[r]
+                                        : a.slot_indptr[r + 1] - a.slot_indptr[r];
   const int D = a.head_dim;
   const int64_t rs = D + 2;  // record stride
   float* out = a.out + ((int64_t)r * a.num_q_heads + qh) * D;
@@ -782,6 +808,14 @@ hipError_t launch_decode_k(const AttnArgs& a, hipStream_t stream) {
 }
 
 }  // namespace
+
+hipError_t launch_append_slots(const AppendArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(append_status_kernel, dim3(1), dim3(64), 0, stream, a);
+  if (a.num_reqs > 0) {
+    hipLaunchKernelGGL(append_slots_kernel, dim3(a.num_reqs), dim3(256), 0, stream, a);
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_slot_mapping(const SlotMapArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(slot_indptr_kernel, dim3(1), dim3(1024), 0, stream, a);

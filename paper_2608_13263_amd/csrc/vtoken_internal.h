@@ -105,6 +105,18 @@ struct SlotMapArgs {
   int32_t* slot_indptr;
   int32_t* slots;
   int64_t slots_capacity;
+  int32_t reserve;        // extra room per request (slot table); 0 for a packed mapping
+  int32_t* slot_count;    // slot table counts, or null
+};
+
+struct AppendArgs {
+  int32_t num_reqs;
+  const int32_t* append_indptr;
+  const int32_t* append_slots;
+  const int32_t* slot_start;
+  int32_t* slot_count;
+  int32_t* slots;
+  int32_t* status;
 };
 
 // Paged decode attention of one layer through a slot mapping.
@@ -127,6 +139,7 @@ struct AttnArgs {
   float* workspace;
   const int32_t* slot_indptr;
   const int32_t* slots;
+  const int32_t* slot_count;  // null: counts from slot_indptr
 };
 
 // Arguments of the partial reclamation pass (vtoken_plan_partial).
@@ -175,6 +188,7 @@ struct PlannerArgs {
 hipError_t launch_planner(const PlannerArgs& a, hipStream_t stream);
 
 hipError_t launch_slot_mapping(const SlotMapArgs& a, hipStream_t stream);
+hipError_t launch_append_slots(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_paged_decode(const AttnArgs& a, hipStream_t stream);
 // Tokens one decode workgroup covers: 8 per thread, 256 threads, head_dim / 8 lanes per
 // token (32, 64, 128 or 256 head_dim -> 512, 256, 128, 64 tokens).

@@ -42,7 +42,7 @@ def test_status_codes_match_binding():
     for name, code in codes.items():
         assert B.status_string(code).startswith(name)
     assert B.status_string(12345) == "unknown vtoken status"
-    assert B.load_library().vtoken_version() == 100
+    assert B.load_library().vtoken_version() == 110
 
 
 def test_struct_layouts_match_header(tmp_path):
@@ -157,7 +157,7 @@ def _good_decode(cache, nreq=2, hq=32, max_tokens=700):
     ws = lib_ws = B.load_library().vtoken_decode_workspace_bytes(nreq, hq, cache.head_dim,
                                                                  max_tokens)
     p = _fake_ptr()
-    return B.CDecode(p, p, hq, 1, B.KV_BF16, 0.088, max_tokens, p, ws), lib_ws
+    return B.CDecode(p, p, hq, 1, B.KV_BF16, 0.088, max_tokens, p, ws, None), lib_ws
 
 
 @pytest.mark.parametrize("mutate,code", [
@@ -242,6 +242,25 @@ def test_plan_partial_rejects_bad_arguments():
     assert call(pl=small) == B.STATUS_CODE["VTOKEN_ERR_CAPACITY"]
     small = B.CPlan(p, p, p, p, p, p, p, p, p, 4, 4 * 16 - 1)
     assert call(pl=small) == B.STATUS_CODE["VTOKEN_ERR_CAPACITY"]
+
+
+def test_slot_table_and_append_reject_bad_arguments():
+    lib = B.load_library()
+    _, batch, plan = _good()
+    p = _fake_ptr()
+    # capacity must cover num_tokens + num_reqs * reserve (40 + 2 * 5)
+    assert lib.vtoken_build_slot_table(ctypes.byref(batch), ctypes.byref(plan), 5, p, p, p, 49,
+                                       None) == B.STATUS_CODE["VTOKEN_ERR_CAPACITY"]
+    assert lib.vtoken_build_slot_table(ctypes.byref(batch), ctypes.byref(plan), -1, p, p, p,
+                                       100, None) == B.STATUS_CODE["VTOKEN_ERR_ARGUMENT"]
+    assert lib.vtoken_build_slot_table(ctypes.byref(batch), ctypes.byref(plan), 5, p, None, p,
+                                       100, None) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    assert lib.vtoken_append_slots(-1, p, p, p, p, p, p, None) == \
+        B.STATUS_CODE["VTOKEN_ERR_SHAPE"]
+    assert lib.vtoken_append_slots(2, p, p, p, p, p, None, None) == \
+        B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    assert lib.vtoken_append_slots(2, p, None, p, p, p, p, None) == \
+        B.STATUS_CODE["VTOKEN_ERR_NULL"]
 
 
 def test_binding_fails_loudly_without_library(tmp_path):

@@ -21,7 +21,7 @@ import numpy as np
 import pytest
 
 from gpu_helpers import kv_bytes, torch
-from oracle.attention import decode_batch, slot_mapping
+from oracle.attention import append_to_table, decode_batch, slot_mapping, slot_table
 from oracle.repack import oracle_repack_inputs
 from paper_2608_13263_amd import workloads as W
 
@@ -388,3 +388,63 @@ def test_graph_replay_with_mutable_slot_buffer():
     # a new query in the captured input buffer
     q.copy_(t.randn(R, Hq, D, device="cuda"))
     replay_and_check("new query")
+
+
+def test_slot_table_append_and_decode():
+    """The append-only translation cache (Sec. 3.2): rebuilt after a pass with room for 8
+    more slots per request, then grown by appends (one request past its room, which must be
+    reported and left unchanged); the table equals the oracle's after each step, and decode
+    through it equals decode through a packed mapping of the same slot lists, bit for bit."""
+    t = torch()
+    B = _B()
+    inp = _layout_inputs(47)
+    sh = inp.shape
+    S = sh.block_size
+    R = inp.num_reqs
+    _label(f"slot table: R={R} T={inp.num_tokens}")
+    kv = W.kv_device(sh, inp.num_blocks, 13)
+    orc = oracle_repack_inputs(inp, None)
+    cache, batch, plan, _, _ = _device_pass(inp, kv)
+    start, count, slots = B.build_slot_table(batch, plan, reserve=8)
+    t.cuda.synchronize()
+    o_start, o_count, o_slots = slot_table(orc.token_slot, inp.tok_indptr, inp.seq_lens, 8)
+    assert np.array_equal(start.cpu().numpy().astype(np.int64), o_start)
+    assert np.array_equal(count.cpu().numpy()[:R].astype(np.int64), o_count)
+    got = slots.cpu().numpy().astype(np.int64)
+    for r in range(R):
+        a = int(o_start[r])
+        assert np.array_equal(got[a:a + o_count[r]], o_slots[a:a + o_count[r]])
+    # appends: new tokens in the free blocks the pass did not consume (any valid slots)
+    rng = np.random.default_rng(3)
+    spare = inp.free_list[int(plan.counters[0]):].astype(np.int64)
+    pool = (spare[:, None] * S + np.arange(S)).reshape(-1)
+    ks = rng.integers(0, 6, size=R)
+    ks[R // 2] = 9                                   # past its room of 8
+    new, o = [], 0
+    for k in ks:
+        new.append(pool[o:o + k])
+        o += k
+    app_indptr = _dev_i32(np.concatenate([[0], np.cumsum(ks)]))
+    app_slots = _dev_i32(np.concatenate(new) if o else np.zeros(1))
+    status = B.append_slots(start, count, slots, app_indptr, app_slots)
+    t.cuda.synchronize()
+    o_count2, o_slots2, overflow = append_to_table(o_start, o_count, o_slots, new)
+    assert overflow and int(status[0]) == B.STATUS_CODE["VTOKEN_ERR_CAPACITY"]
+    assert np.array_equal(count.cpu().numpy()[:R].astype(np.int64), o_count2)
+    got = slots.cpu().numpy().astype(np.int64)
+    lists = []
+    for r in range(R):
+        a = int(o_start[r])
+        assert np.array_equal(got[a:a + o_count2[r]], o_slots2[a:a + o_count2[r]])
+        lists.append(o_slots2[a:a + o_count2[r]])
+    # decode through the table vs through a packed mapping of the same lists
+    indptr = np.concatenate([[0], np.cumsum([len(x) for x in lists])])
+    packed = np.concatenate(lists)
+    max_tokens = int(np.diff(indptr).max())
+    q = t.randn(R, 4 * sh.num_kv_heads, sh.head_dim, device="cuda")
+    for layer in range(sh.num_layers):
+        a_out = B.paged_decode(cache, q, start, slots, layer, max_tokens, slot_count=count)
+        b_out = B.paged_decode(cache, q, _dev_i32(indptr), _dev_i32(packed), layer, max_tokens)
+        assert t.equal(a_out, b_out), f"layer {layer}: table and packed decode differ"
+    del kv
+    t.cuda.empty_cache()

@@ -164,7 +164,36 @@ def pin_order_invariance_and_paging(mod):
         assert np.allclose(out[2][h], v[3, h // 2], atol=1e-12), "batched: one-key request"
 
 
-ALL_PINS = [pin_slot_mapping_worked_example, pin_slot_mapping_bruteforce, pin_one_key,
+def pin_slot_table(mod):
+    """The append-only slot table: hand-derived layout of the worked example with room for two
+    more slots per request; reserve 0 is the packed mapping; appends equal the mapping of the
+    extended token table, and a full region is left unchanged."""
+    g = read_golden("worked_example.txt")
+    S, nb = int(g["block_size"][0]), int(g["num_blocks"][0])
+    masks = [r["live"] for r in g["req"]]
+    tables = [r["table"] for r in g["req"]]
+    seq_lens, tok_indptr, bt_indptr, block_ids, live = _csr(masks, tables)
+    res = oracle_repack(seq_lens, tok_indptr, bt_indptr, block_ids, live,
+                        np.asarray([int(x) for x in g["free_list"]]), S, nb)
+    start, count, slots = mod.slot_table(res.token_slot, tok_indptr, seq_lens, 2)
+    assert [int(x) for x in start] == [0, 7, 14, 16, 20, 24], "slot table starts"
+    assert [int(x) for x in count] == [5, 5, 0, 2, 2], "slot table counts"
+    assert [int(x) for x in slots] == [36, 37, 38, 39, 12, -1, -1, 16, 17, 18, 19, 44, -1, -1,
+                                       -1, -1, 48, 49, -1, -1, 56, 63, -1, -1], "slot table"
+    i0, p0 = mod.slot_mapping(res.token_slot, tok_indptr, seq_lens)
+    s0, c0, t0 = mod.slot_table(res.token_slot, tok_indptr, seq_lens, 0)
+    assert list(s0) == list(i0) and list(t0) == list(p0) and list(c0) == list(np.diff(i0))
+    new = [[60, 61], [], [62, 63], [50, 51, 52], [53]]     # request 3 overflows (2 + 3 > 4)
+    cnt, sl, overflow = mod.append_to_table(start, count, slots, new)
+    assert overflow, "a full region must be reported"
+    assert [int(x) for x in cnt] == [7, 5, 2, 2, 3], "counts after the appends"
+    flat = [[int(x) for x in sl[start[r]:start[r] + cnt[r]]] for r in range(5)]
+    assert flat == [[36, 37, 38, 39, 12, 60, 61], [16, 17, 18, 19, 44], [62, 63], [48, 49],
+                    [56, 63, 53]], "appended regions"
+
+
+ALL_PINS = [pin_slot_mapping_worked_example, pin_slot_mapping_bruteforce, pin_slot_table,
+            pin_one_key,
             pin_equal_keys_and_zero_scale, pin_two_keys_logistic, pin_gqa_mapping,
             pin_order_invariance_and_paging]
 
@@ -188,6 +217,11 @@ MUTATIONS = {
                          "int(block_table[p % S]) * S + p // S"),
     "batch_slot_window": ("slots[int(slot_indptr[r]):int(slot_indptr[r + 1])]",
                           "slots[int(slot_indptr[r]):int(slot_indptr[r + 1]) - 1]"),
+    "reserve_ignored": ("np.cumsum(counts + reserve)", "np.cumsum(counts)"),
+    "append_overwrites": ("slots[start[r] + count[r]:start[r] + count[r] + n] = new",
+                          "slots[start[r]:start[r] + n] = new"),
+    "append_past_region": ("if count[r] + n > start[r + 1] - start[r]:",
+                           "if count[r] + n > start[r + 1] - start[r] + 1:"),
 }
 
 
