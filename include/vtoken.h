@@ -207,8 +207,11 @@ vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* ba
 
 /* Tuning entry for the in-place copy; vtoken_repack_inplace uses the default (variant 0).
  *   variant: how a destination block is staged between its reads and its writes:
- *            0 default (= 3), 1 LDS double buffer (direct global->LDS loads; falls back to
- *            2 when two blocks exceed 64 KiB), 2 LDS single buffer, 3 registers
+ *            0 default (4 for block_size <= 64, else 3), 1 LDS double buffer (direct
+ *            global->LDS loads; falls back to
+ *            2 when two blocks exceed 64 KiB), 2 LDS single buffer, 3 registers, 4 registers
+ *            with the next moving block's reads in flight while a block is written
+ *            (block_size <= 64; larger blocks use 3)
  *   grid, order: must be 0 (one workgroup per (request, plane) chain)
  * All variants produce identical bytes. */
 vtoken_status vtoken_repack_inplace_ex(const vtoken_cache* cache, const vtoken_batch* batch,

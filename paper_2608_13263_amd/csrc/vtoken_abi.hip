@@ -143,7 +143,7 @@ vtoken_status vtoken_repack_inplace_ex(const vtoken_cache* cache, const vtoken_b
                                        const vtoken_repack_options* options,
                                        hipStream_t stream) {
   const int variant = options != nullptr ? options->variant : 0;
-  if (variant < 0 || variant > 3 || (options != nullptr && (options->grid != 0 ||
+  if (variant < 0 || variant > 4 || (options != nullptr && (options->grid != 0 ||
                                                             options->order != 0))) {
     return VTOKEN_ERR_ARGUMENT;
   }

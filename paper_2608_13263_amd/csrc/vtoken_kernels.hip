@@ -589,15 +589,153 @@ __global__ __launch_bounds__(kCopyThreads) void repack_inplace_kernel(InplaceArg
   }
 }
 
+// s_waitcnt immediate (gfx9 encoding): wait until at most n vector-memory operations are
+// outstanding, without waiting on the other counters.
+constexpr int vmcnt_imm(int n) {
+  return (n & 0xF) | (((n >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8);
+}
+
+// Pipelined in-place copy (S <= 64): the reads of the next moving block are in flight while
+// the current block is written. Vector-memory counters retire in order, so a wait for a
+// block's reads is only cheap when nothing after them is waited for too: the plan rows and
+// destination blocks of 32 blocks at a time are staged in LDS first (one drain per 32 blocks),
+// the blocks whose rows move are listed there, and the listed blocks are walked with exactly
+// kV reads and kV writes per thread each (rows already in place inside a moving block are
+// read and written back unchanged; units past the block go to a dropped buffer offset), so
+// every wait count is static.
+// Hazards: the sources of destination block b lie at table positions >= b, so the reads of a
+// later listed block never touch the block being written; a block is written only after the
+// barrier that every thread reaches once its own reads of that block have returned, and the
+// reads of earlier blocks that touched it returned before earlier barriers. Blocks left out
+// of the list have all their rows in place: nothing reads from them for another block.
+template <int kV>
+__global__ __launch_bounds__(kCopyThreads) void repack_inplace_pipe_kernel(InplaceArgs a) {
+  constexpr int kChunkBlocks = 32;
+  constexpr int kWaves = kCopyThreads / 64;
+  __shared__ int plan_s[kChunkBlocks * 64];
+  __shared__ int dblk_s[kChunkBlocks];
+  __shared__ int flag_s[kChunkBlocks];
+  __shared__ int list_s[kChunkBlocks];
+  __shared__ int nlist_s;
+  if (a.counters[3] != 0) return;
+  const int P = a.num_planes;
+  const int r = static_cast<int>(blockIdx.x / P);
+  const int plane = static_cast<int>(blockIdx.x - (int64_t)r * P);
+  if (r >= a.num_reqs || !a.admitted[r]) return;
+  const int g0 = a.dst_indptr[r];
+  const int need = a.dst_indptr[r + 1] - g0;
+  const int nb0 = a.new_bt_indptr[r];
+  const int S = a.block_size;
+  if (g0 < 0 || need <= 0 || nb0 < 0 || (int64_t)(g0 + need) * S > a.src_plan_capacity ||
+      (int64_t)nb0 + need > a.new_bt_capacity) {
+    return;
+  }
+  const int U = a.row_units;
+  const int chunk = a.chunk_units;
+  const uint32_t chunk_bytes = static_cast<uint32_t>(chunk) * 16u;
+  const uint32_t magic = a.row_magic;
+  const bool unit_rows = U == 1;
+  const int tid = static_cast<int>(threadIdx.x);
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const uint8_t* pbase = a.kv + (int64_t)plane * a.plane_bytes;
+
+  // kV reads per thread of listed block lb (index within the chunk): the moving rows, and for
+  // the other units the unit itself (an in-place row, or unit 0 past the block)
+  auto load_block = [&](int lb, u32x4 (&regs)[kV]) {
+    const int dslot0 = dblk_s[lb] * S;
+    const int pv = plan_s[lb * S + (lane < S ? lane : S - 1)];
+#pragma unroll
+    for (int v = 0; v < kV; ++v) {
+      const int u = v * kCopyThreads + tid;
+      const int j = unit_rows ? u : static_cast<int>(__umulhi(static_cast<uint32_t>(u), magic));
+      const int col = u - j * U;
+      const int src = __shfl(pv, j & 63, 64);
+      const bool in = u < chunk;
+      const bool mv = in && static_cast<unsigned>(src) < static_cast<unsigned>(a.num_slots) &&
+                      src != dslot0 + j;
+      const int64_t off = mv ? (int64_t)src * a.row_bytes + col * 16
+                             : (int64_t)dslot0 * a.row_bytes + (in ? (int64_t)u * 16 : 0);
+      const uint8_t* gsrc = pbase + off;
+      regs[v] = load16<true>(reinterpret_cast<const u32x4*>(gsrc));
+    }
+  };
+  auto store_block = [&](int lb, const u32x4 (&regs)[kV]) {
+    uint8_t* dptr = uniform_ptr(a.kv + (int64_t)plane * a.plane_bytes +
+                                (int64_t)dblk_s[lb] * S * a.row_bytes);
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(dptr, 0, chunk_bytes, kBufferDword3);
+#pragma unroll
+    for (int v = 0; v < kV; ++v) {
+      const int u = v * kCopyThreads + tid;
+      const uint32_t off = u < chunk ? static_cast<uint32_t>(u) * 16u : kDropOffset;
+      __builtin_amdgcn_raw_buffer_store_b128(regs[v], rsrc, off, 0, 16);
+    }
+  };
+
+  for (int c0 = 0; c0 < need; c0 += kChunkBlocks) {
+    const int nb = need - c0 < kChunkBlocks ? need - c0 : kChunkBlocks;
+    __syncthreads();  // the previous chunk is done with the LDS arrays
+    for (int i = tid; i < nb * S; i += kCopyThreads) {
+      plan_s[i] = a.src_plan[(int64_t)(g0 + c0) * S + i];
+    }
+    if (tid < nb) dblk_s[tid] = a.new_block_ids[nb0 + c0 + tid];
+    __syncthreads();
+    // which blocks move (a block with an invalid destination is left alone)
+    for (int b = wave; b < nb; b += kWaves) {
+      const int dblk = dblk_s[b];
+      const int pv = lane < S ? plan_s[b * S + lane] : -1;
+      const bool row_moves = static_cast<unsigned>(dblk) < static_cast<unsigned>(a.num_blocks) &&
+                             lane < S && static_cast<unsigned>(pv) <
+                             static_cast<unsigned>(a.num_slots) && pv != dblk * S + lane;
+      const uint64_t m = __ballot(row_moves);
+      if (lane == 0) flag_s[b] = m != 0;
+    }
+    __syncthreads();
+    if (wave == 0) {
+      const bool f = lane < nb && flag_s[lane] != 0;
+      const uint64_t m = __ballot(f);
+      if (f) list_s[lanes_below(m)] = lane;
+      if (lane == 0) nlist_s = __popcll(m);
+    }
+    __syncthreads();
+    const int nl = nlist_s;
+    if (nl == 0) continue;
+    u32x4 ra[kV], rb[kV];
+    load_block(list_s[0], ra);
+    for (int i = 0; i < nl; i += 2) {
+      // past the end of the list the next reads repeat the last block (discarded)
+      load_block(list_s[i + 1 < nl ? i + 1 : nl - 1], rb);
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(kV));     // block i's reads, not block i+1's
+      __syncthreads();
+      store_block(list_s[i], ra);
+      if (i + 1 < nl) {
+        load_block(list_s[i + 2 < nl ? i + 2 : nl - 1], ra);
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(kV));
+        __syncthreads();
+        store_block(list_s[i + 1], rb);
+      }
+    }
+  }
+}
+
 template <int kV, bool kSmallS>
 hipError_t launch_inplace_v(const InplaceArgs& a, int variant, hipStream_t stream) {
   const int64_t grid = (int64_t)a.num_reqs * a.num_planes;
   const int64_t chunk_bytes = (int64_t)a.chunk_units * 16;
-  // default: registers (measured fastest); LDS double buffer when asked and two fit
+  // default: pipelined registers for S <= 64, else registers (measured fastest); LDS double
+  // buffer when asked and two fit
   int stage = variant == 1 ? kLdsDouble : variant == 2 ? kLdsSingle : kRegisters;
   if (stage == kLdsDouble && chunk_bytes * 2 > kMaxInplaceChunkBytes) stage = kLdsSingle;
   const dim3 g(static_cast<unsigned>(grid));
   const dim3 t(kCopyThreads);
+  if constexpr (kSmallS) {
+    if (variant == 4 || variant == 0) {
+      auto kernel = repack_inplace_pipe_kernel<kV>;
+      hipLaunchKernelGGL(kernel, g, t, 0, stream, a);
+      return hipGetLastError();
+    }
+  }
   if (stage == kLdsDouble) {
     auto kernel = repack_inplace_kernel<kV, kSmallS, kLdsDouble>;
     hipLaunchKernelGGL(kernel, g, t, static_cast<size_t>(2 * chunk_bytes), stream, a);
@@ -625,7 +763,7 @@ hipError_t launch_inplace_s(const InplaceArgs& a, int variant, hipStream_t strea
 }  // namespace
 
 hipError_t launch_repack_inplace(const InplaceArgs& a, int variant, hipStream_t stream) {
-  if (variant < 0 || variant > 3) return hipErrorInvalidValue;
+  if (variant < 0 || variant > 4) return hipErrorInvalidValue;
   if ((int64_t)a.num_reqs * a.num_planes <= 0) return hipSuccess;
   if ((int64_t)a.chunk_units * 16 > kMaxInplaceChunkBytes) return hipErrorInvalidValue;
   return a.block_size <= 64 ? launch_inplace_s<true>(a, variant, stream)

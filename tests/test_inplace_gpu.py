@@ -100,7 +100,7 @@ def test_inplace_second_pass_moves_nothing():
     t.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("variant", [1, 2, 3])
+@pytest.mark.parametrize("variant", [1, 2, 3, 4])
 @pytest.mark.parametrize("S", [16, 32])
 def test_inplace_staging_variants(variant, S):
     # LDS double buffer, LDS single buffer, registers: identical bytes
@@ -110,3 +110,26 @@ def test_inplace_staging_variants(variant, S):
                                       for n in rng.integers(50, 900, 6)]
     full_parity(W.from_masks(masks, shape, free_blocks=0, seed=7), seed=11, inplace=True,
                 variant=variant)
+
+
+@pytest.mark.parametrize("S", [1, 2, 16, 32, 48, 64])
+def test_inplace_pipelined_variant(S):
+    """Variant 4 (reads of the next moving block in flight while one is written, plans staged
+    32 blocks at a time): overlap-heavy masks, chains far longer than 32 blocks with identity
+    blocks between moving ones, and rows that do not fill the last unit round."""
+    rng = np.random.default_rng(400 + S)
+    shape = W.KVShape(1, 3, 8, S, "fp16")            # 48-byte rows: chunks of 3*S units
+    n = 80 * S + 5
+    long_masks = [
+        [0] + [1] * (n - 1),                                        # 80-block shifting chain
+        [1] * (40 * S) + [0] + [1] * (n - 40 * S - 1),              # 40 identity blocks first
+        ([1] * S + [0] * (S // 2 + 1) + [1] * (S // 2)) * 30,       # alternating blocks
+        list((rng.random(n) < 0.9).astype(int)),
+    ]
+    inp = W.from_masks(_overlap_masks(S, rng) + long_masks, shape, free_blocks=4, seed=S)
+    full_parity(inp, seed=S, inplace=True, variant=4)
+    shape2 = W.KVShape(2, 4, 128, S, "bf16")                  # 1 KiB rows, chunks <= 64 KiB
+    masks2 = _overlap_masks(S, rng) + [list((rng.random(int(m)) < 0.6).astype(int))
+                                       for m in rng.integers(50, 60 * S, 4)]
+    full_parity(W.from_masks(masks2, shape2, free_blocks=0, seed=9), seed=12, inplace=True,
+                variant=4)
