@@ -21,13 +21,24 @@ from paper_2608_13263_amd import workloads as W
 pytestmark = pytest.mark.gpu
 
 
-def _moves(orc, inp):
+def _moves(orc, inp, inplace=False):
+    """(source slot, destination slot) of every row the oracle moves; the plan's destination
+    block g is free_list[g] out of place, the request's own k-th block in place."""
     S = inp.shape.block_size
     sp = np.asarray(orc.src_plan, dtype=np.int64).reshape(orc.used, S)
     g, j = np.nonzero(sp >= 0)
     src = sp[g, j]
-    dst = np.asarray(inp.free_list, dtype=np.int64)[g] * S + j
-    return src, dst
+    if inplace:
+        dest = np.empty(orc.used, dtype=np.int64)
+        for r in np.nonzero(np.asarray(orc.admitted))[0]:
+            a, b = int(orc.dst_indptr[r]), int(orc.dst_indptr[r + 1])
+            n0 = int(orc.new_bt_indptr[r])
+            dest[a:b] = orc.new_block_ids[n0:n0 + (b - a)]
+    else:
+        dest = np.asarray(inp.free_list, dtype=np.int64)
+    dst = dest[g] * S + j
+    keep = src != dst                       # rows already in place are not moves
+    return src[keep], dst[keep]
 
 
 def _plane_bytes(kv, p, shape):
@@ -71,10 +82,10 @@ def run_full(inp, seed, sample_planes, clone=True):
     t.cuda.empty_cache()
 
 
-def _check_all_planes(kv, before, clone, orc_meta, inp):
+def _check_all_planes(kv, before, clone, orc_meta, inp, inplace=False):
     t = torch()
     shape = inp.shape
-    src, dst = _moves(orc_meta, inp)
+    src, dst = _moves(orc_meta, inp, inplace)
     src_t = t.from_numpy(src).cuda()
     dst_t = t.from_numpy(dst).cuda()
     for p in range(shape.num_planes):
@@ -206,6 +217,82 @@ def test_llama3_8b_scissorhands_partial_rounds():
         if moved_total > 0:
             break
     assert moved_total > 0, "no round triggered the partial pass"
+    del kv
+    gc.collect()
+    t.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("config", ["llama3_8b_h2o", "llama3_70b_bf16"])
+def test_inplace_full_size(config):
+    """In-place mode at full size in the launch configuration the benchmark times: every
+    metadata output equals the oracle's in-place mode, sampled planes byte-exact against the
+    oracle run on their pre-call bytes, every plane by row checksums of the moves (applied
+    to the pre-call rows all at once, the definition of a move)."""
+    t = torch()
+    if config == "llama3_8b_h2o":
+        inp = W.llama3_8b_h2o(301)
+        sample = [0, 33, 63]
+    else:
+        budget = min(240 * 2 ** 30, int(0.85 * _budget()))
+        inp = W.llama3_70b_h2o(501, keep=0.3, dtype="bf16", pool_bytes=budget)
+        sample = [0, 81, 159]
+    shape = inp.shape
+    print(f"[gpu] in-place full-size {inp.name}: pool {inp.pool_bytes() / 2**30:.1f} GiB",
+          flush=True)
+    orc_meta = oracle_repack_inputs(inp, inplace=True)
+    kv = W.kv_device(shape, inp.num_blocks, 7)
+    pre = np.stack([_plane_bytes(kv, p, shape).cpu().numpy() for p in sample])
+    before = t.stack([_row_sums(kv, p, shape) for p in range(shape.num_planes)])
+    gpu = gpu_pass(inp, kv, inplace=True, label=f"in-place full-size {inp.name}")
+    assert_plan_equal(gpu, orc_meta)
+    orc = oracle_repack_inputs(inp, pre, inplace=True)
+    post = np.stack([_plane_bytes(kv, p, shape).cpu().numpy() for p in sample])
+    assert_kv_equal(post, orc.kv)
+    _check_all_planes(kv, before, False, orc_meta, inp, inplace=True)
+    src, _ = _moves(orc_meta, inp, True)
+    print(f"[gpu] in-place full-size {inp.name}: {orc_meta.n_admitted} requests, {len(src)} rows "
+          f"moved per plane", flush=True)
+    del kv, before
+    gc.collect()
+    t.cuda.empty_cache()
+
+
+def test_decode_full_size_sampled():
+    """Decode over the full Llama-3-8B H2O cache after a pass, in the launch configuration the
+    decode benchmark times (every request, layers 0 and 31): eight sampled requests against
+    the float64 oracle computed one by one from their own K/V rows."""
+    t = torch()
+    from oracle.attention import dense_decode, slot_mapping
+    from paper_2608_13263_amd import binding as B
+    inp = W.llama3_8b_h2o(301)
+    shape = inp.shape
+    S, H, D = shape.block_size, shape.num_kv_heads, shape.head_dim
+    kv = W.kv_device(shape, inp.num_blocks, 8)
+    orc = oracle_repack_inputs(inp)
+    gpu = gpu_pass(inp, kv, label="decode full-size pass")
+    assert_plan_equal(gpu, orc)
+    cache = B.KVCache(kv, shape.num_layers, H, D, S)
+    indptr, slots = slot_mapping(orc.token_slot, inp.tok_indptr, inp.seq_lens)
+    d_indptr = t.from_numpy(indptr.astype(np.int32)).cuda()
+    d_slots = t.from_numpy(slots.astype(np.int32)).cuda()
+    max_tokens = int(np.diff(indptr).max())
+    q = t.randn(inp.num_reqs, 4 * H, D, device="cuda", generator=t.Generator(device="cuda").manual_seed(3))
+    rng = np.random.default_rng(9)
+    sample = rng.choice(inp.num_reqs, size=8, replace=False)
+    worst = 0.0
+    for layer in (0, shape.num_layers - 1):
+        out = B.paged_decode(cache, q, d_indptr, d_slots, layer, max_tokens).cpu().numpy()
+        kp = kv[2 * layer].reshape(-1, H, D)
+        vp = kv[2 * layer + 1].reshape(-1, H, D)
+        for r in sample:
+            sl = t.from_numpy(slots[indptr[r]:indptr[r + 1]]).cuda()
+            k = kp[sl].float().cpu().numpy()
+            v = vp[sl].float().cpu().numpy()
+            ref = dense_decode(q[r].cpu().numpy().astype(np.float64), k, v)
+            np.testing.assert_allclose(out[r], ref, atol=1e-4, rtol=1e-4)
+            worst = max(worst, float(np.abs(out[r] - ref).max()))
+    print(f"[gpu] decode full-size: 8 sampled requests x 2 layers, max |diff| {worst:.2e}",
+          flush=True)
     del kv
     gc.collect()
     t.cuda.empty_cache()
