@@ -415,7 +415,9 @@ def run_inplace(args, inp, kv, cache, batch, plan, stream):
                    "rows_moved": moved, "rows_in_place": repacked - moved,
                    "pool_gib": round(inp.pool_bytes() / 2 ** 30, 2),
                    "bytes_alg_per_step": bytes_alg, "admitted": cnt[1], "freed_blocks": cnt[2]},
-        "roofline": {"bound": "hbm", "kernel": "repack_inplace_kernel",
+        "roofline": {"bound": "hbm",
+                     "kernel": ("repack_inplace_pipe_kernel" if sh.block_size <= 64
+                                else "repack_inplace_kernel"),
                      "achieved": round(bytes_alg / (kern / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s",
                      "frac": round(bytes_alg / (kern / 1e3) / 1e9 / HBM_PEAK_GBS, 4),

@@ -608,6 +608,8 @@ constexpr int vmcnt_imm(int n) {
 // barrier that every thread reaches once its own reads of that block have returned, and the
 // reads of earlier blocks that touched it returned before earlier barriers. Blocks left out
 // of the list have all their rows in place: nothing reads from them for another block.
+constexpr int kLongestFirstMaxReqs = 256;
+
 template <int kV>
 __global__ __launch_bounds__(kCopyThreads) void repack_inplace_pipe_kernel(InplaceArgs a) {
   constexpr int kChunkBlocks = 32;
@@ -617,11 +619,32 @@ __global__ __launch_bounds__(kCopyThreads) void repack_inplace_pipe_kernel(Inpla
   __shared__ int flag_s[kChunkBlocks];
   __shared__ int list_s[kChunkBlocks];
   __shared__ int nlist_s;
+  __shared__ int r_s;
   if (a.counters[3] != 0) return;
   const int P = a.num_planes;
-  const int r = static_cast<int>(blockIdx.x / P);
-  const int plane = static_cast<int>(blockIdx.x - (int64_t)r * P);
-  if (r >= a.num_reqs || !a.admitted[r]) return;
+  // longest chains first: workgroup k*P + plane takes the request with the k-th longest
+  // chain (ties by index), so the last workgroups to start are short ones and the tail of the
+  // launch is short; the ranking costs O(R) per thread, so it is done for R <= 256 only
+  const int k = static_cast<int>(blockIdx.x / P);
+  const int plane = static_cast<int>(blockIdx.x - (int64_t)k * P);
+  if (k >= a.num_reqs) return;
+  int r = k;
+  if (a.num_reqs <= kLongestFirstMaxReqs) {
+    if (threadIdx.x == 0) r_s = k;
+    __syncthreads();
+    for (int i = threadIdx.x; i < a.num_reqs; i += kCopyThreads) {
+      const int ni = a.admitted[i] ? a.dst_indptr[i + 1] - a.dst_indptr[i] : 0;
+      int rank = 0;
+      for (int j = 0; j < a.num_reqs; ++j) {
+        const int nj = a.admitted[j] ? a.dst_indptr[j + 1] - a.dst_indptr[j] : 0;
+        rank += (nj > ni) || (nj == ni && j < i);
+      }
+      if (rank == k) r_s = i;
+    }
+    __syncthreads();
+    r = r_s;
+  }
+  if (!a.admitted[r]) return;
   const int g0 = a.dst_indptr[r];
   const int need = a.dst_indptr[r + 1] - g0;
   const int nb0 = a.new_bt_indptr[r];

@@ -133,3 +133,26 @@ def test_inplace_pipelined_variant(S):
                                        for m in rng.integers(50, 60 * S, 4)]
     full_parity(W.from_masks(masks2, shape2, free_blocks=0, seed=9), seed=12, inplace=True,
                 variant=4)
+
+
+@pytest.mark.parametrize("R", [255, 256, 257, 700])
+def test_inplace_pipelined_many_requests(R):
+    """Variant 4 hands chains out longest first when there are at most 256 requests and in
+    request order above that; both sides of the switch, with equal chain lengths (ties broken by
+    request index) and requests that move nothing."""
+    rng = np.random.default_rng(500 + R)
+    S = 16
+    shape = W.KVShape(1, 2, 16, S, "fp16")
+    masks = []
+    for i in range(R):
+        n = int(rng.integers(1, 6 * S))
+        kind = i % 4
+        if kind == 0:
+            m = [1] * n                                           # nothing moves
+        elif kind == 1:
+            m = [0] + [1] * (3 * S)                               # equal lengths: ties
+        else:
+            m = list((rng.random(n) < 0.6).astype(int))
+        masks.append(m)
+    full_parity(W.from_masks(masks, shape, free_blocks=0, seed=R), seed=R, inplace=True,
+                variant=4)
