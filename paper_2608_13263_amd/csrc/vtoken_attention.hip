@@ -248,6 +248,50 @@ __device__ __forceinline__ i16x4 lds_read_tr16(const uint8_t* lds_addr) {
       (lds_i16x4*)(reinterpret_cast<uintptr_t>(lds_addr)));
 }
 
+// Cross-lane steps of the decode without the LDS crossbar (ds_bpermute): DPP rotations inside
+// 16-lane rows and the gfx950 row swaps (v_permlane16_swap, v_permlane32_swap). Every lane of
+// the wave must be active.
+//
+// Lane i of each 16-lane row receives lane (i - kN) mod 16 of its row.
+template <int kN>
+__device__ __forceinline__ float row_ror(float x) {
+  static_assert(kN > 0 && kN < 16, "row rotation");
+  return __int_as_float(
+      __builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x120 + kN, 0xF, 0xF, false));
+}
+
+// x combined with the value of lane i ^ 16 (kDist 16) or i ^ 32 (kDist 32): the swap leaves
+// the even rows' values in one result and the odd rows' (the low half's and the high half's)
+// in the other, in every lane.
+template <int kDist, bool kMax>
+__device__ __forceinline__ float xor_combine(float x) {
+  const uint32_t u = __float_as_uint(x);
+  float a, b;
+  if constexpr (kDist == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    a = __uint_as_float(r[0]);
+    b = __uint_as_float(r[1]);
+  } else {
+    static_assert(kDist == 32, "16 or 32");
+    const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    a = __uint_as_float(r[0]);
+    b = __uint_as_float(r[1]);
+  }
+  return kMax ? fmaxf(a, b) : a + b;
+}
+
+// Sum (or maximum) over the lanes i, i + kStride, i + 2 kStride, ... of the wave (kStride a
+// power of two below 64); every lane receives its class's result.
+template <int kStride, bool kMax>
+__device__ __forceinline__ float lanes_reduce(float x) {
+  if constexpr (kStride <= 1) x = kMax ? fmaxf(x, row_ror<1>(x)) : x + row_ror<1>(x);
+  if constexpr (kStride <= 2) x = kMax ? fmaxf(x, row_ror<2>(x)) : x + row_ror<2>(x);
+  if constexpr (kStride <= 4) x = kMax ? fmaxf(x, row_ror<4>(x)) : x + row_ror<4>(x);
+  if constexpr (kStride <= 8) x = kMax ? fmaxf(x, row_ror<8>(x)) : x + row_ror<8>(x);
+  if constexpr (kStride <= 16) x = xor_combine<16, kMax>(x);
+  return xor_combine<32, kMax>(x);
+}
+
 // Variant for GQA groups up to 4: scores on the matrix cores, weighted V sum on the vector ALUs.
 //
 // kKind: element type; kD: head_dim (32, 64, 128, 256); kG: query heads per KV head.
@@ -376,8 +420,7 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
   for (int g = 0; g < kG; ++g) {
     float m = -INFINITY;
     for (int t = tid; t < nt; t += kAttnThreads) m = fmaxf(m, p_s[g][t]);
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) m = fmaxf(m, __shfl_xor(m, d, 64));
+    m = lanes_reduce<1, true>(m);
     if (lane == 0) red_s[wave][g] = m;
   }
   __syncthreads();
@@ -396,8 +439,7 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
       p_s[g][t] = e;
       l += e;
     }
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) l += __shfl_xor(l, d, 64);
+    l = lanes_reduce<1, false>(l);
     if (lane == 0) red_s[wave][g] = l;
   }
   __syncthreads();
@@ -436,8 +478,7 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
   for (int g = 0; g < kG; ++g)
 #pragma unroll
     for (int e = 0; e < kPer; ++e)
-#pragma unroll
-      for (int d = kLanes; d < 64; d <<= 1) acc[g][e] += __shfl_xor(acc[g][e], d, 64);
+      acc[g][e] = lanes_reduce<kLanes, false>(acc[g][e]);
   if (lane < kLanes) {
 #pragma unroll
     for (int g = 0; g < kG; ++g)
@@ -460,24 +501,26 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
   }
 }
 
-// Variant for large GQA groups (kG = 8), where the weighted V sum (2 kG flops per V byte)
-// would bound the vector ALUs: both products on the matrix cores.
+// Variant for GQA groups of 8, where the weighted V sum (2 kG flops per V byte) would bound
+// the vector ALUs: both products on the matrix cores.
 //
-// kKind: element type; kD: head_dim (32, 64, 128, 256); kG: query heads per KV head.
+// kKind: element type; kD: head_dim (32, 64, 128, 256); kG = 8 query heads per KV head.
 //
 // One workgroup (4 waves) covers kSplit = 16384 / kD tokens of one (request, KV head); wave w
 // owns tokens [w*kTW, (w+1)*kTW), kTW = kSplit / 4, and computes for them, on the matrix
 // cores (MFMA 16x16x32, fp16 for fp16 caches, bf16 otherwise; fp8 widened to bf16):
-//   scores  S[token][head] = K_tile (16 x kD) . Q^T (kD x 16: the kG query heads, zero-padded),
-//           the float32 query split into high and low 16-bit parts (q = hi + lo to ~2^-17),
-//           each multiplied, so the scores keep float32 accuracy;
-//   weights p = exp(S - m_w) with the wave's own maximum m_w per head, l_w = sum of p;
-//   values  O_w[head][d] = P (16 x 32 tokens) . V (32 tokens x 16 elements) per 16-element
-//           chunk, P again split into high and low parts. V goes through LDS (16-bit rows,
-//           padded by 32 bytes against bank conflicts) and comes back in operand layout by
-//           transpose reads. The operand layout fixes which tokens a lane holds: lane l has
-//           head l%16 and, of each 32-token chunk, tokens 4*(l/16)..+3 of its first
-//           16-token tile and the same of its second; the V rows are read in that order.
+//   scores  S[token][col] = K_tile (16 x kD) . Q2^T (kD x 16). The float32 query is split into
+//           high and low 16-bit parts (q = hi + lo to ~2^-17): column c < 8 of Q2 is the high
+//           part of head c, column c + 8 its low part, so one product carries both and the
+//           score of head c is S[.][c] + S[.][c + 8] (float32 accuracy, no padded columns);
+//   weights p = exp(score - m_w) with the wave's own maximum m_w per head, l_w = sum of p;
+//   values  O2[row][d] = P2 (16 x 32 tokens) . V (32 tokens x 16 elements) per 16-element
+//           chunk, row c < 8 of P2 the high part of head c's weights, row c + 8 their low
+//           part, so O_w[c] = O2[c] + O2[c + 8]. V goes through LDS (16-bit rows, padded by
+//           32 bytes against bank conflicts) and comes back in operand layout by transpose
+//           reads. The operand layout fixes which tokens a lane holds: lane l has column
+//           l%16 and, of each 32-token chunk, tokens 4*(l/16)..+3 of its first 16-token tile
+//           and the same of its second; the V rows are read in that order.
 // The four waves are merged with the usual max-rescaling into the split's record.
 // Every thread issues all of its K and V loads (8 + 8 pieces) before any arithmetic.
 // Non-finite K or V values are outside the contract (a zero weight times an infinite value
@@ -501,6 +544,7 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
   constexpr int kRowB = kD * 2 + 32;                 // LDS bytes per V row
   static_assert(kTiles * 16 == kTW && kItV == kDecodeTokensPerThread, "split geometry");
   constexpr int kMergeB = kWaves * kG * (kD + 2) * 4;
+  static_assert(kG == 8, "the high and low parts fill the 16 operand columns");
   constexpr int kLdsB = kSplit * kRowB > kMergeB ? kSplit * kRowB : kMergeB;
   __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsB];
 
@@ -524,22 +568,19 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
   const int row = lane & 15;    // token of a tile (K operand) / head (Q, P operands)
   const int wt0 = wave * kTW;   // first token of this wave
 
-  // ---- query operand first (needed first): head `row` (zero past kG), scaled, split into
-  // high and low parts; the load is unconditional (a padded head re-reads head 0), a
-  // conditional load would wait for every outstanding K/V load
-  OpT qh[kChunks], ql[kChunks];
+  const bool low = row >= 8;    // this lane's column / P row holds low parts
+  // ---- query operand first (needed first): column `row` = head row % 8, scaled, its high
+  // part (row < 8) or its low part (row >= 8)
+  OpT qop[kChunks];
   {
-    const bool real = row < kG;
-    const float* qrow = a.q + ((int64_t)r * a.num_q_heads + h * kG + (real ? row : 0)) * kD;
+    const float* qrow = a.q + ((int64_t)r * a.num_q_heads + h * kG + (row & 7)) * kD;
 #pragma unroll
     for (int ch = 0; ch < kChunks; ++ch) {
 #pragma unroll
       for (int e = 0; e < kPer; ++e) {
-        const float qv = qrow[ch * 32 + grp * kPer + e] * a.scale;
-        const float q = real ? qv : 0.f;
+        const float q = qrow[ch * 32 + grp * kPer + e] * a.scale;
         const ElemT hi = static_cast<ElemT>(q);
-        qh[ch][e] = hi;
-        ql[ch][e] = static_cast<ElemT>(q - static_cast<float>(hi));
+        qop[ch][e] = low ? static_cast<ElemT>(q - static_cast<float>(hi)) : hi;
       }
     }
   }
@@ -571,7 +612,8 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
                                              head0 + vpiece * kPer * kElem);
   }
 
-  // ---- scores of this wave's tiles: lane holds tokens wt0 + 16i + 4*grp + j, head `row`
+  // ---- scores of this wave's tiles: lane holds tokens wt0 + 16i + 4*grp + j of head row % 8
+  // (columns row and row ^ 8 summed: lanes row and row + 8 then hold the same scores)
   f32x4 sc[kTiles];
 #pragma unroll
   for (int i = 0; i < kTiles; ++i) {
@@ -580,12 +622,11 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
     for (int ch = 0; ch < kChunks; ++ch) {
       PieceT w = kw[i][ch];
       if (!kok[i]) w = PieceT{};
-      const OpT kop = k_operand<kKind>(w);
-      acc = score_mfma<kKind>(kop, qh[ch], acc);
-      acc = score_mfma<kKind>(kop, ql[ch], acc);
+      acc = score_mfma<kKind>(k_operand<kKind>(w), qop[ch], acc);
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
+      acc[j] += row_ror<8>(acc[j]);
       if (wt0 + 16 * i + 4 * grp + j >= nt) acc[j] = -INFINITY;
     }
     sc[i] = acc;
@@ -600,26 +641,23 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
     *reinterpret_cast<u32x4*>(lds + tl * kRowB + vpiece * 16) = v_row16<kKind>(w);
   }
 
-  // ---- wave-local softmax per head (the four lanes of a head share `row`)
+  // ---- wave-local softmax per head (the four lanes of a column share `row`)
   float m = -INFINITY;
 #pragma unroll
   for (int i = 0; i < kTiles; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) m = fmaxf(m, sc[i][j]);
-  m = fmaxf(m, __shfl_xor(m, 16, 64));
-  m = fmaxf(m, __shfl_xor(m, 32, 64));
+  m = lanes_reduce<16, true>(m);
   const float msafe = m == -INFINITY ? 0.f : m;   // a wave with no valid token
   float l = 0.f;
 #pragma unroll
   for (int i = 0; i < kTiles; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const float e = __expf(sc[i][j] - msafe);
-      sc[i][j] = row < kG ? e : 0.f;
+      sc[i][j] = __expf(sc[i][j] - msafe);
       l += sc[i][j];
     }
-  l += __shfl_xor(l, 16, 64);
-  l += __shfl_xor(l, 32, 64);
+  l = lanes_reduce<16, false>(l);
   __syncthreads();  // V rows written (each wave reads only its own rows)
 
   // ---- O_w = P . V on the matrix cores
@@ -628,15 +666,15 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
   for (int dc = 0; dc < kDC; ++dc) o[dc] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int kc = 0; kc < kKC; ++kc) {
-    // A operand: head `row`, tokens 4*grp..+3 of tile 2kc then of tile 2kc+1 (zero if absent)
-    OpT ph, pl;
+    // A operand: row `row` (head row % 8, high or low part), tokens 4*grp..+3 of tile 2kc
+    // then of tile 2kc+1 (zero if absent)
+    OpT pop;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int tile = 2 * kc + (j >> 2);
       const float p = tile < kTiles ? sc[tile < kTiles ? tile : 0][j & 3] : 0.f;
       const ElemT hi = static_cast<ElemT>(p);
-      ph[j] = hi;
-      pl[j] = static_cast<ElemT>(p - static_cast<float>(hi));
+      pop[j] = low ? static_cast<ElemT>(p - static_cast<float>(hi)) : hi;
     }
     // B operand rows: lane 16*grp + rho supplies the row of token 4*grp + rho/4 of the first
     // tile (then of the second), elements 4*(rho%4)..+3 of the 16-element chunk
@@ -651,10 +689,14 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
       typedef short i16x8 __attribute__((ext_vector_type(8)));
       const i16x8 xv = {x1[0], x1[1], x1[2], x1[3], x2[0], x2[1], x2[2], x2[3]};
       const OpT vop = __builtin_bit_cast(OpT, xv);
-      o[dc] = score_mfma<kKind>(ph, vop, o[dc]);
-      o[dc] = score_mfma<kKind>(pl, vop, o[dc]);
+      o[dc] = score_mfma<kKind>(pop, vop, o[dc]);
     }
   }
+  // result rows 4*grp + j: high parts in lane groups 0, 1 (heads 0-7), low parts 32 lanes up
+#pragma unroll
+  for (int dc = 0; dc < kDC; ++dc)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) o[dc][j] = xor_combine<32, false>(o[dc][j]);
   __syncthreads();  // the LDS rows are reused for the merge
 
   // ---- merge the four waves: [m_w, l_w] and O_w[head][d] per wave into LDS
@@ -663,13 +705,14 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
     mrg[(wave * kG + row) * (kD + 2)] = m;
     mrg[(wave * kG + row) * (kD + 2) + 1] = l;
   }
+  if (grp < 2) {
 #pragma unroll
-  for (int dc = 0; dc < kDC; ++dc)
+    for (int dc = 0; dc < kDC; ++dc)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int g = 4 * grp + j;                     // result row = head
-      if (g < kG) mrg[(wave * kG + g) * (kD + 2) + 2 + dc * 16 + row] = o[dc][j];
-    }
+      for (int j = 0; j < 4; ++j) {
+        mrg[(wave * kG + 4 * grp + j) * (kD + 2) + 2 + dc * 16 + row] = o[dc][j];
+      }
+  }
   __syncthreads();
   for (int i = tid; i < kG * kD; i += kAttnThreads) {
     const int g = i / kD, d = i - g * kD;
@@ -700,17 +743,14 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
 // 128 splits per chunk with their weights in LDS), so no thread walks the splits alone.
 constexpr int kCombineThreads = 128;
 
-__device__ __forceinline__ float block_reduce(float v, bool is_max, float* red) {
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const float o = __shfl_xor(v, d, 64);
-    v = is_max ? fmaxf(v, o) : v + o;
-  }
+template <bool kMax>
+__device__ __forceinline__ float block_reduce(float v, float* red) {
+  v = lanes_reduce<1, kMax>(v);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
   __syncthreads();
   v = red[0];
 #pragma unroll
-  for (int w = 1; w < kCombineThreads / 64; ++w) v = is_max ? fmaxf(v, red[w]) : v + red[w];
+  for (int w = 1; w < kCombineThreads / 64; ++w) v = kMax ? fmaxf(v, red[w]) : v + red[w];
   __syncthreads();
   return v;
 }
@@ -736,10 +776,10 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(AttnArg
   const float* rec0 = a.workspace + ((int64_t)r * a.num_q_heads + qh) * a.splits * rs;
   float m = -INFINITY;
   for (int s = tid; s < ns; s += kCombineThreads) m = fmaxf(m, rec0[s * rs]);
-  const float M = block_reduce(m, true, red);
+  const float M = block_reduce<true>(m, red);
   float l = 0.f;
   for (int s = tid; s < ns; s += kCombineThreads) l += rec0[s * rs + 1] * __expf(rec0[s * rs] - M);
-  const float L = block_reduce(l, false, red);
+  const float L = block_reduce<false>(l, red);
   const float inv = 1.f / L;
   // each thread owns head elements d = tid, tid + 128 (head_dim <= 256)
   float v0 = 0.f, v1 = 0.f;

@@ -152,6 +152,9 @@ DECODE_CASES = [
     ("fp8_e4m3", 2, 64, 2, 16),
     ("fp8_e4m3", 2, 256, 4, 16),
     ("fp8_e4m3", 4, 32, 1, 16),
+    ("bf16", 2, 64, 8, 16),    # G = 8 at the other head sizes
+    ("bf16", 1, 256, 8, 16),
+    ("fp8_e4m3", 2, 32, 8, 16),
 ]
 
 
