@@ -316,8 +316,11 @@ vtoken_status vtoken_append_slots(int32_t num_reqs, const int32_t* append_indptr
  * and query head qh (GQA: KV head qh / (num_q_heads / num_kv_heads)),
  *   out[r][qh] = softmax(scale * q[r][qh] . K[slot]^T) @ V[slot] over the slots of r,
  * K and V being the layer's K and V planes (float32 math; zeros for a request with no slots).
- * Flash-decoding: splits of 16384/head_dim tokens, then a merge; the workspace holds the split
- * partials and is overwritten by every call (calls sharing it must be stream-ordered). */
+ * Flash-decoding: splits of 32 KiB of K per KV head (32768 / (head_dim * elem_bytes) tokens),
+ * then a merge; the workspace holds the split partials and is overwritten by every call (calls
+ * sharing it must be stream-ordered). A request with more slots than max_tokens provides
+ * for is never truncated: its outputs are NaN, unless its slots still fit the
+ * ceil(max_tokens / split) splits, which are all computed. */
 enum { VTOKEN_KV_FP16 = 0, VTOKEN_KV_BF16 = 1, VTOKEN_KV_FP8_E4M3 = 2 };
 
 typedef struct vtoken_decode {
@@ -327,7 +330,7 @@ typedef struct vtoken_decode {
   int32_t      layer;      /* 0 <= layer < num_layers                                       */
   int32_t      kv_dtype;   /* VTOKEN_KV_*; fp8 (OCP e4m3) iff elem_bytes == 1               */
   float        scale;      /* softmax scale, usually 1/sqrt(head_dim)                       */
-  int32_t      max_tokens; /* [host] >= the slot count of every request                     */
+  int32_t      max_tokens; /* [host] >= the slot count of every request (else NaN outputs)  */
   float*       workspace;  /* device, >= vtoken_decode_workspace_bytes() bytes              */
   int64_t      workspace_bytes;
   const int32_t* slot_count; /* device [R] or NULL: request r's slots are                   */
@@ -336,8 +339,9 @@ typedef struct vtoken_decode {
 } vtoken_decode;
 
 /* Bytes of workspace: num_reqs * num_q_heads * ceil(max_tokens / (16384 / head_dim)) (at
- * least one split) * (head_dim + 2) * 4. head_dim must be 32, 64, 128 or 256 (also for
- * vtoken_paged_decode: VTOKEN_ERR_SHAPE otherwise). Returns -1 for invalid sizes. */
+ * least one split) * (head_dim + 2) * 4, enough for either element size (1-byte caches use
+ * half as many splits). head_dim must be 32, 64, 128 or 256 (also for vtoken_paged_decode:
+ * VTOKEN_ERR_SHAPE otherwise). Returns -1 for invalid sizes. */
 int64_t vtoken_decode_workspace_bytes(int32_t num_reqs, int32_t num_q_heads, int32_t head_dim,
                                       int32_t max_tokens);
 vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode* decode,

@@ -322,7 +322,7 @@ int64_t vtoken_decode_workspace_bytes(int32_t num_reqs, int32_t num_q_heads, int
                                       int32_t max_tokens) {
   if (num_reqs < 0 || num_q_heads <= 0 || max_tokens < 0) return -1;
   if (head_dim != 32 && head_dim != 64 && head_dim != 128 && head_dim != 256) return -1;
-  const int64_t split = vtoken::decode_split_tokens(head_dim);
+  const int64_t split = vtoken::decode_min_split_tokens(head_dim);
   const int64_t splits = max_tokens > 0 ? (max_tokens + split - 1) / split : 1;
   return (int64_t)num_reqs * num_q_heads * splits * (head_dim + 2) * 4;
 }
@@ -363,7 +363,7 @@ vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode
   a.kv_kind = kind;
   a.num_slots = cache->num_blocks * cache->block_size;
   a.num_reqs = num_reqs;
-  const int split = vtoken::decode_split_tokens(D);
+  const int split = vtoken::decode_split_tokens(D, cache->elem_bytes);
   a.split_tokens = split;
   a.splits = d->max_tokens > 0 ? (d->max_tokens + split - 1) / split : 1;
   if ((int64_t)num_reqs * cache->num_kv_heads * a.splits > INT32_MAX ||

@@ -5,10 +5,11 @@
 //   slot_map_kernel      one workgroup per request: wave-ballot compaction of token_slot,
 //                        the live tokens' slots in logical order (Sec. 3.4: the slot mapping
 //                        is built through the token table, once per token)
-//   decode_split_kernel  one workgroup per (request, KV head, split of 16384/D tokens):
-//                        scores of the G query heads that share the KV head on the matrix
-//                        cores, split-local softmax, partial weighted sum of V on the vector
-//                        ALUs (flash-decoding partials)
+//   decode_split_kernel  one workgroup per (request, KV head, split of 32 KiB of K: 32768 /
+//                        (D * element bytes) tokens): scores of the G <= 4 query heads that
+//                        share the KV head on the matrix cores, split-local softmax, partial
+//                        weighted sum of V on the vector ALUs (flash-decoding partials)
+//   decode_split_mfma_kernel  the same for G = 8 with both products on the matrix cores
 //   decode_combine_kernel  one workgroup per (request, query head): merges the splits
 //
 // Decode attention is HBM-bound up to GQA groups of about 4 (2G flops per byte of K/V);
@@ -296,7 +297,8 @@ __device__ __forceinline__ float lanes_reduce(float x) {
 //
 // kKind: element type; kD: head_dim (32, 64, 128, 256); kG: query heads per KV head.
 //
-// One workgroup (4 waves) covers kSplit = 16384 / kD tokens of one (request, KV head).
+// One workgroup (4 waves) covers kSplit = 32768 / (kD * element bytes) tokens of one (request,
+// KV head).
 // Scores on the matrix cores: for a tile of 16 tokens, S[token][head] = K_tile (16 x kD) times
 // Q^T (kD x 16, the kG query heads of this KV head, zero-padded), as kD/32 MFMA 16x16x32 steps;
 // the float32 query is split into a high and a low 16-bit part (q = hi + lo to about 2^-17
@@ -312,14 +314,14 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
   using ElemT = typename ScoreOp<kKind>::elem;
   constexpr int kElem = kKind == 2 ? 1 : 2;
   constexpr int kChunks = kD / 32;
-  constexpr int kSplit = decode_split_tokens(kD);
+  constexpr int kSplit = decode_split_tokens(kD, kElem);
   constexpr int kWaves = kAttnThreads / 64;
   constexpr int kTilesPerWave = kSplit / 16 / kWaves;
   constexpr int kLanes = kD / kPer;                  // V: lanes per token row
   constexpr int kTokPerPass = kAttnThreads / kLanes;
   constexpr int kIters = kSplit / kTokPerPass;       // V: tokens per thread
-  static_assert(kTilesPerWave * 16 * kWaves == kSplit && kIters == kDecodeTokensPerThread,
-                "split geometry");
+  static_assert(kTilesPerWave * 16 * kWaves == kSplit && kIters * kPer * kElem == 128,
+                "split geometry: 128 bytes of V per thread");
   __shared__ float p_s[kG][kSplit];
   __shared__ float red_s[kWaves][kG];
   __shared__ float acc_s[kWaves][kG][kD];
@@ -506,7 +508,8 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
 //
 // kKind: element type; kD: head_dim (32, 64, 128, 256); kG = 8 query heads per KV head.
 //
-// One workgroup (4 waves) covers kSplit = 16384 / kD tokens of one (request, KV head); wave w
+// One workgroup (4 waves) covers kSplit = 32768 / (kD * element bytes) tokens of one (request,
+// KV head); wave w
 // owns tokens [w*kTW, (w+1)*kTW), kTW = kSplit / 4, and computes for them, on the matrix
 // cores (MFMA 16x16x32, fp16 for fp16 caches, bf16 otherwise; fp8 widened to bf16):
 //   scores  S[token][col] = K_tile (16 x kD) . Q2^T (kD x 16). The float32 query is split into
@@ -532,20 +535,24 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
   using ElemT = typename ScoreOp<kKind>::elem;
   constexpr int kElem = kKind == 2 ? 1 : 2;
   constexpr int kChunks = kD / 32;                   // score k-steps
-  constexpr int kSplit = decode_split_tokens(kD);
+  constexpr int kSplit = decode_split_tokens(kD, kElem);
   constexpr int kWaves = kAttnThreads / 64;
-  constexpr int kTW = kSplit / kWaves;               // tokens per wave: 128, 64, 32, 16
+  constexpr int kTW = kSplit / kWaves;               // tokens per wave: 16 .. 256
   constexpr int kTiles = kTW / 16;                   // 16-token score tiles per wave
   constexpr int kKC = (kTiles + 1) / 2;              // 32-token value k-steps per wave
   constexpr int kDC = kD / 16;                       // 16-element value chunks
   constexpr int kLanesV = kD / kPer;                 // V load: lanes per token row
   constexpr int kTokV = 64 / kLanesV;                // V load: tokens per wave pass
   constexpr int kItV = kTW / kTokV;                  // V load: pieces per lane
+  constexpr int kWin = kTW < 32 ? kTW : 32;          // V rows a wave stages per k-step
+  constexpr int kItW = kWin / kTokV;                 // V pieces per lane per k-step
   constexpr int kRowB = kD * 2 + 32;                 // LDS bytes per V row
-  static_assert(kTiles * 16 == kTW && kItV == kDecodeTokensPerThread, "split geometry");
+  static_assert(kTiles * 16 == kTW && kItW * kKC == kItV && kItW * kTokV == kWin,
+                "split geometry");
+  static_assert(kG >= 1 && kG <= 8, "the high and low parts fill the 16 operand columns");
+  constexpr int kVB = kWaves * kWin * kRowB;
   constexpr int kMergeB = kWaves * kG * (kD + 2) * 4;
-  static_assert(kG == 8, "the high and low parts fill the 16 operand columns");
-  constexpr int kLdsB = kSplit * kRowB > kMergeB ? kSplit * kRowB : kMergeB;
+  constexpr int kLdsB = kVB > kMergeB ? kVB : kMergeB;
   __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsB];
 
   const int tid = threadIdx.x;
@@ -568,17 +575,21 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
   const int row = lane & 15;    // token of a tile (K operand) / head (Q, P operands)
   const int wt0 = wave * kTW;   // first token of this wave
 
-  const bool low = row >= 8;    // this lane's column / P row holds low parts
+  const bool low = row >= 8;          // this lane's column / P row holds low parts
+  const bool real = (row & 7) < kG;   // column / P row of a query head (else zero padding)
   // ---- query operand first (needed first): column `row` = head row % 8, scaled, its high
-  // part (row < 8) or its low part (row >= 8)
+  // part (row < 8) or its low part (row >= 8); the load is unconditional (padding re-reads
+  // head 0), a conditional load would wait for every outstanding K/V load
   OpT qop[kChunks];
   {
-    const float* qrow = a.q + ((int64_t)r * a.num_q_heads + h * kG + (row & 7)) * kD;
+    const float* qrow =
+        a.q + ((int64_t)r * a.num_q_heads + h * kG + (real ? row & 7 : 0)) * kD;
 #pragma unroll
     for (int ch = 0; ch < kChunks; ++ch) {
 #pragma unroll
       for (int e = 0; e < kPer; ++e) {
-        const float q = qrow[ch * 32 + grp * kPer + e] * a.scale;
+        const float qv = qrow[ch * 32 + grp * kPer + e] * a.scale;
+        const float q = real ? qv : 0.f;
         const ElemT hi = static_cast<ElemT>(q);
         qop[ch][e] = low ? static_cast<ElemT>(q - static_cast<float>(hi)) : hi;
       }
@@ -632,14 +643,20 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
     sc[i] = acc;
   }
 
-  // ---- V rows into this wave's LDS rows (zero rows past the split's end)
+
+  // ---- V rows of k-step kc into this wave's LDS window
+  uint8_t* vwin = lds + wave * kWin * kRowB;
+  auto stage_v = [&](int kc) {
 #pragma unroll
-  for (int i = 0; i < kItV; ++i) {
-    const int tl = wt0 + lane / kLanesV + i * kTokV;     // row within the split
-    PieceT w = vw[i];
-    if (!vok[i]) w = PieceT{};
-    *reinterpret_cast<u32x4*>(lds + tl * kRowB + vpiece * 16) = v_row16<kKind>(w);
-  }
+    for (int ii = 0; ii < kItW; ++ii) {
+      const int i = kc * kItW + ii;
+      PieceT w = vw[i];
+      if (!vok[i]) w = PieceT{};
+      *reinterpret_cast<u32x4*>(vwin + (lane / kLanesV + ii * kTokV) * kRowB + vpiece * 16) =
+          v_row16<kKind>(w);
+    }
+  };
+  stage_v(0);
 
   // ---- wave-local softmax per head (the four lanes of a column share `row`)
   float m = -INFINITY;
@@ -658,14 +675,20 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
       l += sc[i][j];
     }
   l = lanes_reduce<16, false>(l);
-  __syncthreads();  // V rows written (each wave reads only its own rows)
 
-  // ---- O_w = P . V on the matrix cores
+  // ---- O_w = P . V on the matrix cores, one 32-token k-step at a time; the V rows of a
+  // k-step go through this wave's LDS window (zero rows past the split's end), the first
+  // k-step's before the softmax above
   f32x4 o[kDC];
 #pragma unroll
   for (int dc = 0; dc < kDC; ++dc) o[dc] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int kc = 0; kc < kKC; ++kc) {
+    if (kc > 0) {
+      __syncthreads();  // the previous k-step's reads of the window are done
+      stage_v(kc);
+    }
+    __syncthreads();  // V rows written (each wave reads only its own window)
     // A operand: row `row` (head row % 8, high or low part), tokens 4*grp..+3 of tile 2kc
     // then of tile 2kc+1 (zero if absent)
     OpT pop;
@@ -678,10 +701,10 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
     }
     // B operand rows: lane 16*grp + rho supplies the row of token 4*grp + rho/4 of the first
     // tile (then of the second), elements 4*(rho%4)..+3 of the 16-element chunk
-    const int t1 = 2 * kc * 16 + 4 * grp + row / 4;
-    const int t2 = (2 * kc + 1 < kTiles ? (2 * kc + 1) * 16 : 2 * kc * 16) + 4 * grp + row / 4;
-    const uint8_t* r1 = lds + (wt0 + t1) * kRowB + (row % 4) * 8;
-    const uint8_t* r2 = lds + (wt0 + t2) * kRowB + (row % 4) * 8;
+    const int t1 = 4 * grp + row / 4;                                  // window rows
+    const int t2 = (2 * kc + 1 < kTiles ? 16 : 0) + 4 * grp + row / 4;
+    const uint8_t* r1 = vwin + t1 * kRowB + (row % 4) * 8;
+    const uint8_t* r2 = vwin + t2 * kRowB + (row % 4) * 8;
 #pragma unroll
     for (int dc = 0; dc < kDC; ++dc) {
       const i16x4 x1 = lds_read_tr16(r1 + dc * 32);
@@ -710,7 +733,8 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
     for (int dc = 0; dc < kDC; ++dc)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        mrg[(wave * kG + 4 * grp + j) * (kD + 2) + 2 + dc * 16 + row] = o[dc][j];
+        const int g = 4 * grp + j;                     // result row = head
+        if (g < kG) mrg[(wave * kG + g) * (kD + 2) + 2 + dc * 16 + row] = o[dc][j];
       }
   }
   __syncthreads();
@@ -767,8 +791,12 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(AttnArg
   const int D = a.head_dim;
   const int64_t rs = D + 2;  // record stride
   float* out = a.out + ((int64_t)r * a.num_q_heads + qh) * D;
-  int ns = c <= 0 ? 0 : (c + a.split_tokens - 1) / a.split_tokens;
-  ns = ns < a.splits ? ns : a.splits;  // the workspace holds a.splits records
+  const int ns = c <= 0 ? 0 : (c + a.split_tokens - 1) / a.split_tokens;
+  if (ns > a.splits) {
+    // more slots than max_tokens: the splits past the workspace were never computed
+    for (int d = tid; d < D; d += kCombineThreads) out[d] = __builtin_nanf("");
+    return;
+  }
   if (ns == 0) {
     for (int d = tid; d < D; d += kCombineThreads) out[d] = 0.f;
     return;
@@ -867,7 +895,9 @@ hipError_t launch_slot_mapping(const SlotMapArgs& a, hipStream_t stream) {
 
 hipError_t launch_paged_decode(const AttnArgs& a, hipStream_t stream) {
   if (a.num_reqs <= 0) return hipSuccess;
-  if (a.split_tokens != decode_split_tokens(a.head_dim)) return hipErrorInvalidValue;
+  if (a.split_tokens != decode_split_tokens(a.head_dim, a.kv_kind == 2 ? 1 : 2)) {
+    return hipErrorInvalidValue;
+  }
   hipError_t e;
   switch (a.kv_kind) {
     case 0: e = launch_decode_k<0>(a, stream); break;

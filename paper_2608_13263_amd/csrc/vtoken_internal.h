@@ -132,7 +132,7 @@ struct AttnArgs {
   int32_t num_slots;
   int32_t num_reqs;
   int32_t splits;    // split records per (request, query head) in the workspace
-  int32_t split_tokens;  // tokens per split: decode_split_tokens(head_dim)
+  int32_t split_tokens;  // tokens per split: decode_split_tokens(head_dim, elem bytes)
   float scale;
   const float* q;
   float* out;
@@ -190,12 +190,15 @@ hipError_t launch_planner(const PlannerArgs& a, hipStream_t stream);
 hipError_t launch_slot_mapping(const SlotMapArgs& a, hipStream_t stream);
 hipError_t launch_append_slots(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_paged_decode(const AttnArgs& a, hipStream_t stream);
-// Tokens one decode workgroup covers: 8 per thread, 256 threads, head_dim / 8 lanes per
-// token (32, 64, 128 or 256 head_dim -> 512, 256, 128, 64 tokens).
-constexpr int kDecodeTokensPerThread = 8;
-constexpr int decode_split_tokens(int head_dim) {
-  return kDecodeTokensPerThread * 256 * 8 / head_dim;
+// Tokens one decode workgroup covers: 32 KiB of K (and of V) of one KV head, i.e. 8 pieces
+// of 16 bytes per thread and operand over 256 threads (head_dim 32, 64, 128, 256 -> 512, 256,
+// 128, 64 tokens at 2 bytes per element, twice as many at 1 byte).
+constexpr int kDecodeSplitBytes = 32768;
+constexpr int decode_split_tokens(int head_dim, int elem_bytes) {
+  return kDecodeSplitBytes / (head_dim * elem_bytes);
 }
+// The smallest split over the element sizes: the workspace bound of the C ABI.
+constexpr int decode_min_split_tokens(int head_dim) { return decode_split_tokens(head_dim, 2); }
 
 hipError_t launch_build(const MetaArgs& a, hipStream_t stream);
 // variant: 0 default, 1 LDS double buffer, 2 LDS single buffer, 3 registers

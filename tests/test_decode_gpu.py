@@ -129,12 +129,13 @@ def test_slot_mapping_parity(case, inplace):
 # paged decode parity
 # ------------------------------------------------------------------------------------------
 def _decode_inputs(dtype, H, D, S, seed):
-    """Two layers; live counts 0, 1, 255, 256, 257, 514 and Bernoulli(0.5) requests up to
-    3000 tokens (several 256-token splits with ragged tails)."""
+    """Two layers; live counts 0, 1, 255, 256, 257, 514, 1023, 1024, 1025, 2049 (split edges
+    of every geometry: splits hold 32768 / (D * element bytes) tokens, 64 to 1024) and
+    Bernoulli(0.5) requests up to 3000 tokens (several splits with ragged tails)."""
     sh = W.KVShape(2, H, D, S, dtype)
     rng = np.random.default_rng(seed)
     masks = [[0] * 50, [0] * 9 + [1], [1] * 255, [1] * 256 + [0] * 7, [1] * 257,
-             [1, 1, 0] * 257]
+             [1, 1, 0] * 257, [1] * 1023, [0] * 3 + [1] * 1024, [1] * 1025, [1] * 2049]
     masks += [(rng.random(int(n)) < 0.5).astype(int).tolist()
               for n in rng.integers(1, 3000, size=6)]
     M = sum(-(-len(m) // S) for m in masks)
@@ -142,10 +143,10 @@ def _decode_inputs(dtype, H, D, S, seed):
 
 
 DECODE_CASES = [
-    # dtype, H, D, G, S        (lanes per head row = D / 8; tokens per split = 16384 / D)
+    # dtype, H, D, G, S   (lanes per head row = D / 8; tokens per split = 32768 / (D * bytes))
     ("bf16", 8, 128, 4, 16),   # Llama-3-8B KV geometry
     ("fp16", 2, 64, 1, 16),    # no GQA
-    ("bf16", 4, 32, 2, 16),    # 512-token splits
+    ("bf16", 4, 32, 2, 16),    # 512-token splits (1024 for fp8)
     ("fp16", 4, 128, 8, 16),   # G = 8
     ("bf16", 2, 256, 2, 16),   # 32 lanes per head row, 64-token splits
     ("fp8_e4m3", 8, 128, 8, 32),  # Llama-3-70B fp8 geometry
@@ -183,6 +184,33 @@ def test_paged_decode_parity(dtype, H, D, G, S):
         assert np.array_equal(got[0], np.zeros_like(got[0])), "no live tokens -> zeros"
         worst = max(worst, float(np.abs(got - ref).max()))
     _label(f"paged decode {dtype} H={H} D={D} G={G}: max |diff| {worst:.2e}")
+
+
+@pytest.mark.parametrize("dtype,G", [("bf16", 4), ("fp8_e4m3", 8)])
+def test_paged_decode_max_tokens_too_small(dtype, G):
+    """max_tokens below a request's slot count: requests whose slots fit the splits it implies
+    are exact, the others get NaN rows (never a silently truncated softmax)."""
+    t = torch()
+    B = _B()
+    H, D, S = 2, 128, 16
+    inp = _decode_inputs(dtype, H, D, S, seed=77 + G)
+    sh = inp.shape
+    kv = W.kv_device(sh, inp.num_blocks, 6)
+    orc = oracle_repack_inputs(inp, kv_bytes(kv, sh))
+    cache, _, _, indptr, slots = _device_pass(inp, kv)
+    ref_indptr, ref_slots = slot_mapping(orc.token_slot, inp.tok_indptr, inp.seq_lens)
+    vals = _values(orc.kv, sh)
+    split = 32768 // (D * (1 if dtype == "fp8_e4m3" else 2))
+    max_tokens = split + 1                       # two splits
+    counts = np.diff(ref_indptr)
+    fits = counts <= 2 * split
+    assert fits.any() and (~fits).any()
+    q = np.random.default_rng(3).standard_normal((inp.num_reqs, H * G, D)).astype(np.float32)
+    out = B.paged_decode(cache, t.from_numpy(q).cuda(), indptr, slots, 1, max_tokens)
+    got = out.cpu().numpy().astype(np.float64)
+    ref = decode_batch(q, vals[2], vals[3], ref_indptr, ref_slots)
+    np.testing.assert_allclose(got[fits], ref[fits], atol=ATOL, rtol=RTOL)
+    assert np.isnan(got[~fits]).all()
 
 
 @pytest.mark.parametrize("dtype", ["fp8_e4m3", "fp16", "bf16"])
