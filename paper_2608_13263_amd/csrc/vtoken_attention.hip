@@ -306,7 +306,7 @@ __device__ __forceinline__ float lanes_reduce(float x) {
 // l%16 and elements 8*(l/16)..+7 of each 32-element chunk (the operand layout of the
 // instruction), and receives the scores of tokens 4*(l/16)..+3 for head l%16.
 // Weighted V sum on the vector ALUs: kD/8 lanes per token, 8 elements each.
-// Every thread issues all of its K and V loads (8 + 8 pieces) before any arithmetic.
+// Every thread issues all of its K and V loads (128 + 128 bytes) before any arithmetic.
 template <int kKind, int kD, int kG>
 __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) {
   using PieceT = typename Piece<kKind>::type;
@@ -504,28 +504,29 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
 }
 
 // Variant for GQA groups of 8, where the weighted V sum (2 kG flops per V byte) would bound
-// the vector ALUs: both products on the matrix cores.
+// the vector ALUs: both products on the matrix cores (smaller groups work too, padded, but
+// measured slower than the vector-ALU variant).
 //
-// kKind: element type; kD: head_dim (32, 64, 128, 256); kG = 8 query heads per KV head.
+// kKind: element type; kD: head_dim (32, 64, 128, 256); kG: query heads per KV head (<= 8).
 //
-// One workgroup (4 waves) covers kSplit = 32768 / (kD * element bytes) tokens of one (request,
-// KV head); wave w
-// owns tokens [w*kTW, (w+1)*kTW), kTW = kSplit / 4, and computes for them, on the matrix
-// cores (MFMA 16x16x32, fp16 for fp16 caches, bf16 otherwise; fp8 widened to bf16):
+// One workgroup (4 waves) covers kSplit = 32768 / (kD * element bytes) tokens of one
+// (request, KV head); wave w owns tokens [w*kTW, (w+1)*kTW), kTW = kSplit / 4, and computes
+// for them, on the matrix cores (MFMA 16x16x32, fp16 for fp16 caches, bf16 otherwise; fp8
+// widened to bf16):
 //   scores  S[token][col] = K_tile (16 x kD) . Q2^T (kD x 16). The float32 query is split into
 //           high and low 16-bit parts (q = hi + lo to ~2^-17): column c < 8 of Q2 is the high
-//           part of head c, column c + 8 its low part, so one product carries both and the
-//           score of head c is S[.][c] + S[.][c + 8] (float32 accuracy, no padded columns);
+//           part of head c, column c + 8 its low part (zero for c >= kG), so one product
+//           carries both and the score of head c is S[.][c] + S[.][c + 8] (float32 accuracy);
 //   weights p = exp(score - m_w) with the wave's own maximum m_w per head, l_w = sum of p;
 //   values  O2[row][d] = P2 (16 x 32 tokens) . V (32 tokens x 16 elements) per 16-element
 //           chunk, row c < 8 of P2 the high part of head c's weights, row c + 8 their low
-//           part, so O_w[c] = O2[c] + O2[c + 8]. V goes through LDS (16-bit rows, padded by
-//           32 bytes against bank conflicts) and comes back in operand layout by transpose
-//           reads. The operand layout fixes which tokens a lane holds: lane l has column
+//           part, so O_w[c] = O2[c] + O2[c + 8]. V goes through a per-wave LDS window of 32
+//           rows, one 32-token k-step at a time (16-bit rows, padded by 32 bytes against bank
+//           conflicts), and comes back in operand layout by transpose reads. The operand layout fixes which tokens a lane holds: lane l has column
 //           l%16 and, of each 32-token chunk, tokens 4*(l/16)..+3 of its first 16-token tile
 //           and the same of its second; the V rows are read in that order.
 // The four waves are merged with the usual max-rescaling into the split's record.
-// Every thread issues all of its K and V loads (8 + 8 pieces) before any arithmetic.
+// Every thread issues all of its K and V loads (128 + 128 bytes) before any arithmetic.
 // Non-finite K or V values are outside the contract (a zero weight times an infinite value
 // gives NaN).
 template <int kKind, int kD, int kG>
