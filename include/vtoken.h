@@ -320,7 +320,8 @@ vtoken_status vtoken_append_slots(int32_t num_reqs, const int32_t* append_indptr
  * then a merge; the workspace holds the split partials and is overwritten by every call (calls
  * sharing it must be stream-ordered). A request with more slots than max_tokens provides
  * for is never truncated: its outputs are NaN, unless its slots still fit the
- * ceil(max_tokens / split) splits, which are all computed. */
+ * ceil(max_tokens / split) splits, which are all computed. A slot outside the pool (negative
+ * or >= num_blocks * block_size) is never dereferenced; its request's outputs are NaN. */
 enum { VTOKEN_KV_FP16 = 0, VTOKEN_KV_BF16 = 1, VTOKEN_KV_FP8_E4M3 = 2 };
 
 typedef struct vtoken_decode {

@@ -293,6 +293,47 @@ __device__ __forceinline__ float lanes_reduce(float x) {
   return xor_combine<32, kMax>(x);
 }
 
+// Sums over the token groups of the vector-ALU decode: lane l holds kN partial values for
+// head-row piece l % kLanes of token group l / kLanes (64 / kLanes groups per wave). On return
+// the totals are spread over the lanes: lane l holds out[q] = total of value
+// kSpread * q + l / 16 (kLanes <= 16, kSpread 4) or kSpread * q + l / 32 (kLanes 32, kSpread
+// 2), for every q < kN / kSpread. In-row groups are folded first by DPP rotations; the row
+// swaps then exchange two different values at once (a transposing reduction), so every
+// swap halves the values still held instead of copying one.
+template <int kLanes, int kN>
+__device__ __forceinline__ void token_group_sum(float* v, float* out) {
+  static_assert(kLanes == 4 || kLanes == 8 || kLanes == 16 || kLanes == 32, "lanes per row");
+  if constexpr (kLanes == 32) {
+    static_assert(kN % 2 == 0, "pairs");
+#pragma unroll
+    for (int q = 0; q < kN / 2; ++q) {
+      const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[2 * q]),
+                                                      __float_as_uint(v[2 * q + 1]), false, false);
+      out[q] = __uint_as_float(s[0]) + __uint_as_float(s[1]);
+    }
+  } else {
+    static_assert(kN % 4 == 0, "quads");
+#pragma unroll
+    for (int n = 0; n < kN; ++n) {
+      if constexpr (kLanes <= 8) v[n] += row_ror<8>(v[n]);
+      if constexpr (kLanes <= 4) v[n] += row_ror<4>(v[n]);
+    }
+#pragma unroll
+    for (int q = 0; q < kN / 4; ++q) {
+      // rows 0..3 after the 16-swaps: value 4q (rows 0+1), 4q+1 (0+1), 4q (2+3), 4q+1 (2+3)
+      const auto s0 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[4 * q]),
+                                                       __float_as_uint(v[4 * q + 1]), false, false);
+      const auto s1 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[4 * q + 2]),
+                                                       __float_as_uint(v[4 * q + 3]), false, false);
+      const float a = __uint_as_float(s0[0]) + __uint_as_float(s0[1]);
+      const float b = __uint_as_float(s1[0]) + __uint_as_float(s1[1]);
+      const auto s2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b),
+                                                       false, false);
+      out[q] = __uint_as_float(s2[0]) + __uint_as_float(s2[1]);
+    }
+  }
+}
+
 // Variant for GQA groups up to 4: scores on the matrix cores, weighted V sum on the vector ALUs.
 //
 // kKind: element type; kD: head_dim (32, 64, 128, 256); kG: query heads per KV head.
@@ -384,13 +425,12 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
   const int piece = tid % kLanes;
   const int tg = tid / kLanes;
   PieceT vw[kIters];
-  bool vok[kIters];
 #pragma unroll
   for (int i = 0; i < kIters; ++i) {
     const int t = tg + i * kTokPerPass;
     const int sl = slots[t < nt ? t : nt - 1];
-    vok[i] = static_cast<unsigned>(sl) < static_cast<unsigned>(a.num_slots);
-    vw[i] = *reinterpret_cast<const PieceT*>(vplane + (int64_t)(vok[i] ? sl : 0) * a.row_bytes +
+    const bool ok = static_cast<unsigned>(sl) < static_cast<unsigned>(a.num_slots);
+    vw[i] = *reinterpret_cast<const PieceT*>(vplane + (int64_t)(ok ? sl : 0) * a.row_bytes +
                                              head0 + piece * kPer * kElem);
   }
 
@@ -400,11 +440,15 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ch = 0; ch < kChunks; ++ch) {
-      PieceT w = kw[i][ch];
-      if (!kok[i]) w = PieceT{};
-      const OpT kop = k_operand<kKind>(w);
+      const OpT kop = k_operand<kKind>(kw[i][ch]);
       acc = score_mfma<kKind>(kop, qh[ch], acc);
       acc = score_mfma<kKind>(kop, ql[ch], acc);
+    }
+    // a slot outside the pool (its row was read at slot 0) poisons the request: NaN score
+    const uint64_t okm = __ballot(kok[i]);            // bit k: token k of the tile
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (!((okm >> (4 * grp + j)) & 1)) acc[j] = __builtin_nanf("");
     }
     if (row < kG) {
 #pragma unroll
@@ -463,9 +507,7 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
     const int t = tg + i * kTokPerPass;
     if (t < nt) {
       float vf[kPer];
-      PieceT w = vw[i];
-      if (!vok[i]) w = PieceT{};
-      piece_to_float<kKind>(w, vf);
+      piece_to_float<kKind>(vw[i], vf);
 #pragma unroll
       for (int g = 0; g < kG; ++g) {
         const float p = p_s[g][t];
@@ -474,18 +516,21 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
       }
     }
   }
-  // reduce over the token groups: inside the wave (lanes with the same piece), then across
-  // waves through LDS
+  // reduce over the token groups: inside the wave (lanes with the same piece; the totals end
+  // up spread over the rows), then across waves through LDS
+  {
+    constexpr int kSpread = kLanes == 32 ? 2 : 4;
+    constexpr int kOut = kG * kPer / kSpread;
+    float tot[kOut];
+    token_group_sum<kLanes, kG * kPer>(&acc[0][0], tot);
+    const int part = kLanes == 32 ? lane >> 5 : lane >> 4;    // which of the spread values
+    if ((lane & 15) < kLanes || kLanes == 32) {              // one lane per piece and part
 #pragma unroll
-  for (int g = 0; g < kG; ++g)
-#pragma unroll
-    for (int e = 0; e < kPer; ++e)
-      acc[g][e] = lanes_reduce<kLanes, false>(acc[g][e]);
-  if (lane < kLanes) {
-#pragma unroll
-    for (int g = 0; g < kG; ++g)
-#pragma unroll
-      for (int e = 0; e < kPer; ++e) acc_s[wave][g][piece * kPer + e] = acc[g][e];
+      for (int q = 0; q < kOut; ++q) {
+        const int n = kSpread * q + part;                    // value index g * kPer + e
+        acc_s[wave][n / kPer][piece * kPer + n % kPer] = tot[q];
+      }
+    }
   }
   __syncthreads();
   // partial record per (request, query head, split): [m, l, acc[D]]
@@ -614,13 +659,12 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
   }
   const int vpiece = lane % kLanesV;
   PieceT vw[kItV];
-  bool vok[kItV];
 #pragma unroll
   for (int i = 0; i < kItV; ++i) {
     const int t = wt0 + lane / kLanesV + i * kTokV;
     const int sl = slots[t < nt ? t : nt - 1];
-    vok[i] = t < nt && static_cast<unsigned>(sl) < static_cast<unsigned>(a.num_slots);
-    vw[i] = *reinterpret_cast<const PieceT*>(vplane + (int64_t)(vok[i] ? sl : 0) * a.row_bytes +
+    const bool ok = static_cast<unsigned>(sl) < static_cast<unsigned>(a.num_slots);
+    vw[i] = *reinterpret_cast<const PieceT*>(vplane + (int64_t)(ok ? sl : 0) * a.row_bytes +
                                              head0 + vpiece * kPer * kElem);
   }
 
@@ -632,13 +676,15 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ch = 0; ch < kChunks; ++ch) {
-      PieceT w = kw[i][ch];
-      if (!kok[i]) w = PieceT{};
-      acc = score_mfma<kKind>(k_operand<kKind>(w), qop[ch], acc);
+      acc = score_mfma<kKind>(k_operand<kKind>(kw[i][ch]), qop[ch], acc);
     }
+    // a slot outside the pool (its row was read at slot 0) poisons the request: NaN score;
+    // tokens past the split's end get weight zero
+    const uint64_t okm = __ballot(kok[i]);            // bit k: token k of the tile
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       acc[j] += row_ror<8>(acc[j]);
+      if (!((okm >> (4 * grp + j)) & 1)) acc[j] = __builtin_nanf("");
       if (wt0 + 16 * i + 4 * grp + j >= nt) acc[j] = -INFINITY;
     }
     sc[i] = acc;
@@ -650,11 +696,8 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
   auto stage_v = [&](int kc) {
 #pragma unroll
     for (int ii = 0; ii < kItW; ++ii) {
-      const int i = kc * kItW + ii;
-      PieceT w = vw[i];
-      if (!vok[i]) w = PieceT{};
       *reinterpret_cast<u32x4*>(vwin + (lane / kLanesV + ii * kTokV) * kRowB + vpiece * 16) =
-          v_row16<kKind>(w);
+          v_row16<kKind>(vw[kc * kItW + ii]);
     }
   };
   stage_v(0);
@@ -678,7 +721,7 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
   l = lanes_reduce<16, false>(l);
 
   // ---- O_w = P . V on the matrix cores, one 32-token k-step at a time; the V rows of a
-  // k-step go through this wave's LDS window (zero rows past the split's end), the first
+  // k-step go through this wave's LDS window (rows past the split's end weigh zero), the first
   // k-step's before the softmax above
   f32x4 o[kDC];
 #pragma unroll

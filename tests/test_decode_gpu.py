@@ -186,6 +186,37 @@ def test_paged_decode_parity(dtype, H, D, G, S):
     _label(f"paged decode {dtype} H={H} D={D} G={G}: max |diff| {worst:.2e}")
 
 
+@pytest.mark.parametrize("dtype,G", [("bf16", 4), ("fp8_e4m3", 8), ("fp16", 1)])
+def test_paged_decode_slot_outside_pool_gives_nan(dtype, G):
+    """A slot outside the pool (past the end, or negative) is read nowhere: the requests that
+    hold one get NaN rows, every other request is unaffected."""
+    t = torch()
+    B = _B()
+    H, D, S = 2, 128, 16
+    inp = _decode_inputs(dtype, H, D, S, seed=91 + G)
+    sh = inp.shape
+    kv = W.kv_device(sh, inp.num_blocks, 7)
+    orc = oracle_repack_inputs(inp, kv_bytes(kv, sh))
+    cache, _, _, indptr, slots = _device_pass(inp, kv)
+    ref_indptr, ref_slots = slot_mapping(orc.token_slot, inp.tok_indptr, inp.seq_lens)
+    counts = np.diff(ref_indptr)
+    bad = [int(np.nonzero(counts == 1)[0][0]), int(np.nonzero(counts > 600)[0][0])]
+    host = slots.cpu().numpy()
+    host[ref_indptr[bad[0]]] = inp.num_blocks * S + 3           # past the pool
+    host[ref_indptr[bad[1]] + counts[bad[1]] // 2] = -7         # negative, mid-request
+    bad_slots = t.from_numpy(host).cuda()
+    vals = _values(orc.kv, sh)
+    q = np.random.default_rng(4).standard_normal((inp.num_reqs, H * G, D)).astype(np.float32)
+    out = B.paged_decode(cache, t.from_numpy(q).cuda(), indptr, bad_slots, 0,
+                         int(counts.max()))
+    got = out.cpu().numpy().astype(np.float64)
+    ref = decode_batch(q, vals[0], vals[1], ref_indptr, ref_slots)
+    good = np.ones(inp.num_reqs, bool)
+    good[bad] = False
+    np.testing.assert_allclose(got[good], ref[good], atol=ATOL, rtol=RTOL)
+    assert np.isnan(got[bad]).all()
+
+
 @pytest.mark.parametrize("dtype,G", [("bf16", 4), ("fp8_e4m3", 8)])
 def test_paged_decode_max_tokens_too_small(dtype, G):
     """max_tokens below a request's slot count: requests whose slots fit the splits it implies
