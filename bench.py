@@ -113,43 +113,135 @@ def recorded_traffic(config: str):
     return float(m_bytes.group(1)) if sha == m_sha.group(1) else None
 
 
-def cpu_baseline(inp, planes: int, min_seconds: float = 10.0, max_repeats: int = 8):
-    """The CPU oracle as it stands, on the full metadata and `planes` planes of host KV
-    (64 MiB of random bytes tiled; the oracle's cost does not depend on the values), timed
-    over repeated passes until at least `min_seconds` of CPU work."""
+def host_kv_sample(shape, num_blocks: int, planes: int):
+    """`planes` planes of host KV for the oracle legs: 64 MiB of random bytes tiled (the
+    oracle's cost does not depend on the values)."""
+    import numpy as np
+    rng = np.random.Generator(np.random.PCG64(17))
+    tile = np.frombuffer(rng.bytes(1 << 26), dtype=np.uint8)
+    kv = np.empty((planes, num_blocks * shape.block_size, shape.row_bytes), dtype=np.uint8)
+    flat = kv.reshape(-1)
+    for o in range(0, flat.size, tile.size):
+        n = min(tile.size, flat.size - o)
+        flat[o:o + n] = tile[:n]
+    return kv
+
+
+def timed_passes(fn, min_seconds: float, max_repeats: int):
+    times = []
+    while len(times) < max_repeats and sum(times) < min_seconds:
+        t0 = time.perf_counter()
+        fn()
+        times.append(time.perf_counter() - t0)
+    return times
+
+
+def positional_slots(inp):
+    """Each token's slot before the pass: its request's block table at its position."""
+    import numpy as np
+    S = inp.shape.block_size
+    out = np.empty(inp.num_tokens, dtype=np.int64)
+    for r in range(inp.num_reqs):
+        a, n = int(inp.tok_indptr[r]), int(inp.seq_lens[r])
+        bt = inp.block_ids[inp.bt_indptr[r]:inp.bt_indptr[r + 1]].astype(np.int64)
+        pos = np.arange(n)
+        out[a:a + n] = bt[pos // S] * S + pos % S
+    return out
+
+
+def cpu_baseline(inp, planes: int, min_seconds: float = 10.0, max_repeats: int = 8,
+                 inplace: bool = False):
+    """The CPU oracle as it stands, on the full metadata and `planes` planes of host KV,
+    timed over repeated passes until at least `min_seconds` of CPU work. Bytes as on the
+    GPU: each moved live row read and written once (in place: rows whose slot changes)."""
     import numpy as np
     from oracle.repack import oracle_repack_inputs
     from paper_2608_13263_amd import workloads as W
     sh = inp.shape
     planes = max(2, min(planes, sh.num_planes)) // 2 * 2
     sample_shape = W.KVShape(planes // 2, sh.num_kv_heads, sh.head_dim, sh.block_size, sh.dtype)
-    slots = inp.num_blocks * sh.block_size
-    rng = np.random.Generator(np.random.PCG64(17))
-    tile = np.frombuffer(rng.bytes(1 << 26), dtype=np.uint8)
-    kv = np.empty((planes, slots, sh.row_bytes), dtype=np.uint8)
-    flat = kv.reshape(-1)
-    for o in range(0, flat.size, tile.size):
-        n = min(tile.size, flat.size - o)
-        flat[o:o + n] = tile[:n]
-    times = []
-    while len(times) < max_repeats and sum(times) < min_seconds:
-        t0 = time.perf_counter()
-        res = oracle_repack_inputs(inp, kv)
-        times.append(time.perf_counter() - t0)
-        del res
+    kv = host_kv_sample(sh, inp.num_blocks, planes)
+    times = timed_passes(lambda: oracle_repack_inputs(inp, kv, inplace=inplace), min_seconds,
+                         max_repeats)
     dt = sum(times) / len(times)
-    res = oracle_repack_inputs(inp, None)
+    res = oracle_repack_inputs(inp, None, inplace=inplace)
     live = int(np.asarray(res.live_count, dtype=np.int64)[np.asarray(res.admitted) == 1].sum())
-    bytes_alg = 2 * live * sample_shape.token_bytes
+    rows = live
+    if inplace:
+        ts = np.asarray(res.token_slot, dtype=np.int64)
+        rows = int(((ts != positional_slots(inp)) & (inp.live != 0)).sum())
+    bytes_alg = 2 * rows * sample_shape.token_bytes
     ncpu = len(os.sched_getaffinity(0))
     return {"value": round(bytes_alg / dt / 1e9, 3), "unit": "GB/s", "cores": 1,
             "kind": "oracle",
-            "sample": f"{inp.name}: full metadata and {planes} of {sh.num_planes} KV planes "
-                      f"({kv.nbytes / 2**30:.1f} GiB host), {live} live tokens; "
-                      f"{len(times)} passes of {dt:.2f} s; numpy, single-threaded: 1 core used "
-                      f"of {ncpu} available",
+            "sample": f"{inp.name}{' (in place)' if inplace else ''}: full metadata and "
+                      f"{planes} of {sh.num_planes} KV planes ({kv.nbytes / 2**30:.1f} GiB "
+                      f"host), {live} live tokens, {rows} rows moved; {len(times)} passes of "
+                      f"{dt:.2f} s; numpy, single-threaded: 1 core used of {ncpu} available",
             "seconds_per_pass": round(dt, 3),
             "live_tokens_per_ms": round(live * planes / sh.num_planes / (dt * 1e3), 3)}
+
+
+def cpu_baseline_partial(inp, planes: int, max_sources: int, min_seconds: float = 10.0,
+                         max_repeats: int = 8):
+    """The partial-pass oracle (plan and copy) on one pass that moves rows: full metadata,
+    `planes` planes of host KV."""
+    import numpy as np
+    from oracle.planner import PlannerParams as OracleParams
+    from oracle.planner import plan_partial
+    from paper_2608_13263_amd import workloads as W
+    sh = inp.shape
+    planes = max(2, min(planes, sh.num_planes)) // 2 * 2
+    sample_shape = W.KVShape(planes // 2, sh.num_kv_heads, sh.head_dim, sh.block_size, sh.dtype)
+    kv = host_kv_sample(sh, inp.num_blocks, planes)
+    prm = OracleParams(max_sources=max_sources)
+    run = lambda: plan_partial(inp.seq_lens, inp.tok_indptr, inp.bt_indptr,  # noqa: E731
+                               inp.block_ids, inp.live, inp.slots(), inp.free_list,
+                               sh.block_size, inp.num_blocks, prm, pinned=inp.pinned, kv=kv)
+    times = timed_passes(run, min_seconds, max_repeats)
+    dt = sum(times) / len(times)
+    moved = int(run().tokens_moved)
+    ncpu = len(os.sched_getaffinity(0))
+    return {"value": round(2 * moved * sample_shape.token_bytes / dt / 1e9, 3), "unit": "GB/s",
+            "cores": 1, "kind": "oracle",
+            "sample": f"the round's moving pass: full metadata and {planes} of {sh.num_planes} "
+                      f"KV planes ({kv.nbytes / 2**30:.1f} GiB host), {moved} rows moved; "
+                      f"{len(times)} passes of {dt:.2f} s; numpy, single-threaded: 1 core used "
+                      f"of {ncpu} available",
+            "seconds_per_pass": round(dt, 3)}
+
+
+def cpu_baseline_decode(inp, token_slot, q_heads: int, min_seconds: float = 10.0):
+    """The decode oracle (float64, one request at a time) over requests in order until
+    `min_seconds`, one layer, random K/V values of the requests' live rows; BLAS held to one
+    thread. Bytes as on the GPU: each live token's head rows of K and V."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+    from oracle.attention import decode_batch, slot_mapping
+    sh = inp.shape
+    H, D = sh.num_kv_heads, sh.head_dim
+    indptr, slots = slot_mapping(token_slot, inp.tok_indptr, inp.seq_lens)
+    rng = np.random.default_rng(5)
+    done_tok, done_req, spent = 0, 0, 0.0
+    with threadpool_limits(limits=1):
+        for r in range(inp.num_reqs):
+            n = int(indptr[r + 1] - indptr[r])
+            k = rng.standard_normal((n, H, D))
+            v = rng.standard_normal((n, H, D))
+            q = rng.standard_normal((1, q_heads, D))
+            t0 = time.perf_counter()
+            decode_batch(q, k, v, np.array([0, n]), np.arange(n))
+            spent += time.perf_counter() - t0
+            done_tok += n
+            done_req += 1
+            if spent >= min_seconds:
+                break
+    bytes_alg = done_tok * 2 * H * D * sh.elem_bytes
+    return {"value": round(bytes_alg / spent / 1e9, 3), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{done_req} of {inp.num_reqs} requests ({done_tok} live tokens) of one "
+                      f"layer, {q_heads} query heads; float64 numpy, BLAS limited to 1 thread",
+            "seconds": round(spent, 3)}
 
 
 def run_copy(args):
@@ -283,6 +375,7 @@ def run_partial_stream(args):
                       shape.block_size)
     S = shape.block_size
     params = B.PlannerParams(max_sources=args.max_sources)
+    moving_pass = []          # the inputs of the first timed pass that moves rows
 
     def one_round():
         stream.decode()
@@ -311,6 +404,8 @@ def run_partial_stream(args):
                                copy_ms=ev[1].elapsed_time(ev[2]), moved=int(st[5]),
                                admitted=cnt[1], used=cnt[0], released=cnt[2],
                                F=1.0 - st[0] / max(st[1] * S, 1), attempted=int(st[3])))
+            if cnt[1] > 0 and not moving_pass:
+                moving_pass.append(inp)
             stream.commit(plan.token_slot[:inp.num_tokens].cpu().numpy(), nbi,
                           plan.new_block_ids[:int(nbi[-1])].cpu().numpy(), cnt[0],
                           state.sources[:cnt[2]].cpu().numpy())
@@ -320,6 +415,7 @@ def run_partial_stream(args):
     log(f"scissorhands (partial pass): {len(stream.pos)} requests, pool {stream.num_blocks} "
         f"blocks = {stream.num_blocks * shape.block_bytes / 2**30:.1f} GiB; warm-up round")
     one_round()
+    moving_pass.clear()
     rounds, resident = [], []
     for i in range(args.steps if args.steps != 20 else 4):
         rounds.append(one_round())
@@ -354,7 +450,8 @@ def run_partial_stream(args):
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(bytes_alg / (copy_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)
                      if copy_ms else None, "traffic": None},
-        "cpu_baseline": None,
+        "cpu_baseline": None if args.no_cpu_baseline or not moving_pass else
+        cpu_baseline_partial(moving_pass[0], args.cpu_planes, args.max_sources),
     }
     print(json.dumps(out), flush=True)
     return 0
@@ -422,6 +519,8 @@ def run_inplace(args, inp, kv, cache, batch, plan, stream):
                      "unit": "GB/s",
                      "frac": round(bytes_alg / (kern / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
                      "traffic": None},
+        "cpu_baseline": None if args.no_cpu_baseline else
+        cpu_baseline(inp, args.cpu_planes, inplace=True),
     }
     print(json.dumps(out), flush=True)
     return 0
@@ -500,6 +599,8 @@ def run_decode(args, inp, kv, cache, batch, plan, stream):
                      "achieved": round(after["call_gbs"], 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(after["call_gbs"] / HBM_PEAK_GBS, 4),
                      "traffic": None},
+        "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline_decode(
+            inp, plan.token_slot[:inp.num_tokens].cpu().numpy(), Hq),
     }
     print(json.dumps(out_json), flush=True)
     return 0
