@@ -388,13 +388,15 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
   const int grp = lane >> 4;    // which 8 elements of each 32-element chunk (scores)
   const int row = lane & 15;    // token of the tile (scores) / query head (operand, result)
   // query operand first (needed first): head `row` (zero past kG), scaled, split into high
-  // and low parts
-  OpT qh[kChunks], ql[kChunks];
+  // and low parts. Every wave needs the same operands: wave w builds chunks w, w + 4, ... for
+  // all 64 lanes into LDS, read back after the barrier below.
+  __shared__ OpT q_s[kChunks][2][64];
   {
     const bool real = row < kG;
     const float* qrow = a.q + ((int64_t)r * a.num_q_heads + h * kG + (real ? row : 0)) * kD;
 #pragma unroll
-    for (int ch = 0; ch < kChunks; ++ch) {
+    for (int ch = wave; ch < kChunks; ch += kWaves) {
+      OpT hv, lv;
 #pragma unroll
       for (int e = 0; e < kPer; ++e) {
         // unconditional load (a padded head re-reads head 0), then a select: a conditional
@@ -402,9 +404,11 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
         const float qv = qrow[ch * 32 + grp * kPer + e] * a.scale;
         const float q = real ? qv : 0.f;
         const ElemT hi = static_cast<ElemT>(q);
-        qh[ch][e] = hi;
-        ql[ch][e] = static_cast<ElemT>(q - static_cast<float>(hi));
+        hv[e] = hi;
+        lv[e] = static_cast<ElemT>(q - static_cast<float>(hi));
       }
+      q_s[ch][0][lane] = hv;
+      q_s[ch][1][lane] = lv;
     }
   }
 
@@ -434,7 +438,14 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
                                              head0 + piece * kPer * kElem);
   }
 
-  // ---- scores
+  // ---- scores (the K/V loads above stay in flight across the barrier)
+  __syncthreads();  // query operands in LDS
+  OpT qh[kChunks], ql[kChunks];
+#pragma unroll
+  for (int ch = 0; ch < kChunks; ++ch) {
+    qh[ch] = q_s[ch][0][lane];
+    ql[ch] = q_s[ch][1][lane];
+  }
 #pragma unroll
   for (int i = 0; i < kTilesPerWave; ++i) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -625,20 +636,24 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
   const bool real = (row & 7) < kG;   // column / P row of a query head (else zero padding)
   // ---- query operand first (needed first): column `row` = head row % 8, scaled, its high
   // part (row < 8) or its low part (row >= 8); the load is unconditional (padding re-reads
-  // head 0), a conditional load would wait for every outstanding K/V load
-  OpT qop[kChunks];
+  // head 0), a conditional load would wait for every outstanding K/V load. Every wave needs
+  // the same operands: wave w builds chunks w, w + 4, ... for all 64 lanes into LDS, read back
+  // after the barrier below.
+  __shared__ OpT q_s[kChunks][64];
   {
     const float* qrow =
         a.q + ((int64_t)r * a.num_q_heads + h * kG + (real ? row & 7 : 0)) * kD;
 #pragma unroll
-    for (int ch = 0; ch < kChunks; ++ch) {
+    for (int ch = wave; ch < kChunks; ch += kWaves) {
+      OpT qv8;
 #pragma unroll
       for (int e = 0; e < kPer; ++e) {
         const float qv = qrow[ch * 32 + grp * kPer + e] * a.scale;
         const float q = real ? qv : 0.f;
         const ElemT hi = static_cast<ElemT>(q);
-        qop[ch][e] = low ? static_cast<ElemT>(q - static_cast<float>(hi)) : hi;
+        qv8[e] = low ? static_cast<ElemT>(q - static_cast<float>(hi)) : hi;
       }
+      q_s[ch][lane] = qv8;
     }
   }
 
@@ -669,7 +684,12 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArg
   }
 
   // ---- scores of this wave's tiles: lane holds tokens wt0 + 16i + 4*grp + j of head row % 8
-  // (columns row and row ^ 8 summed: lanes row and row + 8 then hold the same scores)
+  // (columns row and row ^ 8 summed: lanes row and row + 8 then hold the same scores); the
+  // K/V loads above stay in flight across the barrier
+  __syncthreads();  // query operands in LDS
+  OpT qop[kChunks];
+#pragma unroll
+  for (int ch = 0; ch < kChunks; ++ch) qop[ch] = q_s[ch][lane];
   f32x4 sc[kTiles];
 #pragma unroll
   for (int i = 0; i < kTiles; ++i) {
