@@ -334,6 +334,14 @@ __device__ __forceinline__ void token_group_sum(float* v, float* out) {
   }
 }
 
+// Minimum waves per SIMD the decode kernels are compiled for. The fp8 geometries with
+// head_dim 64 or 128 come out a few registers above the four-wave budget (128 registers);
+// held to it they do not spill and run 5-10% faster. Elsewhere the compiler's choice stands
+// (bf16 / fp16 already fit four waves; fp8 with head_dim 32 or 256 would spill).
+constexpr int decode_min_waves(int kind, int head_dim) {
+  return kind == 2 && (head_dim == 64 || head_dim == 128) ? 4 : 1;
+}
+
 // Variant for GQA groups up to 4: scores on the matrix cores, weighted V sum on the vector ALUs.
 //
 // kKind: element type; kD: head_dim (32, 64, 128, 256); kG: query heads per KV head.
@@ -349,7 +357,8 @@ __device__ __forceinline__ void token_group_sum(float* v, float* out) {
 // Weighted V sum on the vector ALUs: kD/8 lanes per token, 8 elements each.
 // Every thread issues all of its K and V loads (128 + 128 bytes) before any arithmetic.
 template <int kKind, int kD, int kG>
-__global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kAttnThreads)
+__attribute__((amdgpu_waves_per_eu(decode_min_waves(kKind, kD)))) void decode_split_kernel(AttnArgs a) {
   using PieceT = typename Piece<kKind>::type;
   using OpT = typename ScoreOp<kKind>::type;
   using ElemT = typename ScoreOp<kKind>::elem;
@@ -586,7 +595,8 @@ __global__ __launch_bounds__(kAttnThreads) void decode_split_kernel(AttnArgs a) 
 // Non-finite K or V values are outside the contract (a zero weight times an infinite value
 // gives NaN).
 template <int kKind, int kD, int kG>
-__global__ __launch_bounds__(kAttnThreads) void decode_split_mfma_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kAttnThreads)
+__attribute__((amdgpu_waves_per_eu(decode_min_waves(kKind, kD)))) void decode_split_mfma_kernel(AttnArgs a) {
   using PieceT = typename Piece<kKind>::type;
   using OpT = typename ScoreOp<kKind>::type;
   using ElemT = typename ScoreOp<kKind>::elem;
