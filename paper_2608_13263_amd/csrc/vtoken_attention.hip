@@ -6,17 +6,14 @@
 //                        the live tokens' slots in logical order (Sec. 3.4: the slot mapping
 //                        is built through the token table, once per token)
 //   decode_split_kernel  one workgroup per (request, KV head, split of 32 KiB of K: 32768 /
-//                        (D * element bytes) tokens): scores of the G <= 4 query heads that
-//                        share the KV head on the matrix cores, split-local softmax, partial
-//                        weighted sum of V on the vector ALUs (flash-decoding partials)
-//   decode_split_mfma_kernel  the same for G = 8 with both products on the matrix cores
+//                        (D * element bytes) tokens): scores and the weighted sum of V of the
+//                        G query heads that share the KV head, both on the matrix cores, with
+//                        a split-local softmax (flash-decoding partials)
 //   decode_combine_kernel  one workgroup per (request, query head): merges the splits
 //
-// Decode attention is HBM-bound up to GQA groups of about 4 (2G flops per byte of K/V);
-// the score product is a small dense contraction (16 tokens x D x the G heads of a KV head)
-// and runs on MFMA, which leaves the vector ALUs to the softmax and the weighted V sum, where
-// a head's D elements are read by D/8 consecutive lanes, 8 elements (16 bytes of fp16 / bf16,
-// 8 of fp8) each.
+// Decode attention is HBM-bound (2G flops per byte of K/V). Both products are small dense
+// contractions (16 tokens x D x the G heads of a KV head, and their transposes) and run on
+// MFMA, which leaves the vector ALUs to the softmax and the operand conversions.
 #include <math.h>
 
 #include "vtoken_internal.h"
@@ -126,7 +123,6 @@ __global__ __launch_bounds__(256) void append_slots_kernel(AppendArgs a) {
 // ------------------------------------------------------------------------------------------
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kPer = 8;  // elements of a head row per lane
 
@@ -139,41 +135,6 @@ template <>
 struct Piece<2> {
   typedef u32x2 type;
 };
-
-__device__ __forceinline__ float half_bits_to_float(uint32_t h) {
-  _Float16 x;
-  const uint16_t s = static_cast<uint16_t>(h);
-  __builtin_memcpy(&x, &s, 2);
-  return static_cast<float>(x);
-}
-
-// kind 0 fp16, 1 bf16 (widening by shifts), 2 fp8: the gfx950 conversion instruction, which
-// reads OCP e4m3 (no infinities, 0x7F / 0xFF are NaN).
-template <int kKind>
-__device__ __forceinline__ void piece_to_float(typename Piece<kKind>::type w, float* out) {
-  if constexpr (kKind == 2) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const f32x2 lo = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w[i]), false);
-      const f32x2 hi = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w[i]), true);
-      out[4 * i] = lo.x;
-      out[4 * i + 1] = lo.y;
-      out[4 * i + 2] = hi.x;
-      out[4 * i + 3] = hi.y;
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if constexpr (kKind == 1) {
-        out[2 * i] = __uint_as_float(w[i] << 16);
-        out[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
-      } else {
-        out[2 * i] = half_bits_to_float(w[i] & 0xFFFFu);
-        out[2 * i + 1] = half_bits_to_float(w[i] >> 16);
-      }
-    }
-  }
-}
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -293,47 +254,6 @@ __device__ __forceinline__ float lanes_reduce(float x) {
   return xor_combine<32, kMax>(x);
 }
 
-// Sums over the token groups of the vector-ALU decode: lane l holds kN partial values for
-// head-row piece l % kLanes of token group l / kLanes (64 / kLanes groups per wave). On return
-// the totals are spread over the lanes: lane l holds out[q] = total of value
-// kSpread * q + l / 16 (kLanes <= 16, kSpread 4) or kSpread * q + l / 32 (kLanes 32, kSpread
-// 2), for every q < kN / kSpread. In-row groups are folded first by DPP rotations; the row
-// swaps then exchange two different values at once (a transposing reduction), so every
-// swap halves the values still held instead of copying one.
-template <int kLanes, int kN>
-__device__ __forceinline__ void token_group_sum(float* v, float* out) {
-  static_assert(kLanes == 4 || kLanes == 8 || kLanes == 16 || kLanes == 32, "lanes per row");
-  if constexpr (kLanes == 32) {
-    static_assert(kN % 2 == 0, "pairs");
-#pragma unroll
-    for (int q = 0; q < kN / 2; ++q) {
-      const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[2 * q]),
-                                                      __float_as_uint(v[2 * q + 1]), false, false);
-      out[q] = __uint_as_float(s[0]) + __uint_as_float(s[1]);
-    }
-  } else {
-    static_assert(kN % 4 == 0, "quads");
-#pragma unroll
-    for (int n = 0; n < kN; ++n) {
-      if constexpr (kLanes <= 8) v[n] += row_ror<8>(v[n]);
-      if constexpr (kLanes <= 4) v[n] += row_ror<4>(v[n]);
-    }
-#pragma unroll
-    for (int q = 0; q < kN / 4; ++q) {
-      // rows 0..3 after the 16-swaps: value 4q (rows 0+1), 4q+1 (0+1), 4q (2+3), 4q+1 (2+3)
-      const auto s0 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[4 * q]),
-                                                       __float_as_uint(v[4 * q + 1]), false, false);
-      const auto s1 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[4 * q + 2]),
-                                                       __float_as_uint(v[4 * q + 3]), false, false);
-      const float a = __uint_as_float(s0[0]) + __uint_as_float(s0[1]);
-      const float b = __uint_as_float(s1[0]) + __uint_as_float(s1[1]);
-      const auto s2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b),
-                                                       false, false);
-      out[q] = __uint_as_float(s2[0]) + __uint_as_float(s2[1]);
-    }
-  }
-}
-
 // Minimum waves per SIMD the decode kernels are compiled for. The fp8 geometries with
 // head_dim 64 or 128 come out a few registers above the four-wave budget (128 registers);
 // held to it they do not spill and run 5-10% faster. Elsewhere the compiler's choice stands
@@ -342,237 +262,10 @@ constexpr int decode_min_waves(int kind, int head_dim) {
   return kind == 2 && (head_dim == 64 || head_dim == 128) ? 4 : 1;
 }
 
-// Variant for GQA groups up to 4: scores on the matrix cores, weighted V sum on the vector ALUs.
+// Split kernel of the paged decode, both products on the matrix cores.
 //
-// kKind: element type; kD: head_dim (32, 64, 128, 256); kG: query heads per KV head.
-//
-// One workgroup (4 waves) covers kSplit = 32768 / (kD * element bytes) tokens of one (request,
-// KV head).
-// Scores on the matrix cores: for a tile of 16 tokens, S[token][head] = K_tile (16 x kD) times
-// Q^T (kD x 16, the kG query heads of this KV head, zero-padded), as kD/32 MFMA 16x16x32 steps;
-// the float32 query is split into a high and a low 16-bit part (q = hi + lo to about 2^-17
-// relative) and both are multiplied, so the scores keep float32 accuracy. Lane l holds token
-// l%16 and elements 8*(l/16)..+7 of each 32-element chunk (the operand layout of the
-// instruction), and receives the scores of tokens 4*(l/16)..+3 for head l%16.
-// Weighted V sum on the vector ALUs: kD/8 lanes per token, 8 elements each.
-// Every thread issues all of its K and V loads (128 + 128 bytes) before any arithmetic.
-template <int kKind, int kD, int kG>
-__global__ __launch_bounds__(kAttnThreads)
-__attribute__((amdgpu_waves_per_eu(decode_min_waves(kKind, kD)))) void decode_split_kernel(AttnArgs a) {
-  using PieceT = typename Piece<kKind>::type;
-  using OpT = typename ScoreOp<kKind>::type;
-  using ElemT = typename ScoreOp<kKind>::elem;
-  constexpr int kElem = kKind == 2 ? 1 : 2;
-  constexpr int kChunks = kD / 32;
-  constexpr int kSplit = decode_split_tokens(kD, kElem);
-  constexpr int kWaves = kAttnThreads / 64;
-  constexpr int kTilesPerWave = kSplit / 16 / kWaves;
-  constexpr int kLanes = kD / kPer;                  // V: lanes per token row
-  constexpr int kTokPerPass = kAttnThreads / kLanes;
-  constexpr int kIters = kSplit / kTokPerPass;       // V: tokens per thread
-  static_assert(kTilesPerWave * 16 * kWaves == kSplit && kIters * kPer * kElem == 128,
-                "split geometry: 128 bytes of V per thread");
-  __shared__ float p_s[kG][kSplit];
-  __shared__ float red_s[kWaves][kG];
-  __shared__ float acc_s[kWaves][kG][kD];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int split = blockIdx.x % a.splits;
-  const int h = (blockIdx.x / a.splits) % a.num_kv_heads;
-  const int r = blockIdx.x / (a.splits * a.num_kv_heads);
-  if (r >= a.num_reqs) return;
-  const int s0 = a.slot_indptr[r];
-  const int c = a.slot_count != nullptr ? a.slot_count[r] : a.slot_indptr[r + 1] - s0;
-  const int t0 = split * kSplit;
-  if (t0 >= c || s0 < 0) return;
-  const int nt = c - t0 < kSplit ? c - t0 : kSplit;
-  const int* slots = a.slots + s0 + t0;
-  const uint8_t* kplane = a.kv + (int64_t)(2 * a.layer) * a.plane_bytes;
-  const uint8_t* vplane = kplane + a.plane_bytes;
-  const int64_t head0 = (int64_t)h * kD * kElem;
-
-  // ---- all loads first; tokens past the split's end re-read its last token (dropped later)
-  const int grp = lane >> 4;    // which 8 elements of each 32-element chunk (scores)
-  const int row = lane & 15;    // token of the tile (scores) / query head (operand, result)
-  // query operand first (needed first): head `row` (zero past kG), scaled, split into high
-  // and low parts. Every wave needs the same operands: wave w builds chunks w, w + 4, ... for
-  // all 64 lanes into LDS, read back after the barrier below.
-  __shared__ OpT q_s[kChunks][2][64];
-  {
-    const bool real = row < kG;
-    const float* qrow = a.q + ((int64_t)r * a.num_q_heads + h * kG + (real ? row : 0)) * kD;
-#pragma unroll
-    for (int ch = wave; ch < kChunks; ch += kWaves) {
-      OpT hv, lv;
-#pragma unroll
-      for (int e = 0; e < kPer; ++e) {
-        // unconditional load (a padded head re-reads head 0), then a select: a conditional
-        // load would wait for every outstanding K/V load
-        const float qv = qrow[ch * 32 + grp * kPer + e] * a.scale;
-        const float q = real ? qv : 0.f;
-        const ElemT hi = static_cast<ElemT>(q);
-        hv[e] = hi;
-        lv[e] = static_cast<ElemT>(q - static_cast<float>(hi));
-      }
-      q_s[ch][0][lane] = hv;
-      q_s[ch][1][lane] = lv;
-    }
-  }
-
-  PieceT kw[kTilesPerWave][kChunks];
-  bool kok[kTilesPerWave];
-#pragma unroll
-  for (int i = 0; i < kTilesPerWave; ++i) {
-    const int t = (wave * kTilesPerWave + i) * 16 + row;
-    const int sl = slots[t < nt ? t : nt - 1];
-    kok[i] = static_cast<unsigned>(sl) < static_cast<unsigned>(a.num_slots);
-    const uint8_t* base = kplane + (int64_t)(kok[i] ? sl : 0) * a.row_bytes + head0 +
-                          grp * kPer * kElem;
-#pragma unroll
-    for (int ch = 0; ch < kChunks; ++ch) {
-      kw[i][ch] = *reinterpret_cast<const PieceT*>(base + ch * 32 * kElem);
-    }
-  }
-  const int piece = tid % kLanes;
-  const int tg = tid / kLanes;
-  PieceT vw[kIters];
-#pragma unroll
-  for (int i = 0; i < kIters; ++i) {
-    const int t = tg + i * kTokPerPass;
-    const int sl = slots[t < nt ? t : nt - 1];
-    const bool ok = static_cast<unsigned>(sl) < static_cast<unsigned>(a.num_slots);
-    vw[i] = *reinterpret_cast<const PieceT*>(vplane + (int64_t)(ok ? sl : 0) * a.row_bytes +
-                                             head0 + piece * kPer * kElem);
-  }
-
-  // ---- scores (the K/V loads above stay in flight across the barrier)
-  __syncthreads();  // query operands in LDS
-  OpT qh[kChunks], ql[kChunks];
-#pragma unroll
-  for (int ch = 0; ch < kChunks; ++ch) {
-    qh[ch] = q_s[ch][0][lane];
-    ql[ch] = q_s[ch][1][lane];
-  }
-#pragma unroll
-  for (int i = 0; i < kTilesPerWave; ++i) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ch = 0; ch < kChunks; ++ch) {
-      const OpT kop = k_operand<kKind>(kw[i][ch]);
-      acc = score_mfma<kKind>(kop, qh[ch], acc);
-      acc = score_mfma<kKind>(kop, ql[ch], acc);
-    }
-    // a slot outside the pool (its row was read at slot 0) poisons the request: NaN score
-    const uint64_t okm = __ballot(kok[i]);            // bit k: token k of the tile
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (!((okm >> (4 * grp + j)) & 1)) acc[j] = __builtin_nanf("");
-    }
-    if (row < kG) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int t = (wave * kTilesPerWave + i) * 16 + grp * 4 + j;
-        if (t < nt) p_s[row][t] = acc[j];
-      }
-    }
-  }
-  __syncthreads();
-
-  // ---- split-local softmax: max and sum of exp per query head
-  float m_g[kG], l_g[kG];
-#pragma unroll
-  for (int g = 0; g < kG; ++g) {
-    float m = -INFINITY;
-    for (int t = tid; t < nt; t += kAttnThreads) m = fmaxf(m, p_s[g][t]);
-    m = lanes_reduce<1, true>(m);
-    if (lane == 0) red_s[wave][g] = m;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int g = 0; g < kG; ++g) {
-    float m = red_s[0][g];
-    for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red_s[w][g]);
-    m_g[g] = m;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int g = 0; g < kG; ++g) {
-    float l = 0.f;
-    for (int t = tid; t < nt; t += kAttnThreads) {
-      const float e = __expf(p_s[g][t] - m_g[g]);
-      p_s[g][t] = e;
-      l += e;
-    }
-    l = lanes_reduce<1, false>(l);
-    if (lane == 0) red_s[wave][g] = l;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int g = 0; g < kG; ++g) {
-    float l = 0.f;
-    for (int w = 0; w < kWaves; ++w) l += red_s[w][g];
-    l_g[g] = l;
-  }
-
-  // ---- weighted sum of V from the registers (kG * 8 <= 64 accumulators per thread)
-  float acc[kG][kPer];
-#pragma unroll
-  for (int g = 0; g < kG; ++g)
-#pragma unroll
-    for (int e = 0; e < kPer; ++e) acc[g][e] = 0.f;
-#pragma unroll
-  for (int i = 0; i < kIters; ++i) {
-    const int t = tg + i * kTokPerPass;
-    if (t < nt) {
-      float vf[kPer];
-      piece_to_float<kKind>(vw[i], vf);
-#pragma unroll
-      for (int g = 0; g < kG; ++g) {
-        const float p = p_s[g][t];
-#pragma unroll
-        for (int e = 0; e < kPer; ++e) acc[g][e] += p * vf[e];
-      }
-    }
-  }
-  // reduce over the token groups: inside the wave (lanes with the same piece; the totals end
-  // up spread over the rows), then across waves through LDS
-  {
-    constexpr int kSpread = kLanes == 32 ? 2 : 4;
-    constexpr int kOut = kG * kPer / kSpread;
-    float tot[kOut];
-    token_group_sum<kLanes, kG * kPer>(&acc[0][0], tot);
-    const int part = kLanes == 32 ? lane >> 5 : lane >> 4;    // which of the spread values
-    if ((lane & 15) < kLanes || kLanes == 32) {              // one lane per piece and part
-#pragma unroll
-      for (int q = 0; q < kOut; ++q) {
-        const int n = kSpread * q + part;                    // value index g * kPer + e
-        acc_s[wave][n / kPer][piece * kPer + n % kPer] = tot[q];
-      }
-    }
-  }
-  __syncthreads();
-  // partial record per (request, query head, split): [m, l, acc[D]]
-  for (int i = tid; i < kG * kD; i += kAttnThreads) {
-    const int g = i / kD, d = i - g * kD;
-    float v = 0.f;
-    for (int w = 0; w < kWaves; ++w) v += acc_s[w][g][d];
-    float* rec = a.workspace +
-                 (((int64_t)r * a.num_q_heads + h * kG + g) * a.splits + split) * (kD + 2);
-    rec[2 + d] = v;
-    if (d == 0) {
-      rec[0] = m_g[g];
-      rec[1] = l_g[g];
-    }
-  }
-}
-
-// Variant for GQA groups of 8, where the weighted V sum (2 kG flops per V byte) would bound
-// the vector ALUs: both products on the matrix cores (smaller groups work too, padded, but
-// measured slower than the vector-ALU variant).
-//
-// kKind: element type; kD: head_dim (32, 64, 128, 256); kG: query heads per KV head (<= 8).
+// kKind: element type; kD: head_dim (32, 64, 128, 256); kG: query heads per KV head (1, 2,
+// 4, 8; smaller groups leave operand columns as zero padding).
 //
 // One workgroup (4 waves) covers kSplit = 32768 / (kD * element bytes) tokens of one
 // (request, KV head); wave w owns tokens [w*kTW, (w+1)*kTW), kTW = kSplit / 4, and computes
@@ -587,16 +280,17 @@ __attribute__((amdgpu_waves_per_eu(decode_min_waves(kKind, kD)))) void decode_sp
 //           chunk, row c < 8 of P2 the high part of head c's weights, row c + 8 their low
 //           part, so O_w[c] = O2[c] + O2[c + 8]. V goes through a per-wave LDS window of 32
 //           rows, one 32-token k-step at a time (16-bit rows, padded by 32 bytes against bank
-//           conflicts), and comes back in operand layout by transpose reads. The operand layout fixes which tokens a lane holds: lane l has column
-//           l%16 and, of each 32-token chunk, tokens 4*(l/16)..+3 of its first 16-token tile
-//           and the same of its second; the V rows are read in that order.
+//           conflicts), and comes back in operand layout by transpose reads. The operand
+//           layout fixes which tokens a lane holds: lane l has column l%16 and, of each
+//           32-token chunk, tokens 4*(l/16)..+3 of its first 16-token tile and the same of its
+//           second; the V rows are read in that order.
 // The four waves are merged with the usual max-rescaling into the split's record.
 // Every thread issues all of its K and V loads (128 + 128 bytes) before any arithmetic.
 // Non-finite K or V values are outside the contract (a zero weight times an infinite value
 // gives NaN).
 template <int kKind, int kD, int kG>
 __global__ __launch_bounds__(kAttnThreads)
-__attribute__((amdgpu_waves_per_eu(decode_min_waves(kKind, kD)))) void decode_split_mfma_kernel(AttnArgs a) {
+__attribute__((amdgpu_waves_per_eu(decode_min_waves(kKind, kD)))) void decode_split_kernel(AttnArgs a) {
   using PieceT = typename Piece<kKind>::type;
   using OpT = typename ScoreOp<kKind>::type;
   using ElemT = typename ScoreOp<kKind>::elem;
@@ -915,15 +609,8 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(AttnArg
 template <int kKind, int kD, int kG>
 hipError_t launch_split(const AttnArgs& a, hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>((int64_t)a.num_reqs * a.num_kv_heads * a.splits));
-  // GQA groups of 8 have both products on the matrix cores; smaller groups keep the value sum
-  // on the vector ALUs (measured faster for them)
-  if constexpr (kG >= 8) {
-    auto kernel = decode_split_mfma_kernel<kKind, kD, kG>;
-    hipLaunchKernelGGL(kernel, grid, dim3(kAttnThreads), 0, stream, a);
-  } else {
-    auto kernel = decode_split_kernel<kKind, kD, kG>;
-    hipLaunchKernelGGL(kernel, grid, dim3(kAttnThreads), 0, stream, a);
-  }
+  auto kernel = decode_split_kernel<kKind, kD, kG>;
+  hipLaunchKernelGGL(kernel, grid, dim3(kAttnThreads), 0, stream, a);
   return hipGetLastError();
 }
 
