@@ -257,7 +257,8 @@ __device__ __forceinline__ float lanes_reduce(float x) {
 // Minimum waves per SIMD the decode kernels are compiled for. The fp8 geometries with
 // head_dim 64 or 128 come out a few registers above the four-wave budget (128 registers);
 // held to it they do not spill and run 5-10% faster. Elsewhere the compiler's choice stands
-// (bf16 / fp16 already fit four waves; fp8 with head_dim 32 or 256 would spill).
+// (bf16 / fp16 up to head_dim 128 already fit four waves; fp8 with head_dim 32 or 256
+// would spill).
 constexpr int decode_min_waves(int kind, int head_dim) {
   return kind == 2 && (head_dim == 64 || head_dim == 128) ? 4 : 1;
 }
@@ -290,7 +291,8 @@ constexpr int decode_min_waves(int kind, int head_dim) {
 // gives NaN).
 template <int kKind, int kD, int kG>
 __global__ __launch_bounds__(kAttnThreads)
-__attribute__((amdgpu_waves_per_eu(decode_min_waves(kKind, kD)))) void decode_split_kernel(AttnArgs a) {
+__attribute__((amdgpu_waves_per_eu(decode_min_waves(kKind, kD))))
+void decode_split_kernel(AttnArgs a) {
   using PieceT = typename Piece<kKind>::type;
   using OpT = typename ScoreOp<kKind>::type;
   using ElemT = typename ScoreOp<kKind>::elem;
