@@ -363,7 +363,7 @@ vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode
   a.kv_kind = kind;
   a.num_slots = cache->num_blocks * cache->block_size;
   a.num_reqs = num_reqs;
-  const int split = vtoken::decode_split_tokens(D, cache->elem_bytes);
+  const int split = vtoken::decode_split_tokens(D, cache->elem_bytes, g);
   a.split_tokens = split;
   a.splits = d->max_tokens > 0 ? (d->max_tokens + split - 1) / split : 1;
   if ((int64_t)num_reqs * cache->num_kv_heads * a.splits > INT32_MAX ||

@@ -21,7 +21,6 @@
 namespace vtoken {
 namespace {
 
-constexpr int kAttnThreads = 256;
 
 __device__ __forceinline__ int lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
@@ -257,8 +256,8 @@ __device__ __forceinline__ float lanes_reduce(float x) {
 // Minimum waves per SIMD the decode kernels are compiled for. The fp8 geometries with
 // head_dim 64 or 128 come out a few registers above the four-wave budget (128 registers);
 // held to it they do not spill and run 5-10% faster. Elsewhere the compiler's choice stands
-// (bf16 / fp16 up to head_dim 128 already fit four waves; fp8 with head_dim 32 or 256
-// would spill).
+// (bf16 / fp16 up to head_dim 128 already fit four waves per SIMD; fp8 with head_dim 32 or
+// 256 would spill).
 constexpr int decode_min_waves(int kind, int head_dim) {
   return kind == 2 && (head_dim == 64 || head_dim == 128) ? 4 : 1;
 }
@@ -268,8 +267,9 @@ constexpr int decode_min_waves(int kind, int head_dim) {
 // kKind: element type; kD: head_dim (32, 64, 128, 256); kG: query heads per KV head (1, 2,
 // 4, 8; smaller groups leave operand columns as zero padding).
 //
-// One workgroup (4 waves) covers kSplit = 32768 / (kD * element bytes) tokens of one
-// (request, KV head); wave w owns tokens [w*kTW, (w+1)*kTW), kTW = kSplit / 4, and computes
+// One workgroup (kWaves = 4 waves, 8 for 16-bit caches at kG = 8) covers kSplit = kWaves *
+// 8192 / (kD * element bytes) tokens of one (request, KV head); wave w owns tokens
+// [w*kTW, (w+1)*kTW), kTW = kSplit / kWaves, and computes
 // for them, on the matrix cores (MFMA 16x16x32, fp16 for fp16 caches, bf16 otherwise; fp8
 // widened to bf16):
 //   scores  S[token][col] = K_tile (16 x kD) . Q2^T (kD x 16). The float32 query is split into
@@ -285,12 +285,12 @@ constexpr int decode_min_waves(int kind, int head_dim) {
 //           layout fixes which tokens a lane holds: lane l has column l%16 and, of each
 //           32-token chunk, tokens 4*(l/16)..+3 of its first 16-token tile and the same of its
 //           second; the V rows are read in that order.
-// The four waves are merged with the usual max-rescaling into the split's record.
+// The waves are merged with the usual max-rescaling into the split's record.
 // Every thread issues all of its K and V loads (128 + 128 bytes) before any arithmetic.
 // Non-finite K or V values are outside the contract (a zero weight times an infinite value
 // gives NaN).
 template <int kKind, int kD, int kG>
-__global__ __launch_bounds__(kAttnThreads)
+__global__ __launch_bounds__(64 * decode_split_waves(kKind == 2 ? 1 : 2, kG))
 __attribute__((amdgpu_waves_per_eu(decode_min_waves(kKind, kD))))
 void decode_split_kernel(AttnArgs a) {
   using PieceT = typename Piece<kKind>::type;
@@ -298,8 +298,9 @@ void decode_split_kernel(AttnArgs a) {
   using ElemT = typename ScoreOp<kKind>::elem;
   constexpr int kElem = kKind == 2 ? 1 : 2;
   constexpr int kChunks = kD / 32;                   // score k-steps
-  constexpr int kSplit = decode_split_tokens(kD, kElem);
-  constexpr int kWaves = kAttnThreads / 64;
+  constexpr int kSplit = decode_split_tokens(kD, kElem, kG);
+  constexpr int kWaves = decode_split_waves(kElem, kG);
+  constexpr int kThreads = 64 * kWaves;
   constexpr int kTW = kSplit / kWaves;               // tokens per wave: 16 .. 256
   constexpr int kTiles = kTW / 16;                   // 16-token score tiles per wave
   constexpr int kKC = (kTiles + 1) / 2;              // 32-token value k-steps per wave
@@ -343,7 +344,7 @@ void decode_split_kernel(AttnArgs a) {
   // ---- query operand first (needed first): column `row` = head row % 8, scaled, its high
   // part (row < 8) or its low part (row >= 8); the load is unconditional (padding re-reads
   // head 0), a conditional load would wait for every outstanding K/V load. Every wave needs
-  // the same operands: wave w builds chunks w, w + 4, ... for all 64 lanes into LDS, read back
+  // the same operands: wave w builds chunks w, w + kWaves, ... for all 64 lanes into LDS, read
   // after the barrier below.
   __shared__ OpT q_s[kChunks][64];
   {
@@ -492,7 +493,7 @@ void decode_split_kernel(AttnArgs a) {
     for (int j = 0; j < 4; ++j) o[dc][j] = xor_combine<32, false>(o[dc][j]);
   __syncthreads();  // the LDS rows are reused for the merge
 
-  // ---- merge the four waves: [m_w, l_w] and O_w[head][d] per wave into LDS
+  // ---- merge the waves: [m_w, l_w] and O_w[head][d] per wave into LDS
   float* mrg = reinterpret_cast<float*>(lds);        // [wave][head][kD + 2]
   if (grp == 0 && row < kG) {
     mrg[(wave * kG + row) * (kD + 2)] = m;
@@ -508,7 +509,7 @@ void decode_split_kernel(AttnArgs a) {
       }
   }
   __syncthreads();
-  for (int i = tid; i < kG * kD; i += kAttnThreads) {
+  for (int i = tid; i < kG * kD; i += kThreads) {
     const int g = i / kD, d = i - g * kD;
     float M = -INFINITY;
 #pragma unroll
@@ -612,7 +613,8 @@ template <int kKind, int kD, int kG>
 hipError_t launch_split(const AttnArgs& a, hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>((int64_t)a.num_reqs * a.num_kv_heads * a.splits));
   auto kernel = decode_split_kernel<kKind, kD, kG>;
-  hipLaunchKernelGGL(kernel, grid, dim3(kAttnThreads), 0, stream, a);
+  hipLaunchKernelGGL(kernel, grid, dim3(64 * decode_split_waves(kKind == 2 ? 1 : 2, kG)), 0,
+                     stream, a);
   return hipGetLastError();
 }
 
@@ -658,7 +660,8 @@ hipError_t launch_slot_mapping(const SlotMapArgs& a, hipStream_t stream) {
 
 hipError_t launch_paged_decode(const AttnArgs& a, hipStream_t stream) {
   if (a.num_reqs <= 0) return hipSuccess;
-  if (a.split_tokens != decode_split_tokens(a.head_dim, a.kv_kind == 2 ? 1 : 2)) {
+  if (a.split_tokens !=
+      decode_split_tokens(a.head_dim, a.kv_kind == 2 ? 1 : 2, a.num_q_heads / a.num_kv_heads)) {
     return hipErrorInvalidValue;
   }
   hipError_t e;

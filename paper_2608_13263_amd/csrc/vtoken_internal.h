@@ -190,15 +190,24 @@ hipError_t launch_planner(const PlannerArgs& a, hipStream_t stream);
 hipError_t launch_slot_mapping(const SlotMapArgs& a, hipStream_t stream);
 hipError_t launch_append_slots(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_paged_decode(const AttnArgs& a, hipStream_t stream);
-// Tokens one decode workgroup covers: 32 KiB of K (and of V) of one KV head, i.e. 8 pieces
-// of 16 bytes per thread and operand over 256 threads (head_dim 32, 64, 128, 256 -> 512, 256,
-// 128, 64 tokens at 2 bytes per element, twice as many at 1 byte).
-constexpr int kDecodeSplitBytes = 32768;
-constexpr int decode_split_tokens(int head_dim, int elem_bytes) {
-  return kDecodeSplitBytes / (head_dim * elem_bytes);
+// Decode split geometry. Each wave of a split workgroup covers 8 KiB of K (and of V) of one
+// KV head: 128 bytes per lane and operand. A workgroup has 4 waves, or 8 for 16-bit caches
+// with GQA groups of 8, whose per-workgroup work (query operands, the merge of the waves, a
+// split record of 8 heads) is then spread over twice the tokens (measured +11%; 8 waves were
+// neutral at G = 4 and slower for fp8, whose waves already cover twice the tokens).
+constexpr int kDecodeWaveBytes = 8192;
+constexpr int decode_split_waves(int elem_bytes, int group) {
+  return elem_bytes == 2 && group == 8 ? 8 : 4;
 }
-// The smallest split over the element sizes: the workspace bound of the C ABI.
-constexpr int decode_min_split_tokens(int head_dim) { return decode_split_tokens(head_dim, 2); }
+// Tokens one split workgroup covers (head_dim 32, 64, 128, 256 -> 512, 256, 128, 64 tokens
+// for 16-bit caches with 4 waves; twice as many with 8 waves or at 1 byte per element).
+constexpr int decode_split_tokens(int head_dim, int elem_bytes, int group) {
+  return decode_split_waves(elem_bytes, group) * kDecodeWaveBytes / (head_dim * elem_bytes);
+}
+// The smallest split over the element sizes and groups: the workspace bound of the C ABI.
+constexpr int decode_min_split_tokens(int head_dim) {
+  return decode_split_tokens(head_dim, 2, 1);
+}
 
 hipError_t launch_build(const MetaArgs& a, hipStream_t stream);
 // variant: 0 default, 1 LDS double buffer, 2 LDS single buffer, 3 registers
