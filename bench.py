@@ -43,7 +43,10 @@ def parse_args(argv=None):
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="llama3_8b_random",
                     choices=["llama3_8b_random", "llama3_8b_h2o", "llama3_70b_h2o", "tiny",
-                             "llama3_8b_scissorhands"])
+                             "llama3_8b_scissorhands", "llama3_8b_block_copy"],
+                    help="llama3_8b_block_copy: whole contiguous blocks to contiguous "
+                         "destinations in the same-size pool, the copy's streaming ceiling "
+                         "(a reference, not a paper workload)")
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--keep", type=float, default=0.3, help="keep ratio (70B config)")
     ap.add_argument("--kv-dtype", default="fp8_e4m3", help="70B config: fp8_e4m3 or bf16")
@@ -91,6 +94,11 @@ def make_workload(args):
         return W.llama3_8b_h2o(args.seed if args.seed is not None else 301)
     if args.config == "tiny":
         return W.tiny_cache(args.seed if args.seed is not None else 101)
+    if args.config == "llama3_8b_block_copy":
+        import torch
+        free, _ = torch.cuda.mem_get_info()
+        return W.llama3_8b_block_copy(pool_bytes=int(args.pool_frac * free)
+                                      if args.pool_frac > 0 else None)
     import torch
     free, _ = torch.cuda.mem_get_info()
     budget = min(240 * 2 ** 30, int(0.85 * free))

@@ -655,11 +655,39 @@ class PartialStream:
         return sum(len(t) for t in self.tables)
 
 
+def llama3_8b_block_copy(num_reqs: int = 3277, num_layers: int = 32,
+                         pool_bytes: Optional[int] = None) -> RepackInputs:
+    """Reference workload for the copy's streaming ceiling (not a paper workload): Llama-3-8B
+    geometry, each request 3 consecutive blocks of which the first two are fully live and the
+    third fully dead, and the free list in address order after them. A repack then copies
+    whole blocks from contiguous sources to contiguous destinations, the same kernel and about
+    the bytes of the Llama-3-8B Random workload (3,277 requests: 27.5 GB). With `pool_bytes`
+    the pool is that large (the other blocks stay free)."""
+    shape = KVShape(num_layers, 8, 128, 16, "bf16")
+    S = shape.block_size
+    R = int(num_reqs)
+    M = 3 * R
+    num_blocks = M + 2 * R + 1024
+    if pool_bytes is not None:
+        num_blocks = max(num_blocks, int(pool_bytes // shape.block_bytes))
+    seq_lens = np.full(R, 3 * S, dtype=np.int32)
+    live = np.tile(np.concatenate([np.ones(2 * S, np.uint8), np.zeros(S, np.uint8)]), R)
+    return RepackInputs(
+        name="llama3_8b_block_copy", shape=shape, num_blocks=num_blocks, seq_lens=seq_lens,
+        tok_indptr=(np.arange(R + 1) * 3 * S).astype(np.int32),
+        bt_indptr=(np.arange(R + 1) * 3).astype(np.int32),
+        block_ids=np.arange(M, dtype=np.int32), live=live,
+        free_list=np.arange(M, num_blocks, dtype=np.int32), seed=0,
+        note=f"bf16 {num_layers}x8x128, S=16, {R} req of 3 consecutive blocks (2 live, 1 dead), "
+             f"sequential free list, {num_blocks * shape.block_bytes / 2**30:.0f} GiB pool")
+
+
 CONFIGS: Dict[str, Callable[..., RepackInputs]] = {
     "tiny": tiny_cache,
     "llama3_8b_random": llama3_8b_random,
     "llama3_8b_h2o": llama3_8b_h2o,
     "llama3_70b_h2o": llama3_70b_h2o,
+    "llama3_8b_block_copy": llama3_8b_block_copy,
 }
 
 
