@@ -29,8 +29,9 @@ Readings where the paper gives no number or order (frozen in the C header as wel
   * a block is a low-utilisation source candidate iff it is in exactly one table, is not
     pinned and n_b <= max_live_per_source (default: its own waste exceeds theta_F,
     n_b < (1 - theta_F) * S);
-  * "enough low-utilisation blocks": at least min_eligible candidates; "near the low
-    watermark": free-list length <= free_watermark (a negative watermark drops the condition);
+  * a sufficient number of low-utilisation blocks: at least min_eligible candidates; a free
+    count close to the low watermark: free-list length <= free_watermark (a negative
+    watermark drops the condition);
     F > theta_F is evaluated exactly as (N*S - sum n_b) * den > num * N*S;
   * B counts the blocks considered: candidates are taken in request order, table order
     within a request, until B are taken, whether or not the request's plan is then admitted;
