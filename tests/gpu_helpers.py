@@ -121,6 +121,12 @@ def gpu_partial(inp, kv, params=None, label=""):
     B.plan_partial(cache, batch, slot_in, plan, state, params)
     B.repack(cache, batch, plan)
     t.cuda.synchronize()
+    return partial_to_host(plan, state, inp)
+
+
+def partial_to_host(plan, state, inp):
+    """Host copies of the partial pass's outputs, trimmed to the sizes the counters report."""
+    sh = inp.shape
     h = {k: getattr(plan, k).cpu().numpy() for k in plan.FIELDS}
     for k in state.FIELDS:
         h[k] = getattr(state, k).cpu().numpy()

@@ -5,7 +5,8 @@ new tables, source plan, released sources) and every KV byte after the copy."""
 import numpy as np
 import pytest
 
-from gpu_helpers import assert_partial_equal, gpu_partial, kv_bytes, run_partial_oracle, torch
+from gpu_helpers import (assert_partial_equal, gpu_partial, kv_bytes, partial_to_host,
+                         run_partial_oracle, torch)
 from oracle.repack import oracle_repack_inputs
 from paper_2608_13263_amd import workloads as W
 
@@ -209,3 +210,60 @@ def test_two_cache_groups_share_liveness():
                                       b.slot_in[a.live == 0])
     for inp, seed in ((a, 1), (b, 2)):
         partial_parity(inp, B.PlannerParams(), seed=seed, label=f"group {inp.shape.dtype}")
+
+
+def test_partial_pass_graph_replay():
+    """Planner and copy captured once in a HIP graph and replayed: before each replay new
+    liveness (a random subset of the tokens that hold a slot) is written into the captured
+    live-mask buffer; every replay equals the oracle on those inputs and the KV bytes the
+    previous replay left. The planner clears its state with a kernel, never a memset."""
+    import dataclasses
+    t = torch()
+    B = _B()
+    inp = W.token_table_inputs(641, W.KVShape(1, 2, 64, 16, "bf16"), num_reqs=16,
+                               len_range=(200, 1500), shared_groups=2, group_size=3,
+                               prefix_tokens=96)
+    sh = inp.shape
+    prm = B.PlannerParams(theta=(-1, 1), max_live_per_source=16, min_eligible=0)
+    kv = W.kv_device(sh, inp.num_blocks, 9)
+    cache = B.KVCache(kv, sh.num_layers, sh.num_kv_heads, sh.head_dim, sh.block_size)
+    batch = B.Batch.from_inputs(inp)
+    slot_in = t.from_numpy(np.ascontiguousarray(inp.slots(), dtype=np.int32)).cuda()
+    plan = B.Plan.allocate(batch, sh.block_size)
+    state = B.PlannerState.allocate(inp.num_blocks, batch, pinned=inp.pinned)
+    print(f"[gpu] partial graph replay: R={inp.num_reqs} T={inp.num_tokens}", flush=True)
+
+    def run():
+        B.plan_partial(cache, batch, slot_in, plan, state, prm)
+        B.repack(cache, batch, plan)
+
+    side = t.cuda.Stream()
+    side.wait_stream(t.cuda.current_stream())
+    before = kv_bytes(kv, sh)
+    with t.cuda.stream(side):
+        run()
+    t.cuda.current_stream().wait_stream(side)
+    t.cuda.synchronize()
+    o = run_partial_oracle(inp, before, prm)
+    assert_partial_equal(partial_to_host(plan, state, inp), o, inp)
+    assert np.array_equal(kv_bytes(kv, sh), o.kv)
+
+    graph = t.cuda.CUDAGraph()
+    with t.cuda.graph(graph):
+        run()
+    rng = np.random.default_rng(3)
+    has_slot = inp.slots() >= 0
+    for step, keep in enumerate((0.3, 0.6, 0.9)):
+        live = (has_slot & (rng.random(inp.num_tokens) < keep)).astype(np.uint8)
+        cur = dataclasses.replace(inp, live=live)
+        batch.live.copy_(t.from_numpy(live).to(batch.live.device))
+        t.cuda.synchronize()
+        before = kv_bytes(kv, sh)
+        noise = t.randn(256, 256, device="cuda")
+        noise = noise @ noise                     # unrelated eager work between replays
+        graph.replay()
+        t.cuda.synchronize()
+        o = run_partial_oracle(cur, before, prm)
+        assert_partial_equal(partial_to_host(plan, state, cur), o, cur)
+        assert np.array_equal(kv_bytes(kv, sh), o.kv), f"KV bytes, replay {step}"
+        assert o.n_admitted > 0
