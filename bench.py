@@ -15,7 +15,10 @@ their destinations and 1024 spare blocks, 56 GiB).
 
 Prints one JSON line. `value` is repacked KV GB/s over the whole step (read+write bytes of
 the live rows: 2 * live tokens * 2*L*H*D*elem_bytes); `roofline` prices the repack kernel
-alone against the 8 TB/s HBM peak, timed with HIP events on its launch stream.
+alone against the 8 TB/s HBM peak, timed with HIP events on its launch stream (the build and
+free calls are timed separately); `ceiling` is the same kernel copying whole contiguous
+blocks of the same pool in the same run (the practical streaming rate) next to torch's
+device copy; `cpu_baseline` is the CPU oracle on a sample of the planes.
 
     python bench.py [--steps K] [--warmup W] [--config NAME] [--variant V] [--grid G]
     python bench.py --mode copy      # plain device-to-device copy of known size
@@ -27,6 +30,7 @@ import hashlib
 import json
 import os
 import re
+import statistics
 import sys
 import time
 
@@ -50,6 +54,12 @@ def parse_args(argv=None):
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--keep", type=float, default=0.3, help="keep ratio (70B config)")
     ap.add_argument("--kv-dtype", default="fp8_e4m3", help="70B config: fp8_e4m3 or bf16")
+    ap.add_argument("--kv-heads", type=int, default=8,
+                    help="70B config: KV heads in the cache (1 = one GPU's share under 8-way "
+                         "tensor parallelism: 256 B / 128 B rows)")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the streaming-ceiling leg (whole contiguous blocks of the same "
+                         "pool through the same kernel, and a torch device copy)")
     ap.add_argument("--variant", type=int, default=0)
     ap.add_argument("--grid", type=int, default=0)
     ap.add_argument("--order", type=int, default=0)
@@ -103,7 +113,7 @@ def make_workload(args):
     free, _ = torch.cuda.mem_get_info()
     budget = min(240 * 2 ** 30, int(0.85 * free))
     return W.llama3_70b_h2o(args.seed if args.seed is not None else 501, keep=args.keep,
-                            dtype=args.kv_dtype, pool_bytes=budget)
+                            dtype=args.kv_dtype, num_kv_heads=args.kv_heads, pool_bytes=budget)
 
 
 def recorded_traffic(config: str):
@@ -250,6 +260,71 @@ def cpu_baseline_decode(inp, token_slot, q_heads: int, min_seconds: float = 10.0
             "sample": f"{done_req} of {inp.num_reqs} requests ({done_tok} live tokens) of one "
                       f"layer, {q_heads} query heads; float64 numpy, BLAS limited to 1 thread",
             "seconds": round(spent, 3)}
+
+
+def inputs_sha256(inp) -> dict:
+    """SHA-256 (first 16 hex digits) of every input array of the pass."""
+    import numpy as np
+    out = {}
+    for k in ("seq_lens", "tok_indptr", "bt_indptr", "block_ids", "live", "free_list"):
+        a = np.ascontiguousarray(getattr(inp, k))
+        out[k] = hashlib.sha256(a.tobytes()).hexdigest()[:16]
+    return out
+
+
+def streaming_ceiling(args, inp, kv, cache, bytes_alg: int, stream, steps: int = 10):
+    """The copy's practical ceiling, timed in the same run on the same pool: the repack kernel
+    on whole contiguous blocks (block-copy metadata over the same KV tensor, about the same
+    bytes), and torch's device copy of 4 GiB when that much HBM is still free. Runs after the
+    timed steps (it overwrites blocks of the pool; the copy is value-agnostic)."""
+    import torch
+    from paper_2608_13263_amd import binding as B
+    from paper_2608_13263_amd import workloads as W
+    sh = inp.shape
+    per_req = 2 * 2 * sh.block_size * sh.token_bytes
+    R = max(1, min(int(round(bytes_alg / per_req)), (inp.num_blocks - 1024) // 5))
+    ref = W.block_copy_inputs(sh, R, inp.num_blocks, name="block_copy")
+    cb = B.Batch.from_inputs(ref)
+    cp = B.Plan.allocate(cb, sh.block_size)
+    B.build_token_table(cache, cb, cp, stream)
+    for _ in range(3):
+        B.repack(cache, cb, cp, stream)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    for a, b in evs:
+        a.record(stream)
+        B.repack(cache, cb, cp, stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    if int(cp.counters[3]) != 0 or int(cp.counters[1]) != R:
+        raise SystemExit("block-copy reference: unexpected plan")
+    ms = sum(a.elapsed_time(b) for a, b in evs) / steps
+    ref_bytes = 2 * R * 2 * sh.block_size * sh.token_bytes
+    gbs = ref_bytes / (ms / 1e3) / 1e9
+    out = {"kind": "repack_direct_kernel on whole contiguous blocks of the same pool",
+           "bytes": ref_bytes, "ms": round(ms, 4), "GBps": round(gbs, 1),
+           "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    del cb, cp
+    free, _ = torch.cuda.mem_get_info()
+    n = 4 << 30
+    if free > 2 * n + (1 << 30):
+        src = torch.empty(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(3)
+        dst.copy_(src)
+        cev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(5)]
+        for a, b in cev:
+            a.record()
+            dst.copy_(src)
+            b.record()
+        torch.cuda.synchronize()
+        cms = sum(a.elapsed_time(b) for a, b in cev) / len(cev)
+        out["torch_copy_4GiB_GBps"] = round(2 * n / (cms / 1e3) / 1e9, 1)
+        del src, dst
+    log(f"ceiling: block copy {gbs:.0f} GB/s, torch copy "
+        f"{out.get('torch_copy_4GiB_GBps', 'skipped')}")
+    return out
 
 
 def run_copy(args):
@@ -650,18 +725,22 @@ def main(argv=None):
     log(f"setup {time.perf_counter() - t_setup:.1f} s; warmup {args.warmup} steps")
 
     def step(ev=None):
-        B.build_token_table(cache, batch, plan, stream)
         if ev is not None:
             ev[0].record(stream)
-        B.repack_ex(cache, batch, plan, args.variant, args.grid, args.order, stream)
+        B.build_token_table(cache, batch, plan, stream)
         if ev is not None:
             ev[1].record(stream)
+        B.repack_ex(cache, batch, plan, args.variant, args.grid, args.order, stream)
+        if ev is not None:
+            ev[2].record(stream)
         B.free_blocks(batch, plan, stream=stream)
+        if ev is not None:
+            ev[3].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4))
            for _ in range(args.steps)]
     log(f"timing {args.steps} steps")
     torch.cuda.synchronize()
@@ -671,8 +750,10 @@ def main(argv=None):
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
-    repack_ms = [a.elapsed_time(b) for a, b in evs]
+    repack_ms = [e[1].elapsed_time(e[2]) for e in evs]
     repack_avg = sum(repack_ms) / len(repack_ms)
+    build_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / len(evs)
+    free_ms = sum(e[2].elapsed_time(e[3]) for e in evs) / len(evs)
 
     counters = plan.counters.cpu().tolist()
     if counters[3] != 0:
@@ -687,6 +768,10 @@ def main(argv=None):
     traffic = recorded_traffic(args.config)
     log(f"step {ms_per_step:.3f} ms, repack {repack_avg:.3f} ms "
         f"(min {min(repack_ms):.3f}), {achieved:.0f} GB/s repack")
+
+    ceiling = None
+    if not args.no_ceiling:
+        ceiling = streaming_ceiling(args, inp, kv, cache, bytes_alg, stream)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -709,7 +794,10 @@ def main(argv=None):
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "live_tokens_per_ms": round(moved_tokens / ms_per_step, 1),
         "repack_ms": round(repack_avg, 4),
+        "repack_ms_median": round(statistics.median(repack_ms), 4),
         "repack_ms_min": round(min(repack_ms), 4),
+        "build_token_table_ms": round(build_ms, 4),
+        "free_blocks_ms": round(free_ms, 4),
         "config": {
             "workload": inp.name,
             "recipe": inp.note,
@@ -719,7 +807,7 @@ def main(argv=None):
             "pool_blocks": inp.num_blocks, "pool_gib": round(inp.pool_bytes() / 2 ** 30, 2),
             "used_blocks": counters[0], "admitted": counters[1], "freed_blocks": counters[2],
             "bytes_alg_per_step": bytes_alg, "variant": args.variant, "grid": args.grid,
-            "order": args.order,
+            "order": args.order, "inputs_sha256": inputs_sha256(inp),
         },
         "roofline": {
             "bound": "hbm", "kernel": "repack_direct_kernel",
@@ -727,6 +815,7 @@ def main(argv=None):
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
         },
+        "ceiling": ceiling,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -284,7 +284,8 @@ def llama3_70b_h2o(seed: int = 501, keep: float = 0.3, dtype: str = "fp8_e4m3",
         used += b
     lens = lens[:keep_n]
     masks = [h2o_live(rng, int(n), keep, recent) for n in lens]
-    return _assemble(f"llama3_70b_h2o_{dtype}_k{keep}", shape, rng, lens, masks,
+    heads = "" if num_kv_heads == 8 else f"_h{num_kv_heads}"
+    return _assemble(f"llama3_70b_h2o_{dtype}_k{keep}{heads}", shape, rng, lens, masks,
                      pool_blocks - used, seed,
                      f"{dtype} {num_layers}x{num_kv_heads}x128, S=32, {keep_n} of {num_reqs} "
                      f"req U{list(len_range)}, H2O keep {keep} + last {recent}")
@@ -655,31 +656,39 @@ class PartialStream:
         return sum(len(t) for t in self.tables)
 
 
-def llama3_8b_block_copy(num_reqs: int = 3277, num_layers: int = 32,
-                         pool_bytes: Optional[int] = None) -> RepackInputs:
-    """Reference workload for the copy's streaming ceiling (not a paper workload): Llama-3-8B
-    geometry, each request 3 consecutive blocks of which the first two are fully live and the
-    third fully dead, and the free list in address order after them. A repack then copies
-    whole blocks from contiguous sources to contiguous destinations, the same kernel and about
-    the bytes of the Llama-3-8B Random workload (3,277 requests: 27.5 GB). With `pool_bytes`
-    the pool is that large (the other blocks stay free)."""
-    shape = KVShape(num_layers, 8, 128, 16, "bf16")
+def block_copy_inputs(shape: KVShape, num_reqs: int, num_blocks: Optional[int] = None,
+                      name: str = "block_copy", note: str = "") -> RepackInputs:
+    """Reference inputs for the copy's streaming ceiling (not a paper workload): each request
+    holds 3 consecutive blocks of which the first two are fully live and the third fully dead,
+    and the free list follows them in address order, so a repack copies whole blocks from
+    contiguous sources to contiguous destinations. The pool has `num_blocks` blocks (at least
+    the 5 per request it needs plus 1024); the blocks past those stay free."""
     S = shape.block_size
     R = int(num_reqs)
     M = 3 * R
-    num_blocks = M + 2 * R + 1024
-    if pool_bytes is not None:
-        num_blocks = max(num_blocks, int(pool_bytes // shape.block_bytes))
-    seq_lens = np.full(R, 3 * S, dtype=np.int32)
+    nb = max(M + 2 * R + 1024, int(num_blocks or 0))
     live = np.tile(np.concatenate([np.ones(2 * S, np.uint8), np.zeros(S, np.uint8)]), R)
     return RepackInputs(
-        name="llama3_8b_block_copy", shape=shape, num_blocks=num_blocks, seq_lens=seq_lens,
+        name=name, shape=shape, num_blocks=nb, seq_lens=np.full(R, 3 * S, dtype=np.int32),
         tok_indptr=(np.arange(R + 1) * 3 * S).astype(np.int32),
         bt_indptr=(np.arange(R + 1) * 3).astype(np.int32),
         block_ids=np.arange(M, dtype=np.int32), live=live,
-        free_list=np.arange(M, num_blocks, dtype=np.int32), seed=0,
-        note=f"bf16 {num_layers}x8x128, S=16, {R} req of 3 consecutive blocks (2 live, 1 dead), "
-             f"sequential free list, {num_blocks * shape.block_bytes / 2**30:.0f} GiB pool")
+        free_list=np.arange(M, nb, dtype=np.int32), seed=0,
+        note=note or f"{R} req of 3 consecutive blocks (2 live, 1 dead), sequential free list")
+
+
+def llama3_8b_block_copy(num_reqs: int = 3277, num_layers: int = 32,
+                         pool_bytes: Optional[int] = None) -> RepackInputs:
+    """The block-copy reference in the Llama-3-8B geometry with the bytes of the Llama-3-8B
+    Random workload (3,277 requests: 27.5 GB per pass); with `pool_bytes` the pool is that
+    large."""
+    shape = KVShape(num_layers, 8, 128, 16, "bf16")
+    nb = int(pool_bytes // shape.block_bytes) if pool_bytes is not None else None
+    inp = block_copy_inputs(shape, num_reqs, nb, name="llama3_8b_block_copy")
+    inp.note = (f"bf16 {num_layers}x8x128, S=16, {num_reqs} req of 3 consecutive blocks (2 live, "
+                f"1 dead), sequential free list, {inp.num_blocks * shape.block_bytes / 2**30:.0f} "
+                f"GiB pool")
+    return inp
 
 
 CONFIGS: Dict[str, Callable[..., RepackInputs]] = {
