@@ -123,6 +123,16 @@ def test_llama3_8b_h2o_full_size():
     run_full(inp, seed=2, sample_planes=[0, 33, 63], clone=False)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "fp8_e4m3"])
+def test_llama3_70b_tensor_parallel_share_full_size(dtype):
+    # one GPU's share under 8-way tensor parallelism: one KV head, 256 B / 128 B rows; all 32
+    # requests fit the pool
+    budget = min(240 * 2 ** 30, int(0.85 * _budget()))
+    inp = W.llama3_70b_h2o(501, keep=0.3, dtype=dtype, num_kv_heads=1, pool_bytes=budget)
+    assert inp.num_reqs == 32
+    run_full(inp, seed=4, sample_planes=[0, 97, 159], clone=False)
+
+
 @pytest.mark.parametrize("dtype,keep", [("fp8_e4m3", 0.3), ("bf16", 0.3), ("fp8_e4m3", 0.1),
                                         ("fp8_e4m3", 0.6)])
 def test_llama3_70b_h2o_full_size(dtype, keep):
