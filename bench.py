@@ -16,9 +16,10 @@ their destinations and 1024 spare blocks, 56 GiB).
 Prints one JSON line. `value` is repacked KV GB/s over the whole step (read+write bytes of
 the live rows: 2 * live tokens * 2*L*H*D*elem_bytes); `roofline` prices the repack kernel
 alone against the 8 TB/s HBM peak, timed with HIP events on its launch stream (the build and
-free calls are timed separately); `ceiling` is the same kernel copying whole contiguous
-blocks of the same pool in the same run (the practical streaming rate) next to torch's
-device copy; `cpu_baseline` is the CPU oracle on a sample of the planes.
+free calls are timed separately); `ceiling` is torch's device copy timed in the same run
+and, with --ceiling all, the same repack kernel copying whole contiguous blocks of the same
+pool (the practical streaming rate); `cpu_baseline` is the CPU oracle on a sample of the
+planes.
 
     python bench.py [--steps K] [--warmup W] [--config NAME] [--variant V] [--grid G]
     python bench.py --mode copy      # plain device-to-device copy of known size
@@ -57,9 +58,11 @@ def parse_args(argv=None):
     ap.add_argument("--kv-heads", type=int, default=8,
                     help="70B config: KV heads in the cache (1 = one GPU's share under 8-way "
                          "tensor parallelism: 256 B / 128 B rows)")
-    ap.add_argument("--no-ceiling", action="store_true",
-                    help="skip the streaming-ceiling leg (whole contiguous blocks of the same "
-                         "pool through the same kernel, and a torch device copy)")
+    ap.add_argument("--ceiling", default="copy", choices=["none", "copy", "all"],
+                    help="practical-ceiling leg after the timed steps: copy = torch's device "
+                         "copy of 4 GiB (another kernel); all = also the repack kernel on "
+                         "whole contiguous blocks of the same pool (adds launches of the "
+                         "timed kernel, so a profile of the run would mix the two)")
     ap.add_argument("--variant", type=int, default=0)
     ap.add_argument("--grid", type=int, default=0)
     ap.add_argument("--order", type=int, default=0)
@@ -272,11 +275,38 @@ def inputs_sha256(inp) -> dict:
     return out
 
 
-def streaming_ceiling(args, inp, kv, cache, bytes_alg: int, stream, steps: int = 10):
-    """The copy's practical ceiling, timed in the same run on the same pool: the repack kernel
-    on whole contiguous blocks (block-copy metadata over the same KV tensor, about the same
-    bytes), and torch's device copy of 4 GiB when that much HBM is still free. Runs after the
-    timed steps (it overwrites blocks of the pool; the copy is value-agnostic)."""
+def streaming_ceiling(args, inp, kv, cache, bytes_alg: int, stream, block_copy: bool,
+                      steps: int = 10):
+    """The copy's practical ceiling, timed in the same run: torch's device copy of 4 GiB when
+    that much HBM is still free, and with `block_copy` the repack kernel on whole contiguous
+    blocks (block-copy metadata over the same KV tensor, about the same bytes). Runs after the
+    timed steps (the block copy overwrites blocks of the pool; the copy is value-agnostic)."""
+    import torch
+    out = {}
+    if block_copy:
+        out.update(block_copy_ceiling(inp, cache, bytes_alg, stream, steps))
+    free, _ = torch.cuda.mem_get_info()
+    n = 4 << 30
+    if free > 2 * n + (1 << 30):
+        src = torch.empty(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(3)
+        dst.copy_(src)
+        cev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(5)]
+        for a, b in cev:
+            a.record()
+            dst.copy_(src)
+            b.record()
+        torch.cuda.synchronize()
+        cms = sum(a.elapsed_time(b) for a, b in cev) / len(cev)
+        out["torch_copy_4GiB_GBps"] = round(2 * n / (cms / 1e3) / 1e9, 1)
+        del src, dst
+    log(f"ceiling: {out}")
+    return out
+
+
+def block_copy_ceiling(inp, cache, bytes_alg: int, stream, steps: int):
     import torch
     from paper_2608_13263_amd import binding as B
     from paper_2608_13263_amd import workloads as W
@@ -301,30 +331,9 @@ def streaming_ceiling(args, inp, kv, cache, bytes_alg: int, stream, steps: int =
     ms = sum(a.elapsed_time(b) for a, b in evs) / steps
     ref_bytes = 2 * R * 2 * sh.block_size * sh.token_bytes
     gbs = ref_bytes / (ms / 1e3) / 1e9
-    out = {"kind": "repack_direct_kernel on whole contiguous blocks of the same pool",
-           "bytes": ref_bytes, "ms": round(ms, 4), "GBps": round(gbs, 1),
-           "frac": round(gbs / HBM_PEAK_GBS, 4)}
-    del cb, cp
-    free, _ = torch.cuda.mem_get_info()
-    n = 4 << 30
-    if free > 2 * n + (1 << 30):
-        src = torch.empty(n, dtype=torch.uint8, device="cuda")
-        dst = torch.empty_like(src)
-        src.fill_(3)
-        dst.copy_(src)
-        cev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(5)]
-        for a, b in cev:
-            a.record()
-            dst.copy_(src)
-            b.record()
-        torch.cuda.synchronize()
-        cms = sum(a.elapsed_time(b) for a, b in cev) / len(cev)
-        out["torch_copy_4GiB_GBps"] = round(2 * n / (cms / 1e3) / 1e9, 1)
-        del src, dst
-    log(f"ceiling: block copy {gbs:.0f} GB/s, torch copy "
-        f"{out.get('torch_copy_4GiB_GBps', 'skipped')}")
-    return out
+    return {"block_copy": "repack_direct_kernel on whole contiguous blocks of the same pool",
+            "block_copy_bytes": ref_bytes, "block_copy_ms": round(ms, 4),
+            "block_copy_GBps": round(gbs, 1), "block_copy_frac": round(gbs / HBM_PEAK_GBS, 4)}
 
 
 def run_copy(args):
@@ -770,8 +779,9 @@ def main(argv=None):
         f"(min {min(repack_ms):.3f}), {achieved:.0f} GB/s repack")
 
     ceiling = None
-    if not args.no_ceiling:
-        ceiling = streaming_ceiling(args, inp, kv, cache, bytes_alg, stream)
+    if args.ceiling != "none":
+        ceiling = streaming_ceiling(args, inp, kv, cache, bytes_alg, stream,
+                                    block_copy=args.ceiling == "all")
 
     cpu = None
     if not args.no_cpu_baseline:
