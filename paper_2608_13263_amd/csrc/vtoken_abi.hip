@@ -483,6 +483,6 @@ const char* vtoken_status_string(int32_t status) {
   }
 }
 
-int32_t vtoken_version(void) { return 110; }
+int32_t vtoken_version(void) { return 111; }
 
 }  // extern "C"

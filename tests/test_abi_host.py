@@ -42,7 +42,7 @@ def test_status_codes_match_binding():
     for name, code in codes.items():
         assert B.status_string(code).startswith(name)
     assert B.status_string(12345) == "unknown vtoken status"
-    assert B.load_library().vtoken_version() == 110
+    assert B.load_library().vtoken_version() == 111
 
 
 def test_struct_layouts_match_header(tmp_path):
