@@ -336,7 +336,7 @@ void decode_split_kernel(AttnArgs a) {
   const uint8_t* vplane = kplane + a.plane_bytes;
   const int64_t head0 = (int64_t)h * kD * kElem;
   const int grp = lane >> 4;    // operand k-group / result row group
-  const int row = lane & 15;    // token of a tile (K operand) / head (Q, P operands)
+  const int row = lane & 15;    // token of a tile (K operand) / column (Q) / row (P)
   const int wt0 = wave * kTW;   // first token of this wave
 
   const bool low = row >= 8;          // this lane's column / P row holds low parts
@@ -416,7 +416,6 @@ void decode_split_kernel(AttnArgs a) {
     }
     sc[i] = acc;
   }
-
 
   // ---- V rows of k-step kc into this wave's LDS window
   uint8_t* vwin = lds + wave * kWin * kRowB;
