@@ -255,3 +255,38 @@ def test_pass_graph_replay(inplace):
         assert_plan_equal(plan_to_host(plan, cur), orc)
         assert_kv_equal(kv_bytes(kv, sh), orc.kv)
         assert orc.n_admitted > 0
+
+
+def _random_case(seed):
+    """A random small geometry, batch and pool: block sizes 1..128 (powers of two and not),
+    1-8 KV heads, head_dim 8..256, fp16 / bf16 / fp8 rows (multiples of 16 bytes), ragged
+    requests at random densities, free lists from empty (deferral) to ample."""
+    rng = np.random.default_rng(seed)
+    dtype = ["fp16", "bf16", "fp8_e4m3"][int(rng.integers(3))]
+    e = 1 if dtype == "fp8_e4m3" else 2
+    while True:
+        S = int(rng.choice([1, 2, 3, 4, 5, 7, 8, 16, 24, 32, 48, 64, 96, 128]))
+        H = int(rng.integers(1, 9))
+        D = int(rng.choice([8, 16, 24, 32, 64, 96, 128, 256]))
+        row = H * D * e
+        if row % 16 == 0 and S * row <= 64 * 1024:
+            break
+    R = int(rng.integers(1, 13))
+    masks = []
+    for _ in range(R):
+        n = int(rng.integers(0, 12 * S + 40))
+        masks.append((rng.random(n) < rng.random()).astype(int).tolist())
+    M = sum(-(-len(m) // S) for m in masks)
+    free = int(rng.integers(0, M + 8))
+    layers = int(rng.integers(1, 3))
+    inp = W.from_masks(masks, W.KVShape(layers, H, D, S, dtype), free_blocks=free, seed=seed,
+                       name=f"fuzz{seed}")
+    return inp
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_geometries(seed):
+    """Seeded random geometries and batches, out of place and in place, bit-exact."""
+    inp = _random_case(1000 + seed)
+    full_parity(inp, seed=seed)
+    full_parity(inp, seed=seed, inplace=True)
