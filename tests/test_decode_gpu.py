@@ -186,6 +186,42 @@ def test_paged_decode_parity(dtype, H, D, G, S):
     _label(f"paged decode {dtype} H={H} D={D} G={G}: max |diff| {worst:.2e}")
 
 
+@pytest.mark.parametrize("seed", range(24))
+def test_paged_decode_random_geometries(seed):
+    """Seeded random decode geometries: KV heads 1-8, head_dim 32-256, GQA groups 1-8, all
+    three dtypes, block sizes 1-64, 1-12 requests of random lengths and densities (splits of
+    every geometry with ragged tails), a softmax scale within 2x of 1/sqrt(head_dim)."""
+    t = torch()
+    B = _B()
+    rng = np.random.default_rng(5000 + seed)
+    dtype = ["fp16", "bf16", "fp8_e4m3"][int(rng.integers(3))]
+    H = int(rng.integers(1, 9))
+    D = int(rng.choice([32, 64, 128, 256]))
+    G = int(rng.choice([1, 2, 4, 8]))
+    S = int(rng.choice([1, 4, 16, 32, 64]))
+    R = int(rng.integers(1, 13))
+    masks = [(rng.random(int(rng.integers(0, 2600))) < rng.random()).astype(int).tolist()
+             for _ in range(R)]
+    M = sum(-(-len(m) // S) for m in masks)
+    inp = W.from_masks(masks, W.KVShape(2, H, D, S, dtype), free_blocks=M + 16, seed=seed,
+                       name=f"decode_fuzz{seed}")
+    sh = inp.shape
+    _label(f"decode fuzz {seed}: {dtype} H={H} D={D} G={G} S={S} R={R}")
+    kv = W.kv_device(sh, inp.num_blocks, seed)
+    orc = oracle_repack_inputs(inp, kv_bytes(kv, sh))
+    cache, _, _, indptr, slots = _device_pass(inp, kv)
+    ref_indptr, ref_slots = slot_mapping(orc.token_slot, inp.tok_indptr, inp.seq_lens)
+    vals = _values(orc.kv, sh)
+    scale = float(rng.uniform(0.5, 2.0)) / np.sqrt(D)     # around the usual 1/sqrt(D)
+    max_tokens = max(int(np.diff(ref_indptr).max()), 1)
+    q = rng.standard_normal((R, H * G, D)).astype(np.float32)
+    out = B.paged_decode(cache, t.from_numpy(q).cuda(), indptr, slots, 1, max_tokens,
+                         scale=scale)
+    got = out.cpu().numpy().astype(np.float64)
+    ref = decode_batch(q, vals[2], vals[3], ref_indptr, ref_slots, scale=scale)
+    np.testing.assert_allclose(got, ref, atol=ATOL, rtol=RTOL)
+
+
 @pytest.mark.parametrize("dtype,G", [("bf16", 4), ("fp8_e4m3", 8), ("fp16", 1)])
 def test_paged_decode_slot_outside_pool_gives_nan(dtype, G):
     """A slot outside the pool (past the end, or negative) is read nowhere: the requests that
