@@ -267,3 +267,43 @@ def test_partial_pass_graph_replay():
         assert_partial_equal(partial_to_host(plan, state, cur), o, cur)
         assert np.array_equal(kv_bytes(kv, sh), o.kv), f"KV bytes, replay {step}"
         assert o.n_admitted > 0
+
+
+def _random_partial_case(seed):
+    """Random geometry, token tables and planner parameters for the partial pass."""
+    B = _B()
+    rng = np.random.default_rng(seed)
+    dtype = ["fp16", "bf16", "fp8_e4m3"][int(rng.integers(3))]
+    e = 1 if dtype == "fp8_e4m3" else 2
+    while True:
+        S = int(rng.choice([1, 2, 3, 4, 8, 16, 24, 32, 64]))
+        H = int(rng.integers(1, 9))
+        D = int(rng.choice([16, 32, 64, 128]))
+        if (H * D * e) % 16 == 0:
+            break
+    R = int(rng.integers(1, 25))
+    lo = int(rng.integers(1, 600))
+    inp = W.token_table_inputs(
+        seed, W.KVShape(int(rng.integers(1, 3)), H, D, S, dtype), num_reqs=R,
+        len_range=(lo, lo + int(rng.integers(0, 1500))), keep=float(rng.uniform(0.05, 0.9)),
+        recent=int(rng.integers(0, 4 * S + 1)), shared_groups=int(rng.integers(0, 3)),
+        group_size=int(rng.integers(2, 4)), prefix_tokens=int(rng.integers(0, 8 * S + 1)),
+        shuffled_frac=float(rng.random()), dropped_frac=float(rng.random() * 0.5),
+        pin_tail=bool(rng.integers(2)),
+        free_blocks=int(rng.choice([0, 5, 40, 300, 3000])), name=f"partial_fuzz{seed}")
+    # mostly parameters under which a pass triggers and moves rows, sometimes the edges
+    theta = [(-1, 1), (-1, 1), (0, 1), (1, 4), (1, 2)][int(rng.integers(5))]
+    prm = B.PlannerParams(
+        theta=theta, max_live_per_source=int(rng.choice([-1, S, S, S // 2, 1, 0])),
+        max_sources=int(rng.choice([1 << 40, 1 << 40, 50, 7, 1, 0])),
+        min_eligible=int(rng.choice([0, 0, 1, 3])),
+        free_watermark=int(rng.choice([-1, -1, -1, 100000, 50, 0])))
+    return inp, prm
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_partial_random_cases(seed):
+    """Seeded random geometries (S 1-64 incl. non-powers of two), token tables (shuffled
+    layouts, dropped slots, shared prefixes, pins) and planner parameters, bit-exact."""
+    inp, prm = _random_partial_case(7000 + seed)
+    partial_parity(inp, prm, seed=seed, label=f"fuzz {seed}")
