@@ -600,9 +600,9 @@ constexpr int vmcnt_imm(int n) {
 // block's reads is only cheap when nothing after them is waited for too: the plan rows and
 // destination blocks of 32 blocks at a time are staged in LDS first (one drain per 32 blocks),
 // the blocks whose rows move are listed there, and the listed blocks are walked with exactly
-// kV reads and kV writes per thread each (rows already in place inside a moving block are
-// read and written back unchanged; units past the block go to a dropped buffer offset), so
-// every wait count is static.
+// kV reads and kV writes per thread each, so every wait count is static: a unit that does not
+// move (a row already in place inside a moving block, a padding row, past the block) reads
+// the plane's first 16 bytes (one cached line) and its store goes to a dropped buffer offset.
 // Hazards: the sources of destination block b lie at table positions >= b, so the reads of a
 // later listed block never touch the block being written; a block is written only after the
 // barrier that every thread reaches once its own reads of that block have returned, and the
@@ -663,27 +663,29 @@ __global__ __launch_bounds__(kCopyThreads) void repack_inplace_pipe_kernel(Inpla
   const int wave = tid >> 6;
   const uint8_t* pbase = a.kv + (int64_t)plane * a.plane_bytes;
 
-  // kV reads per thread of listed block lb (index within the chunk): the moving rows, and for
-  // the other units the unit itself (an in-place row, or unit 0 past the block)
-  auto load_block = [&](int lb, u32x4 (&regs)[kV]) {
-    const int dslot0 = dblk_s[lb] * S;
-    const int pv = plan_s[lb * S + (lane < S ? lane : S - 1)];
+  // kV reads per thread of listed block lb (index within the chunk, or -1 for none): the
+  // moving rows, and for the other units the plane's first 16 bytes; returns which of the kV
+  // units move
+  auto load_block = [&](int lb, u32x4 (&regs)[kV]) -> uint32_t {
+    const int dslot0 = lb >= 0 ? dblk_s[lb] * S : 0;
+    const int pv = lb >= 0 ? plan_s[lb * S + (lane < S ? lane : S - 1)] : -1;
+    uint32_t moving = 0;
 #pragma unroll
     for (int v = 0; v < kV; ++v) {
       const int u = v * kCopyThreads + tid;
       const int j = unit_rows ? u : static_cast<int>(__umulhi(static_cast<uint32_t>(u), magic));
       const int col = u - j * U;
       const int src = __shfl(pv, j & 63, 64);
-      const bool in = u < chunk;
-      const bool mv = in && static_cast<unsigned>(src) < static_cast<unsigned>(a.num_slots) &&
+      const bool mv = u < chunk &&
+                      static_cast<unsigned>(src) < static_cast<unsigned>(a.num_slots) &&
                       src != dslot0 + j;
-      const int64_t off = mv ? (int64_t)src * a.row_bytes + col * 16
-                             : (int64_t)dslot0 * a.row_bytes + (in ? (int64_t)u * 16 : 0);
-      const uint8_t* gsrc = pbase + off;
-      regs[v] = load16<true>(reinterpret_cast<const u32x4*>(gsrc));
+      const int64_t off = mv ? (int64_t)src * a.row_bytes + col * 16 : 0;
+      regs[v] = load16<true>(reinterpret_cast<const u32x4*>(pbase + off));
+      moving |= mv ? 1u << v : 0u;
     }
+    return moving;
   };
-  auto store_block = [&](int lb, const u32x4 (&regs)[kV]) {
+  auto store_block = [&](int lb, const u32x4 (&regs)[kV], uint32_t moving) {
     uint8_t* dptr = uniform_ptr(a.kv + (int64_t)plane * a.plane_bytes +
                                 (int64_t)dblk_s[lb] * S * a.row_bytes);
     const __amdgpu_buffer_rsrc_t rsrc =
@@ -691,7 +693,7 @@ __global__ __launch_bounds__(kCopyThreads) void repack_inplace_pipe_kernel(Inpla
 #pragma unroll
     for (int v = 0; v < kV; ++v) {
       const int u = v * kCopyThreads + tid;
-      const uint32_t off = u < chunk ? static_cast<uint32_t>(u) * 16u : kDropOffset;
+      const uint32_t off = (moving >> v) & 1u ? static_cast<uint32_t>(u) * 16u : kDropOffset;
       __builtin_amdgcn_raw_buffer_store_b128(regs[v], rsrc, off, 0, 16);
     }
   };
@@ -725,18 +727,21 @@ __global__ __launch_bounds__(kCopyThreads) void repack_inplace_pipe_kernel(Inpla
     const int nl = nlist_s;
     if (nl == 0) continue;
     u32x4 ra[kV], rb[kV];
-    load_block(list_s[0], ra);
+    uint32_t ma = load_block(list_s[0], ra), mb;
+    // vector-memory operations retire in order (stores included): after issuing the next
+    // block's kV reads, waiting until kV remain means this block's reads (and the previous
+    // block's stores) are done. Past the end of the list the "next" reads are of no block
+    // (-1: every unit reads the plane's first 16 bytes), so every wait count stays static.
     for (int i = 0; i < nl; i += 2) {
-      // past the end of the list the next reads repeat the last block (discarded)
-      load_block(list_s[i + 1 < nl ? i + 1 : nl - 1], rb);
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(kV));     // block i's reads, not block i+1's
+      mb = load_block(i + 1 < nl ? list_s[i + 1] : -1, rb);
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(kV));
       __syncthreads();
-      store_block(list_s[i], ra);
+      store_block(list_s[i], ra, ma);
       if (i + 1 < nl) {
-        load_block(list_s[i + 2 < nl ? i + 2 : nl - 1], ra);
+        ma = load_block(i + 2 < nl ? list_s[i + 2] : -1, ra);
         __builtin_amdgcn_s_waitcnt(vmcnt_imm(kV));
         __syncthreads();
-        store_block(list_s[i + 1], rb);
+        store_block(list_s[i + 1], rb, mb);
       }
     }
   }
