@@ -620,7 +620,7 @@ __global__ __launch_bounds__(kCopyThreads) void repack_inplace_pipe_kernel(Inpla
   __shared__ int list_s[kChunkBlocks];
   __shared__ int nlist_s;
   __shared__ int r_s;
-  if (a.counters[3] != 0) return;
+  if (a.counters[3] != 0 || a.counters[1] == 0) return;   // error, or nothing admitted
   const int P = a.num_planes;
   // longest chains first: workgroup k*P + plane takes the request with the k-th longest
   // chain (ties by index), so the last workgroups to start are short ones and the tail of the
