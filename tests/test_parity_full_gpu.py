@@ -232,7 +232,7 @@ def test_llama3_8b_scissorhands_partial_rounds():
     t.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("config", ["llama3_8b_h2o", "llama3_70b_bf16"])
+@pytest.mark.parametrize("config", ["llama3_8b_h2o", "llama3_70b_bf16", "llama3_70b_fp8"])
 def test_inplace_full_size(config):
     """In-place mode at full size in the launch configuration the benchmark times: every
     metadata output equals the oracle's in-place mode, sampled planes byte-exact against the
@@ -244,7 +244,8 @@ def test_inplace_full_size(config):
         sample = [0, 33, 63]
     else:
         budget = min(240 * 2 ** 30, int(0.85 * _budget()))
-        inp = W.llama3_70b_h2o(501, keep=0.3, dtype="bf16", pool_bytes=budget)
+        dtype = "bf16" if config == "llama3_70b_bf16" else "fp8_e4m3"
+        inp = W.llama3_70b_h2o(501, keep=0.3, dtype=dtype, pool_bytes=budget)
         sample = [0, 81, 159]
     shape = inp.shape
     print(f"[gpu] in-place full-size {inp.name}: pool {inp.pool_bytes() / 2**30:.1f} GiB",
@@ -267,14 +268,20 @@ def test_inplace_full_size(config):
     t.cuda.empty_cache()
 
 
-def test_decode_full_size_sampled():
-    """Decode over the full Llama-3-8B H2O cache after a pass, in the launch configuration the
-    decode benchmark times (every request, layers 0 and 31): eight sampled requests against
-    the float64 oracle computed one by one from their own K/V rows."""
+@pytest.mark.parametrize("config,G", [("llama3_8b_h2o", 4), ("llama3_70b_fp8", 8)])
+def test_decode_full_size_sampled(config, G):
+    """Decode over a full cache after a pass, in the launch configuration the decode benchmark
+    times (every request, the first and last layers): eight sampled requests against the
+    float64 oracle computed one by one from their own K/V rows. Llama-3-8B H2O with 32 query
+    heads, Llama-3-70B H2O fp8 with 64."""
     t = torch()
     from oracle.attention import dense_decode, slot_mapping
     from paper_2608_13263_amd import binding as B
-    inp = W.llama3_8b_h2o(301)
+    if config == "llama3_8b_h2o":
+        inp = W.llama3_8b_h2o(301)
+    else:
+        budget = min(240 * 2 ** 30, int(0.85 * _budget()))
+        inp = W.llama3_70b_h2o(501, keep=0.3, dtype="fp8_e4m3", pool_bytes=budget)
     shape = inp.shape
     S, H, D = shape.block_size, shape.num_kv_heads, shape.head_dim
     kv = W.kv_device(shape, inp.num_blocks, 8)
@@ -286,9 +293,10 @@ def test_decode_full_size_sampled():
     d_indptr = t.from_numpy(indptr.astype(np.int32)).cuda()
     d_slots = t.from_numpy(slots.astype(np.int32)).cuda()
     max_tokens = int(np.diff(indptr).max())
-    q = t.randn(inp.num_reqs, 4 * H, D, device="cuda", generator=t.Generator(device="cuda").manual_seed(3))
+    q = t.randn(inp.num_reqs, G * H, D, device="cuda",
+                generator=t.Generator(device="cuda").manual_seed(3))
     rng = np.random.default_rng(9)
-    sample = rng.choice(inp.num_reqs, size=8, replace=False)
+    sample = rng.choice(inp.num_reqs, size=min(8, inp.num_reqs), replace=False)
     worst = 0.0
     for layer in (0, shape.num_layers - 1):
         out = B.paged_decode(cache, q, d_indptr, d_slots, layer, max_tokens).cpu().numpy()
@@ -301,8 +309,8 @@ def test_decode_full_size_sampled():
             ref = dense_decode(q[r].cpu().numpy().astype(np.float64), k, v)
             np.testing.assert_allclose(out[r], ref, atol=1e-4, rtol=1e-4)
             worst = max(worst, float(np.abs(out[r] - ref).max()))
-    print(f"[gpu] decode full-size: 8 sampled requests x 2 layers, max |diff| {worst:.2e}",
-          flush=True)
+    print(f"[gpu] decode full-size {inp.name}: {len(sample)} sampled requests x 2 layers, "
+          f"max |diff| {worst:.2e}", flush=True)
     del kv
     gc.collect()
     t.cuda.empty_cache()
