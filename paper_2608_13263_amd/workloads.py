@@ -38,6 +38,7 @@ __all__ = [
     "bernoulli_live",
     "random_live",
     "h2o_live",
+    "slot_limit_inputs",
 ]
 
 
@@ -689,6 +690,40 @@ def llama3_8b_block_copy(num_reqs: int = 3277, num_layers: int = 32,
                 f"1 dead), sequential free list, {inp.num_blocks * shape.block_bytes / 2**30:.0f} "
                 f"GiB pool")
     return inp
+
+
+SLOT_LIMIT = 2 ** 31 - 1   # slots are int32 on the device: num_blocks * S <= 2^31 - 1
+
+
+def slot_limit_inputs(shape: KVShape, masks: Sequence[Sequence[int]], seed: int,
+                      top_block: str = "source", spare: int = 1024,
+                      name: str = "slot_limit") -> RepackInputs:
+    """The largest pool a cache of block size S can have: num_blocks = (2^31 - 1) // S, so
+    slot indices come within S of 2^31. The requests' tables and `spare` free blocks are a
+    seeded permutation of the top blocks of the pool; the pool's last block is moved to the
+    head of the first request's table (top_block="source") or of the free list
+    ("destination")."""
+    if top_block not in ("source", "destination"):
+        raise ValueError("top_block is 'source' or 'destination'")
+    S = shape.block_size
+    num_blocks = SLOT_LIMIT // S
+    rng = np.random.Generator(np.random.PCG64(seed))
+    masks = [np.asarray(m, dtype=np.uint8) for m in masks]
+    seq_lens = np.array([len(m) for m in masks], dtype=np.int64)
+    M = int(sum(_blocks_for(n, S) for n in seq_lens))
+    ids = (num_blocks - (M + spare) + rng.permutation(M + spare)).astype(np.int64)
+    i = int(np.nonzero(ids == num_blocks - 1)[0][0])
+    j = 0 if top_block == "source" else M
+    ids[[i, j]] = ids[[j, i]]
+    tok_indptr = np.concatenate([[0], np.cumsum(seq_lens)])
+    bt_indptr = np.concatenate([[0], np.cumsum([_blocks_for(n, S) for n in seq_lens])])
+    live = np.concatenate(masks) if len(masks) else np.zeros(0, dtype=np.uint8)
+    return RepackInputs(
+        name=name, shape=shape, num_blocks=num_blocks, seq_lens=seq_lens.astype(np.int32),
+        tok_indptr=tok_indptr.astype(np.int32), bt_indptr=bt_indptr.astype(np.int32),
+        block_ids=ids[:M].astype(np.int32), live=live, free_list=ids[M:].astype(np.int32),
+        seed=seed, note=f"{num_blocks} blocks of {S} slots, tables and free list at the top, "
+                        f"last block as {top_block}")
 
 
 CONFIGS: Dict[str, Callable[..., RepackInputs]] = {

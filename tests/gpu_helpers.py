@@ -103,6 +103,26 @@ def full_parity(inp: W.RepackInputs, seed: int = 0, variant=0, grid=0, order=0,
     return gpu, orc
 
 
+def oracle_moves(orc, inp, inplace=False):
+    """(source slot, destination slot) of every row the oracle moves; the plan's destination
+    block g is free_list[g] out of place, the request's own k-th block in place."""
+    S = inp.shape.block_size
+    sp = np.asarray(orc.src_plan, dtype=np.int64).reshape(orc.used, S)
+    g, j = np.nonzero(sp >= 0)
+    src = sp[g, j]
+    if inplace:
+        dest = np.empty(orc.used, dtype=np.int64)
+        for r in np.nonzero(np.asarray(orc.admitted))[0]:
+            a, b = int(orc.dst_indptr[r]), int(orc.dst_indptr[r + 1])
+            n0 = int(orc.new_bt_indptr[r])
+            dest[a:b] = orc.new_block_ids[n0:n0 + (b - a)]
+    else:
+        dest = np.asarray(inp.free_list, dtype=np.int64)
+    dst = dest[g] * S + j
+    keep = src != dst                       # rows already in place are not moves
+    return src[keep], dst[keep]
+
+
 def gpu_partial(inp, kv, params=None, label=""):
     """plan_partial -> repack on the current stream; host copies of every output, trimmed
     to the sizes the counters report."""

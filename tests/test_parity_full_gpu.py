@@ -14,31 +14,11 @@ import numpy as np
 import pytest
 
 from gpu_helpers import (assert_kv_equal, assert_partial_equal, assert_plan_equal, gpu_partial,
-                         gpu_pass, run_partial_oracle, torch)
+                         gpu_pass, oracle_moves, run_partial_oracle, torch)
 from oracle.repack import oracle_repack_inputs
 from paper_2608_13263_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
-
-
-def _moves(orc, inp, inplace=False):
-    """(source slot, destination slot) of every row the oracle moves; the plan's destination
-    block g is free_list[g] out of place, the request's own k-th block in place."""
-    S = inp.shape.block_size
-    sp = np.asarray(orc.src_plan, dtype=np.int64).reshape(orc.used, S)
-    g, j = np.nonzero(sp >= 0)
-    src = sp[g, j]
-    if inplace:
-        dest = np.empty(orc.used, dtype=np.int64)
-        for r in np.nonzero(np.asarray(orc.admitted))[0]:
-            a, b = int(orc.dst_indptr[r]), int(orc.dst_indptr[r + 1])
-            n0 = int(orc.new_bt_indptr[r])
-            dest[a:b] = orc.new_block_ids[n0:n0 + (b - a)]
-    else:
-        dest = np.asarray(inp.free_list, dtype=np.int64)
-    dst = dest[g] * S + j
-    keep = src != dst                       # rows already in place are not moves
-    return src[keep], dst[keep]
 
 
 def _plane_bytes(kv, p, shape):
@@ -85,7 +65,7 @@ def run_full(inp, seed, sample_planes, clone=True):
 def _check_all_planes(kv, before, clone, orc_meta, inp, inplace=False):
     t = torch()
     shape = inp.shape
-    src, dst = _moves(orc_meta, inp, inplace)
+    src, dst = oracle_moves(orc_meta, inp, inplace)
     src_t = t.from_numpy(src).cuda()
     dst_t = t.from_numpy(dst).cuda()
     for p in range(shape.num_planes):
@@ -260,7 +240,7 @@ def test_inplace_full_size(config):
     post = np.stack([_plane_bytes(kv, p, shape).cpu().numpy() for p in sample])
     assert_kv_equal(post, orc.kv)
     _check_all_planes(kv, before, False, orc_meta, inp, inplace=True)
-    src, _ = _moves(orc_meta, inp, True)
+    src, _ = oracle_moves(orc_meta, inp, True)
     print(f"[gpu] in-place full-size {inp.name}: {orc_meta.n_admitted} requests, {len(src)} rows "
           f"moved per plane", flush=True)
     del kv, before

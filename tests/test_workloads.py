@@ -91,3 +91,19 @@ def test_oracle_invariants_on_workload_shapes(maker, kw):
                      inp.free_list, inp.shape.block_size, inp.num_blocks, res.token_slot,
                      res.new_bt_indptr, res.new_block_ids, res.freed, res.used, kv, res.kv)
     assert res.n_admitted > 0
+
+
+@pytest.mark.parametrize("S,top", [(16, "source"), (16, "destination"), (1, "source"),
+                                   (64, "destination")])
+def test_slot_limit_inputs(S, top):
+    masks = [np.ones(40, np.uint8), np.zeros(0, np.uint8), (np.arange(300) % 3 == 0)]
+    inp = W.slot_limit_inputs(W.KVShape(1, 1, 16, S, "fp8_e4m3"), masks, seed=5, top_block=top)
+    nb = inp.num_blocks
+    assert nb * S <= 2 ** 31 - 1 < (nb + 1) * S
+    ids = np.concatenate([inp.block_ids, inp.free_list]).astype(np.int64)
+    assert len(np.unique(ids)) == len(ids) and ids.min() >= nb - len(ids) and ids.max() == nb - 1
+    assert list(np.diff(inp.bt_indptr)) == [-(-len(m) // S) for m in masks]
+    assert list(inp.seq_lens) == [len(m) for m in masks] and len(inp.free_list) == 1024
+    assert (inp.block_ids[0] if top == "source" else inp.free_list[0]) == nb - 1
+    with pytest.raises(ValueError):
+        W.slot_limit_inputs(inp.shape, masks, seed=5, top_block="middle")
