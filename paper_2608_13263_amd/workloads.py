@@ -692,6 +692,27 @@ def llama3_8b_block_copy(num_reqs: int = 3277, num_layers: int = 32,
     return inp
 
 
+def llama3_8b_shared_prefix(seed: int = 701, num_reqs: int = 64, num_layers: int = 32,
+                            groups: int = 16, group_size: int = 4, prefix_tokens: int = 1024,
+                            pool_bytes: Optional[int] = None) -> RepackInputs:
+    """Prefix caching (Sec. 5.7) in the Llama-3-8B geometry: 64 requests of U[2048, 8192]
+    tokens as token tables, 16 groups of 4 sharing their first 1024 tokens (one set of
+    blocks per group, at the front of every member's table), Random keep 0.3 + last 64 drawn
+    per request, append blocks pinned. With `pool_bytes` the free list fills a pool that
+    large (the same request lengths; placement and liveness are drawn over that pool)."""
+    shape = KVShape(num_layers, 8, 128, 16, "bf16")
+    kw = dict(seed=seed, shape=shape, num_reqs=num_reqs, len_range=(2048, 8192), keep=0.3,
+              recent=64, shared_groups=groups, group_size=group_size,
+              prefix_tokens=prefix_tokens, name="llama3_8b_shared_prefix")
+    inp = token_table_inputs(**kw)
+    if pool_bytes is not None:
+        held = inp.num_blocks - len(inp.free_list)
+        free = max(int(pool_bytes // shape.block_bytes) - held, len(inp.free_list))
+        inp = token_table_inputs(free_blocks=free, **kw)
+    inp.note += f", {inp.num_blocks * shape.block_bytes / 2**30:.0f} GiB pool"
+    return inp
+
+
 SLOT_LIMIT = 2 ** 31 - 1   # slots are int32 on the device: num_blocks * S <= 2^31 - 1
 
 
@@ -732,6 +753,7 @@ CONFIGS: Dict[str, Callable[..., RepackInputs]] = {
     "llama3_8b_h2o": llama3_8b_h2o,
     "llama3_70b_h2o": llama3_70b_h2o,
     "llama3_8b_block_copy": llama3_8b_block_copy,
+    "llama3_8b_shared_prefix": llama3_8b_shared_prefix,
 }
 
 
