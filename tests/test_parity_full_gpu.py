@@ -212,6 +212,37 @@ def test_llama3_8b_scissorhands_partial_rounds():
     t.cuda.empty_cache()
 
 
+def test_llama3_8b_shared_prefix_full_size():
+    """The prefix-caching workload the benchmark times (64 requests, 16 groups of 4 sharing
+    1024 tokens, 258 GiB pool), one partial pass: every output against the partial-pass
+    oracle, the shared blocks neither sources nor touched, sampled planes byte-exact against
+    the oracle run on their pre-call bytes, every plane by row checksums of the moves."""
+    t = torch()
+    from paper_2608_13263_amd import binding as B
+    inp = W.llama3_8b_shared_prefix(701, pool_bytes=int(0.9 * _budget()))
+    shape = inp.shape
+    sample = [0, 31, 63]
+    print(f"[gpu] full-size {inp.name}: pool {inp.pool_bytes() / 2**30:.1f} GiB", flush=True)
+    params = B.PlannerParams()
+    orc_meta = run_partial_oracle(inp, None, params)
+    shared = {b for b, n in orc_meta.refs.items() if n > 1}
+    assert len(shared) == 16 * 64 and not shared & set(int(b) for b in orc_meta.freed)
+    kv = W.kv_device(shape, inp.num_blocks, 9)
+    pre = np.stack([_plane_bytes(kv, p, shape).cpu().numpy() for p in sample])
+    before = t.stack([_row_sums(kv, p, shape) for p in range(shape.num_planes)])
+    gpu = gpu_partial(inp, kv, params, label=f"full-size {inp.name}")
+    assert_partial_equal(gpu, orc_meta, inp)
+    orc = run_partial_oracle(inp, pre, params)
+    post = np.stack([_plane_bytes(kv, p, shape).cpu().numpy() for p in sample])
+    assert_kv_equal(post, orc.kv)
+    _check_all_planes(kv, before, False, orc_meta, inp)
+    print(f"[gpu] full-size {inp.name}: {orc_meta.tokens_moved} tokens moved, "
+          f"{len(shared)} shared blocks kept", flush=True)
+    del kv, before
+    gc.collect()
+    t.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("config", ["llama3_8b_h2o", "llama3_70b_bf16", "llama3_70b_fp8"])
 def test_inplace_full_size(config):
     """In-place mode at full size in the launch configuration the benchmark times: every
