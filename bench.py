@@ -81,11 +81,14 @@ def parse_args(argv=None):
     ap.add_argument("--inplace", action="store_true",
                     help="in-place mode: destinations are each request's own leading blocks; "
                          "bytes count only the rows that move")
-    ap.add_argument("--mode", default="repack", choices=["repack", "copy", "decode", "overlap"],
+    ap.add_argument("--mode", default="repack",
+                    choices=["repack", "copy", "decode", "overlap", "stream"],
                     help="decode: the consumer side, paged decode attention of every layer "
                          "through the slot mapping, before and after the repack; overlap: a "
                          "decode step (every layer) on the main stream with the repack pass on "
-                         "a relocation stream, against the two one after the other")
+                         "a relocation stream, against the two one after the other; stream: "
+                         "read / write / copy and decode-pattern probes, the memory system's "
+                         "streaming ceilings")
     ap.add_argument("--q-heads", type=int, default=32, help="decode mode: query heads")
     ap.add_argument("--copy-gib", type=float, default=8.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -369,6 +372,87 @@ def run_copy(args):
     print(json.dumps({"mode": "copy", "bytes_each_way": n, "ms": round(ms, 4),
                       "GBps_read_plus_write": round(gbs, 1),
                       "frac_of_8TBps": round(gbs / HBM_PEAK_GBS, 4)}), flush=True)
+
+
+def run_stream(args):
+    """Streaming rates of the memory system (libvtoken_probe.so) in one pool sized as the
+    repack benchmark's (90% of free HBM by default): reads, writes and copies of 32 KiB chunks
+    and the decode's pattern (256-byte head pieces of 2 KiB token rows through a slot list of
+    shuffled 16-token blocks, K and V planes). These are the ceilings the repack and the
+    decode are set against; HIP events on the launch stream."""
+    import ctypes
+    import torch
+    from paper_2608_13263_amd.build import PROBE_LIB_PATH
+    if not os.path.exists(PROBE_LIB_PATH):
+        raise SystemExit(f"{PROBE_LIB_PATH} is missing: build with "
+                         "`python -m paper_2608_13263_amd.build`")
+    lib = ctypes.CDLL(PROBE_LIB_PATH)
+    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    lib.vtoken_probe_read.argtypes = [vp, i64, i32, vp, vp]
+    lib.vtoken_probe_write.argtypes = [vp, i64, i32, vp]
+    lib.vtoken_probe_copy.argtypes = [vp, vp, i64, i32, vp]
+    lib.vtoken_probe_head_read.argtypes = [vp, i64, i32, vp, i64, i32, vp, vp]
+    free, _ = torch.cuda.mem_get_info()
+    chunk = 32768
+    pool = int((args.pool_frac if args.pool_frac > 0 else 0.5) * free)
+    # two regions (source at 0, destination at half the pool) of up to 64 GiB, whole multiples
+    # of 1024 chunks so that every interleave below divides the chunk count
+    region = min(64 * 2 ** 30, pool // 4) // (1024 * chunk) * (1024 * chunk)
+    buf = torch.zeros(pool // chunk * chunk, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    sh = ctypes.c_void_p(stream.cuda_stream)
+    src = buf.data_ptr()
+    dst = buf.data_ptr() + (buf.numel() // 2) // chunk * chunk
+    log(f"stream probes: pool {buf.numel() / 2**30:.1f} GiB, regions of "
+        f"{region / 2**30:.1f} GiB")
+
+    def timed(call, nbytes):
+        code = call()
+        if code != 0:
+            raise SystemExit(f"probe call failed with {code}")
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(max(args.steps // 4, 3))]
+        for a, b in evs:
+            a.record(stream)
+            call()
+            b.record(stream)
+        torch.cuda.synchronize()
+        ms = sum(a.elapsed_time(b) for a, b in evs) / len(evs)
+        return round(nbytes / (ms / 1e3) / 1e9, 1)
+
+    rates = {}
+    for nt in (1, 0):
+        rates[f"read_{'nt' if nt else 'plain'}"] = timed(
+            lambda: lib.vtoken_probe_read(src, region, nt, sink.data_ptr(), sh), region)
+    for ways in (1, 64):
+        rates[f"write_ways{ways}"] = timed(
+            lambda: lib.vtoken_probe_write(dst, region, ways, sh), region)
+        rates[f"copy_ways{ways}"] = timed(
+            lambda: lib.vtoken_probe_copy(src, dst, region, ways, sh), 2 * region)
+    # decode pattern over the source region as a K plane and a V plane of 2 KiB rows
+    plane = region // 2
+    rows = plane // 2048
+    tokens = rows // 64 * 64
+    g = torch.Generator().manual_seed(5)
+    blocks = torch.randperm(rows // 16, generator=g)
+    slots = (blocks.repeat_interleave(16) * 16 + torch.arange(16).repeat(rows // 16))
+    slots = slots[:tokens].to(torch.int32).cuda()
+    for nt in (1, 0):
+        rates[f"head_pieces_{'nt' if nt else 'plain'}"] = timed(
+            lambda: lib.vtoken_probe_head_read(src, plane, 2048, slots.data_ptr(), tokens, nt,
+                                               sink.data_ptr(), sh), 2 * tokens * 256 * 8)
+    best_copy = max(rates["copy_ways1"], rates["copy_ways64"])
+    out = {"metric": "streaming rates of the memory system (probe kernels)", "mode": "stream",
+           "value": best_copy, "unit": "GB/s", "n_gpus": 1, "higher_is_better": True,
+           "data": "synthetic", "rates_GBps": rates,
+           "frac_of_8TBps": {k: round(v / HBM_PEAK_GBS, 4) for k, v in rates.items()},
+           "config": {"workload": "stream_probes", "pool_gib": round(buf.numel() / 2 ** 30, 1),
+                      "region_gib": round(region / 2 ** 30, 2), "chunk_bytes": chunk,
+                      "decode_pattern": f"{tokens} tokens x 8 heads x 256 B, K and V planes"}}
+    print(json.dumps(out), flush=True)
+    return 0
 
 
 def run_scissorhands(args):
@@ -923,6 +1007,8 @@ def main(argv=None):
         raise SystemExit("bench.py needs a GPU (MI355X, gfx950)")
     if args.mode == "copy":
         return run_copy(args)
+    if args.mode == "stream":
+        return run_stream(args)
     if args.config == "llama3_8b_scissorhands":
         return run_partial_stream(args) if args.partial else run_scissorhands(args)
     if args.config == "llama3_8b_shared_prefix":

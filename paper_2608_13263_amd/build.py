@@ -1,9 +1,10 @@
-"""Build libvtoken.so (the HIP kernels and the C ABI of include/vtoken.h) for gfx950.
+"""Build libvtoken.so (the HIP kernels and the C ABI of include/vtoken.h) and
+libvtoken_probe.so (the memory-system streaming probes of `bench.py --mode stream`) for gfx950.
 
     python -m paper_2608_13263_amd.build
 
-Compiles in-tree with hipcc; the library lands next to this file, where the binding loads
-it. Packed-FP32 instructions are disabled for all device code.
+Compiles in-tree with hipcc; the libraries land next to this file, where the binding and the
+benchmark load them. Packed-FP32 instructions are disabled for all device code.
 """
 from __future__ import annotations
 
@@ -20,6 +21,8 @@ SOURCES = [os.path.join(HERE, "csrc", f)
                      "vtoken_planner.hip")]
 HEADERS = [os.path.join(ROOT, "include", "vtoken.h"),
            os.path.join(HERE, "csrc", "vtoken_internal.h")]
+PROBE_LIB_PATH = os.path.join(HERE, "libvtoken_probe.so")
+PROBE_SOURCES = [os.path.join(HERE, "csrc", "vtoken_stream_probe.hip")]
 ARCH = "gfx950"
 
 
@@ -30,18 +33,24 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found; install ROCm or set HIPCC")
 
 
-def command(out_path: str):
+def command(out_path: str, sources=None):
     return [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
             "-Wall", "-Wno-unused-function",
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
             "-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc"),
-            *SOURCES, "-o", out_path]
+            *(sources or SOURCES), "-o", out_path]
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every source (always, even if a library exists) and install it atomically."""
-    tmp = LIB_PATH + ".tmp"
-    cmd = command(tmp)
+    """Compile both libraries (always, even if they exist); returns libvtoken.so's path."""
+    build_one(PROBE_LIB_PATH, PROBE_SOURCES, verbose)
+    return build_one(LIB_PATH, SOURCES, verbose)
+
+
+def build_one(lib_path: str, sources, verbose: bool = False) -> str:
+    """Compile `sources` into `lib_path`, installed atomically."""
+    tmp = lib_path + ".tmp"
+    cmd = command(tmp, sources)
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -53,8 +62,8 @@ def build(verbose: bool = False) -> str:
         lines = [ln for ln in res.stderr.splitlines() if "packed-fp32-ops" not in ln]
         if any(ln.strip() for ln in lines):
             sys.stderr.write("\n".join(lines) + "\n")
-    os.replace(tmp, LIB_PATH)
-    return LIB_PATH
+    os.replace(tmp, lib_path)
+    return lib_path
 
 
 if __name__ == "__main__":

@@ -279,3 +279,28 @@ def test_no_undefined_library_symbols():
                          capture_output=True, text=True).stdout
     bad = [ln for ln in out.splitlines() if "vtoken" in ln]
     assert not bad, bad
+
+
+def test_stream_probe_library_rejects_bad_sizes():
+    """The memory-system probes of `bench.py --mode stream` (a separate library): every entry
+    point is exported and refuses null pointers and sizes its kernels do not cover before any
+    launch (no device needed)."""
+    import ctypes
+    from paper_2608_13263_amd.build import PROBE_LIB_PATH
+    lib = ctypes.CDLL(PROBE_LIB_PATH)
+    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    lib.vtoken_probe_read.argtypes = [vp, i64, i32, vp, vp]
+    lib.vtoken_probe_write.argtypes = [vp, i64, i32, vp]
+    lib.vtoken_probe_copy.argtypes = [vp, vp, i64, i32, vp]
+    lib.vtoken_probe_head_read.argtypes = [vp, i64, i32, vp, i64, i32, vp, vp]
+    fake = 1 << 40          # never dereferenced: every call below fails its host checks
+    chunk = 32768
+    assert lib.vtoken_probe_read(None, chunk, 1, fake, None) == -2
+    assert lib.vtoken_probe_read(fake, chunk + 16, 1, fake, None) == -2
+    assert lib.vtoken_probe_read(fake, chunk * (1 << 24) + chunk, 1, fake, None) == -2
+    assert lib.vtoken_probe_write(fake, 3 * chunk, 2, None) == -2        # ways must divide
+    assert lib.vtoken_probe_write(fake, 4 * chunk, 0, None) == -2
+    assert lib.vtoken_probe_copy(fake, None, 4 * chunk, 1, None) == -2
+    assert lib.vtoken_probe_head_read(fake, 1 << 20, 2000, fake, 64, 1, fake, None) == -2
+    assert lib.vtoken_probe_head_read(fake, 1 << 20, 2048, fake, 100, 1, fake, None) == -2
+    assert lib.vtoken_probe_head_read(fake, 1024, 2048, fake, 64, 1, fake, None) == -2
