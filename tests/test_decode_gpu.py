@@ -280,6 +280,39 @@ def test_paged_decode_max_tokens_too_small(dtype, G):
     assert np.isnan(got[~fits]).all()
 
 
+@pytest.mark.parametrize("dtype,G,S", [("bf16", 4, 16), ("fp8_e4m3", 8, 32)])
+def test_paged_decode_long_request(dtype, G, S):
+    """One request of ~1M live tokens among short ones (a 1.5M-token context, keep 0.7):
+    8,200 splits per head for bf16 (4,100 for fp8) merged by the combine kernel, after a
+    repack pass, against the float64 oracle."""
+    t = torch()
+    B = _B()
+    H, D = 1, 128
+    rng = np.random.default_rng(1500 + G)
+    masks = [(rng.random(1_500_000) < 0.7).astype(np.uint8), [1] * 5, [0] * 10,
+             (rng.random(3000) < 0.5).astype(np.uint8)]
+    M = sum(-(-len(m) // S) for m in masks)
+    inp = W.from_masks(masks, W.KVShape(1, H, D, S, dtype), free_blocks=M + 16, seed=G,
+                       name="decode_long")
+    sh = inp.shape
+    _label(f"decode long request {dtype} G={G}: {int(inp.live.sum())} live tokens")
+    kv = W.kv_device(sh, inp.num_blocks, 11)
+    orc = oracle_repack_inputs(inp, kv_bytes(kv, sh))
+    cache, _, _, indptr, slots = _device_pass(inp, kv)
+    ref_indptr, ref_slots = slot_mapping(orc.token_slot, inp.tok_indptr, inp.seq_lens)
+    counts = np.diff(ref_indptr)
+    assert counts[0] > 1_000_000
+    vals = _values(orc.kv, sh)
+    q = rng.standard_normal((inp.num_reqs, H * G, D)).astype(np.float32)
+    out = B.paged_decode(cache, t.from_numpy(q).cuda(), indptr, slots, 0, int(counts.max()))
+    got = out.cpu().numpy().astype(np.float64)
+    ref = decode_batch(q, vals[0], vals[1], ref_indptr, ref_slots)
+    np.testing.assert_allclose(got, ref, atol=ATOL, rtol=RTOL)
+    assert np.array_equal(got[2], np.zeros_like(got[2])), "no live tokens -> zeros"
+    del kv, vals
+    t.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("dtype", ["fp8_e4m3", "fp16", "bf16"])
 def test_decode_one_key_returns_value_codes_exactly(dtype):
     """Requests of one live token with a zero key: softmax weight exactly 1, so the output is
