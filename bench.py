@@ -55,6 +55,9 @@ def parse_args(argv=None):
                          "(a reference, not a paper workload); llama3_8b_shared_prefix: "
                          "prefix caching, timed as the partial pass")
     ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--block-size", type=int, default=16,
+                    help="llama3_8b_random: tokens per block (the paper's sensitivity study "
+                         "uses 16, 32 and 48)")
     ap.add_argument("--keep", type=float, default=0.3, help="keep ratio (70B config)")
     ap.add_argument("--kv-dtype", default="fp8_e4m3", help="70B config: fp8_e4m3 or bf16")
     ap.add_argument("--kv-heads", type=int, default=8,
@@ -109,7 +112,8 @@ def make_workload(args):
             import torch
             free, _ = torch.cuda.mem_get_info()
             pool = int(args.pool_frac * free)
-        return W.llama3_8b_random(args.seed if args.seed is not None else 201, pool_bytes=pool)
+        return W.llama3_8b_random(args.seed if args.seed is not None else 201, pool_bytes=pool,
+                                  block_size=args.block_size)
     if args.config == "llama3_8b_h2o":
         return W.llama3_8b_h2o(args.seed if args.seed is not None else 301)
     if args.config == "tiny":
@@ -132,16 +136,18 @@ def make_workload(args):
                             dtype=args.kv_dtype, num_kv_heads=args.kv_heads, pool_bytes=budget)
 
 
-def recorded_traffic(config: str):
-    """HBM bytes per repack launch from the committed rocprofv3 --pmc summary, if it was
-    taken on the current kernel source; None otherwise."""
-    path = os.path.join(PROFILES, f"repack_{config}_traffic.md")
+def recorded_traffic(workload: str, bytes_alg: int):
+    """HBM bytes per repack launch from the committed rocprofv3 --pmc summary of this
+    workload, if it was taken on the current kernel source and on the same algorithmic bytes
+    (the same requests, liveness and layout); None otherwise."""
+    path = os.path.join(PROFILES, f"repack_{workload}_traffic.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
     m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
     m_bytes = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    if not m_sha or not m_bytes:
+    m_alg = re.search(r"algorithmic_bytes_per_launch:\s*([0-9]+)", text)
+    if not m_sha or not m_bytes or not m_alg or int(m_alg.group(1)) != int(bytes_alg):
         return None
     sha = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
     return float(m_bytes.group(1)) if sha == m_sha.group(1) else None
@@ -1075,7 +1081,7 @@ def main(argv=None):
     bytes_alg = 2 * moved_tokens * sh.token_bytes
     value = bytes_alg / (ms_per_step / 1e3) / 1e9
     achieved = bytes_alg / (repack_avg / 1e3) / 1e9
-    traffic = recorded_traffic(args.config)
+    traffic = recorded_traffic(inp.name, bytes_alg)
     log(f"step {ms_per_step:.3f} ms, repack {repack_avg:.3f} ms "
         f"(min {min(repack_ms):.3f}), {achieved:.0f} GB/s repack")
 

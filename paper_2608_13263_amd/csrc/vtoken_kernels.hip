@@ -278,21 +278,24 @@ __global__ __launch_bounds__(kFreeThreads) void free_kernel(MetaArgs a, int32_t*
 }
 
 // ------------------------------------------------------------------------------------------
-// Step 2: the gather-repack. A work item is (destination block g, plane): it gathers up to
-// S rows, each from the source slot src_plan[g*S + j], and writes them as one contiguous
-// chunk of S*row_bytes bytes at block free_list[g] of the same plane. A thread moves
-// 16-byte units; kV units per thread are loaded before any is stored, so every wave keeps
-// kV*1 KiB of reads in flight. Rows are head_dim-contiguous, so a wave's 64 lanes read and
-// write 1 KiB of consecutive bytes per instruction (a whole 2 KiB row takes two).
+// Step 2: the gather-repack. Destination block g of a plane is one contiguous chunk of
+// S*row_bytes bytes at block free_list[g], whose row j comes from the source slot
+// src_plan[g*S + j]. A work item is (part of destination block g, plane), a part being one
+// round of kCopyThreads*kV 16-byte units (32 KiB at kV = 8): every workgroup moves one round
+// whatever the block size, and a chunk of several rounds (S = 32 or 48 at 2 KiB rows) is
+// spread over several workgroups. A thread loads its kV units before storing any, so every
+// wave keeps kV*1 KiB of reads in flight. Rows are head_dim-contiguous, so a wave's 64 lanes
+// read and write 1 KiB of consecutive bytes per instruction (a whole 2 KiB row takes two).
 //
 // Source slots of one destination block: with S <= 64, lane j of every wave holds
 // src_plan[g*S + j] and rows are picked with a cross-lane shuffle; otherwise each unit reads
 // its entry from memory. The copy is branch-free so the compiler can keep every load of a
 // round in flight (a conditional load or store would force a full wait on the vector
 // memory counter): lanes of padding rows (src_plan -1, the tail of a request's last block)
-// load row 0 of the same destination block, which is always live and already being read,
-// and their stores go through a buffer resource spanning only the destination chunk with
-// an out-of-range offset, which the hardware drops.
+// load the part's first row, which the workgroup reads anyway, and their stores go through a
+// buffer resource spanning only the destination chunk with an out-of-range offset, which the
+// hardware drops. Padding rows are a suffix of the block, so a part whose first row is
+// padding is all padding and is skipped.
 // ------------------------------------------------------------------------------------------
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -333,17 +336,21 @@ __device__ __forceinline__ uint8_t* uniform_ptr(uint8_t* p) {
   return reinterpret_cast<uint8_t*>((static_cast<uint64_t>(hi) << 32) | lo);
 }
 
-template <int kPolicy, bool kSmallS, bool kOneRound, int kV>
+template <int kPolicy, bool kSmallS, int kV>
 __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a) {
   constexpr Policy pol = kPolicies[kPolicy];
+  constexpr int kRound = kCopyThreads * kV;  // units of one part
   if (a.counters[3] != 0) return;
   int used = a.counters[0];
   used = used < 0 ? 0 : (used > a.max_used ? a.max_used : used);
   if (used == 0) return;
   const int P = a.num_planes;
-  const int64_t items = (int64_t)used * P;
-  const int S = a.block_size;
   const int chunk = a.chunk_units;
+  const int parts = (chunk + kRound - 1) / kRound;
+  // gp = g * parts + part: the parts of a destination block are consecutive in both orders
+  const int used_parts = used * parts;
+  const int64_t items = (int64_t)used_parts * P;
+  const int S = a.block_size;
   const uint32_t chunk_bytes = static_cast<uint32_t>(chunk) * 16u;
   const int U = a.row_units;
   // j = u / U as a multiply-high with floor(2^32/U)+1: exact for u < 2^20 and
@@ -352,9 +359,9 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
   const bool unit_rows = U == 1;  // 16-byte rows: j = u (the constant would not fit)
   const int lane = threadIdx.x & 63;
   const int tid = static_cast<int>(threadIdx.x);
-  // (hi, lo) = (plane, g) for the plane-major order, (g, plane) for the block-major order
+  // (hi, lo) = (plane, gp) for the plane-major order, (gp, plane) for the block-major order
   const bool plane_major = a.order == 1;
-  const int inner = plane_major ? used : P;
+  const int inner = plane_major ? used_parts : P;
   int64_t w = blockIdx.x;
   if (w >= items) return;
   int hi = static_cast<int>(w / inner);
@@ -365,13 +372,15 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
   // prefetch of the next item's destination block and plan entry (lanes >= S read entry
   // S-1 and never use it; the loads are unconditional so no branch splits the copy loop)
   const int plan_lane = lane < S ? lane : S - 1;
-  int next_g = plane_major ? lo : hi;
+  int next_gp = plane_major ? lo : hi;
+  int next_g = next_gp / parts;
   int next_dblk = a.free_list[next_g];
   int next_pv = kSmallS ? a.src_plan[(int64_t)next_g * S + plan_lane] : -1;
 
   for (; w < items; w += gridDim.x) {
     const int plane = plane_major ? hi : lo;
     const int g = next_g;
+    const int part = next_gp - g * parts;
     const int dblk = __builtin_amdgcn_readfirstlane(next_dblk);
     const int pv = next_pv;
     lo += step_lo;
@@ -381,7 +390,8 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
       ++hi;
     }
     // past the last item the prefetch re-reads item 0's entries (in bounds, unused)
-    next_g = (w + gridDim.x < items) ? (plane_major ? lo : hi) : 0;
+    next_gp = (w + gridDim.x < items) ? (plane_major ? lo : hi) : 0;
+    next_g = next_gp / parts;
     next_dblk = a.free_list[next_g];
     if (kSmallS) next_pv = a.src_plan[(int64_t)next_g * S + plan_lane];
 
@@ -392,11 +402,14 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
     const __amdgpu_buffer_rsrc_t drsrc =
         __builtin_amdgcn_make_buffer_rsrc(dptr, 0, dst_ok ? chunk_bytes : 0u, kBufferDword3);
     const int32_t* plan = a.src_plan + (int64_t)g * S;
-    int s0 = kSmallS ? __builtin_amdgcn_readlane(pv, 0) : __builtin_amdgcn_readfirstlane(plan[0]);
-    s0 = static_cast<unsigned>(s0) < static_cast<unsigned>(a.num_slots) ? s0 : 0;
-    // kOneRound: the chunk is exactly kCopyThreads*kV units, a compile-time trip count
-    const int rounds_end = kOneRound ? kCopyThreads * kV : chunk;
-    for (int u0 = 0; u0 < rounds_end; u0 += kCopyThreads * kV) {
+    const int u0 = part * kRound;
+    const int j0 =
+        unit_rows ? u0 : static_cast<int>(__umulhi(static_cast<uint32_t>(u0), magic));
+    const int s0 = kSmallS ? __builtin_amdgcn_readlane(pv, j0)
+                           : __builtin_amdgcn_readfirstlane(plan[j0]);
+    // the part's first row is padding: so is the rest of the part
+    if (static_cast<unsigned>(s0) >= static_cast<unsigned>(a.num_slots)) continue;
+    {
       int src[kV];
       int col[kV];
       uint32_t off[kV];
@@ -439,24 +452,23 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
 constexpr int64_t kMaxCopyGrid = 1 << 19;
 
 template <void (*kKernel)(CopyArgs)>
-hipError_t launch_kernel(const CopyArgs& a, int grid, hipStream_t stream) {
-  if (grid <= 0) {
-    const int64_t items = (int64_t)a.max_used * a.num_planes;
-    grid = static_cast<int>(items < kMaxCopyGrid ? items : kMaxCopyGrid);
-  }
+hipError_t launch_kernel(const CopyArgs& a, int64_t items, int grid, hipStream_t stream) {
+  if (grid <= 0) grid = static_cast<int>(items < kMaxCopyGrid ? items : kMaxCopyGrid);
   hipLaunchKernelGGL(kKernel, dim3(grid), dim3(kCopyThreads), 0, stream, a);
   return hipGetLastError();
 }
 
 template <int kPolicy, int kV>
 hipError_t launch_direct(const CopyArgs& a, int grid, hipStream_t stream) {
+  // work items: every (part of a destination block, plane) the buffers can hold; the kernel
+  // indexes parts with 32-bit integers
+  const int64_t parts = (a.chunk_units + kCopyThreads * kV - 1) / (kCopyThreads * kV);
+  if ((int64_t)a.max_used * parts > 0x7fffffff) return hipErrorInvalidValue;
+  const int64_t items = (int64_t)a.max_used * parts * a.num_planes;
   if (a.block_size <= 64) {
-    if (a.chunk_units == kCopyThreads * kV) {
-      return launch_kernel<repack_direct_kernel<kPolicy, true, true, kV>>(a, grid, stream);
-    }
-    return launch_kernel<repack_direct_kernel<kPolicy, true, false, kV>>(a, grid, stream);
+    return launch_kernel<repack_direct_kernel<kPolicy, true, kV>>(a, items, grid, stream);
   }
-  return launch_kernel<repack_direct_kernel<kPolicy, false, false, kV>>(a, grid, stream);
+  return launch_kernel<repack_direct_kernel<kPolicy, false, kV>>(a, items, grid, stream);
 }
 
 template <int kPolicy>

@@ -221,24 +221,27 @@ def tiny_cache(seed: int = 101) -> RepackInputs:
 
 def llama3_8b_random(seed: int = 201, num_reqs: int = 64, num_layers: int = 32,
                      len_range=(2048, 8192), keep: float = 0.3, recent: int = 64,
-                     slack_blocks: int = 1024, pool_bytes: Optional[int] = None) -> RepackInputs:
-    """Llama-3-8B KV geometry (32 layers, 8 KV heads, head_dim 128, bf16, block 16); 64 requests
-    of U[2048,8192] tokens; Random policy keeping 30% of the evictable tokens plus the last 64.
-    The free pool holds keep*M + R*(recent/S + 1) + slack blocks, or, with `pool_bytes`, every
-    block of a pool of that size (a serving engine's whole KV cache) that the requests do not
-    hold."""
+                     slack_blocks: int = 1024, pool_bytes: Optional[int] = None,
+                     block_size: int = 16) -> RepackInputs:
+    """Llama-3-8B KV geometry (32 layers, 8 KV heads, head_dim 128, bf16, block 16 unless
+    `block_size` says otherwise); 64 requests of U[2048,8192] tokens; Random policy keeping 30%
+    of the evictable tokens plus the last 64. The free pool holds keep*M + R*(recent/S + 1) +
+    slack blocks, or, with `pool_bytes`, every block of a pool of that size (a serving engine's
+    whole KV cache) that the requests do not hold."""
     rng = np.random.Generator(np.random.PCG64(seed))
-    shape = KVShape(num_layers, 8, 128, 16, "bf16")
+    S = int(block_size)
+    shape = KVShape(num_layers, 8, 128, S, "bf16")
     lens = rng.integers(len_range[0], len_range[1], size=num_reqs, endpoint=True)
     masks = [random_live(rng, int(n), keep, recent) for n in lens]
-    M = sum(_blocks_for(n, 16) for n in lens)
-    free = int(math.ceil(keep * M)) + num_reqs * (recent // 16 + 1) + slack_blocks
+    M = sum(_blocks_for(n, S) for n in lens)
+    free = int(math.ceil(keep * M)) + num_reqs * (recent // S + 1) + slack_blocks
     note = ""
     if pool_bytes is not None:
         free = max(free, int(pool_bytes // shape.block_bytes) - M)
         note = f", {(M + free) * shape.block_bytes / 2**30:.0f} GiB pool"
-    return _assemble("llama3_8b_random", shape, rng, lens, masks, free, seed,
-                     f"bf16 {num_layers}x8x128, S=16, {num_reqs} req U{list(len_range)}, "
+    name = "llama3_8b_random" if S == 16 else f"llama3_8b_random_s{S}"
+    return _assemble(name, shape, rng, lens, masks, free, seed,
+                     f"bf16 {num_layers}x8x128, S={S}, {num_reqs} req U{list(len_range)}, "
                      f"Random keep {keep} + last {recent}{note}")
 
 
