@@ -187,11 +187,11 @@ vtoken_status vtoken_repack_inplace(const vtoken_cache* cache, const vtoken_batc
  *            0 default (= 4), 1 plain loads and stores, 2 non-temporal loads and stores,
  *            3 non-temporal loads and plain stores, 4 non-temporal loads and sc1 stores,
  *            5 non-temporal loads and sc0 sc1 stores, 6 non-temporal loads, sc1 nt stores
- *   grid:    workgroups of the copy launch; 0 = one per (destination block, plane) work
- *            item that the free list and plan can hold, capped at 2^19 (a grid-stride loop
- *            covers any remainder)
- *   order:   work order over (destination block, plane) items: 0 default (= 2),
- *            1 plane-major, 2 block-major (all planes of one destination block together)
+ *   grid:    workgroups of the copy launch; 0 = one per work item that the free list and
+ *            plan can hold, capped at 2^19 (a grid-stride loop covers any remainder); a work
+ *            item is one 32 KiB part (at most) of a destination block in one plane
+ *   order:   work order over (part of a destination block, plane) items: 0 default (= 2),
+ *            1 plane-major, 2 block-major (all planes of one part together)
  * All settings produce identical bytes; they differ only in speed. Invalid values return
  * VTOKEN_ERR_ARGUMENT. */
 typedef struct vtoken_repack_options {
