@@ -38,7 +38,6 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_13263_amd", "csrc", "vtoken_kernels.hip")
 
 
 def parse_args(argv=None):
@@ -136,21 +135,27 @@ def make_workload(args):
                             dtype=args.kv_dtype, num_kv_heads=args.kv_heads, pool_bytes=budget)
 
 
-def recorded_traffic(workload: str, bytes_alg: int):
-    """HBM bytes per repack launch from the committed rocprofv3 --pmc summary of this
-    workload, if it was taken on the current kernel source and on the same algorithmic bytes
-    (the same requests, liveness and layout); None otherwise."""
-    path = os.path.join(PROFILES, f"repack_{workload}_traffic.md")
-    if not os.path.exists(path):
-        return None
-    text = open(path).read()
-    m_sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
-    m_bytes = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    m_alg = re.search(r"algorithmic_bytes_per_launch:\s*([0-9]+)", text)
-    if not m_sha or not m_bytes or not m_alg or int(m_alg.group(1)) != int(bytes_alg):
-        return None
-    sha = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
-    return float(m_bytes.group(1)) if sha == m_sha.group(1) else None
+_TRAFFIC_RECORD = re.compile(
+    r"traffic_record: kernel=(\S+) workload=(\S+) source=(\S+) source_sha256=([0-9a-f]{64}) "
+    r"algorithmic_bytes=(\d+) traffic_bytes=(\d+)")
+
+
+def recorded_traffic(kernel: str, workload: str, bytes_alg: int):
+    """HBM bytes per launch of `kernel` on `workload` from the committed rocprofv3 --pmc
+    summaries in profiles/ (FETCH_SIZE and WRITE_SIZE, calibrated): a `traffic_record` line
+    counts only while its kernel source file still hashes to the recorded SHA-256 and its
+    algorithmic bytes equal this run's (the same requests, liveness and layout); else None."""
+    for name in sorted(os.listdir(PROFILES)):
+        if not name.endswith(".md"):
+            continue
+        for m in _TRAFFIC_RECORD.finditer(open(os.path.join(PROFILES, name)).read()):
+            k, w, src, sha, alg, traffic = m.groups()
+            if k != kernel or w != workload or int(alg) != int(bytes_alg):
+                continue
+            path = os.path.join(ROOT, src)
+            if os.path.exists(path) and hashlib.sha256(open(path, "rb").read()).hexdigest() == sha:
+                return float(traffic)
+    return None
 
 
 def host_kv_sample(shape, num_blocks: int, planes: int):
@@ -745,7 +750,7 @@ def run_partial_pass(args):
                      "achieved": round(achieved, 1) if achieved else None,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None,
-                     "traffic": None},
+                     "traffic": recorded_traffic("repack_direct_kernel", inp.name, bytes_alg)},
         "cpu_baseline": None if args.no_cpu_baseline or moved == 0 else
         cpu_baseline_partial(inp, args.cpu_planes, args.max_sources, what="the pass"),
     }
@@ -798,6 +803,8 @@ def run_inplace(args, inp, kv, cache, batch, plan, stream):
     R = inp.num_reqs
     repacked = int((plan.live_count[:R].long() * plan.admitted[:R].long()).sum())
     bytes_alg = 2 * moved * sh.token_bytes
+    pipelined = sh.block_size <= 64 and args.variant in (0, 4)
+    inplace_kernel = "repack_inplace_pipe_kernel" if pipelined else "repack_inplace_kernel"
     out = {
         "metric": "repacked KV GB/s (read+write) as % of HBM peak; live tokens repacked/ms",
         "mode": "inplace", "value": round(bytes_alg / (step_ms / 1e3) / 1e9, 2), "unit": "GB/s",
@@ -808,13 +815,11 @@ def run_inplace(args, inp, kv, cache, batch, plan, stream):
                    "rows_moved": moved, "rows_in_place": repacked - moved,
                    "pool_gib": round(inp.pool_bytes() / 2 ** 30, 2),
                    "bytes_alg_per_step": bytes_alg, "admitted": cnt[1], "freed_blocks": cnt[2]},
-        "roofline": {"bound": "hbm",
-                     "kernel": ("repack_inplace_pipe_kernel" if sh.block_size <= 64
-                                else "repack_inplace_kernel"),
+        "roofline": {"bound": "hbm", "kernel": inplace_kernel,
                      "achieved": round(bytes_alg / (kern / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s",
                      "frac": round(bytes_alg / (kern / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
-                     "traffic": None},
+                     "traffic": recorded_traffic(inplace_kernel, inp.name, bytes_alg)},
         "cpu_baseline": None if args.no_cpu_baseline else
         cpu_baseline(inp, args.cpu_planes, inplace=True),
     }
@@ -894,7 +899,8 @@ def run_decode(args, inp, kv, cache, batch, plan, stream):
         "roofline": {"bound": "hbm", "kernel": "vtoken_paged_decode (split + combine)",
                      "achieved": round(after["call_gbs"], 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(after["call_gbs"] / HBM_PEAK_GBS, 4),
-                     "traffic": None},
+                     "traffic": recorded_traffic("vtoken_paged_decode", f"{inp.name}_q{Hq}",
+                                                 bytes_layer)},
         "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline_decode(
             inp, plan.token_slot[:inp.num_tokens].cpu().numpy(), Hq),
     }
@@ -1081,7 +1087,7 @@ def main(argv=None):
     bytes_alg = 2 * moved_tokens * sh.token_bytes
     value = bytes_alg / (ms_per_step / 1e3) / 1e9
     achieved = bytes_alg / (repack_avg / 1e3) / 1e9
-    traffic = recorded_traffic(inp.name, bytes_alg)
+    traffic = recorded_traffic("repack_direct_kernel", inp.name, bytes_alg)
     log(f"step {ms_per_step:.3f} ms, repack {repack_avg:.3f} ms "
         f"(min {min(repack_ms):.3f}), {achieved:.0f} GB/s repack")
 
