@@ -93,6 +93,9 @@ def parse_args(argv=None):
                          "streaming ceilings")
     ap.add_argument("--q-heads", type=int, default=32, help="decode mode: query heads")
     ap.add_argument("--copy-gib", type=float, default=8.0)
+    ap.add_argument("--graph", action="store_true",
+                    help="repack mode: also time the whole pass captured once in a HIP graph "
+                         "and replayed (graph_ms_per_step; for launch-bound small batches)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-planes", type=int, default=4,
                     help="planes of the workload the CPU oracle is timed on")
@@ -101,6 +104,29 @@ def parse_args(argv=None):
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def timed_graph(args, cache, batch, plan):
+    """The pass (build, copy, free; the same options as the eager steps) captured once in a
+    HIP graph and replayed: warm-up replays, then the mean of `steps` replays between two
+    events on the replaying stream."""
+    import torch
+    from paper_2608_13263_amd import binding as B
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        B.build_token_table(cache, batch, plan)
+        B.repack_ex(cache, batch, plan, args.variant, args.grid, args.order)
+        B.free_blocks(batch, plan)
+    for _ in range(max(args.warmup, 1)):
+        graph.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(args.steps):
+        graph.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / args.steps
 
 
 def make_workload(args):
@@ -1072,6 +1098,7 @@ def main(argv=None):
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
+    graph_ms = timed_graph(args, cache, batch, plan) if args.graph else None
     repack_ms = [e[1].elapsed_time(e[2]) for e in evs]
     repack_avg = sum(repack_ms) / len(repack_ms)
     build_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / len(evs)
@@ -1119,6 +1146,7 @@ def main(argv=None):
         "repack_ms": round(repack_avg, 4),
         "repack_ms_median": round(statistics.median(repack_ms), 4),
         "repack_ms_min": round(min(repack_ms), 4),
+        "graph_ms_per_step": round(graph_ms, 4) if graph_ms is not None else None,
         "build_token_table_ms": round(build_ms, 4),
         "free_blocks_ms": round(free_ms, 4),
         "config": {
