@@ -51,6 +51,12 @@
  *     destination block and all non-destination bytes keep their previous contents.
  *   - freed = concatenation over admitted requests (ascending) of all their old blocks
  *     in block-table order.
+ *   - Layout precondition of the full pass: every block id appears at most once over all
+ *     block tables and free_list[0 .. free_len). An admitted request releases all its
+ *     blocks, so a block held by two tables would be released twice and a block both held
+ *     and free could be overwritten while live. Caches with shared-prefix blocks use
+ *     vtoken_plan_partial, which keeps blocks held by several tables in place (I4 of Sec.
+ *     3.5, Sec. 5.7). vtoken_check_layout verifies the precondition on the device.
  *
  * KV layout: one contiguous buffer of 2*num_layers planes, plane index 2*layer + (0 for K,
  * 1 for V); each plane is [num_blocks][block_size][num_kv_heads][head_dim] elements of
@@ -87,10 +93,12 @@ typedef enum vtoken_status {
                                 /* or bt_indptr outside [0, num_bt_entries]              */
   VTOKEN_ERR_TOK_LEN = -12,     /* tok_indptr[r+1]-tok_indptr[r] != seq_lens[r] or       */
                                 /* tok_indptr outside [0, num_tokens]                    */
-  VTOKEN_ERR_SLOT = -13         /* vtoken_plan_partial: a live token's slot lies outside */
+  VTOKEN_ERR_SLOT = -13,        /* vtoken_plan_partial: a live token's slot lies outside */
                                 /* [0, num_blocks*S), or the live tokens of a request's  */
                                 /* sources do not match the live slots counted in them   */
                                 /* (two tokens on one slot, a slot outside its table)    */
+  VTOKEN_ERR_LAYOUT = -14       /* vtoken_check_layout: a block id held twice over the   */
+                                /* block tables and the free list                        */
 } vtoken_status;
 
 /* The paged KV cache (Sec. 2.1). */
@@ -163,6 +171,19 @@ vtoken_status vtoken_repack(const vtoken_cache* cache, const vtoken_batch* batch
  * after vtoken_repack is what makes reuse of these blocks safe. freed_capacity >= M. */
 vtoken_status vtoken_free_blocks(const vtoken_batch* batch, const vtoken_plan* plan,
                                  int32_t* freed, int64_t freed_capacity, hipStream_t stream);
+
+/* Debug check of the full pass's layout precondition (see the conventions above): every id
+ * in block_ids[0 .. M) and free_list[0 .. free_len) lies in [0, num_blocks) and appears at
+ * most once over both. Writes to *status (device int32): VTOKEN_OK; VTOKEN_ERR_BLOCK_RANGE if
+ * any id lies outside the pool (reported before duplicates); else VTOKEN_ERR_LAYOUT if any id
+ * appears twice. workspace: device, at least vtoken_check_layout_workspace_bytes(num_blocks)
+ * bytes (a flag word and one bit per block), overwritten by the call. Reads only the batch's
+ * block_ids and free_list (seq_lens, live and the CSR ranges are not inspected); touches no
+ * KV byte; enqueues three small kernels on `stream`. */
+int64_t vtoken_check_layout_workspace_bytes(int32_t num_blocks);
+vtoken_status vtoken_check_layout(const vtoken_cache* cache, const vtoken_batch* batch,
+                                  void* workspace, int64_t workspace_bytes, int32_t* status,
+                                  hipStream_t stream);
 
 /* In-place mode (an extension beyond the paper's out-of-place relocation, Sec. 3.3.2):
  * the destinations of a repacked request are its own first ceil(live/S) blocks, so no free

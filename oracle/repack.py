@@ -205,6 +205,31 @@ def oracle_repack(seq_lens, tok_indptr, bt_indptr, block_ids, live, free_list, b
         n_admitted=int(admitted.sum()), n_freed=int(freed_indptr[-1]), kv=kv_out)
 
 
+# Status codes of the layout check (the values of include/vtoken.h's status enum).
+LAYOUT_OK, LAYOUT_BLOCK_RANGE, LAYOUT_DUPLICATE = 0, -10, -14
+
+
+def check_layout(block_ids, free_list, num_blocks: int) -> int:
+    """The full pass's layout precondition, checked one id at a time.
+
+    Every block of an admitted request is a source and goes back to the pool after the copy
+    (O6; Sec. 3.3.3, Sec. 3.3.4), and destinations are taken from the free list (O3): so each
+    block id may be held by at most one block table or free-list entry, or a block would be
+    released twice, or written as a destination while a table still holds it (the token
+    table's injectivity, I2 of Sec. 3.5). Ids outside [0, num_blocks) are reported first
+    (LAYOUT_BLOCK_RANGE), then any id seen twice (LAYOUT_DUPLICATE); else LAYOUT_OK."""
+    ids = [int(b) for b in block_ids] + [int(b) for b in free_list]
+    for b in ids:
+        if b < 0 or b >= num_blocks:
+            return LAYOUT_BLOCK_RANGE
+    seen = set()
+    for b in ids:
+        if b in seen:
+            return LAYOUT_DUPLICATE
+        seen.add(b)
+    return LAYOUT_OK
+
+
 def oracle_repack_inputs(inp, kv: Optional[np.ndarray] = None,
                          inplace: bool = False) -> OracleResult:
     """oracle_repack over a RepackInputs-like object (attribute access only)."""

@@ -26,6 +26,7 @@ STATUS = {
     0: "VTOKEN_OK", -1: "VTOKEN_ERR_NULL", -2: "VTOKEN_ERR_SHAPE", -3: "VTOKEN_ERR_CAPACITY",
     -4: "VTOKEN_ERR_HIP", -5: "VTOKEN_ERR_ARGUMENT", -10: "VTOKEN_ERR_BLOCK_RANGE",
     -11: "VTOKEN_ERR_BT_LEN", -12: "VTOKEN_ERR_TOK_LEN", -13: "VTOKEN_ERR_SLOT",
+    -14: "VTOKEN_ERR_LAYOUT",
 }
 STATUS_CODE = {v: k for k, v in STATUS.items()}
 
@@ -110,6 +111,10 @@ _SIGNATURES = {
     "vtoken_repack_ex": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
                                           ctypes.POINTER(CPlan), ctypes.POINTER(CRepackOptions),
                                           ctypes.c_void_p]),
+    "vtoken_check_layout_workspace_bytes": (ctypes.c_int64, [ctypes.c_int32]),
+    "vtoken_check_layout": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
+                                             ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                             ctypes.c_void_p]),
     "vtoken_free_blocks": (ctypes.c_int32, [ctypes.POINTER(CBatch), ctypes.POINTER(CPlan),
                                             ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]),
     "vtoken_build_slot_mapping": (ctypes.c_int32, [ctypes.POINTER(CBatch),
@@ -322,6 +327,23 @@ def free_blocks(batch: Batch, plan: Plan, freed=None, stream=None) -> None:
     out = plan.freed if freed is None else freed
     _check(lib.vtoken_free_blocks(ctypes.byref(b), ctypes.byref(p), _ptr(out),
                                   int(out.numel()), _stream(stream)), "vtoken_free_blocks")
+
+
+def check_layout(cache: KVCache, batch: Batch, workspace=None, stream=None):
+    """Device check of the full pass's layout precondition (each block id in the pool and
+    held at most once over the block tables and the free list); returns a device int32 [1]
+    status tensor (VTOKEN_OK, VTOKEN_ERR_BLOCK_RANGE or VTOKEN_ERR_LAYOUT)."""
+    import torch
+    lib = load_library()
+    need = int(lib.vtoken_check_layout_workspace_bytes(cache.num_blocks))
+    if workspace is None:
+        workspace = torch.empty(max(need // 4, 1), dtype=torch.int32, device=cache.kv.device)
+    status = torch.empty(1, dtype=torch.int32, device=cache.kv.device)
+    c, b = cache.c(), batch.c()
+    _check(lib.vtoken_check_layout(ctypes.byref(c), ctypes.byref(b), _ptr(workspace),
+                                   int(workspace.numel() * workspace.element_size()),
+                                   _ptr(status), _stream(stream)), "vtoken_check_layout")
+    return status
 
 
 def run_pass(cache: KVCache, batch: Batch, plan: Optional[Plan] = None, stream=None,

@@ -18,7 +18,7 @@ ROOT = os.path.dirname(HERE)
 LIB_PATH = os.path.join(HERE, "libvtoken.so")
 SOURCES = [os.path.join(HERE, "csrc", f)
            for f in ("vtoken_abi.hip", "vtoken_kernels.hip", "vtoken_attention.hip",
-                     "vtoken_planner.hip")]
+                     "vtoken_planner.hip", "vtoken_layout.hip")]
 HEADERS = [os.path.join(ROOT, "include", "vtoken.h"),
            os.path.join(HERE, "csrc", "vtoken_internal.h")]
 PROBE_LIB_PATH = os.path.join(HERE, "libvtoken_probe.so")

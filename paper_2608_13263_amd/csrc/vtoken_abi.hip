@@ -465,6 +465,33 @@ vtoken_status vtoken_plan_partial(const vtoken_cache* cache, const vtoken_batch*
   return hip_status(vtoken::launch_planner(a, stream));
 }
 
+int64_t vtoken_check_layout_workspace_bytes(int32_t num_blocks) {
+  if (num_blocks <= 0) return -1;
+  return 4 * vtoken::layout_words(num_blocks);
+}
+
+vtoken_status vtoken_check_layout(const vtoken_cache* cache, const vtoken_batch* batch,
+                                  void* workspace, int64_t workspace_bytes, int32_t* status,
+                                  hipStream_t stream) {
+  vtoken_status s = check_cache(cache);
+  if (s != VTOKEN_OK) return s;
+  if ((s = check_batch(batch)) != VTOKEN_OK) return s;
+  if (workspace == nullptr || status == nullptr) return VTOKEN_ERR_NULL;
+  if (workspace_bytes < vtoken_check_layout_workspace_bytes(cache->num_blocks)) {
+    return VTOKEN_ERR_CAPACITY;
+  }
+  vtoken::LayoutArgs a;
+  a.block_ids = batch->block_ids;
+  a.free_list = batch->free_list;
+  a.num_bt_entries = batch->num_bt_entries;
+  a.free_len = batch->free_len;
+  a.num_blocks = cache->num_blocks;
+  a.num_words = vtoken::layout_words(cache->num_blocks);
+  a.words = static_cast<uint32_t*>(workspace);
+  a.status = status;
+  return hip_status(vtoken::launch_check_layout(a, stream));
+}
+
 int32_t vtoken_last_hip_error(void) { return g_last_hip_error; }
 
 const char* vtoken_status_string(int32_t status) {
@@ -479,10 +506,11 @@ const char* vtoken_status_string(int32_t status) {
     case VTOKEN_ERR_BT_LEN: return "VTOKEN_ERR_BT_LEN: block table length != ceil(len/S)";
     case VTOKEN_ERR_TOK_LEN: return "VTOKEN_ERR_TOK_LEN: token range != sequence length";
     case VTOKEN_ERR_SLOT: return "VTOKEN_ERR_SLOT: a live token's slot is invalid for its table";
+    case VTOKEN_ERR_LAYOUT: return "VTOKEN_ERR_LAYOUT: a block id is held twice";
     default: return "unknown vtoken status";
   }
 }
 
-int32_t vtoken_version(void) { return 111; }
+int32_t vtoken_version(void) { return 112; }
 
 }  // extern "C"

@@ -214,6 +214,20 @@ hipError_t launch_build(const MetaArgs& a, hipStream_t stream);
 hipError_t launch_repack_inplace(const InplaceArgs& a, int variant, hipStream_t stream);
 hipError_t launch_free(const MetaArgs& a, int32_t* freed, int64_t freed_capacity,
                        hipStream_t stream);
+// The layout check (vtoken_layout.hip): words[0] is the flag word, words[1 ..] one bit per
+// block; layout_words() words in all.
+struct LayoutArgs {
+  const int32_t* block_ids;
+  const int32_t* free_list;
+  int64_t num_bt_entries;
+  int64_t free_len;
+  int32_t num_blocks;
+  int64_t num_words;
+  uint32_t* words;
+  int32_t* status;
+};
+int64_t layout_words(int32_t num_blocks);
+hipError_t launch_check_layout(const LayoutArgs& a, hipStream_t stream);
 // variant/grid/order as in vtoken_repack_options; returns hipErrorInvalidValue for an
 // unknown variant or order.
 hipError_t launch_repack(const CopyArgs& a, int variant, int grid, int order,

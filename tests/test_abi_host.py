@@ -42,7 +42,7 @@ def test_status_codes_match_binding():
     for name, code in codes.items():
         assert B.status_string(code).startswith(name)
     assert B.status_string(12345) == "unknown vtoken status"
-    assert B.load_library().vtoken_version() == 111
+    assert B.load_library().vtoken_version() == 112
 
 
 def test_struct_layouts_match_header(tmp_path):
@@ -304,3 +304,23 @@ def test_stream_probe_library_rejects_bad_sizes():
     assert lib.vtoken_probe_head_read(fake, 1 << 20, 2000, fake, 64, 1, fake, None) == -2
     assert lib.vtoken_probe_head_read(fake, 1 << 20, 2048, fake, 100, 1, fake, None) == -2
     assert lib.vtoken_probe_head_read(fake, 1024, 2048, fake, 64, 1, fake, None) == -2
+
+
+def test_check_layout_workspace_bytes_and_bad_arguments():
+    lib = B.load_library()
+    # a flag word and one bit per block, in 32-bit words
+    assert [lib.vtoken_check_layout_workspace_bytes(n) for n in (1, 32, 33, 64, 100)] == \
+        [8, 8, 12, 12, 20]
+    assert lib.vtoken_check_layout_workspace_bytes(0) == -1
+    assert lib.vtoken_check_layout_workspace_bytes(2 ** 31 - 1) == 4 * (1 + 2 ** 26)
+    cache, batch, _ = _good()                      # 100 blocks: 20 bytes of workspace
+    ws, st = _fake_ptr(), _fake_ptr()
+    call = lambda c, w, nbytes, s: lib.vtoken_check_layout(  # noqa: E731
+        ctypes.byref(c) if c is not None else None, ctypes.byref(batch), w, nbytes, s, None)
+    assert call(cache, ws, 19, st) == B.STATUS_CODE["VTOKEN_ERR_CAPACITY"]
+    assert call(cache, None, 20, st) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    assert call(cache, ws, 20, None) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    assert call(None, ws, 20, st) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    cache.block_size = 0
+    assert call(cache, ws, 20, st) == B.STATUS_CODE["VTOKEN_ERR_SHAPE"]
+    assert lib.vtoken_status_string(-14).decode().startswith("VTOKEN_ERR_LAYOUT")

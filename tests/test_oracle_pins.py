@@ -69,3 +69,40 @@ def test_invariant_checker_rejects_bad_packings():
         check(kv_after=bad_kv)              # a byte outside the moved rows changed
     with pytest.raises(AssertionError):
         check(fr=res.freed[:-1])            # a source block not released
+
+
+# ---- the full pass's layout precondition (each block id held at most once) ----
+
+def test_check_layout_hand_cases():
+    from oracle.repack import check_layout
+    nb = 10
+    cases = [
+        ([], [], 0),                                   # nothing to check
+        ([0, 1, 2], [3, 4], 0),                         # disjoint, in range
+        ([0, 1, 1], [3], -14),                          # twice in one table
+        ([0, 5], [5, 6], -14),                          # held and free
+        ([2], [7, 7], -14),                             # twice in the free list
+        ([0, 10], [1], -10),                            # past the pool
+        ([0, 1], [-1, 1], -10),                         # negative and a duplicate: range first
+        ([9, 8, 7, 6, 5, 4, 3, 2, 1, 0], [], 0),        # the whole pool, once each
+    ]
+    for tables, free, code in cases:
+        assert check_layout(tables, free, nb) == code, (tables, free)
+
+
+def test_check_layout_on_generated_layouts():
+    """Every generated workload is a permutation of the pool split into tables and free list;
+    planting one repeated id in any position gives the duplicate code."""
+    import numpy as np
+    from oracle.repack import check_layout
+    from paper_2608_13263_amd import workloads as W
+    inp = W.tiny_cache(101)
+    assert check_layout(inp.block_ids, inp.free_list, inp.num_blocks) == 0
+    rng = np.random.default_rng(4)
+    ids = np.concatenate([inp.block_ids, inp.free_list])
+    for _ in range(20):
+        i, j = rng.choice(len(ids), size=2, replace=False)
+        bad = ids.copy()
+        bad[j] = bad[i]
+        M = len(inp.block_ids)
+        assert check_layout(bad[:M], bad[M:], inp.num_blocks) == -14
