@@ -242,5 +242,25 @@ def pin_reductions(mod, seed=2):
     assert list(mod.block_live_counts([5, 2], [20, 21, 23, 9], 4)) == [3, 1]
 
 
+def pin_layout(mod):
+    """Hand-derived codes of the full pass's layout precondition (0 ok, -10 an id outside
+    the pool, reported first, -14 an id held twice)."""
+    nb = 10
+    cases = [
+        ([], [], 0),
+        ([0, 1, 2], [3, 4], 0),
+        ([0, 1, 1], [3], -14),                          # twice in one table
+        ([0, 5], [5, 6], -14),                          # held and free
+        ([2], [7, 7], -14),                             # twice in the free list
+        ([0, 10], [1], -10),                            # past the pool
+        ([0, 1], [-1, 1], -10),                         # negative and a repeat: range first
+        ([3], [9], 0),                                  # the pool's last block, once
+        ([9, 8, 7, 6, 5, 4, 3, 2, 1, 0], [], 0),        # the whole pool, once each
+    ]
+    for tables, free, code in cases:
+        got = mod.check_layout(tables, free, nb)
+        assert got == code, f"check_layout({tables}, {free}) = {got}, expected {code}"
+
+
 ALL_PINS = (pin_worked_example, pin_paper_numbers, pin_reductions, pin_invariants,
-            pin_bruteforce)
+            pin_bruteforce, pin_layout)

@@ -28,6 +28,10 @@ MUTATIONS = {
                        "src_plan[dst_indptr[r] * S + rk[live_pos]] = new_slots"),
     "deferred_gets_moved": ("if admitted[r]:\n            dest", "if profitable[r]:\n            dest"),
     "dead_tokens_kept": ("lv = live[a:b] != 0", "lv = live[a:b] >= 0"),
+    "layout_ignores_free_list": ("ids = [int(b) for b in block_ids] + [int(b) for b in free_list]",
+                                 "ids = [int(b) for b in block_ids]"),
+    "layout_upper_bound": ("if b < 0 or b >= num_blocks:", "if b < 0 or b > num_blocks:"),
+    "layout_no_negative": ("if b < 0 or b >= num_blocks:", "if b >= num_blocks:"),
 }
 
 

@@ -74,20 +74,7 @@ def test_invariant_checker_rejects_bad_packings():
 # ---- the full pass's layout precondition (each block id held at most once) ----
 
 def test_check_layout_hand_cases():
-    from oracle.repack import check_layout
-    nb = 10
-    cases = [
-        ([], [], 0),                                   # nothing to check
-        ([0, 1, 2], [3, 4], 0),                         # disjoint, in range
-        ([0, 1, 1], [3], -14),                          # twice in one table
-        ([0, 5], [5, 6], -14),                          # held and free
-        ([2], [7, 7], -14),                             # twice in the free list
-        ([0, 10], [1], -10),                            # past the pool
-        ([0, 1], [-1, 1], -10),                         # negative and a duplicate: range first
-        ([9, 8, 7, 6, 5, 4, 3, 2, 1, 0], [], 0),        # the whole pool, once each
-    ]
-    for tables, free, code in cases:
-        assert check_layout(tables, free, nb) == code, (tables, free)
+    oracle_pins.pin_layout(oracle_repack_mod)
 
 
 def test_check_layout_on_generated_layouts():
