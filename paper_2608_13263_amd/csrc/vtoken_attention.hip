@@ -346,6 +346,13 @@ void decode_split_kernel(AttnArgs a) {
   // head 0), a conditional load would wait for every outstanding K/V load. Every wave needs
   // the same operands: wave w builds chunks w, w + kWaves, ... for all 64 lanes into LDS, read
   // after the barrier below.
+  // The head dims of a k-chunk's lane group: any assignment gives the same dot products as
+  // long as q and K use the same one. fp8 pairs the chunks (2c, 2c+1) so that a lane's two
+  // 8-byte K pieces are 16 contiguous bytes, read by one load.
+  constexpr bool kPairK = kKind == 2 && kChunks % 2 == 0;
+  auto head_dim_of = [&](int ch, int e) {
+    return kPairK ? (ch >> 1) * 64 + grp * 16 + (ch & 1) * 8 + e : ch * 32 + grp * kPer + e;
+  };
   __shared__ OpT q_s[kChunks][64];
   {
     const float* qrow =
@@ -355,7 +362,7 @@ void decode_split_kernel(AttnArgs a) {
       OpT qv8;
 #pragma unroll
       for (int e = 0; e < kPer; ++e) {
-        const float qv = qrow[ch * 32 + grp * kPer + e] * a.scale;
+        const float qv = qrow[head_dim_of(ch, e)] * a.scale;
         const float q = real ? qv : 0.f;
         const ElemT hi = static_cast<ElemT>(q);
         qv8[e] = low ? static_cast<ElemT>(q - static_cast<float>(hi)) : hi;
@@ -372,11 +379,20 @@ void decode_split_kernel(AttnArgs a) {
     const int t = wt0 + i * 16 + row;
     const int sl = slots[t < nt ? t : nt - 1];
     kok[i] = static_cast<unsigned>(sl) < static_cast<unsigned>(a.num_slots);
-    const uint8_t* base = kplane + (int64_t)(kok[i] ? sl : 0) * a.row_bytes + head0 +
-                          grp * kPer * kElem;
+    const uint8_t* row_base = kplane + (int64_t)(kok[i] ? sl : 0) * a.row_bytes + head0;
+    if constexpr (kPairK) {
 #pragma unroll
-    for (int ch = 0; ch < kChunks; ++ch) {
-      kw[i][ch] = *reinterpret_cast<const PieceT*>(base + ch * 32 * kElem);
+      for (int p = 0; p < kChunks / 2; ++p) {
+        const u32x4 w = *reinterpret_cast<const u32x4*>(row_base + p * 64 + grp * 16);
+        kw[i][2 * p] = PieceT{w.x, w.y};
+        kw[i][2 * p + 1] = PieceT{w.z, w.w};
+      }
+    } else {
+      const uint8_t* base = row_base + grp * kPer * kElem;
+#pragma unroll
+      for (int ch = 0; ch < kChunks; ++ch) {
+        kw[i][ch] = *reinterpret_cast<const PieceT*>(base + ch * 32 * kElem);
+      }
     }
   }
   // V rows: 16 bytes per lane, a whole head row per kLanesV lanes, read with non-temporal
