@@ -305,7 +305,8 @@ void decode_split_kernel(AttnArgs a) {
   constexpr int kTiles = kTW / 16;                   // 16-token score tiles per wave
   constexpr int kKC = (kTiles + 1) / 2;              // 32-token value k-steps per wave
   constexpr int kDC = kD / 16;                       // 16-element value chunks
-  constexpr int kLanesV = kD / kPer;                 // V load: lanes per token row
+  constexpr int kPerV = kKind == 2 ? 16 : kPer;      // V elements per lane load: 16 bytes
+  constexpr int kLanesV = kD / kPerV;                // V load: lanes per token row
   constexpr int kTokV = 64 / kLanesV;                // V load: tokens per wave pass
   constexpr int kItV = kTW / kTokV;                  // V load: pieces per lane
   constexpr int kWin = kTW < 32 ? kTW : 32;          // V rows a wave stages per k-step
@@ -395,19 +396,19 @@ void decode_split_kernel(AttnArgs a) {
       }
     }
   }
-  // V rows: 16 bytes per lane, a whole head row per kLanesV lanes, read with non-temporal
-  // loads (each line is used by one instruction; measured +2-6% over plain loads). The K
-  // pieces above stay plain: in the matrix-core operand order a row's line is split over two
-  // instructions, and non-temporal K loads were slower (bf16 -5%, fp8 -15%).
+  // V rows: 16 bytes per lane (8 elements at 16 bits, 16 fp8), a whole head row per kLanesV
+  // lanes, read with non-temporal loads (each line is used by one instruction; measured
+  // +2-6% over plain loads). The K pieces above stay plain: in the matrix-core operand order
+  // a row's line is split over two instructions, and non-temporal K loads were slower.
   const int vpiece = lane % kLanesV;
-  PieceT vw[kItV];
+  u32x4 vw[kItV];
 #pragma unroll
   for (int i = 0; i < kItV; ++i) {
     const int t = wt0 + lane / kLanesV + i * kTokV;
     const int sl = slots[t < nt ? t : nt - 1];
     const bool ok = static_cast<unsigned>(sl) < static_cast<unsigned>(a.num_slots);
-    vw[i] = __builtin_nontemporal_load(reinterpret_cast<const PieceT*>(
-        vplane + (int64_t)(ok ? sl : 0) * a.row_bytes + head0 + vpiece * kPer * kElem));
+    vw[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(
+        vplane + (int64_t)(ok ? sl : 0) * a.row_bytes + head0 + vpiece * 16));
   }
 
   // ---- scores of this wave's tiles: lane holds tokens wt0 + 16i + 4*grp + j of head row % 8
@@ -442,8 +443,14 @@ void decode_split_kernel(AttnArgs a) {
   auto stage_v = [&](int kc) {
 #pragma unroll
     for (int ii = 0; ii < kItW; ++ii) {
-      *reinterpret_cast<u32x4*>(vwin + (lane / kLanesV + ii * kTokV) * kRowB + vpiece * 16) =
-          v_row16<kKind>(vw[kc * kItW + ii]);
+      const u32x4 w = vw[kc * kItW + ii];
+      uint8_t* dst = vwin + (lane / kLanesV + ii * kTokV) * kRowB + vpiece * kPerV * 2;
+      if constexpr (kKind == 2) {   // 16 fp8 values -> 16 bf16 values (32 bytes)
+        *reinterpret_cast<u32x4*>(dst) = v_row16<kKind>(u32x2{w.x, w.y});
+        *reinterpret_cast<u32x4*>(dst + 16) = v_row16<kKind>(u32x2{w.z, w.w});
+      } else {
+        *reinterpret_cast<u32x4*>(dst) = w;
+      }
     }
   };
   stage_v(0);
