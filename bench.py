@@ -95,7 +95,9 @@ def parse_args(argv=None):
     ap.add_argument("--copy-gib", type=float, default=8.0)
     ap.add_argument("--graph", action="store_true",
                     help="repack mode: also time the whole pass captured once in a HIP graph "
-                         "and replayed (graph_ms_per_step; for launch-bound small batches)")
+                         "and replayed (graph_ms_per_step; for launch-bound small batches); "
+                         "decode mode: the whole decode step (every layer) replayed from a "
+                         "graph (after_repack.graph_step_ms)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-planes", type=int, default=4,
                     help="planes of the workload the CPU oracle is timed on")
@@ -910,6 +912,27 @@ def run_decode(args, inp, kv, cache, batch, plan, stream):
                          call_gbs=bytes_layer / (call_ms / 1e3) / 1e9)
         log(f"decode {name}: step {step_ms:.3f} ms ({res[name]['gbs']:.0f} GB/s), per layer "
             f"{call_ms * 1e3:.1f} us ({res[name]['call_gbs']:.0f} GB/s)")
+        if args.graph and name == "after_repack":
+            # the whole decode step (every layer) captured once and replayed
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                for layer in range(sh.num_layers):
+                    B.paged_decode(cache, q, indptr, slots, layer, max_tokens, out=out,
+                                   workspace=ws)
+            for _ in range(max(args.warmup, 1)):
+                graph.replay()
+            torch.cuda.synchronize()
+            g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            g0.record()
+            for _ in range(args.steps):
+                graph.replay()
+            g1.record()
+            torch.cuda.synchronize()
+            gms = g0.elapsed_time(g1) / args.steps
+            res[name]["graph_step_ms"] = gms
+            res[name]["graph_gbs"] = bytes_step / (gms / 1e3) / 1e9
+            log(f"decode {name} from a HIP graph: step {gms:.3f} ms "
+                f"({res[name]['graph_gbs']:.0f} GB/s)")
     after = res["after_repack"]
     out_json = {
         "metric": "paged decode K/V GB/s through the slot mapping (all layers, all requests)",
