@@ -562,7 +562,11 @@ void decode_split_kernel(AttnArgs a) {
 // weights w_s = exp(m_s - M), out = sum_s w_s acc_s / sum_s w_s l_s. The splits are spread
 // over the threads (maxima, weights) and the head elements over the threads (weighted sum,
 // 128 splits per chunk with their weights in LDS), so no thread walks the splits alone.
+// Each thread reads the (m_s, l_s) pair of its first split once, and the values of the first
+// kCombinePre splits are loaded before the two reductions, so that the call waits for about
+// two dependent rounds of loads instead of four.
 constexpr int kCombineThreads = 128;
+constexpr int kCombinePre = 8;
 
 template <bool kMax>
 __device__ __forceinline__ float block_reduce(float v, float* red) {
@@ -599,22 +603,47 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(AttnArg
     return;
   }
   const float* rec0 = a.workspace + ((int64_t)r * a.num_q_heads + qh) * a.splits * rs;
-  float m = -INFINITY;
-  for (int s = tid; s < ns; s += kCombineThreads) m = fmaxf(m, rec0[s * rs]);
+  // each thread owns head elements d = tid, tid + 128 (head_dim <= 256)
+  const int d0 = tid, d1 = tid + kCombineThreads;
+  float p0[kCombinePre], p1[kCombinePre];
+#pragma unroll
+  for (int j = 0; j < kCombinePre; ++j) {
+    p0[j] = j < ns && d0 < D ? rec0[j * rs + 2 + d0] : 0.f;
+    p1[j] = j < ns && d1 < D ? rec0[j * rs + 2 + d1] : 0.f;
+  }
+  // (m_s, l_s) of split s = tid, both issued before either is used
+  float m0 = -INFINITY, l0 = 0.f;
+  if (tid < ns) {
+    m0 = rec0[tid * rs];
+    l0 = rec0[tid * rs + 1];
+  }
+  float m = m0;
+  for (int s = tid + kCombineThreads; s < ns; s += kCombineThreads) m = fmaxf(m, rec0[s * rs]);
   const float M = block_reduce<true>(m, red);
-  float l = 0.f;
-  for (int s = tid; s < ns; s += kCombineThreads) l += rec0[s * rs + 1] * __expf(rec0[s * rs] - M);
+  const float w0 = tid < ns ? __expf(m0 - M) : 0.f;
+  float l = tid < ns ? l0 * w0 : 0.f;
+  for (int s = tid + kCombineThreads; s < ns; s += kCombineThreads) {
+    l += rec0[s * rs + 1] * __expf(rec0[s * rs] - M);
+  }
   const float L = block_reduce<false>(l, red);
   const float inv = 1.f / L;
-  // each thread owns head elements d = tid, tid + 128 (head_dim <= 256)
   float v0 = 0.f, v1 = 0.f;
-  const int d0 = tid, d1 = tid + kCombineThreads;
   for (int base = 0; base < ns; base += kCombineThreads) {
     const int n = ns - base < kCombineThreads ? ns - base : kCombineThreads;
-    if (tid < n) w_s[tid] = __expf(rec0[(base + tid) * rs] - M);
+    if (tid < n) w_s[tid] = base == 0 ? w0 : __expf(rec0[(base + tid) * rs] - M);
     __syncthreads();
     const float* rb = rec0 + (int64_t)base * rs + 2;
     int j = 0;
+    if (base == 0) {
+#pragma unroll
+      for (int i = 0; i < kCombinePre; ++i) {
+        if (i < n) {
+          v0 += p0[i] * w_s[i];
+          v1 += p1[i] * w_s[i];
+        }
+      }
+      j = n < kCombinePre ? n : kCombinePre;
+    }
     for (; j + 4 <= n; j += 4) {
       if (d0 < D) {
         v0 += rb[j * rs + d0] * w_s[j] + rb[(j + 1) * rs + d0] * w_s[j + 1] +
