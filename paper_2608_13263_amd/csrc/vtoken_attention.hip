@@ -564,7 +564,7 @@ void decode_split_kernel(AttnArgs a) {
 // 128 splits per chunk with their weights in LDS), so no thread walks the splits alone.
 // Each thread reads the (m_s, l_s) pair of its first split once, and the values of the first
 // kCombinePre splits are loaded before the two reductions, so that the call waits for about
-// two dependent rounds of loads instead of four.
+// two dependent rounds of loads instead of four; the remaining splits go 8, then 4 at a time.
 constexpr int kCombineThreads = 128;
 constexpr int kCombinePre = 8;
 
@@ -643,6 +643,22 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(AttnArg
         }
       }
       j = n < kCombinePre ? n : kCombinePre;
+    }
+    for (; j + 8 <= n; j += 8) {
+      if (d0 < D) {
+        float x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] = rb[(j + u) * rs + d0];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v0 += x[u] * w_s[j + u];
+      }
+      if (d1 < D) {
+        float x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] = rb[(j + u) * rs + d1];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v1 += x[u] * w_s[j + u];
+      }
     }
     for (; j + 4 <= n; j += 4) {
       if (d0 < D) {
