@@ -413,24 +413,39 @@ def run_copy(args):
                       "frac_of_8TBps": round(gbs / HBM_PEAK_GBS, 4)}), flush=True)
 
 
+PROBE_SOURCE = os.path.join(ROOT, "bench_probe.hip")
+
+
+def probe_library(rebuild: bool = False):
+    """The memory-system probes (bench_probe.hip; measurement tooling, not part of the C ABI)
+    as a ctypes library, compiled on demand with the package's hipcc flags into
+    _build/libvtoken_probe-<source hash>.so (an existing build of the same source is reused
+    unless `rebuild`)."""
+    import ctypes
+    from paper_2608_13263_amd import build as Bld
+    sha = hashlib.sha256(open(PROBE_SOURCE, "rb").read()).hexdigest()[:16]
+    path = os.path.join(ROOT, "_build", f"libvtoken_probe-{sha}.so")
+    if rebuild or not os.path.exists(path):
+        os.makedirs(os.path.dirname(path), exist_ok=True)
+        Bld.build_one(path, [PROBE_SOURCE])
+    lib = ctypes.CDLL(path)
+    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    lib.vtoken_probe_read.argtypes = [vp, i64, i32, vp, vp]
+    lib.vtoken_probe_write.argtypes = [vp, i64, i32, vp]
+    lib.vtoken_probe_copy.argtypes = [vp, vp, i64, i32, vp]
+    lib.vtoken_probe_head_read.argtypes = [vp, i64, i32, vp, i64, i32, vp, vp]
+    return lib
+
+
 def run_stream(args):
-    """Streaming rates of the memory system (libvtoken_probe.so) in one pool sized as the
+    """Streaming rates of the memory system (bench_probe.hip) in one pool sized as the
     repack benchmark's (90% of free HBM by default): reads, writes and copies of 32 KiB chunks
     and the decode's pattern (256-byte head pieces of 2 KiB token rows through a slot list of
     shuffled 16-token blocks, K and V planes). These are the ceilings the repack and the
     decode are set against; HIP events on the launch stream."""
     import ctypes
     import torch
-    from paper_2608_13263_amd.build import PROBE_LIB_PATH
-    if not os.path.exists(PROBE_LIB_PATH):
-        raise SystemExit(f"{PROBE_LIB_PATH} is missing: build with "
-                         "`python -m paper_2608_13263_amd.build`")
-    lib = ctypes.CDLL(PROBE_LIB_PATH)
-    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
-    lib.vtoken_probe_read.argtypes = [vp, i64, i32, vp, vp]
-    lib.vtoken_probe_write.argtypes = [vp, i64, i32, vp]
-    lib.vtoken_probe_copy.argtypes = [vp, vp, i64, i32, vp]
-    lib.vtoken_probe_head_read.argtypes = [vp, i64, i32, vp, i64, i32, vp, vp]
+    lib = probe_library()
     free, _ = torch.cuda.mem_get_info()
     chunk = 32768
     pool = int((args.pool_frac if args.pool_frac > 0 else 0.5) * free)

@@ -25,8 +25,9 @@
  *   - Host-side argument errors return a negative status synchronously and enqueue
  *     nothing. Errors that only the device can see (a bad block id, inconsistent CSR
  *     lengths, a capacity exceeded) are written to plan->counters[3] by the first
- *     kernel of vtoken_build_token_table; every later kernel reads that word and does
- *     nothing when it is not VTOKEN_OK. The caller inspects it after its own sync.
+ *     kernel of vtoken_build_token_table (a copy handed a plan of the other mode writes
+ *     VTOKEN_ERR_PLAN_MODE there); every later kernel reads that word and does nothing
+ *     when it is not VTOKEN_OK. The caller inspects it after its own sync.
  *     Every kernel bounds-checks what it dereferences, so no status path writes
  *     outside the buffers the caller described.
  *   - The library is re-entrant: calls on different streams with disjoint buffers may
@@ -97,8 +98,13 @@ typedef enum vtoken_status {
                                 /* [0, num_blocks*S), or the live tokens of a request's  */
                                 /* sources do not match the live slots counted in them   */
                                 /* (two tokens on one slot, a slot outside its table)    */
-  VTOKEN_ERR_LAYOUT = -14       /* vtoken_check_layout: a block id held twice over the   */
+  VTOKEN_ERR_LAYOUT = -14,      /* vtoken_check_layout: a block id held twice over the   */
                                 /* block tables and the free list                        */
+  VTOKEN_ERR_PLAN_MODE = -15    /* a copy was handed a plan built for the other mode     */
+                                /* (vtoken_repack[_ex] needs a plan of                   */
+                                /* vtoken_build_token_table or vtoken_plan_partial,      */
+                                /* vtoken_repack_inplace[_ex] one of                     */
+                                /* vtoken_build_token_table_inplace); nothing is copied  */
 } vtoken_status;
 
 /* The paged KV cache (Sec. 2.1). */
@@ -145,8 +151,10 @@ typedef struct vtoken_plan {
                             /*       consumed free-list entry) and offset j, entry g*S+j is */
                             /*       the source slot of the token placed there, -1 if none */
   int32_t* freed_indptr;    /* [R+1] exclusive scan of admitted*old_blocks                  */
-  int32_t* counters;        /* [4]   used free-list entries, admitted requests, freed       */
-                            /*       blocks, status (VTOKEN_OK or a device error code)      */
+  int32_t* counters;        /* [5]   used free-list entries, admitted requests, freed       */
+                            /*       blocks, status (VTOKEN_OK or a device error code),     */
+                            /*       plan mode (1 out of place, 2 in place; checked by the  */
+                            /*       copy, which sets VTOKEN_ERR_PLAN_MODE on a mismatch)   */
   int64_t  new_bt_capacity;   /* entries in new_block_ids, >= M            [host]           */
   int64_t  src_plan_capacity; /* entries in src_plan, >= min(free_len, M)*S [host]         */
 } vtoken_plan;
@@ -194,9 +202,12 @@ vtoken_status vtoken_check_layout(const vtoken_cache* cache, const vtoken_batch*
  * hold src_plan_capacity >= M*S. Call order: vtoken_build_token_table_inplace, then
  * vtoken_repack_inplace, then vtoken_free_blocks (the freed list is the released tails).
  * vtoken_repack_inplace requires block_size*row_bytes <= 64 KiB (VTOKEN_ERR_SHAPE otherwise):
- * it stages one destination block at a time through LDS, walking each (request, plane) in
- * block order so that a block is written only after every read of its own and earlier
- * destination blocks. */
+ * one workgroup walks each (request, plane) chain in block order and holds one destination
+ * block's moving rows at a time (in registers by default; in LDS with the staging variants of
+ * vtoken_repack_inplace_ex), so that a block is written only after every read of its own and
+ * earlier destination blocks. Handed a plan of vtoken_build_token_table, it copies nothing and
+ * sets counters[3] to VTOKEN_ERR_PLAN_MODE (and vtoken_repack does the same with an in-place
+ * plan). */
 vtoken_status vtoken_build_token_table_inplace(const vtoken_cache* cache,
                                                const vtoken_batch* batch,
                                                const vtoken_plan* plan, hipStream_t stream);
@@ -267,8 +278,8 @@ vtoken_status vtoken_repack_inplace_ex(const vtoken_cache* cache, const vtoken_b
  *
  * Outputs go to the vtoken_plan (sizes as for vtoken_build_token_table: token_slot [T],
  * live_count / admitted [R], CSR offsets [R+1], new_block_ids with new_bt_capacity >= M,
- * src_plan with src_plan_capacity >= min(free_len, M)*S, counters [4] = {destination blocks
- * used, requests admitted, sources released, status}) and to the state buffers below. The
+ * src_plan with src_plan_capacity >= min(free_len, M)*S, counters [5] = {destination blocks
+ * used, requests admitted, sources released, status, plan mode 1}) and to the state buffers below. The
  * copy is vtoken_repack on the same plan, enqueued after this call. The released sources are
  * state->sources[0 .. counters[2]) (CSR by freed_indptr): reuse them only after the copy has
  * executed on the stream; vtoken_free_blocks does not apply to this pass. */
@@ -342,7 +353,10 @@ vtoken_status vtoken_append_slots(int32_t num_reqs, const int32_t* append_indptr
  * sharing it must be stream-ordered). A request with more slots than max_tokens provides
  * for is never truncated: its outputs are NaN, unless its slots still fit the
  * ceil(max_tokens / split) splits, which are all computed. A slot outside the pool (negative
- * or >= num_blocks * block_size) is never dereferenced; its request's outputs are NaN. */
+ * or >= num_blocks * block_size) is never dereferenced; its request's outputs are NaN. A
+ * request whose slot range is malformed (slot_indptr[r] < 0, or a negative count:
+ * slot_indptr[r+1] < slot_indptr[r], or slot_count[r] < 0) reads no slot and gets NaN
+ * outputs. */
 enum { VTOKEN_KV_FP16 = 0, VTOKEN_KV_BF16 = 1, VTOKEN_KV_FP8_E4M3 = 2 };
 
 typedef struct vtoken_decode {
@@ -378,6 +392,13 @@ const char* vtoken_status_string(int32_t status);
 
 /* Library ABI version: major*10000 + minor*100 + patch. */
 int32_t vtoken_version(void);
+
+/* The SHA-256 of the sources the library was built from, as 64 lowercase hex digits: over
+ * every file of the package's csrc/ directory and include/vtoken.h, in sorted order of their
+ * paths relative to the repository root, each hashed as its path, a NUL byte, its contents
+ * and a NUL byte (what the package's build script computes and compiles in). "unknown" for a
+ * library built without it. A static string; never NULL. */
+const char* vtoken_build_id(void);
 
 #ifdef __cplusplus
 }

@@ -26,7 +26,7 @@ STATUS = {
     0: "VTOKEN_OK", -1: "VTOKEN_ERR_NULL", -2: "VTOKEN_ERR_SHAPE", -3: "VTOKEN_ERR_CAPACITY",
     -4: "VTOKEN_ERR_HIP", -5: "VTOKEN_ERR_ARGUMENT", -10: "VTOKEN_ERR_BLOCK_RANGE",
     -11: "VTOKEN_ERR_BT_LEN", -12: "VTOKEN_ERR_TOK_LEN", -13: "VTOKEN_ERR_SLOT",
-    -14: "VTOKEN_ERR_LAYOUT",
+    -14: "VTOKEN_ERR_LAYOUT", -15: "VTOKEN_ERR_PLAN_MODE",
 }
 STATUS_CODE = {v: k for k, v in STATUS.items()}
 
@@ -140,6 +140,7 @@ _SIGNATURES = {
     "vtoken_last_hip_error": (ctypes.c_int32, []),
     "vtoken_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
     "vtoken_version": (ctypes.c_int32, []),
+    "vtoken_build_id": (ctypes.c_char_p, []),
 }
 
 _lib = None
@@ -163,6 +164,13 @@ def load_library(path: str = LIB_PATH):
         fn.restype = res
         fn.argtypes = args
     if path == LIB_PATH:
+        # a library built from other sources than this tree's is refused, not run
+        from paper_2608_13263_amd.build import source_sha256
+        built, tree = lib.vtoken_build_id().decode(), source_sha256()
+        if built != tree:
+            raise RuntimeError(f"{path} was built from other sources (build id {built[:16]}, "
+                               f"tree {tree[:16]}): rebuild with "
+                               "`python -m paper_2608_13263_amd.build`")
         _lib = lib
     return lib
 
@@ -265,7 +273,7 @@ class Plan:
         rows = M if inplace else min(f, M)
         return cls(token_slot=e(T), live_count=e(R), admitted=e(R), dst_indptr=e(R + 1),
                    new_bt_indptr=e(R + 1), new_block_ids=e(M),
-                   src_plan=e(rows * block_size), freed_indptr=e(R + 1), counters=e(4),
+                   src_plan=e(rows * block_size), freed_indptr=e(R + 1), counters=e(5),
                    freed=e(M))
 
     def c(self) -> CPlan:

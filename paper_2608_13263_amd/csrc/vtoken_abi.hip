@@ -351,7 +351,8 @@ vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode
   if (D != 32 && D != 64 && D != 128 && D != 256) return VTOKEN_ERR_SHAPE;
   const int64_t need = vtoken_decode_workspace_bytes(num_reqs, d->num_q_heads, cache->head_dim,
                                                      d->max_tokens);
-  if (d->workspace_bytes < need) return VTOKEN_ERR_CAPACITY;
+  if (need < 0) return VTOKEN_ERR_SHAPE;
+  if (need > d->workspace_bytes) return VTOKEN_ERR_CAPACITY;
   vtoken::AttnArgs a;
   a.kv = static_cast<const uint8_t*>(cache->kv);
   a.row_bytes = (int64_t)cache->num_kv_heads * cache->head_dim * cache->elem_bytes;
@@ -379,6 +380,7 @@ vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode
   a.slot_count = d->slot_count;
   return hip_status(vtoken::launch_paged_decode(a, stream));
 }
+
 
 vtoken_status vtoken_plan_partial(const vtoken_cache* cache, const vtoken_batch* batch,
                                   const int32_t* slot_in, const vtoken_planner_params* params,
@@ -507,10 +509,32 @@ const char* vtoken_status_string(int32_t status) {
     case VTOKEN_ERR_TOK_LEN: return "VTOKEN_ERR_TOK_LEN: token range != sequence length";
     case VTOKEN_ERR_SLOT: return "VTOKEN_ERR_SLOT: a live token's slot is invalid for its table";
     case VTOKEN_ERR_LAYOUT: return "VTOKEN_ERR_LAYOUT: a block id is held twice";
+    case VTOKEN_ERR_PLAN_MODE:
+      return "VTOKEN_ERR_PLAN_MODE: the plan was built for the other copy mode";
     default: return "unknown vtoken status";
   }
 }
 
-int32_t vtoken_version(void) { return 112; }
+int32_t vtoken_version(void) { return 200; }
+
+const char* vtoken_build_id(void) {
+#if defined(VTOKEN_SRC_SHA0) && defined(VTOKEN_SRC_SHA1) && defined(VTOKEN_SRC_SHA2) && \
+    defined(VTOKEN_SRC_SHA3)
+  // the four 64-bit words of the sources' SHA-256, as 64 hex digits (a constant string)
+  static const char* id = [] {
+    static char buf[65];
+    const unsigned long long w[4] = {VTOKEN_SRC_SHA0, VTOKEN_SRC_SHA1, VTOKEN_SRC_SHA2,
+                                     VTOKEN_SRC_SHA3};
+    const char* hex = "0123456789abcdef";
+    for (int i = 0; i < 4; ++i)
+      for (int j = 0; j < 16; ++j) buf[16 * i + j] = hex[(w[i] >> (60 - 4 * j)) & 0xF];
+    buf[64] = 0;
+    return buf;
+  }();
+  return id;
+#else
+  return "unknown";
+#endif
+}
 
 }  // extern "C"

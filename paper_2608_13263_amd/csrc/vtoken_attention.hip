@@ -587,14 +587,15 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(AttnArg
   const int r = blockIdx.x / a.num_q_heads;
   if (r >= a.num_reqs) return;
   const int tid = threadIdx.x;
-  const int c = a.slot_count != nullptr ? a.slot_count[r]
-                                        : a.slot_indptr[r + 1] - a.slot_indptr[r];
+  const int s0 = a.slot_indptr[r];
+  const int c = a.slot_count != nullptr ? a.slot_count[r] : a.slot_indptr[r + 1] - s0;
   const int D = a.head_dim;
   const int64_t rs = D + 2;  // record stride
   float* out = a.out + ((int64_t)r * a.num_q_heads + qh) * D;
   const int ns = c <= 0 ? 0 : (c + a.split_tokens - 1) / a.split_tokens;
-  if (ns > a.splits) {
-    // more slots than max_tokens: the splits past the workspace were never computed
+  // a malformed slot range (the split kernel computed nothing for it), or more slots than
+  // max_tokens (the splits past the workspace were never computed): NaN
+  if (s0 < 0 || c < 0 || ns > a.splits) {
     for (int d = tid; d < D; d += kCombineThreads) out[d] = __builtin_nanf("");
     return;
   }

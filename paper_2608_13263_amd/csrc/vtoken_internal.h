@@ -20,6 +20,11 @@ constexpr int kFreeThreads = 256;
 // Copy kernel geometry: 256 threads, each moving 16-byte units.
 constexpr int kCopyThreads = 256;
 
+// The plan's mode word (plan->counters[4]), written by the kernels that build a plan and
+// checked by the copy that consumes it.
+constexpr int32_t kPlanOutOfPlace = 1;   // vtoken_build_token_table, vtoken_plan_partial
+constexpr int32_t kPlanInPlace = 2;      // vtoken_build_token_table_inplace
+
 struct MetaArgs {
   // batch
   const int32_t* seq_lens;
@@ -65,7 +70,7 @@ struct CopyArgs {
   int32_t order;            // 1 plane-major, otherwise block-major work order
   const int32_t* src_plan;
   const int32_t* free_list;
-  const int32_t* counters;
+  int32_t* counters;        // read; the status word is set if the plan's mode does not match
 };
 
 // Arguments of the in-place copy: one workgroup per (request, plane) chain.
@@ -88,7 +93,7 @@ struct InplaceArgs {
   const int32_t* dst_indptr;
   const int32_t* new_bt_indptr;
   const int32_t* admitted;
-  const int32_t* counters;
+  int32_t* counters;        // read; the status word is set if the plan's mode does not match
 };
 
 // Largest chunk (S * row_bytes) the in-place copy stages through LDS.

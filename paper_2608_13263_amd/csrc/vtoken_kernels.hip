@@ -24,6 +24,12 @@ namespace {
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 
+// A copy handed a plan built for the other mode copies nothing and reports it in the status
+// word (first error wins), so the later calls of the pass do nothing either.
+__device__ __forceinline__ void plan_mode_error(int32_t* counters) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) atomicCAS(&counters[3], 0, VTOKEN_ERR_PLAN_MODE);
+}
+
 // Number of set bits of a wave-wide ballot in the lanes below this one.
 __device__ __forceinline__ int lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
@@ -211,6 +217,7 @@ __global__ __launch_bounds__(kAdmitThreads) void admit_kernel(MetaArgs a) {
     a.counters[1] = status == 0 ? n_admitted : 0;
     a.counters[2] = status == 0 ? carry_freed : 0;
     a.counters[3] = status;
+    a.counters[4] = a.inplace ? kPlanInPlace : kPlanOutOfPlace;
   }
 }
 
@@ -341,6 +348,10 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
   constexpr Policy pol = kPolicies[kPolicy];
   constexpr int kRound = kCopyThreads * kV;  // units of one part
   if (a.counters[3] != 0) return;
+  if (a.counters[4] != kPlanOutOfPlace) {
+    plan_mode_error(a.counters);
+    return;
+  }
   int used = a.counters[0];
   used = used < 0 ? 0 : (used > a.max_used ? a.max_used : used);
   if (used == 0) return;
@@ -504,6 +515,10 @@ template <int kV, bool kSmallS, int kStage>
 __global__ __launch_bounds__(kCopyThreads) void repack_inplace_kernel(InplaceArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t stage[];
   if (a.counters[3] != 0) return;
+  if (a.counters[4] != kPlanInPlace) {
+    plan_mode_error(a.counters);
+    return;
+  }
   const int P = a.num_planes;
   const int r = static_cast<int>(blockIdx.x / P);
   const int plane = static_cast<int>(blockIdx.x - (int64_t)r * P);
@@ -632,7 +647,12 @@ __global__ __launch_bounds__(kCopyThreads) void repack_inplace_pipe_kernel(Inpla
   __shared__ int list_s[kChunkBlocks];
   __shared__ int nlist_s;
   __shared__ int r_s;
-  if (a.counters[3] != 0 || a.counters[1] == 0) return;   // error, or nothing admitted
+  if (a.counters[3] != 0) return;
+  if (a.counters[4] != kPlanInPlace) {
+    plan_mode_error(a.counters);
+    return;
+  }
+  if (a.counters[1] == 0) return;   // nothing admitted
   const int P = a.num_planes;
   // longest chains first: workgroup k*P + plane takes the request with the k-th longest
   // chain (ties by index), so the last workgroups to start are short ones and the tail of the

@@ -112,7 +112,10 @@ __global__ __launch_bounds__(256) void pl_clear_kernel(PlannerArgs a) {
     a.refs[i] = 0;
   }
   if (blockIdx.x == 0 && threadIdx.x < 8) a.stats[threadIdx.x] = 0;
-  if (blockIdx.x == 0 && threadIdx.x < 4) a.counters[threadIdx.x] = 0;
+  // the plan's mode word: the partial pass's plan is copied by the out-of-place copy
+  if (blockIdx.x == 0 && threadIdx.x < 5) {
+    a.counters[threadIdx.x] = threadIdx.x == 4 ? kPlanOutOfPlace : 0;
+  }
 }
 
 __global__ __launch_bounds__(256) void pl_count_kernel(PlannerArgs a) {

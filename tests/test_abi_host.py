@@ -42,7 +42,7 @@ def test_status_codes_match_binding():
     for name, code in codes.items():
         assert B.status_string(code).startswith(name)
     assert B.status_string(12345) == "unknown vtoken status"
-    assert B.load_library().vtoken_version() == 112
+    assert B.load_library().vtoken_version() == 200
 
 
 def test_struct_layouts_match_header(tmp_path):
@@ -282,17 +282,11 @@ def test_no_undefined_library_symbols():
 
 
 def test_stream_probe_library_rejects_bad_sizes():
-    """The memory-system probes of `bench.py --mode stream` (a separate library): every entry
+    """The memory-system probes of `bench.py` (bench_probe.hip, bench tooling): every entry
     point is exported and refuses null pointers and sizes its kernels do not cover before any
     launch (no device needed)."""
-    import ctypes
-    from paper_2608_13263_amd.build import PROBE_LIB_PATH
-    lib = ctypes.CDLL(PROBE_LIB_PATH)
-    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
-    lib.vtoken_probe_read.argtypes = [vp, i64, i32, vp, vp]
-    lib.vtoken_probe_write.argtypes = [vp, i64, i32, vp]
-    lib.vtoken_probe_copy.argtypes = [vp, vp, i64, i32, vp]
-    lib.vtoken_probe_head_read.argtypes = [vp, i64, i32, vp, i64, i32, vp, vp]
+    import bench
+    lib = bench.probe_library()
     fake = 1 << 40          # never dereferenced: every call below fails its host checks
     chunk = 32768
     assert lib.vtoken_probe_read(None, chunk, 1, fake, None) == -2
@@ -324,3 +318,26 @@ def test_check_layout_workspace_bytes_and_bad_arguments():
     cache.block_size = 0
     assert call(cache, ws, 20, st) == B.STATUS_CODE["VTOKEN_ERR_SHAPE"]
     assert lib.vtoken_status_string(-14).decode().startswith("VTOKEN_ERR_LAYOUT")
+
+
+def test_build_id_is_the_hash_of_the_sources():
+    """The loaded library carries the SHA-256 of the tree's csrc/ and include/vtoken.h (paths
+    relative to the repository root in sorted order, each hashed as path, NUL, contents,
+    NUL), recomputed here without the build script."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2608_13263_amd", "csrc")
+    paths = [os.path.join("paper_2608_13263_amd", "csrc", f) for f in os.listdir(csrc)
+             if f.endswith((".hip", ".h"))] + [os.path.join("include", "vtoken.h")]
+    h = hashlib.sha256()
+    for rel in sorted(paths):
+        h.update(rel.encode() + b"\0" + open(os.path.join(ROOT, rel), "rb").read() + b"\0")
+    assert B.load_library().vtoken_build_id().decode() == h.hexdigest()
+
+
+def test_binding_refuses_a_library_of_other_sources(tmp_path, monkeypatch):
+    """A library whose build id is not the tree's hash is refused at load time."""
+    from paper_2608_13263_amd import build as Bld
+    monkeypatch.setattr(Bld, "source_sha256", lambda: "0" * 64)
+    monkeypatch.setattr(B, "_lib", None)
+    with pytest.raises(RuntimeError, match="other sources"):
+        B.load_library()

@@ -254,6 +254,41 @@ def test_paged_decode_slot_outside_pool_gives_nan(dtype, G):
 
 
 @pytest.mark.parametrize("dtype,G", [("bf16", 4), ("fp8_e4m3", 8)])
+def test_paged_decode_malformed_slot_indptr_gives_nan(dtype, G):
+    """A request whose slot range is malformed - slot_indptr[r] < 0, which also makes the
+    previous request's count negative - reads no slot and gets NaN rows, also when the
+    workspace still holds a previous call's partials for it; the other requests are exact."""
+    t = torch()
+    B = _B()
+    H, D, S = 2, 128, 16
+    inp = _decode_inputs(dtype, H, D, S, seed=71 + G)
+    sh = inp.shape
+    kv = W.kv_device(sh, inp.num_blocks, 9)
+    orc = oracle_repack_inputs(inp, kv_bytes(kv, sh))
+    cache, _, _, indptr, slots = _device_pass(inp, kv)
+    ref_indptr, ref_slots = slot_mapping(orc.token_slot, inp.tok_indptr, inp.seq_lens)
+    counts = np.diff(ref_indptr)
+    max_tokens = int(counts.max())
+    q = np.random.default_rng(6).standard_normal((inp.num_reqs, H * G, D)).astype(np.float32)
+    qd = t.from_numpy(q).cuda()
+    ws = t.empty(B.decode_workspace_bytes(inp.num_reqs, H * G, D, max_tokens) // 4,
+                 dtype=t.float32, device="cuda")
+    B.paged_decode(cache, qd, indptr, slots, 0, max_tokens, workspace=ws)   # fills ws
+    r = int(np.nonzero(counts[1:] > 600)[0][0]) + 1        # a multi-split request, r >= 1
+    bad_indptr = indptr.clone()
+    bad_indptr[r] = -5
+    _label(f"decode malformed slot_indptr {dtype} G={G}: request {r} (and {r - 1})")
+    out = B.paged_decode(cache, qd, bad_indptr, slots, 0, max_tokens, workspace=ws)
+    got = out.cpu().numpy().astype(np.float64)
+    vals = _values(orc.kv, sh)
+    ref = decode_batch(q, vals[0], vals[1], ref_indptr, ref_slots)
+    good = np.ones(inp.num_reqs, bool)
+    good[[r - 1, r]] = False
+    np.testing.assert_allclose(got[good], ref[good], atol=ATOL, rtol=RTOL)
+    assert np.isnan(got[~good]).all()
+
+
+@pytest.mark.parametrize("dtype,G", [("bf16", 4), ("fp8_e4m3", 8)])
 def test_paged_decode_max_tokens_too_small(dtype, G):
     """max_tokens below a request's slot count: requests whose slots fit the splits it implies
     are exact, the others get NaN rows (never a silently truncated softmax)."""

@@ -156,3 +156,41 @@ def test_inplace_pipelined_many_requests(R):
         masks.append(m)
     full_parity(W.from_masks(masks, shape, free_blocks=0, seed=R), seed=R, inplace=True,
                 variant=4)
+
+
+@pytest.mark.parametrize("built", ["in_place", "out_of_place"])
+def test_copy_rejects_a_plan_of_the_other_mode(built):
+    """A plan carries its mode (counters[4]): the out-of-place copy handed an in-place plan,
+    or the in-place copy handed an out-of-place plan, copies nothing and sets the status word
+    to VTOKEN_ERR_PLAN_MODE; the free call that follows then releases nothing. A plan of the
+    right mode on the same cache is unaffected."""
+    t = torch()
+    from paper_2608_13263_amd import binding as B
+    inp = W.llama3_8b_random(201, num_layers=2, num_reqs=6)
+    sh = inp.shape
+    print(f"[gpu] plan-mode mismatch: {built} plan to the other copy", flush=True)
+    kv = W.kv_device(sh, inp.num_blocks, 11)
+    before = kv.clone()
+    cache = B.KVCache(kv, sh.num_layers, sh.num_kv_heads, sh.head_dim, sh.block_size)
+    batch = B.Batch.from_inputs(inp)
+    plan = B.Plan.allocate(batch, sh.block_size, inplace=True)
+    freed = t.full((max(inp.num_bt_entries, 1),), -9, dtype=t.int32, device="cuda")
+    if built == "in_place":
+        B.build_token_table_inplace(cache, batch, plan)
+        t.cuda.synchronize()
+        assert plan.counters.cpu().tolist()[3:] == [0, 2]
+        B.repack(cache, batch, plan)
+    else:
+        B.build_token_table(cache, batch, plan)
+        t.cuda.synchronize()
+        assert plan.counters.cpu().tolist()[3:] == [0, 1]
+        B.repack_inplace(cache, batch, plan)
+    B.free_blocks(batch, plan, freed=freed)
+    t.cuda.synchronize()
+    assert int(plan.counters[1]) > 0, "the plan admitted requests"
+    assert int(plan.counters[3]) == B.STATUS_CODE["VTOKEN_ERR_PLAN_MODE"]
+    assert t.equal(kv, before), "a mismatched copy wrote KV bytes"
+    assert bool((freed == -9).all()), "blocks were released after the failed copy"
+    # the same cache through the matching copy equals the oracle
+    del before
+    full_parity(inp, seed=11, inplace=built == "in_place")

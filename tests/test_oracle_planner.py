@@ -3,6 +3,7 @@ import os
 import sys
 import types
 
+import numpy as np
 import pytest
 
 import planner_pins
@@ -75,3 +76,44 @@ def test_planner_pins_catch_mutation(name):
         except Exception:
             return
     raise AssertionError(f"no pin catches the planted mistake '{name}'")
+
+
+def test_brute_plan_partial_itself_on_worked_example():
+    """The partial pass's brute-force walk is pinned on its own, not only against
+    plan_partial: every case of the hand-derived example (tests/golden/partial_example.txt)
+    is reproduced output for output, KV moves included."""
+    from oracle.bruteforce import brute_plan_partial
+    head, cases = planner_pins.read_partial_golden()
+    S, nb = int(head["block_size"][0]), int(head["num_blocks"][0])
+    masks = [r["live"] for r in head["req"]]
+    slots = [r["slots"] for r in head["req"]]
+    tables = [r["table"] for r in head["req"]]
+    free = [int(x) for x in head["free_list"]]
+    pinned = [int(x) for x in head["pinned"]]
+    planes = [{s: bytes([s % 251, p]) for s in range(nb * S)} for p in range(2)]
+    ints = lambda c, k: [int(x) for x in c[k]]  # noqa: E731
+    for c in cases:
+        tag = f"brute force, partial example {c['name']}"
+        bf = brute_plan_partial([len(m) for m in masks], tables, masks, slots, free, S,
+                                theta=c["theta"], max_sources=c["B"],
+                                min_eligible=c["min_eligible"], free_watermark=c["watermark"],
+                                pinned=pinned, planes=planes)
+        assert int(bf["triggered"]) == int(c["triggered"][0]), f"{tag}: triggered"
+        assert bf["used"] == int(c["used"][0]), f"{tag}: used"
+        flat = {"admitted": bf["admitted"], "src_count": bf["chosen"],
+                "token_slot": [s for req in bf["token_slot"] for s in req],
+                "src_plan": bf["src_plan"], "freed": bf["freed"],
+                "new_block_ids": [b for t in bf["new_tables"] for b in t]}
+        for key, got in flat.items():
+            if key in c:
+                assert [int(x) for x in got] == ints(c, key), f"{tag}: {key}"
+        if "new_bt_indptr" in c:
+            lens = [0] + [len(t) for t in bf["new_tables"]]
+            assert list(np.cumsum(lens)) == ints(c, "new_bt_indptr"), f"{tag}: new tables"
+        if "moves" in c:
+            expect = [dict(p) for p in planes]
+            for mv in c["moves"]:
+                old, new = (int(x) for x in mv.split(":"))
+                for p in range(2):
+                    expect[p][new] = planes[p][old]
+            assert bf["planes"] == expect, f"{tag}: KV moves"

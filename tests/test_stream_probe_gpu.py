@@ -1,4 +1,4 @@
-"""The memory-system probes of `bench.py --mode stream` (libvtoken_probe.so) do the work
+"""The memory-system probes of `bench.py` (bench_probe.hip, built on demand) do the work
 their rates are counted on: the copy reproduces its source in both work orders, the write
 fills every chunk with its (thread, workgroup) pattern, and the read kernels leave their
 sink untouched on zero-filled input. Small buffers (64 MiB), the same kernels and
@@ -16,14 +16,8 @@ CHUNK = 32768
 
 
 def _lib():
-    from paper_2608_13263_amd.build import PROBE_LIB_PATH
-    lib = ctypes.CDLL(PROBE_LIB_PATH)
-    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
-    lib.vtoken_probe_read.argtypes = [vp, i64, i32, vp, vp]
-    lib.vtoken_probe_write.argtypes = [vp, i64, i32, vp]
-    lib.vtoken_probe_copy.argtypes = [vp, vp, i64, i32, vp]
-    lib.vtoken_probe_head_read.argtypes = [vp, i64, i32, vp, i64, i32, vp, vp]
-    return lib
+    import bench
+    return bench.probe_library()
 
 
 def _stream():
