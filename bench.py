@@ -16,10 +16,17 @@ their destinations and 1024 spare blocks, 56 GiB).
 Prints one JSON line. `value` is repacked KV GB/s over the whole step (read+write bytes of
 the live rows: 2 * live tokens * 2*L*H*D*elem_bytes); `roofline` prices the repack kernel
 alone against the 8 TB/s HBM peak, timed with HIP events on its launch stream (the build and
-free calls are timed separately); `ceiling` is torch's device copy timed in the same run
-and, with --ceiling all, the same repack kernel copying whole contiguous blocks of the same
-pool (the practical streaming rate); `cpu_baseline` is the CPU oracle on a sample of the
-planes.
+free calls are timed separately) and to the practical ceiling measured in the same run:
+`ceiling` holds the streaming probe's copy over the pass's bytes in the same pool (the best
+copy pattern measured on this memory system), torch's device copy and, with --ceiling all,
+the repack kernel copying whole contiguous blocks of the same pool; `cpu_baseline` is the CPU
+oracle on a sample of the planes.
+
+--config llama3_70b_h2o runs a round of waves: the Llama-3-70B batch does not get all its
+destinations from the free list at once, so each pass defers requests, its outputs are
+applied and the batch re-submitted until none is left deferred; every wave's pass is replayed
+--steps times (idempotent on unchanged inputs) and the line reports the round's bytes over the
+sum of the waves' times.
 
     python bench.py [--steps K] [--warmup W] [--config NAME] [--variant V] [--grid G]
     python bench.py --mode copy      # plain device-to-device copy of known size
@@ -63,8 +70,9 @@ def parse_args(argv=None):
                     help="70B config: KV heads in the cache (1 = one GPU's share under 8-way "
                          "tensor parallelism: 256 B / 128 B rows)")
     ap.add_argument("--ceiling", default="copy", choices=["none", "copy", "all"],
-                    help="practical-ceiling leg after the timed steps: copy = torch's device "
-                         "copy of 4 GiB (another kernel); all = also the repack kernel on "
+                    help="practical-ceiling leg after the timed steps: copy = the streaming "
+                         "probe's copy over the pass's bytes in the same pool (another kernel) "
+                         "and torch's device copy of 4 GiB; all = also the repack kernel on "
                          "whole contiguous blocks of the same pool (adds launches of the "
                          "timed kernel, so a profile of the run would mix the two)")
     ap.add_argument("--variant", type=int, default=0)
@@ -84,13 +92,14 @@ def parse_args(argv=None):
                     help="in-place mode: destinations are each request's own leading blocks; "
                          "bytes count only the rows that move")
     ap.add_argument("--mode", default="repack",
-                    choices=["repack", "copy", "decode", "overlap", "stream"],
+                    choices=["repack", "copy", "decode", "overlap", "stream", "placement"],
                     help="decode: the consumer side, paged decode attention of every layer "
                          "through the slot mapping, before and after the repack; overlap: a "
                          "decode step (every layer) on the main stream with the repack pass on "
                          "a relocation stream, against the two one after the other; stream: "
                          "read / write / copy and decode-pattern probes, the memory system's "
-                         "streaming ceilings")
+                         "streaming ceilings; placement: the minimal 56 GiB pool allocated twice, "
+                         "repack and write / read probes on each (for counter runs)")
     ap.add_argument("--q-heads", type=int, default=32, help="decode mode: query heads")
     ap.add_argument("--copy-gib", type=float, default=8.0)
     ap.add_argument("--graph", action="store_true",
@@ -329,12 +338,15 @@ def inputs_sha256(inp) -> dict:
 
 def streaming_ceiling(args, inp, kv, cache, bytes_alg: int, stream, block_copy: bool,
                       steps: int = 10):
-    """The copy's practical ceiling, timed in the same run: torch's device copy of 4 GiB when
-    that much HBM is still free, and with `block_copy` the repack kernel on whole contiguous
-    blocks (block-copy metadata over the same KV tensor, about the same bytes). Runs after the
-    timed steps (the block copy overwrites blocks of the pool; the copy is value-agnostic)."""
+    """The copy's practical ceiling, timed in the same run after the timed steps: the streaming
+    probe's copy (bench_probe.hip; consecutive workgroups 64 chunks apart, the best copy pattern
+    measured) over about the pass's bytes inside the same KV pool; torch's device copy of 4 GiB
+    when that much HBM is still free (a library copy, for reference); with `block_copy` the
+    repack kernel on whole contiguous blocks (block-copy metadata over the same KV tensor,
+    which adds launches of the timed kernel to a profile of the run). The copies overwrite
+    bytes of the pool; the copy is value-agnostic."""
     import torch
-    out = {}
+    out = probe_copy_ceiling(kv, bytes_alg, stream, steps)
     if block_copy:
         out.update(block_copy_ceiling(inp, cache, bytes_alg, stream, steps))
     free, _ = torch.cuda.mem_get_info()
@@ -356,6 +368,39 @@ def streaming_ceiling(args, inp, kv, cache, bytes_alg: int, stream, block_copy: 
         del src, dst
     log(f"ceiling: {out}")
     return out
+
+
+def probe_copy_ceiling(kv, bytes_alg: int, stream, steps: int = 10):
+    """The probe copy (64 chunks apart) of about half the pass's bytes from the first half of
+    the KV tensor to its second half: read + write bytes per second."""
+    import ctypes
+    import torch
+    lib = probe_library()
+    chunk = 32768
+    total = kv.numel() * kv.element_size()
+    unit = 1024 * chunk                      # every interleave divides the chunk count
+    region = min(bytes_alg // 2, total // 2) // unit * unit
+    if region == 0:
+        return {}
+    src = kv.data_ptr()
+    dst = kv.data_ptr() + (total // 2) // chunk * chunk
+    sh = ctypes.c_void_p(stream.cuda_stream)
+    for _ in range(3):
+        if lib.vtoken_probe_copy(src, dst, region, 64, sh) != 0:
+            raise SystemExit("probe copy refused its arguments")
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    for a, b in evs:
+        a.record(stream)
+        lib.vtoken_probe_copy(src, dst, region, 64, sh)
+        b.record(stream)
+    torch.cuda.synchronize()
+    ms = sum(a.elapsed_time(b) for a, b in evs) / steps
+    gbs = 2 * region / (ms / 1e3) / 1e9
+    return {"probe_copy": "bench_probe.hip copy_kernel, workgroups 64 chunks apart, non-temporal "
+                          "loads, sc1 stores, in the same KV pool",
+            "probe_copy_bytes": 2 * region, "probe_copy_ms": round(ms, 4),
+            "probe_copy_GBps": round(gbs, 1), "probe_copy_frac": round(gbs / HBM_PEAK_GBS, 4)}
 
 
 def block_copy_ceiling(inp, cache, bytes_alg: int, stream, steps: int):
@@ -505,6 +550,78 @@ def run_stream(args):
            "config": {"workload": "stream_probes", "pool_gib": round(buf.numel() / 2 ** 30, 1),
                       "region_gib": round(region / 2 ** 30, 2), "chunk_bytes": chunk,
                       "decode_pattern": f"{tokens} tokens x 8 heads x 256 B, K and V planes"}}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def run_placement(args):
+    """The Llama-3-8B Random requests in the minimal pool (their blocks, their destinations and
+    1024 spare blocks: 56 GiB), allocated twice in one process (both held; consecutive
+    allocations of this size land on placements of two speeds). On each pool, in this order:
+    the repack pass (--warmup + --steps, the copy timed with HIP events), the probe write of
+    half the pass's bytes (64 chunks apart, the copy's store pattern), the probe read of the
+    same bytes. Run under rocprofv3 --pmc, the dispatches of the first pool come before those
+    of the second, so counters can be set side by side per placement."""
+    import ctypes
+    import torch
+    from paper_2608_13263_amd import binding as B
+    from paper_2608_13263_amd import workloads as W
+    lib = probe_library()
+    inp = W.llama3_8b_random(args.seed if args.seed is not None else 201)
+    sh = inp.shape
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    batch = B.Batch.from_inputs(inp)
+    pools, kvs = [], []
+    chunk, unit = 32768, 1024 * 32768
+
+    def timed(fn, n):
+        for _ in range(max(args.warmup, 1)):
+            fn()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(n)]
+        for a, b in evs:
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return sum(a.elapsed_time(b) for a, b in evs) / n
+
+    for k in range(2):
+        kv = W.kv_device(sh, inp.num_blocks, 1 + k)
+        kvs.append(kv)
+        cache = B.KVCache(kv, sh.num_layers, sh.num_kv_heads, sh.head_dim, sh.block_size)
+        plan = B.Plan.allocate(batch, sh.block_size)
+        B.build_token_table(cache, batch, plan, stream)
+        torch.cuda.synchronize()
+        log(f"pool {k}: {inp.pool_bytes() / 2**30:.1f} GiB at {kv.data_ptr():#x}")
+        ms = timed(lambda: B.repack(cache, batch, plan, stream), args.steps)
+        cnt = plan.counters.cpu().tolist()
+        if cnt[3] != 0:
+            raise SystemExit(f"device status {B.STATUS.get(cnt[3], cnt[3])}")
+        moved = int((plan.live_count[:inp.num_reqs].long() *
+                     plan.admitted[:inp.num_reqs].long()).sum())
+        bytes_alg = 2 * moved * sh.token_bytes
+        total = kv.numel() * kv.element_size()
+        region = min(bytes_alg // 2, total // 2) // unit * unit
+        dst = kv.data_ptr() + (total // 2) // chunk * chunk
+        sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+        w_ms = timed(lambda: lib.vtoken_probe_write(dst, region, 64, sp), max(args.steps // 2, 3))
+        r_ms = timed(lambda: lib.vtoken_probe_read(kv.data_ptr(), region, 1, sink.data_ptr(), sp),
+                     max(args.steps // 2, 3))
+        pools.append({"pool": k, "address": hex(kv.data_ptr()), "repack_ms": round(ms, 4),
+                      "repack_GBps": round(bytes_alg / (ms / 1e3) / 1e9, 1),
+                      "repack_frac": round(bytes_alg / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                      "probe_write_GBps": round(region / (w_ms / 1e3) / 1e9, 1),
+                      "probe_read_GBps": round(region / (r_ms / 1e3) / 1e9, 1),
+                      "bytes_alg": bytes_alg, "probe_bytes": region})
+        log(f"pool {k}: {pools[-1]}")
+    out = {"metric": "repack and probe rates on two 56 GiB placements", "mode": "placement",
+           "value": min(p["repack_GBps"] for p in pools), "unit": "GB/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
+           "data": "synthetic", "pools": pools,
+           "config": {"workload": inp.name, "recipe": inp.note,
+                      "pool_gib": round(inp.pool_bytes() / 2 ** 30, 2)}}
     print(json.dumps(out), flush=True)
     return 0
 
@@ -801,6 +918,119 @@ def run_partial_pass(args):
     return 0
 
 
+def run_waves(args, inp, kv, cache, stream):
+    """One round of waves over the batch: pass, apply its outputs (W.next_wave), re-submit,
+    until no profitable request is left deferred. Each wave's pass (build, copy, free) is
+    replayed `warmup` + `steps` times on unchanged inputs (the same plan and the same rows
+    between the same addresses each time) with HIP events on the launch stream; then its
+    outputs are read back and applied."""
+    import numpy as np
+    import torch
+    from paper_2608_13263_amd import binding as B
+    from paper_2608_13263_amd import workloads as W
+    sh = inp.shape
+    S = sh.block_size
+    first = inp
+    waves = []
+    for wave in range(64):
+        batch = B.Batch.from_inputs(inp)
+        plan = B.Plan.allocate(batch, S)
+
+        def step(ev=None):
+            if ev is not None:
+                ev[0].record(stream)
+            B.build_token_table(cache, batch, plan, stream)
+            if ev is not None:
+                ev[1].record(stream)
+            B.repack_ex(cache, batch, plan, args.variant, args.grid, args.order, stream)
+            if ev is not None:
+                ev[2].record(stream)
+            B.free_blocks(batch, plan, stream=stream)
+            if ev is not None:
+                ev[3].record(stream)
+
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4))
+               for _ in range(args.steps)]
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            step(evs[i])
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t0) * 1e3 / args.steps
+        cnt = plan.counters.cpu().tolist()
+        if cnt[3] != 0:
+            raise SystemExit(f"wave {wave}: device status {B.STATUS.get(cnt[3], cnt[3])}")
+        R = inp.num_reqs
+        adm = plan.admitted[:R].cpu().numpy()
+        live = plan.live_count[:R].cpu().numpy().astype(np.int64)
+        nbi = plan.new_bt_indptr[:R + 1].cpu().numpy()
+        nbids = plan.new_block_ids[:int(nbi[-1])].cpu().numpy()
+        freed = plan.freed[:cnt[2]].cpu().numpy()
+        m = np.diff(inp.bt_indptr.astype(np.int64))
+        profitable = -(-live // S) < m
+        moved = int((live * adm).sum())
+        waves.append(dict(
+            admitted=cnt[1], deferred=int((profitable & (adm == 0)).sum()),
+            live_tokens_moved=moved, bytes_alg=2 * moved * sh.token_bytes,
+            destinations=cnt[0], freed_blocks=cnt[2], free_list=len(inp.free_list),
+            step_ms=round(wall, 4),
+            repack_ms=round(sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps, 4),
+            build_ms=round(sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps, 4),
+            free_ms=round(sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps, 4)))
+        w = waves[-1]
+        log(f"wave {wave}: {w['admitted']} admitted, {w['deferred']} deferred, "
+            f"{moved} live tokens, {w['repack_ms']:.3f} ms copy, {w['step_ms']:.3f} ms pass")
+        if w["deferred"] == 0:
+            break
+        if cnt[1] == 0:
+            raise SystemExit(f"wave {wave}: requests deferred but none admitted")
+        inp = W.next_wave(inp, adm, live, nbi, nbids, cnt[0], freed)
+    bytes_alg = sum(w["bytes_alg"] for w in waves)
+    moved = sum(w["live_tokens_moved"] for w in waves)
+    step_ms = sum(w["step_ms"] for w in waves)
+    repack_ms = sum(w["repack_ms"] for w in waves)
+    value = bytes_alg / (step_ms / 1e3) / 1e9
+    achieved = bytes_alg / (repack_ms / 1e3) / 1e9
+    ceiling = None
+    if args.ceiling != "none":
+        ceiling = streaming_ceiling(args, inp, kv, cache, waves[0]["bytes_alg"], stream,
+                                    block_copy=False)
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"CPU oracle on {args.cpu_planes} planes of the first wave")
+        cpu = cpu_baseline(first, args.cpu_planes)
+    out = {
+        "metric": "repacked KV GB/s (read+write) as % of HBM peak; live tokens repacked/ms",
+        "mode": "waves", "value": round(value, 2), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u8",
+        "data": "synthetic", "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "live_tokens_per_ms": round(moved / step_ms, 1), "repack_ms": round(repack_ms, 4),
+        "config": {"workload": first.name, "recipe": first.note,
+                   "round": "one step = every wave of the round (pass, outputs applied, "
+                            "re-submitted) until no request is deferred",
+                   "layers": sh.num_layers, "kv_heads": sh.num_kv_heads,
+                   "head_dim": sh.head_dim, "block_size": S, "kv_dtype": sh.dtype,
+                   "requests": first.num_reqs, "tokens": first.num_tokens,
+                   "pool_blocks": first.num_blocks,
+                   "pool_gib": round(first.pool_bytes() / 2 ** 30, 2),
+                   "live_tokens_repacked": moved, "bytes_alg_per_step": bytes_alg,
+                   "waves": waves, "inputs_sha256": inputs_sha256(first)},
+        "roofline": {"bound": "hbm", "kernel": "repack_direct_kernel",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "practical_ceiling": (ceiling or {}).get("probe_copy_GBps"),
+                     "frac_of_practical_ceiling":
+                         round(achieved / ceiling["probe_copy_GBps"], 4)
+                         if ceiling and ceiling.get("probe_copy_GBps") else None},
+        "ceiling": ceiling, "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def run_inplace(args, inp, kv, cache, batch, plan, stream):
     """In-place mode. The pass is re-run on the same inputs: every step computes the same
     plan and moves the same rows between the same addresses (after the first step the bytes
@@ -1038,6 +1268,52 @@ def run_overlap(args, inp, kv, cache, batch, plan, stream):
     repack_ms = timed(lambda: repack_pass(stream))
     serial_ms = timed(lambda: (decode_step(stream), repack_pass(stream)))
     overlap_ms = timed(concurrent)
+
+    # decode latency under a concurrent copy: the copy (its grid capped at `cap` workgroups,
+    # a grid-stride loop covering the rest) starts on the relocation stream, the decode step
+    # on the main stream right after; events on both streams time each one and the pair
+    def under_copy(cap):
+        B.build_token_table(cache, batch, plan, reloc)
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        alone = []
+        for i in range(args.warmup + args.steps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(reloc)
+            B.repack_ex(cache, batch, plan, 0, cap, 0, reloc)
+            b.record(reloc)
+            torch.cuda.synchronize()
+            if i >= args.warmup:
+                alone.append(a.elapsed_time(b))
+        dec, cop, both = [], [], []
+        for i in range(args.warmup + args.steps):
+            torch.cuda.synchronize()
+            ev[0].record(reloc)
+            B.repack_ex(cache, batch, plan, 0, cap, 0, reloc)
+            ev[1].record(reloc)
+            ev[2].record(stream)
+            decode_step(stream)
+            ev[3].record(stream)
+            torch.cuda.synchronize()
+            if i >= args.warmup:
+                dec.append(ev[2].elapsed_time(ev[3]))
+                cop.append(ev[0].elapsed_time(ev[1]))
+                both.append(max(ev[0].elapsed_time(ev[1]), ev[0].elapsed_time(ev[3])))
+        mean = lambda x: sum(x) / len(x)  # noqa: E731
+        return {"grid_cap": cap or 1 << 19, "copy_alone_ms": round(mean(alone), 4),
+                "decode_alone_ms": round(decode_ms, 4),
+                "decode_with_copy_ms": round(mean(dec), 4),
+                "copy_with_decode_ms": round(mean(cop), 4),
+                "together_ms": round(mean(both), 4),
+                "decode_slowdown": round(mean(dec) / decode_ms, 3),
+                "copy_slowdown": round(mean(cop) / mean(alone), 3)}
+
+    caps = [0, 1 << 15, 1 << 12, 1 << 10, 1 << 8]
+    sweep = [under_copy(c) for c in caps]
+    for row in sweep:
+        log(f"copy grid cap {row['grid_cap']}: copy alone {row['copy_alone_ms']:.3f} ms, decode "
+            f"{row['decode_alone_ms']:.3f} -> {row['decode_with_copy_ms']:.3f} ms beside the "
+            f"copy ({row['copy_with_decode_ms']:.3f} ms), both {row['together_ms']:.3f} ms")
     cnt = plan.counters.cpu().tolist()
     if cnt[3] != 0:
         raise SystemExit(f"device status {B.STATUS.get(cnt[3], cnt[3])}")
@@ -1056,6 +1332,7 @@ def run_overlap(args, inp, kv, cache, batch, plan, stream):
         "serial_ms": round(serial_ms, 4), "overlap_ms": round(overlap_ms, 4),
         "serial_GBps": round(total / (serial_ms / 1e3) / 1e9, 1),
         "overlap_saving": round(1 - overlap_ms / serial_ms, 4),
+        "decode_under_copy": sweep,
         "roofline": {"bound": "hbm", "kernel": "decode split + combine and repack_direct_kernel",
                      "achieved": round(total / (overlap_ms / 1e3) / 1e9, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -1085,6 +1362,8 @@ def main(argv=None):
         return run_copy(args)
     if args.mode == "stream":
         return run_stream(args)
+    if args.mode == "placement":
+        return run_placement(args)
     if args.config == "llama3_8b_scissorhands":
         return run_partial_stream(args) if args.partial else run_scissorhands(args)
     if args.config == "llama3_8b_shared_prefix":
@@ -1107,6 +1386,8 @@ def main(argv=None):
         return run_decode(args, inp, kv, cache, batch, plan, stream)
     if args.mode == "overlap":
         return run_overlap(args, inp, kv, cache, batch, plan, stream)
+    if args.config == "llama3_70b_h2o":
+        return run_waves(args, inp, kv, cache, stream)
     torch.cuda.synchronize()
     log(f"setup {time.perf_counter() - t_setup:.1f} s; warmup {args.warmup} steps")
 
@@ -1203,6 +1484,9 @@ def main(argv=None):
             "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
+            "practical_ceiling": (ceiling or {}).get("probe_copy_GBps"),
+            "frac_of_practical_ceiling": round(achieved / ceiling["probe_copy_GBps"], 4)
+            if ceiling and ceiling.get("probe_copy_GBps") else None,
         },
         "ceiling": ceiling,
         "cpu_baseline": cpu,

@@ -20,8 +20,8 @@ ROOT = os.path.dirname(HERE)
 LIB_PATH = os.path.join(HERE, "libvtoken.so")
 CSRC = os.path.join(HERE, "csrc")
 SOURCES = [os.path.join(CSRC, f)
-           for f in ("vtoken_abi.hip", "vtoken_kernels.hip", "vtoken_attention.hip",
-                     "vtoken_planner.hip", "vtoken_layout.hip")]
+           for f in ("vtoken_abi.hip", "vtoken_kernels.hip", "vtoken_copy.hip",
+                     "vtoken_attention.hip", "vtoken_planner.hip", "vtoken_layout.hip")]
 HEADERS = [os.path.join(ROOT, "include", "vtoken.h"), os.path.join(CSRC, "vtoken_internal.h")]
 ARCH = "gfx950"
 

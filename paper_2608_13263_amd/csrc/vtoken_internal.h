@@ -1,4 +1,5 @@
-// Internal declarations shared by the kernels (vtoken_kernels.hip) and the C ABI front end
+// Internal declarations shared by the kernels (vtoken_kernels.hip, vtoken_copy.hip,
+// vtoken_attention.hip, vtoken_planner.hip, vtoken_layout.hip) and the C ABI front end
 // (vtoken_abi.hip). Not installed; the public interface is include/vtoken.h.
 #pragma once
 
@@ -9,12 +10,11 @@
 
 namespace vtoken {
 
-// Launch geometry of the metadata kernels.
-constexpr int kScanThreads = 1024;              // one workgroup per request
-constexpr int kScanWaves = kScanThreads / 64;   // wave64 on CDNA4
-constexpr int kScanBallots = 8;                 // ballots per wave per tile
-constexpr int kScanTile = kScanThreads * kScanBallots;  // tokens per tile (8192)
-constexpr int kAdmitThreads = 1024;             // single workgroup over requests
+// Launch geometry of the metadata kernels (one workgroup per request each).
+constexpr int kCountThreads = 256;
+constexpr int kPlanThreads = 1024;
+constexpr int kPlanBallots = 8;                            // ballots per wave per tile
+constexpr int kPlanTile = kPlanThreads * kPlanBallots;     // tokens per tile (8192)
 constexpr int kFreeThreads = 256;
 
 // Copy kernel geometry: 256 threads, each moving 16-byte units.

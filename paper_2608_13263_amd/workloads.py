@@ -33,6 +33,7 @@ __all__ = [
     "llama3_8b_h2o",
     "llama3_70b_h2o",
     "ScissorhandsStream",
+    "next_wave",
     "kv_host",
     "kv_device",
     "bernoulli_live",
@@ -293,6 +294,45 @@ def llama3_70b_h2o(seed: int = 501, keep: float = 0.3, dtype: str = "fp8_e4m3",
                      pool_blocks - used, seed,
                      f"{dtype} {num_layers}x{num_kv_heads}x128, S=32, {keep_n} of {num_reqs} "
                      f"req U{list(len_range)}, H2O keep {keep} + last {recent}")
+
+
+def next_wave(inp: RepackInputs, admitted, live_count, new_bt_indptr, new_block_ids,
+              used: int, freed) -> RepackInputs:
+    """The caller's side between two passes over one batch ("waves"): apply a pass's outputs
+    and re-submit. A repacked request keeps only its live tokens, in order, all live, in its
+    new block table; every other request is unchanged; the free list becomes the unconsumed
+    entries followed by the freed blocks. A pool too small for every destination at once
+    defers the later requests (prefix admission) to the next wave."""
+    R = inp.num_reqs
+    admitted = np.asarray(admitted)[:R]
+    live_count = np.asarray(live_count, dtype=np.int64)[:R]
+    new_bt_indptr = np.asarray(new_bt_indptr, dtype=np.int64)
+    new_block_ids = np.asarray(new_block_ids, dtype=np.int32)
+    lens, masks, tables = [], [], []
+    for r in range(R):
+        if admitted[r]:
+            n = int(live_count[r])
+            lens.append(n)
+            masks.append(np.ones(n, dtype=np.uint8))
+            tables.append(new_block_ids[new_bt_indptr[r]:new_bt_indptr[r + 1]])
+        else:
+            lens.append(int(inp.seq_lens[r]))
+            masks.append(inp.request_live(r))
+            tables.append(inp.request_blocks(r))
+    seq_lens = np.asarray(lens, dtype=np.int64)
+    tok_indptr = np.zeros(R + 1, dtype=np.int64)
+    tok_indptr[1:] = np.cumsum(seq_lens)
+    bt_indptr = np.zeros(R + 1, dtype=np.int64)
+    bt_indptr[1:] = np.cumsum([len(t) for t in tables])
+    free = np.concatenate([np.asarray(inp.free_list, dtype=np.int32)[int(used):],
+                           np.asarray(freed, dtype=np.int32)])
+    return RepackInputs(
+        name=inp.name, shape=inp.shape, num_blocks=inp.num_blocks,
+        seq_lens=seq_lens.astype(np.int32), tok_indptr=tok_indptr.astype(np.int32),
+        bt_indptr=bt_indptr.astype(np.int32),
+        block_ids=(np.concatenate(tables) if tables else np.zeros(0)).astype(np.int32),
+        live=(np.concatenate(masks) if masks else np.zeros(0)).astype(np.uint8),
+        free_list=free.astype(np.int32), seed=inp.seed, note=inp.note)
 
 
 def from_masks(masks: Sequence[Sequence[int]], shape: KVShape, free_blocks: int,

@@ -107,3 +107,50 @@ def test_slot_limit_inputs(S, top):
     assert (inp.block_ids[0] if top == "source" else inp.free_list[0]) == nb - 1
     with pytest.raises(ValueError):
         W.slot_limit_inputs(inp.shape, masks, seed=5, top_block="middle")
+
+
+@pytest.mark.parametrize("keep", [0.1, 0.3, 0.6])
+def test_waves_pack_every_request(keep):
+    """Passes over one batch with a pool too small for every destination at once (the
+    Llama-3-70B recipe's deferral, Sec. 3.3.2), each re-submitted through next_wave: the first
+    pass defers requests, each later pass admits a prefix of the deferred ones, and when a pass
+    admits nothing every request holds exactly ceil(live/S) blocks. Blocks are conserved and
+    each request's live rows (tracked as bytes through every pass) keep their logical order."""
+    shape = W.KVShape(1, 1, 8, 8, "fp16")           # 16-byte rows
+    inp = W.llama3_70b_h2o(501, keep=keep, dtype="fp16", num_layers=1, num_kv_heads=1,
+                           len_range=(200, 900), num_reqs=12, resident_frac=0.75)
+    inp = W.RepackInputs(**{**inp.__dict__, "shape": W.KVShape(1, 1, 8, 32, "fp16")})
+    S = inp.shape.block_size
+    rng = np.random.default_rng(1)
+    kv = rng.integers(0, 256, size=(2, inp.num_blocks * S, 16), dtype=np.uint8)
+    # each live token's payload before any pass, in logical order per request
+    want = []
+    for r in range(inp.num_reqs):
+        p = np.nonzero(inp.request_live(r))[0]
+        bt = inp.request_blocks(r).astype(np.int64)
+        want.append(kv[:, bt[p // S] * S + p % S].copy())
+    # keep only the free blocks the first pass's deferral needs: about half the destinations
+    need0 = sum(-(-int(inp.request_live(r).sum()) // S) for r in range(inp.num_reqs))
+    inp = W.RepackInputs(**{**inp.__dict__, "free_list": inp.free_list[:max(need0 // 2, 1)]})
+    pool = set(inp.block_ids.tolist()) | set(inp.free_list.tolist())
+    profitable = sum(-(-int(inp.request_live(r).sum()) // S) < len(inp.request_blocks(r))
+                     for r in range(inp.num_reqs))
+    admitted_per_wave = []
+    for wave in range(64):
+        res = oracle_repack_inputs(inp, kv)
+        kv = res.kv
+        admitted_per_wave.append(int(res.n_admitted))
+        if res.n_admitted == 0:
+            break
+        inp = W.next_wave(inp, res.admitted, res.live_count, res.new_bt_indptr,
+                          res.new_block_ids, res.used, res.freed)
+        assert set(inp.block_ids.tolist()) | set(inp.free_list.tolist()) == pool
+        assert len(inp.block_ids) + len(inp.free_list) == len(pool)
+    assert admitted_per_wave[0] < profitable and len(admitted_per_wave) > 2, admitted_per_wave
+    assert sum(admitted_per_wave) == profitable
+    for r in range(inp.num_reqs):
+        c = int(inp.request_live(r).sum())
+        assert inp.request_live(r).all() and len(inp.request_blocks(r)) == -(-c // S)
+        bt = inp.request_blocks(r).astype(np.int64)
+        p = np.arange(c)
+        assert np.array_equal(kv[:, bt[p // S] * S + p % S], want[r]), f"request {r}"
