@@ -384,6 +384,26 @@ vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode
                                   int32_t num_reqs, const int32_t* slot_indptr,
                                   const int32_t* slots, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, serving loops
+ * or harnesses that forbid hipMalloc): vtoken_paged_decode with its split partials in a
+ * workspace the library holds - a static device array of VTOKEN_DECODE_SCRATCH_BYTES on every
+ * GPU the library runs on, kept until the process ends - instead of decode->workspace
+ * (decode->workspace and decode->workspace_bytes are ignored). Same arguments, kernels and
+ * results as vtoken_paged_decode otherwise. Calls no hipMalloc, hipFree or other allocating
+ * routine: the first call on a device looks the array's address up on the device of `stream`
+ * (hipGetSymbolAddress, with that device made current for the lookup) and keeps it.
+ * Limit: vtoken_decode_workspace_bytes(num_reqs, num_q_heads, head_dim, max_tokens) must not
+ * exceed VTOKEN_DECODE_SCRATCH_BYTES; a larger call returns VTOKEN_ERR_CAPACITY and enqueues
+ * nothing. Every call on one GPU shares that GPU's array, which keeps the last call's
+ * partials (the decode writes every partial it reads, so nothing needs clearing): calls on one
+ * GPU must be stream-ordered with respect to each other - calls that may overlap (different
+ * streams without an event between them) race on the array and give wrong outputs. */
+#define VTOKEN_DECODE_SCRATCH_BYTES (64LL << 20)
+vtoken_status vtoken_paged_decode_noalloc(const vtoken_cache* cache,
+                                          const vtoken_decode* decode, int32_t num_reqs,
+                                          const int32_t* slot_indptr, const int32_t* slots,
+                                          hipStream_t stream);
+
 /* The hipError_t behind the calling thread's most recent VTOKEN_ERR_HIP (0 if none yet). */
 int32_t vtoken_last_hip_error(void);
 

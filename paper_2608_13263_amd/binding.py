@@ -133,6 +133,10 @@ _SIGNATURES = {
     "vtoken_paged_decode": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CDecode),
                                              ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                              ctypes.c_void_p]),
+    "vtoken_paged_decode_noalloc": (ctypes.c_int32, [ctypes.POINTER(CCache),
+                                                     ctypes.POINTER(CDecode), ctypes.c_int32,
+                                                     ctypes.c_void_p, ctypes.c_void_p,
+                                                     ctypes.c_void_p]),
     "vtoken_plan_partial": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
                                              ctypes.c_void_p, ctypes.POINTER(CPlannerParams),
                                              ctypes.POINTER(CPlannerState),
@@ -470,6 +474,34 @@ def paged_decode(cache: KVCache, q, slot_indptr, slots, layer: int, max_tokens: 
     c = cache.c()
     _check(lib.vtoken_paged_decode(ctypes.byref(c), ctypes.byref(d), R, _ptr(slot_indptr),
                                    _ptr(slots), _stream(stream)), "vtoken_paged_decode")
+    return out
+
+
+DECODE_SCRATCH_BYTES = 64 << 20   # VTOKEN_DECODE_SCRATCH_BYTES
+
+
+def paged_decode_noalloc(cache: KVCache, q, slot_indptr, slots, layer: int, max_tokens: int,
+                         out, scale: Optional[float] = None, kv_dtype=None, stream=None,
+                         slot_count=None):
+    """paged_decode with the split partials in the library-held array
+    (vtoken_paged_decode_noalloc): `out` is the caller's, nothing is allocated. Calls on one
+    GPU must be stream-ordered (they share the array)."""
+    import torch
+    lib = load_library()
+    if q.dtype != torch.float32 or not q.is_contiguous() or q.dim() != 3:
+        raise ValueError("q must be a contiguous float32 [R][Hq][D] tensor")
+    R, Hq, D = (int(x) for x in q.shape)
+    if out.shape != q.shape or out.dtype != torch.float32 or not out.is_contiguous():
+        raise ValueError("out must match q")
+    code = kv_dtype_code(cache.kv.dtype) if kv_dtype is None else int(kv_dtype)
+    if scale is None:
+        scale = D ** -0.5
+    d = CDecode(_ptr(q), _ptr(out), Hq, int(layer), code, float(scale), int(max_tokens),
+                0, 0, _ptr(slot_count))
+    c = cache.c()
+    _check(lib.vtoken_paged_decode_noalloc(ctypes.byref(c), ctypes.byref(d), R,
+                                           _ptr(slot_indptr), _ptr(slots), _stream(stream)),
+           "vtoken_paged_decode_noalloc")
     return out
 
 

@@ -327,9 +327,15 @@ int64_t vtoken_decode_workspace_bytes(int32_t num_reqs, int32_t num_q_heads, int
   return (int64_t)num_reqs * num_q_heads * splits * (head_dim + 2) * 4;
 }
 
-vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode* d,
-                                  int32_t num_reqs, const int32_t* slot_indptr,
-                                  const int32_t* slots, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// The paged decode with its split partials in `workspace` (the caller's, or the library-held
+// array of the no-alloc entry point; nullptr: the caller's, from *d).
+vtoken_status paged_decode(const vtoken_cache* cache, const vtoken_decode* d, int32_t num_reqs,
+                           const int32_t* slot_indptr, const int32_t* slots,
+                           hipStream_t stream, bool library_workspace) {
   vtoken_status s = check_cache(cache);
   if (s != VTOKEN_OK) return s;
   if (d == nullptr || slot_indptr == nullptr) return VTOKEN_ERR_NULL;
@@ -337,7 +343,8 @@ vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode
     return VTOKEN_ERR_SHAPE;
   }
   if (num_reqs == 0) return VTOKEN_OK;
-  if (d->q == nullptr || d->out == nullptr || d->workspace == nullptr || slots == nullptr) {
+  if (d->q == nullptr || d->out == nullptr || slots == nullptr ||
+      (!library_workspace && d->workspace == nullptr)) {
     return VTOKEN_ERR_NULL;
   }
   const int kind = d->kv_dtype;
@@ -352,7 +359,9 @@ vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode
   const int64_t need = vtoken_decode_workspace_bytes(num_reqs, d->num_q_heads, cache->head_dim,
                                                      d->max_tokens);
   if (need < 0) return VTOKEN_ERR_SHAPE;
-  if (need > d->workspace_bytes) return VTOKEN_ERR_CAPACITY;
+  if (need > (library_workspace ? vtoken::kDecodeScratchBytes : d->workspace_bytes)) {
+    return VTOKEN_ERR_CAPACITY;
+  }
   vtoken::AttnArgs a;
   a.kv = static_cast<const uint8_t*>(cache->kv);
   a.row_bytes = (int64_t)cache->num_kv_heads * cache->head_dim * cache->elem_bytes;
@@ -375,12 +384,32 @@ vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode
   a.q = d->q;
   a.out = d->out;
   a.workspace = d->workspace;
+  if (library_workspace) {
+    // the array's address on the stream's device (no allocation; first call per device)
+    const hipError_t e = vtoken::decode_scratch(stream, &a.workspace);
+    if (e != hipSuccess) return hip_status(e);
+  }
   a.slot_indptr = slot_indptr;
   a.slots = slots;
   a.slot_count = d->slot_count;
   return hip_status(vtoken::launch_paged_decode(a, stream));
 }
 
+}  // namespace
+
+extern "C" {
+
+vtoken_status vtoken_paged_decode(const vtoken_cache* cache, const vtoken_decode* d,
+                                  int32_t num_reqs, const int32_t* slot_indptr,
+                                  const int32_t* slots, hipStream_t stream) {
+  return paged_decode(cache, d, num_reqs, slot_indptr, slots, stream, false);
+}
+
+vtoken_status vtoken_paged_decode_noalloc(const vtoken_cache* cache, const vtoken_decode* d,
+                                          int32_t num_reqs, const int32_t* slot_indptr,
+                                          const int32_t* slots, hipStream_t stream) {
+  return paged_decode(cache, d, num_reqs, slot_indptr, slots, stream, true);
+}
 
 vtoken_status vtoken_plan_partial(const vtoken_cache* cache, const vtoken_batch* batch,
                                   const int32_t* slot_in, const vtoken_planner_params* params,

@@ -16,6 +16,9 @@
 // MFMA, which leaves the vector ALUs to the softmax and the operand conversions.
 #include <math.h>
 
+#include <atomic>
+#include <mutex>
+
 #include "vtoken_internal.h"
 
 namespace vtoken {
@@ -748,6 +751,49 @@ hipError_t launch_paged_decode(const AttnArgs& a, hipStream_t stream) {
                          (int64_t)a.num_reqs * a.num_q_heads)), dim3(kCombineThreads), 0,
                      stream, a);
   return hipGetLastError();
+}
+
+// Split partials of vtoken_paged_decode_noalloc: a library-held workspace for callers that
+// cannot allocate. Each GPU that loads the library holds its own copy of the array until the
+// process ends; its address on a device is looked up once, with that device current, and kept.
+// The name below stands for the array only in device code: host code uses the address.
+static __device__ __align__(256) float scratch[kDecodeScratchBytes / 4];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxScratchDevices];
+std::mutex g_scratch_mu;
+}  // namespace
+
+hipError_t decode_scratch(hipStream_t stream, float** out) {
+  int cur = 0;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return e;
+  int dev = cur;
+  if (stream != nullptr) {
+    e = hipStreamGetDevice(stream, &dev);
+    if (e != hipSuccess) return e;
+  }
+  if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (p == nullptr) {
+      // the lookup is per device and needs the stream's device current
+      if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return e;
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (dev != cur) {
+        const hipError_t back = hipSetDevice(cur);
+        if (e == hipSuccess) e = back;
+      }
+      if (e != hipSuccess) return e;
+      if (p == nullptr) return hipErrorInvalidSymbol;
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = static_cast<float*>(p);
+  return hipSuccess;
 }
 
 }  // namespace vtoken

@@ -195,6 +195,10 @@ hipError_t launch_planner(const PlannerArgs& a, hipStream_t stream);
 hipError_t launch_slot_mapping(const SlotMapArgs& a, hipStream_t stream);
 hipError_t launch_append_slots(const AppendArgs& a, hipStream_t stream);
 hipError_t launch_paged_decode(const AttnArgs& a, hipStream_t stream);
+// The library-held decode workspace (vtoken_paged_decode_noalloc): its size, and its address
+// on the device of `stream` (looked up on the first call per device; allocates nothing).
+constexpr int64_t kDecodeScratchBytes = VTOKEN_DECODE_SCRATCH_BYTES;
+hipError_t decode_scratch(hipStream_t stream, float** out);
 // Decode split geometry. Each wave of a split workgroup covers 8 KiB of K (and of V) of one
 // KV head: 128 bytes per lane and operand. A workgroup has 4 waves, or 8 for 16-bit caches
 // with GQA groups of 8, whose per-workgroup work (query operands, the merge of the waves, a

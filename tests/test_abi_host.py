@@ -320,6 +320,37 @@ def test_check_layout_workspace_bytes_and_bad_arguments():
     assert lib.vtoken_status_string(-14).decode().startswith("VTOKEN_ERR_LAYOUT")
 
 
+@pytest.mark.parametrize("mutate,code", [
+    (lambda c, d: setattr(d, "num_q_heads", 24), "VTOKEN_ERR_SHAPE"),      # G = 3
+    (lambda c, d: setattr(d, "layer", 2), "VTOKEN_ERR_SHAPE"),
+    (lambda c, d: setattr(d, "kv_dtype", B.KV_FP8_E4M3), "VTOKEN_ERR_SHAPE"),
+    (lambda c, d: setattr(d, "q", None), "VTOKEN_ERR_NULL"),
+    (lambda c, d: setattr(d, "out", None), "VTOKEN_ERR_NULL"),
+    # partials beyond the library-held array: 2 requests x 32 heads x 2344 splits x 130 x 4 B
+    (lambda c, d: setattr(d, "max_tokens", 300000), "VTOKEN_ERR_CAPACITY"),
+])
+def test_paged_decode_noalloc_rejects_bad_arguments(mutate, code):
+    """The allocation-free decode checks its arguments like vtoken_paged_decode, ignores the
+    caller workspace fields, and refuses a call whose partials exceed the library-held array
+    (VTOKEN_DECODE_SCRATCH_BYTES) before touching the device."""
+    lib = B.load_library()
+    cache, _, _ = _good()
+    d, _ = _good_decode(cache)
+    d.workspace, d.workspace_bytes = None, 0       # ignored by this entry point
+    mutate(cache, d)
+    p = _fake_ptr()
+    st = lib.vtoken_paged_decode_noalloc(ctypes.byref(cache), ctypes.byref(d), 2, p, p, None)
+    assert st == B.STATUS_CODE[code], (st, code)
+    limit = lib.vtoken_decode_workspace_bytes(2, 32, 128, 300000)
+    assert limit > B.DECODE_SCRATCH_BYTES >= lib.vtoken_decode_workspace_bytes(2, 32, 128, 250000)
+
+
+def test_header_scratch_size_matches_binding():
+    text = open(HEADER).read()
+    m = re.search(r"#define VTOKEN_DECODE_SCRATCH_BYTES \((\d+)LL << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == B.DECODE_SCRATCH_BYTES
+
+
 def test_build_id_is_the_hash_of_the_sources():
     """The loaded library carries the SHA-256 of the tree's csrc/ and include/vtoken.h (paths
     relative to the repository root in sorted order, each hashed as path, NUL, contents,
