@@ -98,7 +98,7 @@ def parse_args(argv=None):
                          "decode step (every layer) on the main stream with the repack pass on "
                          "a relocation stream, against the two one after the other; stream: "
                          "read / write / copy and decode-pattern probes, the memory system's "
-                         "streaming ceilings; placement: the minimal 56 GiB pool allocated twice, "
+                         "streaming ceilings; placement: the minimal 56 GiB pool allocated 4 times, "
                          "repack and write / read probes on each (for counter runs)")
     ap.add_argument("--q-heads", type=int, default=32, help="decode mode: query heads")
     ap.add_argument("--copy-gib", type=float, default=8.0)
@@ -339,14 +339,14 @@ def inputs_sha256(inp) -> dict:
 def streaming_ceiling(args, inp, kv, cache, bytes_alg: int, stream, block_copy: bool,
                       steps: int = 10):
     """The copy's practical ceiling, timed in the same run after the timed steps: the streaming
-    probe's copy (bench_probe.hip; consecutive workgroups 64 chunks apart, the best copy pattern
-    measured) over about the pass's bytes inside the same KV pool; torch's device copy of 4 GiB
+    probe's plane copy (bench_probe.hip; the repack's work order over contiguous chunks) over
+    about the pass's bytes inside the same KV pool; torch's device copy of 4 GiB
     when that much HBM is still free (a library copy, for reference); with `block_copy` the
     repack kernel on whole contiguous blocks (block-copy metadata over the same KV tensor,
     which adds launches of the timed kernel to a profile of the run). The copies overwrite
     bytes of the pool; the copy is value-agnostic."""
     import torch
-    out = probe_copy_ceiling(kv, bytes_alg, stream, steps)
+    out = probe_copy_ceiling(kv, inp.shape.num_planes, bytes_alg, stream, steps)
     if block_copy:
         out.update(block_copy_ceiling(inp, cache, bytes_alg, stream, steps))
     free, _ = torch.cuda.mem_get_info()
@@ -370,36 +370,40 @@ def streaming_ceiling(args, inp, kv, cache, bytes_alg: int, stream, block_copy: 
     return out
 
 
-def probe_copy_ceiling(kv, bytes_alg: int, stream, steps: int = 10):
-    """The probe copy (64 chunks apart) of about half the pass's bytes from the first half of
-    the KV tensor to its second half: read + write bytes per second."""
+def probe_copy_ceiling(kv, num_planes: int, bytes_alg: int, stream, steps: int = 10):
+    """The streaming ceiling of the repack's own work order: bench_probe.hip's plane copy over
+    the KV tensor's planes, consecutive workgroups on one 32 KiB chunk index of different
+    planes (the repack's block-major order), contiguous chunks from the first half of each plane
+    to its second half, about the pass's bytes in all. Read + write bytes per second."""
     import ctypes
     import torch
     lib = probe_library()
     chunk = 32768
-    total = kv.numel() * kv.element_size()
-    unit = 1024 * chunk                      # every interleave divides the chunk count
-    region = min(bytes_alg // 2, total // 2) // unit * unit
-    if region == 0:
+    plane_bytes = kv.numel() * kv.element_size() // num_planes
+    per_plane = plane_bytes // chunk
+    n = min(bytes_alg // 2 // (chunk * num_planes), per_plane // 2)
+    if n == 0 or plane_bytes % chunk:
         return {}
-    src = kv.data_ptr()
-    dst = kv.data_ptr() + (total // 2) // chunk * chunk
     sh = ctypes.c_void_p(stream.cuda_stream)
+    call = lambda: lib.vtoken_probe_plane_copy(kv.data_ptr(), plane_bytes, num_planes, 0,  # noqa: E731
+                                               per_plane // 2, n, sh)
     for _ in range(3):
-        if lib.vtoken_probe_copy(src, dst, region, 64, sh) != 0:
-            raise SystemExit("probe copy refused its arguments")
+        if call() != 0:
+            raise SystemExit("probe plane copy refused its arguments")
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(steps)]
     for a, b in evs:
         a.record(stream)
-        lib.vtoken_probe_copy(src, dst, region, 64, sh)
+        call()
         b.record(stream)
     torch.cuda.synchronize()
     ms = sum(a.elapsed_time(b) for a, b in evs) / steps
-    gbs = 2 * region / (ms / 1e3) / 1e9
-    return {"probe_copy": "bench_probe.hip copy_kernel, workgroups 64 chunks apart, non-temporal "
-                          "loads, sc1 stores, in the same KV pool",
-            "probe_copy_bytes": 2 * region, "probe_copy_ms": round(ms, 4),
+    nbytes = 2 * n * chunk * num_planes
+    gbs = nbytes / (ms / 1e3) / 1e9
+    return {"probe_copy": "bench_probe.hip plane copy: the repack's work order (consecutive "
+                          "workgroups on one chunk of different planes) over contiguous 32 KiB "
+                          "chunks of the same KV pool, non-temporal loads, sc1 stores",
+            "probe_copy_bytes": nbytes, "probe_copy_ms": round(ms, 4),
             "probe_copy_GBps": round(gbs, 1), "probe_copy_frac": round(gbs / HBM_PEAK_GBS, 4)}
 
 
@@ -479,6 +483,7 @@ def probe_library(rebuild: bool = False):
     lib.vtoken_probe_write.argtypes = [vp, i64, i32, vp]
     lib.vtoken_probe_copy.argtypes = [vp, vp, i64, i32, vp]
     lib.vtoken_probe_head_read.argtypes = [vp, i64, i32, vp, i64, i32, vp, vp]
+    lib.vtoken_probe_plane_copy.argtypes = [vp, i64, i32, i64, i64, i64, vp]
     return lib
 
 
@@ -556,12 +561,12 @@ def run_stream(args):
 
 def run_placement(args):
     """The Llama-3-8B Random requests in the minimal pool (their blocks, their destinations and
-    1024 spare blocks: 56 GiB), allocated twice in one process (both held; consecutive
+    1024 spare blocks: 56 GiB), allocated four times in one process (all held; consecutive
     allocations of this size land on placements of two speeds). On each pool, in this order:
     the repack pass (--warmup + --steps, the copy timed with HIP events), the probe write of
     half the pass's bytes (64 chunks apart, the copy's store pattern), the probe read of the
-    same bytes. Run under rocprofv3 --pmc, the dispatches of the first pool come before those
-    of the second, so counters can be set side by side per placement."""
+    same bytes. Run under rocprofv3 --pmc, the dispatches of each pool come before those of the
+    next, so counters can be set side by side per placement."""
     import ctypes
     import torch
     from paper_2608_13263_amd import binding as B
@@ -587,7 +592,7 @@ def run_placement(args):
         torch.cuda.synchronize()
         return sum(a.elapsed_time(b) for a, b in evs) / n
 
-    for k in range(2):
+    for k in range(4):
         kv = W.kv_device(sh, inp.num_blocks, 1 + k)
         kvs.append(kv)
         cache = B.KVCache(kv, sh.num_layers, sh.num_kv_heads, sh.head_dim, sh.block_size)
@@ -616,7 +621,7 @@ def run_placement(args):
                       "probe_read_GBps": round(region / (r_ms / 1e3) / 1e9, 1),
                       "bytes_alg": bytes_alg, "probe_bytes": region})
         log(f"pool {k}: {pools[-1]}")
-    out = {"metric": "repack and probe rates on two 56 GiB placements", "mode": "placement",
+    out = {"metric": "repack and probe rates on four 56 GiB allocations", "mode": "placement",
            "value": min(p["repack_GBps"] for p in pools), "unit": "GB/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
            "data": "synthetic", "pools": pools,

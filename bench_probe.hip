@@ -13,6 +13,8 @@
 //                consecutive workgroups on one block of different planes); stores through a
 //                buffer resource with the repack's cache policy (sc1)
 //   copy         chunk c(w) of src to chunk c(w) of dst, non-temporal loads, sc1 stores
+//   plane_copy   the repack's work order over contiguous chunks: workgroup w copies a chunk of
+//                plane w % planes, consecutive workgroups on different planes
 //   head_read    the decode's pattern: 256-byte head pieces of token rows, reached through a slot
 //                list, from a K plane and a V plane; workgroup (tile, head) reads the K and V
 //                pieces of 64 tokens of one head, grid head-major
@@ -97,6 +99,29 @@ __global__ __launch_bounds__(kThreads) void probe_copy_kernel(const uint8_t* src
   }
 }
 
+// The repack's order over contiguous chunks: workgroup w copies chunk src0 + w / planes of plane
+// w % planes to chunk dst0 + w / planes of the same plane (consecutive workgroups on one chunk
+// index of different planes, as the repack's block-major order puts them), 32 KiB each,
+// non-temporal loads and sc1 stores like the repack.
+__global__ __launch_bounds__(kThreads) void probe_plane_copy_kernel(uint8_t* base,
+                                                                    int64_t plane_bytes,
+                                                                    int planes, int64_t src0,
+                                                                    int64_t dst0) {
+  const int64_t c = blockIdx.x / planes;
+  uint8_t* plane = base + (int64_t)(blockIdx.x - c * planes) * plane_bytes;
+  const u32x4* s = reinterpret_cast<const u32x4*>(plane + (src0 + c) * kChunk);
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      plane + (dst0 + c) * kChunk, 0, static_cast<int>(kChunk), kBufferDword3);
+  u32x4 v[kUnits];
+#pragma unroll
+  for (int k = 0; k < kUnits; ++k) v[k] = load16<true>(s + k * kThreads + threadIdx.x);
+#pragma unroll
+  for (int k = 0; k < kUnits; ++k) {
+    __builtin_amdgcn_raw_buffer_store_b128(v[k], rs, (k * kThreads + threadIdx.x) * 16, 0,
+                                           kStoreSc1);
+  }
+}
+
 // 16 lanes per 256-byte piece, 16 tokens per pass, 4 passes = 64 tokens; each thread loads
 // the K pieces of its 4 tokens, then their V pieces
 template <bool kNT>
@@ -164,6 +189,26 @@ int vtoken_probe_copy(const void* src, void* dst, int64_t bytes, int ways, hipSt
   hipLaunchKernelGGL(probe_copy_kernel, dim3(chunks), dim3(kThreads), 0, stream,
                      static_cast<const uint8_t*>(src), static_cast<uint8_t*>(dst), chunks,
                      (int64_t)ways);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+// The repack's work order over contiguous chunks: `planes` planes of plane_bytes (a multiple
+// of 32 KiB) from `base`; in every plane, chunks [src0, src0 + chunks) are copied to chunks
+// [dst0, dst0 + chunks) (both ranges inside the plane, not overlapping).
+int vtoken_probe_plane_copy(void* base, int64_t plane_bytes, int planes, int64_t src0,
+                            int64_t dst0, int64_t chunks, hipStream_t stream) {
+  if (base == nullptr || plane_bytes <= 0 || plane_bytes % kChunk != 0 || planes <= 0 ||
+      chunks <= 0 || src0 < 0 || dst0 < 0) {
+    return -2;
+  }
+  const int64_t per_plane = plane_bytes / kChunk;
+  if (src0 + chunks > per_plane || dst0 + chunks > per_plane ||
+      (src0 < dst0 + chunks && dst0 < src0 + chunks) || chunks * planes > kMaxGrid) {
+    return -2;
+  }
+  hipLaunchKernelGGL(probe_plane_copy_kernel, dim3(static_cast<unsigned>(chunks * planes)),
+                     dim3(kThreads), 0, stream, static_cast<uint8_t*>(base), plane_bytes, planes,
+                     src0, dst0);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 

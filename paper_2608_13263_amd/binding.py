@@ -201,7 +201,25 @@ def _stream(stream) -> int:
     return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
 
 
-class KVCache:
+class _Cached:
+    """The C struct of an object is built once and reused (it only holds the tensors' device
+    addresses and sizes); assigning any attribute drops it. Building the structs costs a few
+    microseconds of Python per call, which a small pass would otherwise spend in every call."""
+
+    def __setattr__(self, name, value):
+        object.__setattr__(self, name, value)
+        if name != "_c_cache":
+            object.__setattr__(self, "_c_cache", None)
+
+    def c(self):
+        cached = getattr(self, "_c_cache", None)
+        if cached is None:
+            cached = self._make_c()
+            object.__setattr__(self, "_c_cache", cached)
+        return cached
+
+
+class KVCache(_Cached):
     """A paged KV cache tensor [2L][num_blocks][S][H][D] (any 1- or 2-byte dtype)."""
 
     def __init__(self, kv, num_layers: int, num_kv_heads: int, head_dim: int, block_size: int):
@@ -216,12 +234,12 @@ class KVCache:
             raise ValueError("kv size is not a whole number of blocks")
         self.num_blocks = kv.numel() // per_block
 
-    def c(self) -> CCache:
+    def _make_c(self) -> CCache:
         return CCache(_ptr(self.kv), self.num_layers, self.num_kv_heads, self.head_dim,
                       self.block_size, self.num_blocks, self.elem_bytes)
 
 
-class Batch:
+class Batch(_Cached):
     """Device-resident request batch (CSR), matching vtoken_batch."""
 
     def __init__(self, seq_lens, tok_indptr, bt_indptr, block_ids, live, free_list):
@@ -249,13 +267,13 @@ class Batch:
         return cls.from_host(inp.seq_lens, inp.tok_indptr, inp.bt_indptr, inp.block_ids,
                              inp.live, inp.free_list, device)
 
-    def c(self) -> CBatch:
+    def _make_c(self) -> CBatch:
         return CBatch(self.num_reqs, self.num_tokens, self.num_bt_entries, _ptr(self.seq_lens),
                       _ptr(self.tok_indptr), _ptr(self.bt_indptr), _ptr(self.block_ids),
                       _ptr(self.live), _ptr(self.free_list), self.free_len)
 
 
-class Plan:
+class Plan(_Cached):
     """Caller-allocated outputs (vtoken_plan) plus the freed-list buffer."""
 
     FIELDS = ("token_slot", "live_count", "admitted", "dst_indptr", "new_bt_indptr",
@@ -280,7 +298,7 @@ class Plan:
                    src_plan=e(rows * block_size), freed_indptr=e(R + 1), counters=e(5),
                    freed=e(M))
 
-    def c(self) -> CPlan:
+    def _make_c(self) -> CPlan:
         return CPlan(*(_ptr(getattr(self, k)) for k in self.FIELDS),
                      int(self.new_block_ids.numel()), int(self.src_plan.numel()))
 

@@ -15,6 +15,10 @@ constexpr int kCountThreads = 256;
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanBallots = 8;                            // ballots per wave per tile
 constexpr int kPlanTile = kPlanThreads * kPlanBallots;     // tokens per tile (8192)
+// Batches this small are planned by one workgroup in one launch (they are bound by launch
+// latency); larger ones by a count launch and a plan launch of one workgroup per request.
+constexpr int kSmallReqs = 256;
+constexpr int kSmallTokens = 16384;
 constexpr int kFreeThreads = 256;
 
 // Copy kernel geometry: 256 threads, each moving 16-byte units.

@@ -134,6 +134,99 @@ __global__ __launch_bounds__(kCountThreads) void count_kernel(MetaArgs a) {
   }
 }
 
+// The admission over all requests, every thread of the workgroup taking part (R/1024 rounds of
+// two workgroup scans): destination need ceil(live/S), strict gain (Sec. 3.3.3, I4 of Sec.
+// 3.5), prefix admission against the free list (Sec. 3.3.2). count(i) is request i's live count
+// (a negative error code for a request the validation rejected); visit(i, admitted, destination
+// offset, new-table offset, freed offset) is called once per request by the thread holding it.
+struct Admission {
+  int used, n_new, n_freed, n_admitted, first_error;
+};
+
+template <class Count, class Visit>
+__device__ __forceinline__ Admission admit_requests(const MetaArgs& a, Count count, Visit visit,
+                                                    int (*lds)[4], int* first_error_req) {
+  const int tid = threadIdx.x;
+  const int R = a.num_reqs;
+  const int S = a.block_size;
+  if (tid == 0) *first_error_req = INT_MAX;
+  __syncthreads();
+  int carry_e = 0, carry_dst = 0, carry_new = 0, carry_freed = 0, n_admitted = 0;
+  for (int base = 0; base < R; base += kPlanThreads) {
+    const int i = base + tid;
+    const bool valid = i < R;
+    const int c = valid ? count(i) : 0;
+    if (valid && c < 0) atomicMin(first_error_req, i);
+    const int m = valid ? a.bt_indptr[i + 1] - a.bt_indptr[i] : 0;
+    const int need = c > 0 ? (c + S - 1) / S : 0;
+    const bool profitable = valid && c >= 0 && need < m;
+    // position of this request's destinations in the free list: needs of every earlier
+    // profitable request (admitted or not - once one is deferred all later ones are)
+    int s1[4] = {profitable ? need : 0, 0, 0, 0};
+    int t1[4];
+    block_exclusive_scan<4>(s1, t1, lds);
+    // in place the destinations are the request's own blocks: nothing to wait for
+    const bool adm = profitable && (a.inplace || carry_e + s1[0] + need <= a.free_len);
+    // freed: all old blocks out of place, the blocks past the need in place
+    const int n_free = adm ? (a.inplace ? m - need : m) : 0;
+    int s2[4] = {adm ? need : 0, adm ? need : m, n_free, adm ? 1 : 0};
+    int t2[4];
+    block_exclusive_scan<4>(s2, t2, lds);
+    if (valid) visit(i, adm ? 1 : 0, carry_dst + s2[0], carry_new + s2[1], carry_freed + s2[2]);
+    carry_e += t1[0];
+    carry_dst += t2[0];
+    carry_new += t2[1];
+    carry_freed += t2[2];
+    n_admitted += t2[3];
+  }
+  __syncthreads();
+  return Admission{carry_dst, carry_new, carry_freed, n_admitted, *first_error_req};
+}
+
+// The pass's status after the admission: the first rejected request's code, else a capacity
+// shortfall, else (checked by the workgroup that reports) a consumed free-list entry outside
+// the pool. The reporting workgroup writes the offsets' ends and the counters.
+__device__ __forceinline__ int admission_status(const MetaArgs& a, const Admission& adm,
+                                                int request_error, bool report) {
+  const int tid = threadIdx.x;
+  const int S = a.block_size;
+  int status = request_error;
+  if (status == 0 && ((int64_t)adm.n_new > a.new_bt_capacity ||
+                      (int64_t)adm.used * S > a.src_plan_capacity ||
+                      (!a.inplace && adm.used > a.free_len))) {
+    status = VTOKEN_ERR_CAPACITY;
+  }
+  if (!report) return status;
+  if (status == 0 && !a.inplace) {
+    // every consumed free-list entry must be a block of the pool (eight loads in flight per
+    // thread)
+    int bad = 0;
+    for (int j0 = 0; j0 < adm.used; j0 += 8 * kPlanThreads) {
+      int blk[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int j = j0 + k * kPlanThreads + tid;
+        blk[k] = j < adm.used ? a.free_list[j] : 0;
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) bad |= (blk[k] < 0) | (blk[k] >= a.num_blocks);
+    }
+    if (__syncthreads_or(bad)) status = VTOKEN_ERR_BLOCK_RANGE;
+  }
+  if (tid == 0) {
+    const int R = a.num_reqs;
+    a.dst_indptr[R] = adm.used;
+    a.new_bt_indptr[R] = adm.n_new;
+    a.freed_indptr[R] = adm.n_freed;
+    a.counters[0] = status == 0 ? adm.used : 0;
+    a.counters[1] = status == 0 ? adm.n_admitted : 0;
+    a.counters[2] = status == 0 ? adm.n_freed : 0;
+    a.counters[3] = status;
+    a.counters[4] = a.inplace ? kPlanInPlace : kPlanOutOfPlace;
+  }
+  return status;
+}
+
 // ------------------------------------------------------------------------------------------
 // Step 1b: the plan. Every workgroup first runs the admission over all requests (each reads
 // the R live counts; R/1024 rounds of two workgroup scans): destination need ceil(live/S),
@@ -156,78 +249,44 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
   const int wave = tid >> 6;
   const int R = a.num_reqs;
   const int S = a.block_size;
-  if (tid == 0) first_error_req = INT_MAX;
-  __syncthreads();
 
-  int carry_e = 0, carry_dst = 0, carry_new = 0, carry_freed = 0, n_admitted = 0;
-  for (int base = 0; base < R; base += kPlanThreads) {
-    const int i = base + tid;
-    const bool valid = i < R;
-    const int c = valid ? a.live_count[i] : 0;
-    if (valid && c < 0) atomicMin(&first_error_req, i);
-    const int m = valid ? a.bt_indptr[i + 1] - a.bt_indptr[i] : 0;
-    const int need = c > 0 ? (c + S - 1) / S : 0;
-    const bool profitable = valid && c >= 0 && need < m;
-    // position of this request's destinations in the free list: needs of every earlier
-    // profitable request (admitted or not - once one is deferred all later ones are)
-    int s1[4] = {profitable ? need : 0, 0, 0, 0};
-    int t1[4];
-    block_exclusive_scan<4>(s1, t1, lds);
-    // in place the destinations are the request's own blocks: nothing to wait for
-    const bool adm = profitable && (a.inplace || carry_e + s1[0] + need <= a.free_len);
-    // freed: all old blocks out of place, the blocks past the need in place
-    const int n_free = adm ? (a.inplace ? m - need : m) : 0;
-    int s2[4] = {adm ? need : 0, adm ? need : m, n_free, adm ? 1 : 0};
-    int t2[4];
-    block_exclusive_scan<4>(s2, t2, lds);
-    if (i == r) {
-      mine[0] = adm ? 1 : 0;
-      mine[1] = carry_dst + s2[0];
-      mine[2] = carry_new + s2[1];
-      mine[3] = carry_freed + s2[2];
-    }
-    carry_e += t1[0];
-    carry_dst += t2[0];
-    carry_new += t2[1];
-    carry_freed += t2[2];
-    n_admitted += t2[3];
+  // this request's first tile of live bits and the block-table entries of its positions do not
+  // depend on the admission: they are loaded first and arrive during it (ranges checked here,
+  // so even a request the count kernel rejected reads only inside the batch's arrays)
+  int n = 0, t0 = 0, b0 = 0;
+  if (r < R) {
+    n = a.seq_lens[r];
+    t0 = a.tok_indptr[r];
+    b0 = a.bt_indptr[r];
   }
-  __syncthreads();
-  const int used = carry_dst;
-  int status = first_error_req != INT_MAX ? a.live_count[first_error_req] : 0;
-  if (status == 0 && ((int64_t)carry_new > a.new_bt_capacity ||
-                      (int64_t)used * S > a.src_plan_capacity ||
-                      (!a.inplace && used > a.free_len))) {
-    status = VTOKEN_ERR_CAPACITY;
-  }
-  if (r == 0) {
-    if (status == 0 && !a.inplace) {
-      // every consumed free-list entry must be a block of the pool (eight loads in flight
-      // per thread)
-      int bad = 0;
-      for (int j0 = 0; j0 < used; j0 += 8 * kPlanThreads) {
-        int blk[8];
+  const bool in_range = r < R && n >= 0 && t0 >= 0 && (int64_t)t0 + n <= a.num_tokens &&
+                        b0 >= 0 && (int64_t)b0 + ((int64_t)n + S - 1) / S <= a.num_bt_entries;
+  const uint8_t* lv = a.live + t0;
+  const int32_t* bt = a.block_ids + b0;
+  uint8_t live0[kPlanBallots];
+  int phys0[kPlanBallots];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          const int j = j0 + k * kPlanThreads + tid;
-          blk[k] = j < used ? a.free_list[j] : 0;
+  for (int k = 0; k < kPlanBallots; ++k) {
+    const int pos = wave * (64 * kPlanBallots) + k * 64 + lane;
+    const bool ok = in_range && pos < n;
+    live0[k] = ok ? lv[pos] : 0;
+    phys0[k] = ok ? bt[pos / S] : 0;
+  }
+
+  const Admission adm = admit_requests(
+      a, [&](int i) { return a.live_count[i]; },
+      [&](int i, int ad, int dst, int nb, int fr) {
+        if (i == r) {
+          mine[0] = ad;
+          mine[1] = dst;
+          mine[2] = nb;
+          mine[3] = fr;
         }
-#pragma unroll
-        for (int k = 0; k < 8; ++k) bad |= (blk[k] < 0) | (blk[k] >= a.num_blocks);
-      }
-      if (__syncthreads_or(bad)) status = VTOKEN_ERR_BLOCK_RANGE;
-    }
-    if (tid == 0) {
-      a.dst_indptr[R] = carry_dst;
-      a.new_bt_indptr[R] = carry_new;
-      a.freed_indptr[R] = carry_freed;
-      a.counters[0] = status == 0 ? used : 0;
-      a.counters[1] = status == 0 ? n_admitted : 0;
-      a.counters[2] = status == 0 ? carry_freed : 0;
-      a.counters[3] = status;
-      a.counters[4] = a.inplace ? kPlanInPlace : kPlanOutOfPlace;
-    }
-  }
+      },
+      lds, &first_error_req);
+  const int status =
+      admission_status(a, adm, adm.first_error == INT_MAX ? 0 : a.live_count[adm.first_error],
+                       r == 0);
   if (r >= R) return;   // the one workgroup of an empty batch
   if (tid == 0) {
     a.admitted[r] = mine[0];
@@ -238,28 +297,20 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
   // an error anywhere: the status word (request 0's workgroup) reports it, nothing is built
   if (status != 0) return;
 
-  const int n = a.seq_lens[r];
-  const int32_t* bt = a.block_ids + a.bt_indptr[r];
-  int32_t* ts = a.token_slot + a.tok_indptr[r];
+  int32_t* ts = a.token_slot + t0;
   int32_t* nbt = a.new_block_ids + mine[2];
-  const uint8_t* lv = a.live + a.tok_indptr[r];
   if (!mine[0]) {
     // unchanged: the old table, every live token at its positional slot
-    const int m = a.bt_indptr[r + 1] - a.bt_indptr[r];
+    const int m = a.bt_indptr[r + 1] - b0;
     for (int j = tid; j < m; j += kPlanThreads) nbt[j] = bt[j];
-    for (int p0 = 0; p0 < n; p0 += kPlanBallots * kPlanThreads) {
-      uint8_t l[kPlanBallots];
+    for (int base = 0; base < n; base += kPlanTile) {
 #pragma unroll
       for (int k = 0; k < kPlanBallots; ++k) {
-        const int p = p0 + k * kPlanThreads + tid;
-        l[k] = p < n ? lv[p] : 0;
-      }
-#pragma unroll
-      for (int k = 0; k < kPlanBallots; ++k) {
-        const int p = p0 + k * kPlanThreads + tid;
+        const int p = base + wave * (64 * kPlanBallots) + k * 64 + lane;
         if (p < n) {
-          const int q = p / S;
-          ts[p] = l[k] != 0 ? bt[q] * S + (p - q * S) : -1;
+          const bool l = base == 0 ? live0[k] != 0 : lv[p] != 0;
+          const int blk = base == 0 ? phys0[k] : bt[p / S];
+          ts[p] = l ? blk * S + p % S : -1;
         }
       }
     }
@@ -279,7 +330,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
 #pragma unroll
     for (int k = 0; k < kPlanBallots; ++k) {
       const int p = wbase + k * 64 + lane;
-      const bool l = (p < n) && (lv[p] != 0);
+      const bool l = (p < n) && (base == 0 ? live0[k] != 0 : lv[p] != 0);
       const uint64_t mk = __ballot(l);
       rank[k] = l ? local + lanes_below(mk) : -1;
       local += __popcll(mk);
@@ -299,8 +350,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
       if (p < n) {
         if (rank[k] >= 0) {
           const int kk = off + rank[k];
-          const int q = p / S;
-          plan[kk] = bt[q] * S + (p - q * S);
+          plan[kk] = (base == 0 ? phys0[k] : bt[p / S]) * S + p % S;
           const int qk = kk / S;
           ts[p] = dest[qk] * S + (kk - qk * S);
         } else {
@@ -313,6 +363,151 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
   }
   // destination slots past the last live token: nothing to copy
   for (int k = c + tid; k < need * S; k += kPlanThreads) plan[k] = -1;
+}
+
+// ------------------------------------------------------------------------------------------
+// Steps 1a and 1b in one workgroup, for small batches (at most kSmallReqs requests and
+// kSmallTokens tokens), where the pass is bound by launch latency: one launch instead of two.
+// Wave w validates and counts requests w, w + 16, ... (64-token ballots, eight in flight), the
+// workgroup runs the admission over the counts held in LDS, and wave w builds the same requests'
+// tables, token slots and source plans (wave-level ballots and lane prefix counts).
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
+  __shared__ int lds[kPlanThreads / 64][4];
+  __shared__ int first_error_req;
+  __shared__ int count_s[kSmallReqs];
+  __shared__ int plan_s[kSmallReqs][4];   // admitted, destination, new-table and freed offsets
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  constexpr int kWaves = kPlanThreads / 64;
+  const int R = a.num_reqs;
+  const int S = a.block_size;
+
+  for (int r = wave; r < R; r += kWaves) {
+    const int n = a.seq_lens[r];
+    const int t0 = a.tok_indptr[r], t1 = a.tok_indptr[r + 1];
+    const int b0 = a.bt_indptr[r], b1 = a.bt_indptr[r + 1];
+    int code = 0;
+    if (n < 0 || t0 < 0 || t1 > a.num_tokens || (int64_t)t1 - t0 != n) {
+      code = VTOKEN_ERR_TOK_LEN;
+    } else if (b0 < 0 || b1 > a.num_bt_entries ||
+               (int64_t)b1 - b0 != ((int64_t)n + S - 1) / S) {
+      code = VTOKEN_ERR_BT_LEN;
+    }
+    if (code == 0) {
+      bool bad = false;
+      for (int j = b0 + lane; j < b1; j += 64) {
+        const int blk = a.block_ids[j];
+        bad |= blk < 0 || blk >= a.num_blocks;
+      }
+      if (__ballot(bad) != 0) code = VTOKEN_ERR_BLOCK_RANGE;
+    }
+    int c = code;
+    if (code == 0) {
+      const uint8_t* lv = a.live + t0;
+      c = 0;
+      for (int base = 0; base < n; base += 64 * kPlanBallots) {
+        uint8_t l[kPlanBallots];
+#pragma unroll
+        for (int k = 0; k < kPlanBallots; ++k) {
+          const int p = base + k * 64 + lane;
+          l[k] = p < n ? lv[p] : 0;
+        }
+#pragma unroll
+        for (int k = 0; k < kPlanBallots; ++k) c += __popcll(__ballot(l[k] != 0));
+      }
+    }
+    if (lane == 0) {
+      a.live_count[r] = c;
+      count_s[r] = c;
+    }
+  }
+  __syncthreads();
+
+  const Admission adm = admit_requests(
+      a, [&](int i) { return count_s[i]; },
+      [&](int i, int ad, int dst, int nb, int fr) {
+        a.admitted[i] = ad;
+        a.dst_indptr[i] = dst;
+        a.new_bt_indptr[i] = nb;
+        a.freed_indptr[i] = fr;
+        plan_s[i][0] = ad;
+        plan_s[i][1] = dst;
+        plan_s[i][2] = nb;
+        plan_s[i][3] = fr;
+      },
+      lds, &first_error_req);
+  const int status = admission_status(
+      a, adm, adm.first_error == INT_MAX ? 0 : count_s[adm.first_error], true);
+  if (status != 0) return;
+
+  for (int r = wave; r < R; r += kWaves) {
+    const int n = a.seq_lens[r];
+    const int t0 = a.tok_indptr[r];
+    const int b0 = a.bt_indptr[r];
+    const uint8_t* lv = a.live + t0;
+    const int32_t* bt = a.block_ids + b0;
+    int32_t* ts = a.token_slot + t0;
+    int32_t* nbt = a.new_block_ids + plan_s[r][2];
+    if (!plan_s[r][0]) {
+      // unchanged: the old table, every live token at its positional slot
+      const int m = a.bt_indptr[r + 1] - b0;
+      for (int j = lane; j < m; j += 64) nbt[j] = bt[j];
+      for (int base = 0; base < n; base += 64 * kPlanBallots) {
+        uint8_t l[kPlanBallots];
+        int blk[kPlanBallots];
+#pragma unroll
+        for (int k = 0; k < kPlanBallots; ++k) {
+          const int p = base + k * 64 + lane;
+          l[k] = p < n ? lv[p] : 0;
+          blk[k] = p < n ? bt[p / S] : 0;
+        }
+#pragma unroll
+        for (int k = 0; k < kPlanBallots; ++k) {
+          const int p = base + k * 64 + lane;
+          if (p < n) ts[p] = l[k] != 0 ? blk[k] * S + p % S : -1;
+        }
+      }
+      continue;
+    }
+    const int o = plan_s[r][1];
+    const int c = count_s[r];
+    const int need = (c + S - 1) / S;
+    const int32_t* dest = a.inplace ? bt : a.free_list + o;
+    int32_t* plan = a.src_plan + (int64_t)o * S;
+    for (int j = lane; j < need; j += 64) nbt[j] = dest[j];
+    int carry = 0;
+    for (int base = 0; base < n; base += 64 * kPlanBallots) {
+      uint8_t l[kPlanBallots];
+      int blk[kPlanBallots];
+#pragma unroll
+      for (int k = 0; k < kPlanBallots; ++k) {
+        const int p = base + k * 64 + lane;
+        l[k] = p < n ? lv[p] : 0;
+        blk[k] = p < n ? bt[p / S] : 0;
+      }
+#pragma unroll
+      for (int k = 0; k < kPlanBallots; ++k) {
+        const int p = base + k * 64 + lane;
+        const bool live = p < n && l[k] != 0;
+        const uint64_t mk = __ballot(live);
+        if (p < n) {
+          if (live) {
+            const int kk = carry + lanes_below(mk);
+            plan[kk] = blk[k] * S + p % S;
+            const int qk = kk / S;
+            ts[p] = dest[qk] * S + (kk - qk * S);
+          } else {
+            ts[p] = -1;
+          }
+        }
+        carry += __popcll(mk);
+      }
+    }
+    // destination slots past the last live token: nothing to copy
+    for (int k = c + lane; k < need * S; k += 64) plan[k] = -1;
+  }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -339,6 +534,10 @@ __global__ __launch_bounds__(kFreeThreads) void free_kernel(MetaArgs a, int32_t*
 }  // namespace
 
 hipError_t launch_build(const MetaArgs& a, hipStream_t stream) {
+  if (a.num_reqs <= kSmallReqs && a.num_tokens <= kSmallTokens) {
+    hipLaunchKernelGGL(plan_small_kernel, dim3(1), dim3(kPlanThreads), 0, stream, a);
+    return hipGetLastError();
+  }
   if (a.num_reqs > 0) {
     hipLaunchKernelGGL(count_kernel, dim3(a.num_reqs), dim3(kCountThreads), 0, stream, a);
   }

@@ -298,6 +298,13 @@ def test_stream_probe_library_rejects_bad_sizes():
     assert lib.vtoken_probe_head_read(fake, 1 << 20, 2000, fake, 64, 1, fake, None) == -2
     assert lib.vtoken_probe_head_read(fake, 1 << 20, 2048, fake, 100, 1, fake, None) == -2
     assert lib.vtoken_probe_head_read(fake, 1024, 2048, fake, 64, 1, fake, None) == -2
+    # plane copy: ranges inside the plane, not overlapping, planes and chunks positive
+    assert lib.vtoken_probe_plane_copy(None, 8 * chunk, 2, 0, 4, 4, None) == -2
+    assert lib.vtoken_probe_plane_copy(fake, 8 * chunk + 16, 2, 0, 4, 4, None) == -2
+    assert lib.vtoken_probe_plane_copy(fake, 8 * chunk, 2, 0, 5, 4, None) == -2    # past it
+    assert lib.vtoken_probe_plane_copy(fake, 8 * chunk, 2, 0, 3, 4, None) == -2    # overlap
+    assert lib.vtoken_probe_plane_copy(fake, 8 * chunk, 0, 0, 4, 4, None) == -2
+    assert lib.vtoken_probe_plane_copy(fake, 8 * chunk, 2, 0, 4, 0, None) == -2
 
 
 def test_check_layout_workspace_bytes_and_bad_arguments():
@@ -372,3 +379,21 @@ def test_binding_refuses_a_library_of_other_sources(tmp_path, monkeypatch):
     monkeypatch.setattr(B, "_lib", None)
     with pytest.raises(RuntimeError, match="other sources"):
         B.load_library()
+
+
+def test_binding_reuses_structs_until_an_attribute_changes():
+    """The binding builds each object's C struct once (host overhead of small passes) and
+    rebuilds it after any attribute is assigned, so a replaced buffer is never passed stale."""
+    import torch
+    t = lambda n: torch.zeros(n, dtype=torch.int32)  # noqa: E731
+    batch = B.Batch(t(2), t(3), t(3), t(4), torch.zeros(5, dtype=torch.uint8), t(6))
+    first = batch.c()
+    assert batch.c() is first
+    batch.free_list = t(9)
+    second = batch.c()
+    assert second is not first and second.free_list == batch.free_list.data_ptr()
+    assert second.free_len == 6      # sizes are the constructor's; replacing a buffer keeps them
+    plan = B.Plan(**{k: t(4) for k in B.Plan.FIELDS + ("freed",)})
+    p1 = plan.c()
+    plan.counters = t(5)
+    assert plan.c() is not p1 and plan.c().counters == plan.counters.data_ptr()

@@ -163,10 +163,18 @@ def test_side_stream_and_stream_order():
 # device-detected errors: status word set, no KV byte written
 # ------------------------------------------------------------------------------------------
 
-def _error_case(mutate, expect):
+@pytest.fixture(params=["small", "large"])
+def error_batch(request):
+    """A batch under the one-launch planning bound (16384 tokens, 256 requests) and one above it
+    (count launch + plan launch): every device-detected error is checked on both paths."""
+    lens = (300, 900) if request.param == "small" else (4000, 6000)
+    return lambda: W.llama3_8b_random(207, num_layers=1, num_reqs=5, len_range=lens)
+
+
+def _error_case(mutate, expect, make):
     t = torch()
     from paper_2608_13263_amd import binding as B
-    inp = W.llama3_8b_random(207, num_layers=1, num_reqs=5, len_range=(300, 900))
+    inp = make()
     mutate(inp)
     kv = W.kv_device(inp.shape, inp.num_blocks, 5)
     before = kv_bytes(kv, inp.shape)
@@ -176,34 +184,34 @@ def _error_case(mutate, expect):
     assert_kv_equal(kv_bytes(kv, inp.shape), before)
 
 
-def test_error_block_id_out_of_range():
+def test_error_block_id_out_of_range(error_batch):
     def m(inp):
         inp.block_ids[3] = inp.num_blocks
-    _error_case(m, "VTOKEN_ERR_BLOCK_RANGE")
+    _error_case(m, "VTOKEN_ERR_BLOCK_RANGE", error_batch)
 
 
-def test_error_negative_block_id():
+def test_error_negative_block_id(error_batch):
     def m(inp):
         inp.block_ids[-1] = -2
-    _error_case(m, "VTOKEN_ERR_BLOCK_RANGE")
+    _error_case(m, "VTOKEN_ERR_BLOCK_RANGE", error_batch)
 
 
-def test_error_free_list_entry_out_of_range():
+def test_error_free_list_entry_out_of_range(error_batch):
     def m(inp):
         inp.free_list[0] = inp.num_blocks + 5
-    _error_case(m, "VTOKEN_ERR_BLOCK_RANGE")
+    _error_case(m, "VTOKEN_ERR_BLOCK_RANGE", error_batch)
 
 
-def test_error_block_table_length():
+def test_error_block_table_length(error_batch):
     def m(inp):
         inp.bt_indptr[2] += 1
-    _error_case(m, "VTOKEN_ERR_BT_LEN")
+    _error_case(m, "VTOKEN_ERR_BT_LEN", error_batch)
 
 
-def test_error_token_range():
+def test_error_token_range(error_batch):
     def m(inp):
         inp.seq_lens[1] += 1
-    _error_case(m, "VTOKEN_ERR_TOK_LEN")
+    _error_case(m, "VTOKEN_ERR_TOK_LEN", error_batch)
 
 
 @pytest.mark.parametrize("inplace", [False, True], ids=["out_of_place", "in_place"])
@@ -290,3 +298,29 @@ def test_random_geometries(seed):
     inp = _random_case(1000 + seed)
     full_parity(inp, seed=seed)
     full_parity(inp, seed=seed, inplace=True)
+
+
+@pytest.mark.parametrize("extra", [0, 1], ids=["at_token_bound", "past_token_bound"])
+def test_small_batch_planning_bound_tokens(extra):
+    """16384 tokens are planned by the one-launch kernel, 16385 by the count and plan launches:
+    both equal the oracle on the same requests (the last one a token longer)."""
+    rng = np.random.default_rng(40 + extra)
+    lens = [1500] * 10 + [16384 - 15000 + extra]
+    masks = [(rng.random(n) < 0.4).astype(int).tolist() for n in lens]
+    M = sum(-(-n // 16) for n in lens)
+    inp = W.from_masks(masks, W.KVShape(1, 2, 64, 16, "fp16"), free_blocks=M, seed=extra,
+                       name=f"bound_tokens_{extra}")
+    assert inp.num_tokens == 16384 + extra
+    full_parity(inp, seed=3)
+
+
+@pytest.mark.parametrize("R", [256, 257])
+def test_small_batch_planning_bound_requests(R):
+    """256 requests are planned by the one-launch kernel, 257 by the count and plan launches."""
+    rng = np.random.default_rng(R)
+    masks = [(rng.random(int(n)) < 0.5).astype(int).tolist()
+             for n in rng.integers(0, 60, size=R)]
+    M = sum(-(-len(m) // 16) for m in masks)
+    inp = W.from_masks(masks, W.KVShape(1, 2, 64, 16, "bf16"), free_blocks=M // 2, seed=R,
+                       name=f"bound_requests_{R}")
+    full_parity(inp, seed=4)

@@ -78,3 +78,22 @@ def test_read_probes_leave_the_sink_alone():
                                           rows, nt, sink.data_ptr(), _stream()) == 0
     t.cuda.synchronize()
     assert int(sink.item()) == 7
+
+
+def test_plane_copy_probe_copies_in_every_plane():
+    """The ceiling probe of the bench line copies chunks [src0, src0 + n) to [dst0, dst0 + n) in
+    every plane and touches nothing else."""
+    t = torch()
+    lib = _lib()
+    planes, per_plane = 6, 64
+    print("[gpu] stream probe plane copy", flush=True)
+    g = t.Generator(device="cuda").manual_seed(9)
+    buf = t.randint(0, 256, (planes, per_plane, CHUNK), dtype=t.uint8, device="cuda",
+                    generator=g)
+    before = buf.clone()
+    assert lib.vtoken_probe_plane_copy(buf.data_ptr(), per_plane * CHUNK, planes, 3, 40, 20,
+                                       _stream()) == 0
+    t.cuda.synchronize()
+    expect = before.clone()
+    expect[:, 40:60] = before[:, 3:23]
+    assert t.equal(buf, expect)
