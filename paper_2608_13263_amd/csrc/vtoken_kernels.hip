@@ -304,14 +304,18 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
     const int m = a.bt_indptr[r + 1] - b0;
     for (int j = tid; j < m; j += kPlanThreads) nbt[j] = bt[j];
     for (int base = 0; base < n; base += kPlanTile) {
+      if (base > 0) {   // later tiles: unconditional loads, positions clamped
+#pragma unroll
+        for (int k = 0; k < kPlanBallots; ++k) {
+          const int pc = min(base + wave * (64 * kPlanBallots) + k * 64 + lane, n - 1);
+          live0[k] = lv[pc];
+          phys0[k] = bt[pc / S];
+        }
+      }
 #pragma unroll
       for (int k = 0; k < kPlanBallots; ++k) {
         const int p = base + wave * (64 * kPlanBallots) + k * 64 + lane;
-        if (p < n) {
-          const bool l = base == 0 ? live0[k] != 0 : lv[p] != 0;
-          const int blk = base == 0 ? phys0[k] : bt[p / S];
-          ts[p] = l ? blk * S + p % S : -1;
-        }
+        if (p < n) ts[p] = live0[k] != 0 ? phys0[k] * S + p % S : -1;
       }
     }
     return;
@@ -322,15 +326,31 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
   const int32_t* dest = a.inplace ? bt : a.free_list + o;
   int32_t* plan = a.src_plan + (int64_t)o * S;
   for (int j = tid; j < need; j += kPlanThreads) nbt[j] = dest[j];
+  if (need == 0) {
+    // no live token (every block is released): only dead slots to write
+    for (int p = tid; p < n; p += kPlanThreads) ts[p] = -1;
+    return;
+  }
   int carry = 0;
   for (int base = 0; base < n; base += kPlanTile) {
     const int wbase = base + wave * (64 * kPlanBallots);
+    // the tile's live bytes and table entries: the first tile's were loaded before the
+    // admission; later tiles load theirs here, unconditionally (positions clamped to the
+    // request's last token), so all of them are in flight together
+    if (base > 0) {
+#pragma unroll
+      for (int k = 0; k < kPlanBallots; ++k) {
+        const int pc = min(wbase + k * 64 + lane, n - 1);
+        live0[k] = lv[pc];
+        phys0[k] = bt[pc / S];
+      }
+    }
     int rank[kPlanBallots];
     int local = 0;
 #pragma unroll
     for (int k = 0; k < kPlanBallots; ++k) {
       const int p = wbase + k * 64 + lane;
-      const bool l = (p < n) && (base == 0 ? live0[k] != 0 : lv[p] != 0);
+      const bool l = (p < n) && live0[k] != 0;
       const uint64_t mk = __ballot(l);
       rank[k] = l ? local + lanes_below(mk) : -1;
       local += __popcll(mk);
@@ -344,15 +364,22 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
       off += (w < wave) ? x : 0;
       tile += x;
     }
+    // every lane's destination blocks first, one unconditional load each (a dead or absent
+    // token re-reads the first destination), so the eight loads are in flight together
+    int dblk[kPlanBallots];
+#pragma unroll
+    for (int k = 0; k < kPlanBallots; ++k) {
+      const int kk = rank[k] >= 0 ? off + rank[k] : 0;
+      dblk[k] = dest[kk / S];
+    }
 #pragma unroll
     for (int k = 0; k < kPlanBallots; ++k) {
       const int p = wbase + k * 64 + lane;
       if (p < n) {
         if (rank[k] >= 0) {
           const int kk = off + rank[k];
-          plan[kk] = (base == 0 ? phys0[k] : bt[p / S]) * S + p % S;
-          const int qk = kk / S;
-          ts[p] = dest[qk] * S + (kk - qk * S);
+          plan[kk] = phys0[k] * S + p % S;
+          ts[p] = dblk[k] * S + kk % S;
         } else {
           ts[p] = -1;
         }
@@ -408,14 +435,14 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
       const uint8_t* lv = a.live + t0;
       c = 0;
       for (int base = 0; base < n; base += 64 * kPlanBallots) {
+        // unconditional loads (positions clamped to the last token) keep all eight in flight
         uint8_t l[kPlanBallots];
 #pragma unroll
-        for (int k = 0; k < kPlanBallots; ++k) {
-          const int p = base + k * 64 + lane;
-          l[k] = p < n ? lv[p] : 0;
-        }
+        for (int k = 0; k < kPlanBallots; ++k) l[k] = lv[min(base + k * 64 + lane, n - 1)];
 #pragma unroll
-        for (int k = 0; k < kPlanBallots; ++k) c += __popcll(__ballot(l[k] != 0));
+        for (int k = 0; k < kPlanBallots; ++k) {
+          c += __popcll(__ballot(base + k * 64 + lane < n && l[k] != 0));
+        }
       }
     }
     if (lane == 0) {
@@ -459,9 +486,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
         int blk[kPlanBallots];
 #pragma unroll
         for (int k = 0; k < kPlanBallots; ++k) {
-          const int p = base + k * 64 + lane;
-          l[k] = p < n ? lv[p] : 0;
-          blk[k] = p < n ? bt[p / S] : 0;
+          const int pc = min(base + k * 64 + lane, n - 1);
+          l[k] = lv[pc];
+          blk[k] = bt[pc / S];
         }
 #pragma unroll
         for (int k = 0; k < kPlanBallots; ++k) {
@@ -477,32 +504,46 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
     const int32_t* dest = a.inplace ? bt : a.free_list + o;
     int32_t* plan = a.src_plan + (int64_t)o * S;
     for (int j = lane; j < need; j += 64) nbt[j] = dest[j];
+    if (need == 0) {
+      // no live token (every block is released): only dead slots to write
+      for (int p = lane; p < n; p += 64) ts[p] = -1;
+      continue;
+    }
     int carry = 0;
     for (int base = 0; base < n; base += 64 * kPlanBallots) {
       uint8_t l[kPlanBallots];
       int blk[kPlanBallots];
 #pragma unroll
       for (int k = 0; k < kPlanBallots; ++k) {
-        const int p = base + k * 64 + lane;
-        l[k] = p < n ? lv[p] : 0;
-        blk[k] = p < n ? bt[p / S] : 0;
+        const int pc = min(base + k * 64 + lane, n - 1);
+        l[k] = lv[pc];
+        blk[k] = bt[pc / S];
       }
+      // ranks first, then every lane's destination block with one unconditional load each (a
+      // dead or absent token re-reads the first destination): the loads are in flight together
+      int rank[kPlanBallots];
 #pragma unroll
       for (int k = 0; k < kPlanBallots; ++k) {
         const int p = base + k * 64 + lane;
         const bool live = p < n && l[k] != 0;
         const uint64_t mk = __ballot(live);
+        rank[k] = live ? carry + lanes_below(mk) : -1;
+        carry += __popcll(mk);
+      }
+      int dblk[kPlanBallots];
+#pragma unroll
+      for (int k = 0; k < kPlanBallots; ++k) dblk[k] = dest[(rank[k] >= 0 ? rank[k] : 0) / S];
+#pragma unroll
+      for (int k = 0; k < kPlanBallots; ++k) {
+        const int p = base + k * 64 + lane;
         if (p < n) {
-          if (live) {
-            const int kk = carry + lanes_below(mk);
-            plan[kk] = blk[k] * S + p % S;
-            const int qk = kk / S;
-            ts[p] = dest[qk] * S + (kk - qk * S);
+          if (rank[k] >= 0) {
+            plan[rank[k]] = blk[k] * S + p % S;
+            ts[p] = dblk[k] * S + rank[k] % S;
           } else {
             ts[p] = -1;
           }
         }
-        carry += __popcll(mk);
       }
     }
     // destination slots past the last live token: nothing to copy

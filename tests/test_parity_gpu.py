@@ -38,9 +38,12 @@ def test_llama3_70b_shape_block32(dtype):
     full_parity(inp, seed=5)
 
 
+@pytest.mark.parametrize("dtype", ["fp8_e4m3", "bf16"])
 @pytest.mark.parametrize("keep", [0.1, 0.6])
-def test_llama3_70b_keep_ratios(keep):
-    inp = W.llama3_70b_h2o(502, keep=keep, dtype="fp8_e4m3", num_layers=1, num_reqs=3,
+def test_llama3_70b_keep_ratios(keep, dtype):
+    # every KV byte of every plane; the full-size caches of all six variants run in
+    # test_parity_full_gpu.py as waves
+    inp = W.llama3_70b_h2o(502, keep=keep, dtype=dtype, num_layers=1, num_reqs=3,
                            len_range=(2000, 5000))
     full_parity(inp, seed=6)
 
