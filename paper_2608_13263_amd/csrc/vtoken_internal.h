@@ -11,10 +11,11 @@
 namespace vtoken {
 
 // Launch geometry of the metadata kernels (one workgroup per request each).
-constexpr int kCountThreads = 256;
+constexpr int kCountThreads = 512;
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanBallots = 8;                            // ballots per wave per tile
 constexpr int kPlanTile = kPlanThreads * kPlanBallots;     // tokens per tile (8192)
+constexpr int kPlanHead = 8192;   // free-list entries a plan workgroup holds in LDS (32 KiB)
 // Batches this small are planned by one workgroup in one launch (they are bound by launch
 // latency); larger ones by a count launch and a plan launch of one workgroup per request.
 constexpr int kSmallReqs = 256;

@@ -27,17 +27,31 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
 }
 
-__device__ __forceinline__ int wave_inclusive_scan(int v) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const int t = __shfl_up(v, d, 64);
-    if (lane >= d) v += t;
-  }
-  return v;
+// Lane i of each 16-lane row receives lane i - kN of its row, 0 for i < kN (DPP row shift).
+template <int kN>
+__device__ __forceinline__ int row_shr(int x) {
+  static_assert(kN > 0 && kN < 16, "row shift");
+  return __builtin_amdgcn_update_dpp(0, x, 0x110 + kN, 0xF, 0xF, true);
 }
 
-// Exclusive scan of NV values per thread across the workgroup; total[k] is the sum.
+// Inclusive prefix sum over the 64 lanes (every lane active): within each 16-lane row by DPP
+// row shifts (no LDS), then each row adds the totals of the rows below it, read from lanes
+// 15, 31 and 47.
+__device__ __forceinline__ int wave_inclusive_scan(int v) {
+  v += row_shr<1>(v);
+  v += row_shr<2>(v);
+  v += row_shr<4>(v);
+  v += row_shr<8>(v);
+  const int t0 = __builtin_amdgcn_readlane(v, 15);
+  const int t1 = __builtin_amdgcn_readlane(v, 31);
+  const int t2 = __builtin_amdgcn_readlane(v, 47);
+  const int row = lane_id() >> 4;
+  return v + (row >= 1 ? t0 : 0) + (row >= 2 ? t1 : 0) + (row >= 3 ? t2 : 0);
+}
+
+// Exclusive scan of NV values per thread across the workgroup; total[k] is the sum. The wave
+// totals go through LDS once: lane w of every wave reads wave w's total and a second wave scan
+// gives each wave its offset.
 template <int NV>
 __device__ __forceinline__ void block_exclusive_scan(int (&v)[NV], int (&total)[NV],
                                                      int (*lds)[NV]) {
@@ -54,17 +68,23 @@ __device__ __forceinline__ void block_exclusive_scan(int (&v)[NV], int (&total)[
   __syncthreads();
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
-    int off = 0, tot = 0;
-    for (int w = 0; w < nwaves; ++w) {
-      const int x = lds[w][k];
-      off += (w < wave) ? x : 0;
-      tot += x;
-    }
+    const int wt = wave_inclusive_scan(lane < nwaves ? lds[lane][k] : 0);
+    const int off = wave > 0 ? __builtin_amdgcn_readlane(wt, wave - 1) : 0;
+    total[k] = __builtin_amdgcn_readlane(wt, nwaves - 1);
     v[k] = off + incl[k] - v[k];
-    total[k] = tot;
   }
   __syncthreads();
 }
+
+// Division and remainder of non-negative positions and ranks by the block size S: shifts and
+// masks when S is a power of two (the kernels that divide per token are instantiated for both).
+template <bool kPow2>
+struct BlockDiv {
+  int s, sh;
+  __device__ explicit BlockDiv(int S) : s(S), sh(__ffs(S) - 1) {}
+  __device__ int div(int x) const { return kPow2 ? x >> sh : x / s; }
+  __device__ int mod(int x) const { return kPow2 ? x & (s - 1) : x % s; }
+};
 
 // Nonzero bytes of a 32-bit word: each byte's bits are folded into its lowest bit (the bits
 // shifted in from the next byte land at offsets >= 1 and are masked off).
@@ -96,31 +116,33 @@ __global__ __launch_bounds__(kCountThreads) void count_kernel(MetaArgs a) {
              (int64_t)b1 - b0 != ((int64_t)n + S - 1) / S) {
     code = VTOKEN_ERR_BT_LEN;
   }
-  if (code == 0) {
-    int bad = 0;
-    for (int j = b0 + tid; j < b1; j += kCountThreads) {
-      const int blk = a.block_ids[j];
-      bad |= (blk < 0) | (blk >= a.num_blocks);
-    }
-    if (__syncthreads_or(bad)) code = VTOKEN_ERR_BLOCK_RANGE;
-  }
-  if (code != 0) {
+  if (code != 0) {   // uniform: every thread read the same entries
     if (tid == 0) a.live_count[r] = code;
     return;
   }
-  // 16-byte loads over the 16-byte-aligned middle of the request's mask, bytes at the ends
+  // the block ids (validated) and the mask (counted) are read in the same loop, so that their
+  // loads are in flight together; 16-byte loads over the 16-byte-aligned middle of the mask,
+  // bytes at its ends
   const uint8_t* lv = a.live + t0;
   const int lead = static_cast<int>((16 - (reinterpret_cast<uintptr_t>(lv) & 15)) & 15);
   const int head = lead < n ? lead : n;
   const int words = (n - head) / 16;
   const int tail0 = head + words * 16;
-  int cnt = 0;
+  const int m = b1 - b0;
+  const int iters = words > m ? words : m;
+  int cnt = 0, bad = 0;
   if (tid < head) cnt += lv[tid] != 0;
   if (tail0 + tid < n) cnt += lv[tail0 + tid] != 0;
   const uint4* w16 = reinterpret_cast<const uint4*>(lv + head);
-  for (int w = tid; w < words; w += kCountThreads) {
-    const uint4 x = w16[w];
+  for (int w = tid; w < iters; w += kCountThreads) {
+    const int blk = w < m ? a.block_ids[b0 + w] : 0;
+    const uint4 x = w < words ? w16[w] : make_uint4(0, 0, 0, 0);
+    bad |= (blk < 0) | (blk >= a.num_blocks);
     cnt += nonzero_bytes(x.x) + nonzero_bytes(x.y) + nonzero_bytes(x.z) + nonzero_bytes(x.w);
+  }
+  if (__syncthreads_or(bad)) {
+    if (tid == 0) a.live_count[r] = VTOKEN_ERR_BLOCK_RANGE;
+    return;
   }
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) cnt += __shfl_xor(cnt, d, 64);
@@ -137,14 +159,16 @@ __global__ __launch_bounds__(kCountThreads) void count_kernel(MetaArgs a) {
 // The admission over all requests, every thread of the workgroup taking part (R/1024 rounds of
 // two workgroup scans): destination need ceil(live/S), strict gain (Sec. 3.3.3, I4 of Sec.
 // 3.5), prefix admission against the free list (Sec. 3.3.2). count(i) is request i's live count
-// (a negative error code for a request the validation rejected); visit(i, admitted, destination
-// offset, new-table offset, freed offset) is called once per request by the thread holding it.
+// (a negative error code for a request the validation rejected), blocks(i) the length of its
+// old table; visit(i, admitted, destination offset, new-table offset, freed offset) is called
+// once per request by the thread holding it.
 struct Admission {
   int used, n_new, n_freed, n_admitted, first_error;
 };
 
-template <class Count, class Visit>
-__device__ __forceinline__ Admission admit_requests(const MetaArgs& a, Count count, Visit visit,
+template <class Count, class Blocks, class Visit>
+__device__ __forceinline__ Admission admit_requests(const MetaArgs& a, Count count,
+                                                    Blocks blocks, Visit visit,
                                                     int (*lds)[4], int* first_error_req) {
   const int tid = threadIdx.x;
   const int R = a.num_reqs;
@@ -157,7 +181,7 @@ __device__ __forceinline__ Admission admit_requests(const MetaArgs& a, Count cou
     const bool valid = i < R;
     const int c = valid ? count(i) : 0;
     if (valid && c < 0) atomicMin(first_error_req, i);
-    const int m = valid ? a.bt_indptr[i + 1] - a.bt_indptr[i] : 0;
+    const int m = valid ? blocks(i) : 0;
     const int need = c > 0 ? (c + S - 1) / S : 0;
     const bool profitable = valid && c >= 0 && need < m;
     // position of this request's destinations in the free list: needs of every earlier
@@ -185,9 +209,12 @@ __device__ __forceinline__ Admission admit_requests(const MetaArgs& a, Count cou
 
 // The pass's status after the admission: the first rejected request's code, else a capacity
 // shortfall, else (checked by the workgroup that reports) a consumed free-list entry outside
-// the pool. The reporting workgroup writes the offsets' ends and the counters.
+// the pool; head[0 .. head_len) is a copy of the free list's first entries in LDS, checked
+// there. The reporting workgroup writes the offsets' ends and the counters.
 __device__ __forceinline__ int admission_status(const MetaArgs& a, const Admission& adm,
-                                                int request_error, bool report) {
+                                                int request_error, bool report,
+                                                const int32_t* head = nullptr,
+                                                int head_len = 0) {
   const int tid = threadIdx.x;
   const int S = a.block_size;
   int status = request_error;
@@ -201,7 +228,11 @@ __device__ __forceinline__ int admission_status(const MetaArgs& a, const Admissi
     // every consumed free-list entry must be a block of the pool (eight loads in flight per
     // thread)
     int bad = 0;
-    for (int j0 = 0; j0 < adm.used; j0 += 8 * kPlanThreads) {
+    const int in_head = adm.used < head_len ? adm.used : head_len;
+    for (int j = tid; j < in_head; j += kPlanThreads) {
+      bad |= (head[j] < 0) | (head[j] >= a.num_blocks);
+    }
+    for (int j0 = in_head; j0 < adm.used; j0 += 8 * kPlanThreads) {
       int blk[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
@@ -238,17 +269,37 @@ __device__ __forceinline__ int admission_status(const MetaArgs& a, const Admissi
 // fill of Sec. 3.3.3) and its rows of the per-destination source plan. No workgroup waits for
 // another, so the admission costs one extra O(R) pass per workgroup instead of a launch.
 // ------------------------------------------------------------------------------------------
+template <bool kPow2>
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
   __shared__ int lds[kPlanThreads / 64][4];
   __shared__ int wave_total[kPlanThreads / 64];
   __shared__ int first_error_req;
   __shared__ int mine[4];   // admitted, destination offset, new-table offset, freed offset
+  __shared__ int32_t head[kPlanHead];   // free_list[0 .. P)
   const int r = blockIdx.x;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int R = a.num_reqs;
   const int S = a.block_size;
+  const BlockDiv<kPow2> bd(S);
+
+  // Loads that depend on nothing are issued first, so that they are in flight together with
+  // the request's own CSR entries: the admission's inputs for the first 1024 requests, and the
+  // head of the free list (out of place), from which destinations are looked up in LDS
+  // instead of by a load after the admission.
+  int c_pre = 0, m_pre = 0;
+  if (tid < R) {
+    c_pre = a.live_count[tid];
+    m_pre = a.bt_indptr[tid + 1] - a.bt_indptr[tid];
+  }
+  const int P = a.inplace ? 0 : min(a.free_len, kPlanHead);
+  int32_t fl[kPlanHead / kPlanThreads];
+#pragma unroll
+  for (int q = 0; q < kPlanHead / kPlanThreads; ++q) {
+    const int j = q * kPlanThreads + tid;
+    fl[q] = j < P ? a.free_list[j] : 0;
+  }
 
   // this request's first tile of live bits and the block-table entries of its positions do not
   // depend on the admission: they are loaded first and arrive during it (ranges checked here,
@@ -270,11 +321,18 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
     const int pos = wave * (64 * kPlanBallots) + k * 64 + lane;
     const bool ok = in_range && pos < n;
     live0[k] = ok ? lv[pos] : 0;
-    phys0[k] = ok ? bt[pos / S] : 0;
+    phys0[k] = ok ? bt[bd.div(pos)] : 0;
   }
 
+#pragma unroll
+  for (int q = 0; q < kPlanHead / kPlanThreads; ++q) {
+    const int j = q * kPlanThreads + tid;
+    if (j < P) head[j] = fl[q];
+  }
+  // (the admission's first barrier orders these LDS writes before every read)
   const Admission adm = admit_requests(
-      a, [&](int i) { return a.live_count[i]; },
+      a, [&](int i) { return i < kPlanThreads ? c_pre : a.live_count[i]; },
+      [&](int i) { return i < kPlanThreads ? m_pre : a.bt_indptr[i + 1] - a.bt_indptr[i]; },
       [&](int i, int ad, int dst, int nb, int fr) {
         if (i == r) {
           mine[0] = ad;
@@ -286,7 +344,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
       lds, &first_error_req);
   const int status =
       admission_status(a, adm, adm.first_error == INT_MAX ? 0 : a.live_count[adm.first_error],
-                       r == 0);
+                       r == 0, head, P);
   if (r >= R) return;   // the one workgroup of an empty batch
   if (tid == 0) {
     a.admitted[r] = mine[0];
@@ -309,13 +367,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
         for (int k = 0; k < kPlanBallots; ++k) {
           const int pc = min(base + wave * (64 * kPlanBallots) + k * 64 + lane, n - 1);
           live0[k] = lv[pc];
-          phys0[k] = bt[pc / S];
+          phys0[k] = bt[bd.div(pc)];
         }
       }
 #pragma unroll
       for (int k = 0; k < kPlanBallots; ++k) {
         const int p = base + wave * (64 * kPlanBallots) + k * 64 + lane;
-        if (p < n) ts[p] = live0[k] != 0 ? phys0[k] * S + p % S : -1;
+        if (p < n) ts[p] = live0[k] != 0 ? phys0[k] * S + bd.mod(p) : -1;
       }
     }
     return;
@@ -323,9 +381,12 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
   const int o = mine[1];
   const int c = a.live_count[r];
   const int need = (c + S - 1) / S;
+  // this request's destinations: read from the LDS head of the free list when they lie in it
+  const bool dest_lds = !a.inplace && o + need <= P;
   const int32_t* dest = a.inplace ? bt : a.free_list + o;
+  const int32_t* dest_s = head + o;
   int32_t* plan = a.src_plan + (int64_t)o * S;
-  for (int j = tid; j < need; j += kPlanThreads) nbt[j] = dest[j];
+  for (int j = tid; j < need; j += kPlanThreads) nbt[j] = dest_lds ? dest_s[j] : dest[j];
   if (need == 0) {
     // no live token (every block is released): only dead slots to write
     for (int p = tid; p < n; p += kPlanThreads) ts[p] = -1;
@@ -342,7 +403,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
       for (int k = 0; k < kPlanBallots; ++k) {
         const int pc = min(wbase + k * 64 + lane, n - 1);
         live0[k] = lv[pc];
-        phys0[k] = bt[pc / S];
+        phys0[k] = bt[bd.div(pc)];
       }
     }
     int rank[kPlanBallots];
@@ -364,13 +425,19 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
       off += (w < wave) ? x : 0;
       tile += x;
     }
-    // every lane's destination blocks first, one unconditional load each (a dead or absent
-    // token re-reads the first destination), so the eight loads are in flight together
+    // every lane's destination blocks first, one unconditional read each (a dead or absent
+    // token re-reads the first destination), so the eight reads are in flight together
     int dblk[kPlanBallots];
+    if (dest_lds) {
 #pragma unroll
-    for (int k = 0; k < kPlanBallots; ++k) {
-      const int kk = rank[k] >= 0 ? off + rank[k] : 0;
-      dblk[k] = dest[kk / S];
+      for (int k = 0; k < kPlanBallots; ++k) {
+        dblk[k] = dest_s[bd.div(rank[k] >= 0 ? off + rank[k] : 0)];
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < kPlanBallots; ++k) {
+        dblk[k] = dest[bd.div(rank[k] >= 0 ? off + rank[k] : 0)];
+      }
     }
 #pragma unroll
     for (int k = 0; k < kPlanBallots; ++k) {
@@ -378,8 +445,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
       if (p < n) {
         if (rank[k] >= 0) {
           const int kk = off + rank[k];
-          plan[kk] = phys0[k] * S + p % S;
-          ts[p] = dblk[k] * S + kk % S;
+          plan[kk] = phys0[k] * S + bd.mod(p);
+          ts[p] = dblk[k] * S + bd.mod(kk);
         } else {
           ts[p] = -1;
         }
@@ -399,6 +466,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
 // workgroup runs the admission over the counts held in LDS, and wave w builds the same requests'
 // tables, token slots and source plans (wave-level ballots and lane prefix counts).
 // ------------------------------------------------------------------------------------------
+template <bool kPow2>
 __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
   __shared__ int lds[kPlanThreads / 64][4];
   __shared__ int first_error_req;
@@ -410,6 +478,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
   constexpr int kWaves = kPlanThreads / 64;
   const int R = a.num_reqs;
   const int S = a.block_size;
+  const BlockDiv<kPow2> bd(S);
 
   for (int r = wave; r < R; r += kWaves) {
     const int n = a.seq_lens[r];
@@ -454,6 +523,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
 
   const Admission adm = admit_requests(
       a, [&](int i) { return count_s[i]; },
+      [&](int i) { return a.bt_indptr[i + 1] - a.bt_indptr[i]; },
       [&](int i, int ad, int dst, int nb, int fr) {
         a.admitted[i] = ad;
         a.dst_indptr[i] = dst;
@@ -488,12 +558,12 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
         for (int k = 0; k < kPlanBallots; ++k) {
           const int pc = min(base + k * 64 + lane, n - 1);
           l[k] = lv[pc];
-          blk[k] = bt[pc / S];
+          blk[k] = bt[bd.div(pc)];
         }
 #pragma unroll
         for (int k = 0; k < kPlanBallots; ++k) {
           const int p = base + k * 64 + lane;
-          if (p < n) ts[p] = l[k] != 0 ? blk[k] * S + p % S : -1;
+          if (p < n) ts[p] = l[k] != 0 ? blk[k] * S + bd.mod(p) : -1;
         }
       }
       continue;
@@ -517,7 +587,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
       for (int k = 0; k < kPlanBallots; ++k) {
         const int pc = min(base + k * 64 + lane, n - 1);
         l[k] = lv[pc];
-        blk[k] = bt[pc / S];
+        blk[k] = bt[bd.div(pc)];
       }
       // ranks first, then every lane's destination block with one unconditional load each (a
       // dead or absent token re-reads the first destination): the loads are in flight together
@@ -532,14 +602,16 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
       }
       int dblk[kPlanBallots];
 #pragma unroll
-      for (int k = 0; k < kPlanBallots; ++k) dblk[k] = dest[(rank[k] >= 0 ? rank[k] : 0) / S];
+      for (int k = 0; k < kPlanBallots; ++k) {
+        dblk[k] = dest[bd.div(rank[k] >= 0 ? rank[k] : 0)];
+      }
 #pragma unroll
       for (int k = 0; k < kPlanBallots; ++k) {
         const int p = base + k * 64 + lane;
         if (p < n) {
           if (rank[k] >= 0) {
-            plan[rank[k]] = blk[k] * S + p % S;
-            ts[p] = dblk[k] * S + rank[k] % S;
+            plan[rank[k]] = blk[k] * S + bd.mod(p);
+            ts[p] = dblk[k] * S + bd.mod(rank[k]);
           } else {
             ts[p] = -1;
           }
@@ -575,16 +647,18 @@ __global__ __launch_bounds__(kFreeThreads) void free_kernel(MetaArgs a, int32_t*
 }  // namespace
 
 hipError_t launch_build(const MetaArgs& a, hipStream_t stream) {
+  const bool pow2 = (a.block_size & (a.block_size - 1)) == 0;
   if (a.num_reqs <= kSmallReqs && a.num_tokens <= kSmallTokens) {
-    hipLaunchKernelGGL(plan_small_kernel, dim3(1), dim3(kPlanThreads), 0, stream, a);
+    hipLaunchKernelGGL(pow2 ? plan_small_kernel<true> : plan_small_kernel<false>, dim3(1),
+                       dim3(kPlanThreads), 0, stream, a);
     return hipGetLastError();
   }
   if (a.num_reqs > 0) {
     hipLaunchKernelGGL(count_kernel, dim3(a.num_reqs), dim3(kCountThreads), 0, stream, a);
   }
   // at least one workgroup: an empty batch still writes the offsets' ends and the counters
-  hipLaunchKernelGGL(plan_kernel, dim3(a.num_reqs > 0 ? a.num_reqs : 1), dim3(kPlanThreads), 0,
-                     stream, a);
+  hipLaunchKernelGGL(pow2 ? plan_kernel<true> : plan_kernel<false>,
+                     dim3(a.num_reqs > 0 ? a.num_reqs : 1), dim3(kPlanThreads), 0, stream, a);
   return hipGetLastError();
 }
 
