@@ -107,6 +107,9 @@ def parse_args(argv=None):
                          "and replayed (graph_ms_per_step; for launch-bound small batches); "
                          "decode mode: the whole decode step (every layer) replayed from a "
                          "graph (after_repack.graph_step_ms)")
+    ap.add_argument("--three-calls", action="store_true",
+                    help="copy and freed list as two calls (vtoken_repack, vtoken_free_blocks) "
+                         "instead of one launch (vtoken_repack_free)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-planes", type=int, default=4,
                     help="planes of the workload the CPU oracle is timed on")
@@ -115,6 +118,12 @@ def parse_args(argv=None):
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def separate_free(args) -> bool:
+    """The copy and the freed list as two calls: asked for, or needed by copy options that
+    the one-launch call does not take."""
+    return args.three_calls or (args.variant, args.grid, args.order) != (0, 0, 0)
 
 
 def timed_graph(args, cache, batch, plan):
@@ -126,8 +135,11 @@ def timed_graph(args, cache, batch, plan):
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
         B.build_token_table(cache, batch, plan)
-        B.repack_ex(cache, batch, plan, args.variant, args.grid, args.order)
-        B.free_blocks(batch, plan)
+        if separate_free(args):
+            B.repack_ex(cache, batch, plan, args.variant, args.grid, args.order)
+            B.free_blocks(batch, plan)
+        else:
+            B.repack_free(cache, batch, plan)
     for _ in range(max(args.warmup, 1)):
         graph.replay()
     torch.cuda.synchronize()
@@ -1396,16 +1408,22 @@ def main(argv=None):
     torch.cuda.synchronize()
     log(f"setup {time.perf_counter() - t_setup:.1f} s; warmup {args.warmup} steps")
 
+    three = separate_free(args)
+
     def step(ev=None):
         if ev is not None:
             ev[0].record(stream)
         B.build_token_table(cache, batch, plan, stream)
         if ev is not None:
             ev[1].record(stream)
-        B.repack_ex(cache, batch, plan, args.variant, args.grid, args.order, stream)
+        if three:
+            B.repack_ex(cache, batch, plan, args.variant, args.grid, args.order, stream)
+        else:
+            B.repack_free(cache, batch, plan, stream=stream)
         if ev is not None:
             ev[2].record(stream)
-        B.free_blocks(batch, plan, stream=stream)
+        if three:
+            B.free_blocks(batch, plan, stream=stream)
         if ev is not None:
             ev[3].record(stream)
 
@@ -1418,10 +1436,15 @@ def main(argv=None):
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(evs[i])
+        step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
+    # the per-call breakdown: as many steps again with events between the calls (outside the
+    # timed region, so the events do not add to ms_per_step)
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
     graph_ms = timed_graph(args, cache, batch, plan) if args.graph else None
     repack_ms = [e[1].elapsed_time(e[2]) for e in evs]
     repack_avg = sum(repack_ms) / len(repack_ms)
@@ -1472,7 +1495,10 @@ def main(argv=None):
         "repack_ms_min": round(min(repack_ms), 4),
         "graph_ms_per_step": round(graph_ms, 4) if graph_ms is not None else None,
         "build_token_table_ms": round(build_ms, 4),
-        "free_blocks_ms": round(free_ms, 4),
+        "free_blocks_ms": round(free_ms, 4) if three else None,
+        "pass_calls": ("vtoken_build_token_table, vtoken_repack_ex, vtoken_free_blocks" if three
+                       else "vtoken_build_token_table, vtoken_repack_free (copy and freed "
+                            "list in one launch)"),
         "config": {
             "workload": inp.name,
             "recipe": inp.note,

@@ -180,6 +180,16 @@ vtoken_status vtoken_repack(const vtoken_cache* cache, const vtoken_batch* batch
 vtoken_status vtoken_free_blocks(const vtoken_batch* batch, const vtoken_plan* plan,
                                  int32_t* freed, int64_t freed_capacity, hipStream_t stream);
 
+/* Steps 2 and 3 in one launch (Sec. 3.3.4): vtoken_repack followed by vtoken_free_blocks on
+ * a plan of vtoken_build_token_table, for callers that enqueue the two back to back. Same
+ * arguments, checks, outputs and errors as the two calls in that order (freed_capacity >= M;
+ * the copy uses the default options). The freed list is written by the copy's own launch (one
+ * workgroup per request after the copy's); the blocks in it may be reused once that launch
+ * has executed on the stream, as after vtoken_free_blocks. */
+vtoken_status vtoken_repack_free(const vtoken_cache* cache, const vtoken_batch* batch,
+                                 const vtoken_plan* plan, int32_t* freed,
+                                 int64_t freed_capacity, hipStream_t stream);
+
 /* Debug check of the full pass's layout precondition (see the conventions above): every id
  * in block_ids[0 .. M) and free_list[0 .. free_len) lies in [0, num_blocks) and appears at
  * most once over both. Writes to *status (device int32): VTOKEN_OK; VTOKEN_ERR_BLOCK_RANGE if

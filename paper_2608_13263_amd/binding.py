@@ -117,6 +117,9 @@ _SIGNATURES = {
                                              ctypes.c_void_p]),
     "vtoken_free_blocks": (ctypes.c_int32, [ctypes.POINTER(CBatch), ctypes.POINTER(CPlan),
                                             ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]),
+    "vtoken_repack_free": (ctypes.c_int32, [ctypes.POINTER(CCache), ctypes.POINTER(CBatch),
+                                            ctypes.POINTER(CPlan), ctypes.c_void_p,
+                                            ctypes.c_int64, ctypes.c_void_p]),
     "vtoken_build_slot_mapping": (ctypes.c_int32, [ctypes.POINTER(CBatch),
                                                    ctypes.POINTER(CPlan), ctypes.c_void_p,
                                                    ctypes.c_void_p, ctypes.c_int64,
@@ -359,6 +362,15 @@ def free_blocks(batch: Batch, plan: Plan, freed=None, stream=None) -> None:
                                   int(out.numel()), _stream(stream)), "vtoken_free_blocks")
 
 
+def repack_free(cache: KVCache, batch: Batch, plan: Plan, freed=None, stream=None) -> None:
+    """vtoken_repack and vtoken_free_blocks in one launch (vtoken_repack_free)."""
+    lib = load_library()
+    c, b, p = cache.c(), batch.c(), plan.c()
+    out = plan.freed if freed is None else freed
+    _check(lib.vtoken_repack_free(ctypes.byref(c), ctypes.byref(b), ctypes.byref(p), _ptr(out),
+                                  int(out.numel()), _stream(stream)), "vtoken_repack_free")
+
+
 def check_layout(cache: KVCache, batch: Batch, workspace=None, stream=None):
     """Device check of the full pass's layout precondition (each block id in the pool and
     held at most once over the block tables and the free list); returns a device int32 [1]
@@ -378,16 +390,17 @@ def check_layout(cache: KVCache, batch: Batch, workspace=None, stream=None):
 
 def run_pass(cache: KVCache, batch: Batch, plan: Optional[Plan] = None, stream=None,
              inplace: bool = False) -> Plan:
-    """The three calls of one repack pass, enqueued in order on one stream."""
+    """One repack pass enqueued in order on one stream: the table build, then the copy and the
+    freed list (out of place in one launch, vtoken_repack_free; in place as two calls)."""
     if plan is None:
         plan = Plan.allocate(batch, cache.block_size, device=cache.kv.device, inplace=inplace)
     if inplace:
         build_token_table_inplace(cache, batch, plan, stream)
         repack_inplace(cache, batch, plan, stream)
+        free_blocks(batch, plan, stream=stream)
     else:
         build_token_table(cache, batch, plan, stream)
-        repack(cache, batch, plan, stream)
-    free_blocks(batch, plan, stream=stream)
+        repack_free(cache, batch, plan, stream=stream)
     return plan
 
 

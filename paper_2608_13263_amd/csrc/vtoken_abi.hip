@@ -177,9 +177,13 @@ vtoken_status vtoken_repack_inplace_ex(const vtoken_cache* cache, const vtoken_b
   return hip_status(vtoken::launch_repack_inplace(a, variant, stream));
 }
 
-vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* batch,
-                               const vtoken_plan* plan, const vtoken_repack_options* options,
-                               hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+// The out-of-place copy, and with freed != nullptr the freed list in the same launch.
+vtoken_status repack_out_of_place(const vtoken_cache* cache, const vtoken_batch* batch,
+                                  const vtoken_plan* plan, const vtoken_repack_options* options,
+                                  int32_t* freed, int64_t freed_capacity, hipStream_t stream) {
   vtoken_status s = check_cache(cache);
   if (s != VTOKEN_OK) return s;
   if ((s = check_batch(batch)) != VTOKEN_OK) return s;
@@ -200,8 +204,9 @@ vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* ba
   // the copy never needs more destination blocks than the free list or the plan holds
   const int64_t by_plan = plan->src_plan_capacity / cache->block_size;
   int64_t max_used = batch->free_len < by_plan ? batch->free_len : by_plan;
-  if (max_used == 0) return VTOKEN_OK;  // nothing can have been admitted
-  vtoken::CopyArgs a;
+  // nothing can have been copied (requests with no live token may still release blocks)
+  if (max_used == 0 && (freed == nullptr || batch->num_reqs == 0)) return VTOKEN_OK;
+  vtoken::CopyArgs a = {};
   a.kv = static_cast<uint8_t*>(cache->kv);
   a.row_bytes = (int64_t)cache->num_kv_heads * cache->head_dim * cache->elem_bytes;
   a.plane_bytes = (int64_t)cache->num_blocks * cache->block_size * a.row_bytes;
@@ -217,7 +222,43 @@ vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* ba
   a.src_plan = plan->src_plan;
   a.free_list = batch->free_list;
   a.counters = plan->counters;
+  if (freed != nullptr) {
+    a.num_reqs = batch->num_reqs;
+    a.num_bt_entries = batch->num_bt_entries;
+    a.bt_indptr = batch->bt_indptr;
+    a.block_ids = batch->block_ids;
+    a.admitted = plan->admitted;
+    a.freed_indptr = plan->freed_indptr;
+    a.freed = freed;
+    a.freed_capacity = freed_capacity;
+  }
   return hip_status(vtoken::launch_repack(a, variant, grid, order, stream));
+}
+}  // namespace
+
+extern "C" {
+
+vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* batch,
+                               const vtoken_plan* plan, const vtoken_repack_options* options,
+                               hipStream_t stream) {
+  return repack_out_of_place(cache, batch, plan, options, nullptr, 0, stream);
+}
+
+vtoken_status vtoken_repack_free(const vtoken_cache* cache, const vtoken_batch* batch,
+                                 const vtoken_plan* plan, int32_t* freed,
+                                 int64_t freed_capacity, hipStream_t stream) {
+  vtoken_status s = check_batch(batch);
+  if (s != VTOKEN_OK) return s;
+  if (plan == nullptr || plan->counters == nullptr || plan->freed_indptr == nullptr) {
+    return VTOKEN_ERR_NULL;
+  }
+  if (batch->num_reqs > 0 && plan->admitted == nullptr) return VTOKEN_ERR_NULL;
+  if (freed_capacity < batch->num_bt_entries) return VTOKEN_ERR_CAPACITY;
+  if (batch->num_bt_entries > 0 && freed == nullptr) return VTOKEN_ERR_NULL;
+  // with no table entries there is nothing to release: the copy alone
+  return repack_out_of_place(cache, batch, plan, nullptr,
+                             batch->num_bt_entries > 0 ? freed : nullptr, freed_capacity,
+                             stream);
 }
 
 vtoken_status vtoken_repack(const vtoken_cache* cache, const vtoken_batch* batch,

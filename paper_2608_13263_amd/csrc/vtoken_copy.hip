@@ -94,6 +94,12 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
     plan_mode_error(a.counters);
     return;
   }
+  if (static_cast<int>(blockIdx.x) >= a.copy_grid) {   // the freed list (vtoken_repack_free)
+    write_freed_blocks(static_cast<int>(blockIdx.x) - a.copy_grid, a.admitted, a.bt_indptr,
+                       a.freed_indptr, a.block_ids, a.num_bt_entries, a.freed,
+                       a.freed_capacity);
+    return;
+  }
   int used = a.counters[0];
   used = used < 0 ? 0 : (used > a.max_used ? a.max_used : used);
   if (used == 0) return;
@@ -119,8 +125,9 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
   if (w >= items) return;
   int hi = static_cast<int>(w / inner);
   int lo = static_cast<int>(w - (int64_t)hi * inner);
-  const int step_hi = static_cast<int>(gridDim.x / inner);
-  const int step_lo = static_cast<int>(gridDim.x - (int64_t)step_hi * inner);
+  const int grid = a.copy_grid;
+  const int step_hi = grid / inner;
+  const int step_lo = grid - step_hi * inner;
 
   // prefetch of the next item's destination block and plan entry (lanes >= S read entry
   // S-1 and never use it; the loads are unconditional so no branch splits the copy loop)
@@ -130,7 +137,7 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
   int next_dblk = a.free_list[next_g];
   int next_pv = kSmallS ? a.src_plan[(int64_t)next_g * S + plan_lane] : -1;
 
-  for (; w < items; w += gridDim.x) {
+  for (; w < items; w += grid) {
     const int plane = plane_major ? hi : lo;
     const int g = next_g;
     const int part = next_gp - g * parts;
@@ -143,7 +150,7 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
       ++hi;
     }
     // past the last item the prefetch re-reads item 0's entries (in bounds, unused)
-    next_gp = (w + gridDim.x < items) ? (plane_major ? lo : hi) : 0;
+    next_gp = (w + grid < items) ? (plane_major ? lo : hi) : 0;
     next_g = next_gp / parts;
     next_dblk = a.free_list[next_g];
     if (kSmallS) next_pv = a.src_plan[(int64_t)next_g * S + plan_lane];
@@ -205,9 +212,15 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
 constexpr int64_t kMaxCopyGrid = 1 << 19;
 
 template <void (*kKernel)(CopyArgs)>
-hipError_t launch_kernel(const CopyArgs& a, int64_t items, int grid, hipStream_t stream) {
+hipError_t launch_kernel(const CopyArgs& a_in, int64_t items, int grid, hipStream_t stream) {
   if (grid <= 0) grid = static_cast<int>(items < kMaxCopyGrid ? items : kMaxCopyGrid);
-  hipLaunchKernelGGL(kKernel, dim3(grid), dim3(kCopyThreads), 0, stream, a);
+  CopyArgs a = a_in;
+  a.copy_grid = grid;
+  // the freed list's workgroups follow the copy's
+  const int64_t total = grid + (a.freed != nullptr ? (int64_t)a.num_reqs : 0);
+  if (total <= 0) return hipSuccess;
+  hipLaunchKernelGGL(kKernel, dim3(static_cast<unsigned>(total)), dim3(kCopyThreads), 0, stream,
+                     a);
   return hipGetLastError();
 }
 

@@ -76,7 +76,38 @@ struct CopyArgs {
   const int32_t* src_plan;
   const int32_t* free_list;
   int32_t* counters;        // read; the status word is set if the plan's mode does not match
+  int32_t copy_grid;        // workgroups of the copy (set by the launch)
+  // the freed list in the same launch (vtoken_repack_free): the num_reqs workgroups after the
+  // copy's write request r's released blocks; freed == nullptr: none
+  int32_t num_reqs;
+  int64_t num_bt_entries;
+  const int32_t* bt_indptr;
+  const int32_t* block_ids;
+  const int32_t* admitted;
+  const int32_t* freed_indptr;
+  int32_t* freed;
+  int64_t freed_capacity;
 };
+
+// The released blocks of request r, written to freed[freed_indptr[r] ..): the last
+// freed_indptr[r+1] - freed_indptr[r] entries of its old table (all of it out of place, the
+// part past the new table in place), for an admitted request; nothing for the others. The
+// threads of the calling workgroup share the copy; ranges are checked before any access.
+__device__ inline void write_freed_blocks(int r, const int32_t* admitted,
+                                          const int32_t* bt_indptr, const int32_t* freed_indptr,
+                                          const int32_t* block_ids, int64_t num_bt_entries,
+                                          int32_t* freed, int64_t capacity) {
+  if (!admitted[r]) return;
+  const int b0 = bt_indptr[r];
+  const int m = bt_indptr[r + 1] - b0;
+  const int64_t o = freed_indptr[r];
+  const int n = freed_indptr[r + 1] - freed_indptr[r];
+  if (b0 < 0 || m < 0 || (int64_t)b0 + m > num_bt_entries || o < 0 || n < 0 || n > m) return;
+  const int first = b0 + m - n;
+  for (int j = threadIdx.x; j < n; j += blockDim.x) {
+    if (o + j < capacity) freed[o + j] = block_ids[first + j];
+  }
+}
 
 // Arguments of the in-place copy: one workgroup per (request, plane) chain.
 struct InplaceArgs {

@@ -19,6 +19,9 @@
 namespace vtoken {
 namespace {
 
+static_assert(kPlanThreads % 64 == 0 && kPlanThreads <= 1024,
+              "the workgroup scans take at most 16 waves");
+
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 
 // Number of set bits of a wave-wide ballot in the lanes below this one.
@@ -49,18 +52,35 @@ __device__ __forceinline__ int wave_inclusive_scan(int v) {
   return v + (row >= 1 ? t0 : 0) + (row >= 2 ? t1 : 0) + (row >= 3 ? t2 : 0);
 }
 
-// Exclusive scan of NV values per thread across the workgroup; total[k] is the sum. The wave
-// totals go through LDS once: lane w of every wave reads wave w's total and a second wave scan
-// gives each wave its offset.
+// Inclusive prefix sum over lanes 0-15 (the first DPP row); the other rows scan their own.
+__device__ __forceinline__ int row_inclusive_scan(int v) {
+  v += row_shr<1>(v);
+  v += row_shr<2>(v);
+  v += row_shr<4>(v);
+  return v + row_shr<8>(v);
+}
+
+// Exclusive scan of NV values per thread across the workgroup (at most 16 waves); total[k] is
+// the sum. A wave whose values are all zero (requests past the batch's end) skips its own
+// scan. The wave totals go through LDS once: lane w of every wave reads wave w's total and a
+// 16-lane scan gives each wave its offset.
 template <int NV>
 __device__ __forceinline__ void block_exclusive_scan(int (&v)[NV], int (&total)[NV],
                                                      int (*lds)[NV]) {
   const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
   const int nwaves = blockDim.x >> 6;
-  int incl[NV];
+  int any = 0;
 #pragma unroll
-  for (int k = 0; k < NV; ++k) incl[k] = wave_inclusive_scan(v[k]);
+  for (int k = 0; k < NV; ++k) any |= v[k];
+  int incl[NV];
+  if (__ballot(any != 0) != 0) {
+#pragma unroll
+    for (int k = 0; k < NV; ++k) incl[k] = wave_inclusive_scan(v[k]);
+  } else {
+#pragma unroll
+    for (int k = 0; k < NV; ++k) incl[k] = 0;
+  }
   if (lane == 63) {
 #pragma unroll
     for (int k = 0; k < NV; ++k) lds[wave][k] = incl[k];
@@ -68,7 +88,7 @@ __device__ __forceinline__ void block_exclusive_scan(int (&v)[NV], int (&total)[
   __syncthreads();
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
-    const int wt = wave_inclusive_scan(lane < nwaves ? lds[lane][k] : 0);
+    const int wt = row_inclusive_scan(lane < nwaves ? lds[lane][k] : 0);
     const int off = wave > 0 ? __builtin_amdgcn_readlane(wt, wave - 1) : 0;
     total[k] = __builtin_amdgcn_readlane(wt, nwaves - 1);
     v[k] = off + incl[k] - v[k];
@@ -157,8 +177,9 @@ __global__ __launch_bounds__(kCountThreads) void count_kernel(MetaArgs a) {
 }
 
 // The admission over all requests, every thread of the workgroup taking part (R/1024 rounds of
-// two workgroup scans): destination need ceil(live/S), strict gain (Sec. 3.3.3, I4 of Sec.
-// 3.5), prefix admission against the free list (Sec. 3.3.2). count(i) is request i's live count
+// two workgroup scans; one wave alone, with wave scans, when R <= 64): destination need
+// ceil(live/S), strict gain (Sec. 3.3.3, I4 of Sec. 3.5), prefix admission against the free
+// list (Sec. 3.3.2). count(i) is request i's live count
 // (a negative error code for a request the validation rejected), blocks(i) the length of its
 // old table; visit(i, admitted, destination offset, new-table offset, freed offset) is called
 // once per request by the thread holding it.
@@ -173,6 +194,41 @@ __device__ __forceinline__ Admission admit_requests(const MetaArgs& a, Count cou
   const int tid = threadIdx.x;
   const int R = a.num_reqs;
   const int S = a.block_size;
+  if (R <= 64) {
+    // one wave holds every request: the same rules with wave scans only, no workgroup
+    // barrier until the totals are published
+    if (tid < 64) {
+      const int i = tid;
+      const bool valid = i < R;
+      const int c = valid ? count(i) : 0;
+      const int m = valid ? blocks(i) : 0;
+      const uint64_t errors = __ballot(valid && c < 0);
+      const int need = c > 0 ? (c + S - 1) / S : 0;
+      const bool profitable = valid && c >= 0 && need < m;
+      const int e = profitable ? need : 0;
+      const int o = wave_inclusive_scan(e) - e;
+      const bool adm = profitable && (a.inplace || o + need <= a.free_len);
+      const int n_free = adm ? (a.inplace ? m - need : m) : 0;
+      const int d = adm ? need : 0, nb = adm ? need : m;
+      const int di = wave_inclusive_scan(d);
+      const int ni = wave_inclusive_scan(nb);
+      const int fi = wave_inclusive_scan(n_free);
+      if (valid) visit(i, adm ? 1 : 0, di - d, ni - nb, fi - n_free);
+      const int used = __builtin_amdgcn_readlane(di, 63);
+      const int n_new = __builtin_amdgcn_readlane(ni, 63);
+      const int n_freed = __builtin_amdgcn_readlane(fi, 63);
+      const int n_adm = __popcll(__ballot(adm));
+      if (tid == 0) {
+        lds[0][0] = used;
+        lds[0][1] = n_new;
+        lds[0][2] = n_freed;
+        lds[0][3] = n_adm;
+        *first_error_req = errors != 0 ? __builtin_ctzll(errors) : INT_MAX;
+      }
+    }
+    __syncthreads();
+    return Admission{lds[0][0], lds[0][1], lds[0][2], lds[0][3], *first_error_req};
+  }
   if (tid == 0) *first_error_req = INT_MAX;
   __syncthreads();
   int carry_e = 0, carry_dst = 0, carry_new = 0, carry_freed = 0, n_admitted = 0;
@@ -186,9 +242,9 @@ __device__ __forceinline__ Admission admit_requests(const MetaArgs& a, Count cou
     const bool profitable = valid && c >= 0 && need < m;
     // position of this request's destinations in the free list: needs of every earlier
     // profitable request (admitted or not - once one is deferred all later ones are)
-    int s1[4] = {profitable ? need : 0, 0, 0, 0};
-    int t1[4];
-    block_exclusive_scan<4>(s1, t1, lds);
+    int s1[1] = {profitable ? need : 0};
+    int t1[1];
+    block_exclusive_scan<1>(s1, t1, reinterpret_cast<int (*)[1]>(lds));
     // in place the destinations are the request's own blocks: nothing to wait for
     const bool adm = profitable && (a.inplace || carry_e + s1[0] + need <= a.free_len);
     // freed: all old blocks out of place, the blocks past the need in place
@@ -464,22 +520,42 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
 // kSmallTokens tokens), where the pass is bound by launch latency: one launch instead of two.
 // Wave w validates and counts requests w, w + 16, ... (64-token ballots, eight in flight), the
 // workgroup runs the admission over the counts held in LDS, and wave w builds the same requests'
-// tables, token slots and source plans (wave-level ballots and lane prefix counts).
+// tables, token slots and source plans (wave-level ballots and lane prefix counts). The first
+// tile of a wave's first request stays in registers from the counting to the build, and the
+// head of the free list is read once into LDS, so that a small pass waits for few dependent
+// loads.
 // ------------------------------------------------------------------------------------------
 template <bool kPow2>
 __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
   __shared__ int lds[kPlanThreads / 64][4];
   __shared__ int first_error_req;
   __shared__ int count_s[kSmallReqs];
+  __shared__ int meta_s[kSmallReqs][4];   // tokens, first token, first table entry, blocks
   __shared__ int plan_s[kSmallReqs][4];   // admitted, destination, new-table and freed offsets
+  __shared__ int32_t head[kPlanHead];     // free_list[0 .. P)
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   constexpr int kWaves = kPlanThreads / 64;
+  constexpr int kTile = 64 * kPlanBallots;
   const int R = a.num_reqs;
   const int S = a.block_size;
   const BlockDiv<kPow2> bd(S);
 
+  // the head of the free list (out of place), loaded first and written to LDS after the
+  // counting: destinations and the consumed-entry range check read it there
+  const int P = a.inplace ? 0 : min(a.free_len, kPlanHead);
+  int32_t fl[kPlanHead / kPlanThreads];
+#pragma unroll
+  for (int q = 0; q < kPlanHead / kPlanThreads; ++q) {
+    const int j = q * kPlanThreads + tid;
+    fl[q] = j < P ? a.free_list[j] : 0;
+  }
+
+  // validation and live count per request; the first tile of the wave's first request (mask
+  // bytes and table entries) stays in registers for the build below
+  uint8_t keep_l[kPlanBallots] = {};
+  int keep_b[kPlanBallots] = {};
   for (int r = wave; r < R; r += kWaves) {
     const int n = a.seq_lens[r];
     const int t0 = a.tok_indptr[r], t1 = a.tok_indptr[r + 1];
@@ -491,21 +567,43 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
                (int64_t)b1 - b0 != ((int64_t)n + S - 1) / S) {
       code = VTOKEN_ERR_BT_LEN;
     }
-    if (code == 0) {
-      bool bad = false;
-      for (int j = b0 + lane; j < b1; j += 64) {
-        const int blk = a.block_ids[j];
-        bad |= blk < 0 || blk >= a.num_blocks;
-      }
-      if (__ballot(bad) != 0) code = VTOKEN_ERR_BLOCK_RANGE;
-    }
     int c = code;
     if (code == 0) {
       const uint8_t* lv = a.live + t0;
+      const int32_t* bt = a.block_ids + b0;
+      const int m = b1 - b0;
+      // the first block ids and the first tile's mask bytes and table entries are in flight
+      // together (positions clamped to the last token; the ranges were checked above)
+      const int bid = lane < m ? bt[lane] : 0;
+      uint8_t l[kPlanBallots] = {};
+      int blk[kPlanBallots] = {};
+      if (n > 0) {
+#pragma unroll
+        for (int k = 0; k < kPlanBallots; ++k) {
+          const int pc = min(k * 64 + lane, n - 1);
+          l[k] = lv[pc];
+          blk[k] = bt[bd.div(pc)];
+        }
+      }
+      bool bad = lane < m && (bid < 0 || bid >= a.num_blocks);
+      for (int j = 64 + lane; j < m; j += 64) {
+        const int x = bt[j];
+        bad |= x < 0 || x >= a.num_blocks;
+      }
       c = 0;
-      for (int base = 0; base < n; base += 64 * kPlanBallots) {
+#pragma unroll
+      for (int k = 0; k < kPlanBallots; ++k) {
+        c += __popcll(__ballot(k * 64 + lane < n && l[k] != 0));
+      }
+      if (r == wave) {
+#pragma unroll
+        for (int k = 0; k < kPlanBallots; ++k) {
+          keep_l[k] = l[k];
+          keep_b[k] = blk[k];
+        }
+      }
+      for (int base = kTile; base < n; base += kTile) {
         // unconditional loads (positions clamped to the last token) keep all eight in flight
-        uint8_t l[kPlanBallots];
 #pragma unroll
         for (int k = 0; k < kPlanBallots; ++k) l[k] = lv[min(base + k * 64 + lane, n - 1)];
 #pragma unroll
@@ -513,17 +611,26 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
           c += __popcll(__ballot(base + k * 64 + lane < n && l[k] != 0));
         }
       }
+      if (__ballot(bad) != 0) c = VTOKEN_ERR_BLOCK_RANGE;
     }
     if (lane == 0) {
       a.live_count[r] = c;
       count_s[r] = c;
+      meta_s[r][0] = n;
+      meta_s[r][1] = t0;
+      meta_s[r][2] = b0;
+      meta_s[r][3] = b1 - b0;
     }
+  }
+#pragma unroll
+  for (int q = 0; q < kPlanHead / kPlanThreads; ++q) {
+    const int j = q * kPlanThreads + tid;
+    if (j < P) head[j] = fl[q];
   }
   __syncthreads();
 
   const Admission adm = admit_requests(
-      a, [&](int i) { return count_s[i]; },
-      [&](int i) { return a.bt_indptr[i + 1] - a.bt_indptr[i]; },
+      a, [&](int i) { return count_s[i]; }, [&](int i) { return meta_s[i][3]; },
       [&](int i, int ad, int dst, int nb, int fr) {
         a.admitted[i] = ad;
         a.dst_indptr[i] = dst;
@@ -536,30 +643,40 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
       },
       lds, &first_error_req);
   const int status = admission_status(
-      a, adm, adm.first_error == INT_MAX ? 0 : count_s[adm.first_error], true);
+      a, adm, adm.first_error == INT_MAX ? 0 : count_s[adm.first_error], true, head, P);
   if (status != 0) return;
 
   for (int r = wave; r < R; r += kWaves) {
-    const int n = a.seq_lens[r];
-    const int t0 = a.tok_indptr[r];
-    const int b0 = a.bt_indptr[r];
-    const uint8_t* lv = a.live + t0;
-    const int32_t* bt = a.block_ids + b0;
-    int32_t* ts = a.token_slot + t0;
+    const int n = meta_s[r][0];
+    const uint8_t* lv = a.live + meta_s[r][1];
+    const int32_t* bt = a.block_ids + meta_s[r][2];
+    int32_t* ts = a.token_slot + meta_s[r][1];
     int32_t* nbt = a.new_block_ids + plan_s[r][2];
-    if (!plan_s[r][0]) {
-      // unchanged: the old table, every live token at its positional slot
-      const int m = a.bt_indptr[r + 1] - b0;
-      for (int j = lane; j < m; j += 64) nbt[j] = bt[j];
-      for (int base = 0; base < n; base += 64 * kPlanBallots) {
-        uint8_t l[kPlanBallots];
-        int blk[kPlanBallots];
+    const bool kept = r == wave;   // first tile in registers
+    uint8_t l[kPlanBallots];
+    int blk[kPlanBallots];
+    auto tile = [&](int base) {
+      if (base == 0 && kept) {
+#pragma unroll
+        for (int k = 0; k < kPlanBallots; ++k) {
+          l[k] = keep_l[k];
+          blk[k] = keep_b[k];
+        }
+      } else {
 #pragma unroll
         for (int k = 0; k < kPlanBallots; ++k) {
           const int pc = min(base + k * 64 + lane, n - 1);
           l[k] = lv[pc];
           blk[k] = bt[bd.div(pc)];
         }
+      }
+    };
+    if (!plan_s[r][0]) {
+      // unchanged: the old table, every live token at its positional slot
+      const int m = meta_s[r][3];
+      for (int j = lane; j < m; j += 64) nbt[j] = bt[j];
+      for (int base = 0; base < n; base += kTile) {
+        tile(base);
 #pragma unroll
         for (int k = 0; k < kPlanBallots; ++k) {
           const int p = base + k * 64 + lane;
@@ -571,26 +688,22 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
     const int o = plan_s[r][1];
     const int c = count_s[r];
     const int need = (c + S - 1) / S;
+    // destinations: the LDS head of the free list when they lie in it
+    const bool dest_lds = !a.inplace && o + need <= P;
     const int32_t* dest = a.inplace ? bt : a.free_list + o;
+    const int32_t* dest_s = head + o;
     int32_t* plan = a.src_plan + (int64_t)o * S;
-    for (int j = lane; j < need; j += 64) nbt[j] = dest[j];
+    for (int j = lane; j < need; j += 64) nbt[j] = dest_lds ? dest_s[j] : dest[j];
     if (need == 0) {
       // no live token (every block is released): only dead slots to write
       for (int p = lane; p < n; p += 64) ts[p] = -1;
       continue;
     }
     int carry = 0;
-    for (int base = 0; base < n; base += 64 * kPlanBallots) {
-      uint8_t l[kPlanBallots];
-      int blk[kPlanBallots];
-#pragma unroll
-      for (int k = 0; k < kPlanBallots; ++k) {
-        const int pc = min(base + k * 64 + lane, n - 1);
-        l[k] = lv[pc];
-        blk[k] = bt[bd.div(pc)];
-      }
-      // ranks first, then every lane's destination block with one unconditional load each (a
-      // dead or absent token re-reads the first destination): the loads are in flight together
+    for (int base = 0; base < n; base += kTile) {
+      tile(base);
+      // ranks first, then every lane's destination block with one unconditional read each (a
+      // dead or absent token re-reads the first destination): the reads are in flight together
       int rank[kPlanBallots];
 #pragma unroll
       for (int k = 0; k < kPlanBallots; ++k) {
@@ -601,9 +714,16 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
         carry += __popcll(mk);
       }
       int dblk[kPlanBallots];
+      if (dest_lds) {
 #pragma unroll
-      for (int k = 0; k < kPlanBallots; ++k) {
-        dblk[k] = dest[bd.div(rank[k] >= 0 ? rank[k] : 0)];
+        for (int k = 0; k < kPlanBallots; ++k) {
+          dblk[k] = dest_s[bd.div(rank[k] >= 0 ? rank[k] : 0)];
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < kPlanBallots; ++k) {
+          dblk[k] = dest[bd.div(rank[k] >= 0 ? rank[k] : 0)];
+        }
       }
 #pragma unroll
       for (int k = 0; k < kPlanBallots; ++k) {
@@ -629,19 +749,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
 __global__ __launch_bounds__(kFreeThreads) void free_kernel(MetaArgs a, int32_t* freed,
                                                             int64_t capacity) {
   if (a.counters[3] != 0) return;
-  const int r = blockIdx.x;
-  if (!a.admitted[r]) return;
-  // the freed blocks are the last n entries of the old table (all of it out of place, the
-  // part past the new table in place)
-  const int b0 = a.bt_indptr[r];
-  const int m = a.bt_indptr[r + 1] - b0;
-  const int64_t o = a.freed_indptr[r];
-  const int n = a.freed_indptr[r + 1] - a.freed_indptr[r];
-  if (b0 < 0 || m < 0 || (int64_t)b0 + m > a.num_bt_entries || o < 0 || n < 0 || n > m) return;
-  const int first = b0 + m - n;
-  for (int j = threadIdx.x; j < n; j += kFreeThreads) {
-    if (o + j < capacity) freed[o + j] = a.block_ids[first + j];
-  }
+  write_freed_blocks(blockIdx.x, a.admitted, a.bt_indptr, a.freed_indptr, a.block_ids,
+                     a.num_bt_entries, freed, capacity);
 }
 
 }  // namespace

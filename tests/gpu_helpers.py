@@ -22,15 +22,18 @@ def kv_bytes(kv, shape: W.KVShape):
     return kv.view(t.uint8).reshape(shape.num_planes, n, shape.row_bytes).cpu().numpy()
 
 
-def gpu_pass(inp: W.RepackInputs, kv, variant=0, grid=0, order=0, label="", inplace=False):
-    """build_token_table -> repack_ex -> free_blocks on the current stream; returns host
-    copies of every plan output, trimmed to the sizes the counters report."""
+def gpu_pass(inp: W.RepackInputs, kv, variant=0, grid=0, order=0, label="", inplace=False,
+             fused=False):
+    """build_token_table -> repack_ex -> free_blocks on the current stream (fused: the copy and
+    the freed list in one launch, vtoken_repack_free); returns host copies of every plan
+    output, trimmed to the sizes the counters report."""
     t = torch()
     from paper_2608_13263_amd import binding as B
     print(f"[gpu] {label or inp.name}: R={inp.num_reqs} T={inp.num_tokens} "
           f"M={inp.num_bt_entries} f={len(inp.free_list)} S={inp.shape.block_size} "
           f"row={inp.shape.row_bytes}B planes={inp.shape.num_planes} "
-          f"variant={variant} grid={grid} order={order} inplace={inplace}", flush=True)
+          f"variant={variant} grid={grid} order={order} inplace={inplace} fused={fused}",
+          flush=True)
     cache = B.KVCache(kv, inp.shape.num_layers, inp.shape.num_kv_heads, inp.shape.head_dim,
                       inp.shape.block_size)
     batch = B.Batch.from_inputs(inp)
@@ -38,10 +41,15 @@ def gpu_pass(inp: W.RepackInputs, kv, variant=0, grid=0, order=0, label="", inpl
     if inplace:
         B.build_token_table_inplace(cache, batch, plan)
         B.repack_inplace_ex(cache, batch, plan, variant=variant)
+    elif fused:
+        assert (variant, grid, order) == (0, 0, 0), "the fused call uses the default copy"
+        B.build_token_table(cache, batch, plan)
+        B.repack_free(cache, batch, plan)
     else:
         B.build_token_table(cache, batch, plan)
         B.repack_ex(cache, batch, plan, variant=variant, grid=grid, order=order)
-    B.free_blocks(batch, plan)
+    if not fused:
+        B.free_blocks(batch, plan)
     t.cuda.synchronize()
     return plan_to_host(plan, inp)
 
@@ -88,14 +96,15 @@ def assert_kv_equal(got: np.ndarray, expect: np.ndarray) -> None:
 
 
 def full_parity(inp: W.RepackInputs, seed: int = 0, variant=0, grid=0, order=0,
-                inplace=False):
+                inplace=False, fused=False):
     """Seeded KV on the device, one pass through the C ABI, every output and every KV byte
     against the oracle run on the pre-call bytes."""
     t = torch()
     kv = W.kv_device(inp.shape, inp.num_blocks, seed)
     before = kv_bytes(kv, inp.shape)
     orc = oracle_repack_inputs(inp, before, inplace=inplace)
-    gpu = gpu_pass(inp, kv, variant=variant, grid=grid, order=order, inplace=inplace)
+    gpu = gpu_pass(inp, kv, variant=variant, grid=grid, order=order, inplace=inplace,
+                   fused=fused)
     assert_plan_equal(gpu, orc)
     assert_kv_equal(kv_bytes(kv, inp.shape), orc.kv)
     del kv

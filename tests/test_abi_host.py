@@ -139,6 +139,23 @@ def test_repack_and_free_reject_bad_arguments():
                              None) == 0
 
 
+def test_repack_free_rejects_bad_arguments():
+    """The one-launch copy and freed list checks what vtoken_repack and vtoken_free_blocks
+    check, before enqueueing anything."""
+    lib = B.load_library()
+    cache, batch, plan = _good()
+    call = lambda c, b, p, freed, cap: lib.vtoken_repack_free(  # noqa: E731
+        c, b, p, freed, cap, None)
+    C, Bt, P = ctypes.byref(cache), ctypes.byref(batch), ctypes.byref(plan)
+    assert call(C, Bt, P, _fake_ptr(), 3) == B.STATUS_CODE["VTOKEN_ERR_CAPACITY"]
+    assert call(C, Bt, P, None, 4) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    assert call(None, Bt, P, _fake_ptr(), 4) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    assert call(C, None, P, _fake_ptr(), 4) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    assert call(C, Bt, None, _fake_ptr(), 4) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
+    plan.freed_indptr = None
+    assert call(C, Bt, P, _fake_ptr(), 4) == B.STATUS_CODE["VTOKEN_ERR_NULL"]
+
+
 def test_decode_workspace_bytes():
     lib = B.load_library()
     # R * Hq * ceil(max_tokens / (16384 / D)) * (D + 2) float32 partial records, at least one

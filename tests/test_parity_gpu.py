@@ -18,6 +18,10 @@ def test_tiny_cache():
     full_parity(W.tiny_cache(101), seed=1)
 
 
+def test_tiny_cache_copy_and_free_in_one_launch():
+    full_parity(W.tiny_cache(101), seed=1, fused=True)
+
+
 def test_tiny_cache_other_seed():
     full_parity(W.tiny_cache(7), seed=2)
 
@@ -61,13 +65,14 @@ def _edge_masks(S, rng):
     ]
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["three_calls", "repack_free"])
 @pytest.mark.parametrize("S", [1, 2, 16, 32, 48, 128])
-def test_edge_masks_block_sizes(S):
+def test_edge_masks_block_sizes(S, fused):
     # S = 48 (not a power of two, several copy rounds) and S = 128 (plan read from memory)
     rng = np.random.default_rng(S)
     shape = W.KVShape(1, 2, 64, S, "fp16")
     inp = W.from_masks(_edge_masks(S, rng), shape, free_blocks=64, seed=S)
-    full_parity(inp, seed=S)
+    full_parity(inp, seed=S, fused=fused)
 
 
 @pytest.mark.parametrize("heads,dim,dtype", [(3, 8, "fp16"), (1, 8, "fp16"), (1, 16, "fp8_e4m3"),
@@ -80,20 +85,35 @@ def test_row_geometries(heads, dim, dtype):
     full_parity(W.from_masks(masks, shape, free_blocks=80, seed=3), seed=9)
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["three_calls", "repack_free"])
 @pytest.mark.parametrize("free_blocks", [0, 1, 3, 6])
-def test_headroom_deferral(free_blocks):
+def test_headroom_deferral(free_blocks, fused):
     # a short free list: the admitted requests are a prefix of the profitable ones
     rng = np.random.default_rng(11)
     shape = W.KVShape(1, 2, 64, 16, "fp16")
     masks = [list((rng.random(int(n)) < 0.3).astype(int)) for n in rng.integers(40, 120, 8)]
     inp = W.from_masks(masks, shape, free_blocks=free_blocks, seed=5)
-    gpu, orc = full_parity(inp, seed=12)
+    gpu, orc = full_parity(inp, seed=12, fused=fused)
     assert orc.used <= free_blocks
 
 
-def test_no_requests():
+@pytest.mark.parametrize("fused", [False, True], ids=["three_calls", "repack_free"])
+def test_empty_free_list_releases_dead_requests(fused):
+    """No free block at all: only requests with no live token are admitted (they need no
+    destination), so nothing is copied, yet their blocks are released."""
     shape = W.KVShape(1, 2, 64, 16, "fp16")
-    full_parity(W.from_masks([], shape, free_blocks=8, seed=1), seed=1)
+    # two requests with no live token first (admitted: 4 + 2 blocks released), then two that
+    # need destinations (deferred)
+    masks = [[0] * 50, [0] * 17, [1, 0] * 30, [1] * 5 + [0] * 40]
+    inp = W.from_masks(masks, shape, free_blocks=0, seed=2)
+    gpu, orc = full_parity(inp, seed=3, fused=fused)
+    assert orc.used == 0 and orc.n_freed == 4 + 2 and gpu["n_admitted"] == 2
+
+
+@pytest.mark.parametrize("fused", [False, True], ids=["three_calls", "repack_free"])
+def test_no_requests(fused):
+    shape = W.KVShape(1, 2, 64, 16, "fp16")
+    full_parity(W.from_masks([], shape, free_blocks=8, seed=1), seed=1, fused=fused)
 
 
 def test_nan_payloads_are_copied_bit_exactly():
@@ -166,22 +186,25 @@ def test_side_stream_and_stream_order():
 # device-detected errors: status word set, no KV byte written
 # ------------------------------------------------------------------------------------------
 
-@pytest.fixture(params=["small", "large"])
+@pytest.fixture(params=["small", "large", "large_repack_free"])
 def error_batch(request):
     """A batch under the one-launch planning bound (16384 tokens, 256 requests) and one above it
-    (count launch + plan launch): every device-detected error is checked on both paths."""
+    (count launch + plan launch): every device-detected error is checked on both paths, and
+    with the copy and the freed list in one launch."""
     lens = (300, 900) if request.param == "small" else (4000, 6000)
-    return lambda: W.llama3_8b_random(207, num_layers=1, num_reqs=5, len_range=lens)
+    make = lambda: W.llama3_8b_random(207, num_layers=1, num_reqs=5, len_range=lens)  # noqa
+    return make, request.param.endswith("repack_free")
 
 
-def _error_case(mutate, expect, make):
+def _error_case(mutate, expect, batch):
     t = torch()
     from paper_2608_13263_amd import binding as B
+    make, fused = batch
     inp = make()
     mutate(inp)
     kv = W.kv_device(inp.shape, inp.num_blocks, 5)
     before = kv_bytes(kv, inp.shape)
-    gpu = gpu_pass(inp, kv, label=f"error case {expect}")
+    gpu = gpu_pass(inp, kv, label=f"error case {expect}", fused=fused)
     assert gpu["status"] == B.STATUS_CODE[expect]
     assert gpu["used"] == 0 and gpu["n_admitted"] == 0 and gpu["n_freed"] == 0
     assert_kv_equal(kv_bytes(kv, inp.shape), before)
@@ -301,6 +324,7 @@ def test_random_geometries(seed):
     inp = _random_case(1000 + seed)
     full_parity(inp, seed=seed)
     full_parity(inp, seed=seed, inplace=True)
+    full_parity(inp, seed=seed, fused=True)
 
 
 @pytest.mark.parametrize("extra", [0, 1], ids=["at_token_bound", "past_token_bound"])
