@@ -17,6 +17,8 @@
  *                              all KV heads in one launch (the only call touching KV bytes)
  *   vtoken_free_blocks         emits the list of freed source blocks
  *
+ * vtoken_repack_free enqueues the last two in one launch (same effects and errors).
+ *
  * General conventions (all calls):
  *   - Pointers inside the structs are DEVICE pointers unless a field says [host].
  *   - The caller owns every buffer; the library keeps no pointer after a call returns,
