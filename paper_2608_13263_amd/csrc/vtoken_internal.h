@@ -284,4 +284,58 @@ int num_repack_variants();
 constexpr int64_t kMaxChunkUnits = (1 << 20) - 1;
 constexpr int64_t kMaxRowUnits = 1 << 12;
 
+// ---- device helpers shared by the metadata kernels (vtoken_kernels.hip, vtoken_planner.hip,
+// which bring them in with `using namespace vtoken::meta`)
+namespace meta {
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+// Number of set bits of a wave-wide ballot in the lanes below this one.
+__device__ __forceinline__ int lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
+}
+
+// Lane i of each 16-lane row receives lane i - kN of its row, 0 for i < kN (DPP row shift).
+template <int kN>
+__device__ __forceinline__ int row_shr(int x) {
+  static_assert(kN > 0 && kN < 16, "row shift");
+  return __builtin_amdgcn_update_dpp(0, x, 0x110 + kN, 0xF, 0xF, true);
+}
+
+// Inclusive prefix sum over the 64 lanes (every lane active): within each 16-lane row by DPP
+// row shifts (no LDS), then each row adds the totals of the rows below it, read from lanes
+// 15, 31 and 47.
+__device__ __forceinline__ int wave_inclusive_scan(int v) {
+  v += row_shr<1>(v);
+  v += row_shr<2>(v);
+  v += row_shr<4>(v);
+  v += row_shr<8>(v);
+  const int t0 = __builtin_amdgcn_readlane(v, 15);
+  const int t1 = __builtin_amdgcn_readlane(v, 31);
+  const int t2 = __builtin_amdgcn_readlane(v, 47);
+  const int row = lane_id() >> 4;
+  return v + (row >= 1 ? t0 : 0) + (row >= 2 ? t1 : 0) + (row >= 3 ? t2 : 0);
+}
+
+// Inclusive prefix sum over lanes 0-15 (the first DPP row); the other rows scan their own.
+__device__ __forceinline__ int row_inclusive_scan(int v) {
+  v += row_shr<1>(v);
+  v += row_shr<2>(v);
+  v += row_shr<4>(v);
+  return v + row_shr<8>(v);
+}
+
+// Division and remainder of non-negative positions and ranks by the block size S: shifts and
+// masks when S is a power of two (the kernels that divide per token are instantiated for both).
+template <bool kPow2>
+struct BlockDiv {
+  int s, sh;
+  __device__ explicit BlockDiv(int S) : s(S), sh(__ffs(S) - 1) {}
+  __device__ int div(int x) const { return kPow2 ? x >> sh : x / s; }
+  __device__ int mod(int x) const { return kPow2 ? x & (s - 1) : x % s; }
+};
+
+}  // namespace meta
+
 }  // namespace vtoken

@@ -19,46 +19,10 @@
 namespace vtoken {
 namespace {
 
+using namespace vtoken::meta;
+
 static_assert(kPlanThreads % 64 == 0 && kPlanThreads <= 1024,
               "the workgroup scans take at most 16 waves");
-
-__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
-
-// Number of set bits of a wave-wide ballot in the lanes below this one.
-__device__ __forceinline__ int lanes_below(uint64_t mask) {
-  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
-                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
-}
-
-// Lane i of each 16-lane row receives lane i - kN of its row, 0 for i < kN (DPP row shift).
-template <int kN>
-__device__ __forceinline__ int row_shr(int x) {
-  static_assert(kN > 0 && kN < 16, "row shift");
-  return __builtin_amdgcn_update_dpp(0, x, 0x110 + kN, 0xF, 0xF, true);
-}
-
-// Inclusive prefix sum over the 64 lanes (every lane active): within each 16-lane row by DPP
-// row shifts (no LDS), then each row adds the totals of the rows below it, read from lanes
-// 15, 31 and 47.
-__device__ __forceinline__ int wave_inclusive_scan(int v) {
-  v += row_shr<1>(v);
-  v += row_shr<2>(v);
-  v += row_shr<4>(v);
-  v += row_shr<8>(v);
-  const int t0 = __builtin_amdgcn_readlane(v, 15);
-  const int t1 = __builtin_amdgcn_readlane(v, 31);
-  const int t2 = __builtin_amdgcn_readlane(v, 47);
-  const int row = lane_id() >> 4;
-  return v + (row >= 1 ? t0 : 0) + (row >= 2 ? t1 : 0) + (row >= 3 ? t2 : 0);
-}
-
-// Inclusive prefix sum over lanes 0-15 (the first DPP row); the other rows scan their own.
-__device__ __forceinline__ int row_inclusive_scan(int v) {
-  v += row_shr<1>(v);
-  v += row_shr<2>(v);
-  v += row_shr<4>(v);
-  return v + row_shr<8>(v);
-}
 
 // Exclusive scan of NV values per thread across the workgroup (at most 16 waves); total[k] is
 // the sum. A wave whose values are all zero (requests past the batch's end) skips its own
@@ -95,16 +59,6 @@ __device__ __forceinline__ void block_exclusive_scan(int (&v)[NV], int (&total)[
   }
   __syncthreads();
 }
-
-// Division and remainder of non-negative positions and ranks by the block size S: shifts and
-// masks when S is a power of two (the kernels that divide per token are instantiated for both).
-template <bool kPow2>
-struct BlockDiv {
-  int s, sh;
-  __device__ explicit BlockDiv(int S) : s(S), sh(__ffs(S) - 1) {}
-  __device__ int div(int x) const { return kPow2 ? x >> sh : x / s; }
-  __device__ int mod(int x) const { return kPow2 ? x & (s - 1) : x % s; }
-};
 
 // Nonzero bytes of a 32-bit word: each byte's bits are folded into its lowest bit (the bits
 // shifted in from the next byte land at offsets >= 1 and are masked off).

@@ -15,11 +15,13 @@
 //   pl_admit_kernel    one workgroup: the trigger (F > theta_F, enough candidates, free list at
 //                      or below the watermark, Sec. 3.3.2), the bound B over the candidates in
 //                      request order, T_live, ceil(T_live / S), strict gain, admission against
-//                      the free list, and every CSR offset (Sec. 3.3.3)
+//                      the free list, and every CSR offset (Sec. 3.3.3); one wave with wave
+//                      scans for at most 64 requests
 //   pl_table_kernel    one workgroup per request: selected sources, new block table (kept
 //                      blocks then destinations), released sources, and the move list in
 //                      logical order written as token slots and the per-destination source
-//                      plan (Sec. 3.3.3, Sec. 3.2 apply_moves)
+//                      plan (Sec. 3.3.3, Sec. 3.2 apply_moves); tokens in tiles of 8192 with
+//                      every load of a tile in flight before its ballots
 //
 // Every kernel after pl_count_kernel does nothing once plan->counters[3] holds an error;
 // every dereference of caller data is bounds-checked.
@@ -28,15 +30,17 @@
 namespace vtoken {
 namespace {
 
+using namespace vtoken::meta;
+
 constexpr int kPlThreads = 256;
 constexpr int kPlWaves = kPlThreads / 64;
 constexpr int kPlAdmitThreads = 1024;
 constexpr int kPlAdmitWaves = kPlAdmitThreads / 64;
-
-__device__ __forceinline__ int pl_lanes_below(uint64_t mask) {
-  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
-                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
-}
+constexpr int kPlTableThreads = 1024;
+constexpr int kPlTableWaves = kPlTableThreads / 64;
+constexpr int kPlBallots = 8;                          // 64-token ballots per wave per tile
+constexpr int kPlTile = kPlTableThreads * kPlBallots;  // tokens per tile (8192)
+constexpr int kPlDestLds = 4096;   // destinations of a request held in LDS (16 KiB)
 
 __device__ __forceinline__ void pl_error(int32_t* counters, int code) {
   atomicCAS(&counters[3], 0, code);
@@ -78,7 +82,9 @@ __device__ __forceinline__ void pl_scan(int64_t (&v)[NV], int64_t (&tot)[NV],
   __syncthreads();
 }
 
-// Rank of `flag` among the flagged threads of the workgroup (ballots), and their count.
+// Rank of `flag` among the flagged threads of the workgroup (kWaves waves; ballots), and
+// their count.
+template <int kWaves = kPlWaves>
 __device__ __forceinline__ int pl_rank(bool flag, int* total, int* lds) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -87,14 +93,14 @@ __device__ __forceinline__ int pl_rank(bool flag, int* total, int* lds) {
   __syncthreads();
   int off = 0, t = 0;
 #pragma unroll
-  for (int w = 0; w < kPlWaves; ++w) {
+  for (int w = 0; w < kWaves; ++w) {
     const int x = lds[w];
     off += w < wave ? x : 0;
     t += x;
   }
   __syncthreads();
   *total = t;
-  return off + pl_lanes_below(m);
+  return off + lanes_below(m);
 }
 
 __device__ __forceinline__ bool pl_candidate(const PlannerArgs& a, int b) {
@@ -240,6 +246,63 @@ __global__ __launch_bounds__(kPlAdmitThreads) void pl_admit_kernel(PlannerArgs a
   const bool trig = cap > 0 && (cap - L) * a.theta_den > (int64_t)a.theta_num * cap &&
                     E >= a.min_eligible &&
                     (a.free_watermark < 0 || a.free_len <= a.free_watermark);
+  // the totals, written by thread 0 (the capacity check first)
+  auto finish = [&](int64_t c_dst, int64_t c_len, int64_t c_free, int64_t s_k,
+                    int64_t s_moved, int64_t n_adm) {
+    a.dst_indptr[a.num_reqs] = static_cast<int32_t>(c_dst);
+    a.new_bt_indptr[a.num_reqs] = static_cast<int32_t>(c_len);
+    a.freed_indptr[a.num_reqs] = static_cast<int32_t>(c_free);
+    a.stats[3] = trig ? 1 : 0;
+    if (c_dst * S > a.src_plan_capacity || c_len > a.new_bt_capacity) {
+      a.counters[3] = VTOKEN_ERR_CAPACITY;
+      return;
+    }
+    a.counters[0] = static_cast<int32_t>(c_dst);
+    a.counters[1] = static_cast<int32_t>(n_adm);
+    a.counters[2] = static_cast<int32_t>(c_free);
+    a.stats[4] = s_k;
+    a.stats[5] = s_moved;
+    a.stats[6] = c_free;
+    a.stats[7] = c_dst;
+  };
+  if (a.num_reqs <= 64) {
+    // one wave holds every request: the same rules with wave scans and no barrier. Every sum
+    // over the requests is bounded by num_bt_entries or num_tokens and fits 32 bits.
+    if (tid >= 64) return;
+    const int r = tid;
+    const bool in = r < a.num_reqs;
+    const int m = in ? a.bt_indptr[r + 1] - a.bt_indptr[r] : 0;
+    const int e = in && trig ? a.src_count[r] : 0;
+    const int ce = wave_inclusive_scan(e) - e;              // candidates of earlier requests
+    const int64_t room = a.max_sources - ce;                // bound B over the candidates
+    const int64_t k = room <= 0 ? 0 : (e < room ? e : room);
+    const int64_t T = k > 0 ? a.elig_cum[a.bt_indptr[r] + k - 1] : 0;
+    const int64_t need = (T + S - 1) / S;
+    const bool prof = k > 0 && need < k;                    // strict block reduction (I4)
+    const int pn = prof ? static_cast<int>(need) : 0;
+    const int o = wave_inclusive_scan(pn) - pn;
+    const bool adm = prof && o + need <= a.free_len;
+    const int y0 = adm ? static_cast<int>(need) : 0;
+    const int y1 = adm ? m - static_cast<int>(k) + static_cast<int>(need) : m;
+    const int y2 = adm ? static_cast<int>(k) : 0;
+    const int i0 = wave_inclusive_scan(y0), i1 = wave_inclusive_scan(y1);
+    const int i2 = wave_inclusive_scan(y2);
+    const int ik = wave_inclusive_scan(static_cast<int>(k));
+    const int im = wave_inclusive_scan(adm ? static_cast<int>(T) : 0);
+    if (in) {
+      a.src_count[r] = static_cast<int32_t>(k);
+      a.admitted[r] = adm ? 1 : 0;
+      a.dst_indptr[r] = i0 - y0;
+      a.new_bt_indptr[r] = i1 - y1;
+      a.freed_indptr[r] = i2 - y2;
+    }
+    const int t0 = __builtin_amdgcn_readlane(i0, 63), t1 = __builtin_amdgcn_readlane(i1, 63);
+    const int t2 = __builtin_amdgcn_readlane(i2, 63), tk = __builtin_amdgcn_readlane(ik, 63);
+    const int tm = __builtin_amdgcn_readlane(im, 63);
+    const int na = __popcll(__ballot(adm));
+    if (tid == 0) finish(t0, t1, t2, tk, tm, na);
+    return;
+  }
   // carries over the chunks: candidates of earlier requests, needs of earlier profitable
   // requests, destinations, new table entries, released sources; and the totals
   int64_t c_e = 0, c_o = 0, c_dst = 0, c_len = 0, c_free = 0;
@@ -279,31 +342,26 @@ __global__ __launch_bounds__(kPlAdmitThreads) void pl_admit_kernel(PlannerArgs a
     s_moved += tz[1];
     n_adm += tz[2];
   }
-  if (tid == 0) {
-    a.dst_indptr[a.num_reqs] = static_cast<int32_t>(c_dst);
-    a.new_bt_indptr[a.num_reqs] = static_cast<int32_t>(c_len);
-    a.freed_indptr[a.num_reqs] = static_cast<int32_t>(c_free);
-    a.stats[3] = trig ? 1 : 0;
-    if (c_dst * S > a.src_plan_capacity || c_len > a.new_bt_capacity) {
-      a.counters[3] = VTOKEN_ERR_CAPACITY;
-      return;
-    }
-    a.counters[0] = static_cast<int32_t>(c_dst);
-    a.counters[1] = static_cast<int32_t>(n_adm);
-    a.counters[2] = static_cast<int32_t>(c_free);
-    a.stats[4] = s_k;
-    a.stats[5] = s_moved;
-    a.stats[6] = c_free;
-    a.stats[7] = c_dst;
-  }
+  if (tid == 0) finish(c_dst, c_len, c_free, s_k, s_moved, n_adm);
 }
 
-__global__ __launch_bounds__(kPlThreads) void pl_table_kernel(PlannerArgs a) {
-  __shared__ int lds_rank[kPlWaves];
+// One 1024-thread workgroup per request. The sources and the new table first (table entries
+// in rounds of 1024); the request's destinations are read into LDS (when they fit). Then the
+// tokens in tiles of 8192: every lane issues the mask bytes and slots of its eight tokens,
+// then the selection flags of their blocks, before any ballot; ranks of the moving tokens come
+// from wave ballots and one LDS scan of the wave totals per tile.
+template <bool kPow2>
+__global__ __launch_bounds__(kPlTableThreads) void pl_table_kernel(PlannerArgs a) {
+  __shared__ int lds_rank[kPlTableWaves];
+  __shared__ int wave_total[kPlTableWaves];
+  __shared__ int32_t dest_s[kPlDestLds];
   if (a.counters[3] != 0) return;
   const int r = blockIdx.x;
   const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
   const int S = a.block_size;
+  const BlockDiv<kPow2> bd(S);
   const int t0 = a.tok_indptr[r], n = a.tok_indptr[r + 1] - t0;
   const int b0 = a.bt_indptr[r], m = a.bt_indptr[r + 1] - b0;
   const bool adm = a.admitted[r] != 0;
@@ -312,66 +370,107 @@ __global__ __launch_bounds__(kPlThreads) void pl_table_kernel(PlannerArgs a) {
   const int need = a.dst_indptr[r + 1] - d0;
   const int nb0 = a.new_bt_indptr[r];
   const int f0 = a.freed_indptr[r];
+  const bool dest_lds = need <= kPlDestLds;
+  if (dest_lds) {
+    for (int i = tid; i < need; i += kPlTableThreads) dest_s[i] = a.free_list[d0 + i];
+  }
 
   // sources: the first k candidates in table order; kept blocks and released sources
   int cand_carry = 0, keep_carry = 0, sel_carry = 0;
-  for (int base = 0; base < m; base += kPlThreads) {
+  for (int base = 0; base < m; base += kPlTableThreads) {
     const int j = base + tid;
     const bool in = j < m;
     const int b = in ? a.block_ids[b0 + j] : -1;
     const bool cand = in && adm && pl_candidate(a, b);
     int cnt;
-    const int crank = cand_carry + pl_rank(cand, &cnt, lds_rank);
+    const int crank = cand_carry + pl_rank<kPlTableWaves>(cand, &cnt, lds_rank);
     cand_carry += cnt;
     const bool sel = cand && crank < k;
     if (in && b >= 0 && b < a.num_blocks) a.selected[b] = sel ? 1 : 0;
     int nkeep;
-    const int krank = keep_carry + pl_rank(in && !sel, &nkeep, lds_rank);
+    const int krank = keep_carry + pl_rank<kPlTableWaves>(in && !sel, &nkeep, lds_rank);
     keep_carry += nkeep;
     int nsel;
-    const int srank = sel_carry + pl_rank(sel, &nsel, lds_rank);
+    const int srank = sel_carry + pl_rank<kPlTableWaves>(sel, &nsel, lds_rank);
     sel_carry += nsel;
     if (in && !sel && nb0 + krank < a.new_bt_capacity) a.new_block_ids[nb0 + krank] = b;
     if (sel) a.sources[f0 + srank] = b;
   }
-  for (int i = tid; i < need; i += kPlThreads) {
-    a.new_block_ids[nb0 + keep_carry + i] = a.free_list[d0 + i];
+  __syncthreads();  // selected[] of this request's blocks and the LDS destinations
+  for (int i = tid; i < need; i += kPlTableThreads) {
+    a.new_block_ids[nb0 + keep_carry + i] = dest_lds ? dest_s[i] : a.free_list[d0 + i];
   }
-  __syncthreads();  // this workgroup's selected[] entries are visible to it from here on
 
   // move list in logical order: live tokens whose slot lies in a selected source
   const int64_t plan0 = (int64_t)d0 * S;
   const int64_t plan_n = (int64_t)need * S;
   int q_carry = 0;
   bool overflow = false;
-  for (int base = 0; base < n; base += kPlThreads) {
-    const int p = base + tid;
-    const bool in = p < n;
-    const bool lv = in && a.live[t0 + p] != 0;
-    const int s = in ? a.slot_in[t0 + p] : -1;
-    const bool valid = s >= 0 && s < a.num_slots;
-    const bool mv = adm && lv && valid && a.selected[s / S] != 0;
-    int cnt;
-    const int q = q_carry + pl_rank(mv, &cnt, lds_rank);
-    q_carry += cnt;
-    if (in) {
-      int out = lv && valid ? s : -1;
-      if (mv) {
-        if (q < plan_n) {
-          out = a.free_list[d0 + q / S] * S + q % S;
-          a.src_plan[plan0 + q] = s;
+  for (int base = 0; base < n; base += kPlTile) {
+    const int wbase = base + wave * (64 * kPlBallots);
+    // unconditional loads (positions clamped to the last token), all in flight together
+    uint8_t lv[kPlBallots];
+    int sl[kPlBallots];
+#pragma unroll
+    for (int q = 0; q < kPlBallots; ++q) {
+      const int pc = min(wbase + q * 64 + lane, n - 1);
+      lv[q] = a.live[t0 + pc];
+      sl[q] = a.slot_in[t0 + pc];
+    }
+    int sel[kPlBallots];
+#pragma unroll
+    for (int q = 0; q < kPlBallots; ++q) {
+      const bool valid = sl[q] >= 0 && sl[q] < a.num_slots;
+      sel[q] = a.selected[valid ? bd.div(sl[q]) : 0];
+    }
+    int rank[kPlBallots];
+    int local = 0;
+#pragma unroll
+    for (int q = 0; q < kPlBallots; ++q) {
+      const int p = wbase + q * 64 + lane;
+      const bool valid = sl[q] >= 0 && sl[q] < a.num_slots;
+      const bool mv = adm && p < n && lv[q] != 0 && valid && sel[q] != 0;
+      const uint64_t mk = __ballot(mv);
+      rank[q] = mv ? local + lanes_below(mk) : -1;
+      local += __popcll(mk);
+    }
+    if (lane == 0) wave_total[wave] = local;
+    __syncthreads();
+    int off = q_carry, tile = 0;
+#pragma unroll
+    for (int w = 0; w < kPlTableWaves; ++w) {
+      const int x = wave_total[w];
+      off += w < wave ? x : 0;
+      tile += x;
+    }
+#pragma unroll
+    for (int q = 0; q < kPlBallots; ++q) {
+      const int p = wbase + q * 64 + lane;
+      if (p >= n) continue;
+      const int s = sl[q];
+      const bool valid = s >= 0 && s < a.num_slots;
+      int out = lv[q] != 0 && valid ? s : -1;
+      if (rank[q] >= 0) {
+        const int qq = off + rank[q];
+        if (qq < plan_n) {
+          const int g = bd.div(qq);
+          const int dblk = dest_lds ? dest_s[g] : a.free_list[d0 + g];
+          out = dblk * S + bd.mod(qq);
+          a.src_plan[plan0 + qq] = s;
         } else {
           overflow = true;
         }
       }
       a.token_slot[t0 + p] = out;
     }
+    q_carry += tile;
+    __syncthreads();
   }
   if (adm) {
     // the moved tokens must be exactly the live tokens counted in the sources
     const int expect = k > 0 ? a.elig_cum[b0 + k - 1] : 0;
     if (overflow || (tid == 0 && q_carry != expect)) pl_error(a.counters, VTOKEN_ERR_SLOT);
-    for (int64_t q = q_carry + tid; q < plan_n; q += kPlThreads) a.src_plan[plan0 + q] = -1;
+    for (int64_t q = q_carry + tid; q < plan_n; q += kPlTableThreads) a.src_plan[plan0 + q] = -1;
   }
 }
 
@@ -386,13 +485,17 @@ hipError_t launch_planner(const PlannerArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(pl_clear_kernel, dim3(grid_for(a.num_blocks)), dim3(256), 0, stream, a);
   hipLaunchKernelGGL(pl_count_kernel, dim3(grid_for((int64_t)a.num_bt_entries + a.num_tokens)),
                      dim3(256), 0, stream, a);
-  hipLaunchKernelGGL(pl_blocks_kernel, dim3(grid_for(a.num_blocks)), dim3(256), 0, stream, a);
+  // at most 128 workgroups: each adds its totals with two atomics on the same two words
+  const unsigned blocks_grid = grid_for(a.num_blocks) < 128u ? grid_for(a.num_blocks) : 128u;
+  hipLaunchKernelGGL(pl_blocks_kernel, dim3(blocks_grid), dim3(256), 0, stream, a);
   if (a.num_reqs > 0) {
     hipLaunchKernelGGL(pl_request_kernel, dim3(a.num_reqs), dim3(kPlThreads), 0, stream, a);
   }
   hipLaunchKernelGGL(pl_admit_kernel, dim3(1), dim3(kPlAdmitThreads), 0, stream, a);
   if (a.num_reqs > 0) {
-    hipLaunchKernelGGL(pl_table_kernel, dim3(a.num_reqs), dim3(kPlThreads), 0, stream, a);
+    const bool pow2 = (a.block_size & (a.block_size - 1)) == 0;
+    hipLaunchKernelGGL(pow2 ? pl_table_kernel<true> : pl_table_kernel<false>, dim3(a.num_reqs),
+                       dim3(kPlTableThreads), 0, stream, a);
   }
   return hipGetLastError();
 }
