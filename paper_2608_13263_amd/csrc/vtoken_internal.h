@@ -326,6 +326,51 @@ __device__ __forceinline__ int row_inclusive_scan(int v) {
   return v + row_shr<8>(v);
 }
 
+// Exclusive scan of NV values per thread across the workgroup (at most 16 waves); total[k] is
+// the sum. A wave whose values are all zero (requests past the batch's end) skips its own
+// scan. The wave totals go through LDS once: lane w of every wave reads wave w's total and a
+// 16-lane scan gives each wave its offset.
+template <int NV>
+__device__ __forceinline__ void block_exclusive_scan(int (&v)[NV], int (&total)[NV],
+                                                     int (*lds)[NV]) {
+  const int lane = lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  int any = 0;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) any |= v[k];
+  int incl[NV];
+  if (__ballot(any != 0) != 0) {
+#pragma unroll
+    for (int k = 0; k < NV; ++k) incl[k] = wave_inclusive_scan(v[k]);
+  } else {
+#pragma unroll
+    for (int k = 0; k < NV; ++k) incl[k] = 0;
+  }
+  if (lane == 63) {
+#pragma unroll
+    for (int k = 0; k < NV; ++k) lds[wave][k] = incl[k];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int wt = row_inclusive_scan(lane < nwaves ? lds[lane][k] : 0);
+    const int off = wave > 0 ? __builtin_amdgcn_readlane(wt, wave - 1) : 0;
+    total[k] = __builtin_amdgcn_readlane(wt, nwaves - 1);
+    v[k] = off + incl[k] - v[k];
+  }
+  __syncthreads();
+}
+
+// Nonzero bytes of a 32-bit word: each byte's bits are folded into its lowest bit (the bits
+// shifted in from the next byte land at offsets >= 1 and are masked off).
+__device__ __forceinline__ int nonzero_bytes(uint32_t w) {
+  w |= w >> 4;
+  w |= w >> 2;
+  w |= w >> 1;
+  return __popc(w & 0x01010101u);
+}
+
 // Division and remainder of non-negative positions and ranks by the block size S: shifts and
 // masks when S is a power of two (the kernels that divide per token are instantiated for both).
 template <bool kPow2>

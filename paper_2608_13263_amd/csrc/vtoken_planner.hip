@@ -46,42 +46,6 @@ __device__ __forceinline__ void pl_error(int32_t* counters, int code) {
   atomicCAS(&counters[3], 0, code);
 }
 
-// Exclusive scan over the workgroup of NV int64 values per thread; tot[k] is the sum.
-template <int NV, int kWaves>
-__device__ __forceinline__ void pl_scan(int64_t (&v)[NV], int64_t (&tot)[NV],
-                                        int64_t (*lds)[NV]) {
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  int64_t incl[NV];
-#pragma unroll
-  for (int k = 0; k < NV; ++k) {
-    int64_t x = v[k];
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const int64_t t = __shfl_up(x, d, 64);
-      if (lane >= d) x += t;
-    }
-    incl[k] = x;
-  }
-  if (lane == 63) {
-#pragma unroll
-    for (int k = 0; k < NV; ++k) lds[wave][k] = incl[k];
-  }
-  __syncthreads();
-#pragma unroll
-  for (int k = 0; k < NV; ++k) {
-    int64_t off = 0, t = 0;
-    for (int w = 0; w < kWaves; ++w) {
-      const int64_t x = lds[w][k];
-      off += w < wave ? x : 0;
-      t += x;
-    }
-    v[k] = off + incl[k] - v[k];
-    tot[k] = t;
-  }
-  __syncthreads();
-}
-
 // Rank of `flag` among the flagged threads of the workgroup (kWaves waves; ballots), and
 // their count.
 template <int kWaves = kPlWaves>
@@ -124,26 +88,65 @@ __global__ __launch_bounds__(256) void pl_clear_kernel(PlannerArgs a) {
   }
 }
 
+// OR over the 64 lanes (every lane active): DPP row rotations, then the gfx950 row swaps.
+__device__ __forceinline__ uint32_t wave_or(uint32_t x) {
+  x |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x121, 0xF,
+                                                         0xF, false));
+  x |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x122, 0xF,
+                                                         0xF, false));
+  x |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x124, 0xF,
+                                                         0xF, false));
+  x |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x128, 0xF,
+                                                         0xF, false));
+  const auto r16 = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  x = r16[0] | r16[1];
+  const auto r32 = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return r32[0] | r32[1];
+}
+
+// References of every table entry's block; one bit per live slot. Tokens go 64 to a wave:
+// the bits of the wave's tokens that fall in one block are ORed across the wave and set with
+// one atomic (up to 8 blocks per wave; a wave's remaining tokens set their bits one by one).
+template <bool kPow2>
 __global__ __launch_bounds__(256) void pl_count_kernel(PlannerArgs a) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  const int64_t n = (int64_t)a.num_bt_entries + a.num_tokens;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
-    if (i < a.num_bt_entries) {
-      const int b = a.block_ids[i];
-      if (b < 0 || b >= a.num_blocks) {
-        pl_error(a.counters, VTOKEN_ERR_BLOCK_RANGE);
-      } else {
-        atomicAdd(&a.refs[b], 1);
-      }
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < a.num_bt_entries;
+       i += stride) {
+    const int b = a.block_ids[i];
+    if (b < 0 || b >= a.num_blocks) {
+      pl_error(a.counters, VTOKEN_ERR_BLOCK_RANGE);
     } else {
-      const int64_t t = i - a.num_bt_entries;
-      if (a.live[t] == 0) continue;
-      const int s = a.slot_in[t];
-      if (s < 0 || s >= a.num_slots) {
-        pl_error(a.counters, VTOKEN_ERR_SLOT);
-      } else {
-        atomicOr(&a.live_bits[s / a.block_size], 1ull << (s % a.block_size));
+      atomicAdd(&a.refs[b], 1);
+    }
+  }
+  const BlockDiv<kPow2> bd(a.block_size);
+  const int lane = threadIdx.x & 63;
+  const int64_t waves = stride / 64;
+  for (int64_t w0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / 64 * 64;
+       w0 < a.num_tokens; w0 += waves * 64) {
+    const int64_t t = w0 + lane;
+    const bool lv = t < a.num_tokens && a.live[t] != 0;
+    const int s = lv ? a.slot_in[t] : -1;
+    const bool bad = lv && (s < 0 || s >= a.num_slots);
+    if (bad) pl_error(a.counters, VTOKEN_ERR_SLOT);
+    const bool ok = lv && !bad;
+    const int blk = ok ? bd.div(s) : -1;
+    const int off = ok ? bd.mod(s) : 0;
+    uint64_t pending = __ballot(ok);
+    for (int it = 0; it < 8 && pending != 0; ++it) {
+      const int leader = __builtin_ctzll(pending);
+      const int lb = __builtin_amdgcn_readlane(blk, leader);
+      const bool mine = ok && blk == lb;
+      const uint32_t lo = wave_or(mine && off < 32 ? 1u << off : 0u);
+      const uint32_t hi = wave_or(mine && off >= 32 ? 1u << (off - 32) : 0u);
+      if (lane == leader) {
+        atomicOr(reinterpret_cast<unsigned long long*>(&a.live_bits[lb]),
+                 (static_cast<unsigned long long>(hi) << 32) | lo);
       }
+      pending &= ~__ballot(mine);
+    }
+    if ((pending >> lane) & 1) {
+      atomicOr(reinterpret_cast<unsigned long long*>(&a.live_bits[blk]), 1ull << off);
     }
   }
 }
@@ -185,8 +188,8 @@ __global__ __launch_bounds__(256) void pl_blocks_kernel(PlannerArgs a) {
 }
 
 __global__ __launch_bounds__(kPlThreads) void pl_request_kernel(PlannerArgs a) {
-  __shared__ int lds_rank[kPlWaves];
-  __shared__ int64_t lds_scan[kPlWaves][1];
+  __shared__ int lds2[kPlWaves][2];
+  __shared__ int wave_sum[kPlWaves];
   const int r = blockIdx.x;
   const int tid = threadIdx.x;
   const int n = a.seq_lens[r];
@@ -206,27 +209,45 @@ __global__ __launch_bounds__(kPlThreads) void pl_request_kernel(PlannerArgs a) {
     }
     return;
   }
-  // live count of the request
+  // live count of the request: 16-byte loads over the 16-byte-aligned middle of its mask,
+  // bytes at the ends
+  const uint8_t* lv = a.live + t0;
+  const int lead = static_cast<int>((16 - (reinterpret_cast<uintptr_t>(lv) & 15)) & 15);
+  const int head = lead < n ? lead : n;
+  const int words = (n - head) / 16;
+  const int tail0 = head + words * 16;
   int lc = 0;
-  for (int p = tid; p < n; p += kPlThreads) lc += a.live[t0 + p] != 0;
-  int64_t v[1] = {lc}, tot[1];
-  pl_scan<1, kPlWaves>(v, tot, lds_scan);
-  if (tid == 0) a.live_count[r] = static_cast<int32_t>(tot[0]);
+  if (tid < head) lc += lv[tid] != 0;
+  if (tail0 + tid < n) lc += lv[tail0 + tid] != 0;
+  const uint4* w16 = reinterpret_cast<const uint4*>(lv + head);
+  for (int w = tid; w < words; w += kPlThreads) {
+    const uint4 x = w16[w];
+    lc += nonzero_bytes(x.x) + nonzero_bytes(x.y) + nonzero_bytes(x.z) + nonzero_bytes(x.w);
+  }
+  lc = wave_inclusive_scan(lc);
+  if ((tid & 63) == 63) wave_sum[tid >> 6] = lc;
+  __syncthreads();
+  if (tid == 0) {
+    int c = 0;
+#pragma unroll
+    for (int w = 0; w < kPlWaves; ++w) c += wave_sum[w];
+    a.live_count[r] = c;
+  }
 
-  // candidates in table order, with the cumulative live tokens of the candidates so far
+  // candidates in table order, with the cumulative live tokens of the candidates so far (one
+  // workgroup scan per chunk gives both the rank and the live prefix)
   int carry = 0;
   int live_carry = 0;
   for (int base = 0; base < b1 - b0; base += kPlThreads) {
     const int j = base + tid;
     const int b = j < b1 - b0 ? a.block_ids[b0 + j] : -1;
     const bool cand = j < b1 - b0 && pl_candidate(a, b);
-    int cnt;
-    const int rank = pl_rank(cand, &cnt, lds_rank);
-    int64_t lv[1] = {cand ? a.n_b[b] : 0}, ltot[1];
-    pl_scan<1, kPlWaves>(lv, ltot, lds_scan);
-    if (cand) a.elig_cum[b0 + carry + rank] = live_carry + static_cast<int>(lv[0]) + a.n_b[b];
-    carry += cnt;
-    live_carry += static_cast<int>(ltot[0]);
+    const int nb = cand ? a.n_b[b] : 0;
+    int v[2] = {cand ? 1 : 0, nb}, tot[2];
+    block_exclusive_scan<2>(v, tot, lds2);
+    if (cand) a.elig_cum[b0 + carry + v[0]] = live_carry + v[1] + nb;
+    carry += tot[0];
+    live_carry += tot[1];
   }
   if (tid == 0) {
     a.src_count[r] = carry;
@@ -236,8 +257,7 @@ __global__ __launch_bounds__(kPlThreads) void pl_request_kernel(PlannerArgs a) {
 }
 
 __global__ __launch_bounds__(kPlAdmitThreads) void pl_admit_kernel(PlannerArgs a) {
-  __shared__ int64_t lds1[kPlAdmitWaves][1];
-  __shared__ int64_t lds3[kPlAdmitWaves][3];
+  __shared__ int lds6[kPlAdmitWaves][6];
   if (a.counters[3] != 0) return;
   const int tid = threadIdx.x;
   const int S = a.block_size;
@@ -304,28 +324,33 @@ __global__ __launch_bounds__(kPlAdmitThreads) void pl_admit_kernel(PlannerArgs a
     return;
   }
   // carries over the chunks: candidates of earlier requests, needs of earlier profitable
-  // requests, destinations, new table entries, released sources; and the totals
+  // requests, destinations, new table entries, released sources; and the totals. The scans
+  // are 32-bit (DPP wave scans): every sum is bounded by num_bt_entries or num_tokens.
   int64_t c_e = 0, c_o = 0, c_dst = 0, c_len = 0, c_free = 0;
   int64_t s_k = 0, s_moved = 0, n_adm = 0;
   for (int base = 0; base < a.num_reqs; base += kPlAdmitThreads) {
     const int r = base + tid;
     const bool in = r < a.num_reqs;
     const int m = in ? a.bt_indptr[r + 1] - a.bt_indptr[r] : 0;
-    const int64_t e = in && trig ? a.src_count[r] : 0;
-    int64_t v1[1] = {e}, t1[1];
-    pl_scan<1, kPlAdmitWaves>(v1, t1, lds1);
+    const int e = in && trig ? a.src_count[r] : 0;
+    int v1[1] = {e}, t1[1];
+    block_exclusive_scan<1>(v1, t1, reinterpret_cast<int (*)[1]>(lds6));
     const int64_t room = a.max_sources - (c_e + v1[0]);    // bound B over the candidates
     const int64_t k = room <= 0 ? 0 : (e < room ? e : room);
     c_e += t1[0];
     const int64_t T = k > 0 ? a.elig_cum[a.bt_indptr[r] + k - 1] : 0;
     const int64_t need = (T + S - 1) / S;
     const bool prof = k > 0 && need < k;                   // strict block reduction (I4)
-    v1[0] = prof ? need : 0;
-    pl_scan<1, kPlAdmitWaves>(v1, t1, lds1);
+    v1[0] = prof ? static_cast<int>(need) : 0;
+    block_exclusive_scan<1>(v1, t1, reinterpret_cast<int (*)[1]>(lds6));
     const bool adm = prof && c_o + v1[0] + need <= a.free_len;
     c_o += t1[0];
-    int64_t y[3] = {adm ? need : 0, adm ? m - k + need : m, adm ? k : 0}, ty[3];
-    pl_scan<3, kPlAdmitWaves>(y, ty, lds3);
+    int y[6] = {adm ? static_cast<int>(need) : 0,
+                adm ? m - static_cast<int>(k) + static_cast<int>(need) : m,
+                adm ? static_cast<int>(k) : 0, static_cast<int>(k),
+                adm ? static_cast<int>(T) : 0, adm ? 1 : 0};
+    int ty[6];
+    block_exclusive_scan<6>(y, ty, lds6);
     if (in) {
       a.src_count[r] = static_cast<int32_t>(k);
       a.admitted[r] = adm ? 1 : 0;
@@ -336,11 +361,9 @@ __global__ __launch_bounds__(kPlAdmitThreads) void pl_admit_kernel(PlannerArgs a
     c_dst += ty[0];
     c_len += ty[1];
     c_free += ty[2];
-    int64_t z[3] = {k, adm ? T : 0, adm ? 1 : 0}, tz[3];
-    pl_scan<3, kPlAdmitWaves>(z, tz, lds3);
-    s_k += tz[0];
-    s_moved += tz[1];
-    n_adm += tz[2];
+    s_k += ty[3];
+    s_moved += ty[4];
+    n_adm += ty[5];
   }
   if (tid == 0) finish(c_dst, c_len, c_free, s_k, s_moved, n_adm);
 }
@@ -483,8 +506,10 @@ hipError_t launch_planner(const PlannerArgs& a, hipStream_t stream) {
     return static_cast<unsigned>(g < 2048 ? g : 2048);
   };
   hipLaunchKernelGGL(pl_clear_kernel, dim3(grid_for(a.num_blocks)), dim3(256), 0, stream, a);
-  hipLaunchKernelGGL(pl_count_kernel, dim3(grid_for((int64_t)a.num_bt_entries + a.num_tokens)),
-                     dim3(256), 0, stream, a);
+  const bool pow2 = (a.block_size & (a.block_size - 1)) == 0;
+  hipLaunchKernelGGL(pow2 ? pl_count_kernel<true> : pl_count_kernel<false>,
+                     dim3(grid_for((int64_t)a.num_bt_entries + a.num_tokens)), dim3(256), 0,
+                     stream, a);
   // at most 128 workgroups: each adds its totals with two atomics on the same two words
   const unsigned blocks_grid = grid_for(a.num_blocks) < 128u ? grid_for(a.num_blocks) : 128u;
   hipLaunchKernelGGL(pl_blocks_kernel, dim3(blocks_grid), dim3(256), 0, stream, a);
@@ -493,7 +518,6 @@ hipError_t launch_planner(const PlannerArgs& a, hipStream_t stream) {
   }
   hipLaunchKernelGGL(pl_admit_kernel, dim3(1), dim3(kPlAdmitThreads), 0, stream, a);
   if (a.num_reqs > 0) {
-    const bool pow2 = (a.block_size & (a.block_size - 1)) == 0;
     hipLaunchKernelGGL(pow2 ? pl_table_kernel<true> : pl_table_kernel<false>, dim3(a.num_reqs),
                        dim3(kPlTableThreads), 0, stream, a);
   }
