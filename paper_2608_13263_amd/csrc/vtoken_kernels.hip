@@ -7,9 +7,13 @@
 //                  Sec. 3.3.2, 3.3.3, I4 of Sec. 3.5), then the request's new block table,
 //                  token slots (slot = block * S + offset, Sec. 3.4; ranks by wave ballots,
 //                  the order-preserving fill of Sec. 3.3.3) and per-destination source plan.
-//   free_kernel    the freed list: old blocks of admitted requests (Sec. 3.3.4).
+//   plan_small_kernel  both steps in one workgroup and one launch for batches of at most
+//                  256 requests and 16,384 tokens.
+//   free_kernel    the freed list: old blocks of admitted requests (Sec. 3.3.4); the same
+//                  work runs in the copy's launch for vtoken_repack_free.
 //
-// The copies that consume the plan are in vtoken_copy.hip. Kernels after the plan read the
+// Scans across a wave use DPP row shifts and lane reads, never the LDS-routed shuffles
+// (vtoken_internal.h). The copies that consume the plan are in vtoken_copy.hip. Kernels after the plan read the
 // status word plan->counters[3] and do nothing when it is set; every dereference of caller
 // data is bounds-checked.
 #include <limits.h>
