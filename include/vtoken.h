@@ -102,11 +102,13 @@ typedef enum vtoken_status {
                                 /* (two tokens on one slot, a slot outside its table)    */
   VTOKEN_ERR_LAYOUT = -14,      /* vtoken_check_layout: a block id held twice over the   */
                                 /* block tables and the free list                        */
-  VTOKEN_ERR_PLAN_MODE = -15    /* a copy was handed a plan built for the other mode     */
+  VTOKEN_ERR_PLAN_MODE = -15    /* a call was handed a plan built for another mode       */
                                 /* (vtoken_repack[_ex] needs a plan of                   */
                                 /* vtoken_build_token_table or vtoken_plan_partial,      */
                                 /* vtoken_repack_inplace[_ex] one of                     */
-                                /* vtoken_build_token_table_inplace); nothing is copied  */
+                                /* vtoken_build_token_table_inplace; vtoken_free_blocks  */
+                                /* and vtoken_repack_free refuse a plan of               */
+                                /* vtoken_plan_partial); nothing is copied or released   */
 } vtoken_status;
 
 /* The paged KV cache (Sec. 2.1). */
@@ -155,8 +157,9 @@ typedef struct vtoken_plan {
   int32_t* freed_indptr;    /* [R+1] exclusive scan of admitted*old_blocks                  */
   int32_t* counters;        /* [5]   used free-list entries, admitted requests, freed       */
                             /*       blocks, status (VTOKEN_OK or a device error code),     */
-                            /*       plan mode (1 out of place, 2 in place; checked by the  */
-                            /*       copy, which sets VTOKEN_ERR_PLAN_MODE on a mismatch)   */
+                            /*       plan mode (1 out of place, 2 in place, 3 partial pass; */
+                            /*       checked by the copy and the freed list, which set      */
+                            /*       VTOKEN_ERR_PLAN_MODE on a mismatch)                    */
   int64_t  new_bt_capacity;   /* entries in new_block_ids, >= M            [host]           */
   int64_t  src_plan_capacity; /* entries in src_plan, >= min(free_len, M)*S [host]         */
 } vtoken_plan;
@@ -177,17 +180,20 @@ vtoken_status vtoken_repack(const vtoken_cache* cache, const vtoken_batch* batch
 
 /* Step 3 (Sec. 3.3.4: sources are returned only after the packed layout is committed):
  * writes freed[0 .. counters[2]) = old blocks of the admitted requests (in-place mode: the
- * blocks past each admitted request's new table). Stream order
- * after vtoken_repack is what makes reuse of these blocks safe. freed_capacity >= M. */
+ * blocks past each admitted request's new table). Stream order after vtoken_repack is what
+ * makes reuse of these blocks safe. freed_capacity >= M. A plan of vtoken_plan_partial (whose
+ * released blocks are its state's sources) is refused: nothing is written and counters[3]
+ * becomes VTOKEN_ERR_PLAN_MODE. */
 vtoken_status vtoken_free_blocks(const vtoken_batch* batch, const vtoken_plan* plan,
                                  int32_t* freed, int64_t freed_capacity, hipStream_t stream);
 
 /* Steps 2 and 3 in one launch (Sec. 3.3.4): vtoken_repack followed by vtoken_free_blocks on
  * a plan of vtoken_build_token_table, for callers that enqueue the two back to back. Same
  * arguments, checks, outputs and errors as the two calls in that order (freed_capacity >= M;
- * the copy uses the default options). The freed list is written by the copy's own launch (one
- * workgroup per request after the copy's); the blocks in it may be reused once that launch
- * has executed on the stream, as after vtoken_free_blocks. */
+ * the copy uses the default options; a plan of vtoken_plan_partial is refused with
+ * VTOKEN_ERR_PLAN_MODE and nothing is copied). The freed list is written by the copy's own
+ * launch (one workgroup per request after the copy's); the blocks in it may be reused once
+ * that launch has executed on the stream, as after vtoken_free_blocks. */
 vtoken_status vtoken_repack_free(const vtoken_cache* cache, const vtoken_batch* batch,
                                  const vtoken_plan* plan, int32_t* freed,
                                  int64_t freed_capacity, hipStream_t stream);
@@ -291,10 +297,11 @@ vtoken_status vtoken_repack_inplace_ex(const vtoken_cache* cache, const vtoken_b
  * Outputs go to the vtoken_plan (sizes as for vtoken_build_token_table: token_slot [T],
  * live_count / admitted [R], CSR offsets [R+1], new_block_ids with new_bt_capacity >= M,
  * src_plan with src_plan_capacity >= min(free_len, M)*S, counters [5] = {destination blocks
- * used, requests admitted, sources released, status, plan mode 1}) and to the state buffers below. The
- * copy is vtoken_repack on the same plan, enqueued after this call. The released sources are
- * state->sources[0 .. counters[2]) (CSR by freed_indptr): reuse them only after the copy has
- * executed on the stream; vtoken_free_blocks does not apply to this pass. */
+ * used, requests admitted, sources released, status, plan mode 3}) and to the state buffers
+ * below. The copy is vtoken_repack on the same plan, enqueued after this call. The released
+ * sources are state->sources[0 .. counters[2]) (CSR by freed_indptr): reuse them only after
+ * the copy has executed on the stream; vtoken_free_blocks and vtoken_repack_free refuse this
+ * plan (VTOKEN_ERR_PLAN_MODE). */
 typedef struct vtoken_planner_params {
   int32_t theta_num;            /* theta_F = theta_num / theta_den (paper default 1/4)       */
   int32_t theta_den;            /* > 0                                                        */
@@ -361,10 +368,11 @@ vtoken_status vtoken_append_slots(int32_t num_reqs, const int32_t* append_indptr
  *   out[r][qh] = softmax(scale * q[r][qh] . K[slot]^T) @ V[slot] over the slots of r,
  * K and V being the layer's K and V planes (float32 math; zeros for a request with no slots).
  * Flash-decoding: splits of 32 KiB of K per KV head (32768 / (head_dim * elem_bytes) tokens;
- * 64 KiB for 2-byte caches with 8 query heads per KV head), then a merge; the workspace holds the split partials and is overwritten by every call (calls
- * sharing it must be stream-ordered). A request with more slots than max_tokens provides
- * for is never truncated: its outputs are NaN, unless its slots still fit the
- * ceil(max_tokens / split) splits, which are all computed. A slot outside the pool (negative
+ * 64 KiB for 2-byte caches with 8 query heads per KV head), then a merge; the workspace
+ * holds the split partials and is overwritten by every call (calls sharing it must be
+ * stream-ordered). A request with more slots than max_tokens provides for is never
+ * truncated: its outputs are NaN, unless its slots still fit the ceil(max_tokens / split)
+ * splits, which are all computed. A slot outside the pool (negative
  * or >= num_blocks * block_size) is never dereferenced; its request's outputs are NaN. A
  * request whose slot range is malformed (slot_indptr[r] < 0, or a negative count:
  * slot_indptr[r+1] < slot_indptr[r], or slot_count[r] < 0) reads no slot and gets NaN

@@ -580,7 +580,7 @@ const char* vtoken_status_string(int32_t status) {
     case VTOKEN_ERR_SLOT: return "VTOKEN_ERR_SLOT: a live token's slot is invalid for its table";
     case VTOKEN_ERR_LAYOUT: return "VTOKEN_ERR_LAYOUT: a block id is held twice";
     case VTOKEN_ERR_PLAN_MODE:
-      return "VTOKEN_ERR_PLAN_MODE: the plan was built for the other copy mode";
+      return "VTOKEN_ERR_PLAN_MODE: the plan was built for another mode of the pass";
     default: return "unknown vtoken status";
   }
 }

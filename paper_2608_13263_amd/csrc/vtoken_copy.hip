@@ -90,7 +90,10 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
   constexpr Policy pol = kPolicies[kPolicy];
   constexpr int kRound = kCopyThreads * kV;  // units of one part
   if (a.counters[3] != 0) return;
-  if (a.counters[4] != kPlanOutOfPlace) {
+  // plans of the full pass; plans of the partial pass too, but not with the freed list of
+  // vtoken_repack_free (a partial pass releases its selected sources, not table tails)
+  const int mode = a.counters[4];
+  if (mode != kPlanOutOfPlace && (mode != kPlanPartial || a.freed != nullptr)) {
     plan_mode_error(a.counters);
     return;
   }

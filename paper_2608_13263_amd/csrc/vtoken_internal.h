@@ -26,9 +26,11 @@ constexpr int kFreeThreads = 256;
 constexpr int kCopyThreads = 256;
 
 // The plan's mode word (plan->counters[4]), written by the kernels that build a plan and
-// checked by the copy that consumes it.
-constexpr int32_t kPlanOutOfPlace = 1;   // vtoken_build_token_table, vtoken_plan_partial
+// checked by the copy and the freed list that consume it.
+constexpr int32_t kPlanOutOfPlace = 1;   // vtoken_build_token_table
 constexpr int32_t kPlanInPlace = 2;      // vtoken_build_token_table_inplace
+constexpr int32_t kPlanPartial = 3;      // vtoken_plan_partial: the out-of-place copy; its
+                                         // released blocks are the planner state's sources
 
 struct MetaArgs {
   // batch

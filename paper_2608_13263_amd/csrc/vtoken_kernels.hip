@@ -13,9 +13,9 @@
 //                  work runs in the copy's launch for vtoken_repack_free.
 //
 // Scans across a wave use DPP row shifts and lane reads, never the LDS-routed shuffles
-// (vtoken_internal.h). The copies that consume the plan are in vtoken_copy.hip. Kernels after the plan read the
-// status word plan->counters[3] and do nothing when it is set; every dereference of caller
-// data is bounds-checked.
+// (vtoken_internal.h). The copies that consume the plan are in vtoken_copy.hip. Kernels
+// after the plan read the status word plan->counters[3] and do nothing when it is set; every
+// dereference of caller data is bounds-checked.
 #include <limits.h>
 
 #include "vtoken_internal.h"
@@ -663,6 +663,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_small_kernel(MetaArgs a) {
 __global__ __launch_bounds__(kFreeThreads) void free_kernel(MetaArgs a, int32_t* freed,
                                                             int64_t capacity) {
   if (a.counters[3] != 0) return;
+  const int mode = a.counters[4];
+  if (mode != kPlanOutOfPlace && mode != kPlanInPlace) {
+    // a partial pass's plan (its released blocks are the planner state's sources): nothing is
+    // written and the status word says so
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicCAS(&a.counters[3], 0, VTOKEN_ERR_PLAN_MODE);
+    return;
+  }
   write_freed_blocks(blockIdx.x, a.admitted, a.bt_indptr, a.freed_indptr, a.block_ids,
                      a.num_bt_entries, freed, capacity);
 }

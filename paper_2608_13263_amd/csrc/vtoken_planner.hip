@@ -82,9 +82,10 @@ __global__ __launch_bounds__(256) void pl_clear_kernel(PlannerArgs a) {
     a.refs[i] = 0;
   }
   if (blockIdx.x == 0 && threadIdx.x < 8) a.stats[threadIdx.x] = 0;
-  // the plan's mode word: the partial pass's plan is copied by the out-of-place copy
+  // the plan's mode word: the partial pass's plan is copied by the out-of-place copy, and its
+  // released blocks are the state's sources (vtoken_free_blocks refuses it)
   if (blockIdx.x == 0 && threadIdx.x < 5) {
-    a.counters[threadIdx.x] = threadIdx.x == 4 ? kPlanOutOfPlace : 0;
+    a.counters[threadIdx.x] = threadIdx.x == 4 ? kPlanPartial : 0;
   }
 }
 

@@ -81,6 +81,43 @@ def test_partial_parity_params(params):
     partial_parity(inp, B.PlannerParams(**params), label=str(params))
 
 
+@pytest.mark.parametrize("call", ["free_blocks", "repack_free"])
+def test_freed_list_refuses_a_partial_plan(call):
+    """A partial pass's plan carries its own mode (counters[4] = 3): its released blocks are
+    the planner state's sources, so vtoken_free_blocks and vtoken_repack_free refuse it
+    (VTOKEN_ERR_PLAN_MODE, nothing released; vtoken_repack_free copies nothing either), while
+    vtoken_repack copies it (every other test of this file)."""
+    t = torch()
+    B = _B()
+    inp = CASES["tiny_shared"]()
+    sh = inp.shape
+    print(f"[gpu] partial plan handed to {call}", flush=True)
+    kv = W.kv_device(sh, inp.num_blocks, 3)
+    before = kv.clone()
+    cache = B.KVCache(kv, sh.num_layers, sh.num_kv_heads, sh.head_dim, sh.block_size)
+    batch = B.Batch.from_inputs(inp)
+    slot_in = t.from_numpy(np.ascontiguousarray(inp.slots(), dtype=np.int32)).cuda()
+    plan = B.Plan.allocate(batch, sh.block_size)
+    state = B.PlannerState.allocate(inp.num_blocks, batch, pinned=inp.pinned)
+    B.plan_partial(cache, batch, slot_in, plan, state, B.PlannerParams())
+    t.cuda.synchronize()
+    assert plan.counters.cpu().tolist()[3:] == [0, 3]
+    assert int(plan.counters[1]) > 0, "the plan admitted requests"
+    freed = t.full((max(inp.num_bt_entries, 1),), -9, dtype=t.int32, device="cuda")
+    if call == "free_blocks":
+        B.repack(cache, batch, plan)
+        t.cuda.synchronize()
+        assert int(plan.counters[3]) == 0
+        B.free_blocks(batch, plan, freed=freed)
+    else:
+        B.repack_free(cache, batch, plan, freed=freed)
+        t.cuda.synchronize()
+        assert t.equal(kv, before), "vtoken_repack_free copied a partial plan"
+    t.cuda.synchronize()
+    assert int(plan.counters[3]) == B.STATUS_CODE["VTOKEN_ERR_PLAN_MODE"]
+    assert bool((freed == -9).all()), "a freed list was written for a partial plan"
+
+
 def test_partial_pool_short_defers():
     B = _B()
     inp = W.token_table_inputs(622, W.KVShape(1, 2, 64, 16, "fp16"), num_reqs=12,
