@@ -257,12 +257,11 @@ __device__ __forceinline__ float lanes_reduce(float x) {
 }
 
 // Minimum waves per SIMD the decode kernels are compiled for. The fp8 geometries with
-// head_dim 64 or 128 come out a few registers above the four-wave budget (128 registers);
-// held to it they do not spill and run 5-10% faster. Elsewhere the compiler's choice stands
-// (bf16 / fp16 up to head_dim 128 already fit four waves per SIMD; fp8 with head_dim 32 or
-// 256 would spill).
+// head_dim 64 or 128, and the 16-bit ones up to head_dim 128, come out a few registers above
+// the four-wave budget (128 registers); held to it they do not spill (fp8: 5-10% faster).
+// Elsewhere the compiler's choice stands (fp8 with head_dim 32 or 256 would spill).
 constexpr int decode_min_waves(int kind, int head_dim) {
-  return kind == 2 && (head_dim == 64 || head_dim == 128) ? 4 : 1;
+  return kind == 2 ? (head_dim == 64 || head_dim == 128 ? 4 : 1) : (head_dim <= 128 ? 4 : 1);
 }
 
 // Split kernel of the paged decode, both products on the matrix cores.
@@ -345,11 +344,10 @@ void decode_split_kernel(AttnArgs a) {
 
   const bool low = row >= 8;          // this lane's column / P row holds low parts
   const bool real = (row & 7) < kG;   // column / P row of a query head (else zero padding)
-  // ---- query operand first (needed first): column `row` = head row % 8, scaled, its high
-  // part (row < 8) or its low part (row >= 8); the load is unconditional (padding re-reads
-  // head 0), a conditional load would wait for every outstanding K/V load. Every wave needs
-  // the same operands: wave w builds chunks w, w + kWaves, ... for all 64 lanes into LDS, read
-  // after the barrier below.
+  // The query operand of column `row` is head row % 8 (padding columns re-read head 0: the
+  // load is unconditional, since a conditional load would wait for every outstanding K/V
+  // load). Every wave needs the same operands: they are built once per workgroup into LDS and
+  // read after a barrier.
   // The head dims of a k-chunk's lane group: any assignment gives the same dot products as
   // long as q and K use the same one. fp8 pairs the chunks (2c, 2c+1) so that a lane's two
   // 8-byte K pieces are 16 contiguous bytes, read by one load.
@@ -358,30 +356,47 @@ void decode_split_kernel(AttnArgs a) {
     return kPairK ? (ch >> 1) * 64 + grp * 16 + (ch & 1) * 8 + e : ch * 32 + grp * kPer + e;
   };
   __shared__ OpT q_s[kChunks][64];
-  {
-    const float* qrow =
-        a.q + ((int64_t)r * a.num_q_heads + h * kG + (real ? row & 7 : 0)) * kD;
+  // ---- loads in two rounds: the query values and every slot index this lane needs, then
+  // (once the slots are in) every K and V load back to back; the query operands are built
+  // while those are in flight. The vector-memory counter retires loads in order, so a slot
+  // read issued after a K load would hold that slot's K pieces until the earlier K load
+  // returned: interleaving slot reads with K and V loads cost a round trip per tile.
+  constexpr int kQC = (kChunks + kWaves - 1) / kWaves;   // query chunks a wave builds
+  const float* qrow =
+      a.q + ((int64_t)r * a.num_q_heads + h * kG + (real ? row & 7 : 0)) * kD;
+  float qraw[kQC][kPer];
 #pragma unroll
-    for (int ch = wave; ch < kChunks; ch += kWaves) {
-      OpT qv8;
+  for (int c = 0; c < kQC; ++c) {
+    // unconditional (a chunk past the last re-reads the last one, unused)
+    const int ch = wave + c * kWaves < kChunks ? wave + c * kWaves : kChunks - 1;
 #pragma unroll
-      for (int e = 0; e < kPer; ++e) {
-        const float qv = qrow[head_dim_of(ch, e)] * a.scale;
-        const float q = real ? qv : 0.f;
-        const ElemT hi = static_cast<ElemT>(q);
-        qv8[e] = low ? static_cast<ElemT>(q - static_cast<float>(hi)) : hi;
-      }
-      q_s[ch][lane] = qv8;
-    }
+    for (int e = 0; e < kPer; ++e) qraw[c][e] = qrow[head_dim_of(ch, e)];
   }
+  // slot indices of this lane's K tiles and V pieces; tokens past the split's end re-read
+  // its last token
+  int ksl[kTiles];
+#pragma unroll
+  for (int i = 0; i < kTiles; ++i) {
+    const int t = wt0 + i * 16 + row;
+    ksl[i] = slots[t < nt ? t : nt - 1];
+  }
+  const int vpiece = lane % kLanesV;
+  int vsl[kItV];
+#pragma unroll
+  for (int i = 0; i < kItV; ++i) {
+    const int t = wt0 + lane / kLanesV + i * kTokV;
+    vsl[i] = slots[t < nt ? t : nt - 1];
+  }
+  // (the scheduler keeps these reads ahead of the K and V loads, and those ahead of the query
+  // operands' arithmetic)
+  __builtin_amdgcn_sched_barrier(0);
 
-  // ---- all K and V loads; tokens past the split's end re-read its last token
+  // ---- all K and V loads
   PieceT kw[kTiles][kChunks];
   bool kok[kTiles];
 #pragma unroll
   for (int i = 0; i < kTiles; ++i) {
-    const int t = wt0 + i * 16 + row;
-    const int sl = slots[t < nt ? t : nt - 1];
+    const int sl = ksl[i];
     kok[i] = static_cast<unsigned>(sl) < static_cast<unsigned>(a.num_slots);
     const uint8_t* row_base = kplane + (int64_t)(kok[i] ? sl : 0) * a.row_bytes + head0;
     if constexpr (kPairK) {
@@ -403,15 +418,31 @@ void decode_split_kernel(AttnArgs a) {
   // lanes, read with non-temporal loads (each line is used by one instruction; measured
   // +2-6% over plain loads). The K pieces above stay plain: in the matrix-core operand order
   // a row's line is split over two instructions, and non-temporal K loads were slower.
-  const int vpiece = lane % kLanesV;
   u32x4 vw[kItV];
 #pragma unroll
   for (int i = 0; i < kItV; ++i) {
-    const int t = wt0 + lane / kLanesV + i * kTokV;
-    const int sl = slots[t < nt ? t : nt - 1];
+    const int sl = vsl[i];
     const bool ok = static_cast<unsigned>(sl) < static_cast<unsigned>(a.num_slots);
     vw[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(
         vplane + (int64_t)(ok ? sl : 0) * a.row_bytes + head0 + vpiece * 16));
+  }
+
+  __builtin_amdgcn_sched_barrier(0);
+  // ---- query operands (column `row` = head row % 8, scaled; its high part for row < 8, its
+  // low part for row >= 8): wave w builds chunks w, w + kWaves, ... for all 64 lanes into LDS
+#pragma unroll
+  for (int c = 0; c < kQC; ++c) {
+    const int ch = wave + c * kWaves;
+    if (ch < kChunks) {
+      OpT qv8;
+#pragma unroll
+      for (int e = 0; e < kPer; ++e) {
+        const float q = real ? qraw[c][e] * a.scale : 0.f;
+        const ElemT hi = static_cast<ElemT>(q);
+        qv8[e] = low ? static_cast<ElemT>(q - static_cast<float>(hi)) : hi;
+      }
+      q_s[ch][lane] = qv8;
+    }
   }
 
   // ---- scores of this wave's tiles: lane holds tokens wt0 + 16i + 4*grp + j of head row % 8
