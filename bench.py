@@ -677,11 +677,11 @@ def run_scissorhands(args):
                 B.build_token_table_inplace(cache, batch, plan)
                 ev[1].record()
                 B.repack_inplace(cache, batch, plan)
+                B.free_blocks(batch, plan)
             else:
                 B.build_token_table(cache, batch, plan)
                 ev[1].record()
-                B.repack(cache, batch, plan)
-            B.free_blocks(batch, plan)
+                B.repack_free(cache, batch, plan)
             ev[2].record()
             torch.cuda.synchronize()
             cnt = plan.counters.cpu().tolist()
@@ -937,8 +937,9 @@ def run_partial_pass(args):
 
 def run_waves(args, inp, kv, cache, stream):
     """One round of waves over the batch: pass, apply its outputs (W.next_wave), re-submit,
-    until no profitable request is left deferred. Each wave's pass (build, copy, free) is
-    replayed `warmup` + `steps` times on unchanged inputs (the same plan and the same rows
+    until no profitable request is left deferred. Each wave's pass (build, then the copy and
+    the freed list in one launch; --three-calls: three calls) is replayed `warmup` + `steps`
+    times on unchanged inputs (the same plan and the same rows
     between the same addresses each time) with HIP events on the launch stream; then its
     outputs are read back and applied."""
     import numpy as np
@@ -952,6 +953,7 @@ def run_waves(args, inp, kv, cache, stream):
     for wave in range(64):
         batch = B.Batch.from_inputs(inp)
         plan = B.Plan.allocate(batch, S)
+        three = separate_free(args)
 
         def step(ev=None):
             if ev is not None:
@@ -959,10 +961,14 @@ def run_waves(args, inp, kv, cache, stream):
             B.build_token_table(cache, batch, plan, stream)
             if ev is not None:
                 ev[1].record(stream)
-            B.repack_ex(cache, batch, plan, args.variant, args.grid, args.order, stream)
+            if three:
+                B.repack_ex(cache, batch, plan, args.variant, args.grid, args.order, stream)
+            else:
+                B.repack_free(cache, batch, plan, stream=stream)
             if ev is not None:
                 ev[2].record(stream)
-            B.free_blocks(batch, plan, stream=stream)
+            if three:
+                B.free_blocks(batch, plan, stream=stream)
             if ev is not None:
                 ev[3].record(stream)
 
@@ -971,11 +977,16 @@ def run_waves(args, inp, kv, cache, stream):
         torch.cuda.synchronize()
         evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4))
                for _ in range(args.steps)]
+        # the wave's passes with nothing between the calls, then as many again with events
+        # between them for the per-call breakdown
         t0 = time.perf_counter()
+        for i in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t0) * 1e3 / args.steps
         for i in range(args.steps):
             step(evs[i])
         torch.cuda.synchronize()
-        wall = (time.perf_counter() - t0) * 1e3 / args.steps
         cnt = plan.counters.cpu().tolist()
         if cnt[3] != 0:
             raise SystemExit(f"wave {wave}: device status {B.STATUS.get(cnt[3], cnt[3])}")
@@ -995,7 +1006,8 @@ def run_waves(args, inp, kv, cache, stream):
             step_ms=round(wall, 4),
             repack_ms=round(sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps, 4),
             build_ms=round(sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps, 4),
-            free_ms=round(sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps, 4)))
+            free_ms=(round(sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps, 4)
+                     if three else None)))
         w = waves[-1]
         log(f"wave {wave}: {w['admitted']} admitted, {w['deferred']} deferred, "
             f"{moved} live tokens, {w['repack_ms']:.3f} ms copy, {w['step_ms']:.3f} ms pass")
@@ -1256,8 +1268,7 @@ def run_overlap(args, inp, kv, cache, batch, plan, stream):
 
     def repack_pass(st):
         B.build_token_table(cache, batch, plan, st)
-        B.repack(cache, batch, plan, st)
-        B.free_blocks(batch, plan, stream=st)
+        B.repack_free(cache, batch, plan, stream=st)
 
     def timed(fn):
         times = []
