@@ -341,6 +341,23 @@ def test_small_batch_planning_bound_tokens(extra):
     full_parity(inp, seed=3)
 
 
+@pytest.mark.parametrize("mode", ["three_calls", "repack_free", "in_place"])
+@pytest.mark.parametrize("S", [24, 48])
+def test_large_batch_block_size_not_power_of_two(S, mode):
+    """Past both small-batch bounds (340 requests, over 16384 tokens) with a block size that is
+    not a power of two, so the count and plan launches divide positions by S; the admitted
+    requests take more destination blocks than the free list's head the plan kernel stages."""
+    rng = np.random.default_rng(S)
+    lens = rng.integers(0, 64 * S, size=340)
+    masks = [(rng.random(int(n)) < rng.uniform(0.8, 1.0)).astype(int).tolist() for n in lens]
+    M = sum(-(-len(m) // S) for m in masks)
+    inp = W.from_masks(masks, W.KVShape(1, 1, 8, S, "fp16"), free_blocks=M, seed=S,
+                       name=f"large_block{S}")
+    assert inp.num_tokens > 16384 and inp.num_reqs > 256
+    gpu, orc = full_parity(inp, seed=S, fused=mode == "repack_free", inplace=mode == "in_place")
+    assert orc.n_admitted > 256 and (mode == "in_place" or orc.used > 8192)
+
+
 @pytest.mark.parametrize("R", [256, 257])
 def test_small_batch_planning_bound_requests(R):
     """256 requests are planned by the one-launch kernel, 257 by the count and plan launches."""
