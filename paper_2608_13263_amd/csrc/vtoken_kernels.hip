@@ -2,13 +2,16 @@
 //
 //   count_kernel   one workgroup per request: validates the request's CSR ranges and block
 //                  ids and counts its live tokens (16-byte loads of the live mask).
-//   plan_kernel    one workgroup per request: the admission over all requests (destination
-//                  need ceil(live/S), strict gain, prefix admission against the free list:
-//                  Sec. 3.3.2, 3.3.3, I4 of Sec. 3.5), then the request's new block table,
-//                  token slots (slot = block * S + offset, Sec. 3.4; ranks by wave ballots,
-//                  the order-preserving fill of Sec. 3.3.3) and per-destination source plan.
+//   admit_kernel   batches of more than 512 requests: the admission over all requests
+//                  (destination need ceil(live/S), strict gain, prefix admission against the
+//                  free list: Sec. 3.3.2, 3.3.3, I4 of Sec. 3.5) in one workgroup.
+//   plan_kernel    one workgroup per request: the admission (each workgroup over all
+//                  requests, or read from admit_kernel's outputs), then the request's new
+//                  block table, token slots (slot = block * S + offset, Sec. 3.4; ranks by
+//                  wave ballots, the order-preserving fill of Sec. 3.3.3) and
+//                  per-destination source plan.
 //   plan_small_kernel  both steps in one workgroup and one launch for batches of at most
-//                  256 requests and 16,384 tokens.
+//                  24 requests and 8,192 tokens.
 //   free_kernel    the freed list: old blocks of admitted requests (Sec. 3.3.4); the same
 //                  work runs in the copy's launch for vtoken_repack_free.
 //
@@ -229,17 +232,68 @@ __device__ __forceinline__ int admission_status(const MetaArgs& a, const Admissi
 }
 
 // ------------------------------------------------------------------------------------------
-// Step 1b: the plan. Every workgroup first runs the admission over all requests (each reads
-// the R live counts; R/1024 rounds of two workgroup scans): destination need ceil(live/S),
-// strict gain (Sec. 3.3.3, I4 of Sec. 3.5), prefix admission against the free list (Sec.
-// 3.3.2), and the CSR offsets of its own request; the workgroup of request 0 also writes the
-// totals and the status word. Then workgroup r builds request r's part of the bulk apply_moves
-// (Sec. 3.2): its new block table, the slot of every token (slot = block * S + offset, Sec.
-// 3.4; ranks from wave ballots and lane prefix counts over the live mask, the order-preserving
-// fill of Sec. 3.3.3) and its rows of the per-destination source plan. No workgroup waits for
-// another, so the admission costs one extra O(R) pass per workgroup instead of a launch.
+// Step 1b, large batches: the admission alone, in one workgroup (destination need
+// ceil(live/S), strict gain, prefix admission; Sec. 3.3.2, 3.3.3, I4 of Sec. 3.5). It writes
+// every request's admitted flag and CSR offsets, the offsets' ends, the totals and the status
+// word, which plan_kernel<kPow2, true> then reads instead of repeating the admission in each of
+// its R workgroups (R/1024 rounds of workgroup scans each, O(R^2) over the launch). The live
+// counts and table lengths of the first kAdmitStage requests are staged in LDS, all of their
+// loads in flight at once.
 // ------------------------------------------------------------------------------------------
-template <bool kPow2>
+__global__ __launch_bounds__(kPlanThreads) void admit_kernel(MetaArgs a) {
+  __shared__ int lds[kPlanThreads / 64][4];
+  __shared__ int first_error_req;
+  __shared__ int count_s[kAdmitStage];
+  __shared__ int blocks_s[kAdmitStage];
+  const int tid = threadIdx.x;
+  const int R = a.num_reqs;
+  const int staged = min(R, kAdmitStage);
+  int c[kAdmitStage / kPlanThreads], m[kAdmitStage / kPlanThreads];
+#pragma unroll
+  for (int q = 0; q < kAdmitStage / kPlanThreads; ++q) {
+    const int i = q * kPlanThreads + tid;
+    c[q] = i < staged ? a.live_count[i] : 0;
+    m[q] = i < staged ? a.bt_indptr[i + 1] - a.bt_indptr[i] : 0;
+  }
+#pragma unroll
+  for (int q = 0; q < kAdmitStage / kPlanThreads; ++q) {
+    const int i = q * kPlanThreads + tid;
+    if (i < staged) {
+      count_s[i] = c[q];
+      blocks_s[i] = m[q];
+    }
+  }
+  // (the admission's first barrier orders these LDS writes before every read)
+  const Admission adm = admit_requests(
+      a, [&](int i) { return i < kAdmitStage ? count_s[i] : a.live_count[i]; },
+      [&](int i) {
+        return i < kAdmitStage ? blocks_s[i] : a.bt_indptr[i + 1] - a.bt_indptr[i];
+      },
+      [&](int i, int ad, int dst, int nb, int fr) {
+        a.admitted[i] = ad;
+        a.dst_indptr[i] = dst;
+        a.new_bt_indptr[i] = nb;
+        a.freed_indptr[i] = fr;
+      },
+      lds, &first_error_req);
+  admission_status(a, adm, adm.first_error == INT_MAX ? 0 : a.live_count[adm.first_error], true);
+}
+
+// ------------------------------------------------------------------------------------------
+// Step 1b: the plan. For batches of at most kFusedAdmitReqs requests every workgroup first
+// runs the admission over all requests itself (each reads the R live counts; one round of two
+// workgroup scans, one wave alone for R <= 64): destination need ceil(live/S), strict gain
+// (Sec. 3.3.3, I4 of Sec. 3.5), prefix admission against the free list (Sec. 3.3.2), and the
+// CSR offsets of its own request; the workgroup of request 0 also writes the totals and the
+// status word. No workgroup waits for another, so the admission costs one extra pass per
+// workgroup instead of a launch. Larger batches (kAdmitted) take their request's offsets and
+// the status word from admit_kernel, the launch before. Then workgroup r builds request r's
+// part of the bulk apply_moves (Sec. 3.2): its new block table, the slot of every token (slot =
+// block * S + offset, Sec. 3.4; ranks from wave ballots and lane prefix counts over the live
+// mask, the order-preserving fill of Sec. 3.3.3) and its rows of the per-destination source
+// plan.
+// ------------------------------------------------------------------------------------------
+template <bool kPow2, bool kAdmitted>
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
   __shared__ int lds[kPlanThreads / 64][4];
   __shared__ int wave_total[kPlanThreads / 64];
@@ -257,13 +311,22 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
   // Loads that depend on nothing are issued first, so that they are in flight together with
   // the request's own CSR entries: the admission's inputs for the first 1024 requests, and the
   // head of the free list (out of place), from which destinations are looked up in LDS
-  // instead of by a load after the admission.
+  // instead of by a load after the admission. (With the admission done before, the request's
+  // own offsets and the status word instead; its destinations are read from the free list.)
   int c_pre = 0, m_pre = 0;
-  if (tid < R) {
+  int my_adm = 0, my_dst = 0, my_new = 0, pre_status = 0;
+  if constexpr (kAdmitted) {
+    if (r < R) {
+      my_adm = a.admitted[r];
+      my_dst = a.dst_indptr[r];
+      my_new = a.new_bt_indptr[r];
+    }
+    pre_status = a.counters[3];
+  } else if (tid < R) {
     c_pre = a.live_count[tid];
     m_pre = a.bt_indptr[tid + 1] - a.bt_indptr[tid];
   }
-  const int P = a.inplace ? 0 : min(a.free_len, kPlanHead);
+  const int P = kAdmitted || a.inplace ? 0 : min(a.free_len, kPlanHead);
   int32_t fl[kPlanHead / kPlanThreads];
 #pragma unroll
   for (int q = 0; q < kPlanHead / kPlanThreads; ++q) {
@@ -299,35 +362,42 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
     const int j = q * kPlanThreads + tid;
     if (j < P) head[j] = fl[q];
   }
-  // (the admission's first barrier orders these LDS writes before every read)
-  const Admission adm = admit_requests(
-      a, [&](int i) { return i < kPlanThreads ? c_pre : a.live_count[i]; },
-      [&](int i) { return i < kPlanThreads ? m_pre : a.bt_indptr[i + 1] - a.bt_indptr[i]; },
-      [&](int i, int ad, int dst, int nb, int fr) {
-        if (i == r) {
-          mine[0] = ad;
-          mine[1] = dst;
-          mine[2] = nb;
-          mine[3] = fr;
-        }
-      },
-      lds, &first_error_req);
-  const int status =
-      admission_status(a, adm, adm.first_error == INT_MAX ? 0 : a.live_count[adm.first_error],
-                       r == 0, head, P);
-  if (r >= R) return;   // the one workgroup of an empty batch
-  if (tid == 0) {
-    a.admitted[r] = mine[0];
-    a.dst_indptr[r] = mine[1];
-    a.new_bt_indptr[r] = mine[2];
-    a.freed_indptr[r] = mine[3];
+  int status = pre_status;
+  if constexpr (!kAdmitted) {
+    // (the admission's first barrier orders these LDS writes before every read)
+    const Admission adm = admit_requests(
+        a, [&](int i) { return i < kPlanThreads ? c_pre : a.live_count[i]; },
+        [&](int i) { return i < kPlanThreads ? m_pre : a.bt_indptr[i + 1] - a.bt_indptr[i]; },
+        [&](int i, int ad, int dst, int nb, int fr) {
+          if (i == r) {
+            mine[0] = ad;
+            mine[1] = dst;
+            mine[2] = nb;
+            mine[3] = fr;
+          }
+        },
+        lds, &first_error_req);
+    status =
+        admission_status(a, adm, adm.first_error == INT_MAX ? 0 : a.live_count[adm.first_error],
+                         r == 0, head, P);
+    if (r >= R) return;   // the one workgroup of an empty batch
+    my_adm = mine[0];
+    my_dst = mine[1];
+    my_new = mine[2];
+    if (tid == 0) {
+      a.admitted[r] = my_adm;
+      a.dst_indptr[r] = my_dst;
+      a.new_bt_indptr[r] = my_new;
+      a.freed_indptr[r] = mine[3];
+    }
   }
-  // an error anywhere: the status word (request 0's workgroup) reports it, nothing is built
+  // an error anywhere: the status word (request 0's workgroup, or the admission launch)
+  // reports it, nothing is built
   if (status != 0) return;
 
   int32_t* ts = a.token_slot + t0;
-  int32_t* nbt = a.new_block_ids + mine[2];
-  if (!mine[0]) {
+  int32_t* nbt = a.new_block_ids + my_new;
+  if (!my_adm) {
     // unchanged: the old table, every live token at its positional slot
     const int m = a.bt_indptr[r + 1] - b0;
     for (int j = tid; j < m; j += kPlanThreads) nbt[j] = bt[j];
@@ -348,7 +418,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
     }
     return;
   }
-  const int o = mine[1];
+  const int o = my_dst;
   const int c = a.live_count[r];
   const int need = (c + S - 1) / S;
   // this request's destinations: read from the LDS head of the free list when they lie in it
@@ -686,9 +756,16 @@ hipError_t launch_build(const MetaArgs& a, hipStream_t stream) {
   if (a.num_reqs > 0) {
     hipLaunchKernelGGL(count_kernel, dim3(a.num_reqs), dim3(kCountThreads), 0, stream, a);
   }
+  if (a.num_reqs > kFusedAdmitReqs) {
+    hipLaunchKernelGGL(admit_kernel, dim3(1), dim3(kPlanThreads), 0, stream, a);
+    const auto plan = pow2 ? plan_kernel<true, true> : plan_kernel<false, true>;
+    hipLaunchKernelGGL(plan, dim3(a.num_reqs), dim3(kPlanThreads), 0, stream, a);
+    return hipGetLastError();
+  }
   // at least one workgroup: an empty batch still writes the offsets' ends and the counters
-  hipLaunchKernelGGL(pow2 ? plan_kernel<true> : plan_kernel<false>,
-                     dim3(a.num_reqs > 0 ? a.num_reqs : 1), dim3(kPlanThreads), 0, stream, a);
+  const auto plan = pow2 ? plan_kernel<true, false> : plan_kernel<false, false>;
+  hipLaunchKernelGGL(plan, dim3(a.num_reqs > 0 ? a.num_reqs : 1), dim3(kPlanThreads), 0, stream,
+                     a);
   return hipGetLastError();
 }
 

@@ -186,13 +186,15 @@ def test_side_stream_and_stream_order():
 # device-detected errors: status word set, no KV byte written
 # ------------------------------------------------------------------------------------------
 
-@pytest.fixture(params=["small", "large", "large_repack_free"])
+@pytest.fixture(params=["small", "large", "large_repack_free", "many"])
 def error_batch(request):
-    """A batch under the one-launch planning bound (16384 tokens, 256 requests) and one above it
-    (count launch + plan launch): every device-detected error is checked on both paths, and
-    with the copy and the freed list in one launch."""
-    lens = (300, 900) if request.param == "small" else (4000, 6000)
-    make = lambda: W.llama3_8b_random(207, num_layers=1, num_reqs=5, len_range=lens)  # noqa
+    """A batch under the one-launch planning bound (8192 tokens, 24 requests), one above it
+    (count launch + plan launch) and one of more requests than the plan workgroups admit
+    themselves (600: count, admission and plan launches): every device-detected error is
+    checked on each path, and with the copy and the freed list in one launch."""
+    lens = {"small": (300, 900), "many": (40, 120)}.get(request.param, (4000, 6000))
+    R = 600 if request.param == "many" else 5
+    make = lambda: W.llama3_8b_random(207, num_layers=1, num_reqs=R, len_range=lens)  # noqa
     return make, request.param.endswith("repack_free")
 
 
@@ -329,22 +331,22 @@ def test_random_geometries(seed):
 
 @pytest.mark.parametrize("extra", [0, 1], ids=["at_token_bound", "past_token_bound"])
 def test_small_batch_planning_bound_tokens(extra):
-    """16384 tokens are planned by the one-launch kernel, 16385 by the count and plan launches:
+    """8192 tokens are planned by the one-launch kernel, 8193 by the count and plan launches:
     both equal the oracle on the same requests (the last one a token longer)."""
     rng = np.random.default_rng(40 + extra)
-    lens = [1500] * 10 + [16384 - 15000 + extra]
+    lens = [700] * 10 + [8192 - 7000 + extra]
     masks = [(rng.random(n) < 0.4).astype(int).tolist() for n in lens]
     M = sum(-(-n // 16) for n in lens)
     inp = W.from_masks(masks, W.KVShape(1, 2, 64, 16, "fp16"), free_blocks=M, seed=extra,
                        name=f"bound_tokens_{extra}")
-    assert inp.num_tokens == 16384 + extra
+    assert inp.num_tokens == 8192 + extra
     full_parity(inp, seed=3)
 
 
 @pytest.mark.parametrize("mode", ["three_calls", "repack_free", "in_place"])
 @pytest.mark.parametrize("S", [24, 48])
 def test_large_batch_block_size_not_power_of_two(S, mode):
-    """Past both small-batch bounds (340 requests, over 16384 tokens) with a block size that is
+    """Past the one-launch bounds (340 requests, over 16384 tokens) with a block size that is
     not a power of two, so the count and plan launches divide positions by S; the admitted
     requests take more destination blocks than the free list's head the plan kernel stages."""
     rng = np.random.default_rng(S)
@@ -358,13 +360,21 @@ def test_large_batch_block_size_not_power_of_two(S, mode):
     assert orc.n_admitted > 256 and (mode == "in_place" or orc.used > 8192)
 
 
-@pytest.mark.parametrize("R", [256, 257])
-def test_small_batch_planning_bound_requests(R):
-    """256 requests are planned by the one-launch kernel, 257 by the count and plan launches."""
+@pytest.mark.parametrize("R", [24, 25, 512, 513, 1100, 4200])
+def test_planning_bounds_requests(R):
+    """24 requests are planned by the one-launch kernel, 25 by the count and plan launches; up
+    to 512 every plan workgroup runs the admission itself, from 513 one launch runs it before
+    the plan launch (1100: several 1024-request rounds; 4200: past the 4096 live counts that
+    launch stages in LDS). A third of the blocks the requests hold are free, so the admission
+    defers a suffix of the profitable requests."""
     rng = np.random.default_rng(R)
     masks = [(rng.random(int(n)) < 0.5).astype(int).tolist()
              for n in rng.integers(0, 60, size=R)]
     M = sum(-(-len(m) // 16) for m in masks)
-    inp = W.from_masks(masks, W.KVShape(1, 2, 64, 16, "bf16"), free_blocks=M // 2, seed=R,
+    inp = W.from_masks(masks, W.KVShape(1, 2, 64, 16, "bf16"), free_blocks=M // 3, seed=R,
                        name=f"bound_requests_{R}")
-    full_parity(inp, seed=4)
+    gpu, orc = full_parity(inp, seed=4)
+    profitable = sum(-(-sum(m) // 16) < -(-len(m) // 16) for m in masks)
+    assert 0 < orc.n_admitted < profitable
+    full_parity(inp, seed=4, fused=True)
+    full_parity(inp, seed=4, inplace=True)
