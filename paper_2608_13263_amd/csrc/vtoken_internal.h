@@ -16,10 +16,15 @@ constexpr int kPlanThreads = 1024;
 constexpr int kPlanBallots = 8;                            // ballots per wave per tile
 constexpr int kPlanTile = kPlanThreads * kPlanBallots;     // tokens per tile (8192)
 constexpr int kPlanHead = 8192;   // free-list entries a plan workgroup holds in LDS (32 KiB)
-// batches of more requests run the admission once, in a launch of its own, instead of in
-// every plan workgroup; it stages the first kAdmitStage live counts and table lengths in LDS
+// Batches of more than kFusedAdmitReqs requests (kFusedAdmitShortReqs when their requests
+// average fewer than kLongRequestTokens tokens) run the admission once, in a launch of its
+// own, instead of in every plan workgroup; it stages the first kAdmitStage live counts and
+// table lengths in LDS, and their plan workgroups have kPlanThreadsSplit threads.
 constexpr int kFusedAdmitReqs = 512;
+constexpr int kFusedAdmitShortReqs = 256;
+constexpr int kLongRequestTokens = 1024;
 constexpr int kAdmitStage = 4096;
+constexpr int kPlanThreadsSplit = 256;
 // Batches this small are planned by one workgroup in one launch (they are bound by launch
 // latency); larger ones by a count launch and a plan launch of one workgroup per request.
 constexpr int kSmallReqs = 24;

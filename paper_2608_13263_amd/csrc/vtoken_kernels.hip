@@ -2,9 +2,10 @@
 //
 //   count_kernel   one workgroup per request: validates the request's CSR ranges and block
 //                  ids and counts its live tokens (16-byte loads of the live mask).
-//   admit_kernel   batches of more than 512 requests: the admission over all requests
-//                  (destination need ceil(live/S), strict gain, prefix admission against the
-//                  free list: Sec. 3.3.2, 3.3.3, I4 of Sec. 3.5) in one workgroup.
+//   admit_kernel   large batches (over 512 requests; over 256 of short ones): the admission
+//                  over all requests (destination need ceil(live/S), strict gain, prefix
+//                  admission against the free list: Sec. 3.3.2, 3.3.3, I4 of Sec. 3.5) in
+//                  one workgroup.
 //   plan_kernel    one workgroup per request: the admission (each workgroup over all
 //                  requests, or read from admit_kernel's outputs), then the request's new
 //                  block table, token slots (slot = block * S + offset, Sec. 3.4; ranks by
@@ -30,6 +31,8 @@ using namespace vtoken::meta;
 
 static_assert(kPlanThreads % 64 == 0 && kPlanThreads <= 1024,
               "the workgroup scans take at most 16 waves");
+static_assert(kPlanThreadsSplit % 64 == 0 && kPlanThreadsSplit <= kPlanThreads,
+              "plan workgroups of whole waves");
 
 
 // ------------------------------------------------------------------------------------------
@@ -235,8 +238,8 @@ __device__ __forceinline__ int admission_status(const MetaArgs& a, const Admissi
 // Step 1b, large batches: the admission alone, in one workgroup (destination need
 // ceil(live/S), strict gain, prefix admission; Sec. 3.3.2, 3.3.3, I4 of Sec. 3.5). It writes
 // every request's admitted flag and CSR offsets, the offsets' ends, the totals and the status
-// word, which plan_kernel<kPow2, true> then reads instead of repeating the admission in each of
-// its R workgroups (R/1024 rounds of workgroup scans each, O(R^2) over the launch). The live
+// word, which plan_kernel<kPow2, true, ...> then reads instead of repeating the admission in
+// each of its R workgroups (R/1024 rounds of workgroup scans each, O(R^2) over the launch). The live
 // counts and table lengths of the first kAdmitStage requests are staged in LDS, all of their
 // loads in flight at once.
 // ------------------------------------------------------------------------------------------
@@ -280,9 +283,10 @@ __global__ __launch_bounds__(kPlanThreads) void admit_kernel(MetaArgs a) {
 }
 
 // ------------------------------------------------------------------------------------------
-// Step 1b: the plan. For batches of at most kFusedAdmitReqs requests every workgroup first
-// runs the admission over all requests itself (each reads the R live counts; one round of two
-// workgroup scans, one wave alone for R <= 64): destination need ceil(live/S), strict gain
+// Step 1b: the plan. For batches of at most kFusedAdmitReqs requests (kFusedAdmitShortReqs of
+// short ones) every workgroup first runs the admission over all requests itself (each reads
+// the R live counts; one round of two workgroup scans, one wave alone for R <= 64):
+// destination need ceil(live/S), strict gain
 // (Sec. 3.3.3, I4 of Sec. 3.5), prefix admission against the free list (Sec. 3.3.2), and the
 // CSR offsets of its own request; the workgroup of request 0 also writes the totals and the
 // status word. No workgroup waits for another, so the admission costs one extra pass per
@@ -293,13 +297,20 @@ __global__ __launch_bounds__(kPlanThreads) void admit_kernel(MetaArgs a) {
 // mask, the order-preserving fill of Sec. 3.3.3) and its rows of the per-destination source
 // plan.
 // ------------------------------------------------------------------------------------------
-template <bool kPow2, bool kAdmitted>
-__global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
-  __shared__ int lds[kPlanThreads / 64][4];
-  __shared__ int wave_total[kPlanThreads / 64];
+template <bool kPow2, bool kAdmitted, int kThreads>
+__global__ __launch_bounds__(kThreads) void plan_kernel(MetaArgs a) {
+  // With the admission done before, a workgroup only builds its request's table and holds no
+  // free-list head in LDS: kPlanThreadsSplit threads, so that many are resident at once (the
+  // admission in the workgroup takes all kPlanThreads, and a 16-wave workgroup of these
+  // registers leaves room for one per CU).
+  static_assert(kAdmitted || kThreads == kPlanThreads, "the admission takes 16 waves");
+  constexpr int kWaves = kThreads / 64;
+  constexpr int kTile = kThreads * kPlanBallots;   // tokens per tile
+  __shared__ int lds[kWaves][4];
+  __shared__ int wave_total[kWaves];
   __shared__ int first_error_req;
   __shared__ int mine[4];   // admitted, destination offset, new-table offset, freed offset
-  __shared__ int32_t head[kPlanHead];   // free_list[0 .. P)
+  __shared__ int32_t head[kAdmitted ? 1 : kPlanHead];   // free_list[0 .. P)
   const int r = blockIdx.x;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -327,11 +338,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
     m_pre = a.bt_indptr[tid + 1] - a.bt_indptr[tid];
   }
   const int P = kAdmitted || a.inplace ? 0 : min(a.free_len, kPlanHead);
-  int32_t fl[kPlanHead / kPlanThreads];
+  int32_t fl[kPlanHead / kThreads];
+  if constexpr (!kAdmitted) {
 #pragma unroll
-  for (int q = 0; q < kPlanHead / kPlanThreads; ++q) {
-    const int j = q * kPlanThreads + tid;
-    fl[q] = j < P ? a.free_list[j] : 0;
+    for (int q = 0; q < kPlanHead / kThreads; ++q) {
+      const int j = q * kThreads + tid;
+      fl[q] = j < P ? a.free_list[j] : 0;
+    }
   }
 
   // this request's first tile of live bits and the block-table entries of its positions do not
@@ -357,10 +370,12 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
     phys0[k] = ok ? bt[bd.div(pos)] : 0;
   }
 
+  if constexpr (!kAdmitted) {
 #pragma unroll
-  for (int q = 0; q < kPlanHead / kPlanThreads; ++q) {
-    const int j = q * kPlanThreads + tid;
-    if (j < P) head[j] = fl[q];
+    for (int q = 0; q < kPlanHead / kThreads; ++q) {
+      const int j = q * kThreads + tid;
+      if (j < P) head[j] = fl[q];
+    }
   }
   int status = pre_status;
   if constexpr (!kAdmitted) {
@@ -400,8 +415,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
   if (!my_adm) {
     // unchanged: the old table, every live token at its positional slot
     const int m = a.bt_indptr[r + 1] - b0;
-    for (int j = tid; j < m; j += kPlanThreads) nbt[j] = bt[j];
-    for (int base = 0; base < n; base += kPlanTile) {
+    for (int j = tid; j < m; j += kThreads) nbt[j] = bt[j];
+    for (int base = 0; base < n; base += kTile) {
       if (base > 0) {   // later tiles: unconditional loads, positions clamped
 #pragma unroll
         for (int k = 0; k < kPlanBallots; ++k) {
@@ -426,14 +441,14 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
   const int32_t* dest = a.inplace ? bt : a.free_list + o;
   const int32_t* dest_s = head + o;
   int32_t* plan = a.src_plan + (int64_t)o * S;
-  for (int j = tid; j < need; j += kPlanThreads) nbt[j] = dest_lds ? dest_s[j] : dest[j];
+  for (int j = tid; j < need; j += kThreads) nbt[j] = dest_lds ? dest_s[j] : dest[j];
   if (need == 0) {
     // no live token (every block is released): only dead slots to write
-    for (int p = tid; p < n; p += kPlanThreads) ts[p] = -1;
+    for (int p = tid; p < n; p += kThreads) ts[p] = -1;
     return;
   }
   int carry = 0;
-  for (int base = 0; base < n; base += kPlanTile) {
+  for (int base = 0; base < n; base += kTile) {
     const int wbase = base + wave * (64 * kPlanBallots);
     // the tile's live bytes and table entries: the first tile's were loaded before the
     // admission; later tiles load theirs here, unconditionally (positions clamped to the
@@ -460,7 +475,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
     __syncthreads();
     int off = carry, tile = 0;
 #pragma unroll
-    for (int w = 0; w < kPlanThreads / 64; ++w) {
+    for (int w = 0; w < kWaves; ++w) {
       const int x = wave_total[w];
       off += (w < wave) ? x : 0;
       tile += x;
@@ -496,7 +511,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(MetaArgs a) {
     __syncthreads();
   }
   // destination slots past the last live token: nothing to copy
-  for (int k = c + tid; k < need * S; k += kPlanThreads) plan[k] = -1;
+  for (int k = c + tid; k < need * S; k += kThreads) plan[k] = -1;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -756,14 +771,17 @@ hipError_t launch_build(const MetaArgs& a, hipStream_t stream) {
   if (a.num_reqs > 0) {
     hipLaunchKernelGGL(count_kernel, dim3(a.num_reqs), dim3(kCountThreads), 0, stream, a);
   }
-  if (a.num_reqs > kFusedAdmitReqs) {
+  const bool long_reqs = a.num_reqs > 0 && a.num_tokens / a.num_reqs >= kLongRequestTokens;
+  if (a.num_reqs > kFusedAdmitReqs || (a.num_reqs > kFusedAdmitShortReqs && !long_reqs)) {
     hipLaunchKernelGGL(admit_kernel, dim3(1), dim3(kPlanThreads), 0, stream, a);
-    const auto plan = pow2 ? plan_kernel<true, true> : plan_kernel<false, true>;
-    hipLaunchKernelGGL(plan, dim3(a.num_reqs), dim3(kPlanThreads), 0, stream, a);
+    const auto plan = pow2 ? plan_kernel<true, true, kPlanThreadsSplit>
+                           : plan_kernel<false, true, kPlanThreadsSplit>;
+    hipLaunchKernelGGL(plan, dim3(a.num_reqs), dim3(kPlanThreadsSplit), 0, stream, a);
     return hipGetLastError();
   }
   // at least one workgroup: an empty batch still writes the offsets' ends and the counters
-  const auto plan = pow2 ? plan_kernel<true, false> : plan_kernel<false, false>;
+  const auto plan =
+      pow2 ? plan_kernel<true, false, kPlanThreads> : plan_kernel<false, false, kPlanThreads>;
   hipLaunchKernelGGL(plan, dim3(a.num_reqs > 0 ? a.num_reqs : 1), dim3(kPlanThreads), 0, stream,
                      a);
   return hipGetLastError();

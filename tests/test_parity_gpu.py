@@ -344,32 +344,37 @@ def test_small_batch_planning_bound_tokens(extra):
 
 
 @pytest.mark.parametrize("mode", ["three_calls", "repack_free", "in_place"])
-@pytest.mark.parametrize("S", [24, 48])
-def test_large_batch_block_size_not_power_of_two(S, mode):
-    """Past the one-launch bounds (340 requests, over 16384 tokens) with a block size that is
-    not a power of two, so the count and plan launches divide positions by S; the admitted
-    requests take more destination blocks than the free list's head the plan kernel stages."""
-    rng = np.random.default_rng(S)
-    lens = rng.integers(0, 64 * S, size=340)
+@pytest.mark.parametrize("S,R", [(24, 340), (48, 340), (24, 700)])
+def test_large_batch_block_size_not_power_of_two(S, R, mode):
+    """Past the one-launch bounds (340 or 700 requests, over 16384 tokens) with a block size
+    that is not a power of two, so the plan launch divides positions by S: 340 requests of
+    ~48 blocks with S = 48 (~1,536 tokens) are admitted by every plan workgroup itself, whose
+    destinations reach past the free-list head it stages in LDS; with S = 24 (~768 tokens) and
+    with 700 requests the admission runs in a launch of its own before the plan launch."""
+    rng = np.random.default_rng(S + R)
+    lens = rng.integers(0, 64 * S, size=R)
     masks = [(rng.random(int(n)) < rng.uniform(0.8, 1.0)).astype(int).tolist() for n in lens]
     M = sum(-(-len(m) // S) for m in masks)
     inp = W.from_masks(masks, W.KVShape(1, 1, 8, S, "fp16"), free_blocks=M, seed=S,
-                       name=f"large_block{S}")
+                       name=f"large_block{S}_{R}")
     assert inp.num_tokens > 16384 and inp.num_reqs > 256
     gpu, orc = full_parity(inp, seed=S, fused=mode == "repack_free", inplace=mode == "in_place")
     assert orc.n_admitted > 256 and (mode == "in_place" or orc.used > 8192)
 
 
-@pytest.mark.parametrize("R", [24, 25, 512, 513, 1100, 4200])
-def test_planning_bounds_requests(R):
-    """24 requests are planned by the one-launch kernel, 25 by the count and plan launches; up
-    to 512 every plan workgroup runs the admission itself, from 513 one launch runs it before
-    the plan launch (1100: several 1024-request rounds; 4200: past the 4096 live counts that
-    launch stages in LDS). A third of the blocks the requests hold are free, so the admission
-    defers a suffix of the profitable requests."""
+@pytest.mark.parametrize("R,lens", [(24, (0, 60)), (25, (0, 60)), (256, (0, 60)), (257, (0, 60)),
+                                    (512, (1100, 1400)), (513, (1100, 1400)), (1100, (0, 60)),
+                                    (4200, (0, 60))])
+def test_planning_bounds_requests(R, lens):
+    """24 requests are planned by the one-launch kernel, 25 by the count and plan launches. Up
+    to 256 requests every plan workgroup runs the admission itself, and up to 512 when the
+    requests average 1024 tokens or more; past that one launch runs the admission before the
+    plan launch (1100: several 1024-request rounds; 4200: past the 4096 live counts that launch
+    stages in LDS). A third of the blocks the requests hold are free, so the admission defers a
+    suffix of the profitable requests."""
     rng = np.random.default_rng(R)
     masks = [(rng.random(int(n)) < 0.5).astype(int).tolist()
-             for n in rng.integers(0, 60, size=R)]
+             for n in rng.integers(lens[0], lens[1], size=R)]
     M = sum(-(-len(m) // 16) for m in masks)
     inp = W.from_masks(masks, W.KVShape(1, 2, 64, 16, "bf16"), free_blocks=M // 3, seed=R,
                        name=f"bound_requests_{R}")
