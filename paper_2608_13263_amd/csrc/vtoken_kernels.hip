@@ -300,9 +300,9 @@ __global__ __launch_bounds__(kPlanThreads) void admit_kernel(MetaArgs a) {
 template <bool kPow2, bool kAdmitted, int kThreads>
 __global__ __launch_bounds__(kThreads) void plan_kernel(MetaArgs a) {
   // With the admission done before, a workgroup only builds its request's table and holds no
-  // free-list head in LDS: kPlanThreadsSplit threads, so that many are resident at once (the
-  // admission in the workgroup takes all kPlanThreads, and a 16-wave workgroup of these
-  // registers leaves room for one per CU).
+  // free-list head in LDS: kPlanThreadsSplit threads, so that more requests are in progress at
+  // once (the admission in the workgroup takes all kPlanThreads; with 1024 threads per request
+  // the plan of 257 short requests takes 4-5 us longer than that of 256, one per CU).
   static_assert(kAdmitted || kThreads == kPlanThreads, "the admission takes 16 waves");
   constexpr int kWaves = kThreads / 64;
   constexpr int kTile = kThreads * kPlanBallots;   // tokens per tile
