@@ -329,6 +329,32 @@ def test_random_geometries(seed):
     full_parity(inp, seed=seed, fused=True)
 
 
+def _random_large_case(seed):
+    """A random batch of 200-1500 requests (either side of the separate admission, short and
+    long requests), block sizes 1-96, small rows, a free list from a tenth of the requests'
+    blocks (deferral) to ample."""
+    rng = np.random.default_rng(seed)
+    S = int(rng.choice([1, 3, 8, 16, 24, 32, 48, 96]))
+    R = int(rng.integers(200, 1501))
+    top = int(rng.choice([60, 400, 3000]))
+    masks = [(rng.random(int(n)) < rng.random()).astype(int).tolist()
+             for n in rng.integers(0, top, size=R)]
+    M = sum(-(-len(m) // S) for m in masks)
+    free = int(M * rng.choice([0.1, 0.5, 2.0]))
+    return W.from_masks(masks, W.KVShape(1, 1, 8, S, "fp16"), free_blocks=free, seed=seed,
+                        name=f"fuzz_large{seed}")
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_large_batches(seed):
+    """Seeded random large batches, out of place (three calls and repack_free) and in place,
+    bit-exact."""
+    inp = _random_large_case(5000 + seed)
+    full_parity(inp, seed=seed)
+    full_parity(inp, seed=seed, fused=True)
+    full_parity(inp, seed=seed, inplace=True)
+
+
 @pytest.mark.parametrize("extra", [0, 1], ids=["at_token_bound", "past_token_bound"])
 def test_small_batch_planning_bound_tokens(extra):
     """8192 tokens are planned by the one-launch kernel, 8193 by the count and plan launches:
