@@ -203,7 +203,7 @@ def recorded_traffic(kernel: str, workload: str, bytes_alg: int):
                 continue
             path = os.path.join(ROOT, src)
             if os.path.exists(path) and hashlib.sha256(open(path, "rb").read()).hexdigest() == sha:
-                return float(traffic)
+                return int(traffic)
     return None
 
 

@@ -34,7 +34,7 @@ def test_traffic_records_resolve_only_on_their_source():
     for kernel, workload, src, sha, alg, traffic in recs:
         assert 0.99 < int(traffic) / int(alg) < 1.2
         digest = hashlib.sha256(open(os.path.join(ROOT, src), "rb").read()).hexdigest()
-        expect = float(traffic) if digest == sha else None
+        expect = int(traffic) if digest == sha else None
         assert bench.recorded_traffic(kernel, workload, int(alg)) == expect
 
 
