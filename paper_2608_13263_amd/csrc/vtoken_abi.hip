@@ -180,10 +180,12 @@ vtoken_status vtoken_repack_inplace_ex(const vtoken_cache* cache, const vtoken_b
 }  // extern "C"
 
 namespace {
-// The out-of-place copy, and with freed != nullptr the freed list in the same launch.
+// The out-of-place copy, and with with_free the freed list in the same launch.
+// with_free: vtoken_repack_free, the freed list written by workgroups of the copy's launch
 vtoken_status repack_out_of_place(const vtoken_cache* cache, const vtoken_batch* batch,
                                   const vtoken_plan* plan, const vtoken_repack_options* options,
-                                  int32_t* freed, int64_t freed_capacity, hipStream_t stream) {
+                                  bool with_free, int32_t* freed, int64_t freed_capacity,
+                                  hipStream_t stream) {
   vtoken_status s = check_cache(cache);
   if (s != VTOKEN_OK) return s;
   if ((s = check_batch(batch)) != VTOKEN_OK) return s;
@@ -204,8 +206,9 @@ vtoken_status repack_out_of_place(const vtoken_cache* cache, const vtoken_batch*
   // the copy never needs more destination blocks than the free list or the plan holds
   const int64_t by_plan = plan->src_plan_capacity / cache->block_size;
   int64_t max_used = batch->free_len < by_plan ? batch->free_len : by_plan;
-  // nothing can have been copied (requests with no live token may still release blocks)
-  if (max_used == 0 && (freed == nullptr || batch->num_reqs == 0)) return VTOKEN_OK;
+  // nothing can have been copied (the freed-list workgroups still run: requests with no live
+  // token may release blocks, and they check the plan's mode)
+  if (max_used == 0 && (!with_free || batch->num_reqs == 0)) return VTOKEN_OK;
   vtoken::CopyArgs a = {};
   a.kv = static_cast<uint8_t*>(cache->kv);
   a.row_bytes = (int64_t)cache->num_kv_heads * cache->head_dim * cache->elem_bytes;
@@ -222,7 +225,7 @@ vtoken_status repack_out_of_place(const vtoken_cache* cache, const vtoken_batch*
   a.src_plan = plan->src_plan;
   a.free_list = batch->free_list;
   a.counters = plan->counters;
-  if (freed != nullptr) {
+  if (with_free) {
     a.num_reqs = batch->num_reqs;
     a.num_bt_entries = batch->num_bt_entries;
     a.bt_indptr = batch->bt_indptr;
@@ -241,7 +244,7 @@ extern "C" {
 vtoken_status vtoken_repack_ex(const vtoken_cache* cache, const vtoken_batch* batch,
                                const vtoken_plan* plan, const vtoken_repack_options* options,
                                hipStream_t stream) {
-  return repack_out_of_place(cache, batch, plan, options, nullptr, 0, stream);
+  return repack_out_of_place(cache, batch, plan, options, false, nullptr, 0, stream);
 }
 
 vtoken_status vtoken_repack_free(const vtoken_cache* cache, const vtoken_batch* batch,
@@ -255,10 +258,7 @@ vtoken_status vtoken_repack_free(const vtoken_cache* cache, const vtoken_batch* 
   if (batch->num_reqs > 0 && plan->admitted == nullptr) return VTOKEN_ERR_NULL;
   if (freed_capacity < batch->num_bt_entries) return VTOKEN_ERR_CAPACITY;
   if (batch->num_bt_entries > 0 && freed == nullptr) return VTOKEN_ERR_NULL;
-  // with no table entries there is nothing to release: the copy alone
-  return repack_out_of_place(cache, batch, plan, nullptr,
-                             batch->num_bt_entries > 0 ? freed : nullptr, freed_capacity,
-                             stream);
+  return repack_out_of_place(cache, batch, plan, nullptr, true, freed, freed_capacity, stream);
 }
 
 vtoken_status vtoken_repack(const vtoken_cache* cache, const vtoken_batch* batch,

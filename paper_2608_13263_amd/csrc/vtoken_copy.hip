@@ -93,7 +93,7 @@ __global__ __launch_bounds__(kCopyThreads) void repack_direct_kernel(CopyArgs a)
   // plans of the full pass; plans of the partial pass too, but not with the freed list of
   // vtoken_repack_free (a partial pass releases its selected sources, not table tails)
   const int mode = a.counters[4];
-  if (mode != kPlanOutOfPlace && (mode != kPlanPartial || a.freed != nullptr)) {
+  if (mode != kPlanOutOfPlace && (mode != kPlanPartial || a.num_reqs > 0)) {
     plan_mode_error(a.counters);
     return;
   }
@@ -220,7 +220,7 @@ hipError_t launch_kernel(const CopyArgs& a_in, int64_t items, int grid, hipStrea
   CopyArgs a = a_in;
   a.copy_grid = grid;
   // the freed list's workgroups follow the copy's
-  const int64_t total = grid + (a.freed != nullptr ? (int64_t)a.num_reqs : 0);
+  const int64_t total = (int64_t)grid + a.num_reqs;
   if (total <= 0) return hipSuccess;
   hipLaunchKernelGGL(kKernel, dim3(static_cast<unsigned>(total)), dim3(kCopyThreads), 0, stream,
                      a);

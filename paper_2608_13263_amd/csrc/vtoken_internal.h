@@ -89,7 +89,8 @@ struct CopyArgs {
   int32_t* counters;        // read; the status word is set if the plan's mode does not match
   int32_t copy_grid;        // workgroups of the copy (set by the launch)
   // the freed list in the same launch (vtoken_repack_free): the num_reqs workgroups after the
-  // copy's write request r's released blocks; freed == nullptr: none
+  // copy's write request r's released blocks; num_reqs == 0: none (vtoken_repack). freed may be
+  // null when the batch has no table entries (nothing to write)
   int32_t num_reqs;
   int64_t num_bt_entries;
   const int32_t* bt_indptr;

@@ -118,6 +118,38 @@ def test_freed_list_refuses_a_partial_plan(call):
     assert bool((freed == -9).all()), "a freed list was written for a partial plan"
 
 
+@pytest.mark.parametrize("call", ["free_blocks", "repack_free"])
+def test_partial_plan_refused_with_no_table_entries(call):
+    """The same refusal for a batch whose requests hold no blocks (M = 0): the freed-list
+    workgroups of vtoken_repack_free still run and find the partial mode, as vtoken_free_blocks
+    does after vtoken_repack."""
+    t = torch()
+    B = _B()
+    inp = W.from_masks([[], [], []], W.KVShape(1, 2, 64, 16, "fp16"), free_blocks=8, seed=1,
+                       name="no_table_entries")
+    assert inp.num_bt_entries == 0 and inp.num_reqs == 3
+    sh = inp.shape
+    print(f"[gpu] partial plan of a batch without table entries handed to {call}", flush=True)
+    kv = W.kv_device(sh, inp.num_blocks, 3)
+    cache = B.KVCache(kv, sh.num_layers, sh.num_kv_heads, sh.head_dim, sh.block_size)
+    batch = B.Batch.from_inputs(inp)
+    slot_in = t.zeros(1, dtype=t.int32, device="cuda")
+    plan = B.Plan.allocate(batch, sh.block_size)
+    state = B.PlannerState.allocate(inp.num_blocks, batch)
+    B.plan_partial(cache, batch, slot_in, plan, state, B.PlannerParams())
+    t.cuda.synchronize()
+    assert plan.counters.cpu().tolist()[3:] == [0, 3]
+    if call == "free_blocks":
+        B.repack(cache, batch, plan)
+        t.cuda.synchronize()
+        assert int(plan.counters[3]) == 0
+        B.free_blocks(batch, plan)
+    else:
+        B.repack_free(cache, batch, plan)
+    t.cuda.synchronize()
+    assert int(plan.counters[3]) == B.STATUS_CODE["VTOKEN_ERR_PLAN_MODE"]
+
+
 def test_partial_pool_short_defers():
     B = _B()
     inp = W.token_table_inputs(622, W.KVShape(1, 2, 64, 16, "fp16"), num_reqs=12,
