@@ -643,6 +643,14 @@ def run_placement(args):
     return 0
 
 
+def gpu_busy_while_host_enqueues():
+    """Enqueue a spin kernel of about half a millisecond: the calls enqueued after it (their
+    argument marshalling included) are in the queue before it ends, so that events recorded
+    after it time the GPU work, not the host, when the GPU was idle before."""
+    import torch
+    torch.cuda._sleep(1_000_000)
+
+
 def run_scissorhands(args):
     """Scissorhands-style repeated repack: 256 requests, a repack every 512 decode steps in a
     pool of min(240 GiB, 85% of free HBM). A round is the host-side decode bookkeeping
@@ -672,6 +680,7 @@ def run_scissorhands(args):
             ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
                   torch.cuda.Event(enable_timing=True))
             torch.cuda.synchronize()
+            gpu_busy_while_host_enqueues()
             ev[0].record()
             if args.inplace:
                 B.build_token_table_inplace(cache, batch, plan)
@@ -775,6 +784,7 @@ def run_partial_stream(args):
             state = B.PlannerState.allocate(inp.num_blocks, batch, pinned=inp.pinned)
             ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
             torch.cuda.synchronize()
+            gpu_busy_while_host_enqueues()
             ev[0].record()
             B.plan_partial(cache, batch, slot_in, plan, state, params)
             ev[1].record()
