@@ -7,11 +7,11 @@
 //                      and the counters
 //   pl_count_kernel    references of every block over all tables; one bit per live slot
 //                      (a slot held live by several requests of a shared prefix counts once)
-//   pl_blocks_kernel   n_b = live bits of each allocated block (Sec. 2.3.1, Sec. 3.3.1); the
-//                      totals behind the waste ratio F
-//   pl_request_kernel  one workgroup per request: live count, its candidate blocks (unshared,
-//                      unpinned, n_b <= max_live) in table order with their cumulative live
-//                      tokens
+//   pl_blocks_request_kernel  two kinds of workgroups in one launch: up to 128 compute
+//                      n_b = live bits of each allocated block (Sec. 2.3.1, Sec. 3.3.1) and
+//                      the totals behind the waste ratio F; one per request finds its live
+//                      count and its candidate blocks (unshared, unpinned, n_b <= max_live) in
+//                      table order with their cumulative live tokens
 //   pl_admit_kernel    one workgroup: the trigger (F > theta_F, enough candidates, free list at
 //                      or below the watermark, Sec. 3.3.2), the bound B over the candidates in
 //                      request order, T_live, ceil(T_live / S), strict gain, admission against
@@ -67,11 +67,14 @@ __device__ __forceinline__ int pl_rank(bool flag, int* total, int* lds) {
   return off + lanes_below(m);
 }
 
-__device__ __forceinline__ bool pl_candidate(const PlannerArgs& a, int b) {
-  if (b < 0 || b >= a.num_blocks) return false;
-  if (a.refs[b] != 1) return false;                      // shared-prefix blocks never move
-  if (a.pinned != nullptr && a.pinned[b] != 0) return false;
-  return a.n_b[b] <= a.max_live;
+// n_b of block b if it is a candidate source (unshared, unpinned, n_b <= max_live), else -1;
+// n_b from the block's live bits, so that it does not wait for pl_blocks (the same launch)
+__device__ __forceinline__ int pl_candidate_live(const PlannerArgs& a, int b) {
+  if (b < 0 || b >= a.num_blocks) return -1;
+  if (a.refs[b] != 1) return -1;                         // shared-prefix blocks never move
+  if (a.pinned != nullptr && a.pinned[b] != 0) return -1;
+  const int n = __popcll(a.live_bits[b]);
+  return n <= a.max_live ? n : -1;
 }
 
 __global__ __launch_bounds__(256) void pl_clear_kernel(PlannerArgs a) {
@@ -152,12 +155,12 @@ __global__ __launch_bounds__(256) void pl_count_kernel(PlannerArgs a) {
   }
 }
 
-__global__ __launch_bounds__(256) void pl_blocks_kernel(PlannerArgs a) {
+// n_b of every block and the totals behind F, by workgroups wg of nwg
+__device__ __forceinline__ void pl_blocks(const PlannerArgs& a, int wg, int nwg) {
   __shared__ int64_t red[2][4];
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t stride = (int64_t)nwg * blockDim.x;
   int64_t live = 0, alloc = 0;
-  for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < a.num_blocks;
-       b += stride) {
+  for (int64_t b = (int64_t)wg * blockDim.x + threadIdx.x; b < a.num_blocks; b += stride) {
     const bool held = a.refs[b] > 0;
     const int n = held ? __popcll(a.live_bits[b]) : 0;
     a.n_b[b] = n;
@@ -188,10 +191,10 @@ __global__ __launch_bounds__(256) void pl_blocks_kernel(PlannerArgs a) {
   }
 }
 
-__global__ __launch_bounds__(kPlThreads) void pl_request_kernel(PlannerArgs a) {
+// request r: live count and candidate blocks
+__device__ __forceinline__ void pl_request(const PlannerArgs& a, int r) {
   __shared__ int lds2[kPlWaves][2];
   __shared__ int wave_sum[kPlWaves];
-  const int r = blockIdx.x;
   const int tid = threadIdx.x;
   const int n = a.seq_lens[r];
   const int t0 = a.tok_indptr[r], t1 = a.tok_indptr[r + 1];
@@ -242,8 +245,9 @@ __global__ __launch_bounds__(kPlThreads) void pl_request_kernel(PlannerArgs a) {
   for (int base = 0; base < b1 - b0; base += kPlThreads) {
     const int j = base + tid;
     const int b = j < b1 - b0 ? a.block_ids[b0 + j] : -1;
-    const bool cand = j < b1 - b0 && pl_candidate(a, b);
-    const int nb = cand ? a.n_b[b] : 0;
+    const int cl = j < b1 - b0 ? pl_candidate_live(a, b) : -1;
+    const bool cand = cl >= 0;
+    const int nb = cand ? cl : 0;
     int v[2] = {cand ? 1 : 0, nb}, tot[2];
     block_exclusive_scan<2>(v, tot, lds2);
     if (cand) a.elig_cum[b0 + carry + v[0]] = live_carry + v[1] + nb;
@@ -254,6 +258,19 @@ __global__ __launch_bounds__(kPlThreads) void pl_request_kernel(PlannerArgs a) {
     a.src_count[r] = carry;
     if (carry) atomicAdd(reinterpret_cast<unsigned long long*>(&a.stats[2]),
                          static_cast<unsigned long long>(carry));
+  }
+}
+
+// Steps 2 and 3 of the planner in one launch: workgroups [0, blocks_grid) count the live
+// bits of every block (pl_blocks), the rest take one request each (pl_request). Both read only
+// what pl_count_kernel wrote.
+__global__ __launch_bounds__(kPlThreads) void pl_blocks_request_kernel(PlannerArgs a,
+                                                                       int blocks_grid) {
+  const int wg = static_cast<int>(blockIdx.x);
+  if (wg < blocks_grid) {
+    pl_blocks(a, wg, blocks_grid);
+  } else {
+    pl_request(a, wg - blocks_grid);
   }
 }
 
@@ -405,7 +422,7 @@ __global__ __launch_bounds__(kPlTableThreads) void pl_table_kernel(PlannerArgs a
     const int j = base + tid;
     const bool in = j < m;
     const int b = in ? a.block_ids[b0 + j] : -1;
-    const bool cand = in && adm && pl_candidate(a, b);
+    const bool cand = in && adm && pl_candidate_live(a, b) >= 0;
     int cnt;
     const int crank = cand_carry + pl_rank<kPlTableWaves>(cand, &cnt, lds_rank);
     cand_carry += cnt;
@@ -513,10 +530,9 @@ hipError_t launch_planner(const PlannerArgs& a, hipStream_t stream) {
                      stream, a);
   // at most 128 workgroups: each adds its totals with two atomics on the same two words
   const unsigned blocks_grid = grid_for(a.num_blocks) < 128u ? grid_for(a.num_blocks) : 128u;
-  hipLaunchKernelGGL(pl_blocks_kernel, dim3(blocks_grid), dim3(256), 0, stream, a);
-  if (a.num_reqs > 0) {
-    hipLaunchKernelGGL(pl_request_kernel, dim3(a.num_reqs), dim3(kPlThreads), 0, stream, a);
-  }
+  hipLaunchKernelGGL(pl_blocks_request_kernel,
+                     dim3(blocks_grid + static_cast<unsigned>(a.num_reqs > 0 ? a.num_reqs : 0)),
+                     dim3(kPlThreads), 0, stream, a, static_cast<int>(blocks_grid));
   hipLaunchKernelGGL(pl_admit_kernel, dim3(1), dim3(kPlAdmitThreads), 0, stream, a);
   if (a.num_reqs > 0) {
     hipLaunchKernelGGL(pow2 ? pl_table_kernel<true> : pl_table_kernel<false>, dim3(a.num_reqs),
