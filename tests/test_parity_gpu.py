@@ -66,9 +66,11 @@ def _edge_masks(S, rng):
 
 
 @pytest.mark.parametrize("fused", [False, True], ids=["three_calls", "repack_free"])
-@pytest.mark.parametrize("S", [1, 2, 16, 32, 48, 128])
+@pytest.mark.parametrize("S", [1, 2, 16, 32, 48, 128, 256, 1000])
 def test_edge_masks_block_sizes(S, fused):
-    # S = 48 (not a power of two, several copy rounds) and S = 128 (plan read from memory)
+    # S = 48 (not a power of two, several copy rounds), S = 128 and 256 (plan read from
+    # memory; 64 KiB chunks: two parts) and S = 1000 (not a power of two, 250 KiB chunks: eight
+    # parts, the last one partial)
     rng = np.random.default_rng(S)
     shape = W.KVShape(1, 2, 64, S, "fp16")
     inp = W.from_masks(_edge_masks(S, rng), shape, free_blocks=64, seed=S)
