@@ -92,14 +92,17 @@ def parse_args(argv=None):
                     help="in-place mode: destinations are each request's own leading blocks; "
                          "bytes count only the rows that move")
     ap.add_argument("--mode", default="repack",
-                    choices=["repack", "copy", "decode", "overlap", "stream", "placement"],
+                    choices=["repack", "copy", "decode", "overlap", "stream", "placement",
+                             "plan"],
                     help="decode: the consumer side, paged decode attention of every layer "
                          "through the slot mapping, before and after the repack; overlap: a "
                          "decode step (every layer) on the main stream with the repack pass on "
                          "a relocation stream, against the two one after the other; stream: "
                          "read / write / copy and decode-pattern probes, the memory system's "
                          "streaming ceilings; placement: the minimal 56 GiB pool allocated 4 times, "
-                         "repack and write / read probes on each (for counter runs)")
+                         "repack and write / read probes on each (for counter runs); plan: "
+                         "the table build alone on batches of 8 to 3277 requests, short and "
+                         "long, either side of its launch bounds")
     ap.add_argument("--q-heads", type=int, default=32, help="decode mode: query heads")
     ap.add_argument("--copy-gib", type=float, default=8.0)
     ap.add_argument("--graph", action="store_true",
@@ -497,6 +500,58 @@ def probe_library(rebuild: bool = False):
     lib.vtoken_probe_head_read.argtypes = [vp, i64, i32, vp, i64, i32, vp, vp]
     lib.vtoken_probe_plane_copy.argtypes = [vp, i64, i32, i64, i64, i64, vp]
     return lib
+
+
+def run_plan(args):
+    """vtoken_build_token_table alone on synthetic batches either side of its launch bounds
+    (one planning launch up to 24 requests and 8192 tokens; count and plan launches, the plan
+    workgroups admitting for themselves, up to 256 requests, or 512 averaging 1024 tokens or
+    more; a separate admission launch above): the median of 30 calls, each between HIP events
+    on the launch stream (a call's launch overhead included). 16-byte rows (the table build
+    does not read the cache), Bernoulli(0.5) liveness, free list of every request's blocks."""
+    import numpy as np
+    import torch
+    from paper_2608_13263_amd import binding as B
+    from paper_2608_13263_amd import workloads as W
+    rng = np.random.default_rng(args.seed if args.seed is not None else 0)
+    shapes = [("short", 32, 96, R) for R in (8, 24, 64, 256, 257, 512, 1024, 3277)]
+    shapes += [("long", 2048, 8192, R) for R in (64, 128, 256, 512, 1024)]
+    stream = torch.cuda.current_stream()
+    out = []
+    for kind, lo, hi, R in shapes:
+        lens = rng.integers(lo, hi + 1, size=R)
+        masks = [(rng.random(int(n)) < 0.5).astype(np.int8) for n in lens]
+        M = sum(-(-len(m) // 16) for m in masks)
+        inp = W.from_masks([m.tolist() for m in masks], W.KVShape(1, 1, 8, 16, "fp16"),
+                           free_blocks=M, seed=1, name=f"{kind}_{R}")
+        kv = W.kv_device(inp.shape, inp.num_blocks, 0)
+        cache = B.KVCache(kv, 1, 1, 8, 16)
+        batch = B.Batch.from_inputs(inp)
+        plan = B.Plan.allocate(batch, 16)
+        for _ in range(5):
+            B.build_token_table(cache, batch, plan, stream)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(30):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            B.build_token_table(cache, batch, plan, stream)
+            b.record(stream)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b) * 1e3)
+        status = int(plan.counters[3])
+        if status != 0:
+            raise SystemExit(f"device status {B.STATUS.get(status, status)}")
+        out.append({"requests": R, "tokens": inp.num_tokens, "kind": kind,
+                    "build_us": round(float(np.median(ts)), 1)})
+        log(f"plan {kind} R={R} T={inp.num_tokens}: {out[-1]['build_us']} us")
+        del kv, cache, batch, plan
+    print(json.dumps({"metric": "vtoken_build_token_table time per call (us)", "mode": "plan",
+                      "value": None, "unit": "us", "n_gpus": 1, "higher_is_better": False,
+                      "data": "synthetic", "cases": out,
+                      "config": {"workload": "plan_batches", "row_bytes": 16,
+                                 "block_size": 16, "keep": 0.5}}), flush=True)
+    return 0
 
 
 def run_stream(args):
@@ -1402,6 +1457,8 @@ def main(argv=None):
         return run_stream(args)
     if args.mode == "placement":
         return run_placement(args)
+    if args.mode == "plan":
+        return run_plan(args)
     if args.config == "llama3_8b_scissorhands":
         return run_partial_stream(args) if args.partial else run_scissorhands(args)
     if args.config == "llama3_8b_shared_prefix":
