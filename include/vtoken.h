@@ -26,10 +26,11 @@
  *     `stream` and returns. The calls therefore may be captured into a HIP graph.
  *   - Host-side argument errors return a negative status synchronously and enqueue
  *     nothing. Errors that only the device can see (a bad block id, inconsistent CSR
- *     lengths, a capacity exceeded) are written to plan->counters[3] by the first
- *     kernel of vtoken_build_token_table (a copy handed a plan of the other mode writes
- *     VTOKEN_ERR_PLAN_MODE there); every later kernel reads that word and does nothing
- *     when it is not VTOKEN_OK. The caller inspects it after its own sync.
+ *     lengths, a capacity exceeded) are written to plan->counters[3] by the kernels of
+ *     vtoken_build_token_table, before any table is built (a copy handed a plan of the
+ *     other mode writes VTOKEN_ERR_PLAN_MODE there); every later kernel reads that word
+ *     and does nothing when it is not VTOKEN_OK. The caller inspects it after its own
+ *     sync.
  *     Every kernel bounds-checks what it dereferences, so no status path writes
  *     outside the buffers the caller described.
  *   - The library is re-entrant: calls on different streams with disjoint buffers may
@@ -166,7 +167,9 @@ typedef struct vtoken_plan {
 
 /* Step 1 (Sec. 3.2, 3.3.2, 3.3.3): scan, admission, token table, block tables, plan.
  * Writes every field of *plan (device memory) except new_bt/src_plan capacity beyond
- * what is used. Returns VTOKEN_OK once the kernels are enqueued. */
+ * what is used. Returns VTOKEN_OK once the kernels are enqueued: one kernel for batches of
+ * at most 24 requests and 8,192 tokens, two (counts, then tables) up to 256 requests or up
+ * to 512 averaging at least 1,024 tokens, three (counts, admission, tables) above. */
 vtoken_status vtoken_build_token_table(const vtoken_cache* cache, const vtoken_batch* batch,
                                        const vtoken_plan* plan, hipStream_t stream);
 
