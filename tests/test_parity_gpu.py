@@ -244,8 +244,9 @@ def test_error_token_range(error_batch):
     _error_case(m, "VTOKEN_ERR_TOK_LEN", error_batch)
 
 
+@pytest.mark.parametrize("batch_kind", ["one_launch", "count_plan", "admission"])
 @pytest.mark.parametrize("inplace", [False, True], ids=["out_of_place", "in_place"])
-def test_pass_graph_replay(inplace):
+def test_pass_graph_replay(inplace, batch_kind):
     """The whole pass (build, copy, free) captured once in a HIP graph over fixed buffers and
     replayed: before each replay new liveness is written into the captured live-mask buffer
     and the KV bytes are whatever the previous replay left; every replay equals the oracle on
@@ -254,7 +255,11 @@ def test_pass_graph_replay(inplace):
     import dataclasses
     t = torch()
     from paper_2608_13263_amd import binding as B
-    inp = W.llama3_8b_random(231, num_layers=2, num_reqs=8, len_range=(300, 1500))
+    # the table build as one launch (8 requests), as count and plan launches (40) and with the
+    # admission in a launch of its own (600 short requests)
+    R, lens, layers = {"one_launch": (8, (300, 1500), 2), "count_plan": (40, (300, 1500), 1),
+                       "admission": (600, (40, 120), 1)}[batch_kind]
+    inp = W.llama3_8b_random(231, num_layers=layers, num_reqs=R, len_range=lens)
     sh = inp.shape
     kv = W.kv_device(sh, inp.num_blocks, 21)
     cache = B.KVCache(kv, sh.num_layers, sh.num_kv_heads, sh.head_dim, sh.block_size)
