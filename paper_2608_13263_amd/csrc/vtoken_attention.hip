@@ -66,6 +66,11 @@ __global__ __launch_bounds__(1024) void slot_indptr_kernel(SlotMapArgs a) {
   if (tid == 0) a.slot_indptr[a.num_reqs] = carry;
 }
 
+// One workgroup per request compacts its live token slots in logical order: tiles of
+// 16 waves x kSlotBallots x 64 tokens, every token_slot load of a tile in flight before its
+// ballots, one pair of barriers per tile.
+constexpr int kSlotBallots = 8;
+
 __global__ __launch_bounds__(1024) void slot_map_kernel(SlotMapArgs a) {
   __shared__ int wave_tot[16];
   if (a.counters[3] != 0) return;
@@ -77,21 +82,37 @@ __global__ __launch_bounds__(1024) void slot_map_kernel(SlotMapArgs a) {
   const int n = a.tok_indptr[r + 1] - t0;
   const int o = a.slot_indptr[r];
   if (t0 < 0 || n < 0 || (int64_t)t0 + n > a.num_tokens || o < 0) return;
+  const int32_t* ts = a.token_slot + t0;
   int carry = 0;
-  for (int base = 0; base < n; base += 1024) {
-    const int p = base + tid;
-    const int s = p < n ? a.token_slot[t0 + p] : -1;
-    const bool live = s >= 0;
-    const uint64_t m = __ballot(live);
-    if (lane == 0) wave_tot[wave] = __popcll(m);
+  for (int base = 0; base < n; base += 1024 * kSlotBallots) {
+    // wave w holds positions base + w*64*kSlotBallots + k*64 + lane
+    const int wbase = base + wave * (64 * kSlotBallots);
+    int s[kSlotBallots];
+#pragma unroll
+    for (int k = 0; k < kSlotBallots; ++k) {
+      const int p = wbase + k * 64 + lane;
+      s[k] = p < n ? ts[p] : -1;
+    }
+    int rank[kSlotBallots];
+    int local = 0;
+#pragma unroll
+    for (int k = 0; k < kSlotBallots; ++k) {
+      const uint64_t m = __ballot(s[k] >= 0);
+      rank[k] = local + lanes_below(m);
+      local += __popcll(m);
+    }
+    if (lane == 0) wave_tot[wave] = local;
     __syncthreads();
     int off = carry, tot = 0;
     for (int w = 0; w < 16; ++w) {
       off += w < wave ? wave_tot[w] : 0;
       tot += wave_tot[w];
     }
-    const int64_t k = (int64_t)o + off + lanes_below(m);
-    if (live && k < a.slots_capacity) a.slots[k] = s;
+#pragma unroll
+    for (int k = 0; k < kSlotBallots; ++k) {
+      const int64_t dst = (int64_t)o + off + rank[k];
+      if (s[k] >= 0 && dst < a.slots_capacity) a.slots[dst] = s[k];
+    }
     carry += tot;
     __syncthreads();
   }

@@ -104,6 +104,9 @@ SLOT_CASES = {
     "llama3_8b_random": lambda: W.llama3_8b_random(221, num_layers=1, num_reqs=16),
     "llama3_70b_fp8": lambda: W.llama3_70b_h2o(521, num_layers=1, num_reqs=4,
                                                len_range=(2000, 9000)),
+    # requests of two to three 8192-token compaction tiles with ragged tails
+    "long_requests": lambda: W.llama3_70b_h2o(522, num_layers=1, num_reqs=3,
+                                              len_range=(17000, 23000)),
 }
 
 
