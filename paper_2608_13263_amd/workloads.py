@@ -360,7 +360,7 @@ class ScissorhandsStream:
     A round is decode() followed by passes ("waves") until a pass repacks nothing: a pool
     too small for every destination at once defers the later requests to the next wave.
 
-    Initial state (before round 1): logical length L0 ~ U[len_range] - decode_steps; the
+    Initial state (before the first round): logical length L0 ~ U[len_range] - decode_steps; the
     request was packed by the previous round, holding a sorted random subset of
     [0, L0 - window) of size floor(budget * L0) - window plus the window [L0 - window, L0),
     with persistence scores Binomial(2 * decode_steps, min(1, 1/sqrt(1+age))).
