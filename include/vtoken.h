@@ -379,7 +379,10 @@ vtoken_status vtoken_append_slots(int32_t num_reqs, const int32_t* append_indptr
  * or >= num_blocks * block_size) is never dereferenced; its request's outputs are NaN. A
  * request whose slot range is malformed (slot_indptr[r] < 0, or a negative count:
  * slot_indptr[r+1] < slot_indptr[r], or slot_count[r] < 0) reads no slot and gets NaN
- * outputs. */
+ * outputs. The split launch has R * num_kv_heads * ceil(max_tokens / split) workgroups, and
+ * those past a request's slots return at once: pass the batch's largest slot count rather
+ * than a model's context limit (a bound 8 times too large cost the Llama-3-8B Random decode
+ * about 10% on MI355X). */
 enum { VTOKEN_KV_FP16 = 0, VTOKEN_KV_BF16 = 1, VTOKEN_KV_FP8_E4M3 = 2 };
 
 typedef struct vtoken_decode {
