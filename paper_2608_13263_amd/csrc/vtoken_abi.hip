@@ -417,7 +417,8 @@ vtoken_status paged_decode(const vtoken_cache* cache, const vtoken_decode* d, in
   const int split = vtoken::decode_split_tokens(D, cache->elem_bytes, g);
   a.split_tokens = split;
   a.splits = d->max_tokens > 0 ? (d->max_tokens + split - 1) / split : 1;
-  if ((int64_t)num_reqs * cache->num_kv_heads * a.splits > INT32_MAX ||
+  const int64_t grid_splits = vtoken::decode_grid_splits(a.splits);
+  if ((int64_t)num_reqs * cache->num_kv_heads * grid_splits > INT32_MAX ||
       (int64_t)num_reqs * d->num_q_heads > INT32_MAX) {
     return VTOKEN_ERR_SHAPE;
   }

@@ -346,10 +346,13 @@ void decode_split_kernel(AttnArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int split = blockIdx.x % a.splits;
-  const int h = (blockIdx.x / a.splits) % a.num_kv_heads;
-  const int r = blockIdx.x / (a.splits * a.num_kv_heads);
-  if (r >= a.num_reqs) return;
+  // the grid holds decode_grid_splits(a.splits) split slots per (request, KV head); one past
+  // a.splits (a count rounded up to an odd one) returns at once
+  const int gs = decode_grid_splits(a.splits);
+  const int split = blockIdx.x % gs;
+  const int h = (blockIdx.x / gs) % a.num_kv_heads;
+  const int r = blockIdx.x / (gs * a.num_kv_heads);
+  if (r >= a.num_reqs || split >= a.splits) return;
   const int s0 = a.slot_indptr[r];
   const int c = a.slot_count != nullptr ? a.slot_count[r] : a.slot_indptr[r + 1] - s0;
   const int t0 = split * kSplit;
@@ -738,7 +741,8 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(AttnArg
 
 template <int kKind, int kD, int kG>
 hipError_t launch_split(const AttnArgs& a, hipStream_t stream) {
-  const dim3 grid(static_cast<unsigned>((int64_t)a.num_reqs * a.num_kv_heads * a.splits));
+  const dim3 grid(
+      static_cast<unsigned>((int64_t)a.num_reqs * a.num_kv_heads * decode_grid_splits(a.splits)));
   auto kernel = decode_split_kernel<kKind, kD, kG>;
   hipLaunchKernelGGL(kernel, grid, dim3(64 * decode_split_waves(kKind == 2 ? 1 : 2, kG)), 0,
                      stream, a);
