@@ -12,6 +12,7 @@ namespace vtoken {
 
 // Launch geometry of the metadata kernels (one workgroup per request each).
 constexpr int kCountThreads = 512;
+constexpr int kCountThreadsShort = 128;   // for requests averaging < kLongRequestTokens
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanBallots = 8;                            // ballots per wave per tile
 constexpr int kPlanTile = kPlanThreads * kPlanBallots;     // tokens per tile (8192)

@@ -1,7 +1,8 @@
 // HIP kernels of the vToken repack's metadata steps for CDNA4 (gfx950, wave64).
 //
-//   count_kernel   one workgroup per request: validates the request's CSR ranges and block
-//                  ids and counts its live tokens (16-byte loads of the live mask).
+//   count_kernel   one workgroup per request (512 threads, 128 for short requests):
+//                  validates the request's CSR ranges and block ids and counts its live
+//                  tokens (16-byte loads of the live mask).
 //   admit_kernel   large batches (over 512 requests; over 256 of short ones): the admission
 //                  over all requests (destination need ceil(live/S), strict gain, prefix
 //                  admission against the free list: Sec. 3.3.2, 3.3.3, I4 of Sec. 3.5) in
@@ -40,8 +41,9 @@ static_assert(kPlanThreadsSplit % 64 == 0 && kPlanThreadsSplit <= kPlanThreads,
 // (Sec. 3.2: the token table's liveness bits). A request with an error stores the (negative)
 // error code as its live count, which the plan kernel picks up.
 // ------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kCountThreads) void count_kernel(MetaArgs a) {
-  __shared__ int wave_sum[kCountThreads / 64];
+template <int kThreads>
+__global__ __launch_bounds__(kThreads) void count_kernel(MetaArgs a) {
+  __shared__ int wave_sum[kThreads / 64];
   const int r = blockIdx.x;
   const int tid = threadIdx.x;
   const int S = a.block_size;
@@ -74,7 +76,7 @@ __global__ __launch_bounds__(kCountThreads) void count_kernel(MetaArgs a) {
   if (tid < head) cnt += lv[tid] != 0;
   if (tail0 + tid < n) cnt += lv[tail0 + tid] != 0;
   const uint4* w16 = reinterpret_cast<const uint4*>(lv + head);
-  for (int w = tid; w < iters; w += kCountThreads) {
+  for (int w = tid; w < iters; w += kThreads) {
     const int blk = w < m ? a.block_ids[b0 + w] : 0;
     const uint4 x = w < words ? w16[w] : make_uint4(0, 0, 0, 0);
     bad |= (blk < 0) | (blk >= a.num_blocks);
@@ -91,7 +93,7 @@ __global__ __launch_bounds__(kCountThreads) void count_kernel(MetaArgs a) {
   if (tid == 0) {
     int c = 0;
 #pragma unroll
-    for (int w = 0; w < kCountThreads / 64; ++w) c += wave_sum[w];
+    for (int w = 0; w < kThreads / 64; ++w) c += wave_sum[w];
     a.live_count[r] = c;
   }
 }
@@ -768,10 +770,18 @@ hipError_t launch_build(const MetaArgs& a, hipStream_t stream) {
                        dim3(kPlanThreads), 0, stream, a);
     return hipGetLastError();
   }
-  if (a.num_reqs > 0) {
-    hipLaunchKernelGGL(count_kernel, dim3(a.num_reqs), dim3(kCountThreads), 0, stream, a);
-  }
+  // requests averaging fewer than kLongRequestTokens tokens need one 16-byte load per thread
+  // even at kCountThreadsShort threads, and smaller workgroups are resident more at a time
   const bool long_reqs = a.num_reqs > 0 && a.num_tokens / a.num_reqs >= kLongRequestTokens;
+  if (a.num_reqs > 0) {
+    if (long_reqs) {
+      hipLaunchKernelGGL(count_kernel<kCountThreads>, dim3(a.num_reqs), dim3(kCountThreads), 0,
+                         stream, a);
+    } else {
+      hipLaunchKernelGGL(count_kernel<kCountThreadsShort>, dim3(a.num_reqs),
+                         dim3(kCountThreadsShort), 0, stream, a);
+    }
+  }
   if (a.num_reqs > kFusedAdmitReqs || (a.num_reqs > kFusedAdmitShortReqs && !long_reqs)) {
     hipLaunchKernelGGL(admit_kernel, dim3(1), dim3(kPlanThreads), 0, stream, a);
     const auto plan = pow2 ? plan_kernel<true, true, kPlanThreadsSplit>
