@@ -381,8 +381,8 @@ vtoken_status vtoken_append_slots(int32_t num_reqs, const int32_t* append_indptr
  * slot_indptr[r+1] < slot_indptr[r], or slot_count[r] < 0) reads no slot and gets NaN
  * outputs. The split launch has R * num_kv_heads * ceil(max_tokens / split) workgroups, and
  * those past a request's slots return at once: pass the batch's largest slot count rather
- * than a model's context limit (a bound 8 times too large cost the Llama-3-8B Random decode
- * about 10% on MI355X). */
+ * than a model's context limit (on MI355X a bound 2, 4 and 8 times too large cost the
+ * Llama-3-8B Random decode 2%, 8% and 25%). */
 enum { VTOKEN_KV_FP16 = 0, VTOKEN_KV_BF16 = 1, VTOKEN_KV_FP8_E4M3 = 2 };
 
 typedef struct vtoken_decode {
