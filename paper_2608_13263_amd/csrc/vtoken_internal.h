@@ -259,6 +259,13 @@ constexpr int decode_split_waves(int elem_bytes, int group) {
 }
 // Tokens one split workgroup covers (head_dim 32, 64, 128, 256 -> 512, 256, 128, 64 tokens
 // for 16-bit caches with 4 waves; twice as many with 8 waves or at 1 byte per element).
+constexpr int decode_split_tokens(int head_dim, int elem_bytes, int group) {
+  return decode_split_waves(elem_bytes, group) * kDecodeWaveBytes / (head_dim * elem_bytes);
+}
+// The smallest split over the element sizes and groups: the workspace bound of the C ABI.
+constexpr int decode_min_split_tokens(int head_dim) {
+  return decode_split_tokens(head_dim, 2, 1);
+}
 // Split slots per (request, KV head) in the split launch's grid. Workgroups are handed to the
 // 8 XCDs in turn, so with an even count and few splits the requests' first splits, which hold
 // the work, fall on the same XCDs (Llama-3-8B Random, 20 splits: one XCD 12% above the mean);
@@ -267,14 +274,6 @@ constexpr int decode_split_waves(int elem_bytes, int group) {
 // measured 0.2-0.7% slower (Llama-3-70B, 78 splits), so those keep theirs.
 __host__ __device__ constexpr int decode_grid_splits(int splits) {
   return splits < 64 ? (splits | 1) : splits;
-}
-
-constexpr int decode_split_tokens(int head_dim, int elem_bytes, int group) {
-  return decode_split_waves(elem_bytes, group) * kDecodeWaveBytes / (head_dim * elem_bytes);
-}
-// The smallest split over the element sizes and groups: the workspace bound of the C ABI.
-constexpr int decode_min_split_tokens(int head_dim) {
-  return decode_split_tokens(head_dim, 2, 1);
 }
 
 hipError_t launch_build(const MetaArgs& a, hipStream_t stream);
