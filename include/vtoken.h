@@ -371,7 +371,8 @@ vtoken_status vtoken_append_slots(int32_t num_reqs, const int32_t* append_indptr
  *   out[r][qh] = softmax(scale * q[r][qh] . K[slot]^T) @ V[slot] over the slots of r,
  * K and V being the layer's K and V planes (float32 math; zeros for a request with no slots).
  * Flash-decoding: splits of 32 KiB of K per KV head (32768 / (head_dim * elem_bytes) tokens;
- * 64 KiB for 2-byte caches with 8 query heads per KV head), then a merge; the workspace
+ * 64 KiB for 2-byte caches with 8 query heads per KV head, or when max_tokens spans 64 or
+ * more 32 KiB splits), then a merge; the workspace
  * holds the split partials and is overwritten by every call (calls sharing it must be
  * stream-ordered). A request with more slots than max_tokens provides for is never
  * truncated: its outputs are NaN, unless its slots still fit the ceil(max_tokens / split)

@@ -414,7 +414,8 @@ vtoken_status paged_decode(const vtoken_cache* cache, const vtoken_decode* d, in
   a.kv_kind = kind;
   a.num_slots = cache->num_blocks * cache->block_size;
   a.num_reqs = num_reqs;
-  const int split = vtoken::decode_split_tokens(D, cache->elem_bytes, g);
+  const int split = vtoken::decode_split_tokens_w(
+      D, cache->elem_bytes, vtoken::decode_waves_for(D, cache->elem_bytes, g, d->max_tokens));
   a.split_tokens = split;
   a.splits = d->max_tokens > 0 ? (d->max_tokens + split - 1) / split : 1;
   const int64_t grid_splits = vtoken::decode_grid_splits(a.splits);

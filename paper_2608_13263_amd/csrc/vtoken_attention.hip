@@ -312,8 +312,8 @@ constexpr int decode_min_waves(int kind, int head_dim) {
 // Every thread issues all of its K and V loads (128 + 128 bytes) before any arithmetic.
 // Non-finite K or V values are outside the contract (a zero weight times an infinite value
 // gives NaN).
-template <int kKind, int kD, int kG>
-__global__ __launch_bounds__(64 * decode_split_waves(kKind == 2 ? 1 : 2, kG))
+template <int kKind, int kD, int kG, int kWaves>
+__global__ __launch_bounds__(64 * kWaves)
 __attribute__((amdgpu_waves_per_eu(decode_min_waves(kKind, kD))))
 void decode_split_kernel(AttnArgs a) {
   using PieceT = typename Piece<kKind>::type;
@@ -321,8 +321,7 @@ void decode_split_kernel(AttnArgs a) {
   using ElemT = typename ScoreOp<kKind>::elem;
   constexpr int kElem = kKind == 2 ? 1 : 2;
   constexpr int kChunks = kD / 32;                   // score k-steps
-  constexpr int kSplit = decode_split_tokens(kD, kElem, kG);
-  constexpr int kWaves = decode_split_waves(kElem, kG);
+  constexpr int kSplit = decode_split_tokens_w(kD, kElem, kWaves);
   constexpr int kThreads = 64 * kWaves;
   constexpr int kTW = kSplit / kWaves;               // tokens per wave: 16 .. 256
   constexpr int kTiles = kTW / 16;                   // 16-token score tiles per wave
@@ -739,14 +738,26 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(AttnArg
   if (d1 < D) out[d1] = v1 * inv;
 }
 
-template <int kKind, int kD, int kG>
-hipError_t launch_split(const AttnArgs& a, hipStream_t stream) {
+template <int kKind, int kD, int kG, int kWaves>
+hipError_t launch_split_w(const AttnArgs& a, hipStream_t stream) {
   const dim3 grid(
       static_cast<unsigned>((int64_t)a.num_reqs * a.num_kv_heads * decode_grid_splits(a.splits)));
-  auto kernel = decode_split_kernel<kKind, kD, kG>;
-  hipLaunchKernelGGL(kernel, grid, dim3(64 * decode_split_waves(kKind == 2 ? 1 : 2, kG)), 0,
-                     stream, a);
+  auto kernel = decode_split_kernel<kKind, kD, kG, kWaves>;
+  hipLaunchKernelGGL(kernel, grid, dim3(64 * kWaves), 0, stream, a);
   return hipGetLastError();
+}
+
+// the split size the host chose (decode_waves_for) selects the workgroup's waves
+template <int kKind, int kD, int kG>
+hipError_t launch_split(const AttnArgs& a, hipStream_t stream) {
+  constexpr int kElem = kKind == 2 ? 1 : 2;
+  constexpr int kBase = decode_split_waves(kElem, kG);
+  if constexpr (kElem == 2 && kBase == 4) {
+    if (a.split_tokens == decode_split_tokens_w(kD, kElem, 8)) {
+      return launch_split_w<kKind, kD, kG, 8>(a, stream);
+    }
+  }
+  return launch_split_w<kKind, kD, kG, kBase>(a, stream);
 }
 
 template <int kKind, int kD>
@@ -791,8 +802,10 @@ hipError_t launch_slot_mapping(const SlotMapArgs& a, hipStream_t stream) {
 
 hipError_t launch_paged_decode(const AttnArgs& a, hipStream_t stream) {
   if (a.num_reqs <= 0) return hipSuccess;
-  if (a.split_tokens !=
-      decode_split_tokens(a.head_dim, a.kv_kind == 2 ? 1 : 2, a.num_q_heads / a.num_kv_heads)) {
+  const int elem = a.kv_kind == 2 ? 1 : 2;
+  const int group = a.num_q_heads / a.num_kv_heads;
+  if (a.split_tokens != decode_split_tokens(a.head_dim, elem, group) &&
+      (elem != 2 || a.split_tokens != decode_split_tokens_w(a.head_dim, elem, 8))) {
     return hipErrorInvalidValue;
   }
   hipError_t e;

@@ -186,7 +186,7 @@ struct AttnArgs {
   int32_t num_slots;
   int32_t num_reqs;
   int32_t splits;    // split records per (request, query head) in the workspace
-  int32_t split_tokens;  // tokens per split: decode_split_tokens(head_dim, elem bytes)
+  int32_t split_tokens;  // tokens per split: decode_split_tokens_w(head_dim, elem bytes, waves)
   float scale;
   const float* q;
   float* out;
@@ -252,15 +252,32 @@ hipError_t decode_scratch(hipStream_t stream, float** out);
 // KV head: 128 bytes per lane and operand. A workgroup has 4 waves, or 8 for 16-bit caches
 // with GQA groups of 8, whose per-workgroup work (query operands, the merge of the waves, a
 // split record of 8 heads) is then spread over twice the tokens (measured +11%; 8 waves were
-// neutral at G = 4 and slower for fp8, whose waves already cover twice the tokens).
+// slower for fp8, whose waves already cover twice the tokens). 16-bit caches at smaller
+// groups take 8 waves too when the batch's longest request spans kDecodeLongSplits 4-wave
+// splits or more (half the split records: Llama-3-70B bf16, requests of 16-64K tokens, G = 1,
+// 2, 4 faster by 4.8%, 4.4%, 2.8%; on the Llama-3-8B batches, ~27 splits, 8 waves were 0-4%
+// slower: fewer, longer workgroups leave a longer tail).
 constexpr int kDecodeWaveBytes = 8192;
+constexpr int kDecodeLongSplits = 64;
 constexpr int decode_split_waves(int elem_bytes, int group) {
   return elem_bytes == 2 && group == 8 ? 8 : 4;
 }
-// Tokens one split workgroup covers (head_dim 32, 64, 128, 256 -> 512, 256, 128, 64 tokens
-// for 16-bit caches with 4 waves; twice as many with 8 waves or at 1 byte per element).
+// Tokens one split workgroup of `waves` waves covers (head_dim 32, 64, 128, 256 -> 512, 256,
+// 128, 64 tokens for 16-bit caches with 4 waves; twice as many with 8 waves or at 1 byte per
+// element).
+constexpr int decode_split_tokens_w(int head_dim, int elem_bytes, int waves) {
+  return waves * kDecodeWaveBytes / (head_dim * elem_bytes);
+}
 constexpr int decode_split_tokens(int head_dim, int elem_bytes, int group) {
-  return decode_split_waves(elem_bytes, group) * kDecodeWaveBytes / (head_dim * elem_bytes);
+  return decode_split_tokens_w(head_dim, elem_bytes, decode_split_waves(elem_bytes, group));
+}
+// Waves per split workgroup for a batch whose requests hold at most max_tokens slots.
+constexpr int decode_waves_for(int head_dim, int elem_bytes, int group, int64_t max_tokens) {
+  return elem_bytes == 2 && decode_split_waves(elem_bytes, group) == 4 &&
+                 max_tokens >= (int64_t)kDecodeLongSplits *
+                                   decode_split_tokens_w(head_dim, elem_bytes, 4)
+             ? 8
+             : decode_split_waves(elem_bytes, group);
 }
 // The smallest split over the element sizes and groups: the workspace bound of the C ABI.
 constexpr int decode_min_split_tokens(int head_dim) {

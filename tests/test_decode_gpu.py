@@ -318,11 +318,44 @@ def test_paged_decode_max_tokens_too_small(dtype, G):
     assert np.isnan(got[~fits]).all()
 
 
+@pytest.mark.parametrize("dtype,G,D", [("bf16", 1, 128), ("fp16", 2, 128), ("bf16", 4, 128),
+                                     ("fp16", 4, 64), ("bf16", 2, 256)])
+def test_paged_decode_long_batch_eight_wave_splits(dtype, G, D):
+    """A batch whose longest request spans 64 or more 4-wave splits takes 8-wave split
+    workgroups for 16-bit caches at G < 8 (twice the tokens per split): requests of ~18K live
+    tokens and a short one, against the float64 oracle."""
+    t = torch()
+    B = _B()
+    H, S = 2, 16
+    rng = np.random.default_rng(1700 + 10 * G + D)
+    masks = [(rng.random(n) < 0.9).astype(np.uint8) for n in (20_000, 19_000, 17_500)]
+    masks.append((rng.random(300) < 0.5).astype(np.uint8))
+    M = sum(-(-len(m) // S) for m in masks)
+    inp = W.from_masks(masks, W.KVShape(1, H, D, S, dtype), free_blocks=M + 16, seed=G,
+                       name="decode_long_batch")
+    sh = inp.shape
+    _label(f"decode 8-wave splits {dtype} G={G} D={D}: {int(inp.live.sum())} live tokens")
+    kv = W.kv_device(sh, inp.num_blocks, 12)
+    orc = oracle_repack_inputs(inp, kv_bytes(kv, sh))
+    cache, _, _, indptr, slots = _device_pass(inp, kv)
+    ref_indptr, ref_slots = slot_mapping(orc.token_slot, inp.tok_indptr, inp.seq_lens)
+    counts = np.diff(ref_indptr)
+    assert counts.max() >= 64 * (32768 // (D * 2))
+    vals = _values(orc.kv, sh)
+    q = rng.standard_normal((inp.num_reqs, H * G, D)).astype(np.float32)
+    out = B.paged_decode(cache, t.from_numpy(q).cuda(), indptr, slots, 0, int(counts.max()))
+    got = out.cpu().numpy().astype(np.float64)
+    ref = decode_batch(q, vals[0], vals[1], ref_indptr, ref_slots)
+    np.testing.assert_allclose(got, ref, atol=ATOL, rtol=RTOL)
+    del kv, vals
+    t.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("dtype,G,S", [("bf16", 4, 16), ("fp8_e4m3", 8, 32)])
 def test_paged_decode_long_request(dtype, G, S):
     """One request of ~1M live tokens among short ones (a 1.5M-token context, keep 0.7):
-    8,200 splits per head for bf16 (4,100 for fp8) merged by the combine kernel, after a
-    repack pass, against the float64 oracle."""
+    4,100 splits per head (8-wave splits for bf16, 1-byte elements for fp8) merged by the
+    combine kernel, after a repack pass, against the float64 oracle."""
     t = torch()
     B = _B()
     H, D = 1, 128
