@@ -417,7 +417,10 @@ vtoken_status paged_decode(const vtoken_cache* cache, const vtoken_decode* d, in
   const int split = vtoken::decode_split_tokens_w(
       D, cache->elem_bytes, vtoken::decode_waves_for(D, cache->elem_bytes, g, d->max_tokens));
   a.split_tokens = split;
-  a.splits = d->max_tokens > 0 ? (d->max_tokens + split - 1) / split : 1;
+  // in 64 bits: max_tokens may lie within one split of INT32_MAX
+  a.splits = d->max_tokens > 0
+                 ? static_cast<int32_t>(((int64_t)d->max_tokens + split - 1) / split)
+                 : 1;
   const int64_t grid_splits = vtoken::decode_grid_splits(a.splits);
   if ((int64_t)num_reqs * cache->num_kv_heads * grid_splits > INT32_MAX ||
       (int64_t)num_reqs * d->num_q_heads > INT32_MAX) {

@@ -204,6 +204,19 @@ def test_paged_decode_rejects_bad_arguments(mutate, code):
     assert st == B.STATUS_CODE[code], (st, code)
 
 
+def test_paged_decode_max_tokens_at_int32_limit():
+    """A bound within one split of INT32_MAX: the split count is taken in 64 bits, so the
+    200 x 8 x 8,388,608-workgroup grid is refused rather than wrapped to a negative size."""
+    lib = B.load_library()
+    cache, _, _ = _good()
+    d, _ = _good_decode(cache, nreq=200)
+    d.max_tokens, d.workspace_bytes = 2 ** 31 - 1, 2 ** 62
+    assert lib.vtoken_decode_workspace_bytes(200, 32, 128, 2 ** 31 - 1) < 2 ** 62
+    p = _fake_ptr()
+    assert lib.vtoken_paged_decode(ctypes.byref(cache), ctypes.byref(d), 200, p, p, None) == \
+        B.STATUS_CODE["VTOKEN_ERR_SHAPE"]
+
+
 def test_paged_decode_fp8_kind_requires_one_byte_cache():
     lib = B.load_library()
     cache, _, _ = _good()
