@@ -319,16 +319,18 @@ def test_paged_decode_max_tokens_too_small(dtype, G):
 
 
 @pytest.mark.parametrize("dtype,G,D", [("bf16", 1, 128), ("fp16", 2, 128), ("bf16", 4, 128),
-                                     ("fp16", 4, 64), ("bf16", 2, 256)])
+                                     ("fp16", 4, 64), ("bf16", 2, 256), ("fp16", 1, 32)])
 def test_paged_decode_long_batch_eight_wave_splits(dtype, G, D):
     """A batch whose longest request spans 64 or more 4-wave splits takes 8-wave split
     workgroups for 16-bit caches at G < 8 (twice the tokens per split): requests of ~18K live
-    tokens and a short one, against the float64 oracle."""
+    tokens (~36K at head_dim 32, whose 4-wave split is 512 tokens) and a short one, against
+    the float64 oracle."""
     t = torch()
     B = _B()
     H, S = 2, 16
     rng = np.random.default_rng(1700 + 10 * G + D)
-    masks = [(rng.random(n) < 0.9).astype(np.uint8) for n in (20_000, 19_000, 17_500)]
+    scale = 2 if D == 32 else 1
+    masks = [(rng.random(scale * n) < 0.9).astype(np.uint8) for n in (20_000, 19_000, 17_500)]
     masks.append((rng.random(300) < 0.5).astype(np.uint8))
     M = sum(-(-len(m) // S) for m in masks)
     inp = W.from_masks(masks, W.KVShape(1, H, D, S, dtype), free_blocks=M + 16, seed=G,
@@ -347,6 +349,45 @@ def test_paged_decode_long_batch_eight_wave_splits(dtype, G, D):
     got = out.cpu().numpy().astype(np.float64)
     ref = decode_batch(q, vals[0], vals[1], ref_indptr, ref_slots)
     np.testing.assert_allclose(got, ref, atol=ATOL, rtol=RTOL)
+    del kv, vals
+    t.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("dtype,G", [("bf16", 4), ("fp16", 1), ("fp8_e4m3", 4)])
+def test_paged_decode_split_size_by_bound(dtype, G):
+    """The host picks the split size from max_tokens alone (16-bit caches at G < 8: 8-wave
+    splits from 64 four-wave splits, 8,192 tokens at head_dim 128). One batch whose longest
+    request holds 8,191 live tokens, decoded with the tight bound (4-wave splits), with 8,192
+    and 20,000 (8-wave splits for 16-bit caches, most split slots empty) and with 65,536: every
+    output within the bar of the float64 oracle, and the calls agree to float32 rounding."""
+    t = torch()
+    B = _B()
+    H, D, S = 2, 128, 16
+    rng = np.random.default_rng(1800 + G)
+    masks = [np.ones(8191, np.uint8), (rng.random(9000) < 0.6).astype(np.uint8),
+             (rng.random(700) < 0.5).astype(np.uint8), np.ones(1, np.uint8)]
+    M = sum(-(-len(m) // S) for m in masks)
+    inp = W.from_masks(masks, W.KVShape(1, H, D, S, dtype), free_blocks=M + 16, seed=G,
+                       name="decode_bound")
+    sh = inp.shape
+    _label(f"decode split size by bound {dtype} G={G}")
+    kv = W.kv_device(sh, inp.num_blocks, 13)
+    orc = oracle_repack_inputs(inp, kv_bytes(kv, sh))
+    cache, _, _, indptr, slots = _device_pass(inp, kv)
+    ref_indptr, ref_slots = slot_mapping(orc.token_slot, inp.tok_indptr, inp.seq_lens)
+    counts = np.diff(ref_indptr)
+    assert counts.max() == 8191
+    vals = _values(orc.kv, sh)
+    q = rng.standard_normal((inp.num_reqs, H * G, D)).astype(np.float32)
+    ref = decode_batch(q, vals[0], vals[1], ref_indptr, ref_slots)
+    qd = t.from_numpy(q).cuda()
+    outs = []
+    for bound in (8191, 8192, 20_000, 65_536):
+        got = B.paged_decode(cache, qd, indptr, slots, 0, bound).cpu().numpy().astype(np.float64)
+        np.testing.assert_allclose(got, ref, atol=ATOL, rtol=RTOL, err_msg=f"bound {bound}")
+        outs.append(got)
+    for got in outs[1:]:
+        np.testing.assert_allclose(got, outs[0], atol=1e-5, rtol=1e-5)
     del kv, vals
     t.cuda.empty_cache()
 
