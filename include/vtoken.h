@@ -242,7 +242,12 @@ vtoken_status vtoken_repack_inplace(const vtoken_cache* cache, const vtoken_batc
  *            5 non-temporal loads and sc0 sc1 stores, 6 non-temporal loads, sc1 nt stores
  *   grid:    workgroups of the copy launch; 0 = one per work item that the free list and
  *            plan can hold, capped at 2^19 (a grid-stride loop covers any remainder); a work
- *            item is one 32 KiB part (at most) of a destination block in one plane
+ *            item is one 32 KiB part (at most) of a destination block in one plane. Every
+ *            workgroup is dispatched even when the plan admits nothing (the work is counted
+ *            on the device), at about 4.7 per ns on MI355X: such a pass takes 0.112 ms at
+ *            2^19, 0.016 ms at 2^16. Measured, 2^16 costs a full copy 0.1% (Llama-3-8B
+ *            Random) to 0.5% (Llama-3-8B H2O); callers whose passes mostly admit nothing
+ *            may prefer it
  *   order:   work order over (part of a destination block, plane) items: 0 default (= 2),
  *            1 plane-major, 2 block-major (all planes of one part together)
  * All settings produce identical bytes; they differ only in speed. Invalid values return
