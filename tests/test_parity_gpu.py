@@ -142,6 +142,20 @@ def test_copy_variants_agree(variant, order, grid):
     full_parity(inp, seed=13, variant=variant, order=order, grid=grid)
 
 
+@pytest.mark.parametrize("order", [1, 2])
+def test_copy_grid_around_item_count(order):
+    """Grids just below, at, just above and three times the pass's work items (destination
+    blocks x planes, 32 KiB parts): below, the grid-stride loop takes the rest; above, the
+    items are spread over the grid and the workgroups without one leave. Bytes and metadata
+    equal the oracle's every time."""
+    inp = W.llama3_8b_random(205, num_layers=2, num_reqs=6, len_range=(500, 2500))
+    items = oracle_repack_inputs(inp).used * inp.shape.num_planes
+    assert items > 8
+    for grid in (items - 1, items, items + 1, 3 * items):
+        print(f"[gpu] copy grid {grid} for {items} items, order {order}", flush=True)
+        full_parity(inp, seed=14, variant=0, order=order, grid=grid)
+
+
 def test_repack_is_idempotent():
     t = torch()
     from paper_2608_13263_amd import binding as B
