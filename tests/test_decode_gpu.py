@@ -358,8 +358,10 @@ def test_paged_decode_split_size_by_bound(dtype, G):
     """The host picks the split size from max_tokens alone (16-bit caches at G < 8: 8-wave
     splits from 64 four-wave splits, 8,192 tokens at head_dim 128). One batch whose longest
     request holds 8,191 live tokens, decoded with the tight bound (4-wave splits), with 8,192
-    and 20,000 (8-wave splits for 16-bit caches, most split slots empty) and with 65,536: every
-    output within the bar of the float64 oracle, and the calls agree to float32 rounding."""
+    and 20,000 (8-wave splits for 16-bit caches, most split slots empty), with 15,872 and
+    16,384 (62 and 64 splits of 256 tokens: the grid's split count rounded up to 63 below 64,
+    kept at 64) and with 65,536: every output within the bar of the float64 oracle, and the
+    calls agree to float32 rounding."""
     t = torch()
     B = _B()
     H, D, S = 2, 128, 16
@@ -382,7 +384,7 @@ def test_paged_decode_split_size_by_bound(dtype, G):
     ref = decode_batch(q, vals[0], vals[1], ref_indptr, ref_slots)
     qd = t.from_numpy(q).cuda()
     outs = []
-    for bound in (8191, 8192, 20_000, 65_536):
+    for bound in (8191, 8192, 20_000, 15_872, 16_384, 65_536):
         got = B.paged_decode(cache, qd, indptr, slots, 0, bound).cpu().numpy().astype(np.float64)
         np.testing.assert_allclose(got, ref, atol=ATOL, rtol=RTOL, err_msg=f"bound {bound}")
         outs.append(got)
